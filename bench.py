@@ -1,0 +1,258 @@
+#!/usr/bin/env python3
+"""Verify-step benchmark on one MI355X.
+
+One step = the whole verify hot path at one verifier level for one batch:
+verification attention, accept-and-diverge, rollback (three C-ABI calls on
+one stream). Inputs are seeded synthetic data of the named workload and are
+resident in HBM before timing starts. To keep the 256 MB last-level cache
+from serving repeated steps, R copies of the inputs live at different HBM
+addresses and step s uses copy s mod R.
+
+Prints ONE JSON line (rank 0) with the throughput in verified draft tokens/s,
+the roofline of the dominant kernel (HIP events over the timed region), and
+the CPU reference timed on a bounded sample of the same workload.
+
+  python bench.py [--steps K] [--warmup W] [--config 2|5|...] [--no-cpu]
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, HERE)
+
+PEAK_HBM_GBS = 8000.0
+PROFILE_COUNTERS = os.path.join(HERE, "profiles", "counters.json")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--rotate", type=int, default=0, help="input copies (0 = enough to exceed 1 GB)")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--cpu-seqs", type=int, default=0, help="sequences in the CPU-baseline sample")
+    return ap.parse_args()
+
+
+def kernel_source_hash(names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(HERE, "paper_2505_07680_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: this build runs on exactly one GPU (the verify step shards by sequence with "
+              "no cross-GPU exchange; see DESIGN.md). Use --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2505_07680_amd as sr
+    from workloads import CONFIGS, level_inputs
+
+    sr.load()
+    if not torch.cuda.is_available():
+        print("bench.py: no HIP device visible", file=sys.stderr)
+        sys.exit(3)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    shape = CONFIGS[args.config]
+    t0 = time.time()
+    inp = level_inputs(shape)
+    gen_s = time.time() - t0
+
+    B, G1, Hq, D = inp.q.shape
+    gmax = G1 - 1
+    Hkv, cap = inp.k.shape[1], inp.k.shape[2]
+    V = inp.p_logits.shape[2]
+    code = sr.SR_BF16 if shape.logits == "bf16" else sr.SR_F32
+    esz = 2 if code == sr.SR_BF16 else 4
+
+    def up(x):
+        x = np.ascontiguousarray(x)
+        if x.dtype == np.uint16:
+            x = x.view(np.int16)
+        return torch.from_numpy(x).to(dev)
+
+    # bytes the method must move per step (algorithmic)
+    kv_len = inp.kv_len.astype(np.int64)
+    gam = inp.gamma.astype(np.int64)
+    att_bytes = int((2 * Hkv * kv_len * D * 2).sum() + ((gam + 1) * Hq * D * 2).sum()
+                    + ((gam + 1) * Hq * D * 4).sum() + kv_len.sum())
+    acc_bytes = int(((2 * gam + 1) * V * esz).sum())
+    set_bytes = inp.k.nbytes + inp.v.nbytes + inp.p_logits.nbytes + inp.q_logits.nbytes
+    R = args.rotate or max(2, int(np.ceil(1.2e9 / set_bytes)))
+
+    sets = []
+    base_mask = np.zeros((B, cap), np.uint8)
+    for b in range(B):
+        base_mask[b, : inp.kv_len[b]] = 1
+    for r in range(R):
+        s = dict(
+            q=up(inp.q), k=up(inp.k), v=up(inp.v), kv_in=up(inp.kv_len), kv_work=up(inp.kv_len),
+            gamma=up(inp.gamma), mask_in=up(base_mask), mask_work=up(base_mask),
+            p=up(inp.p_logits), ql=up(inp.q_logits), drafts=up(inp.drafts),
+            u_acc=up(inp.u_acc), u_res=up(inp.u_res),
+            out=torch.empty((B, G1, Hq, D), dtype=torch.float32, device=dev),
+            ws=sr.attention_workspace(B, gmax, Hq, Hkv, D, cap, device=dev),
+            acc=sr.AcceptBuffers(B, gmax, V, code, device=dev),
+            phys=torch.zeros(1, dtype=torch.int32, device=dev),
+            st=torch.zeros(1, dtype=torch.int32, device=dev),
+        )
+        sets.append(s)
+
+    # calibration copy of known size (for HBM byte counters read by rocprofv3)
+    cal_src = torch.empty(256 << 20, dtype=torch.uint8, device=dev).fill_(1)
+    cal_dst = torch.empty_like(cal_src)
+    cal_dst.copy_(cal_src)
+    torch.cuda.synchronize()
+    del cal_src, cal_dst
+
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+
+    def step(s, evs=None):
+        if evs:
+            evs[0].record()
+        sr.specrouter_verify_attention(s["q"], s["k"], s["v"], s["mask_in"], s["kv_in"], s["gamma"],
+                                       s["out"], inp.scale, s["ws"], s["st"])
+        if evs:
+            evs[1].record()
+        a = s["acc"]
+        sr.specrouter_accept_and_diverge(s["p"], s["ql"], s["drafts"], s["gamma"], s["u_acc"], s["u_res"],
+                                         s["kv_in"], a.accept_len, a.out_tokens, a.new_len, a.accept_prob,
+                                         a.p_tok, a.q_tok, a.kl, a.tv, a.workspace, s["st"])
+        if evs:
+            evs[2].record()
+        sr.specrouter_rollback(s["kv_work"], s["mask_work"], a.new_len, s["phys"], s["st"])
+        if evs:
+            evs[3].record()
+
+    for i in range(args.warmup):
+        step(sets[i % R])
+    torch.cuda.synchronize()
+
+    K = args.steps
+    evs = [[ev() for _ in range(4)] for _ in range(K)]
+    start, stop = ev(), ev()
+    torch.cuda.synchronize()
+    start.record()
+    t_wall = time.perf_counter()
+    for i in range(K):
+        step(sets[i % R], evs[i])
+    stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    total_ms = start.elapsed_time(stop)
+    att_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    acc_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    rb_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+
+    status = int(sum(int(s["st"].item()) for s in sets))
+    acc0 = sets[0]["acc"]
+    mean_accept = float(acc0.accept_len.float().mean().item())
+    drafts_per_step = int(gam.sum())
+    ms_per_step = total_ms / K
+    value = drafts_per_step * K / (total_ms / 1e3)
+
+    att_gbs = att_bytes / (att_ms / 1e3) / 1e9
+    acc_gbs = acc_bytes / (acc_ms / 1e3) / 1e9
+    traffic = None
+    src_hash = kernel_source_hash(["attention.hip", "sr_internal.h"])
+    if os.path.exists(PROFILE_COUNTERS):
+        try:
+            c = json.load(open(PROFILE_COUNTERS))
+            ent = c.get("attention", {}).get(shape.name)
+            if ent and ent.get("source_hash") == src_hash:
+                traffic = ent["bytes_per_launch"]
+        except (ValueError, KeyError):
+            traffic = None
+    roofline = {
+        "bound": "hbm", "kernel": "specrouter_verify_attention",
+        "achieved": round(att_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+        "frac": round(att_gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
+        "algorithmic_bytes": att_bytes, "avg_launch_us": round(att_ms * 1e3, 2),
+    }
+
+    cpu = None
+    if not args.no_cpu:
+        cpu = cpu_baseline(inp, args.cpu_seqs)
+
+    line = {
+        "metric": "verified draft tokens/s per verify step; HBM GB/s (KV + logits) vs MI355X peak",
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 KV / fp32 logits" if code == sr.SR_F32 else "bf16 KV / bf16 logits",
+        "data": "synthetic (seeded Philox; Q,K,V ~ N(0,1) bf16; logits N(0,9) + draft noise)",
+        "config": {
+            "workload": f"{shape.name}: {shape.note}",
+            "B": B, "gamma": int(gam.max()), "heads": f"{Hq}/{Hkv}", "head_dim": D,
+            "cache_len": int(kv_len.max()), "vocab": V, "input_copies": R,
+            "parallelism": "single GPU",
+        },
+        "roofline": roofline,
+        "kernels": {
+            "verify_attention": {"us": round(att_ms * 1e3, 2), "GB/s": round(att_gbs, 1),
+                                 "frac": round(att_gbs / PEAK_HBM_GBS, 4)},
+            "accept_and_diverge": {"us": round(acc_ms * 1e3, 2), "GB/s": round(acc_gbs, 1),
+                                   "frac": round(acc_gbs / PEAK_HBM_GBS, 4), "algorithmic_bytes": acc_bytes},
+            "rollback": {"us": round(rb_ms * 1e3, 2)},
+        },
+        "mean_accept_len": round(mean_accept, 3),
+        "status_bits": status,
+        "cpu_baseline": cpu,
+        "host_wall_s": round(wall, 4),
+        "input_gen_s": round(gen_s, 2),
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(inp, n_seqs):
+    """The CPU reference, untuned, on a bounded sample of the same workload."""
+    import oracle
+
+    B = inp.B
+    n = n_seqs or B
+    seqs = list(range(min(n, B)))
+    t0 = time.perf_counter()
+    oracle.verify_attention(inp.q, inp.k, inp.v, inp.kv_len, inp.gamma, inp.scale, seqs=seqs)
+    r = oracle.accept_and_diverge(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, inp.u_acc, inp.u_res,
+                                  kv_len=inp.kv_len, seqs=seqs)
+    oracle.rollback(inp.kv_len[seqs], None, r["new_len"][seqs])
+    dt = time.perf_counter() - t0
+    drafts = int(inp.gamma[seqs].sum())
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        cores = os.cpu_count()
+    threads = os.environ.get("OPENBLAS_NUM_THREADS") or os.environ.get("OMP_NUM_THREADS") or str(cores)
+    return {
+        "value": round(drafts / dt, 2), "unit": "tokens/s", "cores": int(min(cores, int(threads))),
+        "kind": "oracle",
+        "sample": f"{len(seqs)} of {B} sequences, one full verify step each (fp64 numpy), {dt:.2f} s",
+    }
+
+
+if __name__ == "__main__":
+    main()

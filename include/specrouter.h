@@ -1,0 +1,192 @@
+/*
+ * specrouter.h -- C ABI of the speculative-decoding verify step on MI355X (gfx950).
+ *
+ * One verify step at one verifier level of a multi-level speculative-decoding
+ * chain (SpecRouter, arXiv 2505.07680) is three calls, enqueued in this order
+ * on one stream:
+ *
+ *   specrouter_verify_attention    attention of the gamma_b + 1 new query rows of
+ *                                  every sequence against that sequence's own KV
+ *                                  cache, under the logical validity mask
+ *                                  (Section 2.2 step 2; Section 4.4, Eq. 8);
+ *   specrouter_accept_and_diverge  speculative accept/reject of the drafts with
+ *                                  residual resampling and the bonus token
+ *                                  (Section 2.2 steps 3-4), plus per-position
+ *                                  total variation distance (Eq. 5) and KL
+ *                                  divergence that feed the chain scheduler's
+ *                                  similarity estimate (Section 4.2, Eq. 6);
+ *   specrouter_rollback            logical rollback of every sequence's cache to
+ *                                  its accepted prefix, no KV data moved
+ *                                  (Section 4.4, rollback mechanism, Eq. 9).
+ *
+ * Conventions shared by every call
+ *   - Pointers named in a signature are DEVICE (HBM) pointers owned by the
+ *     caller unless stated otherwise. The library never allocates, frees or
+ *     keeps a pointer after a call returns, and never synchronizes: each call
+ *     only enqueues kernels on `stream` (a hipStream_t passed as void*; NULL =
+ *     the default stream) and returns.
+ *   - Return value: SR_OK, or a negative SR_E* code for an error detected on the
+ *     host before anything was enqueued (bad sizes, NULL or misaligned
+ *     pointers, a workspace that is too small) or a failed launch.
+ *   - Values that live on the device (lengths, gamma, tokens, uniforms) cannot
+ *     be checked on the host without a synchronization; they are checked by the
+ *     kernels, which OR SR_ST_* bits into *status (if status is non-NULL; the
+ *     caller clears it) and give the affected sequence defined "invalid"
+ *     outputs instead of computing on bad data.
+ *   - Calls that share a workspace, or whose outputs alias, must not overlap
+ *     in time (put them on one stream). Different calls on different streams
+ *     with separate buffers are independent. The library holds no global state
+ *     beyond cached device properties, so it is reentrant and thread-safe.
+ *
+ * Shapes: B sequences; gamma_max >= max_b gamma_b (0..16); Hq query heads and
+ * Hkv kv heads with Hq % Hkv == 0 (query head h reads kv head h / (Hq/Hkv));
+ * head dimension D in {64, 128}; L_cap cache rows per (sequence, kv head);
+ * vocabulary size V.
+ */
+#ifndef SPECROUTER_H
+#define SPECROUTER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPECROUTER_ABI_VERSION 1
+#define SPECROUTER_MAX_GAMMA 16
+
+/* Host-side return codes. */
+enum {
+  SR_OK = 0,
+  SR_EINVAL = -1,       /* bad size, NULL required pointer, misaligned pointer */
+  SR_EUNSUPPORTED = -2, /* D not in {64,128}, unknown logits dtype */
+  SR_EWORKSPACE = -3,   /* workspace NULL or smaller than the *_workspace_size query */
+  SR_ELAUNCH = -4,      /* the HIP runtime refused a launch or a device query */
+};
+
+/* Logits element types. */
+enum { SR_F32 = 0, SR_BF16 = 1 };
+
+/* Device-side data-error bits OR-ed into *status. */
+enum {
+  SR_ST_GAMMA = 1,          /* gamma_b outside [0, gamma_max] */
+  SR_ST_KVLEN = 2,          /* kv_len_b outside its valid range, or a negative new_len_b */
+  SR_ST_TOKEN = 4,          /* a draft token outside [0, V) */
+  SR_ST_UNIFORM = 8,        /* a needed uniform outside [0, 1) (NaN included) */
+  SR_ST_ROLLBACK_GROW = 16, /* rollback asked to grow a sequence (treated as a no-op) */
+  SR_ST_TIMEOUT = 32,       /* an inter-workgroup wait gave up (results of that call are invalid) */
+};
+
+/* SPECROUTER_ABI_VERSION of the loaded library. */
+int specrouter_abi_version(void);
+
+/* Static English text for an SR_E* return code or a single SR_ST_* bit. Never NULL. */
+const char* specrouter_status_string(int code);
+
+/* ------------------------------------------------------------------------ */
+/* Verification attention (Section 2.2 step 2; Section 4.4, Eq. 8).
+ *
+ * For sequence b, query head h (kv head g = h / (Hq/Hkv)) and new row
+ * i in [0, gamma_b], at cache position pos = kv_len_b - (gamma_b + 1) + i:
+ *
+ *   out[b][i][h][:] = softmax_j(scale * q[b][i][h] . k[b][g][j]) v[b][g][j]
+ *
+ * over the keys j <= pos with cache_mask[b][j] != 0 (all j < kv_len_b when
+ * cache_mask is NULL). Entries under mask 0 or at j >= kv_len_b are ignored
+ * whatever they hold (even NaN/Inf). A row with no visible key, and every row
+ * i > gamma_b, is written as 0. The caller has already written this step's
+ * gamma_b + 1 new K/V rows at [kv_len_b - gamma_b - 1, kv_len_b).
+ *
+ * q          bf16 [B][gamma_max+1][Hq][D]          (16-byte aligned)
+ * k_cache    bf16 [B][Hkv][L_cap][D]               (16-byte aligned)
+ * v_cache    bf16 [B][Hkv][L_cap][D]               (16-byte aligned)
+ * cache_mask u8   [B][L_cap] in {0,1}, or NULL
+ * kv_len     i32  [B]  valid physical length incl. the new rows; must lie in
+ *                      [gamma_b + 1, L_cap], else SR_ST_KVLEN and zero output
+ * gamma      i32  [B]  in [0, gamma_max] (0 = plain decode), else SR_ST_GAMMA
+ * out        fp32 [B][gamma_max+1][Hq][D]          (16-byte aligned)
+ * scale      score scale, normally 1/sqrt(D)
+ * workspace  device scratch of specrouter_verify_attention_workspace_size()
+ *            bytes (may be NULL when that size is 0); contents need no
+ *            initialisation and are dead after the call
+ * Precision: bf16 products, fp32 accumulation and softmax.
+ */
+size_t specrouter_verify_attention_workspace_size(int B, int gamma_max, int Hq, int Hkv, int D,
+                                                  int L_cap);
+int specrouter_verify_attention(const void* q, const void* k_cache, const void* v_cache,
+                                const uint8_t* cache_mask, const int32_t* kv_len,
+                                const int32_t* gamma, float* out, int B, int gamma_max, int Hq,
+                                int Hkv, int D, int L_cap, float scale, void* workspace,
+                                size_t workspace_bytes, int32_t* status, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Accept and diverge (Section 2.2 steps 3-4, probabilistic acceptance; Eq. 2;
+ * Eq. 5), one sweep over the logits.
+ *
+ * With p_j = softmax(p_logits[b][j]) (j = 0..gamma_b) and
+ * q_j = softmax(q_logits[b][j]) (j < gamma_b), for each sequence b:
+ *   a_j  = min(1, p_j(x_j) / q_j(x_j)), x_j = draft_tokens[b][j];
+ *   k_b  = first j < gamma_b with NOT (u_accept[b][j] < a_j), else gamma_b;
+ *   t_b  = one token drawn by CDF inversion (ascending vocabulary order,
+ *          smallest x with C(x) > u_resample[b][k_b] * C(V-1)) from
+ *          max(0, p_k - q_k) if k_b < gamma_b (p_k if that residual is all
+ *          zero), else from p_gamma;
+ *   TV_j = 1/2 sum_v |p_j - q_j|,  KL_j = KL(p_j || q_j) in nats, j < gamma_b.
+ *
+ * p_logits      [B][gamma_max+1][V], rows contiguous, batch stride
+ *               p_batch_stride ELEMENTS; rows j > gamma_b are never read
+ * q_logits      [B][gamma_max][V], batch stride q_batch_stride elements (may be
+ *               a view into another level's p_logits); rows j >= gamma_b never read
+ * logits_dtype  SR_F32 or SR_BF16 (both tensors; bf16 is widened in-kernel)
+ * draft_tokens  i32 [B][gamma_max];  gamma i32 [B]
+ * u_accept      fp32 [B][gamma_max] in [0,1);  u_resample fp32 [B][gamma_max+1] in [0,1)
+ * kv_len        i32 [B] or NULL; when given, new_len[b] = kv_len[b] - gamma_b + k_b
+ *               (the accepted prefix, ready for specrouter_rollback)
+ * accept_len    i32 [B]: k_b, or -1 for a sequence with bad data
+ * out_tokens    i32 [B][gamma_max+1]: x_0..x_{k-1}, t_b, then -1
+ * new_len       i32 [B] or NULL (must be NULL when kv_len is NULL); -> kv_len[b]
+ *               unchanged for a sequence with bad data
+ * accept_prob, p_tok, q_tok, kl, tv: fp32 [B][gamma_max] or NULL each; entries
+ *               j >= gamma_b (and all entries of a bad sequence) are NaN
+ * workspace     device scratch of specrouter_accept_workspace_size() bytes; it
+ *               must be zero-filled before its FIRST use and every call leaves
+ *               it zero-filled again (its counters reset themselves)
+ * Logits must be finite or -inf; a row that is entirely -inf is not supported.
+ * Requires (V * element size) % 16 == 0 and 16-byte aligned logits pointers and
+ * strides, else SR_EUNSUPPORTED.
+ */
+size_t specrouter_accept_workspace_size(int B, int gamma_max, int V, int logits_dtype);
+int specrouter_accept_and_diverge(const void* p_logits, int64_t p_batch_stride,
+                                  const void* q_logits, int64_t q_batch_stride, int logits_dtype,
+                                  const int32_t* draft_tokens, const int32_t* gamma,
+                                  const float* u_accept, const float* u_resample,
+                                  const int32_t* kv_len, int32_t* accept_len,
+                                  int32_t* out_tokens, int32_t* new_len, float* accept_prob,
+                                  float* p_tok, float* q_tok, float* kl, float* tv, int B,
+                                  int gamma_max, int V, void* workspace, size_t workspace_bytes,
+                                  int32_t* status, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Rollback (Section 4.4, logical rollback and Eq. 9).
+ *
+ * For every sequence: n = min(kv_len[b], new_len[b]); cache_mask[b][n:kv_len[b]) = 0;
+ * kv_len[b] = n. Idempotent (new_len holds absolute lengths L'_b). No K/V byte
+ * is read or written. phys_len = max_b kv_len[b] afterwards, which is Eq. 9's
+ * L - r_min when every sequence started at the common length L.
+ *
+ * kv_len      i32 [B] in/out; entries outside [0, L_cap] set SR_ST_KVLEN and are
+ *             left unchanged
+ * cache_mask  u8 [B][L_cap] in/out, or NULL
+ * new_len     i32 [B]; negative -> SR_ST_KVLEN (unchanged), > kv_len ->
+ *             SR_ST_ROLLBACK_GROW (unchanged)
+ * phys_len    i32 [1] out, or NULL
+ */
+int specrouter_rollback(int32_t* kv_len, uint8_t* cache_mask, const int32_t* new_len,
+                        int32_t* phys_len, int B, int L_cap, int32_t* status, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPECROUTER_H */

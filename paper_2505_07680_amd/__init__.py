@@ -1,0 +1,38 @@
+"""MI355X (gfx950) verify step of multi-level speculative decoding.
+
+The compute lives in libspecrouter.so (hand-written HIP kernels behind a C
+ABI, declared in include/specrouter.h); this package holds the kernels'
+sources, the build script and a thin ctypes binding with the same function
+names as the C entry points.
+"""
+
+from . import _lib
+from ._lib import (
+    SR_BF16,
+    SR_F32,
+    AcceptBuffers,
+    attention_workspace,
+    load,
+    specrouter_abi_version,
+    specrouter_accept_and_diverge,
+    specrouter_accept_workspace_size,
+    specrouter_rollback,
+    specrouter_status_string,
+    specrouter_verify_attention,
+    specrouter_verify_attention_workspace_size,
+)
+
+__all__ = [
+    "SR_BF16",
+    "SR_F32",
+    "AcceptBuffers",
+    "attention_workspace",
+    "load",
+    "specrouter_abi_version",
+    "specrouter_accept_and_diverge",
+    "specrouter_accept_workspace_size",
+    "specrouter_rollback",
+    "specrouter_status_string",
+    "specrouter_verify_attention",
+    "specrouter_verify_attention_workspace_size",
+]

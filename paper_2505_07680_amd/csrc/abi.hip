@@ -1,0 +1,135 @@
+// C ABI of the verify step: host-side argument checks, workspace queries and
+// dispatch to the kernels. Every check here happens before anything is
+// enqueued; data that lives on the device is checked by the kernels.
+
+#include <atomic>
+#include <stdint.h>
+
+#include "sr_internal.h"
+
+namespace sr {
+
+int device_cu_count() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return -1;
+  if (dev >= 0 && dev < 64) {
+    const int c = cache[dev].load(std::memory_order_relaxed);
+    if (c > 0) return c;
+  }
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return -1;
+  if (dev >= 0 && dev < 64) cache[dev].store(n, std::memory_order_relaxed);
+  return n;
+}
+
+}  // namespace sr
+
+namespace {
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+bool attention_shape_ok(int B, int gamma_max, int Hq, int Hkv, int L_cap) {
+  return B > 0 && gamma_max >= 0 && gamma_max <= SPECROUTER_MAX_GAMMA && Hq > 0 && Hkv > 0 &&
+         Hq % Hkv == 0 && L_cap >= gamma_max + 1 && B <= 65535;
+}
+
+}  // namespace
+
+extern "C" {
+
+int specrouter_abi_version(void) { return SPECROUTER_ABI_VERSION; }
+
+const char* specrouter_status_string(int code) {
+  switch (code) {
+    case SR_OK: return "ok";
+    case SR_EINVAL: return "invalid argument (size, NULL or misaligned pointer)";
+    case SR_EUNSUPPORTED: return "unsupported configuration (head dim, dtype or vocabulary alignment)";
+    case SR_EWORKSPACE: return "workspace missing or too small";
+    case SR_ELAUNCH: return "HIP launch or device query failed";
+    case SR_ST_GAMMA: return "device data: gamma outside [0, gamma_max]";
+    case SR_ST_KVLEN: return "device data: kv_len or new_len out of range";
+    case SR_ST_TOKEN: return "device data: draft token outside [0, V)";
+    case SR_ST_UNIFORM: return "device data: uniform outside [0, 1)";
+    case SR_ST_ROLLBACK_GROW: return "device data: rollback would grow a sequence (ignored)";
+    case SR_ST_TIMEOUT: return "device: inter-workgroup wait timed out";
+    default: return "unknown code";
+  }
+}
+
+size_t specrouter_verify_attention_workspace_size(int B, int gamma_max, int Hq, int Hkv, int D,
+                                                  int L_cap) {
+  if (!attention_shape_ok(B, gamma_max, Hq, Hkv, L_cap) || (D != 64 && D != 128)) return 0;
+  sr::AttentionPlan plan;
+  if (sr::attention_plan(B, gamma_max, Hq, Hkv, D, L_cap, &plan) != SR_OK) return 0;
+  return plan.workspace_bytes;
+}
+
+int specrouter_verify_attention(const void* q, const void* k_cache, const void* v_cache,
+                                const uint8_t* cache_mask, const int32_t* kv_len,
+                                const int32_t* gamma, float* out, int B, int gamma_max, int Hq,
+                                int Hkv, int D, int L_cap, float scale, void* workspace,
+                                size_t workspace_bytes, int32_t* status, void* stream) {
+  if (!q || !k_cache || !v_cache || !kv_len || !gamma || !out) return SR_EINVAL;
+  if (!attention_shape_ok(B, gamma_max, Hq, Hkv, L_cap)) return SR_EINVAL;
+  if (D != 64 && D != 128) return SR_EUNSUPPORTED;
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out)) return SR_EINVAL;
+  sr::AttentionPlan plan;
+  const int rc = sr::attention_plan(B, gamma_max, Hq, Hkv, D, L_cap, &plan);
+  if (rc != SR_OK) return rc;
+  if (plan.workspace_bytes > 0 &&
+      (!workspace || workspace_bytes < plan.workspace_bytes || !aligned16(workspace)))
+    return SR_EWORKSPACE;
+  return sr::launch_verify_attention(q, k_cache, v_cache, cache_mask, kv_len, gamma, out, B,
+                                     gamma_max, Hq, Hkv, D, L_cap, scale, workspace, plan, status,
+                                     (hipStream_t)stream);
+}
+
+size_t specrouter_accept_workspace_size(int B, int gamma_max, int V, int logits_dtype) {
+  if (B <= 0 || gamma_max < 0 || gamma_max > SPECROUTER_MAX_GAMMA || V <= 0) return 0;
+  if (logits_dtype != SR_F32 && logits_dtype != SR_BF16) return 0;
+  sr::AcceptPlan plan;
+  if (sr::accept_plan(B, gamma_max, V, logits_dtype, &plan) != SR_OK) return 0;
+  return plan.workspace_bytes;
+}
+
+int specrouter_accept_and_diverge(const void* p_logits, int64_t p_batch_stride,
+                                  const void* q_logits, int64_t q_batch_stride, int logits_dtype,
+                                  const int32_t* draft_tokens, const int32_t* gamma,
+                                  const float* u_accept, const float* u_resample,
+                                  const int32_t* kv_len, int32_t* accept_len,
+                                  int32_t* out_tokens, int32_t* new_len, float* accept_prob,
+                                  float* p_tok, float* q_tok, float* kl, float* tv, int B,
+                                  int gamma_max, int V, void* workspace, size_t workspace_bytes,
+                                  int32_t* status, void* stream) {
+  if (B <= 0 || gamma_max < 0 || gamma_max > SPECROUTER_MAX_GAMMA || V <= 0) return SR_EINVAL;
+  if (logits_dtype != SR_F32 && logits_dtype != SR_BF16) return SR_EUNSUPPORTED;
+  if (!p_logits || !gamma || !u_resample || !accept_len || !out_tokens) return SR_EINVAL;
+  if (gamma_max > 0 && (!q_logits || !draft_tokens || !u_accept)) return SR_EINVAL;
+  if (new_len && !kv_len) return SR_EINVAL;
+  if (p_batch_stride < (int64_t)(gamma_max + 1) * V) return SR_EINVAL;
+  if (gamma_max > 0 && q_batch_stride < (int64_t)gamma_max * V) return SR_EINVAL;
+  const int esz = logits_dtype == SR_BF16 ? 2 : 4;
+  if (((int64_t)V * esz) % 16 != 0 || (p_batch_stride * esz) % 16 != 0 || !aligned16(p_logits))
+    return SR_EUNSUPPORTED;
+  if (gamma_max > 0 && ((q_batch_stride * esz) % 16 != 0 || !aligned16(q_logits)))
+    return SR_EUNSUPPORTED;
+  sr::AcceptPlan plan;
+  const int rc = sr::accept_plan(B, gamma_max, V, logits_dtype, &plan);
+  if (rc != SR_OK) return rc;
+  if (!workspace || workspace_bytes < plan.workspace_bytes || !aligned16(workspace))
+    return SR_EWORKSPACE;
+  return sr::launch_accept(p_logits, p_batch_stride, q_logits, q_batch_stride, logits_dtype,
+                           draft_tokens, gamma, u_accept, u_resample, kv_len, accept_len,
+                           out_tokens, new_len, accept_prob, p_tok, q_tok, kl, tv, B, gamma_max,
+                           V, workspace, plan, status, (hipStream_t)stream);
+}
+
+int specrouter_rollback(int32_t* kv_len, uint8_t* cache_mask, const int32_t* new_len,
+                        int32_t* phys_len, int B, int L_cap, int32_t* status, void* stream) {
+  if (!kv_len || !new_len || B <= 0 || L_cap <= 0) return SR_EINVAL;
+  return sr::launch_rollback(kv_len, cache_mask, new_len, phys_len, B, L_cap, status,
+                             (hipStream_t)stream);
+}
+
+}  // extern "C"

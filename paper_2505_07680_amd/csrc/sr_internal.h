@@ -1,0 +1,104 @@
+// Internal declarations and device helpers shared by the verify-step kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "specrouter.h"
+
+namespace sr {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kNegInf = -__builtin_inff();
+
+// Widen the two bf16 halves of a 32-bit word to fp32 (exact).
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Wave-wide reductions over the 64 lanes (result valid in every lane).
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x = fmaxf(x, __shfl_xor(x, off, 64));
+  return x;
+}
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
+  return x;
+}
+__device__ __forceinline__ double wave_sum_d(double x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
+  return x;
+}
+
+// Merge two (max, sum-of-exp2(x*log2e - max*log2e)) partials.
+__device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2) {
+  const float M = fmaxf(m, m2);
+  if (M == kNegInf) {
+    m = M;
+    s = 0.f;
+    return;
+  }
+  s = s * exp2f((m - M) * kLog2e) + s2 * exp2f((m2 - M) * kLog2e);
+  m = M;
+}
+
+// Device-scope (agent) synchronisation primitives.
+__device__ __forceinline__ uint32_t atomic_load_agent(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t atomic_add_release(uint32_t* p, uint32_t v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void fence_acquire_agent() {
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+}
+
+// ---------------------------------------------------------------------------
+// Host-side launchers (one per translation unit). Arguments are already
+// validated by the C ABI layer.
+
+struct AttentionPlan {
+  int nq;          // 16-row query groups per workgroup
+  int q_chunks;    // workgroups along the query rows of one (sequence, kv head)
+  int split_keys;  // keys per split (multiple of 32)
+  int n_splits;    // splits along the cache
+  size_t workspace_bytes;
+};
+
+int attention_plan(int B, int gamma_max, int Hq, int Hkv, int D, int L_cap, AttentionPlan* plan);
+
+int launch_verify_attention(const void* q, const void* k_cache, const void* v_cache,
+                            const uint8_t* cache_mask, const int32_t* kv_len,
+                            const int32_t* gamma, float* out, int B, int gamma_max, int Hq,
+                            int Hkv, int D, int L_cap, float scale, void* workspace,
+                            const AttentionPlan& plan, int32_t* status, hipStream_t stream);
+
+struct AcceptPlan {
+  int chunk;          // vocabulary entries per workgroup task
+  int n_chunks;       // chunks per row
+  int grid;           // persistent grid size (multiple of n_chunks)
+  size_t workspace_bytes;
+};
+
+int accept_plan(int B, int gamma_max, int V, int dtype, AcceptPlan* plan);
+
+int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, int64_t q_stride,
+                  int dtype, const int32_t* drafts, const int32_t* gamma, const float* u_acc,
+                  const float* u_res, const int32_t* kv_len, int32_t* accept_len,
+                  int32_t* out_tokens, int32_t* new_len, float* accept_prob, float* p_tok,
+                  float* q_tok, float* kl, float* tv, int B, int gamma_max, int V,
+                  void* workspace, const AcceptPlan& plan, int32_t* status, hipStream_t stream);
+
+int launch_rollback(int32_t* kv_len, uint8_t* cache_mask, const int32_t* new_len,
+                    int32_t* phys_len, int B, int L_cap, int32_t* status, hipStream_t stream);
+
+// Cached per-device properties.
+int device_cu_count();
+
+}  // namespace sr

@@ -1,0 +1,99 @@
+"""The C-ABI library loads and exports every symbol the header declares, and
+rejects bad host-side arguments before touching the device (CPU only)."""
+
+import ctypes
+import os
+
+import pytest
+
+from paper_2505_07680_amd import _lib
+
+
+# The argument-check tests pass placeholder addresses that must never reach a
+# kernel launch; they are host-logic tests and only run where no device is visible.
+no_device = pytest.mark.skipif(
+    __import__("torch").cuda.device_count() > 0, reason="host-only argument checks"
+)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2505_07680_amd.build import build
+
+        build()
+    return _lib.load()
+
+
+def test_header_declares_the_three_calls():
+    names = _lib.header_functions()
+    for n in ("specrouter_verify_attention", "specrouter_accept_and_diverge", "specrouter_rollback"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in _lib.header_functions():
+        assert hasattr(lib, name), name
+
+
+def test_version_and_status_strings(lib):
+    assert lib.specrouter_abi_version() == 1
+    for code in (0, -1, -2, -3, -4, 1, 2, 4, 8, 16, 32):
+        s = lib.specrouter_status_string(code)
+        assert s and s != b"unknown code"
+    assert lib.specrouter_status_string(12345) == b"unknown code"
+
+
+def _null():
+    return ctypes.c_void_p(0)
+
+
+@no_device
+def test_attention_rejects_bad_host_arguments(lib):
+    p = ctypes.c_void_p(4096)  # never dereferenced: every case fails before a launch
+    args = [p, p, p, None, p, p, p, 2, 4, 8, 2, 128, 512, 0.1, None, 0, None, None]
+    bad = list(args)
+    bad[0] = None
+    assert lib.specrouter_verify_attention(*bad) == _lib.SR_EINVAL
+    bad = list(args)
+    bad[9] = 3  # Hq % Hkv != 0
+    assert lib.specrouter_verify_attention(*bad) == _lib.SR_EINVAL
+    bad = list(args)
+    bad[11] = 96  # head dim
+    assert lib.specrouter_verify_attention(*bad) == _lib.SR_EUNSUPPORTED
+    bad = list(args)
+    bad[8] = 17  # gamma_max above 16
+    assert lib.specrouter_verify_attention(*bad) == _lib.SR_EINVAL
+    bad = list(args)
+    bad[0] = ctypes.c_void_p(4100)  # misaligned
+    assert lib.specrouter_verify_attention(*bad) == _lib.SR_EINVAL
+
+
+@no_device
+def test_accept_rejects_bad_host_arguments(lib):
+    p = ctypes.c_void_p(4096)
+    B, G, V = 2, 4, 1000
+    base = [p, (G + 1) * V, p, G * V, _lib.SR_F32] + [p] * 4 + [None] + [p, p] + [None] * 6 + [B, G, V, p, 1 << 20, None, None]
+    bad = list(base)
+    bad[4] = 7
+    assert lib.specrouter_accept_and_diverge(*bad) == _lib.SR_EUNSUPPORTED
+    bad = list(base)
+    bad[1] = V  # batch stride too small
+    assert lib.specrouter_accept_and_diverge(*bad) == _lib.SR_EINVAL
+    bad = list(base)
+    bad[20] = 1001  # fp32 rows of 1001 entries are not 16-byte multiples
+    bad[1], bad[3] = (G + 1) * 1001, G * 1001
+    assert lib.specrouter_accept_and_diverge(*bad) == _lib.SR_EUNSUPPORTED
+    bad = list(base)
+    bad[12] = p  # new_len without kv_len
+    assert lib.specrouter_accept_and_diverge(*bad) == _lib.SR_EINVAL
+    bad = list(base)
+    bad[2] = None  # q_logits missing with gamma_max > 0
+    assert lib.specrouter_accept_and_diverge(*bad) == _lib.SR_EINVAL
+
+
+@no_device
+def test_rollback_rejects_bad_host_arguments(lib):
+    p = ctypes.c_void_p(4096)
+    assert lib.specrouter_rollback(None, None, p, None, 4, 16, None, None) == _lib.SR_EINVAL
+    assert lib.specrouter_rollback(p, None, p, None, 0, 16, None, None) == _lib.SR_EINVAL

@@ -1,0 +1,318 @@
+"""GPU parity: the HIP verify step (through the C ABI) against the CPU
+reference on the same seeded inputs, at the parity tolerances:
+
+  * attention |o - o_ref| <= 2e-2 + 1e-2 |o_ref| (bf16 in, fp32 accumulate);
+  * accept lengths, emitted tokens and new lengths bit-exact, except sequences
+    whose reference decision margin is below 1e-6 (counted and reported);
+  * accept_prob / p_tok / q_tok within 1e-5 relative, KL / TV within 1e-4
+    relative (1e-7 absolute floor);
+  * rollback bit-exact.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from workloads import CONFIGS, level_inputs, small_shape
+from workloads.gen import bf16_bits_from_f32, f32_from_bf16_bits
+
+from gpu_util import (
+    check_accept,
+    check_attention,
+    dev,
+    host,
+    run_accept,
+    run_attention,
+    run_rollback,
+)
+
+pytestmark = pytest.mark.gpu
+
+
+def say(msg):
+    print(f"[gpu-test] {msg}", flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _library():
+    import paper_2505_07680_amd as sr
+
+    sr.load()  # raises if the HIP library is not built
+    assert torch.cuda.is_available()
+    yield
+    torch.cuda.synchronize()
+
+
+def _mask_holes(inp, frac, seed):
+    """Validity mask with holes below kv_len (rolled-back entries left in place)."""
+    rng = np.random.default_rng(seed)
+    B, cap = inp.kv_len.shape[0], inp.k.shape[2]
+    mask = np.zeros((B, cap), np.uint8)
+    for b in range(B):
+        L = int(inp.kv_len[b])
+        mask[b, :L] = (rng.random(L) >= frac).astype(np.uint8)
+        mask[b, L - int(inp.gamma[b]) - 1: L] = 1  # this step's rows are valid
+    return mask
+
+
+def full_step(inp, mask=None, att_seqs=None, acc_seqs=None, label=""):
+    say(f"{label}: attention B={inp.B} q={inp.q.shape} kv={inp.k.shape}")
+    att, st = run_attention(inp, mask)
+    ref, rst = oracle.verify_attention(inp.q, inp.k, inp.v, inp.kv_len, inp.gamma, inp.scale, mask,
+                                       seqs=att_seqs)
+    assert st == rst == 0
+    worst_l2 = check_attention(att, ref, seqs=att_seqs)
+    say(f"{label}: attention ok, worst relative L2 {worst_l2:.2e}; accept V={inp.p_logits.shape[2]}")
+    acc = run_accept(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, inp.u_acc, inp.u_res, inp.kv_len)
+    aref = oracle.accept_and_diverge(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, inp.u_acc,
+                                     inp.u_res, kv_len=inp.kv_len, seqs=acc_seqs)
+    assert acc["status"] == 0
+    nb, nbm = check_accept(acc, aref, seqs=acc_seqs)
+    say(f"{label}: accept ok ({nb} boundary cases, {nbm} differing); mean accept "
+        f"{np.mean(acc['accept_len']):.2f} of {np.mean(inp.gamma):.2f}")
+    # rollback to the reference's accepted prefix
+    kv2, m2, phys, st = run_rollback(inp.kv_len, mask, aref["new_len"] if acc_seqs is None else acc["new_len"],
+                                     inp.k.shape[2])
+    rkv, rm, rphys, rst = oracle.rollback(inp.kv_len, mask, aref["new_len"] if acc_seqs is None else acc["new_len"],
+                                          cap=inp.k.shape[2])
+    assert st == rst and phys == rphys
+    np.testing.assert_array_equal(kv2, rkv)
+    if mask is not None:
+        np.testing.assert_array_equal(m2, rm)
+    return att, acc, aref
+
+
+SMALL = [
+    small_shape(name="d128-g4-f32", seed=11),
+    small_shape(name="d64-mha-bf16", Hq=4, Hkv=4, D=64, V=2056, gamma=(1, 8), ctx=(1, 300),
+                logits="bf16", seed=12),
+    small_shape(name="d128-g8-gamma8-2chunks", B=3, Hq=16, Hkv=2, gamma=(8, 8), ctx=(500, 1500),
+                V=9000, seed=13),
+    small_shape(name="d64-g16-qchunks-bf16", B=2, Hq=32, Hkv=2, D=64, gamma=(3, 8), ctx=(100, 900),
+                V=20000, logits="bf16", seed=14),
+    small_shape(name="d128-gamma16-long", B=2, Hq=4, Hkv=2, gamma=(16, 16), ctx=(3000, 3500),
+                V=17000, seed=15),
+    small_shape(name="decode-gamma0", B=4, Hq=8, Hkv=2, D=64, gamma=(0, 0), ctx=(10, 2000),
+                V=1000, seed=16),
+]
+
+
+@pytest.mark.parametrize("shape", SMALL, ids=lambda s: s.name)
+@pytest.mark.parametrize("masked", [False, True], ids=["nomask", "mask"])
+def test_small_shapes(shape, masked):
+    inp = level_inputs(shape)
+    mask = _mask_holes(inp, 0.2, shape.seed) if masked else None
+    full_step(inp, mask, label=f"{shape.name}/{'mask' if masked else 'nomask'}")
+
+
+def test_config1_tiny():
+    inp = level_inputs(CONFIGS[1])
+    full_step(inp, label="config1")
+
+
+def test_config2_llama8b_b16():
+    inp = level_inputs(CONFIGS[2])
+    full_step(inp, label="config2")
+
+
+def test_config4_long_context():
+    inp = level_inputs(CONFIGS[4])
+    full_step(inp, label="config4")
+
+
+def test_config5_ragged_b256_sampled():
+    inp = level_inputs(CONFIGS[5])
+    L = inp.kv_len
+    order = np.argsort(L)
+    rng = np.random.default_rng(5)
+    att_seqs = sorted(set([int(order[0]), int(order[-1])] + rng.choice(inp.B, 10, replace=False).tolist()))
+    acc_seqs = sorted(set(att_seqs + rng.choice(inp.B, 40, replace=False).tolist()))
+    full_step(inp, att_seqs=att_seqs, acc_seqs=acc_seqs, label="config5")
+
+
+def test_config3_three_level_chain():
+    from workloads import chain_inputs
+
+    shape = CONFIGS[3]
+    say("config3: generating chain inputs")
+    ci = chain_inputs(shape)
+    B, ctx, gt = shape.B, shape.ctx, shape.gamma_tgt
+    inter = ci["inter"]
+    # intermediate level: full verify step
+    att, acc, aref = full_step(inter, att_seqs=range(0, B, 4), label="config3/intermediate")
+    # target level inputs from the reference's intermediate outcome
+    g3 = oracle.chain.target_window(aref["accept_len"], gt)
+    d3 = oracle.chain.target_drafts(aref["out_tokens"], g3, gt)
+    kv3 = (ctx + g3 + 1).astype(np.int32)
+    t = ci["target"]
+    z1, z2, z3 = ci["z"]
+    # target attention
+    from workloads.gen import LevelInputs
+
+    tin = LevelInputs(shape=shape, q=t["q"], k=t["k"], v=t["v"], kv_len=kv3, gamma=g3, mask=None,
+                      p_logits=t["p_logits"], q_logits=None, drafts=d3, u_acc=t["u_acc"],
+                      u_res=t["u_res"], scale=t["scale"])
+    say("config3/target: attention")
+    att3, st = run_attention(tin)
+    ref3, rst = oracle.verify_attention(tin.q, tin.k, tin.v, kv3, g3, tin.scale, seqs=range(0, B, 4))
+    assert st == rst == 0
+    check_attention(att3, ref3, seqs=range(0, B, 4))
+    # target accept: q rows are a strided view of the intermediate level's p logits
+    p_dev = dev(t["p_logits"])
+    z2_dev = dev(z2)  # [B, gamma_int+1, V]; the view keeps its batch stride
+    q_view = z2_dev[:, :gt]
+    acc3 = run_accept(t["p_logits"], None, d3, g3, t["u_acc"], t["u_res"], kv3, p_dev=p_dev, q_dev=q_view)
+    aref3 = oracle.accept_and_diverge(t["p_logits"], z2[:, :gt], d3, g3, t["u_acc"], t["u_res"], kv_len=kv3)
+    nb, nbm = check_accept(acc3, aref3)
+    say(f"config3/target: accept ok ({nb} boundary); mean k3 {acc3['accept_len'].mean():.2f}")
+    # consensus rollbacks
+    tgt_len, int_len, dr_len = oracle.chain.rollback_targets(ctx, aref["accept_len"], aref3["accept_len"])
+    for old, new, cap in ((kv3, tgt_len, shape.cap), (inter.kv_len, int_len, shape.cap)):
+        g_kv, _, g_phys, g_st = run_rollback(old, None, new, cap)
+        r_kv, _, r_phys, r_st = oracle.rollback(old, None, new, cap=cap)
+        np.testing.assert_array_equal(g_kv, r_kv)
+        assert g_phys == r_phys and g_st == r_st == 0
+    # draft level: one decode-attention call (gamma = 0)
+    d = ci["draft"]
+    din = LevelInputs(shape=shape, q=d["q"], k=d["k"], v=d["v"], kv_len=d["kv_len"],
+                      gamma=np.zeros(B, np.int32), mask=None, p_logits=None, q_logits=None,
+                      drafts=None, u_acc=None, u_res=None, scale=d["scale"])
+    attd, st = run_attention(din)
+    refd, _ = oracle.verify_attention(din.q, din.k, din.v, din.kv_len, din.gamma, din.scale, seqs=range(0, B, 4))
+    check_attention(attd, refd, seqs=range(0, B, 4))
+
+
+# ----------------------------------------------------------------------------- invariants
+
+def test_equal_draft_and_verifier_accepts_everything():
+    shape = small_shape(name="eq", B=6, V=5000, gamma=(1, 7), seed=21)
+    inp = level_inputs(shape, kv=False)
+    qlog = inp.p_logits[:, : shape.gmax].copy()
+    for b in range(inp.B):
+        qlog[b, int(inp.gamma[b]):] = np.nan
+    acc = run_accept(inp.p_logits, qlog, inp.drafts, inp.gamma, inp.u_acc, inp.u_res, inp.kv_len)
+    for b in range(inp.B):
+        g = int(inp.gamma[b])
+        assert acc["accept_len"][b] == g
+        assert (acc["kl"][b, :g] == 0).all() and (acc["tv"][b, :g] == 0).all()
+        assert (acc["accept_prob"][b, :g] == 1).all()
+    aref = oracle.accept_and_diverge(inp.p_logits, qlog, inp.drafts, inp.gamma, inp.u_acc, inp.u_res,
+                                     kv_len=inp.kv_len)
+    check_accept(acc, aref)
+
+
+def test_attention_ignores_nonfinite_dead_entries():
+    shape = small_shape(name="garbage", B=3, D=128, seed=22)
+    inp = level_inputs(shape)
+    mask = _mask_holes(inp, 0.3, 22)
+    base, _ = run_attention(inp, mask)
+    k2, v2 = inp.k.copy(), inp.v.copy()
+    for b in range(inp.B):
+        dead = np.flatnonzero(mask[b] == 0)
+        k2[b, :, dead] = 0x7FC0  # NaN
+        v2[b, :, dead] = 0x7F80  # +Inf
+    inp2 = level_inputs(shape, kv=False)
+    inp2.k, inp2.v = k2, v2
+    got, _ = run_attention(inp2, mask)
+    np.testing.assert_array_equal(got, base)
+
+
+def test_runs_are_bitwise_deterministic():
+    inp = level_inputs(small_shape(name="det", B=4, V=20000, seed=23))
+    a1, _ = run_attention(inp)
+    a2, _ = run_attention(inp)
+    np.testing.assert_array_equal(a1, a2)
+    r1 = run_accept(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, inp.u_acc, inp.u_res, inp.kv_len)
+    r2 = run_accept(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, inp.u_acc, inp.u_res, inp.kv_len)
+    for k in r1:
+        np.testing.assert_array_equal(r1[k], r2[k])
+
+
+def test_sharp_softmax_attention():
+    shape = small_shape(name="sharp", B=2, seed=24)
+    inp = level_inputs(shape)
+    q = bf16_bits_from_f32(f32_from_bf16_bits(inp.q) * 8.0)
+    got, _ = run_attention(inp, q=q)
+    ref, _ = oracle.verify_attention(q, inp.k, inp.v, inp.kv_len, inp.gamma, inp.scale)
+    check_attention(got, ref)
+
+
+def test_rollback_idempotent_and_eq9():
+    rng = np.random.default_rng(25)
+    B, L, cap = 37, 500, 512
+    mask = np.ones((B, cap), np.uint8)
+    r = rng.integers(0, 9, B)
+    kv = np.full(B, L, np.int32)
+    new = (L - r).astype(np.int32)
+    kv1, m1, phys1, st1 = run_rollback(kv, mask, new, cap)
+    kv2, m2, phys2, st2 = run_rollback(kv1, m1, new, cap)
+    np.testing.assert_array_equal(kv1, kv2)
+    np.testing.assert_array_equal(m1, m2)
+    assert phys1 == phys2 == L - r.min() and st1 == st2 == 0
+    rkv, rm, rphys, rst = oracle.rollback(kv, mask, new)
+    np.testing.assert_array_equal(kv1, rkv)
+    np.testing.assert_array_equal(m1, rm)
+
+
+def test_device_data_errors_are_flagged():
+    shape = small_shape(name="bad", B=5, V=1000, gamma=(2, 4), seed=26)
+    inp = level_inputs(shape)
+    gamma = inp.gamma.copy()
+    gamma[0] = shape.gmax + 1                 # bad gamma
+    drafts = inp.drafts.copy()
+    drafts[1, 0] = shape.V                    # bad token
+    u_res = inp.u_res.copy()
+    u_res[2, 0] = 1.0                         # bad uniform
+    kv_len = inp.kv_len.copy()
+    kv_len[3] = 1                             # kv_len < gamma + 1
+    acc = run_accept(inp.p_logits, inp.q_logits, drafts, gamma, inp.u_acc, u_res, kv_len)
+    ref = oracle.accept_and_diverge(inp.p_logits, inp.q_logits, drafts, gamma, inp.u_acc, u_res, kv_len=kv_len)
+    assert acc["status"] == ref["status"] == 1 | 2 | 4 | 8
+    for b in range(4):
+        assert acc["accept_len"][b] == -1 and (acc["out_tokens"][b] == -1).all()
+        assert acc["new_len"][b] == kv_len[b] and np.isnan(acc["kl"][b]).all()
+    check_accept(acc, ref, seqs=[4])
+    # attention: bad gamma / kv_len -> zero output and status bits
+    inp2 = level_inputs(shape)
+    inp2.gamma = gamma
+    inp2.kv_len = np.where(np.arange(5) == 3, shape.cap + 1, inp.kv_len).astype(np.int32)
+    out, st = run_attention(inp2)
+    assert st == 1 | 2
+    assert (out[0] == 0).all() and (out[3] == 0).all()
+    # rollback: growth and negative lengths
+    kv, m, phys, st = run_rollback([10, 10, 10], np.ones((3, 16), np.uint8), [12, -1, 4], 16)
+    assert list(kv) == [10, 10, 4] and st == 16 | 2 and phys == 10
+
+
+def test_sampler_statistics():
+    """The GPU sampler alone (no reference): with drafts drawn from q, the first
+    emitted token is distributed as p_0 and P(k >= i) = prod_{j<i} (1 - TV_j)."""
+    rng = np.random.default_rng(27)
+    V, g, B = 8, 3, 1 << 17
+    zp = rng.normal(0, 1.5, (g + 1, V)).astype(np.float32)
+    zq = (zp[:g] + rng.normal(0, 1.0, (g, V))).astype(np.float32)
+
+    def sm(z):
+        e = np.exp(z - z.max())
+        return e / e.sum()
+
+    p = [sm(zp[j].astype(np.float64)) for j in range(g + 1)]
+    q = [sm(zq[j].astype(np.float64)) for j in range(g)]
+    tv = [0.5 * np.abs(p[j] - q[j]).sum() for j in range(g)]
+    drafts = np.stack([rng.choice(V, size=B, p=q[j]) for j in range(g)], axis=1).astype(np.int32)
+    P = np.broadcast_to(zp, (B, g + 1, V)).copy()
+    Q = np.broadcast_to(zq, (B, g, V)).copy()
+    u_acc = rng.random((B, g), dtype=np.float32)
+    u_res = rng.random((B, g + 1), dtype=np.float32)
+    acc = run_accept(P, Q, drafts, np.full(B, g, np.int32), u_acc, u_res)
+    first = acc["out_tokens"][:, 0]
+    counts = np.bincount(first, minlength=V)
+    chi2 = (((counts - B * p[0]) ** 2) / (B * p[0])).sum()
+    assert chi2 < 30.0, chi2  # 7 degrees of freedom
+    k = acc["accept_len"]
+    surv = 1.0
+    for i in range(1, g + 1):
+        surv *= 1 - tv[i - 1]
+        emp = (k >= i).mean()
+        assert abs(emp - surv) < 5 * np.sqrt(surv * (1 - surv) / B) + 1e-4
