@@ -1,34 +1,41 @@
 // Accept-and-diverge for gfx950: speculative accept/reject with residual
 // resampling and the bonus token (Section 2.2 steps 3-4, probabilistic
 // acceptance), plus per-position total variation distance (Eq. 5) and KL
-// divergence, in one sweep over the verifier and draft logits.
+// divergence, with one sweep over the verifier and draft logits.
 //
 // Decomposition. A "row" is one (sequence b, position j) pair: for j < gamma_b
 // the verifier row p_j together with the draft row q_j, for j = gamma_b the
 // verifier row alone (it feeds the bonus token). Each row is cut into chunks
-// of 8192 vocabulary entries, one chunk per workgroup, and each of the
-// workgroup's four waves owns 2048 contiguous entries (32 per lane, loaded
-// with coalesced 16-byte loads and kept in registers).
+// of 256*E vocabulary entries, one chunk per workgroup task, and each of the
+// workgroup's four waves owns 64*E contiguous entries (E per lane, loaded with
+// coalesced 16-byte loads and kept in registers): a "span".
 //
-// Single sweep. TV and the residual max(0, p - q) need both rows' log-
-// normalisers, which depend on the whole row. Every wave therefore
+// Sweep kernel (the single pass over HBM). TV and the residual max(0, p - q)
+// need both rows' log-normalisers, which depend on the whole row, so every
+// wave
 //   1. computes its span's (max, sum of exp) for p and q and its share of
-//      sum p (z_p - z_q) (the KL numerator), publishes them, and waits at a
-//      per-row counter until every wave of the row has published;
-//   2. merges all partials of the row (in a fixed order, in fp64, so every wave
-//      gets bit-identical log-normalisers) and finishes TV and the residual mass
-//      of its span from the values still in registers.
-// The last wave to finish a row computes the row's TV, KL, p(x), q(x) and
-// acceptance probability; the last row of a sequence to finish runs the
-// sequence epilogue: the accept chain, and one token drawn by CDF inversion.
-// The inversion locates the 2048-entry span that holds the target from the
-// per-span residual (or p) masses and re-reads only that span, scanning it in
-// fp64 in ascending vocabulary order.
+//      sum p (z_p - z_q) (the KL numerator) and publishes them;
+//   2. once every span of the row has published, merges the partials (fixed
+//      order, fp64 sums, so every wave gets bit-identical log-normalisers)
+//      and finishes TV and the residual mass of its span from the values still
+//      in registers.
+// Each published value is one 64-bit word (value, call epoch), written and
+// polled with device-coherent atomics, so a reader needs no separate flag and
+// no cache maintenance, and nothing has to be cleared between calls. The loop
+// over tasks is software-pipelined: the next task's loads are in flight while
+// the wave waits for the current row.
 //
-// The grid is persistent and launched cooperatively, so all workgroups are
-// co-resident and the per-row wait always completes; a wait is still bounded
-// (SR_ST_TIMEOUT) so the kernel always drains. Counters live in the caller's
-// workspace and are reset by the kernel that used them.
+// Finish kernel (one workgroup per sequence, one wave per row). With every
+// partial in memory it computes each row's TV, KL, p(x), q(x) and acceptance
+// probability, runs the accept chain, and draws one token by CDF inversion:
+// the wave holding the sampling row finds the span that contains the target
+// from its per-span residual (or p) masses with a prefix scan, re-reads only
+// that span and scans it in fp64 in ascending vocabulary order. It then
+// advances the call epoch.
+//
+// The sweep grid is persistent and launched cooperatively, so all workgroups
+// are co-resident and every wait completes; waits are still bounded
+// (SR_ST_TIMEOUT) so the kernel always drains.
 
 #include <math.h>
 
@@ -39,20 +46,23 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
-constexpr int kE = 32;                  // entries per lane per row
-constexpr int kChunk = kThreads * kE;   // entries per workgroup task
-constexpr int kSpan = 64 * kE;          // contiguous entries per wave
+constexpr int kMaxSpans = 256;  // spans per row handled by the wave-parallel merges
+constexpr int kMaxRows = SPECROUTER_MAX_GAMMA + 1;
+constexpr int kSpanSlots = kMaxSpans / 64;
 constexpr uint32_t kSpinLimit = 1u << 22;
 
-struct WavePart {
-  float mp, sp, mq, sq, kl, tv, res, pad;
+// Per-span record. Tagged words (value bits | epoch << 32) for the values
+// read during the sweep; plain floats for the pass-2 values read after it.
+struct SpanRec {
+  uint64_t mp, sp, mq, sq, kl;
+  float tv, res;
 };
 
-struct RowRes {
-  double lp, lq, a;
-  int32_t ok;
-  int32_t pad;
+struct RowLogits {  // p and q logits of the row's draft token
+  float zp, zq;
 };
+
+typedef float floatx8 __attribute__((ext_vector_type(8)));
 
 template <bool BF16>
 struct Elt;
@@ -60,29 +70,24 @@ struct Elt;
 template <>
 struct Elt<false> {
   static constexpr int VEC = 4;
-  __device__ static void load(const void* row, int idx, float* o) {
-    const float4 v = *(const float4*)((const float*)row + idx);
-    o[0] = v.x;
-    o[1] = v.y;
-    o[2] = v.z;
-    o[3] = v.w;
-  }
+  typedef floatx4 Vec;
+  __device__ static Vec load(const void* row, int idx) { return *(const floatx4*)((const float*)row + idx); }
   __device__ static float one(const void* row, int idx) { return ((const float*)row)[idx]; }
 };
 
 template <>
 struct Elt<true> {
   static constexpr int VEC = 8;
-  __device__ static void load(const void* row, int idx, float* o) {
-    const uint4 u = *(const uint4*)((const uint16_t*)row + idx);
-    o[0] = bf16_lo(u.x);
-    o[1] = bf16_hi(u.x);
-    o[2] = bf16_lo(u.y);
-    o[3] = bf16_hi(u.y);
-    o[4] = bf16_lo(u.z);
-    o[5] = bf16_hi(u.z);
-    o[6] = bf16_lo(u.w);
-    o[7] = bf16_hi(u.w);
+  typedef floatx8 Vec;
+  __device__ static Vec load(const void* row, int idx) {
+    const u32x4 u = *(const u32x4*)((const uint16_t*)row + idx);
+    Vec o;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      o[2 * i] = bf16_lo(u[i]);
+      o[2 * i + 1] = bf16_hi(u[i]);
+    }
+    return o;
   }
   __device__ static float one(const void* row, int idx) {
     return __uint_as_float((uint32_t)((const uint16_t*)row)[idx] << 16);
@@ -107,52 +112,232 @@ struct Args {
   float* q_tok;
   float* kl;
   float* tv;
-  int B, gmax, V, n_chunks;
-  WavePart* parts;   // [rows][n_chunks * kWaves]
-  RowRes* rowres;    // [rows]
-  uint32_t* cnt1;    // [rows] waves past pass 1
-  uint32_t* cnt2;    // [rows] waves done with the row
-  uint32_t* cnt_seq; // [B] rows done
+  int B, gmax, V, n_chunks, chunk, span;
+  SpanRec* recs;      // [rows][spans]
+  RowLogits* rowx;    // [rows]
+  uint32_t* epoch;    // [1] epoch of the previous call
   int32_t* status;
 };
 
-__device__ __forceinline__ bool wait_count(const uint32_t* c, uint32_t target) {
-  uint32_t it = 0;
-  while (atomic_load_agent(c) < target) {
-    __builtin_amdgcn_s_sleep(2);
-    if (++it > kSpinLimit) return false;
-  }
-  return true;
+__device__ __forceinline__ uint64_t tag(float v, uint32_t ep) {
+  return (uint64_t)__float_as_uint(v) | ((uint64_t)ep << 32);
+}
+__device__ __forceinline__ float untag(uint64_t w) { return __uint_as_float((uint32_t)w); }
+__device__ __forceinline__ void st_dev(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t ld_dev(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// (max, sum) merge in fp64 of the partials of one row, identical in every wave.
-template <int FIELD_M, int FIELD_S>
-__device__ double row_lse(const WavePart* parts, int n) {
-  const int lane = threadIdx.x & 63;
-  double m = -INFINITY, s = 0.0;
-  for (int i = lane; i < n; i += 64) {
-    const float* f = (const float*)&parts[i];
-    const double m2 = f[FIELD_M], s2 = f[FIELD_S];
-    const double M = fmax(m, m2);
-    if (M != -INFINITY) {
-      s = s * exp(m - M) + s2 * exp(m2 - M);
-      m = M;
-    }
-  }
+// Merge (max, sum) pairs held lane-wise (up to kSpanSlots per lane) into the
+// row's natural-log normaliser; fixed order, fp64 sum.
+__device__ __forceinline__ double merge_lse(const float (&m)[kSpanSlots], const float (&s)[kSpanSlots], int nslot) {
+  float ml = kNegInf;
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    const double m2 = __shfl_xor(m, off, 64);
-    const double s2 = __shfl_xor(s, off, 64);
-    const double M = fmax(m, m2);
-    if (M != -INFINITY) {
-      s = s * exp(m - M) + s2 * exp(m2 - M);
-      m = M;
-    }
-  }
-  return m + log(s);
+  for (int i = 0; i < kSpanSlots; ++i)
+    if (i < nslot) ml = fmaxf(ml, m[i]);
+  const float M = wave_max(ml);
+  double acc = 0.0;
+#pragma unroll
+  for (int i = 0; i < kSpanSlots; ++i)
+    if (i < nslot && m[i] != kNegInf) acc += (double)s[i] * exp((double)m[i] - (double)M);
+  return (double)M + log(wave_sum_d(acc));
 }
+
+// ============================================================================
+// Sweep kernel
+
+struct Task {
+  int row, span, base, j;
+  bool exists, live, pair;
+  const void* prow;
+  const void* qrow;
+};
 
 template <bool BF16>
+__device__ __forceinline__ Task make_task(const Args& A, long task, long total, int w) {
+  Task t;
+  t.exists = task < total;
+  t.live = false;
+  t.pair = false;
+  if (!t.exists) return t;
+  const int G1 = A.gmax + 1;
+  t.row = (int)(task / A.n_chunks);
+  const int c = (int)(task % A.n_chunks);
+  const int b = t.row / G1;
+  t.j = t.row % G1;
+  const int gam = A.gamma[b];
+  t.live = gam >= 0 && gam <= A.gmax && t.j <= gam;
+  t.pair = t.live && t.j < gam;
+  t.span = c * kWaves + w;
+  t.base = c * A.chunk + w * A.span;
+  const size_t esz = BF16 ? 2 : 4;
+  t.prow = (const char*)A.p + ((size_t)b * A.p_stride + (size_t)t.j * A.V) * esz;
+  t.qrow = (const char*)A.q + ((size_t)b * A.q_stride + (size_t)t.j * A.V) * esz;
+  return t;
+}
+
+template <bool BF16, int E>
+__device__ __forceinline__ void load_span(const Args& A, const Task& t, float (&zp)[E], float (&zq)[E]) {
+  typedef Elt<BF16> L;
+  constexpr int VEC = L::VEC;
+  const int lane = threadIdx.x & 63;
+  if (!t.live) return;
+#pragma unroll
+  for (int v = 0; v < E / VEC; ++v) {
+    const int x = t.base + (v * 64 + lane) * VEC;
+    const bool in = x < A.V;
+    typename L::Vec pv, qv;
+    pv = kNegInf;
+    qv = kNegInf;
+    if (in) pv = L::load(t.prow, x);
+    if (in && t.pair) qv = L::load(t.qrow, x);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      zp[v * VEC + e] = pv[e];
+      zq[v * VEC + e] = qv[e];
+    }
+  }
+}
+
+// Pass 1: span maxima, exponentials (in place), sums and KL numerator; publish.
+template <bool BF16, int E>
+__device__ __forceinline__ void pass1(const Args& A, const Task& t, uint32_t ep_tag, float (&zp)[E],
+                                      float (&zq)[E], float& mp, float& mq) {
+  const int lane = threadIdx.x & 63;
+  if (!t.live) return;
+  mp = kNegInf;
+  mq = kNegInf;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    mp = fmaxf(mp, zp[e]);
+    mq = fmaxf(mq, zq[e]);
+  }
+  mp = wave_max(mp);
+  if (t.pair) mq = wave_max(mq);
+  const float rp = mp == kNegInf ? 0.f : mp * kLog2e;
+  const float rq = mq == kNegInf ? 0.f : mq * kLog2e;
+  float sp = 0.f, sq = 0.f, klp = 0.f;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const float ep = exp2f(fmaf(zp[e], kLog2e, -rp));
+    sp += ep;
+    if (t.pair) {
+      const float eq = exp2f(fmaf(zq[e], kLog2e, -rq));
+      sq += eq;
+      klp += ep > 0.f ? ep * (zp[e] - zq[e]) : 0.f;
+      zq[e] = eq;
+    }
+    zp[e] = ep;
+  }
+  sp = wave_sum(sp);
+  if (t.pair) {
+    sq = wave_sum(sq);
+    klp = wave_sum(klp);
+  }
+  SpanRec* rec = A.recs + (size_t)t.row * A.n_chunks * kWaves + t.span;
+  if (lane < 5) {
+    const float val = lane == 0 ? mp : lane == 1 ? sp : lane == 2 ? mq : lane == 3 ? sq : klp;
+    st_dev(&rec->mp + lane, tag(val, ep_tag));
+  }
+  if (t.pair && t.span == 0 && lane == 0) {
+    // the draft token's logits, for the acceptance probability
+    const int b = t.row / (A.gmax + 1);
+    const int x = A.drafts[(size_t)b * A.gmax + t.j];
+    if (x >= 0 && x < A.V) A.rowx[t.row] = RowLogits{Elt<BF16>::one(t.prow, x), Elt<BF16>::one(t.qrow, x)};
+  }
+}
+
+// Pass 2 (pair rows): wait for the row's partials, merge, TV and residual mass.
+template <int E>
+__device__ __forceinline__ void pass2(const Args& A, const Task& t, uint32_t ep_tag, const float (&zp)[E],
+                                      const float (&zq)[E], float mp, float mq) {
+  const int lane = threadIdx.x & 63;
+  if (!t.pair) return;
+  const int n_spans = A.n_chunks * kWaves;
+  const int nslot = (n_spans + 63) / 64;
+  const SpanRec* rr = A.recs + (size_t)t.row * n_spans;
+  float m1[kSpanSlots], s1[kSpanSlots], m2[kSpanSlots], s2[kSpanSlots];
+  bool ok = false;
+  for (uint32_t it = 0; it <= kSpinLimit; ++it) {
+    bool mine = true;
+#pragma unroll
+    for (int i = 0; i < kSpanSlots; ++i) {
+      const int s = lane * nslot + i;  // lane-major blocks: same merge order as the finish kernel
+      if (i < nslot && s < n_spans) {
+        const uint64_t a = ld_dev(&rr[s].mp), bq = ld_dev(&rr[s].sp), c = ld_dev(&rr[s].mq), d = ld_dev(&rr[s].sq);
+        mine = mine && (uint32_t)(a >> 32) == ep_tag && (uint32_t)(bq >> 32) == ep_tag &&
+               (uint32_t)(c >> 32) == ep_tag && (uint32_t)(d >> 32) == ep_tag;
+        m1[i] = untag(a);
+        s1[i] = untag(bq);
+        m2[i] = untag(c);
+        s2[i] = untag(d);
+      } else {
+        m1[i] = m2[i] = kNegInf;
+        s1[i] = s2[i] = 0.f;
+      }
+    }
+    if (__all(mine)) {
+      ok = true;
+      break;
+    }
+    __builtin_amdgcn_s_sleep(1);
+  }
+  if (!ok && lane == 0 && A.status) atomicOr(A.status, SR_ST_TIMEOUT);
+  const double Lp = merge_lse(m1, s1, nslot);
+  const double Lq = merge_lse(m2, s2, nslot);
+  const float fp = mp == kNegInf ? 0.f : (float)exp((double)mp - Lp);
+  const float fq = mq == kNegInf ? 0.f : (float)exp((double)mq - Lq);
+  float tvs = 0.f, res = 0.f;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    // separately rounded products (no fused multiply-add), so identical p and
+    // q rows give exactly zero
+#pragma clang fp contract(off)
+    const float d = zp[e] * fp - zq[e] * fq;
+    tvs += fabsf(d);
+    res += fmaxf(d, 0.f);
+  }
+  tvs = wave_sum(tvs);
+  res = wave_sum(res);
+  SpanRec* rec = A.recs + (size_t)t.row * n_spans + t.span;
+  if (lane < 2) (&rec->tv)[lane] = lane == 0 ? tvs : res;  // read only after the sweep
+}
+
+template <bool BF16, int E>
+__global__ void __launch_bounds__(kThreads)
+accept_sweep_kernel(Args A) {
+  const int w = threadIdx.x >> 6;
+  const long total = (long)A.B * (A.gmax + 1) * A.n_chunks;
+  const long stride = gridDim.x;
+  const uint32_t ep_tag = *A.epoch + 1u;  // this call's epoch; the finish kernel advances the stored one
+  float pa[E], qa[E], pb[E], qb[E];
+  float mpa = kNegInf, mqa = kNegInf, mpb = kNegInf, mqb = kNegInf;
+  long next = blockIdx.x;
+  Task ta = make_task<BF16>(A, next, total, w);
+  load_span<BF16, E>(A, ta, pa, qa);
+  pass1<BF16, E>(A, ta, ep_tag, pa, qa, mpa, mqa);
+  next += stride;
+  while (ta.exists) {
+    Task tb = make_task<BF16>(A, next, total, w);
+    load_span<BF16, E>(A, tb, pb, qb);  // in flight while waiting for ta's row
+    pass2<E>(A, ta, ep_tag, pa, qa, mpa, mqa);
+    if (!tb.exists) break;
+    pass1<BF16, E>(A, tb, ep_tag, pb, qb, mpb, mqb);
+    next += stride;
+    ta = make_task<BF16>(A, next, total, w);
+    load_span<BF16, E>(A, ta, pa, qa);
+    pass2<E>(A, tb, ep_tag, pb, qb, mpb, mqb);
+    if (!ta.exists) break;
+    pass1<BF16, E>(A, ta, ep_tag, pa, qa, mpa, mqa);
+    next += stride;
+  }
+}
+
+// ============================================================================
+// Finish kernel
+
 __device__ void write_invalid(const Args& A, int b, uint32_t bits) {
   const int lane = threadIdx.x & 63;
   if (lane == 0) {
@@ -172,137 +357,119 @@ __device__ void write_invalid(const Args& A, int b, uint32_t bits) {
   }
 }
 
-// Weight of vocabulary entry x of the sampling row, in fp64.
-template <bool BF16>
-__device__ __forceinline__ double sample_weight(const void* prow, const void* qrow, int x,
-                                                double lp, double lq, bool residual) {
-  const double pz = exp((double)Elt<BF16>::one(prow, x) - lp);
-  if (!residual) return pz;
-  const double qz = exp((double)Elt<BF16>::one(qrow, x) - lq);
-  return fmax(0.0, pz - qz);
+// Wave-wide inclusive prefix sum (fp64).
+__device__ __forceinline__ double wave_incl_scan(double x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const double y = __shfl_up(x, off, 64);
+    if (lane >= off) x += y;
+  }
+  return x;
 }
 
-// Sequence epilogue: accept chain, token draw, outputs. Run by one wave.
+struct RowRes {
+  double a;
+  float p_tok, q_tok, kl, tv;
+};
+
+// Draw one token from the row the wave holds. mass[i] is the mass of span
+// lane*nslot + i (spans in lane-major blocks so the prefix is a lane scan).
 template <bool BF16>
-__device__ void sequence_epilogue(const Args& A, int b) {
-  const int lane = threadIdx.x & 63;
-  const int gam = A.gamma[b];
-  const int rows_per_seq = A.gmax + 1;
-  // ---- data checks
-  uint32_t bad = 0;
-  for (int j = lane; j <= gam; j += 64) {
-    if (j < gam) {
-      const int x = A.drafts[(size_t)b * A.gmax + j];
-      if (x < 0 || x >= A.V) bad |= SR_ST_TOKEN;
-      const float u = A.u_acc[(size_t)b * A.gmax + j];
-      if (!(u >= 0.f && u < 1.f)) bad |= SR_ST_UNIFORM;
-    }
-    const float u = A.u_res[(size_t)b * rows_per_seq + j];
-    if (!(u >= 0.f && u < 1.f)) bad |= SR_ST_UNIFORM;
-  }
-  if (A.kv_len && lane == 0 && A.kv_len[b] < gam + 1) bad |= SR_ST_KVLEN;
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) bad |= __shfl_xor(bad, off, 64);
-  if (bad) {
-    write_invalid<BF16>(A, b, bad);
-    return;
-  }
-  // ---- accept chain
-  const RowRes* rr = A.rowres + (size_t)b * rows_per_seq;
-  int k = gam;
-  for (int j = 0; j < gam; ++j) {
-    const double u = (double)A.u_acc[(size_t)b * A.gmax + j];
-    if (!(u < rr[j].a)) {
-      k = j;
-      break;
-    }
-  }
-  // ---- span masses of the sampling row
-  const int row = b * rows_per_seq + k;
-  const WavePart* parts = A.parts + (size_t)row * A.n_chunks * kWaves;
-  const int n_spans = A.n_chunks * kWaves;
-  const double lp = rr[k].lp, lq = rr[k].lq;
-  bool residual = k < gam;
-  double W = 0.0;
-  if (residual) {
-    for (int s = 0; s < n_spans; ++s) W += (double)parts[s].res;
-    if (!(W > 0.0)) residual = false;
-  }
-  if (!residual) {
-    W = 0.0;
-    for (int s = 0; s < n_spans; ++s)
-      if (parts[s].mp != -INFINITY) W += (double)parts[s].sp * exp((double)parts[s].mp - lp);
-  }
-  const double target = (double)A.u_res[(size_t)b * rows_per_seq + k] * W;
-  // locate the span
-  int s0 = 0;
-  double prefix = 0.0;
-  int last_pos = -1;
-  for (int s = 0; s < n_spans; ++s) {
-    const double ws = residual ? (double)parts[s].res
-                               : (parts[s].mp == -INFINITY ? 0.0 : (double)parts[s].sp * exp((double)parts[s].mp - lp));
-    if (ws > 0.0) last_pos = s;
-    if (ws > 0.0 && prefix + ws > target) {
-      s0 = s;
-      break;
-    }
-    prefix += ws;
-    s0 = s + 1;
-  }
-  if (s0 >= n_spans) {  // rounding left the target past the last mass: take the last span with mass
-    s0 = last_pos < 0 ? 0 : last_pos;
-    prefix = 0.0;
-    for (int s = 0; s < s0; ++s)
-      prefix += residual ? (double)parts[s].res
-                         : (parts[s].mp == -INFINITY ? 0.0 : (double)parts[s].sp * exp((double)parts[s].mp - lp));
-  }
-  // ---- scan spans s0.. in fp64, ascending vocabulary order
-  const void* prow = (const char*)A.p + ((size_t)b * A.p_stride + (size_t)k * A.V) * (BF16 ? 2 : 4);
-  const void* qrow = residual ? (const char*)A.q + ((size_t)b * A.q_stride + (size_t)k * A.V) * (BF16 ? 2 : 4) : nullptr;
+__device__ int draw_token(const Args& A, int b, int k, bool residual, double lp, double lq,
+                          const double (&mass)[kSpanSlots], int n_spans) {
   constexpr int VEC = Elt<BF16>::VEC;
+  const int lane = threadIdx.x & 63;
+  const int nslot = (n_spans + 63) / 64;
+  const int G1 = A.gmax + 1;
+  double my = 0.0;
+  int my_last = -1;
+#pragma unroll
+  for (int i = 0; i < kSpanSlots; ++i) {
+    if (i < nslot) {
+      my += mass[i];
+      if (mass[i] > 0.0) my_last = lane * nslot + i;
+    }
+  }
+  const double incl = wave_incl_scan(my);
+  const double W = __shfl(incl, 63, 64);
+  const double target = (double)A.u_res[(size_t)b * G1 + k] * W;
+  int last_span = my_last;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) last_span = max(last_span, __shfl_xor(last_span, off, 64));
+  int s0 = -1;
+  double prefix = 0.0;
+  const unsigned long long hit = __ballot(incl > target && my > 0.0);
+  if (hit) {
+    const int hl = __ffsll((long long)hit) - 1;
+    double c = incl - my;
+    int found = -1;
+    double pre = 0.0;
+#pragma unroll
+    for (int i = 0; i < kSpanSlots; ++i) {
+      if (i < nslot && found < 0 && mass[i] > 0.0 && c + mass[i] > target) {
+        found = lane * nslot + i;
+        pre = c;
+      }
+      if (i < nslot) c += mass[i];
+    }
+    s0 = __shfl(found, hl, 64);
+    prefix = __shfl(pre, hl, 64);
+  }
+  if (s0 < 0) {  // rounding put the target past the total: the last span with mass
+    s0 = max(last_span, 0);
+    double pre = 0.0;
+#pragma unroll
+    for (int i = 0; i < kSpanSlots; ++i)
+      if (i < nslot && lane * nslot + i < s0) pre += mass[i];
+    prefix = wave_sum_d(pre);
+  }
+  // scan spans s0.. in fp64, ascending vocabulary order
+  const size_t esz = BF16 ? 2 : 4;
+  const void* prow = (const char*)A.p + ((size_t)b * A.p_stride + (size_t)k * A.V) * esz;
+  const void* qrow = residual ? (const char*)A.q + ((size_t)b * A.q_stride + (size_t)k * A.V) * esz : nullptr;
+  const int E = A.span / 64;
   double rem = target - prefix;
   int tok = -1;
   int last_tok = -1;
   for (int s = s0; s < n_spans && tok < 0; ++s) {
-    const int base = (s / kWaves) * kChunk + (s % kWaves) * kSpan;
-    for (int v = 0; v < kE / VEC && tok < 0; ++v) {
+    const int base = (s / kWaves) * A.chunk + (s % kWaves) * A.span;
+    for (int v = 0; v < E / VEC && tok < 0; ++v) {
       const int x0 = base + (v * 64 + lane) * VEC;
       double wl[VEC];
       double sum = 0.0;
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
-        wl[e] = (x0 + e < A.V) ? sample_weight<BF16>(prow, qrow, x0 + e, lp, lq, residual) : 0.0;
-        sum += wl[e];
+        double wt = 0.0;
+        if (x0 + e < A.V) {
+          wt = exp((double)Elt<BF16>::one(prow, x0 + e) - lp);
+          if (residual) wt = fmax(0.0, wt - exp((double)Elt<BF16>::one(qrow, x0 + e) - lq));
+        }
+        wl[e] = wt;
+        sum += wt;
       }
-      // inclusive scan over lanes
-      double incl = sum;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const double y = __shfl_up(incl, off, 64);
-        if (lane >= off) incl += y;
-      }
-      const double total = __shfl(incl, 63, 64);
-      // last entry with positive weight so far (fallback)
-      int my_last = -1;
+      const double inc = wave_incl_scan(sum);
+      const double total = __shfl(inc, 63, 64);
+      int mine = -1;
 #pragma unroll
       for (int e = 0; e < VEC; ++e)
-        if (wl[e] > 0.0) my_last = x0 + e;
-      int lmax = my_last;
+        if (wl[e] > 0.0) mine = x0 + e;
+      int lmax = mine;
 #pragma unroll
       for (int off = 32; off > 0; off >>= 1) lmax = max(lmax, __shfl_xor(lmax, off, 64));
       if (lmax >= 0) last_tok = lmax;
       if (rem < total) {
-        const unsigned long long hit = __ballot(incl > rem);
-        const int hl = __ffsll((long long)hit) - 1;
+        const unsigned long long h = __ballot(inc > rem);
+        const int hl = __ffsll((long long)h) - 1;
         int found = -1;
         if (lane == hl) {
-          double c = incl - sum;
+          double c = inc - sum;
 #pragma unroll
           for (int e = 0; e < VEC; ++e) {
             c += wl[e];
             if (found < 0 && wl[e] > 0.0 && c > rem) found = x0 + e;
           }
-          if (found < 0) found = my_last;
+          if (found < 0) found = mine;
         }
         tok = __shfl(found, hl, 64);
       } else {
@@ -311,22 +478,164 @@ __device__ void sequence_epilogue(const Args& A, int b) {
     }
   }
   if (tok < 0) tok = last_tok < 0 ? 0 : last_tok;
-  // ---- outputs
-  int32_t* ot = A.out_tokens + (size_t)b * rows_per_seq;
-  for (int j = lane; j <= A.gmax; j += 64) {
-    int v = -1;
-    if (j < k) v = A.drafts[(size_t)b * A.gmax + j];
-    else if (j == k) v = tok;
-    ot[j] = v;
+  return tok;
+}
+
+template <bool BF16>
+__global__ void __launch_bounds__(1024)
+accept_finish_kernel(Args A) {
+  __shared__ RowRes rr[kMaxRows];
+  __shared__ uint32_t s_bad;
+  const int b = blockIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int nw = blockDim.x >> 6;
+  const int G1 = A.gmax + 1;
+  const int n_spans = A.n_chunks * kWaves;
+  const int nslot = (n_spans + 63) / 64;
+  const int gam = A.gamma[b];
+  if (b == 0 && threadIdx.x == 0) *A.epoch = *A.epoch + 1u;  // the sweep is over: next call's epoch
+  if (gam < 0 || gam > A.gmax) {
+    if (w == 0) write_invalid(A, b, SR_ST_GAMMA);
+    return;  // the sweep touched no row of this sequence
   }
+  if (threadIdx.x == 0) s_bad = 0;
+  __syncthreads();
+  // ---- data checks
+  uint32_t bad = 0;
+  for (int j = threadIdx.x; j <= gam; j += blockDim.x) {
+    if (j < gam) {
+      const int x = A.drafts[(size_t)b * A.gmax + j];
+      if (x < 0 || x >= A.V) bad |= SR_ST_TOKEN;
+      const float u = A.u_acc[(size_t)b * A.gmax + j];
+      if (!(u >= 0.f && u < 1.f)) bad |= SR_ST_UNIFORM;
+    }
+    const float u = A.u_res[(size_t)b * G1 + j];
+    if (!(u >= 0.f && u < 1.f)) bad |= SR_ST_UNIFORM;
+  }
+  if (threadIdx.x == 0 && A.kv_len && A.kv_len[b] < gam + 1) bad |= SR_ST_KVLEN;
+  if (bad) atomicOr(&s_bad, bad);
+  // ---- finalise rows (one wave per row); spans in lane-major blocks of nslot
+  double lp_k = 0.0, lq_k = 0.0;
+  double mass[kSpanSlots];
+  int my_row = -1;
+  for (int j = w; j <= gam; j += nw) {
+    const SpanRec* rp = A.recs + (size_t)(b * G1 + j) * n_spans;
+    const bool pair = j < gam;
+    float mp[kSpanSlots], sp[kSpanSlots], mq[kSpanSlots], sq[kSpanSlots], klv[kSpanSlots], tvv[kSpanSlots],
+        rsv[kSpanSlots];
+#pragma unroll
+    for (int i = 0; i < kSpanSlots; ++i) {
+      const int s = lane * nslot + i;
+      const bool in = i < nslot && s < n_spans;
+      mp[i] = in ? untag(rp[s].mp) : kNegInf;
+      sp[i] = in ? untag(rp[s].sp) : 0.f;
+      mq[i] = in && pair ? untag(rp[s].mq) : kNegInf;
+      sq[i] = in && pair ? untag(rp[s].sq) : 0.f;
+      klv[i] = in && pair ? untag(rp[s].kl) : 0.f;
+      tvv[i] = in && pair ? rp[s].tv : 0.f;
+      rsv[i] = in && pair ? rp[s].res : 0.f;
+    }
+    const double Lp = merge_lse(mp, sp, nslot);
+    double Lq = 0.0, tvd = 0.0, kld = 0.0;
+    if (pair) {
+      Lq = merge_lse(mq, sq, nslot);
+#pragma unroll
+      for (int i = 0; i < kSpanSlots; ++i) {
+        tvd += (double)tvv[i];
+        if (mp[i] != kNegInf) kld += (double)klv[i] * exp((double)mp[i] - Lp);
+      }
+      tvd = 0.5 * wave_sum_d(tvd);
+      kld = wave_sum_d(kld) - (Lp - Lq);
+    }
+    // span masses for a possible draw from this row: residual (pair rows) and p
+    double res_tot = 0.0;
+#pragma unroll
+    for (int i = 0; i < kSpanSlots; ++i) res_tot += (double)rsv[i];
+    const bool residual = pair && wave_sum_d(res_tot) > 0.0;
+#pragma unroll
+    for (int i = 0; i < kSpanSlots; ++i)
+      mass[i] = residual ? (double)rsv[i] : (mp[i] == kNegInf ? 0.0 : (double)sp[i] * exp((double)mp[i] - Lp));
+    my_row = j;
+    lp_k = Lp;
+    lq_k = Lq;
+    if (lane == 0) {
+      double a = 1.0, pt = __builtin_nan(""), qt = __builtin_nan("");
+      if (pair) {
+        const int x = A.drafts[(size_t)b * A.gmax + j];
+        a = __builtin_nan("");
+        if (x >= 0 && x < A.V) {
+          const RowLogits rl = A.rowx[b * G1 + j];
+          const double lpx = (double)rl.zp - Lp;
+          const double lqx = (double)rl.zq - Lq;
+          pt = exp(lpx);
+          qt = exp(lqx);
+          a = (lqx == -INFINITY || lpx >= lqx) ? 1.0 : exp(lpx - lqx);
+        }
+      }
+      rr[j] = RowRes{a, (float)pt, (float)qt, (float)kld, (float)tvd};
+    }
+    // a wave keeps the masses of its last row only; more rows than waves
+    // (gamma_max = 16) are re-derived below by the owning wave if needed
+    if (j + nw <= gam) my_row = -1;
+  }
+  __syncthreads();
+  if (s_bad) {
+    if (w == 0) write_invalid(A, b, s_bad);
+    return;
+  }
+  // ---- accept chain: first j with NOT (u_acc < a_j) (every wave computes it)
+  bool rej = false;
+  if (lane < gam) rej = !((double)A.u_acc[(size_t)b * A.gmax + lane] < rr[lane].a);
+  const unsigned long long rmask = __ballot(rej);
+  const int k = rmask ? (__ffsll((long long)rmask) - 1) : gam;
+  const int owner = k % nw;
+  if (w != owner) return;
+  if (my_row != k) {
+    // the owning wave processed row k before its last row: rebuild its masses
+    const SpanRec* rp = A.recs + (size_t)(b * G1 + k) * n_spans;
+    const bool pair = k < gam;
+    float mp[kSpanSlots], sp[kSpanSlots], mq[kSpanSlots], sq[kSpanSlots], rsv[kSpanSlots];
+#pragma unroll
+    for (int i = 0; i < kSpanSlots; ++i) {
+      const int s = lane * nslot + i;
+      const bool in = i < nslot && s < n_spans;
+      mp[i] = in ? untag(rp[s].mp) : kNegInf;
+      sp[i] = in ? untag(rp[s].sp) : 0.f;
+      mq[i] = in && pair ? untag(rp[s].mq) : kNegInf;
+      sq[i] = in && pair ? untag(rp[s].sq) : 0.f;
+      rsv[i] = in && pair ? rp[s].res : 0.f;
+    }
+    lp_k = merge_lse(mp, sp, nslot);
+    lq_k = pair ? merge_lse(mq, sq, nslot) : 0.0;
+    double res_tot = 0.0;
+#pragma unroll
+    for (int i = 0; i < kSpanSlots; ++i) res_tot += (double)rsv[i];
+    const bool residual = pair && wave_sum_d(res_tot) > 0.0;
+#pragma unroll
+    for (int i = 0; i < kSpanSlots; ++i)
+      mass[i] = residual ? (double)rsv[i] : (mp[i] == kNegInf ? 0.0 : (double)sp[i] * exp((double)mp[i] - lp_k));
+  }
+  bool residual = false;
+  if (k < gam) {
+    double tot = 0.0;
+    const SpanRec* rp = A.recs + (size_t)(b * G1 + k) * n_spans;
+    for (int s = lane; s < n_spans; s += 64) tot += (double)rp[s].res;
+    residual = wave_sum_d(tot) > 0.0;
+  }
+  const int tok = draw_token<BF16>(A, b, k, residual, lp_k, lq_k, mass, n_spans);
+  // ---- outputs
+  int32_t* ot = A.out_tokens + (size_t)b * G1;
+  for (int j = lane; j <= A.gmax; j += 64) ot[j] = j < k ? A.drafts[(size_t)b * A.gmax + j] : (j == k ? tok : -1);
   const float nan = __builtin_nanf("");
-  for (int j = gam + lane; j < A.gmax; j += 64) {
+  for (int j = lane; j < A.gmax; j += 64) {
     const size_t o = (size_t)b * A.gmax + j;
-    if (A.accept_prob) A.accept_prob[o] = nan;
-    if (A.p_tok) A.p_tok[o] = nan;
-    if (A.q_tok) A.q_tok[o] = nan;
-    if (A.kl) A.kl[o] = nan;
-    if (A.tv) A.tv[o] = nan;
+    const bool live = j < gam;
+    if (A.accept_prob) A.accept_prob[o] = live ? (float)rr[j].a : nan;
+    if (A.p_tok) A.p_tok[o] = live ? rr[j].p_tok : nan;
+    if (A.q_tok) A.q_tok[o] = live ? rr[j].q_tok : nan;
+    if (A.kl) A.kl[o] = live ? rr[j].kl : nan;
+    if (A.tv) A.tv[o] = live ? rr[j].tv : nan;
   }
   if (lane == 0) {
     A.accept_len[b] = k;
@@ -334,199 +643,43 @@ __device__ void sequence_epilogue(const Args& A, int b) {
   }
 }
 
-template <bool BF16>
-__global__ void __launch_bounds__(kThreads)
-accept_kernel(Args A) {
-  constexpr int VEC = Elt<BF16>::VEC;
-  constexpr int NV = kE / VEC;
-  const int lane = threadIdx.x & 63;
-  const int w = threadIdx.x >> 6;
-  const int rows_per_seq = A.gmax + 1;
-  const long total_tasks = (long)A.B * rows_per_seq * A.n_chunks;
-  const int n_spans = A.n_chunks * kWaves;
-
-  for (long task = blockIdx.x; task < total_tasks; task += gridDim.x) {
-    const int row = (int)(task / A.n_chunks);
-    const int c = (int)(task % A.n_chunks);
-    const int b = row / rows_per_seq;
-    const int j = row % rows_per_seq;
-    const int gam = A.gamma[b];
-    if (gam < 0 || gam > A.gmax) {
-      if (j == 0 && c == 0 && w == 0) write_invalid<BF16>(A, b, SR_ST_GAMMA);
-      continue;
-    }
-    if (j > gam) continue;
-    const bool pair = j < gam;
-    const int span = c * kWaves + w;
-    const int base = c * kChunk + w * kSpan;
-    WavePart* rparts = A.parts + (size_t)row * n_spans;
-    const void* prow = (const char*)A.p + ((size_t)b * A.p_stride + (size_t)j * A.V) * (BF16 ? 2 : 4);
-    const void* qrow = (const char*)A.q + ((size_t)b * A.q_stride + (size_t)j * A.V) * (BF16 ? 2 : 4);
-
-    // ---- load this wave's span (kept in registers through pass 2)
-    float zp[kE], zq[kE];
-#pragma unroll
-    for (int v = 0; v < NV; ++v) {
-      const int x = base + (v * 64 + lane) * VEC;
-      if (x < A.V) {
-        Elt<BF16>::load(prow, x, zp + v * VEC);
-        if (pair) Elt<BF16>::load(qrow, x, zq + v * VEC);
-      } else {
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) zp[v * VEC + e] = kNegInf;
-      }
-      if (!pair || x >= A.V) {
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) zq[v * VEC + e] = kNegInf;
-      }
-    }
-    // ---- pass 1: span maxima, exp sums, KL numerator
-    float mp = kNegInf, mq = kNegInf;
-#pragma unroll
-    for (int e = 0; e < kE; ++e) {
-      mp = fmaxf(mp, zp[e]);
-      mq = fmaxf(mq, zq[e]);
-    }
-    mp = wave_max(mp);
-    mq = wave_max(mq);
-    const float rp = mp == kNegInf ? 0.f : mp * kLog2e;
-    const float rq = mq == kNegInf ? 0.f : mq * kLog2e;
-    float sp = 0.f, sq = 0.f, klp = 0.f;
-#pragma unroll
-    for (int e = 0; e < kE; ++e) {
-      const float ep = exp2f(fmaf(zp[e], kLog2e, -rp));
-      const float eq = exp2f(fmaf(zq[e], kLog2e, -rq));
-      sp += ep;
-      sq += eq;
-      klp += ep > 0.f ? ep * (zp[e] - zq[e]) : 0.f;
-      zp[e] = ep;  // keep the exponentials for pass 2
-      zq[e] = eq;
-    }
-    sp = wave_sum(sp);
-    if (pair) {
-      sq = wave_sum(sq);
-      klp = wave_sum(klp);
-    }
-    if (lane == 0) {
-      WavePart& wp = rparts[span];
-      wp.mp = mp;
-      wp.sp = sp;
-      wp.mq = mq;
-      wp.sq = sq;
-      wp.kl = klp;
-      wp.tv = 0.f;
-      wp.res = 0.f;
-    }
-    bool ok = true;
-    if (pair) {
-      // ---- barrier: all waves of the row have published pass 1
-      if (lane == 0) atomic_add_release(A.cnt1 + row, 1u);
-      ok = wait_count(A.cnt1 + row, (uint32_t)n_spans);
-      fence_acquire_agent();
-      const double Lp = row_lse<0, 1>(rparts, n_spans);
-      const double Lq = row_lse<2, 3>(rparts, n_spans);
-      // ---- pass 2: TV and residual mass of this span
-      const float fp = mp == kNegInf ? 0.f : (float)exp((double)mp - Lp);
-      const float fq = mq == kNegInf ? 0.f : (float)exp((double)mq - Lq);
-      float tvs = 0.f, res = 0.f;
-#pragma unroll
-      for (int e = 0; e < kE; ++e) {
-        const float d = zp[e] * fp - zq[e] * fq;
-        tvs += fabsf(d);
-        res += fmaxf(d, 0.f);
-      }
-      tvs = wave_sum(tvs);
-      res = wave_sum(res);
-      if (lane == 0) {
-        rparts[span].tv = tvs;
-        rparts[span].res = res;
-      }
-    }
-    if (!ok && lane == 0 && A.status) atomicOr(A.status, SR_ST_TIMEOUT);
-    // ---- last wave of the row finalises it
-    uint32_t prev = 0;
-    if (lane == 0) prev = atomic_add_release(A.cnt2 + row, 1u);
-    prev = __shfl(prev, 0, 64);
-    if (prev != (uint32_t)n_spans - 1) continue;
-    fence_acquire_agent();
-    {
-      const double Lp = row_lse<0, 1>(rparts, n_spans);
-      double Lq = 0.0, tvd = 0.0, kld = 0.0;
-      if (pair) {
-        Lq = row_lse<2, 3>(rparts, n_spans);
-        for (int i = lane; i < n_spans; i += 64) {
-          tvd += (double)rparts[i].tv;
-          if (rparts[i].mp != -INFINITY) kld += (double)rparts[i].kl * exp((double)rparts[i].mp - Lp);
-        }
-        tvd = 0.5 * wave_sum_d(tvd);
-        kld = wave_sum_d(kld) - (Lp - Lq);
-      }
-      if (lane == 0) {
-        RowRes& r = A.rowres[row];
-        r.lp = Lp;
-        r.lq = Lq;
-        r.a = 1.0;
-        if (pair) {
-          const int x = A.drafts[(size_t)b * A.gmax + j];
-          const size_t o = (size_t)b * A.gmax + j;
-          double pt = __builtin_nan(""), qt = __builtin_nan(""), a = __builtin_nan("");
-          if (x >= 0 && x < A.V) {
-            const double lpx = (double)Elt<BF16>::one(prow, x) - Lp;
-            const double lqx = (double)Elt<BF16>::one(qrow, x) - Lq;
-            pt = exp(lpx);
-            qt = exp(lqx);
-            a = (lqx == -INFINITY || lpx >= lqx) ? 1.0 : exp(lpx - lqx);
-          }
-          r.a = a;
-          if (A.accept_prob) A.accept_prob[o] = (float)a;
-          if (A.p_tok) A.p_tok[o] = (float)pt;
-          if (A.q_tok) A.q_tok[o] = (float)qt;
-          if (A.kl) A.kl[o] = (float)kld;
-          if (A.tv) A.tv[o] = (float)tvd;
-        }
-        __hip_atomic_store(A.cnt1 + row, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(A.cnt2 + row, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
-    }
-    // ---- last row of the sequence runs the epilogue
-    if (lane == 0) prev = atomic_add_release(A.cnt_seq + b, 1u);
-    prev = __shfl(prev, 0, 64);
-    if (prev != (uint32_t)gam) continue;
-    fence_acquire_agent();
-    sequence_epilogue<BF16>(A, b);
-    if (lane == 0) __hip_atomic_store(A.cnt_seq + b, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-}
+// Entries per lane per row: the sweep's register tile.
+constexpr int kE = 16;
 
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 struct Layout {
-  size_t parts, rowres, cnt1, cnt2, cnt_seq, total;
+  size_t recs, rowx, epoch, total;
 };
 
 Layout layout(int B, int gamma_max, int n_chunks) {
   const size_t rows = (size_t)B * (gamma_max + 1);
+  const size_t spans = rows * n_chunks * kWaves;
   Layout L;
-  L.parts = 0;
-  L.rowres = L.parts + align256(rows * n_chunks * kWaves * sizeof(WavePart));
-  L.cnt1 = L.rowres + align256(rows * sizeof(RowRes));
-  L.cnt2 = L.cnt1 + align256(rows * sizeof(uint32_t));
-  L.cnt_seq = L.cnt2 + align256(rows * sizeof(uint32_t));
-  L.total = L.cnt_seq + align256((size_t)B * sizeof(uint32_t));
+  L.recs = 0;
+  L.rowx = L.recs + align256(spans * sizeof(SpanRec));
+  L.epoch = L.rowx + align256(rows * sizeof(RowLogits));
+  L.total = L.epoch + 256;
   return L;
+}
+
+const void* sweep_for(int dtype) {
+  return dtype == SR_BF16 ? (const void*)accept_sweep_kernel<true, kE>
+                          : (const void*)accept_sweep_kernel<false, kE>;
 }
 
 }  // namespace
 
 int accept_plan(int B, int gamma_max, int V, int dtype, AcceptPlan* plan) {
-  plan->chunk = kChunk;
-  plan->n_chunks = (V + kChunk - 1) / kChunk;
+  plan->chunk = kThreads * kE;
+  plan->n_chunks = (V + plan->chunk - 1) / plan->chunk;
+  if (plan->n_chunks * kWaves > kMaxSpans) return SR_EUNSUPPORTED;
   plan->workspace_bytes = layout(B, gamma_max, plan->n_chunks).total;
   const int cus = device_cu_count();
   if (cus <= 0) return SR_ELAUNCH;
   int per_cu = 0;
-  const void* fn = dtype == SR_BF16 ? (const void*)accept_kernel<true> : (const void*)accept_kernel<false>;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kThreads, 0) != hipSuccess || per_cu < 1)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sweep_for(dtype), kThreads, 0) != hipSuccess ||
+      per_cu < 1)
     return SR_ELAUNCH;
   const long tasks = (long)B * (gamma_max + 1) * plan->n_chunks;
   long grid = (long)cus * per_cu;
@@ -567,16 +720,22 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
   A.gmax = gamma_max;
   A.V = V;
   A.n_chunks = plan.n_chunks;
-  A.parts = (WavePart*)(ws + L.parts);
-  A.rowres = (RowRes*)(ws + L.rowres);
-  A.cnt1 = (uint32_t*)(ws + L.cnt1);
-  A.cnt2 = (uint32_t*)(ws + L.cnt2);
-  A.cnt_seq = (uint32_t*)(ws + L.cnt_seq);
+  A.chunk = plan.chunk;
+  A.span = plan.chunk / kWaves;
+  A.recs = (SpanRec*)(ws + L.recs);
+  A.rowx = (RowLogits*)(ws + L.rowx);
+  A.epoch = (uint32_t*)(ws + L.epoch);
   A.status = status;
   void* args[] = {&A};
-  const void* fn = dtype == SR_BF16 ? (const void*)accept_kernel<true> : (const void*)accept_kernel<false>;
-  const hipError_t e = hipLaunchCooperativeKernel(fn, dim3(plan.grid), dim3(kThreads), args, 0, stream);
-  return e == hipSuccess ? SR_OK : SR_ELAUNCH;
+  if (hipLaunchCooperativeKernel(sweep_for(dtype), dim3(plan.grid), dim3(kThreads), args, 0, stream) !=
+      hipSuccess)
+    return SR_ELAUNCH;
+  const int nw = gamma_max + 1 < 16 ? gamma_max + 1 : 16;
+  if (dtype == SR_BF16)
+    hipLaunchKernelGGL(accept_finish_kernel<true>, dim3(B), dim3(64 * nw), 0, stream, A);
+  else
+    hipLaunchKernelGGL(accept_finish_kernel<false>, dim3(B), dim3(64 * nw), 0, stream, A);
+  return hipGetLastError() == hipSuccess ? SR_OK : SR_ELAUNCH;
 }
 
 }  // namespace sr
