@@ -19,23 +19,25 @@
 //      order, fp64 sums, so every wave gets bit-identical log-normalisers)
 //      and finishes TV and the residual mass of its span from the values still
 //      in registers.
-// Each published value is one 64-bit word (value, call epoch), written and
-// polled with device-coherent atomics, so a reader needs no separate flag and
-// no cache maintenance, and nothing has to be cleared between calls. The loop
-// over tasks is software-pipelined: the next task's loads are in flight while
-// the wave waits for the current row.
+// Partials are written with device-coherent stores; once a workgroup's
+// stores have completed it bumps the row's counter (one atomic per
+// workgroup), and a single lane polls that counter, so waiting costs no
+// memory traffic beyond one word and no cache maintenance is needed. The
+// sweep launches one workgroup per (row, chunk) task, in row-major order.
 //
 // Finish kernel (one workgroup per sequence, one wave per row). With every
 // partial in memory it computes each row's TV, KL, p(x), q(x) and acceptance
 // probability, runs the accept chain, and draws one token by CDF inversion:
 // the wave holding the sampling row finds the span that contains the target
 // from its per-span residual (or p) masses with a prefix scan, re-reads only
-// that span and scans it in fp64 in ascending vocabulary order. It then
-// advances the call epoch.
+// that span and scans it in fp64 in ascending vocabulary order. It also
+// resets the sweep's row counters for the next call.
 //
-// The sweep grid is persistent and launched cooperatively, so all workgroups
-// are co-resident and every wait completes; waits are still bounded
-// (SR_ST_TIMEOUT) so the kernel always drains.
+// A workgroup waits only for the other workgroups of its own row, which have
+// neighbouring indices: workgroups are dispatched in index order, so the
+// earlier rows never wait on later ones and the rows complete in order as
+// slots free up (a row needs only its own chunks resident at once). Waits are
+// still bounded (SR_ST_TIMEOUT) so the kernel always drains.
 
 #include <math.h>
 
@@ -51,11 +53,9 @@ constexpr int kMaxRows = SPECROUTER_MAX_GAMMA + 1;
 constexpr int kSpanSlots = kMaxSpans / 64;
 constexpr uint32_t kSpinLimit = 1u << 22;
 
-// Per-span record. Tagged words (value bits | epoch << 32) for the values
-// read during the sweep; plain floats for the pass-2 values read after it.
+// Per-span partial record.
 struct SpanRec {
-  uint64_t mp, sp, mq, sq, kl;
-  float tv, res;
+  float mp, sp, mq, sq, kl, tv, res, pad;
 };
 
 struct RowLogits {  // p and q logits of the row's draft token
@@ -115,19 +115,25 @@ struct Args {
   int B, gmax, V, n_chunks, chunk, span;
   SpanRec* recs;      // [rows][spans]
   RowLogits* rowx;    // [rows]
-  uint32_t* epoch;    // [1] epoch of the previous call
+  uint32_t* cnt;      // [rows] workgroups whose pass-1 partials are complete
   int32_t* status;
 };
 
-__device__ __forceinline__ uint64_t tag(float v, uint32_t ep) {
-  return (uint64_t)__float_as_uint(v) | ((uint64_t)ep << 32);
-}
-__device__ __forceinline__ float untag(uint64_t w) { return __uint_as_float((uint32_t)w); }
-__device__ __forceinline__ void st_dev(uint64_t* p, uint64_t v) {
+__device__ __forceinline__ void st_dev(float* p, float v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ uint64_t ld_dev(const uint64_t* p) {
+__device__ __forceinline__ float ld_dev(const float* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t ld_dev(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Wait until this wave's earlier stores have completed (they are then visible
+// to device-coherent loads anywhere on the device).
+__device__ __forceinline__ void stores_done() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
 // Merge (max, sum) pairs held lane-wise (up to kSpanSlots per lane) into the
@@ -203,8 +209,8 @@ __device__ __forceinline__ void load_span(const Args& A, const Task& t, float (&
 
 // Pass 1: span maxima, exponentials (in place), sums and KL numerator; publish.
 template <bool BF16, int E>
-__device__ __forceinline__ void pass1(const Args& A, const Task& t, uint32_t ep_tag, float (&zp)[E],
-                                      float (&zq)[E], float& mp, float& mq) {
+__device__ __forceinline__ void pass1(const Args& A, const Task& t, float (&zp)[E], float (&zq)[E], float& mp,
+                                      float& mq) {
   const int lane = threadIdx.x & 63;
   if (!t.live) return;
   mp = kNegInf;
@@ -239,7 +245,7 @@ __device__ __forceinline__ void pass1(const Args& A, const Task& t, uint32_t ep_
   SpanRec* rec = A.recs + (size_t)t.row * A.n_chunks * kWaves + t.span;
   if (lane < 5) {
     const float val = lane == 0 ? mp : lane == 1 ? sp : lane == 2 ? mq : lane == 3 ? sq : klp;
-    st_dev(&rec->mp + lane, tag(val, ep_tag));
+    st_dev(&rec->mp + lane, val);
   }
   if (t.pair && t.span == 0 && lane == 0) {
     // the draft token's logits, for the acceptance probability
@@ -249,42 +255,25 @@ __device__ __forceinline__ void pass1(const Args& A, const Task& t, uint32_t ep_
   }
 }
 
-// Pass 2 (pair rows): wait for the row's partials, merge, TV and residual mass.
+// Pass 2 (pair rows, after the row's counter is complete): merge, TV and
+// residual mass of this span.
 template <int E>
-__device__ __forceinline__ void pass2(const Args& A, const Task& t, uint32_t ep_tag, const float (&zp)[E],
-                                      const float (&zq)[E], float mp, float mq) {
+__device__ __forceinline__ void pass2(const Args& A, const Task& t, const float (&zp)[E], const float (&zq)[E],
+                                      float mp, float mq) {
   const int lane = threadIdx.x & 63;
-  if (!t.pair) return;
   const int n_spans = A.n_chunks * kWaves;
   const int nslot = (n_spans + 63) / 64;
   const SpanRec* rr = A.recs + (size_t)t.row * n_spans;
   float m1[kSpanSlots], s1[kSpanSlots], m2[kSpanSlots], s2[kSpanSlots];
-  bool ok = false;
-  for (uint32_t it = 0; it <= kSpinLimit; ++it) {
-    bool mine = true;
 #pragma unroll
-    for (int i = 0; i < kSpanSlots; ++i) {
-      const int s = lane * nslot + i;  // lane-major blocks: same merge order as the finish kernel
-      if (i < nslot && s < n_spans) {
-        const uint64_t a = ld_dev(&rr[s].mp), bq = ld_dev(&rr[s].sp), c = ld_dev(&rr[s].mq), d = ld_dev(&rr[s].sq);
-        mine = mine && (uint32_t)(a >> 32) == ep_tag && (uint32_t)(bq >> 32) == ep_tag &&
-               (uint32_t)(c >> 32) == ep_tag && (uint32_t)(d >> 32) == ep_tag;
-        m1[i] = untag(a);
-        s1[i] = untag(bq);
-        m2[i] = untag(c);
-        s2[i] = untag(d);
-      } else {
-        m1[i] = m2[i] = kNegInf;
-        s1[i] = s2[i] = 0.f;
-      }
-    }
-    if (__all(mine)) {
-      ok = true;
-      break;
-    }
-    __builtin_amdgcn_s_sleep(1);
+  for (int i = 0; i < kSpanSlots; ++i) {
+    const int s = lane * nslot + i;  // lane-major blocks: same merge order as the finish kernel
+    const bool in = i < nslot && s < n_spans;
+    m1[i] = in ? ld_dev(&rr[s].mp) : kNegInf;
+    s1[i] = in ? ld_dev(&rr[s].sp) : 0.f;
+    m2[i] = in ? ld_dev(&rr[s].mq) : kNegInf;
+    s2[i] = in ? ld_dev(&rr[s].sq) : 0.f;
   }
-  if (!ok && lane == 0 && A.status) atomicOr(A.status, SR_ST_TIMEOUT);
   const double Lp = merge_lse(m1, s1, nslot);
   const double Lq = merge_lse(m2, s2, nslot);
   const float fp = mp == kNegInf ? 0.f : (float)exp((double)mp - Lp);
@@ -308,31 +297,35 @@ __device__ __forceinline__ void pass2(const Args& A, const Task& t, uint32_t ep_
 template <bool BF16, int E>
 __global__ void __launch_bounds__(kThreads)
 accept_sweep_kernel(Args A) {
+  __shared__ uint32_t s_ok;
   const int w = threadIdx.x >> 6;
   const long total = (long)A.B * (A.gmax + 1) * A.n_chunks;
-  const long stride = gridDim.x;
-  const uint32_t ep_tag = *A.epoch + 1u;  // this call's epoch; the finish kernel advances the stored one
-  float pa[E], qa[E], pb[E], qb[E];
-  float mpa = kNegInf, mqa = kNegInf, mpb = kNegInf, mqb = kNegInf;
-  long next = blockIdx.x;
-  Task ta = make_task<BF16>(A, next, total, w);
-  load_span<BF16, E>(A, ta, pa, qa);
-  pass1<BF16, E>(A, ta, ep_tag, pa, qa, mpa, mqa);
-  next += stride;
-  while (ta.exists) {
-    Task tb = make_task<BF16>(A, next, total, w);
-    load_span<BF16, E>(A, tb, pb, qb);  // in flight while waiting for ta's row
-    pass2<E>(A, ta, ep_tag, pa, qa, mpa, mqa);
-    if (!tb.exists) break;
-    pass1<BF16, E>(A, tb, ep_tag, pb, qb, mpb, mqb);
-    next += stride;
-    ta = make_task<BF16>(A, next, total, w);
-    load_span<BF16, E>(A, ta, pa, qa);
-    pass2<E>(A, tb, ep_tag, pb, qb, mpb, mqb);
-    if (!ta.exists) break;
-    pass1<BF16, E>(A, ta, ep_tag, pa, qa, mpa, mqa);
-    next += stride;
+  const Task t = make_task<BF16>(A, blockIdx.x, total, w);
+  if (!t.live) return;  // workgroup-uniform
+  float zp[E], zq[E];
+  float mp = kNegInf, mq = kNegInf;
+  load_span<BF16, E>(A, t, zp, zq);
+  pass1<BF16, E>(A, t, zp, zq, mp, mq);
+  if (!t.pair) return;
+  // ---- wait until every chunk of the row has published pass 1
+  stores_done();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t* c = A.cnt + t.row;
+    __hip_atomic_fetch_add(c, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint32_t ok = 0;
+    for (uint32_t it = 0; it <= kSpinLimit; ++it) {
+      if (ld_dev(c) >= (uint32_t)A.n_chunks) {
+        ok = 1;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+    }
+    if (!ok && A.status) atomicOr(A.status, SR_ST_TIMEOUT);
+    s_ok = ok;
   }
+  __syncthreads();
+  pass2<E>(A, t, zp, zq, mp, mq);
 }
 
 // ============================================================================
@@ -494,7 +487,6 @@ accept_finish_kernel(Args A) {
   const int n_spans = A.n_chunks * kWaves;
   const int nslot = (n_spans + 63) / 64;
   const int gam = A.gamma[b];
-  if (b == 0 && threadIdx.x == 0) *A.epoch = *A.epoch + 1u;  // the sweep is over: next call's epoch
   if (gam < 0 || gam > A.gmax) {
     if (w == 0) write_invalid(A, b, SR_ST_GAMMA);
     return;  // the sweep touched no row of this sequence
@@ -515,6 +507,8 @@ accept_finish_kernel(Args A) {
   }
   if (threadIdx.x == 0 && A.kv_len && A.kv_len[b] < gam + 1) bad |= SR_ST_KVLEN;
   if (bad) atomicOr(&s_bad, bad);
+  // ---- reset the sweep's row counters for the next call
+  for (int j = threadIdx.x; j < gam; j += blockDim.x) A.cnt[b * G1 + j] = 0u;
   // ---- finalise rows (one wave per row); spans in lane-major blocks of nslot
   double lp_k = 0.0, lq_k = 0.0;
   double mass[kSpanSlots];
@@ -528,11 +522,11 @@ accept_finish_kernel(Args A) {
     for (int i = 0; i < kSpanSlots; ++i) {
       const int s = lane * nslot + i;
       const bool in = i < nslot && s < n_spans;
-      mp[i] = in ? untag(rp[s].mp) : kNegInf;
-      sp[i] = in ? untag(rp[s].sp) : 0.f;
-      mq[i] = in && pair ? untag(rp[s].mq) : kNegInf;
-      sq[i] = in && pair ? untag(rp[s].sq) : 0.f;
-      klv[i] = in && pair ? untag(rp[s].kl) : 0.f;
+      mp[i] = in ? rp[s].mp : kNegInf;
+      sp[i] = in ? rp[s].sp : 0.f;
+      mq[i] = in && pair ? rp[s].mq : kNegInf;
+      sq[i] = in && pair ? rp[s].sq : 0.f;
+      klv[i] = in && pair ? rp[s].kl : 0.f;
       tvv[i] = in && pair ? rp[s].tv : 0.f;
       rsv[i] = in && pair ? rp[s].res : 0.f;
     }
@@ -600,10 +594,10 @@ accept_finish_kernel(Args A) {
     for (int i = 0; i < kSpanSlots; ++i) {
       const int s = lane * nslot + i;
       const bool in = i < nslot && s < n_spans;
-      mp[i] = in ? untag(rp[s].mp) : kNegInf;
-      sp[i] = in ? untag(rp[s].sp) : 0.f;
-      mq[i] = in && pair ? untag(rp[s].mq) : kNegInf;
-      sq[i] = in && pair ? untag(rp[s].sq) : 0.f;
+      mp[i] = in ? rp[s].mp : kNegInf;
+      sp[i] = in ? rp[s].sp : 0.f;
+      mq[i] = in && pair ? rp[s].mq : kNegInf;
+      sq[i] = in && pair ? rp[s].sq : 0.f;
       rsv[i] = in && pair ? rp[s].res : 0.f;
     }
     lp_k = merge_lse(mp, sp, nslot);
@@ -649,7 +643,7 @@ constexpr int kE = 16;
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 struct Layout {
-  size_t recs, rowx, epoch, total;
+  size_t recs, rowx, cnt, total;
 };
 
 Layout layout(int B, int gamma_max, int n_chunks) {
@@ -658,14 +652,9 @@ Layout layout(int B, int gamma_max, int n_chunks) {
   Layout L;
   L.recs = 0;
   L.rowx = L.recs + align256(spans * sizeof(SpanRec));
-  L.epoch = L.rowx + align256(rows * sizeof(RowLogits));
-  L.total = L.epoch + 256;
+  L.cnt = L.rowx + align256(rows * sizeof(RowLogits));
+  L.total = L.cnt + align256(rows * sizeof(uint32_t));
   return L;
-}
-
-const void* sweep_for(int dtype) {
-  return dtype == SR_BF16 ? (const void*)accept_sweep_kernel<true, kE>
-                          : (const void*)accept_sweep_kernel<false, kE>;
 }
 
 }  // namespace
@@ -675,17 +664,9 @@ int accept_plan(int B, int gamma_max, int V, int dtype, AcceptPlan* plan) {
   plan->n_chunks = (V + plan->chunk - 1) / plan->chunk;
   if (plan->n_chunks * kWaves > kMaxSpans) return SR_EUNSUPPORTED;
   plan->workspace_bytes = layout(B, gamma_max, plan->n_chunks).total;
-  const int cus = device_cu_count();
-  if (cus <= 0) return SR_ELAUNCH;
-  int per_cu = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sweep_for(dtype), kThreads, 0) != hipSuccess ||
-      per_cu < 1)
-    return SR_ELAUNCH;
   const long tasks = (long)B * (gamma_max + 1) * plan->n_chunks;
-  long grid = (long)cus * per_cu;
-  if (grid > tasks) grid = tasks;
-  grid = grid / plan->n_chunks * plan->n_chunks;
-  if (grid < plan->n_chunks) return SR_EUNSUPPORTED;  // a row would not fit on the device at once
+  if (tasks > 0x7fffffffL) return SR_EINVAL;
+  const long grid = tasks;
   plan->grid = (int)grid;
   return SR_OK;
 }
@@ -724,12 +705,14 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
   A.span = plan.chunk / kWaves;
   A.recs = (SpanRec*)(ws + L.recs);
   A.rowx = (RowLogits*)(ws + L.rowx);
-  A.epoch = (uint32_t*)(ws + L.epoch);
+  A.cnt = (uint32_t*)(ws + L.cnt);
   A.status = status;
-  void* args[] = {&A};
-  if (hipLaunchCooperativeKernel(sweep_for(dtype), dim3(plan.grid), dim3(kThreads), args, 0, stream) !=
-      hipSuccess)
-    return SR_ELAUNCH;
+  const long tasks = (long)B * (gamma_max + 1) * plan.n_chunks;
+  if (dtype == SR_BF16)
+    hipLaunchKernelGGL((accept_sweep_kernel<true, kE>), dim3((unsigned)tasks), dim3(kThreads), 0, stream, A);
+  else
+    hipLaunchKernelGGL((accept_sweep_kernel<false, kE>), dim3((unsigned)tasks), dim3(kThreads), 0, stream, A);
+  if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
   const int nw = gamma_max + 1 < 16 ? gamma_max + 1 : 16;
   if (dtype == SR_BF16)
     hipLaunchKernelGGL(accept_finish_kernel<true>, dim3(B), dim3(64 * nw), 0, stream, A);

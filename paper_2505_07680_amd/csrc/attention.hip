@@ -3,23 +3,24 @@
 // Work decomposition. One workgroup (4 waves) handles one (sequence b, kv head
 // g, query chunk, key split). All G*(gamma_b+1) query rows that read kv head g
 // (the GQA group times the new positions) are processed together, so every K/V
-// byte of the split is read from HBM exactly once. Inside the workgroup each
-// wave owns 32 of every 128 keys and keeps its own online-softmax state; the
-// four states are merged through LDS at the end. Splits of one (b, g) are
-// merged by a small combine kernel (skipped when one split covers the cache).
+// byte of the split is read from HBM exactly once. Each wave owns 16 of every
+// 64 keys and keeps its own online-softmax state (no workgroup barrier inside
+// the key loop); the four states are merged through LDS at the end. Splits of
+// one (b, g) are merged by a small combine kernel (skipped when one split
+// covers the cache).
 //
-// Per 32-key wave tile:
-//   * K and V rows are fetched with coalesced 16-byte loads (one tile ahead,
-//     held in registers) and staged in a wave-private LDS region; V rows that
-//     are invalid (past the split/kv_len, or mask 0) are zeroed while staging,
-//     so whatever those rows hold never reaches the output;
-//   * S^T = K Q^T on MFMA (v_mfma_f32_16x16x32_bf16: keys x queries, K=32 over
-//     the head dimension); each lane then holds 8 scores of ONE query, so the
-//     softmax max/sum need only two cross-lane steps;
-//   * P is rounded to bf16 in place and used directly as the B operand of
-//     O^T += V^T P^T (the contraction order over keys is permuted identically
-//     in both operands, so no register shuffle is needed); the V^T operand is
-//     gathered from LDS with 16-bit reads.
+// Per 16-key wave tile:
+//   * K and V rows are fetched with coalesced 16-byte loads into a two-deep
+//     register ring, so two tiles are in flight while one is computed, and
+//     staged in a wave-private LDS slot; V rows that are invalid (past the
+//     split/kv_len, or mask 0) are zeroed while staging, so whatever those
+//     rows hold never reaches the output;
+//   * S^T = K Q^T on MFMA (v_mfma_f32_16x16x32_bf16: 16 keys x 16 queries per
+//     block, K=32 over the head dimension); each lane then holds 4 scores of
+//     ONE query, so the softmax max/sum need only two cross-lane steps;
+//   * P is rounded to bf16 in place: its accumulator layout is exactly the B
+//     operand of O^T += V^T P^T (v_mfma_f32_16x16x16_bf16, K=16 over the keys);
+//     the V^T operand is gathered from LDS with 16-bit reads.
 // Scores are kept in log2 units (scale * log2(e) folded in) and exponentiated
 // with exp2.
 
@@ -28,10 +29,12 @@
 namespace sr {
 namespace {
 
+typedef short shortx4 __attribute__((ext_vector_type(4)));
+
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
-constexpr int kKeysPerWave = 32;
-constexpr int kTileKeys = kWaves * kKeysPerWave;
+constexpr int kWaveKeys = 16;
+constexpr int kTileKeys = kWaves * kWaveKeys;
 constexpr int kMaxNQ = 5;
 
 template <int D>
@@ -40,9 +43,9 @@ struct Geo {
   static constexpr int kVStride = D * 2 + 8;   // LDS bytes per staged V row
   static constexpr int kChunksPerRow = D / 8;  // 16-byte chunks per row
   static constexpr int kRowsPerLoad = 64 / kChunksPerRow;
-  static constexpr int kLoads = kKeysPerWave / kRowsPerLoad;
-  static constexpr int kWaveK = kKeysPerWave * kKStride;
-  static constexpr int kWaveBytes = kWaveK + kKeysPerWave * kVStride;
+  static constexpr int kLoads = kWaveKeys / kRowsPerLoad;  // 16-byte loads per lane per tensor per tile
+  static constexpr int kSlotK = kWaveKeys * kKStride;
+  static constexpr int kWaveBytes = kSlotK + kWaveKeys * kVStride;
 };
 
 template <int D, int NQ>
@@ -59,8 +62,28 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
 }
 
+// Order LDS accesses of one wave around a point (compiler barrier; the LDS
+// unit serves one wave's requests in order).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+template <int D>
+struct Stage {  // one 16-key wave tile in flight
+  u32x4 k[Geo<D>::kLoads], v[Geo<D>::kLoads];
+  uint32_t mbyte;  // validity byte of key (lane mod 16), evaluated when consumed
+};
+
+// 2 waves per SIMD for up to 3 query groups (all fits in 256 registers).
+template <int NQ>
+struct Occ {
+  static constexpr int kMinWaves = NQ <= 3 ? 2 : 1;
+};
+
 template <int D, int NQ>
-__global__ void __launch_bounds__(kThreads)
+__global__ void __launch_bounds__(kThreads, Occ<NQ>::kMinWaves)
 attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
                   const uint16_t* __restrict__ vc, const uint8_t* __restrict__ mask,
                   const int32_t* __restrict__ kv_len, const int32_t* __restrict__ gamma,
@@ -124,9 +147,10 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
     }
     *(u32x4*)(qst + rl * GG::kKStride + c * 16) = val;
   }
+  __syncthreads();
 
   unsigned char* kst = lds + w * GG::kWaveBytes;
-  unsigned char* vst = kst + GG::kWaveK;
+  unsigned char* vst = kst + GG::kSlotK;
   const size_t slab = ((size_t)b * Hkv + g) * (size_t)L_cap;
   const uint16_t* kslab = kc + slab * D;
   const uint16_t* vslab = vc + slab * D;
@@ -143,130 +167,121 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
     for (int db = 0; db < DB; ++db) o[db][qg] = floatx4{0.f, 0.f, 0.f, 0.f};
   }
 
-  u32x4 kr[GG::kLoads], vr[GG::kLoads];
-  uint32_t mbit = 0;
-  auto fetch = [&](int t) __attribute__((always_inline)) {
-    const int kb0 = key_begin + t * kTileKeys + w * kKeysPerWave;
-    if (kb0 < key_end) {
+  const int n_tiles = (key_end - key_begin + kTileKeys - 1) / kTileKeys;
+
+  // Loads are unconditional (rows clamped to the split's last valid key), so
+  // the loop body issues a fixed number of loads per tile and each stage
+  // waits only for its own loads; refetches past the end hit the same line.
+  const uint8_t* mload = mrow ? mrow : (const uint8_t*)kslab;
+  auto fetch = [&](int t, Stage<D>& st) __attribute__((always_inline)) {
+    const int kb0 = key_begin + t * kTileKeys + w * kWaveKeys;
 #pragma unroll
-      for (int u = 0; u < GG::kLoads; ++u) {
-        int row = kb0 + u * GG::kRowsPerLoad + lane / GG::kChunksPerRow;
-        row = min(row, L_cap - 1);
-        const size_t off = (size_t)row * D + (lane % GG::kChunksPerRow) * 8;
-        kr[u] = *(const u32x4*)(kslab + off);
-        vr[u] = *(const u32x4*)(vslab + off);
-      }
-      const int key = kb0 + lane;
-      mbit = (lane < kKeysPerWave && key < key_end) ? (mrow ? (mrow[key] != 0) : 1u) : 0u;
+    for (int u = 0; u < GG::kLoads; ++u) {
+      const int row = min(kb0 + u * GG::kRowsPerLoad + lane / GG::kChunksPerRow, key_end - 1);
+      const size_t off = (size_t)row * D + (lane % GG::kChunksPerRow) * 8;
+      st.k[u] = *(const u32x4*)(kslab + off);
+      st.v[u] = *(const u32x4*)(vslab + off);
     }
+    st.mbyte = mload[min(kb0 + (lane & (kWaveKeys - 1)), key_end - 1)];
   };
 
-  const int n_tiles = (key_end - key_begin + kTileKeys - 1) / kTileKeys;
-  fetch(0);
-  for (int t = 0; t < n_tiles; ++t) {
-    const int kb0 = key_begin + t * kTileKeys + w * kKeysPerWave;
-    const bool live = kb0 < key_end;  // wave-uniform
-    uint32_t vbits = 0;
-    if (live) {
-      vbits = (uint32_t)__ballot(mbit != 0);
+  auto consume = [&](int t, Stage<D>& st) __attribute__((always_inline)) {
+    const int kb0 = key_begin + t * kTileKeys + w * kWaveKeys;
+    const bool key_ok = lane < kWaveKeys && kb0 + lane < key_end && (mrow == nullptr || st.mbyte != 0u);
+    const uint32_t vbits = (uint32_t)__ballot(key_ok) & 0xffffu;
 #pragma unroll
-      for (int u = 0; u < GG::kLoads; ++u) {
-        const int rl = u * GG::kRowsPerLoad + lane / GG::kChunksPerRow;
-        const int c = lane % GG::kChunksPerRow;
-        *(u32x4*)(kst + rl * GG::kKStride + c * 16) = kr[u];
-        const u32x4 vv = ((vbits >> rl) & 1u) ? vr[u] : u32x4{0u, 0u, 0u, 0u};
-        uint32_t* dst = (uint32_t*)(vst + rl * GG::kVStride + c * 16);
-        *(uint2*)dst = make_uint2(vv.x, vv.y);
-        *(uint2*)(dst + 2) = make_uint2(vv.z, vv.w);
-      }
+    for (int u = 0; u < GG::kLoads; ++u) {
+      const int rl = u * GG::kRowsPerLoad + lane / GG::kChunksPerRow;
+      const int c = lane % GG::kChunksPerRow;
+      *(u32x4*)(kst + rl * GG::kKStride + c * 16) = st.k[u];
+      const u32x4 vv = ((vbits >> rl) & 1u) ? st.v[u] : u32x4{0u, 0u, 0u, 0u};
+      uint32_t* dst = (uint32_t*)(vst + rl * GG::kVStride + c * 16);
+      *(uint2*)dst = make_uint2(vv.x, vv.y);
+      *(uint2*)(dst + 2) = make_uint2(vv.z, vv.w);
     }
-    __syncthreads();
-    if (t + 1 < n_tiles) fetch(t + 1);
-    if (live) {
-      // ---- S^T = K Q^T (keys x queries)
-      floatx4 sacc[2][NQ];
+    wave_lds_sync();
+    fetch(t + 2, st);  // refill this ring entry: two tiles in flight during the compute below
+    if (t >= n_tiles || kb0 >= key_end) return;  // wave-uniform: nothing of this tile to compute
+    // ---- S^T = K Q^T (16 keys x 16 queries per group)
+    floatx4 sacc[NQ];
 #pragma unroll
-      for (int qg = 0; qg < NQ; ++qg) sacc[0][qg] = sacc[1][qg] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int qg = 0; qg < NQ; ++qg) sacc[qg] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int ks = 0; ks < D / 32; ++ks) {
-        const int col = (ks * 32 + lg * 8) * 2;
-        const bf16x8 ka0 = *(const bf16x8*)(kst + l16 * GG::kKStride + col);
-        const bf16x8 ka1 = *(const bf16x8*)(kst + (16 + l16) * GG::kKStride + col);
-#pragma unroll
-        for (int qg = 0; qg < NQ; ++qg) {
-          if (row0 + qg * 16 < Mb) {
-            const bf16x8 qb = *(const bf16x8*)(qst + (qg * 16 + l16) * GG::kKStride + col);
-            sacc[0][qg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka0, qb, sacc[0][qg], 0, 0, 0);
-            sacc[1][qg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka1, qb, sacc[1][qg], 0, 0, 0);
-          }
-        }
-      }
-      // ---- mask, online softmax, P in bf16
-      bf16x8 pb[NQ];
+    for (int ks = 0; ks < D / 32; ++ks) {
+      const int col = (ks * 32 + lg * 8) * 2;
+      const bf16x8 ka = *(const bf16x8*)(kst + l16 * GG::kKStride + col);
 #pragma unroll
       for (int qg = 0; qg < NQ; ++qg) {
         if (row0 + qg * 16 < Mb) {
-          const int r = row0 + qg * 16 + l16;
-          const int lim = r < Mb ? causal0 + r / G : -1;  // last key this query row sees
-          float s[8];
-          float mt = kNegInf;
-#pragma unroll
-          for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const int kl = kb * 16 + lg * 4 + e;
-              const bool vis = ((vbits >> kl) & 1u) && (kb0 + kl <= lim);
-              const float x = vis ? sacc[kb][qg][e] * scale_log2 : kNegInf;
-              s[kb * 4 + e] = x;
-              mt = fmaxf(mt, x);
-            }
-          }
-          mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
-          mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-          const float mn = fmaxf(m_run[qg], mt);
-          const bool none = (mn == kNegInf);
-          const float alpha = none ? 1.f : exp2f(m_run[qg] - mn);
-          float pk[8];
-          float ls = 0.f;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            pk[e] = none ? 0.f : exp2f(s[e] - mn);
-            ls += pk[e];
-          }
-          ls += __shfl_xor(ls, 16, 64);
-          ls += __shfl_xor(ls, 32, 64);
-          l_run[qg] = l_run[qg] * alpha + ls;
-          m_run[qg] = mn;
-#pragma unroll
-          for (int db = 0; db < DB; ++db) o[db][qg] *= alpha;
-          uint32_t pw[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) pw[e] = pack_bf16x2(pk[2 * e], pk[2 * e + 1]);
-          pb[qg] = __builtin_bit_cast(bf16x8, u32x4{pw[0], pw[1], pw[2], pw[3]});
-        }
-      }
-      // ---- O^T += V^T P^T
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        uint32_t vw[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          // elements 2e, 2e+1 of the operand = keys (kb, lg*4 + i) with kb*4+i = 2e, 2e+1
-          const int k0 = ((2 * e) >> 2) * 16 + lg * 4 + ((2 * e) & 3);
-          const int k1 = ((2 * e + 1) >> 2) * 16 + lg * 4 + ((2 * e + 1) & 3);
-          const uint32_t lo = *(const uint16_t*)(vst + k0 * GG::kVStride + (db * 16 + l16) * 2);
-          const uint32_t hi = *(const uint16_t*)(vst + k1 * GG::kVStride + (db * 16 + l16) * 2);
-          vw[e] = lo | (hi << 16);
-        }
-        const bf16x8 va = __builtin_bit_cast(bf16x8, u32x4{vw[0], vw[1], vw[2], vw[3]});
-#pragma unroll
-        for (int qg = 0; qg < NQ; ++qg) {
-          if (row0 + qg * 16 < Mb) o[db][qg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[qg], o[db][qg], 0, 0, 0);
+          const bf16x8 qb = *(const bf16x8*)(qst + (qg * 16 + l16) * GG::kKStride + col);
+          sacc[qg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb, sacc[qg], 0, 0, 0);
         }
       }
     }
-    __syncthreads();
+    // ---- mask, online softmax, P in bf16 (lane: keys lg*4 + e of query l16)
+    shortx4 pb[NQ];
+#pragma unroll
+    for (int qg = 0; qg < NQ; ++qg) {
+      if (row0 + qg * 16 < Mb) {
+        const int r = row0 + qg * 16 + l16;
+        const int lim = r < Mb ? causal0 + r / G : -1;  // last key this query row sees
+        float s[4];
+        float mt = kNegInf;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int kl = lg * 4 + e;
+          const bool vis = ((vbits >> kl) & 1u) && (kb0 + kl <= lim);
+          s[e] = vis ? sacc[qg][e] * scale_log2 : kNegInf;
+          mt = fmaxf(mt, s[e]);
+        }
+        mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+        mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+        const float mn = fmaxf(m_run[qg], mt);
+        const bool none = (mn == kNegInf);
+        const float alpha = none ? 1.f : exp2f(m_run[qg] - mn);
+        float pk[4];
+        float ls = 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          pk[e] = none ? 0.f : exp2f(s[e] - mn);
+          ls += pk[e];
+        }
+        ls += __shfl_xor(ls, 16, 64);
+        ls += __shfl_xor(ls, 32, 64);
+        l_run[qg] = l_run[qg] * alpha + ls;
+        m_run[qg] = mn;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) o[db][qg] *= alpha;
+        const uint32_t w0 = pack_bf16x2(pk[0], pk[1]);
+        const uint32_t w1 = pack_bf16x2(pk[2], pk[3]);
+        pb[qg] = __builtin_bit_cast(shortx4, make_uint2(w0, w1));
+      }
+    }
+    // ---- O^T += V^T P^T (K = 16 keys)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const unsigned char* vcol = vst + (lg * 4) * GG::kVStride + (db * 16 + l16) * 2;
+      const uint32_t v0 = *(const uint16_t*)(vcol);
+      const uint32_t v1 = *(const uint16_t*)(vcol + GG::kVStride);
+      const uint32_t v2 = *(const uint16_t*)(vcol + 2 * GG::kVStride);
+      const uint32_t v3 = *(const uint16_t*)(vcol + 3 * GG::kVStride);
+      const shortx4 va = __builtin_bit_cast(shortx4, make_uint2(v0 | (v1 << 16), v2 | (v3 << 16)));
+#pragma unroll
+      for (int qg = 0; qg < NQ; ++qg) {
+        if (row0 + qg * 16 < Mb) o[db][qg] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb[qg], o[db][qg], 0, 0, 0);
+      }
+    }
+    wave_lds_sync();  // this tile's LDS reads are issued before the slot is rewritten
+  };
+
+  Stage<D> sa, sb;
+  fetch(0, sa);
+  fetch(1, sb);
+  for (int t = 0; t < n_tiles; t += 2) {
+    consume(t, sa);
+    consume(t + 1, sb);
   }
+  __syncthreads();
 
   // ---- merge the four waves' states: (2,3) -> (0,1), then 1 -> 0
   float* cm = (float*)lds;  // 2 slots of [MQ] m, [MQ] l, [MQ][D] o
@@ -420,11 +435,11 @@ int attention_plan(int B, int gamma_max, int Hq, int Hkv, int D, int L_cap, Atte
   const long pairs = (long)B * Hkv * plan->q_chunks;
   const long target = (long)cus * per_cu;
   long splits = (target + pairs - 1) / pairs;
-  const long max_splits = (L_cap + kKeysPerWave - 1) / kKeysPerWave;
+  const long max_splits = (L_cap + kWaveKeys - 1) / kWaveKeys;
   if (splits < 1) splits = 1;
   if (splits > max_splits) splits = max_splits;
   int sk = (int)((L_cap + splits - 1) / splits);
-  sk = (sk + kKeysPerWave - 1) / kKeysPerWave * kKeysPerWave;
+  sk = (sk + kWaveKeys - 1) / kWaveKeys * kWaveKeys;
   plan->split_keys = sk;
   plan->n_splits = (L_cap + sk - 1) / sk;
   plan->workspace_bytes =
