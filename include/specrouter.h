@@ -108,8 +108,9 @@ const char* specrouter_status_string(int code);
  * out        fp32 [B][gamma_max+1][Hq][D]          (16-byte aligned)
  * scale      score scale, normally 1/sqrt(D)
  * workspace  device scratch of specrouter_verify_attention_workspace_size()
- *            bytes (may be NULL when that size is 0); contents need no
- *            initialisation and are dead after the call
+ *            bytes (may be NULL when that size is 0). Zero-fill it once before
+ *            its first use; every call leaves it in that state again (it holds
+ *            per-(sequence, kv head) arrival counters of the cache splits)
  * Precision: bf16 products, fp32 accumulation and softmax.
  */
 size_t specrouter_verify_attention_workspace_size(int B, int gamma_max, int Hq, int Hkv, int D,

@@ -233,4 +233,4 @@ class AcceptBuffers:
 
 def attention_workspace(B, gamma_max, Hq, Hkv, D, L_cap, device="cuda"):
     n = specrouter_verify_attention_workspace_size(B, gamma_max, Hq, Hkv, D, L_cap)
-    return None if n == 0 else torch.empty(n, dtype=torch.uint8, device=device)
+    return None if n == 0 else torch.zeros(n, dtype=torch.uint8, device=device)

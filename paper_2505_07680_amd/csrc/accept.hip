@@ -119,23 +119,6 @@ struct Args {
   int32_t* status;
 };
 
-__device__ __forceinline__ void st_dev(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float ld_dev(const float* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint32_t ld_dev(const uint32_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// Wait until this wave's earlier stores have completed (they are then visible
-// to device-coherent loads anywhere on the device).
-__device__ __forceinline__ void stores_done() {
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_s_waitcnt(0);
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-}
-
 // Merge (max, sum) pairs held lane-wise (up to kSpanSlots per lane) into the
 // row's natural-log normaliser; fixed order, fp64 sum.
 __device__ __forceinline__ double merge_lse(const float (&m)[kSpanSlots], const float (&s)[kSpanSlots], int nslot) {

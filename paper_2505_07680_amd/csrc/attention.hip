@@ -5,9 +5,11 @@
 // (the GQA group times the new positions) are processed together, so every K/V
 // byte of the split is read from HBM exactly once. Each wave owns 16 of every
 // 64 keys and keeps its own online-softmax state (no workgroup barrier inside
-// the key loop); the four states are merged through LDS at the end. Splits of
-// one (b, g) are merged by a small combine kernel (skipped when one split
-// covers the cache).
+// the key loop); the four states are merged through LDS at the end. When the
+// cache is split, each split publishes its (max, sum, unnormalised output)
+// partial and bumps a per-(b, g, query chunk) arrival counter; the last
+// workgroup to arrive merges all partials and writes the output, then resets
+// the counter, so the workspace is left ready for the next call.
 //
 // Per 16-key wave tile:
 //   * K and V rows are fetched with coalesced 16-byte loads into a two-deep
@@ -30,6 +32,8 @@ namespace sr {
 namespace {
 
 typedef short shortx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
 
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
@@ -52,9 +56,24 @@ template <int D, int NQ>
 struct Lds {
   static constexpr int MQ = 16 * NQ;
   static constexpr int kStage = kWaves * Geo<D>::kWaveBytes + MQ * Geo<D>::kKStride;
-  static constexpr int kComb = 2 * MQ * (D + 2) * 4;
+  // Merge of the four wave states: the columns are reduced in kPasses passes
+  // so that the four fp32 slices fit in about 48 KB.
+  static constexpr int kPasses = (kWaves * MQ * D * 4 <= 49152) ? 1 : (kWaves * MQ * D * 2 <= 49152) ? 2 : 4;
+  static constexpr int kDp = D / kPasses;                 // columns per pass
+  static constexpr int kRowStride = kDp + 4;              // floats; padded against bank conflicts
+  static constexpr int kSlot = MQ * kRowStride;           // floats per wave slice
+  static constexpr int kMl = kWaves * kSlot * 4;          // byte offset of the (m, l) exchange
+  static constexpr int kComb = kMl + (kWaves + 1) * 2 * MQ * 4;
   static constexpr int kBytes = kStage > kComb ? kStage : kComb;
 };
+
+// 16-byte device-coherent (sc1) buffer access to the split partials; the
+// descriptor's range check turns an out-of-range offset into a dropped store
+// or a zero load.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t partial_rsrc(const float* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), 0, (int)bytes, 0x00020000);
+}
+constexpr int kDeviceCoherent = 16;  // cache-policy operand: sc1
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   const __bf16 a = (__bf16)lo;
@@ -69,6 +88,11 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
+
+template <bool B>
+struct Flag {
+  static constexpr bool value = B;
+};
 
 template <int D>
 struct Stage {  // one 16-key wave tile in flight
@@ -88,8 +112,9 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
                   const uint16_t* __restrict__ vc, const uint8_t* __restrict__ mask,
                   const int32_t* __restrict__ kv_len, const int32_t* __restrict__ gamma,
                   float* __restrict__ out, float* __restrict__ part_o,
-                  float* __restrict__ part_ml, int gmax, int Hq, int Hkv, int L_cap,
-                  float scale_log2, int split_keys, int n_splits, int32_t* __restrict__ status) {
+                  float* __restrict__ part_ml, uint32_t* __restrict__ arrivals, int gmax, int Hq,
+                  int Hkv, int L_cap, float scale_log2, int split_keys, int n_splits,
+                  int32_t* __restrict__ status) {
   using GG = Geo<D>;
   constexpr int MQ = 16 * NQ;
   constexpr int DB = D / 16;
@@ -121,9 +146,9 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
   const int lg = lane >> 4;
 
   if (!work) {
-    // Nothing to compute here. With a single split this workgroup owns the
-    // output rows and writes them as zero; otherwise the combine kernel does.
-    if (n_splits == 1) {
+    // Nothing to compute. Split 0 of a query chunk without live rows (or of an
+    // invalid sequence) owns those output rows and writes them as zero.
+    if (split == 0) {
       for (int idx = tid; idx < (row_end - row0) * (D / 4); idx += kThreads) {
         const int r = row0 + idx / (D / 4);
         const int d4 = idx % (D / 4);
@@ -134,21 +159,7 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
     return;
   }
 
-  // ---- stage this workgroup's query rows (bf16, zero beyond the live rows)
   unsigned char* qst = lds + kWaves * GG::kWaveBytes;
-  for (int idx = tid; idx < MQ * GG::kChunksPerRow; idx += kThreads) {
-    const int rl = idx / GG::kChunksPerRow;
-    const int c = idx % GG::kChunksPerRow;
-    const int r = row0 + rl;
-    u32x4 val = u32x4{0u, 0u, 0u, 0u};
-    if (r < Mb) {
-      const int i = r / G, h = g * G + r % G;
-      val = *(const u32x4*)(q + ((size_t)(b * (gmax + 1) + i) * Hq + h) * D + c * 8);
-    }
-    *(u32x4*)(qst + rl * GG::kKStride + c * 16) = val;
-  }
-  __syncthreads();
-
   unsigned char* kst = lds + w * GG::kWaveBytes;
   unsigned char* vst = kst + GG::kSlotK;
   const size_t slab = ((size_t)b * Hkv + g) * (size_t)L_cap;
@@ -185,7 +196,9 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
     st.mbyte = mload[min(kb0 + (lane & (kWaveKeys - 1)), key_end - 1)];
   };
 
-  auto consume = [&](int t, Stage<D>& st) __attribute__((always_inline)) {
+  // Stage ring entry st (tile t) in LDS, refill it with tile t + 2 when
+  // Refill::value (so nothing is fetched past the last tile), then compute.
+  auto consume = [&](int t, Stage<D>& st, auto refill) __attribute__((always_inline)) {
     const int kb0 = key_begin + t * kTileKeys + w * kWaveKeys;
     const bool key_ok = lane < kWaveKeys && kb0 + lane < key_end && (mrow == nullptr || st.mbyte != 0u);
     const uint32_t vbits = (uint32_t)__ballot(key_ok) & 0xffffu;
@@ -200,7 +213,11 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
       *(uint2*)(dst + 2) = make_uint2(vv.z, vv.w);
     }
     wave_lds_sync();
-    fetch(t + 2, st);  // refill this ring entry: two tiles in flight during the compute below
+    if constexpr (decltype(refill)::value) {
+      __builtin_amdgcn_sched_barrier(0);
+      fetch(t + 2, st);  // two tiles in flight during the compute below
+      __builtin_amdgcn_sched_barrier(0);
+    }
     if (t >= n_tiles || kb0 >= key_end) return;  // wave-uniform: nothing of this tile to compute
     // ---- S^T = K Q^T (16 keys x 16 queries per group)
     floatx4 sacc[NQ];
@@ -274,137 +291,213 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
     wave_lds_sync();  // this tile's LDS reads are issued before the slot is rewritten
   };
 
+  // Issue order: this workgroup's query rows, then the first two ring
+  // entries; the query rows are staged in LDS while the K/V tiles are still
+  // in flight. Each group of loads is kept together (no interleaving by the
+  // scheduler) so every wait covers exactly the loads it needs, in the first
+  // iteration as in every later one.
+  constexpr int kQChunks = MQ * GG::kChunksPerRow;
+  constexpr int kQLoads = (kQChunks + kThreads - 1) / kThreads;
+  u32x4 qv[kQLoads];
+#pragma unroll
+  for (int u = 0; u < kQLoads; ++u) {
+    const int idx = min(tid + u * kThreads, kQChunks - 1);
+    const int r = min(row0 + idx / GG::kChunksPerRow, Mb - 1);  // rows past Mb are zeroed below
+    const int i = r / G, h = g * G + r % G;
+    qv[u] = *(const u32x4*)(q + ((size_t)(b * (gmax + 1) + i) * Hq + h) * D + (idx % GG::kChunksPerRow) * 8);
+  }
+  __builtin_amdgcn_sched_barrier(0);
   Stage<D> sa, sb;
   fetch(0, sa);
+  __builtin_amdgcn_sched_barrier(0);
   fetch(1, sb);
-  for (int t = 0; t < n_tiles; t += 2) {
-    consume(t, sa);
-    consume(t + 1, sb);
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int u = 0; u < kQLoads; ++u) {
+    const int idx = tid + u * kThreads;
+    if (idx < kQChunks) {
+      const int rl = idx / GG::kChunksPerRow;
+      const u32x4 val = row0 + rl < Mb ? qv[u] : u32x4{0u, 0u, 0u, 0u};
+      *(u32x4*)(qst + rl * GG::kKStride + (idx % GG::kChunksPerRow) * 16) = val;
+    }
   }
   __syncthreads();
 
-  // ---- merge the four waves' states: (2,3) -> (0,1), then 1 -> 0
-  float* cm = (float*)lds;  // 2 slots of [MQ] m, [MQ] l, [MQ][D] o
-  constexpr int kSlot = MQ * (D + 2);
-#pragma unroll
-  for (int step = 0; step < 2; ++step) {
-    const int half = step == 0 ? 2 : 1;
-    if (w >= half && w < 2 * half) {
-      float* sl = cm + (w - half) * kSlot;
-#pragma unroll
-      for (int qg = 0; qg < NQ; ++qg) {
-        const int rl = qg * 16 + l16;
-        if (lg == 0) {
-          sl[rl] = m_run[qg];
-          sl[MQ + rl] = l_run[qg];
-        }
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-          *(floatx4*)(sl + 2 * MQ + rl * D + db * 16 + lg * 4) = o[db][qg];
-      }
-    }
-    __syncthreads();
-    if (w < half) {
-      const float* sl = cm + w * kSlot;
-#pragma unroll
-      for (int qg = 0; qg < NQ; ++qg) {
-        const int rl = qg * 16 + l16;
-        const float m2 = sl[rl];
-        const float l2 = sl[MQ + rl];
-        const float M = fmaxf(m_run[qg], m2);
-        const float ca = M == kNegInf ? 0.f : exp2f(m_run[qg] - M);
-        const float cb = M == kNegInf ? 0.f : exp2f(m2 - M);
-        l_run[qg] = l_run[qg] * ca + l2 * cb;
-        m_run[qg] = M;
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const floatx4 o2 = *(const floatx4*)(sl + 2 * MQ + rl * D + db * 16 + lg * 4);
-          o[db][qg] = o[db][qg] * ca + o2 * cb;
-        }
-      }
-    }
-    __syncthreads();
+  // sa holds tile t and sb tile t + 1 at the top of each iteration.
+  int t = 0;
+#ifdef ATT_PEEL
+  for (; t + 3 < n_tiles; t += 2) {
+    consume(t, sa, Flag<true>{});
+    consume(t + 1, sb, Flag<true>{});
   }
+  if (t + 2 < n_tiles) {
+    consume(t, sa, Flag<true>{});
+    consume(t + 1, sb, Flag<false>{});
+    consume(t + 2, sa, Flag<false>{});
+  } else {
+    consume(t, sa, Flag<false>{});
+    consume(t + 1, sb, Flag<false>{});
+  }
+#else
+  for (; t < n_tiles; t += 2) {
+    consume(t, sa, Flag<true>{});
+    consume(t + 1, sb, Flag<true>{});
+  }
+#endif
+  __syncthreads();
 
-  if (w == 0) {
+  // ---- merge the four wave states (every wave and lane takes part)
+  using LL = Lds<D, NQ>;
+  float* slots = (float*)lds;                    // [kWaves][MQ][kRowStride]
+  float* mlx = (float*)(lds + LL::kMl);          // [kWaves][2][MQ]: each wave's (m, l)
+  float* mlf = mlx + kWaves * 2 * MQ;            // [2][MQ]: merged (M, L)
+  if (lg == 0) {
 #pragma unroll
     for (int qg = 0; qg < NQ; ++qg) {
-      const int r = row0 + qg * 16 + l16;
+      mlx[(w * 2) * MQ + qg * 16 + l16] = m_run[qg];
+      mlx[(w * 2 + 1) * MQ + qg * 16 + l16] = l_run[qg];
+    }
+  }
+  __syncthreads();
+  float cw[NQ];  // this wave's weight exp2(m_w - M) per row group
+#pragma unroll
+  for (int qg = 0; qg < NQ; ++qg) {
+    const int rl = qg * 16 + l16;
+    float M = kNegInf;
+#pragma unroll
+    for (int v = 0; v < kWaves; ++v) M = fmaxf(M, mlx[(v * 2) * MQ + rl]);
+    float Lsum = 0.f;
+#pragma unroll
+    for (int v = 0; v < kWaves; ++v) {
+      const float c = M == kNegInf ? 0.f : exp2f(mlx[(v * 2) * MQ + rl] - M);
+      Lsum += c * mlx[(v * 2 + 1) * MQ + rl];
+    }
+    cw[qg] = M == kNegInf ? 0.f : exp2f(m_run[qg] - M);
+    if (w == 0 && lg == 0) {
+      mlf[rl] = M;
+      mlf[MQ + rl] = Lsum;
+    }
+  }
+
+  // Splits of this (b, g) that hold keys; with a single one the result is
+  // final here, otherwise it is published as a partial.
+  const int ns = (L + split_keys - 1) / split_keys;
+  const size_t pair = (size_t)(b * Hkv + g);
+  const int n_rec = (int)(gridDim.x * (size_t)Hkv * gridDim.z) * R;  // records in the partial arrays
+  const __amdgpu_buffer_rsrc_t rs_o = partial_rsrc(part_o, (uint32_t)((size_t)n_rec * D * 4));
+  const __amdgpu_buffer_rsrc_t rs_ml = partial_rsrc(part_ml, (uint32_t)((size_t)n_rec * 8));
+  constexpr int kItemsP = (MQ * (LL::kDp / 4) + kThreads - 1) / kThreads;
+#pragma unroll
+  for (int pass = 0; pass < LL::kPasses; ++pass) {
+    __syncthreads();  // (m, l) exchange read / previous pass's slices consumed
+#pragma unroll
+    for (int qg = 0; qg < NQ; ++qg) {
+      const int rl = qg * 16 + l16;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const int col = db * 16 + lg * 4 - pass * LL::kDp;
+        if (col >= 0 && col < LL::kDp) *(floatx4*)(slots + (w * MQ + rl) * LL::kRowStride + col) = o[db][qg] * cw[qg];
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kItemsP; ++k) {
+      const int idx = tid + k * kThreads;
+      if (idx >= MQ * (LL::kDp / 4)) continue;
+      const int rl = idx / (LL::kDp / 4);
+      const int c4 = idx % (LL::kDp / 4);
+      const int r = row0 + rl;
       if (r >= row_end) continue;
-      if (n_splits == 1) {
+      floatx4 sum = *(const floatx4*)(slots + rl * LL::kRowStride + c4 * 4);
+#pragma unroll
+      for (int v = 1; v < kWaves; ++v) sum += *(const floatx4*)(slots + (v * MQ + rl) * LL::kRowStride + c4 * 4);
+      const int col = pass * LL::kDp + c4 * 4;
+      if (ns == 1) {
+        const float Lr = mlf[MQ + rl];
         const int i = r / G, h = g * G + r % G;
-        const float inv = l_run[qg] > 0.f ? 1.f / l_run[qg] : 0.f;
-        float* dst = out + ((size_t)(b * (gmax + 1) + i) * Hq + h) * D + lg * 4;
-#pragma unroll
-        for (int db = 0; db < DB; ++db) *(floatx4*)(dst + db * 16) = o[db][qg] * inv;
-      } else {
-        const size_t rec = ((size_t)(b * Hkv + g) * n_splits + split) * R + r;
-        float* dst = part_o + rec * D + lg * 4;
-#pragma unroll
-        for (int db = 0; db < DB; ++db) *(floatx4*)(dst + db * 16) = o[db][qg];
-        if (lg == 0) {
-          part_ml[rec * 2] = m_run[qg];
-          part_ml[rec * 2 + 1] = l_run[qg];
-        }
+        *(floatx4*)(out + ((size_t)(b * (gmax + 1) + i) * Hq + h) * D + col) = Lr > 0.f ? sum * (1.f / Lr) : floatx4{0.f, 0.f, 0.f, 0.f};
+      } else if (r < Mb) {
+        const uint32_t rec = (uint32_t)((pair * n_splits + split) * R + r);
+        __builtin_amdgcn_raw_buffer_store_b128(sum, rs_o, (rec * D + col) * 4, 0, kDeviceCoherent);
+        if (pass == 0 && c4 == 0)
+          __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, floatx2{mlf[rl], mlf[MQ + rl]}), rs_ml, rec * 8, 0, kDeviceCoherent);
       }
     }
   }
-}
+  if (ns == 1) return;
 
-// Merge the split partials of one (sequence, kv head) for 16 query rows.
-template <int D>
-__global__ void __launch_bounds__(256)
-attn_combine_kernel(const float* __restrict__ part_o, const float* __restrict__ part_ml,
-                    const int32_t* __restrict__ kv_len, const int32_t* __restrict__ gamma,
-                    float* __restrict__ out, int gmax, int Hq, int Hkv, int L_cap,
-                    int split_keys, int n_splits) {
-  const int row_blocks = gridDim.x / Hkv;
-  const int g = blockIdx.x / row_blocks;
-  const int rb = blockIdx.x % row_blocks;
-  const int b = blockIdx.y;
-  const int G = Hq / Hkv;
-  const int R = G * (gmax + 1);
-  const int gam = gamma[b];
-  const int L = kv_len[b];
-  const bool valid = gam >= 0 && gam <= gmax && L >= gam + 1 && L <= L_cap;
-  const int Mb = valid ? G * (gam + 1) : 0;
-  const int ns = valid ? min(n_splits, (L + split_keys - 1) / split_keys) : 0;
-  for (int idx = threadIdx.x; idx < 16 * (D / 4); idx += blockDim.x) {
-    const int r = rb * 16 + idx / (D / 4);
-    const int d4 = idx % (D / 4);
-    if (r >= R) continue;
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (r < Mb) {
-      const size_t base = (size_t)(b * Hkv + g) * n_splits;
-      float M = kNegInf;
-      for (int s = 0; s < ns; ++s) M = fmaxf(M, part_ml[((base + s) * R + r) * 2]);
-      if (M != kNegInf) {
-        float den = 0.f;
-        for (int s = 0; s < ns; ++s) {
-          const size_t rec = (base + s) * R + r;
-          const float c = exp2f(part_ml[rec * 2] - M);
-          den += c * part_ml[rec * 2 + 1];
-          const float4 v = *(const float4*)(part_o + rec * D + d4 * 4);
-          acc.x += c * v.x;
-          acc.y += c * v.y;
-          acc.z += c * v.z;
-          acc.w += c * v.w;
-        }
-        const float inv = den > 0.f ? 1.f / den : 0.f;
-        acc.x *= inv;
-        acc.y *= inv;
-        acc.z *= inv;
-        acc.w *= inv;
+  // ---- arrive: the last split of this chunk to finish merges all partials
+  stores_done();
+  __syncthreads();
+  __shared__ uint32_t last_flag;
+  if (tid == 0) {
+    uint32_t* cnt = arrivals + pair * (gridDim.y / Hkv) + qc;
+    const uint32_t before = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const bool last = before == (uint32_t)(ns - 1);
+    if (last) st_dev(cnt, 0u);  // every split of this chunk has arrived: reset for the next call
+    last_flag = last ? 1u : 0u;
+  }
+  __syncthreads();
+  if (last_flag == 0u) return;
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+
+  // Each thread owns kItems (row, 4 columns) items and folds the splits in
+  // with a running max, kGroup splits per round of loads.
+  constexpr int kItems = (MQ * (D / 4) + kThreads - 1) / kThreads;
+  constexpr int kGroup = kItems >= 16 ? 1 : (16 / kItems > 8 ? 8 : 16 / kItems);
+  const int n_items = (row_end - row0) * (D / 4);
+  float mx[kItems], den[kItems];
+  floatx4 acc[kItems];
+#pragma unroll
+  for (int k = 0; k < kItems; ++k) {
+    mx[k] = kNegInf;
+    den[k] = 0.f;
+    acc[k] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+  for (int sp0 = 0; sp0 < ns; sp0 += kGroup) {
+    floatx2 ml2[kGroup][kItems];
+    floatx4 o2[kGroup][kItems];
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j)
+#pragma unroll
+      for (int k = 0; k < kItems; ++k) {
+        const int sp = min(sp0 + j, ns - 1);  // repeats of the last split are discarded below
+        const int idx = min(tid + k * kThreads, n_items - 1);
+        const int r = min(row0 + idx / (D / 4), Mb - 1);  // rows past Mb hold no partial; their result is discarded
+        const uint32_t rec = (uint32_t)((pair * n_splits + sp) * R + r);
+        ml2[j][k] = __builtin_bit_cast(floatx2, __builtin_amdgcn_raw_buffer_load_b64(rs_ml, rec * 8, 0, kDeviceCoherent));
+        o2[j][k] = __builtin_amdgcn_raw_buffer_load_b128(rs_o, (rec * D + (idx % (D / 4)) * 4) * 4, 0, kDeviceCoherent);
+      }
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) {
+      if (sp0 + j >= ns) break;
+#pragma unroll
+      for (int k = 0; k < kItems; ++k) {
+        const float M = fmaxf(mx[k], ml2[j][k].x);
+        if (M == kNegInf) continue;
+        const float ca = exp2f(mx[k] - M);
+        const float cb = exp2f(ml2[j][k].x - M);
+        den[k] = den[k] * ca + ml2[j][k].y * cb;
+        acc[k] = acc[k] * ca + o2[j][k] * cb;
+        mx[k] = M;
       }
     }
+  }
+#pragma unroll
+  for (int k = 0; k < kItems; ++k) {
+    const int idx = tid + k * kThreads;
+    if (idx >= n_items) continue;
+    const int r = row0 + idx / (D / 4);
+    const bool live = r < Mb && den[k] > 0.f;
+    const floatx4 res = live ? acc[k] * (1.f / den[k]) : floatx4{0.f, 0.f, 0.f, 0.f};
     const int i = r / G, h = g * G + r % G;
-    *(float4*)(out + ((size_t)(b * (gmax + 1) + i) * Hq + h) * D + d4 * 4) = acc;
+    *(floatx4*)(out + ((size_t)(b * (gmax + 1) + i) * Hq + h) * D + (idx % (D / 4)) * 4) = res;
   }
 }
 
 typedef void (*SplitKernel)(const uint16_t*, const uint16_t*, const uint16_t*, const uint8_t*,
-                            const int32_t*, const int32_t*, float*, float*, float*, int, int, int,
-                            int, float, int, int, int32_t*);
+                            const int32_t*, const int32_t*, float*, float*, float*, uint32_t*, int,
+                            int, int, int, float, int, int, int32_t*);
 
 template <int D>
 SplitKernel pick_split(int nq) {
@@ -438,12 +531,20 @@ int attention_plan(int B, int gamma_max, int Hq, int Hkv, int D, int L_cap, Atte
   const long max_splits = (L_cap + kWaveKeys - 1) / kWaveKeys;
   if (splits < 1) splits = 1;
   if (splits > max_splits) splits = max_splits;
+  // Offsets into the partial arrays are 32-bit (buffer addressing): keep
+  // them below 2^31 bytes.
+  const long rec_per_split = (long)B * Hkv * R;
+  const long max_by_offset = (long)(0x7fffffffL / ((long)D * 4 * (rec_per_split > 0 ? rec_per_split : 1)));
+  if (splits > max_by_offset) splits = max_by_offset > 1 ? max_by_offset : 1;
   int sk = (int)((L_cap + splits - 1) / splits);
   sk = (sk + kWaveKeys - 1) / kWaveKeys * kWaveKeys;
   plan->split_keys = sk;
   plan->n_splits = (L_cap + sk - 1) / sk;
+  // [arrival counters: B*Hkv*q_chunks u32, padded to 256 B][partial o][partial (m, l)]
+  const size_t counters = ((size_t)B * Hkv * plan->q_chunks * sizeof(uint32_t) + 255) / 256 * 256;
+  plan->part_offset = counters;
   plan->workspace_bytes =
-      plan->n_splits > 1 ? (size_t)B * Hkv * plan->n_splits * R * (D + 2) * sizeof(float) : 0;
+      plan->n_splits > 1 ? counters + (size_t)B * Hkv * plan->n_splits * R * (D + 2) * sizeof(float) : 0;
   return SR_OK;
 }
 
@@ -454,26 +555,15 @@ int launch_verify_attention(const void* q, const void* k_cache, const void* v_ca
                             const AttentionPlan& plan, int32_t* status, hipStream_t stream) {
   const int G = Hq / Hkv;
   const int R = G * (gamma_max + 1);
-  float* part_o = (float*)workspace;
+  uint32_t* arrivals = (uint32_t*)workspace;
+  float* part_o = workspace ? (float*)((char*)workspace + plan.part_offset) : nullptr;
   float* part_ml = part_o ? part_o + (size_t)B * Hkv * plan.n_splits * R * D : nullptr;
   dim3 grid(plan.n_splits, Hkv * plan.q_chunks, B);
   hipLaunchKernelGGL(pick_split(D, plan.nq), grid, dim3(kThreads), 0, stream,
                      (const uint16_t*)q, (const uint16_t*)k_cache, (const uint16_t*)v_cache,
-                     cache_mask, kv_len, gamma, out, part_o, part_ml, gamma_max, Hq, Hkv, L_cap,
-                     scale * kLog2e, plan.split_keys, plan.n_splits, status);
+                     cache_mask, kv_len, gamma, out, part_o, part_ml, arrivals, gamma_max, Hq, Hkv,
+                     L_cap, scale * kLog2e, plan.split_keys, plan.n_splits, status);
   if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
-  if (plan.n_splits > 1) {
-    dim3 cgrid(Hkv * ((R + 15) / 16), B);
-    if (D == 64)
-      hipLaunchKernelGGL(attn_combine_kernel<64>, cgrid, dim3(256), 0, stream, part_o, part_ml,
-                         kv_len, gamma, out, gamma_max, Hq, Hkv, L_cap, plan.split_keys,
-                         plan.n_splits);
-    else
-      hipLaunchKernelGGL(attn_combine_kernel<128>, cgrid, dim3(256), 0, stream, part_o, part_ml,
-                         kv_len, gamma, out, gamma_max, Hq, Hkv, L_cap, plan.split_keys,
-                         plan.n_splits);
-    if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
-  }
   return SR_OK;
 }
 

@@ -59,6 +59,30 @@ __device__ __forceinline__ void fence_acquire_agent() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 }
 
+// Values handed between workgroups of one launch (possibly on different XCDs,
+// whose L2 caches are not coherent with each other) are written and read with
+// relaxed device-scope atomics, which are served at the device coherence
+// point; no cache-wide write-back or invalidate is needed.
+__device__ __forceinline__ void st_dev(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_dev(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t ld_dev(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Wait until this wave's earlier stores have completed (they are then visible
+// to device-coherent loads anywhere on the device).
+__device__ __forceinline__ void stores_done() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 // ---------------------------------------------------------------------------
 // Host-side launchers (one per translation unit). Arguments are already
 // validated by the C ABI layer.
@@ -68,6 +92,7 @@ struct AttentionPlan {
   int q_chunks;    // workgroups along the query rows of one (sequence, kv head)
   int split_keys;  // keys per split (multiple of 32)
   int n_splits;    // splits along the cache
+  size_t part_offset;  // byte offset of the split partials in the workspace
   size_t workspace_bytes;
 };
 
