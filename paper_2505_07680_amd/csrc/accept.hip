@@ -1,43 +1,48 @@
 // Accept-and-diverge for gfx950: speculative accept/reject with residual
 // resampling and the bonus token (Section 2.2 steps 3-4, probabilistic
-// acceptance), plus per-position total variation distance (Eq. 5) and KL
-// divergence, with one sweep over the verifier and draft logits.
+// acceptance; Eq. 2), plus per-position total variation distance (Eq. 5) and
+// KL divergence, in one pass over the verifier and draft logits.
 //
-// Decomposition. A "row" is one (sequence b, position j) pair: for j < gamma_b
-// the verifier row p_j together with the draft row q_j, for j = gamma_b the
-// verifier row alone (it feeds the bonus token). Each row is cut into chunks
-// of 256*E vocabulary entries, one chunk per workgroup task, and each of the
-// workgroup's four waves owns 64*E contiguous entries (E per lane, loaded with
-// coalesced 16-byte loads and kept in registers): a "span".
+// Rows and chunks. A live row is one (sequence b, position j <= gamma_b): for
+// j < gamma_b the verifier row p_j together with the draft row q_j (a "pair
+// row"), for j = gamma_b the verifier row alone (it feeds the bonus token).
+// Each row is cut into chunks of 256*E vocabulary entries; a workgroup task is
+// one (row, chunk), each lane holding E entries of p and q in registers.
 //
-// Sweep kernel (the single pass over HBM). TV and the residual max(0, p - q)
-// need both rows' log-normalisers, which depend on the whole row, so every
-// wave
-//   1. computes its span's (max, sum of exp) for p and q and its share of
-//      sum p (z_p - z_q) (the KL numerator) and publishes them;
-//   2. once every span of the row has published, merges the partials (fixed
-//      order, fp64 sums, so every wave gets bit-identical log-normalisers)
-//      and finishes TV and the residual mass of its span from the values still
-//      in registers.
-// Partials are written with device-coherent stores; once a workgroup's
-// stores have completed it bumps the row's counter (one atomic per
-// workgroup), and a single lane polls that counter, so waiting costs no
-// memory traffic beyond one word and no cache maintenance is needed. The
-// sweep launches one workgroup per (row, chunk) task, in row-major order.
+// Sweep kernel (persistent; the single pass over HBM). The grid is sized to be
+// resident at once. Workgroup w takes tasks w, w + G, w + 2G, ... over the live
+// rows only (a row table built from gamma in LDS), with G a multiple of the
+// chunks per row, so the chunks of one row are processed at the same time by
+// neighbouring workgroups. Per task:
+//   1. chunk maxima of p and q, then the sums of exp(z - max) and the KL
+//      numerator sum exp(p - max_p) (p - q), merged over the four waves in a
+//      fixed order and published as one record with device-coherent stores;
+//   2. pair rows only: one wave re-loads the row's records until all of them
+//      are present, merges them into the two log-normalisers (fp64, fixed
+//      order; the finish kernel merges identically, so both get bit-identical
+//      values), and every lane finishes sum |P - Q| over the entries still in
+//      its registers. The chunk's sum is stored for the finish kernel.
+// A record is four 8-byte words stored bit-inverted: a word that reads as all
+// zeros has not been written yet (the inverted pattern would be a NaN, which
+// no record holds), and naturally aligned 8-byte accesses are single-copy
+// atomic, so a waiting wave needs no counter, no atomics and no wait for its
+// own stores to complete. The finish kernel zeroes the records after use.
+// Only sum |P - Q| is needed: with d = P - Q, a chunk's residual mass
+// sum max(0, d) is (sum |d| + sum d) / 2 and sum d is the difference of the
+// chunk's P and Q masses, which the records already hold.
 //
-// Finish kernel (one workgroup per sequence, one wave per row). With every
-// partial in memory it computes each row's TV, KL, p(x), q(x) and acceptance
-// probability, runs the accept chain, and draws one token by CDF inversion:
-// the wave holding the sampling row finds the span that contains the target
-// from its per-span residual (or p) masses with a prefix scan, re-reads only
-// that span and scans it in fp64 in ascending vocabulary order. It also
-// resets the sweep's row counters for the next call.
+// Finish kernel (one workgroup per sequence, one wave per row): merges the
+// records into TV, KL, p(x), q(x) and a_j, runs the accept chain, and draws the
+// token: a prefix scan over the stopping row's chunk masses finds the chunk
+// that holds u*W, and that chunk alone is re-read and scanned in ascending
+// vocabulary order with its element weights computed exactly as in the sweep.
+// It also zeroes the sequence's records for the next call.
 //
-// A workgroup waits only for the other workgroups of its own row, which have
-// neighbouring indices: workgroups are dispatched in index order, so the
-// earlier rows never wait on later ones and the rows complete in order as
-// slots free up (a row needs only its own chunks resident at once). Waits are
-// still bounded (SR_ST_TIMEOUT) so the kernel always drains.
+// Precision: exponentials in fp32 (relative error ~1e-7; weights below 2^-126
+// of their chunk's largest flush to zero), every sum in fp64
+// beyond a lane's own entries; TV and KL carry ~1e-7 relative error, and a
+// draw can differ from exact arithmetic only when u*W lies within ~1e-7 W of
+// a CDF breakpoint.
 
 #include <math.h>
 
@@ -48,49 +53,72 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
-constexpr int kMaxSpans = 256;  // spans per row handled by the wave-parallel merges
+constexpr int kSlots = 2;                // chunk records per lane in the row merges
+constexpr int kMaxChunks = 64 * kSlots;  // chunks per row
 constexpr int kMaxRows = SPECROUTER_MAX_GAMMA + 1;
-constexpr int kSpanSlots = kMaxSpans / 64;
+constexpr int kMaxSeqs = 4096;           // sequences per sweep launch (row table in LDS)
 constexpr uint32_t kSpinLimit = 1u << 22;
+constexpr int kDeviceCoherent = 16;      // buffer cache-policy operand: sc1
 
-// Per-span partial record.
-struct SpanRec {
-  float mp, sp, mq, sq, kl, tv, res, pad;
+// Per-(row, chunk) record of the first pass, as values.
+struct StatRec {
+  float mp, mq;  // chunk maxima of the p and q logits (-inf: none)
+  double sp;     // sum exp(p - mp)
+  double sq;     // sum exp(q - mq)
+  double kl;     // sum exp(p - mp) (p - q)
 };
+// In memory: four 8-byte words {mp | mq << 32, sp, sq, kl}, each inverted.
+constexpr int kRecBytes = 32;
 
-struct RowLogits {  // p and q logits of the row's draft token
-  float zp, zq;
-};
-
-typedef float floatx8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ void pack_rec(const StatRec& r, u32x4& w0, u32x4& w1) {
+  const uint64_t a = ~((uint64_t)__float_as_uint(r.mp) | ((uint64_t)__float_as_uint(r.mq) << 32));
+  const uint64_t b = ~__builtin_bit_cast(uint64_t, r.sp);
+  const uint64_t c = ~__builtin_bit_cast(uint64_t, r.sq);
+  const uint64_t d = ~__builtin_bit_cast(uint64_t, r.kl);
+  w0 = u32x4{(uint32_t)a, (uint32_t)(a >> 32), (uint32_t)b, (uint32_t)(b >> 32)};
+  w1 = u32x4{(uint32_t)c, (uint32_t)(c >> 32), (uint32_t)d, (uint32_t)(d >> 32)};
+}
+// True when all four words have been written.
+__device__ __forceinline__ bool rec_present(const u32x4& w0, const u32x4& w1) {
+  return (w0[0] | w0[1]) != 0u && (w0[2] | w0[3]) != 0u && (w1[0] | w1[1]) != 0u && (w1[2] | w1[3]) != 0u;
+}
+__device__ __forceinline__ StatRec unpack_rec(const u32x4& w0, const u32x4& w1) {
+  StatRec r;
+  r.mp = __uint_as_float(~w0[0]);
+  r.mq = __uint_as_float(~w0[1]);
+  r.sp = __builtin_bit_cast(double, ~((uint64_t)w0[2] | ((uint64_t)w0[3] << 32)));
+  r.sq = __builtin_bit_cast(double, ~((uint64_t)w1[0] | ((uint64_t)w1[1] << 32)));
+  r.kl = __builtin_bit_cast(double, ~((uint64_t)w1[2] | ((uint64_t)w1[3] << 32)));
+  return r;
+}
 
 template <bool BF16>
 struct Elt;
 
 template <>
 struct Elt<false> {
-  static constexpr int VEC = 4;
-  typedef floatx4 Vec;
-  __device__ static Vec load(const void* row, int idx) { return *(const floatx4*)((const float*)row + idx); }
-  __device__ static float one(const void* row, int idx) { return ((const float*)row)[idx]; }
+  static constexpr int VEC = 4;  // entries per 16-byte load
+  __device__ static void load(const void* row, int x, float* out) {
+    const floatx4 v = *(const floatx4*)((const float*)row + x);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) out[i] = v[i];
+  }
+  __device__ static float one(const void* row, int x) { return ((const float*)row)[x]; }
 };
 
 template <>
 struct Elt<true> {
   static constexpr int VEC = 8;
-  typedef floatx8 Vec;
-  __device__ static Vec load(const void* row, int idx) {
-    const u32x4 u = *(const u32x4*)((const uint16_t*)row + idx);
-    Vec o;
+  __device__ static void load(const void* row, int x, float* out) {
+    const u32x4 u = *(const u32x4*)((const uint16_t*)row + x);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      o[2 * i] = bf16_lo(u[i]);
-      o[2 * i + 1] = bf16_hi(u[i]);
+      out[2 * i] = bf16_lo(u[i]);
+      out[2 * i + 1] = bf16_hi(u[i]);
     }
-    return o;
   }
-  __device__ static float one(const void* row, int idx) {
-    return __uint_as_float((uint32_t)((const uint16_t*)row)[idx] << 16);
+  __device__ static float one(const void* row, int x) {
+    return __uint_as_float((uint32_t)((const uint16_t*)row)[x] << 16);
   }
 };
 
@@ -112,203 +140,283 @@ struct Args {
   float* q_tok;
   float* kl;
   float* tv;
-  int B, gmax, V, n_chunks, chunk, span;
-  SpanRec* recs;      // [rows][spans]
-  RowLogits* rowx;    // [rows]
-  uint32_t* cnt;      // [rows] workgroups whose pass-1 partials are complete
+  int B, gmax, V, nc;
+  u32x4* stats;     // [B][gmax+1][nc] records, two 16-byte halves each
+  double* tvabs;    // [B][gmax+1][nc] sum |P - Q| per chunk (pair rows)
   int32_t* status;
 };
 
-// Merge (max, sum) pairs held lane-wise (up to kSpanSlots per lane) into the
-// row's natural-log normaliser; fixed order, fp64 sum.
-__device__ __forceinline__ double merge_lse(const float (&m)[kSpanSlots], const float (&s)[kSpanSlots], int nslot) {
+// Hardware 2^x (one instruction; results below 2^-126 flush to zero, i.e.
+// weights under 2^-126 of their chunk's largest are dropped). The sweep and
+// the finish kernel both use it, so a draw sees the same weights the chunk
+// sums were built from.
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Pairwise sum of a lane's entries (a fixed tree, log2(N) roundings deep).
+template <int N>
+__device__ __forceinline__ float tree_sum(float (&v)[N]) {
+#pragma unroll
+  for (int s = N / 2; s > 0; s /= 2)
+#pragma unroll
+    for (int i = 0; i < s; ++i) v[i] += v[i + s];
+  return v[0];
+}
+
+// Log-normaliser of a row from its chunk records held lane-wise (chunk
+// lane*nslot + i in slot i): max, then an fp64 sum in a fixed order. Both
+// kernels call this with the same layout and get bit-identical results.
+__device__ __forceinline__ double merge_lse(const float (&m)[kSlots], const double (&s)[kSlots]) {
   float ml = kNegInf;
 #pragma unroll
-  for (int i = 0; i < kSpanSlots; ++i)
-    if (i < nslot) ml = fmaxf(ml, m[i]);
+  for (int i = 0; i < kSlots; ++i) ml = fmaxf(ml, m[i]);
   const float M = wave_max(ml);
+  if (M == kNegInf) return -INFINITY;
   double acc = 0.0;
 #pragma unroll
-  for (int i = 0; i < kSpanSlots; ++i)
-    if (i < nslot && m[i] != kNegInf) acc += (double)s[i] * exp((double)m[i] - (double)M);
+  for (int i = 0; i < kSlots; ++i)
+    if (m[i] != kNegInf) acc += s[i] * exp((double)m[i] - (double)M);
   return (double)M + log(wave_sum_d(acc));
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, size_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
+}
+
+// Inclusive prefix over sequences of their live-row counts (gamma_b + 1, or 0
+// for an invalid gamma), in LDS. Each thread scans a contiguous segment.
+__device__ void build_row_table(const int32_t* gamma, int gmax, int B, int* rows) {
+  __shared__ int part[kThreads];
+  const int tid = threadIdx.x;
+  const int per = (B + kThreads - 1) / kThreads;
+  const int b0 = min(tid * per, B), b1 = min(b0 + per, B);
+  int run = 0;
+  for (int b = b0; b < b1; ++b) {
+    const int g = gamma[b];
+    run += (g >= 0 && g <= gmax) ? g + 1 : 0;
+    rows[b] = run;
+  }
+  part[tid] = run;
+  __syncthreads();
+  if (tid == 0) {
+    int acc = 0;
+    for (int i = 0; i < kThreads; ++i) {
+      const int v = part[i];
+      part[i] = acc;
+      acc += v;
+    }
+  }
+  __syncthreads();
+  const int off = part[tid];
+  for (int b = b0; b < b1; ++b) rows[b] += off;
+  __syncthreads();
 }
 
 // ============================================================================
 // Sweep kernel
 
-struct Task {
-  int row, span, base, j;
-  bool exists, live, pair;
-  const void* prow;
-  const void* qrow;
-};
-
-template <bool BF16>
-__device__ __forceinline__ Task make_task(const Args& A, long task, long total, int w) {
-  Task t;
-  t.exists = task < total;
-  t.live = false;
-  t.pair = false;
-  if (!t.exists) return t;
-  const int G1 = A.gmax + 1;
-  t.row = (int)(task / A.n_chunks);
-  const int c = (int)(task % A.n_chunks);
-  const int b = t.row / G1;
-  t.j = t.row % G1;
-  const int gam = A.gamma[b];
-  t.live = gam >= 0 && gam <= A.gmax && t.j <= gam;
-  t.pair = t.live && t.j < gam;
-  t.span = c * kWaves + w;
-  t.base = c * A.chunk + w * A.span;
-  const size_t esz = BF16 ? 2 : 4;
-  t.prow = (const char*)A.p + ((size_t)b * A.p_stride + (size_t)t.j * A.V) * esz;
-  t.qrow = (const char*)A.q + ((size_t)b * A.q_stride + (size_t)t.j * A.V) * esz;
-  return t;
-}
-
-template <bool BF16, int E>
-__device__ __forceinline__ void load_span(const Args& A, const Task& t, float (&zp)[E], float (&zq)[E]) {
-  typedef Elt<BF16> L;
-  constexpr int VEC = L::VEC;
-  const int lane = threadIdx.x & 63;
-  if (!t.live) return;
-#pragma unroll
-  for (int v = 0; v < E / VEC; ++v) {
-    const int x = t.base + (v * 64 + lane) * VEC;
-    const bool in = x < A.V;
-    typename L::Vec pv, qv;
-    pv = kNegInf;
-    qv = kNegInf;
-    if (in) pv = L::load(t.prow, x);
-    if (in && t.pair) qv = L::load(t.qrow, x);
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) {
-      zp[v * VEC + e] = pv[e];
-      zq[v * VEC + e] = qv[e];
-    }
-  }
-}
-
-// Pass 1: span maxima, exponentials (in place), sums and KL numerator; publish.
-template <bool BF16, int E>
-__device__ __forceinline__ void pass1(const Args& A, const Task& t, float (&zp)[E], float (&zq)[E], float& mp,
-                                      float& mq) {
-  const int lane = threadIdx.x & 63;
-  if (!t.live) return;
-  mp = kNegInf;
-  mq = kNegInf;
-#pragma unroll
-  for (int e = 0; e < E; ++e) {
-    mp = fmaxf(mp, zp[e]);
-    mq = fmaxf(mq, zq[e]);
-  }
-  mp = wave_max(mp);
-  if (t.pair) mq = wave_max(mq);
-  const float rp = mp == kNegInf ? 0.f : mp * kLog2e;
-  const float rq = mq == kNegInf ? 0.f : mq * kLog2e;
-  float sp = 0.f, sq = 0.f, klp = 0.f;
-#pragma unroll
-  for (int e = 0; e < E; ++e) {
-    const float ep = exp2f(fmaf(zp[e], kLog2e, -rp));
-    sp += ep;
-    if (t.pair) {
-      const float eq = exp2f(fmaf(zq[e], kLog2e, -rq));
-      sq += eq;
-      klp += ep > 0.f ? ep * (zp[e] - zq[e]) : 0.f;
-      zq[e] = eq;
-    }
-    zp[e] = ep;
-  }
-  sp = wave_sum(sp);
-  if (t.pair) {
-    sq = wave_sum(sq);
-    klp = wave_sum(klp);
-  }
-  SpanRec* rec = A.recs + (size_t)t.row * A.n_chunks * kWaves + t.span;
-  if (lane < 5) {
-    const float val = lane == 0 ? mp : lane == 1 ? sp : lane == 2 ? mq : lane == 3 ? sq : klp;
-    st_dev(&rec->mp + lane, val);
-  }
-  if (t.pair && t.span == 0 && lane == 0) {
-    // the draft token's logits, for the acceptance probability
-    const int b = t.row / (A.gmax + 1);
-    const int x = A.drafts[(size_t)b * A.gmax + t.j];
-    if (x >= 0 && x < A.V) A.rowx[t.row] = RowLogits{Elt<BF16>::one(t.prow, x), Elt<BF16>::one(t.qrow, x)};
-  }
-}
-
-// Pass 2 (pair rows, after the row's counter is complete): merge, TV and
-// residual mass of this span.
-template <int E>
-__device__ __forceinline__ void pass2(const Args& A, const Task& t, const float (&zp)[E], const float (&zq)[E],
-                                      float mp, float mq) {
-  const int lane = threadIdx.x & 63;
-  const int n_spans = A.n_chunks * kWaves;
-  const int nslot = (n_spans + 63) / 64;
-  const SpanRec* rr = A.recs + (size_t)t.row * n_spans;
-  float m1[kSpanSlots], s1[kSpanSlots], m2[kSpanSlots], s2[kSpanSlots];
-#pragma unroll
-  for (int i = 0; i < kSpanSlots; ++i) {
-    const int s = lane * nslot + i;  // lane-major blocks: same merge order as the finish kernel
-    const bool in = i < nslot && s < n_spans;
-    m1[i] = in ? ld_dev(&rr[s].mp) : kNegInf;
-    s1[i] = in ? ld_dev(&rr[s].sp) : 0.f;
-    m2[i] = in ? ld_dev(&rr[s].mq) : kNegInf;
-    s2[i] = in ? ld_dev(&rr[s].sq) : 0.f;
-  }
-  const double Lp = merge_lse(m1, s1, nslot);
-  const double Lq = merge_lse(m2, s2, nslot);
-  const float fp = mp == kNegInf ? 0.f : (float)exp((double)mp - Lp);
-  const float fq = mq == kNegInf ? 0.f : (float)exp((double)mq - Lq);
-  float tvs = 0.f, res = 0.f;
-#pragma unroll
-  for (int e = 0; e < E; ++e) {
-    // separately rounded products (no fused multiply-add), so identical p and
-    // q rows give exactly zero
-#pragma clang fp contract(off)
-    const float d = zp[e] * fp - zq[e] * fq;
-    tvs += fabsf(d);
-    res += fmaxf(d, 0.f);
-  }
-  tvs = wave_sum(tvs);
-  res = wave_sum(res);
-  SpanRec* rec = A.recs + (size_t)t.row * n_spans + t.span;
-  if (lane < 2) (&rec->tv)[lane] = lane == 0 ? tvs : res;  // read only after the sweep
-}
-
 template <bool BF16, int E>
 __global__ void __launch_bounds__(kThreads)
 accept_sweep_kernel(Args A) {
-  __shared__ uint32_t s_ok;
-  const int w = threadIdx.x >> 6;
-  const long total = (long)A.B * (A.gmax + 1) * A.n_chunks;
-  const Task t = make_task<BF16>(A, blockIdx.x, total, w);
-  if (!t.live) return;  // workgroup-uniform
-  float zp[E], zq[E];
-  float mp = kNegInf, mq = kNegInf;
-  load_span<BF16, E>(A, t, zp, zq);
-  pass1<BF16, E>(A, t, zp, zq, mp, mq);
-  if (!t.pair) return;
-  // ---- wait until every chunk of the row has published pass 1
-  stores_done();
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t* c = A.cnt + t.row;
-    __hip_atomic_fetch_add(c, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    uint32_t ok = 0;
-    for (uint32_t it = 0; it <= kSpinLimit; ++it) {
-      if (ld_dev(c) >= (uint32_t)A.n_chunks) {
-        ok = 1;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(2);
+  typedef Elt<BF16> L;
+  constexpr int VEC = L::VEC;
+  constexpr int NV = E / VEC;
+  constexpr int kChunk = kThreads * E;
+  __shared__ int s_rows[kMaxSeqs];
+  __shared__ float s_m[2][kWaves];
+  __shared__ double s_s[3][kWaves];
+  __shared__ double s_L[2];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = tid >> 6;
+  const int nc = A.nc;
+  const int nslot = (nc + 63) / 64;
+  const size_t esz = BF16 ? 2 : 4;
+  const size_t n_rec = (size_t)A.B * (A.gmax + 1) * nc;
+  const __amdgpu_buffer_rsrc_t rs_stats = make_rsrc(A.stats, n_rec * kRecBytes);
+
+  build_row_table(A.gamma, A.gmax, A.B, s_rows);
+  const long n_tasks = (long)s_rows[A.B - 1] * nc;
+
+  for (long task = blockIdx.x; task < n_tasks; task += gridDim.x) {
+    const int rank = (int)(task / nc);
+    const int c = (int)(task % nc);
+    int lo = 0, hi = A.B - 1;  // first sequence whose prefix exceeds rank
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (s_rows[mid] > rank) hi = mid;
+      else lo = mid + 1;
     }
-    if (!ok && A.status) atomicOr(A.status, SR_ST_TIMEOUT);
-    s_ok = ok;
+    const int b = lo;
+    const int first = b ? s_rows[b - 1] : 0;
+    const int j = rank - first;
+    const bool pair = j < s_rows[b] - first - 1;
+    const int row = b * (A.gmax + 1) + j;
+    const char* prow = (const char*)A.p + ((size_t)b * A.p_stride + (size_t)j * A.V) * esz;
+    const char* qrow = (const char*)A.q + ((size_t)b * A.q_stride + (size_t)j * A.V) * esz;
+    const int base = c * kChunk + w * (64 * E);
+
+    // ---- load this wave's 64*E entries (16-byte coalesced loads, all issued
+    // before any is used; entries past V are masked afterwards)
+    float zp[E], zq[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) zq[e] = kNegInf;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) L::load(prow, min(base + (v * 64 + lane) * VEC, A.V - VEC), zp + v * VEC);
+    if (pair) {
+#pragma unroll
+      for (int v = 0; v < NV; ++v) L::load(qrow, min(base + (v * 64 + lane) * VEC, A.V - VEC), zq + v * VEC);
+    }
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const bool in = base + (v * 64 + lane) * VEC < A.V;  // V is a multiple of VEC
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        zp[v * VEC + e] = in ? zp[v * VEC + e] : kNegInf;
+        zq[v * VEC + e] = in ? zq[v * VEC + e] : kNegInf;
+      }
+    }
+
+    // ---- chunk maxima
+    float mp = kNegInf, mq = kNegInf;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      mp = fmaxf(mp, zp[e]);
+      mq = fmaxf(mq, zq[e]);
+    }
+    mp = wave_max(mp);
+    if (pair) mq = wave_max(mq);
+    if (lane == 0) {
+      s_m[0][w] = mp;
+      s_m[1][w] = mq;
+    }
+    __syncthreads();
+    const float cmp = fmaxf(fmaxf(s_m[0][0], s_m[0][1]), fmaxf(s_m[0][2], s_m[0][3]));
+    const float cmq = fmaxf(fmaxf(s_m[1][0], s_m[1][1]), fmaxf(s_m[1][2], s_m[1][3]));
+
+    // ---- exponentials (in place), sums, KL numerator
+    const float rp = cmp == kNegInf ? 0.f : cmp * kLog2e;
+    const float rq = cmq == kNegInf ? 0.f : cmq * kLog2e;
+    double dsp, dsq = 0.0, dkl = 0.0;
+    if (pair) {
+      // groups of four summed as (a0 + a1) + (a2 + a3), then a tree over groups
+      float gp[E / 4], gq[E / 4], gk[E / 4];
+#pragma unroll
+      for (int g = 0; g < E / 4; ++g) {
+        float ep[4], eq[4], kt[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int e = g * 4 + i;
+          const float d = zp[e] - zq[e];
+          ep[i] = exp2_hw(fmaf(zp[e], kLog2e, -rp));
+          eq[i] = exp2_hw(fmaf(zq[e], kLog2e, -rq));
+          kt[i] = ep[i] > 0.f ? ep[i] * d : 0.f;
+          zp[e] = ep[i];
+          zq[e] = eq[i];
+        }
+        gp[g] = (ep[0] + ep[1]) + (ep[2] + ep[3]);
+        gq[g] = (eq[0] + eq[1]) + (eq[2] + eq[3]);
+        gk[g] = (kt[0] + kt[1]) + (kt[2] + kt[3]);
+      }
+      dsp = wave_sum_d((double)tree_sum(gp));
+      dsq = wave_sum_d((double)tree_sum(gq));
+      dkl = wave_sum_d((double)tree_sum(gk));
+    } else {
+      float gp[E / 4];
+#pragma unroll
+      for (int g = 0; g < E / 4; ++g) {
+        float ep[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          ep[i] = exp2_hw(fmaf(zp[g * 4 + i], kLog2e, -rp));
+          zp[g * 4 + i] = ep[i];
+        }
+        gp[g] = (ep[0] + ep[1]) + (ep[2] + ep[3]);
+      }
+      dsp = wave_sum_d((double)tree_sum(gp));
+    }
+    if (lane == 0) {
+      s_s[0][w] = dsp;
+      s_s[1][w] = dsq;
+      s_s[2][w] = dkl;
+    }
+    __syncthreads();
+
+    // ---- publish the chunk record; pair rows then wait for the whole row
+    const size_t rec = (size_t)row * nc + c;
+    if (tid == 0) {
+      StatRec r;
+      r.mp = cmp;
+      r.mq = cmq;
+      r.sp = ((s_s[0][0] + s_s[0][1]) + s_s[0][2]) + s_s[0][3];
+      r.sq = ((s_s[1][0] + s_s[1][1]) + s_s[1][2]) + s_s[1][3];
+      r.kl = ((s_s[2][0] + s_s[2][1]) + s_s[2][2]) + s_s[2][3];
+      u32x4 w0, w1;
+      pack_rec(r, w0, w1);
+      __builtin_amdgcn_raw_buffer_store_b128(w0, rs_stats, (uint32_t)(rec * kRecBytes), 0, kDeviceCoherent);
+      __builtin_amdgcn_raw_buffer_store_b128(w1, rs_stats, (uint32_t)(rec * kRecBytes + 16), 0, kDeviceCoherent);
+    }
+    // Workgroup-uniform. The LDS slots are rewritten only after two more
+    // barriers, when every wave has read them.
+    if (!pair) continue;
+
+    if (w == 0) {
+      // ---- wait until every chunk record of the row is present, then merge
+      float m1[kSlots], m2[kSlots];
+      double s1[kSlots], s2[kSlots];
+      for (uint32_t it = 0;; ++it) {
+        bool ok = true;
+#pragma unroll
+        for (int i = 0; i < kSlots; ++i) {
+          const int cc = lane * nslot + i;
+          const bool in = i < nslot && cc < nc;
+          const uint32_t off = (uint32_t)(((size_t)row * nc + (in ? cc : 0)) * kRecBytes);
+          const u32x4 w0 = __builtin_amdgcn_raw_buffer_load_b128(rs_stats, off, 0, kDeviceCoherent);
+          const u32x4 w1 = __builtin_amdgcn_raw_buffer_load_b128(rs_stats, off + 16, 0, kDeviceCoherent);
+          ok = ok && (!in || rec_present(w0, w1));
+          const StatRec r = unpack_rec(w0, w1);
+          m1[i] = in ? r.mp : kNegInf;
+          m2[i] = in ? r.mq : kNegInf;
+          s1[i] = in ? r.sp : 0.0;
+          s2[i] = in ? r.sq : 0.0;
+        }
+        if (__ballot(!ok) == 0ull) break;
+        if (it == kSpinLimit) {
+          if (lane == 0 && A.status) atomicOr(A.status, SR_ST_TIMEOUT);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(2);
+      }
+      const double Lp = merge_lse(m1, s1);
+      const double Lq = merge_lse(m2, s2);
+      if (lane == 0) {
+        s_L[0] = Lp;
+        s_L[1] = Lq;
+      }
+    }
+    __syncthreads();
+
+    // ---- second pass over the registers: sum |P - Q|
+    const double Lp = s_L[0], Lq = s_L[1];
+    const float fp = cmp == kNegInf ? 0.f : (float)exp((double)cmp - Lp);
+    const float fq = cmq == kNegInf ? 0.f : (float)exp((double)cmq - Lq);
+    float ga[E / 4];
+    {
+      // separately rounded products: identical p and q rows give exactly zero
+#pragma clang fp contract(off)
+#pragma unroll
+      for (int g = 0; g < E / 4; ++g) {
+        float a[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) a[i] = fabsf(zp[g * 4 + i] * fp - zq[g * 4 + i] * fq);
+        ga[g] = (a[0] + a[1]) + (a[2] + a[3]);
+      }
+    }
+    const double dtv = wave_sum_d((double)tree_sum(ga));
+    if (lane == 0) s_s[0][w] = dtv;
+    __syncthreads();
+    if (tid == 0) A.tvabs[rec] = ((s_s[0][0] + s_s[0][1]) + s_s[0][2]) + s_s[0][3];
   }
-  __syncthreads();
-  pass2<E>(A, t, zp, zq, mp, mq);
 }
 
 // ============================================================================
@@ -333,6 +441,14 @@ __device__ void write_invalid(const Args& A, int b, uint32_t bits) {
   }
 }
 
+// Zero the records of sequence b's live rows (the "not yet written" state the
+// next call's sweep waits on). Called by one whole wave.
+__device__ void clear_records(const Args& A, int b, int gam) {
+  const size_t first = (size_t)b * (A.gmax + 1) * A.nc * 2;
+  const size_t n = (size_t)(gam + 1) * A.nc * 2;
+  for (size_t i = threadIdx.x & 63; i < n; i += 64) A.stats[first + i] = u32x4{0u, 0u, 0u, 0u};
+}
+
 // Wave-wide inclusive prefix sum (fp64).
 __device__ __forceinline__ double wave_incl_scan(double x) {
   const int lane = threadIdx.x & 63;
@@ -349,115 +465,177 @@ struct RowRes {
   float p_tok, q_tok, kl, tv;
 };
 
-// Draw one token from the row the wave holds. mass[i] is the mass of span
-// lane*nslot + i (spans in lane-major blocks so the prefix is a lane scan).
-template <bool BF16>
-__device__ int draw_token(const Args& A, int b, int k, bool residual, double lp, double lq,
-                          const double (&mass)[kSpanSlots], int n_spans) {
-  constexpr int VEC = Elt<BF16>::VEC;
+// A row's chunk records, lane-wise (chunk lane*nslot + i in slot i).
+struct RowRecs {
+  float mp[kSlots], mq[kSlots];
+  double sp[kSlots], sq[kSlots], kl[kSlots], ta[kSlots];
+};
+
+__device__ __forceinline__ void load_row(const Args& A, int row, bool pair, RowRecs& R) {
   const int lane = threadIdx.x & 63;
-  const int nslot = (n_spans + 63) / 64;
+  const int nslot = (A.nc + 63) / 64;
+#pragma unroll
+  for (int i = 0; i < kSlots; ++i) {
+    const int cc = lane * nslot + i;
+    const bool in = i < nslot && cc < A.nc;
+    const StatRec r = in ? unpack_rec(A.stats[((size_t)row * A.nc + cc) * 2], A.stats[((size_t)row * A.nc + cc) * 2 + 1])
+                         : StatRec{kNegInf, kNegInf, 0.0, 0.0, 0.0};
+    R.mp[i] = r.mp;
+    R.sp[i] = r.sp;
+    R.mq[i] = pair ? r.mq : kNegInf;
+    R.sq[i] = pair ? r.sq : 0.0;
+    R.kl[i] = pair ? r.kl : 0.0;
+    R.ta[i] = in && pair ? A.tvabs[(size_t)row * A.nc + cc] : 0.0;
+  }
+}
+
+// Draw the token of stopping row k by CDF inversion in ascending vocabulary
+// order (one whole wave).
+template <bool BF16, int E>
+__device__ int draw_token(const Args& A, int b, int k, int gam) {
+  typedef Elt<BF16> L;
+  constexpr int VEC = L::VEC;
+  constexpr int kChunk = kThreads * E;
+  constexpr int kPer = 32;  // entries per lane per 2048-entry block of the chunk
+  const int lane = threadIdx.x & 63;
+  const int nslot = (A.nc + 63) / 64;
   const int G1 = A.gmax + 1;
+  const bool pair = k < gam;
+  RowRecs R;
+  load_row(A, b * G1 + k, pair, R);
+  const double Lp = merge_lse(R.mp, R.sp);
+  const double Lq = pair ? merge_lse(R.mq, R.sq) : 0.0;
+  double pm[kSlots], rm[kSlots];
+  double my_res = 0.0;
+#pragma unroll
+  for (int i = 0; i < kSlots; ++i) {
+    pm[i] = R.mp[i] == kNegInf ? 0.0 : R.sp[i] * exp((double)R.mp[i] - Lp);
+    const double qm = R.mq[i] == kNegInf ? 0.0 : R.sq[i] * exp((double)R.mq[i] - Lq);
+    rm[i] = pair ? fmax(0.0, 0.5 * (R.ta[i] + pm[i] - qm)) : 0.0;
+    my_res += rm[i];
+  }
+  const bool residual = pair && wave_sum_d(my_res) > 0.0;
+  double mass[kSlots];
   double my = 0.0;
   int my_last = -1;
 #pragma unroll
-  for (int i = 0; i < kSpanSlots; ++i) {
-    if (i < nslot) {
-      my += mass[i];
-      if (mass[i] > 0.0) my_last = lane * nslot + i;
-    }
+  for (int i = 0; i < kSlots; ++i) {
+    mass[i] = residual ? rm[i] : pm[i];
+    my += mass[i];
+    if (mass[i] > 0.0) my_last = lane * nslot + i;
   }
   const double incl = wave_incl_scan(my);
   const double W = __shfl(incl, 63, 64);
   const double target = (double)A.u_res[(size_t)b * G1 + k] * W;
-  int last_span = my_last;
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) last_span = max(last_span, __shfl_xor(last_span, off, 64));
-  int s0 = -1;
-  double prefix = 0.0;
+  // the chunk holding the target: the first with positive mass whose end exceeds it
+  int cs = -1;
+  double pre = 0.0;
   const unsigned long long hit = __ballot(incl > target && my > 0.0);
   if (hit) {
     const int hl = __ffsll((long long)hit) - 1;
-    double c = incl - my;
+    double run = incl - my;
     int found = -1;
-    double pre = 0.0;
+    double fpre = 0.0;
 #pragma unroll
-    for (int i = 0; i < kSpanSlots; ++i) {
-      if (i < nslot && found < 0 && mass[i] > 0.0 && c + mass[i] > target) {
+    for (int i = 0; i < kSlots; ++i) {
+      if (found < 0 && mass[i] > 0.0 && run + mass[i] > target) {
         found = lane * nslot + i;
-        pre = c;
+        fpre = run;
       }
-      if (i < nslot) c += mass[i];
+      run += mass[i];
     }
-    s0 = __shfl(found, hl, 64);
-    prefix = __shfl(pre, hl, 64);
+    cs = __shfl(found, hl, 64);
+    pre = __shfl(fpre, hl, 64);
   }
-  if (s0 < 0) {  // rounding put the target past the total: the last span with mass
-    s0 = max(last_span, 0);
-    double pre = 0.0;
+  if (cs < 0) {  // rounding put the target at the very end: the last chunk with mass
+    int last = my_last;
 #pragma unroll
-    for (int i = 0; i < kSpanSlots; ++i)
-      if (i < nslot && lane * nslot + i < s0) pre += mass[i];
-    prefix = wave_sum_d(pre);
+    for (int off = 32; off > 0; off >>= 1) last = max(last, __shfl_xor(last, off, 64));
+    cs = max(last, 0);
+    double before = 0.0;
+#pragma unroll
+    for (int i = 0; i < kSlots; ++i)
+      if (lane * nslot + i < cs) before += mass[i];
+    pre = wave_sum_d(before);
   }
-  // scan spans s0.. in fp64, ascending vocabulary order
+  // the chunk's maxima, exactly as the sweep used them
+  float cmp = kNegInf, cmq = kNegInf;
+#pragma unroll
+  for (int i = 0; i < kSlots; ++i)
+    if (lane * nslot + i == cs) {
+      cmp = R.mp[i];
+      cmq = R.mq[i];
+    }
+  cmp = wave_max(cmp);
+  cmq = wave_max(cmq);
+  const float rp = cmp == kNegInf ? 0.f : cmp * kLog2e;
+  const float rq = cmq == kNegInf ? 0.f : cmq * kLog2e;
+  const float fp = cmp == kNegInf ? 0.f : (float)exp((double)cmp - Lp);
+  const float fq = cmq == kNegInf ? 0.f : (float)exp((double)cmq - Lq);
   const size_t esz = BF16 ? 2 : 4;
-  const void* prow = (const char*)A.p + ((size_t)b * A.p_stride + (size_t)k * A.V) * esz;
-  const void* qrow = residual ? (const char*)A.q + ((size_t)b * A.q_stride + (size_t)k * A.V) * esz : nullptr;
-  const int E = A.span / 64;
-  double rem = target - prefix;
-  int tok = -1;
-  int last_tok = -1;
-  for (int s = s0; s < n_spans && tok < 0; ++s) {
-    const int base = (s / kWaves) * A.chunk + (s % kWaves) * A.span;
-    for (int v = 0; v < E / VEC && tok < 0; ++v) {
-      const int x0 = base + (v * 64 + lane) * VEC;
-      double wl[VEC];
-      double sum = 0.0;
+  const char* prow = (const char*)A.p + ((size_t)b * A.p_stride + (size_t)k * A.V) * esz;
+  const char* qrow = (const char*)A.q + ((size_t)b * A.q_stride + (size_t)k * A.V) * esz;
+  double rem = target - pre;
+  int tok = -1, last_tok = -1;
+  for (int blk = 0; blk < kChunk / (64 * kPer) && tok < 0; ++blk) {
+    const int x0 = cs * kChunk + blk * 64 * kPer + lane * kPer;
+    float wt[kPer];
+    double sum = 0.0;
+    int mine = -1;
+#pragma unroll
+    for (int v = 0; v < kPer / VEC; ++v) {
+      const int x = x0 + v * VEC;
+      const int xl = min(x, A.V - VEC);
+      float zp[VEC], zq[VEC];
+      L::load(prow, xl, zp);
+      if (residual) L::load(qrow, xl, zq);
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
-        double wt = 0.0;
-        if (x0 + e < A.V) {
-          wt = exp((double)Elt<BF16>::one(prow, x0 + e) - lp);
-          if (residual) wt = fmax(0.0, wt - exp((double)Elt<BF16>::one(qrow, x0 + e) - lq));
-        }
-        wl[e] = wt;
-        sum += wt;
-      }
-      const double inc = wave_incl_scan(sum);
-      const double total = __shfl(inc, 63, 64);
-      int mine = -1;
-#pragma unroll
-      for (int e = 0; e < VEC; ++e)
-        if (wl[e] > 0.0) mine = x0 + e;
-      int lmax = mine;
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) lmax = max(lmax, __shfl_xor(lmax, off, 64));
-      if (lmax >= 0) last_tok = lmax;
-      if (rem < total) {
-        const unsigned long long h = __ballot(inc > rem);
-        const int hl = __ffsll((long long)h) - 1;
-        int found = -1;
-        if (lane == hl) {
-          double c = inc - sum;
-#pragma unroll
-          for (int e = 0; e < VEC; ++e) {
-            c += wl[e];
-            if (found < 0 && wl[e] > 0.0 && c > rem) found = x0 + e;
+        float wv = 0.f;
+        if (x < A.V) {
+#pragma clang fp contract(off)
+          const float ep = exp2_hw(fmaf(zp[e], kLog2e, -rp));
+          if (residual) {
+            const float eq = exp2_hw(fmaf(zq[e], kLog2e, -rq));
+            wv = fmaxf(ep * fp - eq * fq, 0.f);
+          } else {
+            wv = ep * fp;
           }
-          if (found < 0) found = mine;
         }
-        tok = __shfl(found, hl, 64);
-      } else {
-        rem -= total;
+        wt[v * VEC + e] = wv;
+        sum += (double)wv;
+        if (wv > 0.f) mine = x + e;
       }
+    }
+    int lmax = mine;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) lmax = max(lmax, __shfl_xor(lmax, off, 64));
+    if (lmax >= 0) last_tok = lmax;
+    const double inc = wave_incl_scan(sum);
+    const double total = __shfl(inc, 63, 64);
+    if (rem < total) {
+      const unsigned long long h = __ballot(inc > rem);
+      const int hl = __ffsll((long long)h) - 1;
+      int found = -1;
+      if (lane == hl) {
+        double run = inc - sum;
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+          run += (double)wt[e];
+          if (found < 0 && wt[e] > 0.f && run > rem) found = x0 + e;
+        }
+        if (found < 0) found = mine;
+      }
+      tok = __shfl(found, hl, 64);
+    } else {
+      rem -= total;
     }
   }
   if (tok < 0) tok = last_tok < 0 ? 0 : last_tok;
   return tok;
 }
 
-template <bool BF16>
+template <bool BF16, int E>
 __global__ void __launch_bounds__(1024)
 accept_finish_kernel(Args A) {
   __shared__ RowRes rr[kMaxRows];
@@ -467,8 +645,6 @@ accept_finish_kernel(Args A) {
   const int w = threadIdx.x >> 6;
   const int nw = blockDim.x >> 6;
   const int G1 = A.gmax + 1;
-  const int n_spans = A.n_chunks * kWaves;
-  const int nslot = (n_spans + 63) / 64;
   const int gam = A.gamma[b];
   if (gam < 0 || gam > A.gmax) {
     if (w == 0) write_invalid(A, b, SR_ST_GAMMA);
@@ -490,117 +666,52 @@ accept_finish_kernel(Args A) {
   }
   if (threadIdx.x == 0 && A.kv_len && A.kv_len[b] < gam + 1) bad |= SR_ST_KVLEN;
   if (bad) atomicOr(&s_bad, bad);
-  // ---- reset the sweep's row counters for the next call
-  for (int j = threadIdx.x; j < gam; j += blockDim.x) A.cnt[b * G1 + j] = 0u;
-  // ---- finalise rows (one wave per row); spans in lane-major blocks of nslot
-  double lp_k = 0.0, lq_k = 0.0;
-  double mass[kSpanSlots];
-  int my_row = -1;
-  for (int j = w; j <= gam; j += nw) {
-    const SpanRec* rp = A.recs + (size_t)(b * G1 + j) * n_spans;
-    const bool pair = j < gam;
-    float mp[kSpanSlots], sp[kSpanSlots], mq[kSpanSlots], sq[kSpanSlots], klv[kSpanSlots], tvv[kSpanSlots],
-        rsv[kSpanSlots];
+  // ---- per-row results (one wave per row)
+  const size_t esz = BF16 ? 2 : 4;
+  for (int j = w; j < gam; j += nw) {
+    RowRecs R;
+    load_row(A, b * G1 + j, true, R);
+    const double Lp = merge_lse(R.mp, R.sp);
+    const double Lq = merge_lse(R.mq, R.sq);
+    double tvd = 0.0, kld = 0.0;
 #pragma unroll
-    for (int i = 0; i < kSpanSlots; ++i) {
-      const int s = lane * nslot + i;
-      const bool in = i < nslot && s < n_spans;
-      mp[i] = in ? rp[s].mp : kNegInf;
-      sp[i] = in ? rp[s].sp : 0.f;
-      mq[i] = in && pair ? rp[s].mq : kNegInf;
-      sq[i] = in && pair ? rp[s].sq : 0.f;
-      klv[i] = in && pair ? rp[s].kl : 0.f;
-      tvv[i] = in && pair ? rp[s].tv : 0.f;
-      rsv[i] = in && pair ? rp[s].res : 0.f;
+    for (int i = 0; i < kSlots; ++i) {
+      tvd += R.ta[i];
+      if (R.mp[i] != kNegInf) kld += R.kl[i] * exp((double)R.mp[i] - Lp);
     }
-    const double Lp = merge_lse(mp, sp, nslot);
-    double Lq = 0.0, tvd = 0.0, kld = 0.0;
-    if (pair) {
-      Lq = merge_lse(mq, sq, nslot);
-#pragma unroll
-      for (int i = 0; i < kSpanSlots; ++i) {
-        tvd += (double)tvv[i];
-        if (mp[i] != kNegInf) kld += (double)klv[i] * exp((double)mp[i] - Lp);
-      }
-      tvd = 0.5 * wave_sum_d(tvd);
-      kld = wave_sum_d(kld) - (Lp - Lq);
-    }
-    // span masses for a possible draw from this row: residual (pair rows) and p
-    double res_tot = 0.0;
-#pragma unroll
-    for (int i = 0; i < kSpanSlots; ++i) res_tot += (double)rsv[i];
-    const bool residual = pair && wave_sum_d(res_tot) > 0.0;
-#pragma unroll
-    for (int i = 0; i < kSpanSlots; ++i)
-      mass[i] = residual ? (double)rsv[i] : (mp[i] == kNegInf ? 0.0 : (double)sp[i] * exp((double)mp[i] - Lp));
-    my_row = j;
-    lp_k = Lp;
-    lq_k = Lq;
+    tvd = 0.5 * wave_sum_d(tvd);
+    kld = wave_sum_d(kld) - (Lp - Lq);
     if (lane == 0) {
-      double a = 1.0, pt = __builtin_nan(""), qt = __builtin_nan("");
-      if (pair) {
-        const int x = A.drafts[(size_t)b * A.gmax + j];
-        a = __builtin_nan("");
-        if (x >= 0 && x < A.V) {
-          const RowLogits rl = A.rowx[b * G1 + j];
-          const double lpx = (double)rl.zp - Lp;
-          const double lqx = (double)rl.zq - Lq;
-          pt = exp(lpx);
-          qt = exp(lqx);
-          a = (lqx == -INFINITY || lpx >= lqx) ? 1.0 : exp(lpx - lqx);
-        }
+      double a = __builtin_nan(""), pt = __builtin_nan(""), qt = __builtin_nan("");
+      const int x = A.drafts[(size_t)b * A.gmax + j];
+      if (x >= 0 && x < A.V) {
+        const char* prow = (const char*)A.p + ((size_t)b * A.p_stride + (size_t)j * A.V) * esz;
+        const char* qrow = (const char*)A.q + ((size_t)b * A.q_stride + (size_t)j * A.V) * esz;
+        const double lpx = (double)Elt<BF16>::one(prow, x) - Lp;
+        const double lqx = (double)Elt<BF16>::one(qrow, x) - Lq;
+        pt = exp(lpx);
+        qt = exp(lqx);
+        a = (lqx == -INFINITY || lpx >= lqx) ? 1.0 : exp(lpx - lqx);
       }
       rr[j] = RowRes{a, (float)pt, (float)qt, (float)kld, (float)tvd};
     }
-    // a wave keeps the masses of its last row only; more rows than waves
-    // (gamma_max = 16) are re-derived below by the owning wave if needed
-    if (j + nw <= gam) my_row = -1;
   }
   __syncthreads();
   if (s_bad) {
-    if (w == 0) write_invalid(A, b, s_bad);
+    if (w == 0) {
+      clear_records(A, b, gam);  // every wave has finished reading them
+      write_invalid(A, b, s_bad);
+    }
     return;
   }
-  // ---- accept chain: first j with NOT (u_acc < a_j) (every wave computes it)
+  if (w != 0) return;
+  // ---- accept chain: first j with NOT (u_acc < a_j)
   bool rej = false;
   if (lane < gam) rej = !((double)A.u_acc[(size_t)b * A.gmax + lane] < rr[lane].a);
   const unsigned long long rmask = __ballot(rej);
   const int k = rmask ? (__ffsll((long long)rmask) - 1) : gam;
-  const int owner = k % nw;
-  if (w != owner) return;
-  if (my_row != k) {
-    // the owning wave processed row k before its last row: rebuild its masses
-    const SpanRec* rp = A.recs + (size_t)(b * G1 + k) * n_spans;
-    const bool pair = k < gam;
-    float mp[kSpanSlots], sp[kSpanSlots], mq[kSpanSlots], sq[kSpanSlots], rsv[kSpanSlots];
-#pragma unroll
-    for (int i = 0; i < kSpanSlots; ++i) {
-      const int s = lane * nslot + i;
-      const bool in = i < nslot && s < n_spans;
-      mp[i] = in ? rp[s].mp : kNegInf;
-      sp[i] = in ? rp[s].sp : 0.f;
-      mq[i] = in && pair ? rp[s].mq : kNegInf;
-      sq[i] = in && pair ? rp[s].sq : 0.f;
-      rsv[i] = in && pair ? rp[s].res : 0.f;
-    }
-    lp_k = merge_lse(mp, sp, nslot);
-    lq_k = pair ? merge_lse(mq, sq, nslot) : 0.0;
-    double res_tot = 0.0;
-#pragma unroll
-    for (int i = 0; i < kSpanSlots; ++i) res_tot += (double)rsv[i];
-    const bool residual = pair && wave_sum_d(res_tot) > 0.0;
-#pragma unroll
-    for (int i = 0; i < kSpanSlots; ++i)
-      mass[i] = residual ? (double)rsv[i] : (mp[i] == kNegInf ? 0.0 : (double)sp[i] * exp((double)mp[i] - lp_k));
-  }
-  bool residual = false;
-  if (k < gam) {
-    double tot = 0.0;
-    const SpanRec* rp = A.recs + (size_t)(b * G1 + k) * n_spans;
-    for (int s = lane; s < n_spans; s += 64) tot += (double)rp[s].res;
-    residual = wave_sum_d(tot) > 0.0;
-  }
-  const int tok = draw_token<BF16>(A, b, k, residual, lp_k, lq_k, mass, n_spans);
+  const int tok = draw_token<BF16, E>(A, b, k, gam);
+  clear_records(A, b, gam);  // every read of them is done
   // ---- outputs
   int32_t* ot = A.out_tokens + (size_t)b * G1;
   for (int j = lane; j <= A.gmax; j += 64) ot[j] = j < k ? A.drafts[(size_t)b * A.gmax + j] : (j == k ? tok : -1);
@@ -620,36 +731,53 @@ accept_finish_kernel(Args A) {
   }
 }
 
-// Entries per lane per row: the sweep's register tile.
-constexpr int kE = 16;
+// Entries per lane per chunk.
+constexpr int kEf32 = 16;
+constexpr int kEbf16 = 32;
 
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 struct Layout {
-  size_t recs, rowx, cnt, total;
+  size_t stats, tvabs, total;
 };
 
 Layout layout(int B, int gamma_max, int n_chunks) {
   const size_t rows = (size_t)B * (gamma_max + 1);
-  const size_t spans = rows * n_chunks * kWaves;
   Layout L;
-  L.recs = 0;
-  L.rowx = L.recs + align256(spans * sizeof(SpanRec));
-  L.cnt = L.rowx + align256(rows * sizeof(RowLogits));
-  L.total = L.cnt + align256(rows * sizeof(uint32_t));
+  L.stats = 0;
+  L.tvabs = align256(rows * n_chunks * kRecBytes);
+  L.total = L.tvabs + align256(rows * n_chunks * sizeof(double));
   return L;
+}
+
+template <bool BF16>
+const void* sweep_fn() {
+  return (const void*)accept_sweep_kernel<BF16, BF16 ? kEbf16 : kEf32>;
 }
 
 }  // namespace
 
 int accept_plan(int B, int gamma_max, int V, int dtype, AcceptPlan* plan) {
-  plan->chunk = kThreads * kE;
+  const bool bf16 = dtype == SR_BF16;
+  plan->chunk = kThreads * (bf16 ? kEbf16 : kEf32);
   plan->n_chunks = (V + plan->chunk - 1) / plan->chunk;
-  if (plan->n_chunks * kWaves > kMaxSpans) return SR_EUNSUPPORTED;
+  if (plan->n_chunks > kMaxChunks) return SR_EUNSUPPORTED;
+  const int Bl = B < kMaxSeqs ? B : kMaxSeqs;
+  if ((size_t)Bl * (gamma_max + 1) * plan->n_chunks * kRecBytes >= 0x7fffffffu) return SR_EUNSUPPORTED;
   plan->workspace_bytes = layout(B, gamma_max, plan->n_chunks).total;
-  const long tasks = (long)B * (gamma_max + 1) * plan->n_chunks;
-  if (tasks > 0x7fffffffL) return SR_EINVAL;
-  const long grid = tasks;
+  // persistent grid: every workgroup resident at once, a multiple of the
+  // chunks per row, and no more than the largest possible task count
+  const int cus = device_cu_count();
+  if (cus <= 0) return SR_ELAUNCH;
+  int per_cu = 1;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, bf16 ? sweep_fn<true>() : sweep_fn<false>(),
+                                                   kThreads, 0) != hipSuccess || per_cu < 1)
+    per_cu = 1;
+  const long cap = (long)cus * per_cu;
+  long grid = cap / plan->n_chunks * plan->n_chunks;
+  if (grid == 0) grid = cap;
+  const long max_tasks = (long)Bl * (gamma_max + 1) * plan->n_chunks;
+  if (grid > max_tasks) grid = max_tasks;
   plan->grid = (int)grid;
   return SR_OK;
 }
@@ -661,47 +789,50 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
                   float* q_tok, float* kl, float* tv, int B, int gamma_max, int V,
                   void* workspace, const AcceptPlan& plan, int32_t* status, hipStream_t stream) {
   const Layout L = layout(B, gamma_max, plan.n_chunks);
+  const int G1 = gamma_max + 1;
+  const size_t esz = dtype == SR_BF16 ? 2 : 4;
   char* ws = (char*)workspace;
-  Args A;
-  A.p = p_logits;
-  A.p_stride = p_stride;
-  A.q = q_logits;
-  A.q_stride = q_stride;
-  A.drafts = drafts;
-  A.gamma = gamma;
-  A.u_acc = u_acc;
-  A.u_res = u_res;
-  A.kv_len = kv_len;
-  A.accept_len = accept_len;
-  A.out_tokens = out_tokens;
-  A.new_len = new_len;
-  A.accept_prob = accept_prob;
-  A.p_tok = p_tok;
-  A.q_tok = q_tok;
-  A.kl = kl;
-  A.tv = tv;
-  A.B = B;
-  A.gmax = gamma_max;
-  A.V = V;
-  A.n_chunks = plan.n_chunks;
-  A.chunk = plan.chunk;
-  A.span = plan.chunk / kWaves;
-  A.recs = (SpanRec*)(ws + L.recs);
-  A.rowx = (RowLogits*)(ws + L.rowx);
-  A.cnt = (uint32_t*)(ws + L.cnt);
-  A.status = status;
-  const long tasks = (long)B * (gamma_max + 1) * plan.n_chunks;
-  if (dtype == SR_BF16)
-    hipLaunchKernelGGL((accept_sweep_kernel<true, kE>), dim3((unsigned)tasks), dim3(kThreads), 0, stream, A);
-  else
-    hipLaunchKernelGGL((accept_sweep_kernel<false, kE>), dim3((unsigned)tasks), dim3(kThreads), 0, stream, A);
-  if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
-  const int nw = gamma_max + 1 < 16 ? gamma_max + 1 : 16;
-  if (dtype == SR_BF16)
-    hipLaunchKernelGGL(accept_finish_kernel<true>, dim3(B), dim3(64 * nw), 0, stream, A);
-  else
-    hipLaunchKernelGGL(accept_finish_kernel<false>, dim3(B), dim3(64 * nw), 0, stream, A);
-  return hipGetLastError() == hipSuccess ? SR_OK : SR_ELAUNCH;
+  const int nw = G1 < 16 ? G1 : 16;
+  // sequences in launches of at most kMaxSeqs (the sweep's row table)
+  for (int b0 = 0; b0 < B; b0 += kMaxSeqs) {
+    const int Bl = B - b0 < kMaxSeqs ? B - b0 : kMaxSeqs;
+    Args A;
+    A.p = (const char*)p_logits + (size_t)b0 * p_stride * esz;
+    A.p_stride = p_stride;
+    A.q = q_logits ? (const char*)q_logits + (size_t)b0 * q_stride * esz : nullptr;
+    A.q_stride = q_stride;
+    A.drafts = drafts ? drafts + (size_t)b0 * gamma_max : nullptr;
+    A.gamma = gamma + b0;
+    A.u_acc = u_acc ? u_acc + (size_t)b0 * gamma_max : nullptr;
+    A.u_res = u_res + (size_t)b0 * G1;
+    A.kv_len = kv_len ? kv_len + b0 : nullptr;
+    A.accept_len = accept_len + b0;
+    A.out_tokens = out_tokens + (size_t)b0 * G1;
+    A.new_len = new_len ? new_len + b0 : nullptr;
+    A.accept_prob = accept_prob ? accept_prob + (size_t)b0 * gamma_max : nullptr;
+    A.p_tok = p_tok ? p_tok + (size_t)b0 * gamma_max : nullptr;
+    A.q_tok = q_tok ? q_tok + (size_t)b0 * gamma_max : nullptr;
+    A.kl = kl ? kl + (size_t)b0 * gamma_max : nullptr;
+    A.tv = tv ? tv + (size_t)b0 * gamma_max : nullptr;
+    A.B = Bl;
+    A.gmax = gamma_max;
+    A.V = V;
+    A.nc = plan.n_chunks;
+    A.stats = (u32x4*)(ws + L.stats) + (size_t)b0 * G1 * plan.n_chunks * 2;
+    A.tvabs = (double*)(ws + L.tvabs) + (size_t)b0 * G1 * plan.n_chunks;
+    A.status = status;
+    if (dtype == SR_BF16)
+      hipLaunchKernelGGL((accept_sweep_kernel<true, kEbf16>), dim3(plan.grid), dim3(kThreads), 0, stream, A);
+    else
+      hipLaunchKernelGGL((accept_sweep_kernel<false, kEf32>), dim3(plan.grid), dim3(kThreads), 0, stream, A);
+    if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
+    if (dtype == SR_BF16)
+      hipLaunchKernelGGL((accept_finish_kernel<true, kEbf16>), dim3(Bl), dim3(64 * nw), 0, stream, A);
+    else
+      hipLaunchKernelGGL((accept_finish_kernel<false, kEf32>), dim3(Bl), dim3(64 * nw), 0, stream, A);
+    if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
+  }
+  return SR_OK;
 }
 
 }  // namespace sr
