@@ -162,20 +162,37 @@ __device__ __forceinline__ float tree_sum(float (&v)[N]) {
   return v[0];
 }
 
-// Log-normaliser of a row from its chunk records held lane-wise (chunk
-// lane*nslot + i in slot i): max, then an fp64 sum in a fixed order. Both
-// kernels call this with the same layout and get bit-identical results.
-__device__ __forceinline__ double merge_lse(const float (&m)[kSlots], const double (&s)[kSlots]) {
+// Normaliser of a row: its maximum M and S = sum over chunks of
+// s_c 2^((m_c - M) log2 e), so that softmax(z) = e^(z - M) / S. A chunk's
+// entries e^(z - m_c) (as the chunk sums hold them) turn into probabilities
+// by the factor f_c = 2^((m_c - M) log2 e) / S. The chunk records are held
+// lane-wise (chunk lane*nslot + i in slot i) and merged in a fixed order, so
+// the sweep and the finish kernel get bit-identical M, S and f_c.
+struct RowNorm {
+  float M;     // row maximum (-inf: none)
+  double S;    // sum of the chunks' rescaled sums (>= 1 when M is finite)
+  float invS;  // 1/S rounded to fp32
+  __device__ float factor(float m) const {  // f_c for a chunk whose maximum is m
+    return m == kNegInf ? 0.f : exp2_hw((m - M) * kLog2e) * invS;
+  }
+  __device__ double log_norm() const { return (double)M + log(S); }  // ln sum e^z
+};
+
+__device__ __forceinline__ RowNorm row_norm(const float (&m)[kSlots], const double (&s)[kSlots]) {
+  RowNorm r;
   float ml = kNegInf;
 #pragma unroll
   for (int i = 0; i < kSlots; ++i) ml = fmaxf(ml, m[i]);
-  const float M = wave_max(ml);
-  if (M == kNegInf) return -INFINITY;
+  r.M = wave_max(ml);
   double acc = 0.0;
+  if (r.M != kNegInf) {
 #pragma unroll
-  for (int i = 0; i < kSlots; ++i)
-    if (m[i] != kNegInf) acc += s[i] * exp((double)m[i] - (double)M);
-  return (double)M + log(wave_sum_d(acc));
+    for (int i = 0; i < kSlots; ++i)
+      if (m[i] != kNegInf) acc += s[i] * (double)exp2_hw((m[i] - r.M) * kLog2e);
+  }
+  r.S = wave_sum_d(acc);
+  r.invS = r.S > 0.0 ? (float)(1.0 / r.S) : 0.f;
+  return r;
 }
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, size_t bytes) {
@@ -214,78 +231,151 @@ __device__ void build_row_table(const int32_t* gamma, int gmax, int B, int* rows
 // ============================================================================
 // Sweep kernel
 
+// One task's entries as loaded: fp32 entries are replaced by their
+// exponentials in the first pass and kept for the second; bf16 entries stay
+// packed and the second pass recomputes the exponentials (the registers then
+// hold twice as many entries per byte of HBM read).
+template <bool BF16, int E>
+struct Raw;
+template <int E>
+struct Raw<false, E> {
+  float p[E], q[E];  // exponentials after the first pass
+  __device__ float gp(int e) const { return p[e]; }
+  __device__ float gq(int e) const { return q[e]; }
+};
+// An opaque copy: each phase unpacks bf16 entries afresh instead of the
+// compiler keeping every unpacked value live from the first use to the last.
+__device__ __forceinline__ uint32_t fresh(uint32_t x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+template <int E>
+struct Raw<true, E> {
+  u32x4 p[E / 8], q[E / 8];
+  __device__ float gp(int e) const {
+    const uint32_t w = fresh(p[e / 8][(e % 8) / 2]);
+    return (e & 1) ? bf16_hi(w) : bf16_lo(w);
+  }
+  __device__ float gq(int e) const {
+    const uint32_t w = fresh(q[e / 8][(e % 8) / 2]);
+    return (e & 1) ? bf16_hi(w) : bf16_lo(w);
+  }
+};
+
+struct TaskInfo {
+  int b, j, c, row;
+  bool pair;
+  const char* prow;
+  const char* qrow;  // the p row itself for a bonus row (its loads then hit cached lines)
+};
+
+template <bool BF16>
+__device__ __forceinline__ TaskInfo decode_task(const Args& A, const int* rows, long task) {
+  TaskInfo t;
+  const int rank = (int)(task / A.nc);
+  t.c = (int)(task % A.nc);
+  int lo = 0, hi = A.B - 1;  // first sequence whose prefix exceeds rank
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (rows[mid] > rank) hi = mid;
+    else lo = mid + 1;
+  }
+  t.b = lo;
+  const int first = lo ? rows[lo - 1] : 0;
+  t.j = rank - first;
+  t.pair = t.j < rows[lo] - first - 1;
+  t.row = t.b * (A.gmax + 1) + t.j;
+  const size_t esz = BF16 ? 2 : 4;
+  t.prow = (const char*)A.p + ((size_t)t.b * A.p_stride + (size_t)t.j * A.V) * esz;
+  t.qrow = t.pair ? (const char*)A.q + ((size_t)t.b * A.q_stride + (size_t)t.j * A.V) * esz : t.prow;
+  return t;
+}
+
+// Issue the loads of one task (always the same count, so the waits of the
+// task before it stay exact). Offsets past V are clamped into the row.
+template <bool BF16, int E>
+__device__ __forceinline__ void issue_loads(const Args& A, const TaskInfo& t, Raw<BF16, E>& r) {
+  constexpr int VEC = Elt<BF16>::VEC;
+  constexpr int NV = E / VEC;
+  const int lane = threadIdx.x & 63;
+  const int base = t.c * (kThreads * E) + (threadIdx.x >> 6) * (64 * E);
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    const int x = min(base + (v * 64 + lane) * VEC, A.V - VEC);
+    if constexpr (BF16) {
+      r.p[v] = *(const u32x4*)((const uint16_t*)t.prow + x);
+    } else {
+      const floatx4 f = *(const floatx4*)((const float*)t.prow + x);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) r.p[v * 4 + i] = f[i];
+    }
+  }
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    const int x = min(base + (v * 64 + lane) * VEC, A.V - VEC);
+    if constexpr (BF16) {
+      r.q[v] = *(const u32x4*)((const uint16_t*)t.qrow + x);
+    } else {
+      const floatx4 f = *(const floatx4*)((const float*)t.qrow + x);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) r.q[v * 4 + i] = f[i];
+    }
+  }
+}
+
 template <bool BF16, int E>
 __global__ void __launch_bounds__(kThreads)
 accept_sweep_kernel(Args A) {
-  typedef Elt<BF16> L;
-  constexpr int VEC = L::VEC;
-  constexpr int NV = E / VEC;
+  constexpr int VEC = Elt<BF16>::VEC;
   constexpr int kChunk = kThreads * E;
-  __shared__ int s_rows[kMaxSeqs];
+  extern __shared__ int s_rows[];  // [B] inclusive prefix of live rows
   __shared__ float s_m[2][kWaves];
   __shared__ double s_s[3][kWaves];
-  __shared__ double s_L[2];
+  __shared__ float s_f[2];  // this chunk's factors f_c for p and q
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = tid >> 6;
   const int nc = A.nc;
   const int nslot = (nc + 63) / 64;
-  const size_t esz = BF16 ? 2 : 4;
   const size_t n_rec = (size_t)A.B * (A.gmax + 1) * nc;
   const __amdgpu_buffer_rsrc_t rs_stats = make_rsrc(A.stats, n_rec * kRecBytes);
 
   build_row_table(A.gamma, A.gmax, A.B, s_rows);
   const long n_tasks = (long)s_rows[A.B - 1] * nc;
+  long task = blockIdx.x;
+  if (task >= n_tasks) return;
+  TaskInfo t = decode_task<BF16>(A, s_rows, task);
+  Raw<BF16, E> cur;
+  issue_loads<BF16, E>(A, t, cur);
 
-  for (long task = blockIdx.x; task < n_tasks; task += gridDim.x) {
-    const int rank = (int)(task / nc);
-    const int c = (int)(task % nc);
-    int lo = 0, hi = A.B - 1;  // first sequence whose prefix exceeds rank
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (s_rows[mid] > rank) hi = mid;
-      else lo = mid + 1;
-    }
-    const int b = lo;
-    const int first = b ? s_rows[b - 1] : 0;
-    const int j = rank - first;
-    const bool pair = j < s_rows[b] - first - 1;
-    const int row = b * (A.gmax + 1) + j;
-    const char* prow = (const char*)A.p + ((size_t)b * A.p_stride + (size_t)j * A.V) * esz;
-    const char* qrow = (const char*)A.q + ((size_t)b * A.q_stride + (size_t)j * A.V) * esz;
-    const int base = c * kChunk + w * (64 * E);
+  for (;;) {
+    // ---- prefetch the next task (the current one again past the end)
+    const long task_n = task + gridDim.x;
+    const bool more = task_n < n_tasks;
+    const TaskInfo tn = decode_task<BF16>(A, s_rows, more ? task_n : task);
+    Raw<BF16, E> nxt;
+    __builtin_amdgcn_sched_barrier(0);
+    issue_loads<BF16, E>(A, tn, nxt);
+    __builtin_amdgcn_sched_barrier(0);
 
-    // ---- load this wave's 64*E entries (16-byte coalesced loads, all issued
-    // before any is used; entries past V are masked afterwards)
-    float zp[E], zq[E];
-#pragma unroll
-    for (int e = 0; e < E; ++e) zq[e] = kNegInf;
-#pragma unroll
-    for (int v = 0; v < NV; ++v) L::load(prow, min(base + (v * 64 + lane) * VEC, A.V - VEC), zp + v * VEC);
-    if (pair) {
-#pragma unroll
-      for (int v = 0; v < NV; ++v) L::load(qrow, min(base + (v * 64 + lane) * VEC, A.V - VEC), zq + v * VEC);
-    }
-#pragma unroll
-    for (int v = 0; v < NV; ++v) {
-      const bool in = base + (v * 64 + lane) * VEC < A.V;  // V is a multiple of VEC
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) {
-        zp[v * VEC + e] = in ? zp[v * VEC + e] : kNegInf;
-        zq[v * VEC + e] = in ? zq[v * VEC + e] : kNegInf;
-      }
-    }
+    const int base = t.c * kChunk + w * (64 * E);
+    auto in_v = [&](int e) __attribute__((always_inline)) {  // entry e lies below V
+      return base + ((e / VEC) * 64 + lane) * VEC < A.V;
+    };
 
     // ---- chunk maxima
     float mp = kNegInf, mq = kNegInf;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-      mp = fmaxf(mp, zp[e]);
-      mq = fmaxf(mq, zq[e]);
+      const bool in = in_v(e);
+      const float zp = cur.gp(e), zq = cur.gq(e);  // unconditional: then a select
+      mp = fmaxf(mp, in ? zp : kNegInf);
+      mq = fmaxf(mq, in && t.pair ? zq : kNegInf);
+      if (e % 8 == 7) __builtin_amdgcn_sched_barrier(0);  // unpack eight entries at a time
     }
     mp = wave_max(mp);
-    if (pair) mq = wave_max(mq);
+    if (t.pair) mq = wave_max(mq);
     if (lane == 0) {
       s_m[0][w] = mp;
       s_m[1][w] = mq;
@@ -294,12 +384,12 @@ accept_sweep_kernel(Args A) {
     const float cmp = fmaxf(fmaxf(s_m[0][0], s_m[0][1]), fmaxf(s_m[0][2], s_m[0][3]));
     const float cmq = fmaxf(fmaxf(s_m[1][0], s_m[1][1]), fmaxf(s_m[1][2], s_m[1][3]));
 
-    // ---- exponentials (in place), sums, KL numerator
+    // ---- exponentials, sums, KL numerator. Groups of four are summed as
+    // (a0 + a1) + (a2 + a3), then a tree over groups.
     const float rp = cmp == kNegInf ? 0.f : cmp * kLog2e;
     const float rq = cmq == kNegInf ? 0.f : cmq * kLog2e;
     double dsp, dsq = 0.0, dkl = 0.0;
-    if (pair) {
-      // groups of four summed as (a0 + a1) + (a2 + a3), then a tree over groups
+    if (t.pair) {
       float gp[E / 4], gq[E / 4], gk[E / 4];
 #pragma unroll
       for (int g = 0; g < E / 4; ++g) {
@@ -307,16 +397,20 @@ accept_sweep_kernel(Args A) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int e = g * 4 + i;
-          const float d = zp[e] - zq[e];
-          ep[i] = exp2_hw(fmaf(zp[e], kLog2e, -rp));
-          eq[i] = exp2_hw(fmaf(zq[e], kLog2e, -rq));
-          kt[i] = ep[i] > 0.f ? ep[i] * d : 0.f;
-          zp[e] = ep[i];
-          zq[e] = eq[i];
+          const bool in = in_v(e);
+          const float zp = cur.gp(e), zq = cur.gq(e);
+          ep[i] = in ? exp2_hw(fmaf(zp, kLog2e, -rp)) : 0.f;
+          eq[i] = in ? exp2_hw(fmaf(zq, kLog2e, -rq)) : 0.f;
+          kt[i] = ep[i] > 0.f ? ep[i] * (zp - zq) : 0.f;
+          if constexpr (!BF16) {
+            cur.p[e] = ep[i];
+            cur.q[e] = eq[i];
+          }
         }
         gp[g] = (ep[0] + ep[1]) + (ep[2] + ep[3]);
         gq[g] = (eq[0] + eq[1]) + (eq[2] + eq[3]);
         gk[g] = (kt[0] + kt[1]) + (kt[2] + kt[3]);
+        __builtin_amdgcn_sched_barrier(0);  // bounds live ranges: one group at a time
       }
       dsp = wave_sum_d((double)tree_sum(gp));
       dsq = wave_sum_d((double)tree_sum(gq));
@@ -328,8 +422,8 @@ accept_sweep_kernel(Args A) {
         float ep[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          ep[i] = exp2_hw(fmaf(zp[g * 4 + i], kLog2e, -rp));
-          zp[g * 4 + i] = ep[i];
+          const float zp = cur.gp(g * 4 + i);
+          ep[i] = in_v(g * 4 + i) ? exp2_hw(fmaf(zp, kLog2e, -rp)) : 0.f;
         }
         gp[g] = (ep[0] + ep[1]) + (ep[2] + ep[3]);
       }
@@ -342,8 +436,8 @@ accept_sweep_kernel(Args A) {
     }
     __syncthreads();
 
-    // ---- publish the chunk record; pair rows then wait for the whole row
-    const size_t rec = (size_t)row * nc + c;
+    // ---- publish the chunk record
+    const size_t rec = (size_t)t.row * nc + t.c;
     if (tid == 0) {
       StatRec r;
       r.mp = cmp;
@@ -356,66 +450,83 @@ accept_sweep_kernel(Args A) {
       __builtin_amdgcn_raw_buffer_store_b128(w0, rs_stats, (uint32_t)(rec * kRecBytes), 0, kDeviceCoherent);
       __builtin_amdgcn_raw_buffer_store_b128(w1, rs_stats, (uint32_t)(rec * kRecBytes + 16), 0, kDeviceCoherent);
     }
-    // Workgroup-uniform. The LDS slots are rewritten only after two more
-    // barriers, when every wave has read them.
-    if (!pair) continue;
 
-    if (w == 0) {
-      // ---- wait until every chunk record of the row is present, then merge
-      float m1[kSlots], m2[kSlots];
-      double s1[kSlots], s2[kSlots];
-      for (uint32_t it = 0;; ++it) {
-        bool ok = true;
+    if (t.pair) {  // workgroup-uniform
+      if (w == 0) {
+        // ---- wait until every chunk record of the row is present, then merge
+        float m1[kSlots], m2[kSlots];
+        double s1[kSlots], s2[kSlots];
+        for (uint32_t it = 0;; ++it) {
+          bool ok = true;
 #pragma unroll
-        for (int i = 0; i < kSlots; ++i) {
-          const int cc = lane * nslot + i;
-          const bool in = i < nslot && cc < nc;
-          const uint32_t off = (uint32_t)(((size_t)row * nc + (in ? cc : 0)) * kRecBytes);
-          const u32x4 w0 = __builtin_amdgcn_raw_buffer_load_b128(rs_stats, off, 0, kDeviceCoherent);
-          const u32x4 w1 = __builtin_amdgcn_raw_buffer_load_b128(rs_stats, off + 16, 0, kDeviceCoherent);
-          ok = ok && (!in || rec_present(w0, w1));
-          const StatRec r = unpack_rec(w0, w1);
-          m1[i] = in ? r.mp : kNegInf;
-          m2[i] = in ? r.mq : kNegInf;
-          s1[i] = in ? r.sp : 0.0;
-          s2[i] = in ? r.sq : 0.0;
+          for (int i = 0; i < kSlots; ++i) {
+            const int cc = lane * nslot + i;
+            const bool in = i < nslot && cc < nc;
+            const uint32_t off = (uint32_t)(((size_t)t.row * nc + (in ? cc : 0)) * kRecBytes);
+            const u32x4 w0 = __builtin_amdgcn_raw_buffer_load_b128(rs_stats, off, 0, kDeviceCoherent);
+            const u32x4 w1 = __builtin_amdgcn_raw_buffer_load_b128(rs_stats, off + 16, 0, kDeviceCoherent);
+            ok = ok && (!in || rec_present(w0, w1));
+            const StatRec r = unpack_rec(w0, w1);
+            m1[i] = in ? r.mp : kNegInf;
+            m2[i] = in ? r.mq : kNegInf;
+            s1[i] = in ? r.sp : 0.0;
+            s2[i] = in ? r.sq : 0.0;
+          }
+          if (__ballot(!ok) == 0ull) break;
+          if (it == kSpinLimit) {
+            if (lane == 0 && A.status) atomicOr(A.status, SR_ST_TIMEOUT);
+            break;
+          }
+          __builtin_amdgcn_s_sleep(2);
         }
-        if (__ballot(!ok) == 0ull) break;
-        if (it == kSpinLimit) {
-          if (lane == 0 && A.status) atomicOr(A.status, SR_ST_TIMEOUT);
-          break;
+        const RowNorm np = row_norm(m1, s1);
+        const RowNorm nq = row_norm(m2, s2);
+        if (lane == 0) {
+          s_f[0] = np.factor(cmp);
+          s_f[1] = nq.factor(cmq);
         }
-        __builtin_amdgcn_s_sleep(2);
       }
-      const double Lp = merge_lse(m1, s1);
-      const double Lq = merge_lse(m2, s2);
-      if (lane == 0) {
-        s_L[0] = Lp;
-        s_L[1] = Lq;
-      }
-    }
-    __syncthreads();
+      __syncthreads();
 
-    // ---- second pass over the registers: sum |P - Q|
-    const double Lp = s_L[0], Lq = s_L[1];
-    const float fp = cmp == kNegInf ? 0.f : (float)exp((double)cmp - Lp);
-    const float fq = cmq == kNegInf ? 0.f : (float)exp((double)cmq - Lq);
-    float ga[E / 4];
-    {
-      // separately rounded products: identical p and q rows give exactly zero
-#pragma clang fp contract(off)
+      // ---- second pass: sum |P - Q| over this lane's entries
+      const float fp = s_f[0], fq = s_f[1];
+      float ga[E / 4];
 #pragma unroll
       for (int g = 0; g < E / 4; ++g) {
         float a[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) a[i] = fabsf(zp[g * 4 + i] * fp - zq[g * 4 + i] * fq);
+        for (int i = 0; i < 4; ++i) {
+          const int e = g * 4 + i;
+          float ep, eq;
+          if constexpr (BF16) {
+            const bool in = in_v(e);
+            const float zp = cur.gp(e), zq = cur.gq(e);
+            ep = in ? exp2_hw(fmaf(zp, kLog2e, -rp)) : 0.f;
+            eq = in ? exp2_hw(fmaf(zq, kLog2e, -rq)) : 0.f;
+          } else {
+            ep = cur.p[e];
+            eq = cur.q[e];
+          }
+          {
+            // separately rounded products: identical p and q rows give exactly zero
+#pragma clang fp contract(off)
+            a[i] = fabsf(ep * fp - eq * fq);
+          }
+        }
         ga[g] = (a[0] + a[1]) + (a[2] + a[3]);
+        __builtin_amdgcn_sched_barrier(0);
       }
+      const double dtv = wave_sum_d((double)tree_sum(ga));
+      if (lane == 0) s_s[0][w] = dtv;
+      __syncthreads();
+      if (tid == 0) A.tvabs[rec] = ((s_s[0][0] + s_s[0][1]) + s_s[0][2]) + s_s[0][3];
     }
-    const double dtv = wave_sum_d((double)tree_sum(ga));
-    if (lane == 0) s_s[0][w] = dtv;
-    __syncthreads();
-    if (tid == 0) A.tvabs[rec] = ((s_s[0][0] + s_s[0][1]) + s_s[0][2]) + s_s[0][3];
+    // The LDS slots of the next task are written only after its first
+    // barrier, which every wave reaches after finishing with this task's.
+    if (!more) break;
+    task = task_n;
+    t = tn;
+    cur = nxt;
   }
 }
 
@@ -503,14 +614,15 @@ __device__ int draw_token(const Args& A, int b, int k, int gam) {
   const bool pair = k < gam;
   RowRecs R;
   load_row(A, b * G1 + k, pair, R);
-  const double Lp = merge_lse(R.mp, R.sp);
-  const double Lq = pair ? merge_lse(R.mq, R.sq) : 0.0;
+  const RowNorm np = row_norm(R.mp, R.sp);
+  const RowNorm nq = row_norm(R.mq, R.sq);
   double pm[kSlots], rm[kSlots];
   double my_res = 0.0;
 #pragma unroll
   for (int i = 0; i < kSlots; ++i) {
-    pm[i] = R.mp[i] == kNegInf ? 0.0 : R.sp[i] * exp((double)R.mp[i] - Lp);
-    const double qm = R.mq[i] == kNegInf ? 0.0 : R.sq[i] * exp((double)R.mq[i] - Lq);
+    // chunk masses with the same factors the sweep's sum |P - Q| used
+    pm[i] = R.sp[i] * (double)np.factor(R.mp[i]);
+    const double qm = R.sq[i] * (double)nq.factor(R.mq[i]);
     rm[i] = pair ? fmax(0.0, 0.5 * (R.ta[i] + pm[i] - qm)) : 0.0;
     my_res += rm[i];
   }
@@ -570,8 +682,8 @@ __device__ int draw_token(const Args& A, int b, int k, int gam) {
   cmq = wave_max(cmq);
   const float rp = cmp == kNegInf ? 0.f : cmp * kLog2e;
   const float rq = cmq == kNegInf ? 0.f : cmq * kLog2e;
-  const float fp = cmp == kNegInf ? 0.f : (float)exp((double)cmp - Lp);
-  const float fq = cmq == kNegInf ? 0.f : (float)exp((double)cmq - Lq);
+  const float fp = np.factor(cmp);
+  const float fq = nq.factor(cmq);
   const size_t esz = BF16 ? 2 : 4;
   const char* prow = (const char*)A.p + ((size_t)b * A.p_stride + (size_t)k * A.V) * esz;
   const char* qrow = (const char*)A.q + ((size_t)b * A.q_stride + (size_t)k * A.V) * esz;
@@ -671,13 +783,14 @@ accept_finish_kernel(Args A) {
   for (int j = w; j < gam; j += nw) {
     RowRecs R;
     load_row(A, b * G1 + j, true, R);
-    const double Lp = merge_lse(R.mp, R.sp);
-    const double Lq = merge_lse(R.mq, R.sq);
+    const RowNorm np = row_norm(R.mp, R.sp);
+    const RowNorm nq = row_norm(R.mq, R.sq);
+    const double Lp = np.log_norm(), Lq = nq.log_norm();
     double tvd = 0.0, kld = 0.0;
 #pragma unroll
     for (int i = 0; i < kSlots; ++i) {
       tvd += R.ta[i];
-      if (R.mp[i] != kNegInf) kld += R.kl[i] * exp((double)R.mp[i] - Lp);
+      kld += R.kl[i] * (double)np.factor(R.mp[i]);
     }
     tvd = 0.5 * wave_sum_d(tvd);
     kld = wave_sum_d(kld) - (Lp - Lq);
@@ -771,7 +884,7 @@ int accept_plan(int B, int gamma_max, int V, int dtype, AcceptPlan* plan) {
   if (cus <= 0) return SR_ELAUNCH;
   int per_cu = 1;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, bf16 ? sweep_fn<true>() : sweep_fn<false>(),
-                                                   kThreads, 0) != hipSuccess || per_cu < 1)
+                                                   kThreads, Bl * sizeof(int)) != hipSuccess || per_cu < 1)
     per_cu = 1;
   const long cap = (long)cus * per_cu;
   long grid = cap / plan->n_chunks * plan->n_chunks;
@@ -822,9 +935,11 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
     A.tvabs = (double*)(ws + L.tvabs) + (size_t)b0 * G1 * plan.n_chunks;
     A.status = status;
     if (dtype == SR_BF16)
-      hipLaunchKernelGGL((accept_sweep_kernel<true, kEbf16>), dim3(plan.grid), dim3(kThreads), 0, stream, A);
+      hipLaunchKernelGGL((accept_sweep_kernel<true, kEbf16>), dim3(plan.grid), dim3(kThreads), Bl * sizeof(int),
+                         stream, A);
     else
-      hipLaunchKernelGGL((accept_sweep_kernel<false, kEf32>), dim3(plan.grid), dim3(kThreads), 0, stream, A);
+      hipLaunchKernelGGL((accept_sweep_kernel<false, kEf32>), dim3(plan.grid), dim3(kThreads), Bl * sizeof(int),
+                         stream, A);
     if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
     if (dtype == SR_BF16)
       hipLaunchKernelGGL((accept_finish_kernel<true, kEbf16>), dim3(Bl), dim3(64 * nw), 0, stream, A);
