@@ -343,33 +343,20 @@ accept_sweep_kernel(Args A) {
 
   build_row_table(A.gamma, A.gmax, A.B, s_rows);
   const long n_tasks = (long)s_rows[A.B - 1] * nc;
-  long task = blockIdx.x;
-  if (task >= n_tasks) return;
-  TaskInfo t = decode_task<BF16>(A, s_rows, task);
-  Raw<BF16, E> cur;
-  issue_loads<BF16, E>(A, t, cur);
 
-  for (;;) {
-    // ---- prefetch the next task (the current one again past the end)
-    const long task_n = task + gridDim.x;
-    const bool more = task_n < n_tasks;
-    const TaskInfo tn = decode_task<BF16>(A, s_rows, more ? task_n : task);
-    Raw<BF16, E> nxt;
-    __builtin_amdgcn_sched_barrier(0);
-    issue_loads<BF16, E>(A, tn, nxt);
-    __builtin_amdgcn_sched_barrier(0);
-
+  // First pass over a task's entries: chunk maxima, exponentials, sums, KL
+  // numerator, and the published record. Leaves the chunk maxima in cmp/cmq
+  // (and, for fp32, the exponentials in r).
+  auto first_pass = [&](const TaskInfo& t, Raw<BF16, E>& r, float& cmp, float& cmq) __attribute__((always_inline)) {
     const int base = t.c * kChunk + w * (64 * E);
     auto in_v = [&](int e) __attribute__((always_inline)) {  // entry e lies below V
       return base + ((e / VEC) * 64 + lane) * VEC < A.V;
     };
-
-    // ---- chunk maxima
     float mp = kNegInf, mq = kNegInf;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       const bool in = in_v(e);
-      const float zp = cur.gp(e), zq = cur.gq(e);  // unconditional: then a select
+      const float zp = r.gp(e), zq = r.gq(e);  // unconditional: then a select
       mp = fmaxf(mp, in ? zp : kNegInf);
       mq = fmaxf(mq, in && t.pair ? zq : kNegInf);
       if (e % 8 == 7) __builtin_amdgcn_sched_barrier(0);  // unpack eight entries at a time
@@ -381,11 +368,11 @@ accept_sweep_kernel(Args A) {
       s_m[1][w] = mq;
     }
     __syncthreads();
-    const float cmp = fmaxf(fmaxf(s_m[0][0], s_m[0][1]), fmaxf(s_m[0][2], s_m[0][3]));
-    const float cmq = fmaxf(fmaxf(s_m[1][0], s_m[1][1]), fmaxf(s_m[1][2], s_m[1][3]));
+    cmp = fmaxf(fmaxf(s_m[0][0], s_m[0][1]), fmaxf(s_m[0][2], s_m[0][3]));
+    cmq = fmaxf(fmaxf(s_m[1][0], s_m[1][1]), fmaxf(s_m[1][2], s_m[1][3]));
 
-    // ---- exponentials, sums, KL numerator. Groups of four are summed as
-    // (a0 + a1) + (a2 + a3), then a tree over groups.
+    // exponentials, sums, KL numerator; groups of four are summed as
+    // (a0 + a1) + (a2 + a3), then a tree over groups
     const float rp = cmp == kNegInf ? 0.f : cmp * kLog2e;
     const float rq = cmq == kNegInf ? 0.f : cmq * kLog2e;
     double dsp, dsq = 0.0, dkl = 0.0;
@@ -398,13 +385,13 @@ accept_sweep_kernel(Args A) {
         for (int i = 0; i < 4; ++i) {
           const int e = g * 4 + i;
           const bool in = in_v(e);
-          const float zp = cur.gp(e), zq = cur.gq(e);
+          const float zp = r.gp(e), zq = r.gq(e);
           ep[i] = in ? exp2_hw(fmaf(zp, kLog2e, -rp)) : 0.f;
           eq[i] = in ? exp2_hw(fmaf(zq, kLog2e, -rq)) : 0.f;
           kt[i] = ep[i] > 0.f ? ep[i] * (zp - zq) : 0.f;
           if constexpr (!BF16) {
-            cur.p[e] = ep[i];
-            cur.q[e] = eq[i];
+            r.p[e] = ep[i];
+            r.q[e] = eq[i];
           }
         }
         gp[g] = (ep[0] + ep[1]) + (ep[2] + ep[3]);
@@ -422,7 +409,7 @@ accept_sweep_kernel(Args A) {
         float ep[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float zp = cur.gp(g * 4 + i);
+          const float zp = r.gp(g * 4 + i);
           ep[i] = in_v(g * 4 + i) ? exp2_hw(fmaf(zp, kLog2e, -rp)) : 0.f;
         }
         gp[g] = (ep[0] + ep[1]) + (ep[2] + ep[3]);
@@ -435,98 +422,122 @@ accept_sweep_kernel(Args A) {
       s_s[2][w] = dkl;
     }
     __syncthreads();
-
-    // ---- publish the chunk record
-    const size_t rec = (size_t)t.row * nc + t.c;
     if (tid == 0) {
-      StatRec r;
-      r.mp = cmp;
-      r.mq = cmq;
-      r.sp = ((s_s[0][0] + s_s[0][1]) + s_s[0][2]) + s_s[0][3];
-      r.sq = ((s_s[1][0] + s_s[1][1]) + s_s[1][2]) + s_s[1][3];
-      r.kl = ((s_s[2][0] + s_s[2][1]) + s_s[2][2]) + s_s[2][3];
+      const size_t rec = (size_t)t.row * nc + t.c;
+      StatRec sr;
+      sr.mp = cmp;
+      sr.mq = cmq;
+      sr.sp = ((s_s[0][0] + s_s[0][1]) + s_s[0][2]) + s_s[0][3];
+      sr.sq = ((s_s[1][0] + s_s[1][1]) + s_s[1][2]) + s_s[1][3];
+      sr.kl = ((s_s[2][0] + s_s[2][1]) + s_s[2][2]) + s_s[2][3];
       u32x4 w0, w1;
-      pack_rec(r, w0, w1);
+      pack_rec(sr, w0, w1);
       __builtin_amdgcn_raw_buffer_store_b128(w0, rs_stats, (uint32_t)(rec * kRecBytes), 0, kDeviceCoherent);
       __builtin_amdgcn_raw_buffer_store_b128(w1, rs_stats, (uint32_t)(rec * kRecBytes + 16), 0, kDeviceCoherent);
     }
+  };
 
-    if (t.pair) {  // workgroup-uniform
-      if (w == 0) {
-        // ---- wait until every chunk record of the row is present, then merge
-        float m1[kSlots], m2[kSlots];
-        double s1[kSlots], s2[kSlots];
-        for (uint32_t it = 0;; ++it) {
-          bool ok = true;
+  // Second pass of a pair row's task: wait for every chunk record of the row,
+  // then sum |P - Q| over the entries kept from the first pass.
+  auto second_pass = [&](const TaskInfo& t, const Raw<BF16, E>& r, float cmp, float cmq) __attribute__((always_inline)) {
+    if (w == 0) {
+      float m1[kSlots], m2[kSlots];
+      double s1[kSlots], s2[kSlots];
+      for (uint32_t it = 0;; ++it) {
+        bool ok = true;
 #pragma unroll
-          for (int i = 0; i < kSlots; ++i) {
-            const int cc = lane * nslot + i;
-            const bool in = i < nslot && cc < nc;
-            const uint32_t off = (uint32_t)(((size_t)t.row * nc + (in ? cc : 0)) * kRecBytes);
-            const u32x4 w0 = __builtin_amdgcn_raw_buffer_load_b128(rs_stats, off, 0, kDeviceCoherent);
-            const u32x4 w1 = __builtin_amdgcn_raw_buffer_load_b128(rs_stats, off + 16, 0, kDeviceCoherent);
-            ok = ok && (!in || rec_present(w0, w1));
-            const StatRec r = unpack_rec(w0, w1);
-            m1[i] = in ? r.mp : kNegInf;
-            m2[i] = in ? r.mq : kNegInf;
-            s1[i] = in ? r.sp : 0.0;
-            s2[i] = in ? r.sq : 0.0;
-          }
-          if (__ballot(!ok) == 0ull) break;
-          if (it == kSpinLimit) {
-            if (lane == 0 && A.status) atomicOr(A.status, SR_ST_TIMEOUT);
-            break;
-          }
-          __builtin_amdgcn_s_sleep(2);
+        for (int i = 0; i < kSlots; ++i) {
+          const int cc = lane * nslot + i;
+          const bool in = i < nslot && cc < nc;
+          const uint32_t off = (uint32_t)(((size_t)t.row * nc + (in ? cc : 0)) * kRecBytes);
+          const u32x4 w0 = __builtin_amdgcn_raw_buffer_load_b128(rs_stats, off, 0, kDeviceCoherent);
+          const u32x4 w1 = __builtin_amdgcn_raw_buffer_load_b128(rs_stats, off + 16, 0, kDeviceCoherent);
+          ok = ok && (!in || rec_present(w0, w1));
+          const StatRec sr = unpack_rec(w0, w1);
+          m1[i] = in ? sr.mp : kNegInf;
+          m2[i] = in ? sr.mq : kNegInf;
+          s1[i] = in ? sr.sp : 0.0;
+          s2[i] = in ? sr.sq : 0.0;
         }
-        const RowNorm np = row_norm(m1, s1);
-        const RowNorm nq = row_norm(m2, s2);
-        if (lane == 0) {
-          s_f[0] = np.factor(cmp);
-          s_f[1] = nq.factor(cmq);
+        if (__ballot(!ok) == 0ull) break;
+        if (it == kSpinLimit) {
+          if (lane == 0 && A.status) atomicOr(A.status, SR_ST_TIMEOUT);
+          break;
         }
+        __builtin_amdgcn_s_sleep(2);
       }
-      __syncthreads();
-
-      // ---- second pass: sum |P - Q| over this lane's entries
-      const float fp = s_f[0], fq = s_f[1];
-      float ga[E / 4];
-#pragma unroll
-      for (int g = 0; g < E / 4; ++g) {
-        float a[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int e = g * 4 + i;
-          float ep, eq;
-          if constexpr (BF16) {
-            const bool in = in_v(e);
-            const float zp = cur.gp(e), zq = cur.gq(e);
-            ep = in ? exp2_hw(fmaf(zp, kLog2e, -rp)) : 0.f;
-            eq = in ? exp2_hw(fmaf(zq, kLog2e, -rq)) : 0.f;
-          } else {
-            ep = cur.p[e];
-            eq = cur.q[e];
-          }
-          {
-            // separately rounded products: identical p and q rows give exactly zero
-#pragma clang fp contract(off)
-            a[i] = fabsf(ep * fp - eq * fq);
-          }
-        }
-        ga[g] = (a[0] + a[1]) + (a[2] + a[3]);
-        __builtin_amdgcn_sched_barrier(0);
+      const RowNorm np = row_norm(m1, s1);
+      const RowNorm nq = row_norm(m2, s2);
+      if (lane == 0) {
+        s_f[0] = np.factor(cmp);
+        s_f[1] = nq.factor(cmq);
       }
-      const double dtv = wave_sum_d((double)tree_sum(ga));
-      if (lane == 0) s_s[0][w] = dtv;
-      __syncthreads();
-      if (tid == 0) A.tvabs[rec] = ((s_s[0][0] + s_s[0][1]) + s_s[0][2]) + s_s[0][3];
     }
-    // The LDS slots of the next task are written only after its first
-    // barrier, which every wave reaches after finishing with this task's.
+    __syncthreads();
+    const float fp = s_f[0], fq = s_f[1];
+    const float rp = cmp == kNegInf ? 0.f : cmp * kLog2e;
+    const float rq = cmq == kNegInf ? 0.f : cmq * kLog2e;
+    const int base = t.c * kChunk + w * (64 * E);
+    float ga[E / 4];
+#pragma unroll
+    for (int g = 0; g < E / 4; ++g) {
+      float a[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int e = g * 4 + i;
+        float ep, eq;
+        if constexpr (BF16) {
+          const bool in = base + ((e / VEC) * 64 + lane) * VEC < A.V;
+          const float zp = r.gp(e), zq = r.gq(e);
+          ep = in ? exp2_hw(fmaf(zp, kLog2e, -rp)) : 0.f;
+          eq = in ? exp2_hw(fmaf(zq, kLog2e, -rq)) : 0.f;
+        } else {
+          ep = r.p[e];
+          eq = r.q[e];
+        }
+        {
+          // separately rounded products: identical p and q rows give exactly zero
+#pragma clang fp contract(off)
+          a[i] = fabsf(ep * fp - eq * fq);
+        }
+      }
+      ga[g] = (a[0] + a[1]) + (a[2] + a[3]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    const double dtv = wave_sum_d((double)tree_sum(ga));
+    if (lane == 0) s_s[0][w] = dtv;
+    __syncthreads();
+    if (tid == 0) A.tvabs[(size_t)t.row * nc + t.c] = ((s_s[0][0] + s_s[0][1]) + s_s[0][2]) + s_s[0][3];
+  };
+
+  // Pipeline: the second pass of task i runs after the loads of task i+1 are
+  // issued and before its first pass, so the other chunks of task i's row have
+  // had a whole first pass to publish. Every LDS slot is rewritten only after a
+  // barrier that follows its last read.
+  long task = blockIdx.x;
+  if (task >= n_tasks) return;
+  TaskInfo t = decode_task<BF16>(A, s_rows, task);
+  Raw<BF16, E> cur;
+  issue_loads<BF16, E>(A, t, cur);
+  float cmp, cmq;
+  first_pass(t, cur, cmp, cmq);
+  for (;;) {
+    const long task_n = task + gridDim.x;
+    const bool more = task_n < n_tasks;
+    const TaskInfo tn = decode_task<BF16>(A, s_rows, more ? task_n : task);  // past the end: reload (cached)
+    Raw<BF16, E> nxt;
+    __builtin_amdgcn_sched_barrier(0);
+    issue_loads<BF16, E>(A, tn, nxt);
+    __builtin_amdgcn_sched_barrier(0);
+    if (t.pair) second_pass(t, cur, cmp, cmq);  // workgroup-uniform
     if (!more) break;
+    float cmp_n, cmq_n;
+    first_pass(tn, nxt, cmp_n, cmq_n);
     task = task_n;
     t = tn;
     cur = nxt;
+    cmp = cmp_n;
+    cmq = cmq_n;
   }
 }
 
@@ -600,161 +611,30 @@ __device__ __forceinline__ void load_row(const Args& A, int row, bool pair, RowR
   }
 }
 
-// Draw the token of stopping row k by CDF inversion in ascending vocabulary
-// order (one whole wave).
-template <bool BF16, int E>
-__device__ int draw_token(const Args& A, int b, int k, int gam) {
-  typedef Elt<BF16> L;
-  constexpr int VEC = L::VEC;
-  constexpr int kChunk = kThreads * E;
-  constexpr int kPer = 32;  // entries per lane per 2048-entry block of the chunk
-  const int lane = threadIdx.x & 63;
-  const int nslot = (A.nc + 63) / 64;
-  const int G1 = A.gmax + 1;
-  const bool pair = k < gam;
-  RowRecs R;
-  load_row(A, b * G1 + k, pair, R);
-  const RowNorm np = row_norm(R.mp, R.sp);
-  const RowNorm nq = row_norm(R.mq, R.sq);
-  double pm[kSlots], rm[kSlots];
-  double my_res = 0.0;
-#pragma unroll
-  for (int i = 0; i < kSlots; ++i) {
-    // chunk masses with the same factors the sweep's sum |P - Q| used
-    pm[i] = R.sp[i] * (double)np.factor(R.mp[i]);
-    const double qm = R.sq[i] * (double)nq.factor(R.mq[i]);
-    rm[i] = pair ? fmax(0.0, 0.5 * (R.ta[i] + pm[i] - qm)) : 0.0;
-    my_res += rm[i];
-  }
-  const bool residual = pair && wave_sum_d(my_res) > 0.0;
-  double mass[kSlots];
-  double my = 0.0;
-  int my_last = -1;
-#pragma unroll
-  for (int i = 0; i < kSlots; ++i) {
-    mass[i] = residual ? rm[i] : pm[i];
-    my += mass[i];
-    if (mass[i] > 0.0) my_last = lane * nslot + i;
-  }
-  const double incl = wave_incl_scan(my);
-  const double W = __shfl(incl, 63, 64);
-  const double target = (double)A.u_res[(size_t)b * G1 + k] * W;
-  // the chunk holding the target: the first with positive mass whose end exceeds it
-  int cs = -1;
-  double pre = 0.0;
-  const unsigned long long hit = __ballot(incl > target && my > 0.0);
-  if (hit) {
-    const int hl = __ffsll((long long)hit) - 1;
-    double run = incl - my;
-    int found = -1;
-    double fpre = 0.0;
-#pragma unroll
-    for (int i = 0; i < kSlots; ++i) {
-      if (found < 0 && mass[i] > 0.0 && run + mass[i] > target) {
-        found = lane * nslot + i;
-        fpre = run;
-      }
-      run += mass[i];
-    }
-    cs = __shfl(found, hl, 64);
-    pre = __shfl(fpre, hl, 64);
-  }
-  if (cs < 0) {  // rounding put the target at the very end: the last chunk with mass
-    int last = my_last;
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) last = max(last, __shfl_xor(last, off, 64));
-    cs = max(last, 0);
-    double before = 0.0;
-#pragma unroll
-    for (int i = 0; i < kSlots; ++i)
-      if (lane * nslot + i < cs) before += mass[i];
-    pre = wave_sum_d(before);
-  }
-  // the chunk's maxima, exactly as the sweep used them
-  float cmp = kNegInf, cmq = kNegInf;
-#pragma unroll
-  for (int i = 0; i < kSlots; ++i)
-    if (lane * nslot + i == cs) {
-      cmp = R.mp[i];
-      cmq = R.mq[i];
-    }
-  cmp = wave_max(cmp);
-  cmq = wave_max(cmq);
-  const float rp = cmp == kNegInf ? 0.f : cmp * kLog2e;
-  const float rq = cmq == kNegInf ? 0.f : cmq * kLog2e;
-  const float fp = np.factor(cmp);
-  const float fq = nq.factor(cmq);
-  const size_t esz = BF16 ? 2 : 4;
-  const char* prow = (const char*)A.p + ((size_t)b * A.p_stride + (size_t)k * A.V) * esz;
-  const char* qrow = (const char*)A.q + ((size_t)b * A.q_stride + (size_t)k * A.V) * esz;
-  double rem = target - pre;
-  int tok = -1, last_tok = -1;
-  for (int blk = 0; blk < kChunk / (64 * kPer) && tok < 0; ++blk) {
-    const int x0 = cs * kChunk + blk * 64 * kPer + lane * kPer;
-    float wt[kPer];
-    double sum = 0.0;
-    int mine = -1;
-#pragma unroll
-    for (int v = 0; v < kPer / VEC; ++v) {
-      const int x = x0 + v * VEC;
-      const int xl = min(x, A.V - VEC);
-      float zp[VEC], zq[VEC];
-      L::load(prow, xl, zp);
-      if (residual) L::load(qrow, xl, zq);
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) {
-        float wv = 0.f;
-        if (x < A.V) {
-#pragma clang fp contract(off)
-          const float ep = exp2_hw(fmaf(zp[e], kLog2e, -rp));
-          if (residual) {
-            const float eq = exp2_hw(fmaf(zq[e], kLog2e, -rq));
-            wv = fmaxf(ep * fp - eq * fq, 0.f);
-          } else {
-            wv = ep * fp;
-          }
-        }
-        wt[v * VEC + e] = wv;
-        sum += (double)wv;
-        if (wv > 0.f) mine = x + e;
-      }
-    }
-    int lmax = mine;
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) lmax = max(lmax, __shfl_xor(lmax, off, 64));
-    if (lmax >= 0) last_tok = lmax;
-    const double inc = wave_incl_scan(sum);
-    const double total = __shfl(inc, 63, 64);
-    if (rem < total) {
-      const unsigned long long h = __ballot(inc > rem);
-      const int hl = __ffsll((long long)h) - 1;
-      int found = -1;
-      if (lane == hl) {
-        double run = inc - sum;
-#pragma unroll
-        for (int e = 0; e < kPer; ++e) {
-          run += (double)wt[e];
-          if (found < 0 && wt[e] > 0.f && run > rem) found = x0 + e;
-        }
-        if (found < 0) found = mine;
-      }
-      tok = __shfl(found, hl, 64);
-    } else {
-      rem -= total;
-    }
-  }
-  if (tok < 0) tok = last_tok < 0 ? 0 : last_tok;
-  return tok;
-}
-
+// Finish kernel: one workgroup per sequence with at least four waves.
+//   rows:  one wave per pair row j merges the row's records (the draft
+//          token's two logits are loaded alongside) into a_j, p(x), q(x),
+//          TV_j and KL_j;
+//   chain: wave 0 finds the stopping row k and, from k's chunk masses, the
+//          chunk that holds u*W and the offset of u*W inside it;
+//   draw:  waves 0-3 re-read that chunk (each thread a contiguous run of
+//          entries), weigh it exactly as the sweep did, and a block-wide
+//          prefix scan in ascending vocabulary order finds the token.
 template <bool BF16, int E>
 __global__ void __launch_bounds__(1024)
 accept_finish_kernel(Args A) {
+  constexpr int VEC = Elt<BF16>::VEC;
+  constexpr int kChunk = kThreads * E;
+  constexpr int kPerT = kChunk / 256;  // entries per thread in the draw
   __shared__ RowRes rr[kMaxRows];
   __shared__ uint32_t s_bad;
+  __shared__ int s_k, s_cs, s_resid, s_hit[4], s_last[4], s_tok;
+  __shared__ double s_rem, s_wt[4];
+  __shared__ float s_fac[4];  // rp, rq, fp, fq of the draw chunk
   const int b = blockIdx.x;
-  const int lane = threadIdx.x & 63;
-  const int w = threadIdx.x >> 6;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = tid >> 6;
   const int nw = blockDim.x >> 6;
   const int G1 = A.gmax + 1;
   const int gam = A.gamma[b];
@@ -762,11 +642,11 @@ accept_finish_kernel(Args A) {
     if (w == 0) write_invalid(A, b, SR_ST_GAMMA);
     return;  // the sweep touched no row of this sequence
   }
-  if (threadIdx.x == 0) s_bad = 0;
+  if (tid == 0) s_bad = 0;
   __syncthreads();
   // ---- data checks
   uint32_t bad = 0;
-  for (int j = threadIdx.x; j <= gam; j += blockDim.x) {
+  for (int j = tid; j <= gam; j += blockDim.x) {
     if (j < gam) {
       const int x = A.drafts[(size_t)b * A.gmax + j];
       if (x < 0 || x >= A.V) bad |= SR_ST_TOKEN;
@@ -776,11 +656,18 @@ accept_finish_kernel(Args A) {
     const float u = A.u_res[(size_t)b * G1 + j];
     if (!(u >= 0.f && u < 1.f)) bad |= SR_ST_UNIFORM;
   }
-  if (threadIdx.x == 0 && A.kv_len && A.kv_len[b] < gam + 1) bad |= SR_ST_KVLEN;
+  if (tid == 0 && A.kv_len && A.kv_len[b] < gam + 1) bad |= SR_ST_KVLEN;
   if (bad) atomicOr(&s_bad, bad);
-  // ---- per-row results (one wave per row)
+  // ---- per-row results (one wave per pair row)
   const size_t esz = BF16 ? 2 : 4;
   for (int j = w; j < gam; j += nw) {
+    const int x = A.drafts[(size_t)b * A.gmax + j];
+    const bool xin = x >= 0 && x < A.V;
+    float zpx = 0.f, zqx = 0.f;
+    if (lane == 0 && xin) {  // issued with the record loads below
+      zpx = Elt<BF16>::one((const char*)A.p + ((size_t)b * A.p_stride + (size_t)j * A.V) * esz, x);
+      zqx = Elt<BF16>::one((const char*)A.q + ((size_t)b * A.q_stride + (size_t)j * A.V) * esz, x);
+    }
     RowRecs R;
     load_row(A, b * G1 + j, true, R);
     const RowNorm np = row_norm(R.mp, R.sp);
@@ -796,12 +683,9 @@ accept_finish_kernel(Args A) {
     kld = wave_sum_d(kld) - (Lp - Lq);
     if (lane == 0) {
       double a = __builtin_nan(""), pt = __builtin_nan(""), qt = __builtin_nan("");
-      const int x = A.drafts[(size_t)b * A.gmax + j];
-      if (x >= 0 && x < A.V) {
-        const char* prow = (const char*)A.p + ((size_t)b * A.p_stride + (size_t)j * A.V) * esz;
-        const char* qrow = (const char*)A.q + ((size_t)b * A.q_stride + (size_t)j * A.V) * esz;
-        const double lpx = (double)Elt<BF16>::one(prow, x) - Lp;
-        const double lqx = (double)Elt<BF16>::one(qrow, x) - Lq;
+      if (xin) {
+        const double lpx = (double)zpx - Lp;
+        const double lqx = (double)zqx - Lq;
         pt = exp(lpx);
         qt = exp(lqx);
         a = (lqx == -INFINITY || lpx >= lqx) ? 1.0 : exp(lpx - lqx);
@@ -817,13 +701,171 @@ accept_finish_kernel(Args A) {
     }
     return;
   }
+  // ---- accept chain and the chunk of the draw (wave 0)
+  if (w == 0) {
+    bool rej = false;
+    if (lane < gam) rej = !((double)A.u_acc[(size_t)b * A.gmax + lane] < rr[lane].a);
+    const unsigned long long rmask = __ballot(rej);
+    const int k = rmask ? (__ffsll((long long)rmask) - 1) : gam;
+    const bool pair = k < gam;
+    const int nslot = (A.nc + 63) / 64;
+    RowRecs R;
+    load_row(A, b * G1 + k, pair, R);
+    const RowNorm np = row_norm(R.mp, R.sp);
+    const RowNorm nq = row_norm(R.mq, R.sq);
+    double pm[kSlots], rm[kSlots];
+    double my_res = 0.0;
+#pragma unroll
+    for (int i = 0; i < kSlots; ++i) {
+      // chunk masses with the same factors the sweep's sum |P - Q| used
+      pm[i] = R.sp[i] * (double)np.factor(R.mp[i]);
+      const double qm = R.sq[i] * (double)nq.factor(R.mq[i]);
+      rm[i] = pair ? fmax(0.0, 0.5 * (R.ta[i] + pm[i] - qm)) : 0.0;
+      my_res += rm[i];
+    }
+    const bool residual = pair && wave_sum_d(my_res) > 0.0;
+    double mass[kSlots];
+    double my = 0.0;
+    int my_last = -1;
+#pragma unroll
+    for (int i = 0; i < kSlots; ++i) {
+      mass[i] = residual ? rm[i] : pm[i];
+      my += mass[i];
+      if (mass[i] > 0.0) my_last = lane * nslot + i;
+    }
+    const double incl = wave_incl_scan(my);
+    const double W = __shfl(incl, 63, 64);
+    const double target = (double)A.u_res[(size_t)b * G1 + k] * W;
+    // the first chunk with positive mass whose end exceeds the target
+    int cs = -1;
+    double pre = 0.0;
+    const unsigned long long hit = __ballot(incl > target && my > 0.0);
+    if (hit) {
+      const int hl = __ffsll((long long)hit) - 1;
+      double run = incl - my;
+      int found = -1;
+      double fpre = 0.0;
+#pragma unroll
+      for (int i = 0; i < kSlots; ++i) {
+        if (found < 0 && mass[i] > 0.0 && run + mass[i] > target) {
+          found = lane * nslot + i;
+          fpre = run;
+        }
+        run += mass[i];
+      }
+      cs = __shfl(found, hl, 64);
+      pre = __shfl(fpre, hl, 64);
+    }
+    if (cs < 0) {  // rounding put the target at the very end: the last chunk with mass
+      int last = my_last;
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) last = max(last, __shfl_xor(last, off, 64));
+      cs = max(last, 0);
+      double before = 0.0;
+#pragma unroll
+      for (int i = 0; i < kSlots; ++i)
+        if (lane * nslot + i < cs) before += mass[i];
+      pre = wave_sum_d(before);
+    }
+    float cmp = kNegInf, cmq = kNegInf;  // the chunk's maxima, as the sweep used them
+#pragma unroll
+    for (int i = 0; i < kSlots; ++i)
+      if (lane * nslot + i == cs) {
+        cmp = R.mp[i];
+        cmq = R.mq[i];
+      }
+    cmp = wave_max(cmp);
+    cmq = wave_max(cmq);
+    if (lane == 0) {
+      s_k = k;
+      s_cs = cs;
+      s_resid = residual ? 1 : 0;
+      s_rem = target - pre;
+      s_fac[0] = cmp == kNegInf ? 0.f : cmp * kLog2e;
+      s_fac[1] = cmq == kNegInf ? 0.f : cmq * kLog2e;
+      s_fac[2] = np.factor(cmp);
+      s_fac[3] = nq.factor(cmq);
+    }
+  }
+  __syncthreads();
+  // ---- the draw: waves 0-3 scan chunk cs in ascending vocabulary order
+  // (thread t holds entries cs*kChunk + t*kPerT ...; every wave reaches every
+  // barrier, only waves 0-3 work between them)
+  const int k = s_k;
+  float wt[kPerT];
+  double sum = 0.0, incl = 0.0;
+  int mine = -1;
+  const int x0 = s_cs * kChunk + tid * kPerT;
+  if (w < 4) {
+    const bool residual = s_resid != 0;
+    const float rp = s_fac[0], rq = s_fac[1], fp = s_fac[2], fq = s_fac[3];
+    const char* prow = (const char*)A.p + ((size_t)b * A.p_stride + (size_t)k * A.V) * esz;
+    const char* qrow = (const char*)A.q + ((size_t)b * A.q_stride + (size_t)k * A.V) * esz;
+    float zp[kPerT], zq[kPerT];
+#pragma unroll
+    for (int v = 0; v < kPerT / VEC; ++v) Elt<BF16>::load(prow, min(x0 + v * VEC, A.V - VEC), zp + v * VEC);
+    if (residual) {
+#pragma unroll
+      for (int v = 0; v < kPerT / VEC; ++v) Elt<BF16>::load(qrow, min(x0 + v * VEC, A.V - VEC), zq + v * VEC);
+    }
+#pragma unroll
+    for (int e = 0; e < kPerT; ++e) {
+      float wv = 0.f;
+      if (x0 + e < A.V) {
+#pragma clang fp contract(off)
+        const float ep = exp2_hw(fmaf(zp[e], kLog2e, -rp));
+        if (residual) {
+          const float eq = exp2_hw(fmaf(zq[e], kLog2e, -rq));
+          wv = fmaxf(ep * fp - eq * fq, 0.f);
+        } else {
+          wv = ep * fp;
+        }
+      }
+      wt[e] = wv;
+      sum += (double)wv;
+      if (wv > 0.f) mine = x0 + e;
+    }
+    const double winc = wave_incl_scan(sum);
+    int lmax = mine;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) lmax = max(lmax, __shfl_xor(lmax, off, 64));
+    if (lane == 63) s_wt[w] = winc;
+    if (lane == 0) s_last[w] = lmax;
+    incl = winc;
+  }
+  __syncthreads();
+  if (w < 4) {
+    double excl_w = 0.0;
+    for (int i = 0; i < w; ++i) excl_w += s_wt[i];
+    incl += excl_w;
+    const unsigned long long h = __ballot(incl > s_rem && sum > 0.0);
+    if (lane == 0) s_hit[w] = h ? __ffsll((long long)h) - 1 : -1;
+  }
+  __syncthreads();
+  if (w < 4) {
+    int hw = -1;
+    for (int i = 0; i < 4; ++i)
+      if (hw < 0 && s_hit[i] >= 0) hw = i;
+    if (hw == w && lane == s_hit[w]) {
+      const double rem = s_rem;
+      double run = incl - sum;
+      int found = -1;
+#pragma unroll
+      for (int e = 0; e < kPerT; ++e) {
+        run += (double)wt[e];
+        if (found < 0 && wt[e] > 0.f && run > rem) found = x0 + e;
+      }
+      s_tok = found >= 0 ? found : mine;
+    }
+    if (hw < 0 && tid == 0) {  // the target lies past the chunk's total (rounding)
+      int last = -1;
+      for (int i = 0; i < 4; ++i) last = max(last, s_last[i]);
+      s_tok = last < 0 ? 0 : last;
+    }
+  }
+  __syncthreads();
   if (w != 0) return;
-  // ---- accept chain: first j with NOT (u_acc < a_j)
-  bool rej = false;
-  if (lane < gam) rej = !((double)A.u_acc[(size_t)b * A.gmax + lane] < rr[lane].a);
-  const unsigned long long rmask = __ballot(rej);
-  const int k = rmask ? (__ffsll((long long)rmask) - 1) : gam;
-  const int tok = draw_token<BF16, E>(A, b, k, gam);
+  const int tok = s_tok;
   clear_records(A, b, gam);  // every read of them is done
   // ---- outputs
   int32_t* ot = A.out_tokens + (size_t)b * G1;
@@ -905,7 +947,7 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
   const int G1 = gamma_max + 1;
   const size_t esz = dtype == SR_BF16 ? 2 : 4;
   char* ws = (char*)workspace;
-  const int nw = G1 < 16 ? G1 : 16;
+  const int nw = G1 < 4 ? 4 : (G1 < 16 ? G1 : 16);  // the draw uses waves 0-3
   // sequences in launches of at most kMaxSeqs (the sweep's row table)
   for (int b0 = 0; b0 < B; b0 += kMaxSeqs) {
     const int Bl = B - b0 < kMaxSeqs ? B - b0 : kMaxSeqs;
