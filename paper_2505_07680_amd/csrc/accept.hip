@@ -439,7 +439,8 @@ accept_sweep_kernel(Args A) {
 
   // Second pass of a pair row's task: wait for every chunk record of the row,
   // then sum |P - Q| over the entries kept from the first pass.
-  auto second_pass = [&](const TaskInfo& t, const Raw<BF16, E>& r, float cmp, float cmq) __attribute__((always_inline)) {
+  auto second_pass = [&](const TaskInfo& t, const Raw<BF16, E>& r, float cmp, float cmq, const TaskInfo& tn,
+                         Raw<BF16, E>& nxt) __attribute__((always_inline)) {
     if (w == 0) {
       float m1[kSlots], m2[kSlots];
       double s1[kSlots], s2[kSlots];
@@ -466,6 +467,9 @@ accept_sweep_kernel(Args A) {
         }
         __builtin_amdgcn_s_sleep(2);
       }
+      __builtin_amdgcn_sched_barrier(0);
+      issue_loads<BF16, E>(A, tn, nxt);
+      __builtin_amdgcn_sched_barrier(0);
       const RowNorm np = row_norm(m1, s1);
       const RowNorm nq = row_norm(m2, s2);
       if (lane == 0) {
@@ -526,10 +530,13 @@ accept_sweep_kernel(Args A) {
     const bool more = task_n < n_tasks;
     const TaskInfo tn = decode_task<BF16>(A, s_rows, more ? task_n : task);  // past the end: reload (cached)
     Raw<BF16, E> nxt;
+    // Waves 1-3 prefetch first. Wave 0 polls the row's records first (a wave's
+    // loads complete in issue order, so its poll would otherwise also wait for
+    // its prefetch) and prefetches after.
     __builtin_amdgcn_sched_barrier(0);
-    issue_loads<BF16, E>(A, tn, nxt);
+    if (w != 0 || !t.pair) issue_loads<BF16, E>(A, tn, nxt);
     __builtin_amdgcn_sched_barrier(0);
-    if (t.pair) second_pass(t, cur, cmp, cmq);  // workgroup-uniform
+    if (t.pair) second_pass(t, cur, cmp, cmq, tn, nxt);  // workgroup-uniform
     if (!more) break;
     float cmp_n, cmq_n;
     first_pass(tn, nxt, cmp_n, cmq_n);
