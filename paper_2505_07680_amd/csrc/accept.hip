@@ -146,11 +146,9 @@ struct Args {
   int32_t* status;
 };
 
-// Hardware 2^x (one instruction; results below 2^-126 flush to zero, i.e.
-// weights under 2^-126 of their chunk's largest are dropped). The sweep and
+// exp2_hw drops weights under 2^-126 of their chunk's largest. The sweep and
 // the finish kernel both use it, so a draw sees the same weights the chunk
 // sums were built from.
-__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Pairwise sum of a lane's entries (a fixed tree, log2(N) roundings deep).
 template <int N>
@@ -195,9 +193,6 @@ __device__ __forceinline__ RowNorm row_norm(const float (&m)[kSlots], const doub
   return r;
 }
 
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, size_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
-}
 
 // Inclusive prefix over sequences of their live-row counts (gamma_b + 1, or 0
 // for an invalid gamma), in LDS. Each thread scans a contiguous segment.

@@ -20,6 +20,8 @@
 //   * S^T = K Q^T on MFMA (v_mfma_f32_16x16x32_bf16: 16 keys x 16 queries per
 //     block, K=32 over the head dimension); each lane then holds 4 scores of
 //     ONE query, so the softmax max/sum need only two cross-lane steps;
+//   * the softmax reference maximum of a row is raised only when a tile exceeds
+//     it by more than 2^8, so the output accumulators are rarely rescaled;
 //   * P is rounded to bf16 in place: its accumulator layout is exactly the B
 //     operand of O^T += V^T P^T (v_mfma_f32_16x16x16_bf16, K=16 over the keys);
 //     the V^T operand is gathered from LDS with 16-bit reads.
@@ -39,7 +41,12 @@ constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kWaveKeys = 16;
 constexpr int kTileKeys = kWaves * kWaveKeys;
-constexpr int kMaxNQ = 5;
+// At most three 16-row query groups per workgroup: more rows than that go to
+// further query chunks (their K/V reads are largely served by the XCD's L2,
+// as the chunks of one (sequence, kv head, split) run on one XCD at the same
+// time), which keeps the accumulators in VGPRs at two waves per SIMD.
+constexpr int kMaxNQ = 3;
+constexpr float kLazy = 8.f;  // log2 headroom of the lazily rescaled softmax reference
 
 template <int D>
 struct Geo {
@@ -184,14 +191,19 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
   // the loop body issues a fixed number of loads per tile and each stage
   // waits only for its own loads; refetches past the end hit the same line.
   const uint8_t* mload = mrow ? mrow : (const uint8_t*)kslab;
+  // K/V slabs of (b, g) as buffer resources: 32-bit row offsets
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(kslab, (size_t)L_cap * D * 2);
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(vslab, (size_t)L_cap * D * 2);
+  const uint32_t lane_off = (uint32_t)(lane / GG::kChunksPerRow) * (D * 2) + (uint32_t)(lane % GG::kChunksPerRow) * 16;
   auto fetch = [&](int t, Stage<D>& st) __attribute__((always_inline)) {
     const int kb0 = key_begin + t * kTileKeys + w * kWaveKeys;
 #pragma unroll
     for (int u = 0; u < GG::kLoads; ++u) {
-      const int row = min(kb0 + u * GG::kRowsPerLoad + lane / GG::kChunksPerRow, key_end - 1);
-      const size_t off = (size_t)row * D + (lane % GG::kChunksPerRow) * 8;
-      st.k[u] = *(const u32x4*)(kslab + off);
-      st.v[u] = *(const u32x4*)(vslab + off);
+      // rows past the split's last key re-read that key (same cache lines)
+      const int r0 = min(kb0 + u * GG::kRowsPerLoad, key_end - 1);
+      const uint32_t off = (uint32_t)r0 * (D * 2) + lane_off;
+      st.k[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, 0));
+      st.v[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, 0));
     }
     st.mbyte = mload[min(kb0 + (lane & (kWaveKeys - 1)), key_end - 1)];
   };
@@ -219,6 +231,7 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
       __builtin_amdgcn_sched_barrier(0);
     }
     if (t >= n_tiles || kb0 >= key_end) return;  // wave-uniform: nothing of this tile to compute
+    const bool full = vbits == 0xffffu && kb0 + kWaveKeys - 1 <= causal0;  // wave-uniform
     // ---- S^T = K Q^T (16 keys x 16 queries per group)
     floatx4 sacc[NQ];
 #pragma unroll
@@ -241,34 +254,48 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
     for (int qg = 0; qg < NQ; ++qg) {
       if (row0 + qg * 16 < Mb) {
         const int r = row0 + qg * 16 + l16;
-        const int lim = r < Mb ? causal0 + r / G : -1;  // last key this query row sees
         float s[4];
         float mt = kNegInf;
+        if (full) {  // every row of the wave sees all 16 keys (rows past Mb are dropped at the end)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int kl = lg * 4 + e;
-          const bool vis = ((vbits >> kl) & 1u) && (kb0 + kl <= lim);
-          s[e] = vis ? sacc[qg][e] * scale_log2 : kNegInf;
-          mt = fmaxf(mt, s[e]);
+          for (int e = 0; e < 4; ++e) {
+            s[e] = sacc[qg][e] * scale_log2;
+            mt = fmaxf(mt, s[e]);
+          }
+        } else {
+          const int lim = r < Mb ? causal0 + r / G : -1;  // last key this query row sees
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int kl = lg * 4 + e;
+            const bool vis = ((vbits >> kl) & 1u) && (kb0 + kl <= lim);
+            s[e] = vis ? sacc[qg][e] * scale_log2 : kNegInf;
+            mt = fmaxf(mt, s[e]);
+          }
         }
         mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
         mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-        const float mn = fmaxf(m_run[qg], mt);
-        const bool none = (mn == kNegInf);
-        const float alpha = none ? 1.f : exp2f(m_run[qg] - mn);
+        // Lazy rescaling: a row keeps its reference maximum until a tile
+        // exceeds it by more than kLazy (log2 units), so P stays below
+        // 2^kLazy and the output accumulators are rescaled only then
+        // (skipped by the whole wave when no row needs it).
+        const bool grow = mt > m_run[qg] + kLazy;
+        const float mref = grow ? mt : m_run[qg];
+        const float alpha = grow ? (m_run[qg] == kNegInf ? 0.f : exp2_hw(m_run[qg] - mt)) : 1.f;
         float pk[4];
         float ls = 0.f;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          pk[e] = none ? 0.f : exp2f(s[e] - mn);
+          pk[e] = mref == kNegInf ? 0.f : exp2_hw(s[e] - mref);
           ls += pk[e];
         }
         ls += __shfl_xor(ls, 16, 64);
         ls += __shfl_xor(ls, 32, 64);
         l_run[qg] = l_run[qg] * alpha + ls;
-        m_run[qg] = mn;
+        m_run[qg] = mref;
+        if (__ballot(grow) != 0ull) {
 #pragma unroll
-        for (int db = 0; db < DB; ++db) o[db][qg] *= alpha;
+          for (int db = 0; db < DB; ++db) o[db][qg] *= alpha;
+        }
         const uint32_t w0 = pack_bf16x2(pk[0], pk[1]);
         const uint32_t w1 = pack_bf16x2(pk[2], pk[3]);
         pb[qg] = __builtin_bit_cast(shortx4, make_uint2(w0, w1));
@@ -415,7 +442,8 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
       if (ns == 1) {
         const float Lr = mlf[MQ + rl];
         const int i = r / G, h = g * G + r % G;
-        *(floatx4*)(out + ((size_t)(b * (gmax + 1) + i) * Hq + h) * D + col) = Lr > 0.f ? sum * (1.f / Lr) : floatx4{0.f, 0.f, 0.f, 0.f};
+        *(floatx4*)(out + ((size_t)(b * (gmax + 1) + i) * Hq + h) * D + col) =
+            (r < Mb && Lr > 0.f) ? sum * (1.f / Lr) : floatx4{0.f, 0.f, 0.f, 0.f};
       } else if (r < Mb) {
         const uint32_t rec = (uint32_t)((pair * n_splits + split) * R + r);
         __builtin_amdgcn_raw_buffer_store_b128(sum, rs_o, (rec * D + col) * 4, 0, kDeviceCoherent);
@@ -504,9 +532,7 @@ SplitKernel pick_split(int nq) {
   switch (nq) {
     case 1: return attn_split_kernel<D, 1>;
     case 2: return attn_split_kernel<D, 2>;
-    case 3: return attn_split_kernel<D, 3>;
-    case 4: return attn_split_kernel<D, 4>;
-    default: return attn_split_kernel<D, 5>;
+    default: return attn_split_kernel<D, 3>;
   }
 }
 
