@@ -106,7 +106,7 @@ const char* specrouter_status_string(int code);
  *                      [gamma_b + 1, L_cap], else SR_ST_KVLEN and zero output
  * gamma      i32  [B]  in [0, gamma_max] (0 = plain decode), else SR_ST_GAMMA
  * out        fp32 [B][gamma_max+1][Hq][D]          (16-byte aligned)
- * scale      score scale, normally 1/sqrt(D)
+ * scale      score scale, normally 1/sqrt(D); must be positive and finite (else SR_EINVAL)
  * workspace  device scratch of specrouter_verify_attention_workspace_size()
  *            bytes (may be NULL when that size is 0). Zero-fill it once before
  *            its first use; every call leaves it in that state again (it holds

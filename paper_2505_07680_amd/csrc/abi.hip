@@ -73,6 +73,7 @@ int specrouter_verify_attention(const void* q, const void* k_cache, const void* 
   if (!q || !k_cache || !v_cache || !kv_len || !gamma || !out) return SR_EINVAL;
   if (!attention_shape_ok(B, gamma_max, Hq, Hkv, L_cap)) return SR_EINVAL;
   if (D != 64 && D != 128) return SR_EUNSUPPORTED;
+  if (!(scale > 0.f && scale < __builtin_inff())) return SR_EINVAL;  // a positive, finite score scale
   if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out)) return SR_EINVAL;
   sr::AttentionPlan plan;
   const int rc = sr::attention_plan(B, gamma_max, Hq, Hkv, D, L_cap, &plan);

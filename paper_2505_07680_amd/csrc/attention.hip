@@ -214,12 +214,13 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
     const int kb0 = key_begin + t * kTileKeys + w * kWaveKeys;
     const bool key_ok = lane < kWaveKeys && kb0 + lane < key_end && (mrow == nullptr || st.mbyte != 0u);
     const uint32_t vbits = (uint32_t)__ballot(key_ok) & 0xffffu;
+    const bool all_rows = vbits == 0xffffu;  // wave-uniform
 #pragma unroll
     for (int u = 0; u < GG::kLoads; ++u) {
       const int rl = u * GG::kRowsPerLoad + lane / GG::kChunksPerRow;
       const int c = lane % GG::kChunksPerRow;
       *(u32x4*)(kst + rl * GG::kKStride + c * 16) = st.k[u];
-      const u32x4 vv = ((vbits >> rl) & 1u) ? st.v[u] : u32x4{0u, 0u, 0u, 0u};
+      const u32x4 vv = (all_rows || ((vbits >> rl) & 1u)) ? st.v[u] : u32x4{0u, 0u, 0u, 0u};
       uint32_t* dst = (uint32_t*)(vst + rl * GG::kVStride + c * 16);
       *(uint2*)dst = make_uint2(vv.x, vv.y);
       *(uint2*)(dst + 2) = make_uint2(vv.z, vv.w);
@@ -256,12 +257,13 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
         const int r = row0 + qg * 16 + l16;
         float s[4];
         float mt = kNegInf;
-        if (full) {  // every row of the wave sees all 16 keys (rows past Mb are dropped at the end)
+        if (full) {
+          // every row of the wave sees all 16 keys (rows past Mb are dropped
+          // at the end); the scale is positive, so the maximum is taken on the
+          // raw products and each probability below is one fma and one exp2
+          mt = fmaxf(fmaxf(sacc[qg][0], sacc[qg][1]), fmaxf(sacc[qg][2], sacc[qg][3])) * scale_log2;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            s[e] = sacc[qg][e] * scale_log2;
-            mt = fmaxf(mt, s[e]);
-          }
+          for (int e = 0; e < 4; ++e) s[e] = sacc[qg][e];
         } else {
           const int lim = r < Mb ? causal0 + r / G : -1;  // last key this query row sees
 #pragma unroll
@@ -285,7 +287,7 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
         float ls = 0.f;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          pk[e] = mref == kNegInf ? 0.f : exp2_hw(s[e] - mref);
+          pk[e] = mref == kNegInf ? 0.f : (full ? exp2_hw(fmaf(s[e], scale_log2, -mref)) : exp2_hw(s[e] - mref));
           ls += pk[e];
         }
         ls += __shfl_xor(ls, 16, 64);

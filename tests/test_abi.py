@@ -67,6 +67,10 @@ def test_attention_rejects_bad_host_arguments(lib):
     bad = list(args)
     bad[0] = ctypes.c_void_p(4100)  # misaligned
     assert lib.specrouter_verify_attention(*bad) == _lib.SR_EINVAL
+    for scale in (0.0, -0.1, float("nan"), float("inf")):  # the score scale must be positive and finite
+        bad = list(args)
+        bad[13] = scale
+        assert lib.specrouter_verify_attention(*bad) == _lib.SR_EINVAL
 
 
 @no_device
