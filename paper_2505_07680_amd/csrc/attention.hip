@@ -46,7 +46,11 @@ constexpr int kTileKeys = kWaves * kWaveKeys;
 // as the chunks of one (sequence, kv head, split) run on one XCD at the same
 // time), which keeps the accumulators in VGPRs at two waves per SIMD.
 constexpr int kMaxNQ = 3;
-constexpr float kLazy = 8.f;  // log2 headroom of the lazily rescaled softmax reference
+constexpr float kLazy = 8.f;
+// Arrival counters sit one per 128-byte line: the splits of different
+// (sequence, kv head) pairs then never contend for one line.
+constexpr int kCounterStride = 32;
+constexpr int kMaxSplitKeys = 4224;  // keys per split at most (about 2 MB of K/V at D = 128)  // log2 headroom of the lazily rescaled softmax reference
 
 template <int D>
 struct Geo {
@@ -119,18 +123,26 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
                   const uint16_t* __restrict__ vc, const uint8_t* __restrict__ mask,
                   const int32_t* __restrict__ kv_len, const int32_t* __restrict__ gamma,
                   float* __restrict__ out, float* __restrict__ part_o,
-                  float* __restrict__ part_ml, uint32_t* __restrict__ arrivals, int gmax, int Hq,
-                  int Hkv, int L_cap, float scale_log2, int split_keys, int n_splits,
-                  int32_t* __restrict__ status) {
+                  float* __restrict__ part_ml, uint32_t* __restrict__ arrivals, int B, int gmax,
+                  int Hq, int Hkv, int L_cap, float scale_log2, int split_keys, int n_splits,
+                  int q_chunks, int32_t* __restrict__ status) {
   using GG = Geo<D>;
   constexpr int MQ = 16 * NQ;
   constexpr int DB = D / 16;
   __shared__ __attribute__((aligned(16))) unsigned char lds[Lds<D, NQ>::kBytes];
 
-  const int split = blockIdx.x;
-  const int g = blockIdx.y % Hkv;
-  const int qc = blockIdx.y / Hkv;
-  const int b = blockIdx.z;
+  // Workgroup order: (sequence, kv head) pair fastest, then key split in
+  // descending order, then query chunk. Workgroups are dealt to the XCDs
+  // round-robin, so each XCD gets every split of an even share of the pairs
+  // (and the query chunks of one pair and split share an XCD and its L2), and
+  // the later splits, which only long sequences have, start first.
+  const int P = B * Hkv;
+  const int pair_id = (int)(blockIdx.x % (unsigned)P);
+  const int rest = (int)(blockIdx.x / (unsigned)P);
+  const int split = n_splits - 1 - rest % n_splits;
+  const int qc = rest / n_splits;
+  const int g = pair_id % Hkv;
+  const int b = pair_id / Hkv;
   const int G = Hq / Hkv;
   const int R = G * (gmax + 1);
   const int gam = gamma[b];
@@ -412,7 +424,7 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
   // final here, otherwise it is published as a partial.
   const int ns = (L + split_keys - 1) / split_keys;
   const size_t pair = (size_t)(b * Hkv + g);
-  const int n_rec = (int)(gridDim.x * (size_t)Hkv * gridDim.z) * R;  // records in the partial arrays
+  const int n_rec = (int)((size_t)n_splits * P) * R;  // records in the partial arrays
   const __amdgpu_buffer_rsrc_t rs_o = partial_rsrc(part_o, (uint32_t)((size_t)n_rec * D * 4));
   const __amdgpu_buffer_rsrc_t rs_ml = partial_rsrc(part_ml, (uint32_t)((size_t)n_rec * 8));
   constexpr int kItemsP = (MQ * (LL::kDp / 4) + kThreads - 1) / kThreads;
@@ -461,7 +473,7 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
   __syncthreads();
   __shared__ uint32_t last_flag;
   if (tid == 0) {
-    uint32_t* cnt = arrivals + pair * (gridDim.y / Hkv) + qc;
+    uint32_t* cnt = arrivals + (pair * q_chunks + qc) * kCounterStride;
     const uint32_t before = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const bool last = before == (uint32_t)(ns - 1);
     if (last) st_dev(cnt, 0u);  // every split of this chunk has arrived: reset for the next call
@@ -527,7 +539,7 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
 
 typedef void (*SplitKernel)(const uint16_t*, const uint16_t*, const uint16_t*, const uint8_t*,
                             const int32_t*, const int32_t*, float*, float*, float*, uint32_t*, int,
-                            int, int, int, float, int, int, int32_t*);
+                            int, int, int, int, float, int, int, int, int32_t*);
 
 template <int D>
 SplitKernel pick_split(int nq) {
@@ -556,6 +568,10 @@ int attention_plan(int B, int gamma_max, int Hq, int Hkv, int D, int L_cap, Atte
   const long pairs = (long)B * Hkv * plan->q_chunks;
   const long target = (long)cus * per_cu;
   long splits = (target + pairs - 1) / pairs;
+  // Bound a workgroup's keys, so the last workgroups of a ragged batch do not
+  // run long after the rest have finished.
+  const long by_length = (L_cap + kMaxSplitKeys - 1) / kMaxSplitKeys;
+  if (splits < by_length) splits = by_length;
   const long max_splits = (L_cap + kWaveKeys - 1) / kWaveKeys;
   if (splits < 1) splits = 1;
   if (splits > max_splits) splits = max_splits;
@@ -568,8 +584,8 @@ int attention_plan(int B, int gamma_max, int Hq, int Hkv, int D, int L_cap, Atte
   sk = (sk + kWaveKeys - 1) / kWaveKeys * kWaveKeys;
   plan->split_keys = sk;
   plan->n_splits = (L_cap + sk - 1) / sk;
-  // [arrival counters: B*Hkv*q_chunks u32, padded to 256 B][partial o][partial (m, l)]
-  const size_t counters = ((size_t)B * Hkv * plan->q_chunks * sizeof(uint32_t) + 255) / 256 * 256;
+  // [arrival counters: B*Hkv*q_chunks, one per 128-byte line][partial o][partial (m, l)]
+  const size_t counters = (size_t)B * Hkv * plan->q_chunks * kCounterStride * sizeof(uint32_t);
   plan->part_offset = counters;
   plan->workspace_bytes =
       plan->n_splits > 1 ? counters + (size_t)B * Hkv * plan->n_splits * R * (D + 2) * sizeof(float) : 0;
@@ -586,11 +602,11 @@ int launch_verify_attention(const void* q, const void* k_cache, const void* v_ca
   uint32_t* arrivals = (uint32_t*)workspace;
   float* part_o = workspace ? (float*)((char*)workspace + plan.part_offset) : nullptr;
   float* part_ml = part_o ? part_o + (size_t)B * Hkv * plan.n_splits * R * D : nullptr;
-  dim3 grid(plan.n_splits, Hkv * plan.q_chunks, B);
+  dim3 grid((unsigned)((long)plan.n_splits * plan.q_chunks * B * Hkv));
   hipLaunchKernelGGL(pick_split(D, plan.nq), grid, dim3(kThreads), 0, stream,
                      (const uint16_t*)q, (const uint16_t*)k_cache, (const uint16_t*)v_cache,
-                     cache_mask, kv_len, gamma, out, part_o, part_ml, arrivals, gamma_max, Hq, Hkv,
-                     L_cap, scale * kLog2e, plan.split_keys, plan.n_splits, status);
+                     cache_mask, kv_len, gamma, out, part_o, part_ml, arrivals, B, gamma_max, Hq, Hkv,
+                     L_cap, scale * kLog2e, plan.split_keys, plan.n_splits, plan.q_chunks, status);
   if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
   return SR_OK;
 }
