@@ -51,8 +51,22 @@
 namespace sr {
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 256;  // sweep workgroup: four waves, one chunk per task
 constexpr int kWaves = kThreads / 64;
+
+// Fixed-order merges of the per-wave partials.
+__device__ __forceinline__ float max_waves(const float* v) {
+  float m = v[0];
+#pragma unroll
+  for (int i = 1; i < kWaves; ++i) m = fmaxf(m, v[i]);
+  return m;
+}
+__device__ __forceinline__ double sum_waves(const double* v) {
+  double a = v[0];
+#pragma unroll
+  for (int i = 1; i < kWaves; ++i) a += v[i];
+  return a;
+}
 constexpr int kSlots = 2;                // chunk records per lane in the row merges
 constexpr int kMaxChunks = 64 * kSlots;  // chunks per row
 constexpr int kMaxRows = SPECROUTER_MAX_GAMMA + 1;
@@ -363,8 +377,8 @@ accept_sweep_kernel(Args A) {
       s_m[1][w] = mq;
     }
     __syncthreads();
-    cmp = fmaxf(fmaxf(s_m[0][0], s_m[0][1]), fmaxf(s_m[0][2], s_m[0][3]));
-    cmq = fmaxf(fmaxf(s_m[1][0], s_m[1][1]), fmaxf(s_m[1][2], s_m[1][3]));
+    cmp = max_waves(s_m[0]);
+    cmq = max_waves(s_m[1]);
 
     // exponentials, sums, KL numerator; groups of four are summed as
     // (a0 + a1) + (a2 + a3), then a tree over groups
@@ -422,9 +436,9 @@ accept_sweep_kernel(Args A) {
       StatRec sr;
       sr.mp = cmp;
       sr.mq = cmq;
-      sr.sp = ((s_s[0][0] + s_s[0][1]) + s_s[0][2]) + s_s[0][3];
-      sr.sq = ((s_s[1][0] + s_s[1][1]) + s_s[1][2]) + s_s[1][3];
-      sr.kl = ((s_s[2][0] + s_s[2][1]) + s_s[2][2]) + s_s[2][3];
+      sr.sp = sum_waves(s_s[0]);
+      sr.sq = sum_waves(s_s[1]);
+      sr.kl = sum_waves(s_s[2]);
       u32x4 w0, w1;
       pack_rec(sr, w0, w1);
       __builtin_amdgcn_raw_buffer_store_b128(w0, rs_stats, (uint32_t)(rec * kRecBytes), 0, kDeviceCoherent);
@@ -506,7 +520,7 @@ accept_sweep_kernel(Args A) {
     const double dtv = wave_sum_d((double)tree_sum(ga));
     if (lane == 0) s_s[0][w] = dtv;
     __syncthreads();
-    if (tid == 0) A.tvabs[(size_t)t.row * nc + t.c] = ((s_s[0][0] + s_s[0][1]) + s_s[0][2]) + s_s[0][3];
+    if (tid == 0) A.tvabs[(size_t)t.row * nc + t.c] = sum_waves(s_s[0]);
   };
 
   // Pipeline: the second pass of task i runs after the loads of task i+1 are
@@ -790,80 +804,94 @@ accept_finish_kernel(Args A) {
     }
   }
   __syncthreads();
-  // ---- the draw: waves 0-3 scan chunk cs in ascending vocabulary order
-  // (thread t holds entries cs*kChunk + t*kPerT ...; every wave reaches every
-  // barrier, only waves 0-3 work between them)
+  // ---- the draw: waves 0-3 scan chunk cs in ascending vocabulary order, in
+  // passes of 4096 entries (thread t of a pass holds 16 consecutive entries);
+  // every wave reaches every barrier, only waves 0-3 work between them
   const int k = s_k;
-  float wt[kPerT];
-  double sum = 0.0, incl = 0.0;
-  int mine = -1;
-  const int x0 = s_cs * kChunk + tid * kPerT;
-  if (w < 4) {
+  {
+    constexpr int kPerT = 16;
+    constexpr int kPass = 256 * kPerT;
     const bool residual = s_resid != 0;
     const float rp = s_fac[0], rq = s_fac[1], fp = s_fac[2], fq = s_fac[3];
     const char* prow = (const char*)A.p + ((size_t)b * A.p_stride + (size_t)k * A.V) * esz;
     const char* qrow = (const char*)A.q + ((size_t)b * A.q_stride + (size_t)k * A.V) * esz;
-    float zp[kPerT], zq[kPerT];
+    const double rem0 = s_rem;
+    double carry = 0.0;  // mass of the earlier passes
+    int last_tok = -1;
+    if (tid == 0) s_tok = -1;
+    for (int pass = 0; pass < kChunk / kPass; ++pass) {
+      float wt[kPerT];
+      double sum = 0.0, incl = 0.0;
+      int mine = -1;
+      const int x0 = s_cs * kChunk + pass * kPass + tid * kPerT;
+      if (w < 4) {
+        float zp[kPerT], zq[kPerT];
 #pragma unroll
-    for (int v = 0; v < kPerT / VEC; ++v) Elt<BF16>::load(prow, min(x0 + v * VEC, A.V - VEC), zp + v * VEC);
-    if (residual) {
-#pragma unroll
-      for (int v = 0; v < kPerT / VEC; ++v) Elt<BF16>::load(qrow, min(x0 + v * VEC, A.V - VEC), zq + v * VEC);
-    }
-#pragma unroll
-    for (int e = 0; e < kPerT; ++e) {
-      float wv = 0.f;
-      if (x0 + e < A.V) {
-#pragma clang fp contract(off)
-        const float ep = exp2_hw(fmaf(zp[e], kLog2e, -rp));
+        for (int v = 0; v < kPerT / VEC; ++v) Elt<BF16>::load(prow, min(x0 + v * VEC, A.V - VEC), zp + v * VEC);
         if (residual) {
-          const float eq = exp2_hw(fmaf(zq[e], kLog2e, -rq));
-          wv = fmaxf(ep * fp - eq * fq, 0.f);
-        } else {
-          wv = ep * fp;
+#pragma unroll
+          for (int v = 0; v < kPerT / VEC; ++v) Elt<BF16>::load(qrow, min(x0 + v * VEC, A.V - VEC), zq + v * VEC);
         }
-      }
-      wt[e] = wv;
-      sum += (double)wv;
-      if (wv > 0.f) mine = x0 + e;
-    }
-    const double winc = wave_incl_scan(sum);
-    int lmax = mine;
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) lmax = max(lmax, __shfl_xor(lmax, off, 64));
-    if (lane == 63) s_wt[w] = winc;
-    if (lane == 0) s_last[w] = lmax;
-    incl = winc;
-  }
-  __syncthreads();
-  if (w < 4) {
-    double excl_w = 0.0;
-    for (int i = 0; i < w; ++i) excl_w += s_wt[i];
-    incl += excl_w;
-    const unsigned long long h = __ballot(incl > s_rem && sum > 0.0);
-    if (lane == 0) s_hit[w] = h ? __ffsll((long long)h) - 1 : -1;
-  }
-  __syncthreads();
-  if (w < 4) {
-    int hw = -1;
-    for (int i = 0; i < 4; ++i)
-      if (hw < 0 && s_hit[i] >= 0) hw = i;
-    if (hw == w && lane == s_hit[w]) {
-      const double rem = s_rem;
-      double run = incl - sum;
-      int found = -1;
+        for (int e = 0; e < kPerT; ++e) {
+          float wv = 0.f;
+          if (x0 + e < A.V) {
+#pragma clang fp contract(off)
+            const float ep = exp2_hw(fmaf(zp[e], kLog2e, -rp));
+            if (residual) {
+              const float eq = exp2_hw(fmaf(zq[e], kLog2e, -rq));
+              wv = fmaxf(ep * fp - eq * fq, 0.f);
+            } else {
+              wv = ep * fp;
+            }
+          }
+          wt[e] = wv;
+          sum += (double)wv;
+          if (wv > 0.f) mine = x0 + e;
+        }
+        incl = wave_incl_scan(sum);
+        int lmax = mine;
 #pragma unroll
-      for (int e = 0; e < kPerT; ++e) {
-        run += (double)wt[e];
-        if (found < 0 && wt[e] > 0.f && run > rem) found = x0 + e;
+        for (int off = 32; off > 0; off >>= 1) lmax = max(lmax, __shfl_xor(lmax, off, 64));
+        if (lane == 63) s_wt[w] = incl;
+        if (lane == 0) s_last[w] = lmax;
       }
-      s_tok = found >= 0 ? found : mine;
+      __syncthreads();
+      const double total = ((s_wt[0] + s_wt[1]) + s_wt[2]) + s_wt[3];
+      const double rem = rem0 - carry;
+      for (int i = 0; i < 4; ++i) last_tok = max(last_tok, s_last[i]);
+      const bool here = rem < total;  // workgroup-uniform
+      if (here && w < 4) {
+        double excl_w = 0.0;
+        for (int i = 0; i < w; ++i) excl_w += s_wt[i];
+        incl += excl_w;
+        const unsigned long long h = __ballot(incl > rem && sum > 0.0);
+        if (lane == 0) s_hit[w] = h ? __ffsll((long long)h) - 1 : -1;
+      }
+      __syncthreads();
+      if (here) {
+        if (w < 4) {
+          int hw = -1;
+          for (int i = 0; i < 4; ++i)
+            if (hw < 0 && s_hit[i] >= 0) hw = i;
+          if (hw == w && lane == s_hit[w]) {
+            double run = incl - sum;
+            int found = -1;
+#pragma unroll
+            for (int e = 0; e < kPerT; ++e) {
+              run += (double)wt[e];
+              if (found < 0 && wt[e] > 0.f && run > rem) found = x0 + e;
+            }
+            s_tok = found >= 0 ? found : mine;
+          }
+          if (hw < 0 && tid == 0) s_tok = last_tok < 0 ? 0 : last_tok;  // rounding: the pass's last positive entry
+        }
+        break;  // workgroup-uniform
+      }
+      carry += total;
     }
-    if (hw < 0 && tid == 0) {  // the target lies past the chunk's total (rounding)
-      int last = -1;
-      for (int i = 0; i < 4; ++i) last = max(last, s_last[i]);
-      s_tok = last < 0 ? 0 : last;
-    }
+    __syncthreads();
+    if (tid == 0 && s_tok < 0) s_tok = last_tok < 0 ? 0 : last_tok;  // the target lies past the chunk's total
   }
   __syncthreads();
   if (w != 0) return;
