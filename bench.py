@@ -212,6 +212,7 @@ def main():
     cpu = None
     if not args.no_cpu:
         cpu = cpu_baseline(inp, args.cpu_seqs)
+    sched = scheduler_timing(sr, sets[0]["gamma"], acc0.accept_len, acc0.tv)
 
     line = {
         "metric": "verified draft tokens/s per verify step; HBM GB/s (KV + logits) vs MI355X peak",
@@ -245,10 +246,40 @@ def main():
         "mean_accept_len": round(mean_accept, 3),
         "status_bits": status,
         "cpu_baseline": cpu,
+        "scheduler": sched,
         "host_wall_s": round(wall, 4),
         "input_gen_s": round(gen_s, 2),
     }
     print(json.dumps(line), flush=True)
+
+
+def scheduler_timing(sr, gamma, accept_len, tv, reps=2000):
+    """Host cost of the chain scheduler around this step: one observation of
+    the step's accept outputs (gamma, accept_len, tv; copied to the host once,
+    outside the timing) and one Algorithm 1 selection, over a five-model pool
+    shaped like the paper's Llama family (68M, 1.1B, 7B, 13B, 70B parameters;
+    target 70B; window = the workload's gamma_max)."""
+    g = gamma.cpu().numpy()
+    k = accept_len.cpu().numpy()
+    t = tv.cpu().numpy()
+    cap = [0.068, 1.1, 7.0, 13.0, 70.0]
+    s = sr.ChainScheduler(cap, 4, max(1, t.shape[1]))
+    for m, c in enumerate(cap):
+        s.observe_time(m, 2e-4 * c ** 0.5)  # synthetic per-token times
+    for i in range(5):
+        for j in range(i + 1, 5):
+            s.set_similarity(i, j, 0.5 + 0.08 * i)
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        s.observe_step(3, 4, g, k, t)
+    obs_us = (time.perf_counter() - t0) / reps * 1e6
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        chain, t_eff, n_cand = s.optimal_chain()
+    sel_us = (time.perf_counter() - t0) / reps * 1e6
+    s.close()
+    return {"observe_step_us": round(obs_us, 2), "optimal_chain_us": round(sel_us, 2), "models": len(cap),
+            "candidates": n_cand, "chain": chain, "note": "host C++ via the ctypes binding, per call"}
 
 
 def cpu_baseline(inp, n_seqs, target_s=10.0, cap_s=30.0):

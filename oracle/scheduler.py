@@ -142,11 +142,25 @@ def calibration_objective(params, obs, lam: float) -> float:
     return tot
 
 
+def calibration_gradient(params, obs, lam: float):
+    """Gradient of calibration_objective: with z = A x + B and n = a + r
+    trials, d/dz of an observation's term is n sigmoid(z) - a."""
+    A, B = params
+    gA, gB = lam * (A - 1.0), lam * B
+    for s, a, r in obs:
+        x = _logit(s)
+        e = (a + r) * _sigmoid(A * x + B) - a
+        gA += e * x
+        gB += e
+    return np.array([gA, gB])
+
+
 def calibrate(obs, lam: float = 1.0):
-    """(A, B) maximising the penalised likelihood (R3). The objective is
+    """(A, B) minimising calibration_objective (R3). The objective is
     strictly convex (lam > 0), so the minimiser is unique."""
-    res = optimize.minimize(calibration_objective, x0=np.array([1.0, 0.0]), args=(list(obs), lam),
-                            method="BFGS", options={"gtol": 1e-11, "maxiter": 10000})
+    obs = list(obs)
+    res = optimize.minimize(calibration_objective, x0=np.array([1.0, 0.0]), args=(obs, lam),
+                            jac=calibration_gradient, method="BFGS", options={"gtol": 1e-10, "maxiter": 10000})
     return float(res.x[0]), float(res.x[1])
 
 

@@ -1,9 +1,10 @@
 """MI355X (gfx950) verify step of multi-level speculative decoding.
 
 The compute lives in libspecrouter.so (hand-written HIP kernels behind a C
-ABI, declared in include/specrouter.h); this package holds the kernels'
-sources, the build script and a thin ctypes binding with the same function
-names as the C entry points.
+ABI, declared in include/specrouter.h) together with the host-side chain
+scheduler (include/specrouter_sched.h); this package holds their sources, the
+build script and a thin ctypes binding with the same function names as the C
+entry points.
 """
 
 from . import _lib
@@ -11,6 +12,7 @@ from ._lib import (
     SR_BF16,
     SR_F32,
     AcceptBuffers,
+    ChainScheduler,
     attention_workspace,
     load,
     specrouter_abi_version,
@@ -26,6 +28,7 @@ __all__ = [
     "SR_BF16",
     "SR_F32",
     "AcceptBuffers",
+    "ChainScheduler",
     "attention_workspace",
     "load",
     "specrouter_abi_version",

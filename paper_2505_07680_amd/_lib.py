@@ -17,7 +17,8 @@ import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libspecrouter.so")
-HEADER = os.path.join(os.path.dirname(HERE), "include", "specrouter.h")
+INCLUDE = os.path.join(os.path.dirname(HERE), "include")
+HEADERS = [os.path.join(INCLUDE, "specrouter.h"), os.path.join(INCLUDE, "specrouter_sched.h")]
 
 SR_OK, SR_EINVAL, SR_EUNSUPPORTED, SR_EWORKSPACE, SR_ELAUNCH = 0, -1, -2, -3, -4
 SR_F32, SR_BF16 = 0, 1
@@ -28,6 +29,9 @@ _c_i = ctypes.c_int
 _c_i64 = ctypes.c_int64
 _c_sz = ctypes.c_size_t
 _c_f = ctypes.c_float
+_c_d = ctypes.c_double
+_c_dp = ctypes.POINTER(ctypes.c_double)
+_c_ip = ctypes.POINTER(ctypes.c_int32)
 
 _SIGNATURES = {
     "specrouter_abi_version": (_c_i, []),
@@ -43,6 +47,17 @@ _SIGNATURES = {
         [_c_p, _c_i64, _c_p, _c_i64, _c_i] + [_c_p] * 13 + [_c_i] * 3 + [_c_p, _c_sz, _c_p, _c_p],
     ),
     "specrouter_rollback": (_c_i, [_c_p] * 4 + [_c_i, _c_i, _c_p, _c_p]),
+    # chain scheduler (host code; host pointers)
+    "specrouter_sched_create": (_c_i, [_c_i, _c_dp, _c_i, _c_i, _c_i, _c_d, _c_d, _c_d, ctypes.POINTER(_c_p)]),
+    "specrouter_sched_destroy": (None, [_c_p]),
+    "specrouter_sched_observe_time": (_c_i, [_c_p, _c_i, _c_d]),
+    "specrouter_sched_set_similarity": (_c_i, [_c_p, _c_i, _c_i, _c_d]),
+    "specrouter_sched_observe_step": (_c_i, [_c_p, _c_i, _c_i, _c_i, _c_i, _c_ip, _c_ip,
+                                             ctypes.POINTER(ctypes.c_float)]),
+    "specrouter_sched_calibrate": (_c_i, [_c_p, _c_dp, _c_dp]),
+    "specrouter_sched_metrics": (_c_i, [_c_p, _c_dp, _c_dp, _c_dp, ctypes.POINTER(_c_i)]),
+    "specrouter_sched_effective_time": (_c_i, [_c_p, _c_ip, _c_i, _c_dp]),
+    "specrouter_sched_optimal_chain": (_c_i, [_c_p, _c_ip, ctypes.POINTER(_c_i), _c_dp, ctypes.POINTER(_c_i)]),
 }
 
 _lib = None
@@ -66,10 +81,12 @@ def load() -> ctypes.CDLL:
 
 
 def header_functions() -> list[str]:
-    """Names of the functions declared in include/specrouter.h."""
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(specrouter_\w+)\s*\(", text)))
+    """Names of the functions declared in include/*.h."""
+    names = set()
+    for h in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names.update(re.findall(r"\b(specrouter_\w+)\s*\(", text))
+    return sorted(names)
 
 
 def _ptr(t):
@@ -234,3 +251,150 @@ class AcceptBuffers:
 def attention_workspace(B, gamma_max, Hq, Hkv, D, L_cap, device="cuda"):
     n = specrouter_verify_attention_workspace_size(B, gamma_max, Hq, Hkv, D, L_cap)
     return None if n == 0 else torch.zeros(n, dtype=torch.uint8, device=device)
+
+
+# ----------------------------------------------------------------------------
+# Chain scheduler (host code). Inputs are copied into host arrays; the
+# arithmetic is the library's.
+
+def _host(t, dtype):
+    """A contiguous host numpy array of `t` (a torch tensor on any device, or
+    array-like) with the given numpy dtype."""
+    import numpy as np
+
+    if isinstance(t, torch.Tensor):
+        t = t.detach().cpu().numpy()
+    return np.ascontiguousarray(np.asarray(t), dtype=dtype)
+
+
+def _as_ptr(a, ctype):
+    return a.ctypes.data_as(ctypes.POINTER(ctype))
+
+
+def specrouter_sched_create(capability, target, window, max_levels=None, ema_time=0.2, ema_sim=0.1,
+                            prior_weight=1.0):
+    import numpy as np
+
+    cap = _host(capability, np.float64)
+    n = int(cap.shape[0])
+    h = ctypes.c_void_p()
+    rc = load().specrouter_sched_create(n, _as_ptr(cap, ctypes.c_double), int(target), int(window),
+                                        n if max_levels is None else int(max_levels), float(ema_time),
+                                        float(ema_sim), float(prior_weight), ctypes.byref(h))
+    _check(rc, "specrouter_sched_create")
+    return h
+
+
+def specrouter_sched_destroy(handle) -> None:
+    load().specrouter_sched_destroy(handle)
+
+
+def specrouter_sched_observe_time(handle, model, seconds_per_token) -> None:
+    _check(load().specrouter_sched_observe_time(handle, int(model), float(seconds_per_token)),
+           "specrouter_sched_observe_time")
+
+
+def specrouter_sched_set_similarity(handle, draft, verifier, simscore) -> None:
+    _check(load().specrouter_sched_set_similarity(handle, int(draft), int(verifier), float(simscore)),
+           "specrouter_sched_set_similarity")
+
+
+def specrouter_sched_observe_step(handle, draft, verifier, gamma, accept_len, tv) -> None:
+    """gamma [B], accept_len [B], tv [B, gamma_max]: the accept call's outputs
+    (device tensors are copied to the host)."""
+    import numpy as np
+
+    g = _host(gamma, np.int32)
+    k = _host(accept_len, np.int32)
+    t = _host(tv, np.float32)
+    if t.ndim != 2 or g.shape != (t.shape[0],) or k.shape != g.shape:
+        raise ValueError("gamma [B], accept_len [B] and tv [B, gamma_max] expected")
+    rc = load().specrouter_sched_observe_step(handle, int(draft), int(verifier), int(t.shape[0]), int(t.shape[1]),
+                                              _as_ptr(g, ctypes.c_int32), _as_ptr(k, ctypes.c_int32),
+                                              _as_ptr(t, ctypes.c_float))
+    _check(rc, "specrouter_sched_observe_step")
+
+
+def specrouter_sched_calibrate(handle):
+    A, B = ctypes.c_double(), ctypes.c_double()
+    _check(load().specrouter_sched_calibrate(handle, ctypes.byref(A), ctypes.byref(B)), "specrouter_sched_calibrate")
+    return A.value, B.value
+
+
+def specrouter_sched_metrics(handle, n_models):
+    """(T [n], SimScore [n, n], (A, B), number of kept observations)."""
+    import numpy as np
+
+    T = np.empty(n_models, np.float64)
+    S = np.empty((n_models, n_models), np.float64)
+    c = np.empty(2, np.float64)
+    n_obs = ctypes.c_int()
+    _check(load().specrouter_sched_metrics(handle, _as_ptr(T, ctypes.c_double), _as_ptr(S, ctypes.c_double),
+                                           _as_ptr(c, ctypes.c_double), ctypes.byref(n_obs)),
+           "specrouter_sched_metrics")
+    return T, S, (float(c[0]), float(c[1])), n_obs.value
+
+
+def specrouter_sched_effective_time(handle, chain) -> float:
+    import numpy as np
+
+    c = _host(chain, np.int32)
+    t = ctypes.c_double()
+    _check(load().specrouter_sched_effective_time(handle, _as_ptr(c, ctypes.c_int32), int(c.shape[0]),
+                                                  ctypes.byref(t)), "specrouter_sched_effective_time")
+    return t.value
+
+
+def specrouter_sched_optimal_chain(handle, n_models):
+    """(chain as a list of model indices, predicted T_eff, number of candidates)."""
+    import numpy as np
+
+    out = np.empty(n_models, np.int32)
+    n, cnt = ctypes.c_int(), ctypes.c_int()
+    t = ctypes.c_double()
+    _check(load().specrouter_sched_optimal_chain(handle, _as_ptr(out, ctypes.c_int32), ctypes.byref(n),
+                                                 ctypes.byref(t), ctypes.byref(cnt)),
+           "specrouter_sched_optimal_chain")
+    return out[:n.value].tolist(), t.value, cnt.value
+
+
+class ChainScheduler:
+    """Owning wrapper of a scheduler handle (Section 4.2, Algorithm 1)."""
+
+    def __init__(self, capability, target, window, max_levels=None, ema_time=0.2, ema_sim=0.1,
+                 prior_weight=1.0):
+        self.n = len(capability)
+        self.handle = specrouter_sched_create(capability, target, window, max_levels, ema_time, ema_sim,
+                                              prior_weight)
+
+    def close(self):
+        if self.handle is not None:
+            specrouter_sched_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def observe_time(self, model, seconds_per_token):
+        specrouter_sched_observe_time(self.handle, model, seconds_per_token)
+
+    def set_similarity(self, draft, verifier, simscore):
+        specrouter_sched_set_similarity(self.handle, draft, verifier, simscore)
+
+    def observe_step(self, draft, verifier, gamma, accept_len, tv):
+        specrouter_sched_observe_step(self.handle, draft, verifier, gamma, accept_len, tv)
+
+    def calibrate(self):
+        return specrouter_sched_calibrate(self.handle)
+
+    def metrics(self):
+        return specrouter_sched_metrics(self.handle, self.n)
+
+    def effective_time(self, chain):
+        return specrouter_sched_effective_time(self.handle, chain)
+
+    def optimal_chain(self):
+        return specrouter_sched_optimal_chain(self.handle, self.n)

@@ -2,8 +2,10 @@
 
 Usage: python -m paper_2505_07680_amd.build [-v]
 
-Compiles every csrc/*.hip translation unit in parallel and links them into
-paper_2505_07680_amd/libspecrouter.so (in-tree, next to the binding).
+Compiles every csrc/*.hip translation unit (device code, hipcc) and every
+csrc/*.cpp translation unit (host-only code, the system C++ compiler) in
+parallel and links them into paper_2505_07680_amd/libspecrouter.so (in-tree,
+next to the binding).
 """
 
 from __future__ import annotations
@@ -35,7 +37,20 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build the HIP library)")
 
 
+def cxx() -> str:
+    for cand in (os.environ.get("CXX"), shutil.which("g++"), shutil.which("c++")):
+        if cand:
+            return cand
+    raise RuntimeError("no host C++ compiler found")
+
+
 def _compile(src: str, obj: str, verbose: bool) -> None:
+    if src.endswith(".cpp"):
+        cmd = [cxx(), "-O2", "-std=c++17", "-fPIC", "-Wall", "-c", "-I", INCLUDE, "-I", CSRC, src, "-o", obj]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"{cmd[0]} failed on {os.path.basename(src)}:\n{r.stderr}")
+        return
     cmd = [
         hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-c",
         "-I", INCLUDE, "-I", CSRC, *DEVICE_FLAGS, src, "-o", obj,
@@ -50,7 +65,7 @@ def _compile(src: str, obj: str, verbose: bool) -> None:
 
 
 def build(verbose: bool = False) -> str:
-    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
     if not srcs:
         raise RuntimeError("no HIP sources found")
     with tempfile.TemporaryDirectory(prefix="srbuild_") as tmp:

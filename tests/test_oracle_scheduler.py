@@ -254,3 +254,14 @@ def test_optimal_chain_special_cases():
     # nothing measured at all: default [M_t] with infinite time
     best, t, _ = sch.optimal_chain(cap, 2, [np.nan] * 3, np.full((3, 3), np.nan), 4, 3)
     assert best == [2] and t == math.inf
+
+
+def test_calibration_gradient_matches_finite_differences():
+    rng = np.random.default_rng(6)
+    obs = [(float(s), int(rng.integers(0, 30)), int(rng.integers(0, 5))) for s in rng.uniform(0.05, 0.98, 25)]
+    for A, B in ((1.0, 0.0), (1.7, -0.3), (0.6, 0.8)):
+        g = sch.calibration_gradient((A, B), obs, 0.7)
+        h = 1e-6
+        fd = [(sch.calibration_objective((A + h, B), obs, 0.7) - sch.calibration_objective((A - h, B), obs, 0.7)) / (2 * h),
+              (sch.calibration_objective((A, B + h), obs, 0.7) - sch.calibration_objective((A, B - h), obs, 0.7)) / (2 * h)]
+        np.testing.assert_allclose(g, fd, rtol=1e-6, atol=1e-6)
