@@ -476,15 +476,15 @@ accept_sweep_kernel(Args A) {
         }
         __builtin_amdgcn_s_sleep(2);
       }
-      __builtin_amdgcn_sched_barrier(0);
-      issue_loads<BF16, E>(A, tn, nxt);
-      __builtin_amdgcn_sched_barrier(0);
       const RowNorm np = row_norm(m1, s1);
       const RowNorm nq = row_norm(m2, s2);
       if (lane == 0) {
         s_f[0] = np.factor(cmp);
         s_f[1] = nq.factor(cmq);
       }
+      __builtin_amdgcn_sched_barrier(0);
+      issue_loads<BF16, E>(A, tn, nxt);
+      __builtin_amdgcn_sched_barrier(0);
     }
     __syncthreads();
     const float fp = s_f[0], fq = s_f[1];
@@ -750,7 +750,7 @@ accept_finish_kernel(Args A) {
       if (mass[i] > 0.0) my_last = lane * nslot + i;
     }
     const double incl = wave_incl_scan(my);
-    const double W = __shfl(incl, 63, 64);
+    const double W = lane_value(incl, 63);
     const double target = (double)A.u_res[(size_t)b * G1 + k] * W;
     // the first chunk with positive mass whose end exceeds the target
     int cs = -1;
@@ -769,14 +769,11 @@ accept_finish_kernel(Args A) {
         }
         run += mass[i];
       }
-      cs = __shfl(found, hl, 64);
-      pre = __shfl(fpre, hl, 64);
+      cs = lane_value(found, hl);
+      pre = lane_value(fpre, hl);
     }
     if (cs < 0) {  // rounding put the target at the very end: the last chunk with mass
-      int last = my_last;
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) last = max(last, __shfl_xor(last, off, 64));
-      cs = max(last, 0);
+      cs = max(wave_max_i(my_last), 0);
       double before = 0.0;
 #pragma unroll
       for (int i = 0; i < kSlots; ++i)
@@ -850,9 +847,7 @@ accept_finish_kernel(Args A) {
           if (wv > 0.f) mine = x0 + e;
         }
         incl = wave_incl_scan(sum);
-        int lmax = mine;
-#pragma unroll
-        for (int off = 32; off > 0; off >>= 1) lmax = max(lmax, __shfl_xor(lmax, off, 64));
+        const int lmax = wave_max_i(mine);
         if (lane == 63) s_wt[w] = incl;
         if (lane == 0) s_last[w] = lmax;
       }

@@ -286,8 +286,7 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
             mt = fmaxf(mt, s[e]);
           }
         }
-        mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
-        mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+        mt = max_across_rows(mt);
         // Lazy rescaling: a row keeps its reference maximum until a tile
         // exceeds it by more than kLazy (log2 units), so P stays below
         // 2^kLazy and the output accumulators are rescaled only then
@@ -302,8 +301,7 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
           pk[e] = mref == kNegInf ? 0.f : (full ? exp2_hw(fmaf(s[e], scale_log2, -mref)) : exp2_hw(s[e] - mref));
           ls += pk[e];
         }
-        ls += __shfl_xor(ls, 16, 64);
-        ls += __shfl_xor(ls, 32, 64);
+        ls = sum_across_rows(ls);
         l_run[qg] = l_run[qg] * alpha + ls;
         m_run[qg] = mref;
         if (__ballot(grow) != 0ull) {

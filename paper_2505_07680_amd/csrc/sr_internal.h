@@ -28,21 +28,128 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, si
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// Wave-wide reductions over the 64 lanes (result valid in every lane).
+// Cross-lane moves without LDS: DPP within each row of 16 lanes, and the
+// gfx950 row swaps across 16- and 32-lane halves.
+namespace dpp {
+constexpr int kXor1 = 0xB1;         // quad_perm [1,0,3,2]: lane i reads lane i^1
+constexpr int kXor2 = 0x4E;         // quad_perm [2,3,0,1]: lane i reads lane i^2
+constexpr int kHalfMirror = 0x141;  // lane i reads lane 7-i within its group of 8
+constexpr int kMirror = 0x140;      // lane i reads lane 15-i within its row of 16
+}  // namespace dpp
+
+template <int C>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, C, 0xf, 0xf, false);
+}
+template <int C>
+__device__ __forceinline__ float dpp_f32(float x) {
+  return __uint_as_float(dpp_u32<C>(__float_as_uint(x)));
+}
+template <int C>
+__device__ __forceinline__ double dpp_f64(double x) {
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  const uint64_t lo = dpp_u32<C>((uint32_t)u), hi = dpp_u32<C>((uint32_t)(u >> 32));
+  return __longlong_as_double((long long)(lo | (hi << 32)));
+}
+
+// (value of the even row, value of the odd row) of each pair of 16-lane rows,
+// in every lane; with kHalf32 the same for the two 32-lane halves.
+template <bool kHalf32>
+__device__ __forceinline__ void swap_halves(uint32_t x, uint32_t& even, uint32_t& odd) {
+  const auto r = kHalf32 ? __builtin_amdgcn_permlane32_swap(x, x, false, false)
+                         : __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  even = r[0];
+  odd = r[1];
+}
+template <bool kHalf32>
+__device__ __forceinline__ void swap_halves_f32(float x, float& even, float& odd) {
+  uint32_t e, o;
+  swap_halves<kHalf32>(__float_as_uint(x), e, o);
+  even = __uint_as_float(e);
+  odd = __uint_as_float(o);
+}
+template <bool kHalf32>
+__device__ __forceinline__ void swap_halves_f64(double x, double& even, double& odd) {
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  uint32_t el, ol, eh, oh;
+  swap_halves<kHalf32>((uint32_t)u, el, ol);
+  swap_halves<kHalf32>((uint32_t)(u >> 32), eh, oh);
+  even = __longlong_as_double((long long)((uint64_t)el | ((uint64_t)eh << 32)));
+  odd = __longlong_as_double((long long)((uint64_t)ol | ((uint64_t)oh << 32)));
+}
+
+// Wave-wide reductions over the 64 lanes, bit-identical in every lane: a fixed
+// tree (pairs, quads, groups of 8, rows of 16, then the row pairs and halves,
+// the lower part always on the left).
 __device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) x = fmaxf(x, __shfl_xor(x, off, 64));
-  return x;
+  x = fmaxf(x, dpp_f32<dpp::kXor1>(x));
+  x = fmaxf(x, dpp_f32<dpp::kXor2>(x));
+  x = fmaxf(x, dpp_f32<dpp::kHalfMirror>(x));
+  x = fmaxf(x, dpp_f32<dpp::kMirror>(x));
+  float e, o;
+  swap_halves_f32<false>(x, e, o);
+  x = fmaxf(e, o);
+  swap_halves_f32<true>(x, e, o);
+  return fmaxf(e, o);
 }
 __device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
-  return x;
+  x = x + dpp_f32<dpp::kXor1>(x);
+  x = x + dpp_f32<dpp::kXor2>(x);
+  x = x + dpp_f32<dpp::kHalfMirror>(x);
+  x = x + dpp_f32<dpp::kMirror>(x);
+  float e, o;
+  swap_halves_f32<false>(x, e, o);
+  x = e + o;
+  swap_halves_f32<true>(x, e, o);
+  return e + o;
 }
 __device__ __forceinline__ double wave_sum_d(double x) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
-  return x;
+  x = x + dpp_f64<dpp::kXor1>(x);
+  x = x + dpp_f64<dpp::kXor2>(x);
+  x = x + dpp_f64<dpp::kHalfMirror>(x);
+  x = x + dpp_f64<dpp::kMirror>(x);
+  double e, o;
+  swap_halves_f64<false>(x, e, o);
+  x = e + o;
+  swap_halves_f64<true>(x, e, o);
+  return e + o;
+}
+__device__ __forceinline__ int wave_max_i(int x) {
+  x = max(x, (int)dpp_u32<dpp::kXor1>((uint32_t)x));
+  x = max(x, (int)dpp_u32<dpp::kXor2>((uint32_t)x));
+  x = max(x, (int)dpp_u32<dpp::kHalfMirror>((uint32_t)x));
+  x = max(x, (int)dpp_u32<dpp::kMirror>((uint32_t)x));
+  uint32_t e, o;
+  swap_halves<false>((uint32_t)x, e, o);
+  x = max((int)e, (int)o);
+  swap_halves<true>((uint32_t)x, e, o);
+  return max((int)e, (int)o);
+}
+
+// Reductions over the four 16-lane rows only (lanes i, i^16, i^32, i^48),
+// as ((row 0, row 1), (row 2, row 3)) in every lane.
+__device__ __forceinline__ float max_across_rows(float x) {
+  float e, o;
+  swap_halves_f32<false>(x, e, o);
+  x = fmaxf(e, o);
+  swap_halves_f32<true>(x, e, o);
+  return fmaxf(e, o);
+}
+__device__ __forceinline__ float sum_across_rows(float x) {
+  float e, o;
+  swap_halves_f32<false>(x, e, o);
+  x = e + o;
+  swap_halves_f32<true>(x, e, o);
+  return e + o;
+}
+
+// The value of lane `src` (wave-uniform) in every lane.
+__device__ __forceinline__ int lane_value(int x, int src) { return __builtin_amdgcn_readlane(x, src); }
+__device__ __forceinline__ double lane_value(double x, int src) {
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, src);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), src);
+  return __longlong_as_double((long long)((uint64_t)lo | ((uint64_t)hi << 32)));
 }
 
 // Merge two (max, sum-of-exp2(x*log2e - max*log2e)) partials.
