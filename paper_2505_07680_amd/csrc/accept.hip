@@ -157,6 +157,7 @@ struct Args {
   int B, gmax, V, nc;
   u32x4* stats;     // [B][gmax+1][nc] records, two 16-byte halves each
   double* tvabs;    // [B][gmax+1][nc] sum |P - Q| per chunk (pair rows)
+  float* xlogit;    // [B][gmax+1][2] the draft token's p and q logits (pair rows)
   int32_t* status;
 };
 
@@ -273,6 +274,7 @@ struct Raw<true, E> {
 
 struct TaskInfo {
   int b, j, c, row;
+  int x;  // the row's draft token (pair rows; -1 for a bonus row)
   bool pair;
   const char* prow;
   const char* qrow;  // the p row itself for a bonus row (its loads then hit cached lines)
@@ -297,6 +299,7 @@ __device__ __forceinline__ TaskInfo decode_task(const Args& A, const int* rows, 
   const size_t esz = BF16 ? 2 : 4;
   t.prow = (const char*)A.p + ((size_t)t.b * A.p_stride + (size_t)t.j * A.V) * esz;
   t.qrow = t.pair ? (const char*)A.q + ((size_t)t.b * A.q_stride + (size_t)t.j * A.V) * esz : t.prow;
+  t.x = t.pair ? A.drafts[(size_t)t.b * A.gmax + t.j] : -1;  // uniform: a scalar load
   return t;
 }
 
@@ -332,32 +335,47 @@ __device__ __forceinline__ void issue_loads(const Args& A, const TaskInfo& t, Ra
   }
 }
 
+// Workgroup state of the sweep and its two passes over a task.
+struct SweepShared {
+  float m[2][kWaves];
+  double s[3][kWaves];
+  float f[2];  // this chunk's factors f_c for p and q
+};
+
 template <bool BF16, int E>
-__global__ void __launch_bounds__(kThreads)
-accept_sweep_kernel(Args A) {
-  constexpr int VEC = Elt<BF16>::VEC;
-  constexpr int kChunk = kThreads * E;
-  extern __shared__ int s_rows[];  // [B] inclusive prefix of live rows
-  __shared__ float s_m[2][kWaves];
-  __shared__ double s_s[3][kWaves];
-  __shared__ float s_f[2];  // this chunk's factors f_c for p and q
+struct Sweep {
+  static constexpr int VEC = Elt<BF16>::VEC;
+  static constexpr int kChunk = kThreads * E;
+  const Args& A;
+  SweepShared& sh;
+  const int tid, lane, w, nc, nslot;
+  const __amdgpu_buffer_rsrc_t rs_stats;
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int w = tid >> 6;
-  const int nc = A.nc;
-  const int nslot = (nc + 63) / 64;
-  const size_t n_rec = (size_t)A.B * (A.gmax + 1) * nc;
-  const __amdgpu_buffer_rsrc_t rs_stats = make_rsrc(A.stats, n_rec * kRecBytes);
-
-  build_row_table(A.gamma, A.gmax, A.B, s_rows);
-  const long n_tasks = (long)s_rows[A.B - 1] * nc;
+  __device__ Sweep(const Args& a, SweepShared& s)
+      : A(a), sh(s), tid(threadIdx.x), lane(threadIdx.x & 63), w(threadIdx.x >> 6), nc(a.nc),
+        nslot((a.nc + 63) / 64),
+        rs_stats(make_rsrc(a.stats, (size_t)a.B * (a.gmax + 1) * a.nc * kRecBytes)) {}
 
   // First pass over a task's entries: chunk maxima, exponentials, sums, KL
   // numerator, and the published record. Leaves the chunk maxima in cmp/cmq
   // (and, for fp32, the exponentials in r).
-  auto first_pass = [&](const TaskInfo& t, Raw<BF16, E>& r, float& cmp, float& cmq) __attribute__((always_inline)) {
+  __device__ __forceinline__ void first_pass(const TaskInfo& t, Raw<BF16, E>& r, float& cmp, float& cmq) {
     const int base = t.c * kChunk + w * (64 * E);
+    // The draft token's two logits, for the finish kernel's acceptance test:
+    // the lane that holds entry x stores them (once per row).
+    const int xo = t.x - base;  // offset of x in this wave's entries
+    if (xo >= 0 && xo < 64 * E && lane == (xo % (64 * VEC)) / VEC) {
+      const int ex = (xo / (64 * VEC)) * VEC + xo % VEC;
+      float zp = 0.f, zq = 0.f;
+#pragma unroll
+      for (int e = 0; e < E; ++e)
+        if (e == ex) {
+          zp = r.gp(e);
+          zq = r.gq(e);
+        }
+      A.xlogit[(size_t)t.row * 2] = zp;
+      A.xlogit[(size_t)t.row * 2 + 1] = zq;
+    }
     auto in_v = [&](int e) __attribute__((always_inline)) {  // entry e lies below V
       return base + ((e / VEC) * 64 + lane) * VEC < A.V;
     };
@@ -373,12 +391,12 @@ accept_sweep_kernel(Args A) {
     mp = wave_max(mp);
     if (t.pair) mq = wave_max(mq);
     if (lane == 0) {
-      s_m[0][w] = mp;
-      s_m[1][w] = mq;
+      sh.m[0][w] = mp;
+      sh.m[1][w] = mq;
     }
     __syncthreads();
-    cmp = max_waves(s_m[0]);
-    cmq = max_waves(s_m[1]);
+    cmp = max_waves(sh.m[0]);
+    cmq = max_waves(sh.m[1]);
 
     // exponentials, sums, KL numerator; groups of four are summed as
     // (a0 + a1) + (a2 + a3), then a tree over groups
@@ -426,9 +444,9 @@ accept_sweep_kernel(Args A) {
       dsp = wave_sum_d((double)tree_sum(gp));
     }
     if (lane == 0) {
-      s_s[0][w] = dsp;
-      s_s[1][w] = dsq;
-      s_s[2][w] = dkl;
+      sh.s[0][w] = dsp;
+      sh.s[1][w] = dsq;
+      sh.s[2][w] = dkl;
     }
     __syncthreads();
     if (tid == 0) {
@@ -436,58 +454,58 @@ accept_sweep_kernel(Args A) {
       StatRec sr;
       sr.mp = cmp;
       sr.mq = cmq;
-      sr.sp = sum_waves(s_s[0]);
-      sr.sq = sum_waves(s_s[1]);
-      sr.kl = sum_waves(s_s[2]);
+      sr.sp = sum_waves(sh.s[0]);
+      sr.sq = sum_waves(sh.s[1]);
+      sr.kl = sum_waves(sh.s[2]);
       u32x4 w0, w1;
       pack_rec(sr, w0, w1);
       __builtin_amdgcn_raw_buffer_store_b128(w0, rs_stats, (uint32_t)(rec * kRecBytes), 0, kDeviceCoherent);
       __builtin_amdgcn_raw_buffer_store_b128(w1, rs_stats, (uint32_t)(rec * kRecBytes + 16), 0, kDeviceCoherent);
     }
-  };
+  }
 
-  // Second pass of a pair row's task: wait for every chunk record of the row,
-  // then sum |P - Q| over the entries kept from the first pass.
-  auto second_pass = [&](const TaskInfo& t, const Raw<BF16, E>& r, float cmp, float cmq, const TaskInfo& tn,
-                         Raw<BF16, E>& nxt) __attribute__((always_inline)) {
-    if (w == 0) {
-      float m1[kSlots], m2[kSlots];
-      double s1[kSlots], s2[kSlots];
-      for (uint32_t it = 0;; ++it) {
-        bool ok = true;
+  // One wave: re-load the records of a pair row until all of them are
+  // present, merge them into the row's normalisers and leave the chunk's
+  // factors in sh.f (lane 0 writes them).
+  __device__ __forceinline__ void row_factors(const TaskInfo& t, float cmp, float cmq) {
+    float m1[kSlots], m2[kSlots];
+    double s1[kSlots], s2[kSlots];
+    for (uint32_t it = 0;; ++it) {
+      bool ok = true;
 #pragma unroll
-        for (int i = 0; i < kSlots; ++i) {
-          const int cc = lane * nslot + i;
-          const bool in = i < nslot && cc < nc;
-          const uint32_t off = (uint32_t)(((size_t)t.row * nc + (in ? cc : 0)) * kRecBytes);
-          const u32x4 w0 = __builtin_amdgcn_raw_buffer_load_b128(rs_stats, off, 0, kDeviceCoherent);
-          const u32x4 w1 = __builtin_amdgcn_raw_buffer_load_b128(rs_stats, off + 16, 0, kDeviceCoherent);
-          ok = ok && (!in || rec_present(w0, w1));
-          const StatRec sr = unpack_rec(w0, w1);
-          m1[i] = in ? sr.mp : kNegInf;
-          m2[i] = in ? sr.mq : kNegInf;
-          s1[i] = in ? sr.sp : 0.0;
-          s2[i] = in ? sr.sq : 0.0;
-        }
-        if (__ballot(!ok) == 0ull) break;
-        if (it == kSpinLimit) {
-          if (lane == 0 && A.status) atomicOr(A.status, SR_ST_TIMEOUT);
-          break;
-        }
-        __builtin_amdgcn_s_sleep(2);
+      for (int i = 0; i < kSlots; ++i) {
+        const int cc = lane * nslot + i;
+        const bool in = i < nslot && cc < nc;
+        const uint32_t off = (uint32_t)(((size_t)t.row * nc + (in ? cc : 0)) * kRecBytes);
+        const u32x4 w0 = __builtin_amdgcn_raw_buffer_load_b128(rs_stats, off, 0, kDeviceCoherent);
+        const u32x4 w1 = __builtin_amdgcn_raw_buffer_load_b128(rs_stats, off + 16, 0, kDeviceCoherent);
+        ok = ok && (!in || rec_present(w0, w1));
+        const StatRec sr = unpack_rec(w0, w1);
+        m1[i] = in ? sr.mp : kNegInf;
+        m2[i] = in ? sr.mq : kNegInf;
+        s1[i] = in ? sr.sp : 0.0;
+        s2[i] = in ? sr.sq : 0.0;
       }
-      const RowNorm np = row_norm(m1, s1);
-      const RowNorm nq = row_norm(m2, s2);
-      if (lane == 0) {
-        s_f[0] = np.factor(cmp);
-        s_f[1] = nq.factor(cmq);
+      if (__ballot(!ok) == 0ull) break;
+      if (it == kSpinLimit) {
+        if (lane == 0 && A.status) atomicOr(A.status, SR_ST_TIMEOUT);
+        break;
       }
-      __builtin_amdgcn_sched_barrier(0);
-      issue_loads<BF16, E>(A, tn, nxt);
-      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_sleep(2);
     }
-    __syncthreads();
-    const float fp = s_f[0], fq = s_f[1];
+    const RowNorm np = row_norm(m1, s1);
+    const RowNorm nq = row_norm(m2, s2);
+    if (lane == 0) {
+      sh.f[0] = np.factor(cmp);
+      sh.f[1] = nq.factor(cmq);
+    }
+  }
+
+  // Every wave, after a barrier that follows row_factors: sum |P - Q| over the
+  // entries kept from the first pass; the chunk's sum is stored for the finish
+  // kernel.
+  __device__ __forceinline__ void tv_pass(const TaskInfo& t, const Raw<BF16, E>& r, float cmp, float cmq) {
+    const float fp = sh.f[0], fq = sh.f[1];
     const float rp = cmp == kNegInf ? 0.f : cmp * kLog2e;
     const float rq = cmq == kNegInf ? 0.f : cmq * kLog2e;
     const int base = t.c * kChunk + w * (64 * E);
@@ -518,10 +536,23 @@ accept_sweep_kernel(Args A) {
       __builtin_amdgcn_sched_barrier(0);
     }
     const double dtv = wave_sum_d((double)tree_sum(ga));
-    if (lane == 0) s_s[0][w] = dtv;
+    if (lane == 0) sh.s[0][w] = dtv;
     __syncthreads();
-    if (tid == 0) A.tvabs[(size_t)t.row * nc + t.c] = sum_waves(s_s[0]);
-  };
+    if (tid == 0) A.tvabs[(size_t)t.row * nc + t.c] = sum_waves(sh.s[0]);
+  }
+};
+
+// Persistent sweep: workgroup w takes tasks w, w + G, w + 2G, ... two deep.
+template <bool BF16, int E>
+__global__ void __launch_bounds__(kThreads)
+accept_sweep_kernel(Args A) {
+  extern __shared__ int s_rows[];  // [B] inclusive prefix of live rows
+  __shared__ SweepShared sh;
+  Sweep<BF16, E> S(A, sh);
+  const int w = S.w;
+
+  build_row_table(A.gamma, A.gmax, A.B, s_rows);
+  const long n_tasks = (long)s_rows[A.B - 1] * S.nc;
 
   // Pipeline: the second pass of task i runs after the loads of task i+1 are
   // issued and before its first pass, so the other chunks of task i's row have
@@ -533,7 +564,7 @@ accept_sweep_kernel(Args A) {
   Raw<BF16, E> cur;
   issue_loads<BF16, E>(A, t, cur);
   float cmp, cmq;
-  first_pass(t, cur, cmp, cmq);
+  S.first_pass(t, cur, cmp, cmq);
   for (;;) {
     const long task_n = task + gridDim.x;
     const bool more = task_n < n_tasks;
@@ -545,10 +576,19 @@ accept_sweep_kernel(Args A) {
     __builtin_amdgcn_sched_barrier(0);
     if (w != 0 || !t.pair) issue_loads<BF16, E>(A, tn, nxt);
     __builtin_amdgcn_sched_barrier(0);
-    if (t.pair) second_pass(t, cur, cmp, cmq, tn, nxt);  // workgroup-uniform
+    if (t.pair) {  // workgroup-uniform
+      if (w == 0) {
+        S.row_factors(t, cmp, cmq);
+        __builtin_amdgcn_sched_barrier(0);
+        issue_loads<BF16, E>(A, tn, nxt);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      __syncthreads();
+      S.tv_pass(t, cur, cmp, cmq);
+    }
     if (!more) break;
     float cmp_n, cmq_n;
-    first_pass(tn, nxt, cmp_n, cmq_n);
+    S.first_pass(tn, nxt, cmp_n, cmq_n);
     task = task_n;
     t = tn;
     cur = nxt;
@@ -587,15 +627,17 @@ __device__ void clear_records(const Args& A, int b, int gam) {
   for (size_t i = threadIdx.x & 63; i < n; i += 64) A.stats[first + i] = u32x4{0u, 0u, 0u, 0u};
 }
 
-// Wave-wide inclusive prefix sum (fp64).
+// Wave-wide inclusive prefix sum (fp64) in ascending lane order: DPP row
+// shifts inside each 16-lane row, then the totals of the earlier rows.
 __device__ __forceinline__ double wave_incl_scan(double x) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const double y = __shfl_up(x, off, 64);
-    if (lane >= off) x += y;
-  }
-  return x;
+  x = x + dpp_f64<0x111>(x);  // row_shr:1 (lanes without a source read 0)
+  x = x + dpp_f64<0x112>(x);  // row_shr:2
+  x = x + dpp_f64<0x114>(x);  // row_shr:4
+  x = x + dpp_f64<0x118>(x);  // row_shr:8
+  const double r0 = lane_value(x, 15), r1 = lane_value(x, 31), r2 = lane_value(x, 47);
+  const int row = (threadIdx.x & 63) >> 4;
+  const double r01 = r0 + r1;
+  return x + (row == 0 ? 0.0 : row == 1 ? r0 : row == 2 ? r01 : r01 + r2);
 }
 
 struct RowRes {
@@ -627,10 +669,26 @@ __device__ __forceinline__ void load_row(const Args& A, int row, bool pair, RowR
   }
 }
 
+// What the accept chain and the draw need of one row, kept in LDS by the
+// wave that merged the row: the chunks' masses (p, and the residual
+// max(0, p - q) for a pair row) and maxima, and the row's normalisers.
+struct FinishShared {
+  double mass[kMaxRows][2][kMaxChunks];  // [row][p, residual][chunk]
+  float cmax[kMaxRows][2][kMaxChunks];   // [row][p, q][chunk] chunk maxima
+  float norm[kMaxRows][4];               // M_p, 1/S_p, M_q, 1/S_q
+  int resid[kMaxRows];                   // the residual has positive mass
+  RowRes rr[kMaxRows];
+  int x[kMaxRows];
+  float uacc[kMaxRows], ures[kMaxRows];
+};
+
 // Finish kernel: one workgroup per sequence with at least four waves.
-//   rows:  one wave per pair row j merges the row's records (the draft
-//          token's two logits are loaded alongside) into a_j, p(x), q(x),
-//          TV_j and KL_j;
+//   load:  every thread loads its position's draft and uniforms together
+//          with gamma (one round trip);
+//   rows:  one wave per live row j <= gamma merges the row's records (the
+//          draft token's two logits are loaded alongside) into a_j, p(x),
+//          q(x), TV_j and KL_j, and leaves the row's chunk masses, maxima
+//          and normalisers in LDS;
 //   chain: wave 0 finds the stopping row k and, from k's chunk masses, the
 //          chunk that holds u*W and the offset of u*W inside it;
 //   draw:  waves 0-3 re-read that chunk (each thread a contiguous run of
@@ -641,8 +699,7 @@ __global__ void __launch_bounds__(1024)
 accept_finish_kernel(Args A) {
   constexpr int VEC = Elt<BF16>::VEC;
   constexpr int kChunk = kThreads * E;
-  constexpr int kPerT = kChunk / 256;  // entries per thread in the draw
-  __shared__ RowRes rr[kMaxRows];
+  __shared__ FinishShared F;
   __shared__ uint32_t s_bad;
   __shared__ int s_k, s_cs, s_resid, s_hit[4], s_last[4], s_tok;
   __shared__ double s_rem, s_wt[4];
@@ -653,41 +710,104 @@ accept_finish_kernel(Args A) {
   const int w = tid >> 6;
   const int nw = blockDim.x >> 6;
   const int G1 = A.gmax + 1;
+  const int nslot = (A.nc + 63) / 64;
+  // ---- load: gamma and the per-position inputs in one round trip
   const int gam = A.gamma[b];
+  if (tid == 0) s_bad = 0;
+  if (tid < G1) {
+    const int j = tid;
+    const int x = j < A.gmax ? A.drafts[(size_t)b * A.gmax + j] : -1;
+    const float ua = j < A.gmax ? A.u_acc[(size_t)b * A.gmax + j] : 0.f;
+    const float ur = A.u_res[(size_t)b * G1 + j];
+    F.x[j] = x;
+    F.uacc[j] = ua;
+    F.ures[j] = ur;
+  }
+  const int kvl = A.kv_len ? A.kv_len[b] : 0;
+  // row w's records and draft logits, in the same round trip (pair or bonus
+  // row is decided once gamma has arrived)
+  RowRecs R0;
+  float zx0[2] = {0.f, 0.f};
+  if (w <= A.gmax) {
+    load_row(A, b * G1 + w, true, R0);
+    if (w < A.gmax) {
+      zx0[0] = A.xlogit[((size_t)b * G1 + w) * 2];
+      zx0[1] = A.xlogit[((size_t)b * G1 + w) * 2 + 1];
+    }
+  }
   if (gam < 0 || gam > A.gmax) {
     if (w == 0) write_invalid(A, b, SR_ST_GAMMA);
     return;  // the sweep touched no row of this sequence
   }
-  if (tid == 0) s_bad = 0;
   __syncthreads();
   // ---- data checks
-  uint32_t bad = 0;
-  for (int j = tid; j <= gam; j += blockDim.x) {
+  if (tid <= gam) {
+    uint32_t bad = 0;
+    const int j = tid;
     if (j < gam) {
-      const int x = A.drafts[(size_t)b * A.gmax + j];
+      const int x = F.x[j];
       if (x < 0 || x >= A.V) bad |= SR_ST_TOKEN;
-      const float u = A.u_acc[(size_t)b * A.gmax + j];
+      const float u = F.uacc[j];
       if (!(u >= 0.f && u < 1.f)) bad |= SR_ST_UNIFORM;
     }
-    const float u = A.u_res[(size_t)b * G1 + j];
+    const float u = F.ures[j];
     if (!(u >= 0.f && u < 1.f)) bad |= SR_ST_UNIFORM;
+    if (j == 0 && A.kv_len && kvl < gam + 1) bad |= SR_ST_KVLEN;
+    if (bad) atomicOr(&s_bad, bad);
   }
-  if (tid == 0 && A.kv_len && A.kv_len[b] < gam + 1) bad |= SR_ST_KVLEN;
-  if (bad) atomicOr(&s_bad, bad);
-  // ---- per-row results (one wave per pair row)
+  // ---- rows (one wave per live row)
   const size_t esz = BF16 ? 2 : 4;
-  for (int j = w; j < gam; j += nw) {
-    const int x = A.drafts[(size_t)b * A.gmax + j];
+  for (int j = w; j <= gam; j += nw) {
+    const bool pair = j < gam;
+    const int x = pair ? F.x[j] : -1;
     const bool xin = x >= 0 && x < A.V;
-    float zpx = 0.f, zqx = 0.f;
-    if (lane == 0 && xin) {  // issued with the record loads below
-      zpx = Elt<BF16>::one((const char*)A.p + ((size_t)b * A.p_stride + (size_t)j * A.V) * esz, x);
-      zqx = Elt<BF16>::one((const char*)A.q + ((size_t)b * A.q_stride + (size_t)j * A.V) * esz, x);
-    }
     RowRecs R;
-    load_row(A, b * G1 + j, true, R);
+    float zpx, zqx;
+    if (j == w) {
+      R = R0;
+      zpx = zx0[0];
+      zqx = zx0[1];
+    } else {  // a second row for this wave (gamma_max + 1 > waves)
+      load_row(A, b * G1 + j, true, R);
+      zpx = A.xlogit[((size_t)b * G1 + j) * 2];
+      zqx = A.xlogit[((size_t)b * G1 + j) * 2 + 1];
+    }
+    if (!pair) {  // the bonus row: p only
+#pragma unroll
+      for (int i = 0; i < kSlots; ++i) {
+        R.mq[i] = kNegInf;
+        R.sq[i] = 0.0;
+        R.kl[i] = 0.0;
+        R.ta[i] = 0.0;
+      }
+    }
     const RowNorm np = row_norm(R.mp, R.sp);
     const RowNorm nq = row_norm(R.mq, R.sq);
+    // chunk masses with the same factors the sweep's sum |P - Q| used
+    double my_res = 0.0;
+#pragma unroll
+    for (int i = 0; i < kSlots; ++i) {
+      const int cc = lane * nslot + i;
+      const double pm = R.sp[i] * (double)np.factor(R.mp[i]);
+      const double qm = R.sq[i] * (double)nq.factor(R.mq[i]);
+      const double rm = pair ? fmax(0.0, 0.5 * (R.ta[i] + pm - qm)) : 0.0;
+      my_res += rm;
+      if (i < nslot && cc < A.nc) {
+        F.mass[j][0][cc] = pm;
+        F.mass[j][1][cc] = rm;
+        F.cmax[j][0][cc] = R.mp[i];
+        F.cmax[j][1][cc] = R.mq[i];
+      }
+    }
+    const bool residual = pair && wave_sum_d(my_res) > 0.0;
+    if (lane == 0) {
+      F.norm[j][0] = np.M;
+      F.norm[j][1] = np.invS;
+      F.norm[j][2] = nq.M;
+      F.norm[j][3] = nq.invS;
+      F.resid[j] = residual ? 1 : 0;
+    }
+    if (!pair) continue;  // the bonus row needs no divergences
     const double Lp = np.log_norm(), Lq = nq.log_norm();
     double tvd = 0.0, kld = 0.0;
 #pragma unroll
@@ -697,16 +817,17 @@ accept_finish_kernel(Args A) {
     }
     tvd = 0.5 * wave_sum_d(tvd);
     kld = wave_sum_d(kld) - (Lp - Lq);
+    // p(x), q(x) and a = min(1, p(x)/q(x)): one exponential per lane (0-2)
+    const double lpx = (double)zpx - Lp;
+    const double lqx = (double)zqx - Lq;
+    const double arg = lane == 0 ? lpx : (lane == 1 ? lqx : lpx - lqx);
+    const double ex = exp(arg);
+    const double pt = lane_value(ex, 0), qt = lane_value(ex, 1), rt = lane_value(ex, 2);
     if (lane == 0) {
-      double a = __builtin_nan(""), pt = __builtin_nan(""), qt = __builtin_nan("");
-      if (xin) {
-        const double lpx = (double)zpx - Lp;
-        const double lqx = (double)zqx - Lq;
-        pt = exp(lpx);
-        qt = exp(lqx);
-        a = (lqx == -INFINITY || lpx >= lqx) ? 1.0 : exp(lpx - lqx);
-      }
-      rr[j] = RowRes{a, (float)pt, (float)qt, (float)kld, (float)tvd};
+      double a = __builtin_nan("");
+      if (xin) a = (lqx == -INFINITY || lpx >= lqx) ? 1.0 : rt;
+      F.rr[j] = RowRes{a, xin ? (float)pt : __builtin_nanf(""), xin ? (float)qt : __builtin_nanf(""), (float)kld,
+                       (float)tvd};
     }
   }
   __syncthreads();
@@ -720,38 +841,24 @@ accept_finish_kernel(Args A) {
   // ---- accept chain and the chunk of the draw (wave 0)
   if (w == 0) {
     bool rej = false;
-    if (lane < gam) rej = !((double)A.u_acc[(size_t)b * A.gmax + lane] < rr[lane].a);
+    if (lane < gam) rej = !((double)F.uacc[lane] < F.rr[lane].a);
     const unsigned long long rmask = __ballot(rej);
     const int k = rmask ? (__ffsll((long long)rmask) - 1) : gam;
-    const bool pair = k < gam;
-    const int nslot = (A.nc + 63) / 64;
-    RowRecs R;
-    load_row(A, b * G1 + k, pair, R);
-    const RowNorm np = row_norm(R.mp, R.sp);
-    const RowNorm nq = row_norm(R.mq, R.sq);
-    double pm[kSlots], rm[kSlots];
-    double my_res = 0.0;
-#pragma unroll
-    for (int i = 0; i < kSlots; ++i) {
-      // chunk masses with the same factors the sweep's sum |P - Q| used
-      pm[i] = R.sp[i] * (double)np.factor(R.mp[i]);
-      const double qm = R.sq[i] * (double)nq.factor(R.mq[i]);
-      rm[i] = pair ? fmax(0.0, 0.5 * (R.ta[i] + pm[i] - qm)) : 0.0;
-      my_res += rm[i];
-    }
-    const bool residual = pair && wave_sum_d(my_res) > 0.0;
+    const bool residual = F.resid[k] != 0;
     double mass[kSlots];
     double my = 0.0;
     int my_last = -1;
 #pragma unroll
     for (int i = 0; i < kSlots; ++i) {
-      mass[i] = residual ? rm[i] : pm[i];
+      const int cc = lane * nslot + i;
+      const bool in = i < nslot && cc < A.nc;
+      mass[i] = in ? F.mass[k][residual ? 1 : 0][cc] : 0.0;
       my += mass[i];
-      if (mass[i] > 0.0) my_last = lane * nslot + i;
+      if (mass[i] > 0.0) my_last = cc;
     }
     const double incl = wave_incl_scan(my);
     const double W = lane_value(incl, 63);
-    const double target = (double)A.u_res[(size_t)b * G1 + k] * W;
+    const double target = (double)F.ures[k] * W;
     // the first chunk with positive mass whose end exceeds the target
     int cs = -1;
     double pre = 0.0;
@@ -780,16 +887,16 @@ accept_finish_kernel(Args A) {
         if (lane * nslot + i < cs) before += mass[i];
       pre = wave_sum_d(before);
     }
-    float cmp = kNegInf, cmq = kNegInf;  // the chunk's maxima, as the sweep used them
-#pragma unroll
-    for (int i = 0; i < kSlots; ++i)
-      if (lane * nslot + i == cs) {
-        cmp = R.mp[i];
-        cmq = R.mq[i];
-      }
-    cmp = wave_max(cmp);
-    cmq = wave_max(cmq);
     if (lane == 0) {
+      // the chunk's maxima and factors, as the sweep used them
+      const bool pair = k < gam;
+      const float cmp = F.cmax[k][0][cs];
+      const float cmq = pair ? F.cmax[k][1][cs] : kNegInf;
+      RowNorm np, nq;
+      np.M = F.norm[k][0];
+      np.invS = F.norm[k][1];
+      nq.M = pair ? F.norm[k][2] : kNegInf;
+      nq.invS = pair ? F.norm[k][3] : 0.f;
       s_k = k;
       s_cs = cs;
       s_resid = residual ? 1 : 0;
@@ -894,20 +1001,20 @@ accept_finish_kernel(Args A) {
   clear_records(A, b, gam);  // every read of them is done
   // ---- outputs
   int32_t* ot = A.out_tokens + (size_t)b * G1;
-  for (int j = lane; j <= A.gmax; j += 64) ot[j] = j < k ? A.drafts[(size_t)b * A.gmax + j] : (j == k ? tok : -1);
+  for (int j = lane; j <= A.gmax; j += 64) ot[j] = j < k ? F.x[j] : (j == k ? tok : -1);
   const float nan = __builtin_nanf("");
   for (int j = lane; j < A.gmax; j += 64) {
     const size_t o = (size_t)b * A.gmax + j;
     const bool live = j < gam;
-    if (A.accept_prob) A.accept_prob[o] = live ? (float)rr[j].a : nan;
-    if (A.p_tok) A.p_tok[o] = live ? rr[j].p_tok : nan;
-    if (A.q_tok) A.q_tok[o] = live ? rr[j].q_tok : nan;
-    if (A.kl) A.kl[o] = live ? rr[j].kl : nan;
-    if (A.tv) A.tv[o] = live ? rr[j].tv : nan;
+    if (A.accept_prob) A.accept_prob[o] = live ? (float)F.rr[j].a : nan;
+    if (A.p_tok) A.p_tok[o] = live ? F.rr[j].p_tok : nan;
+    if (A.q_tok) A.q_tok[o] = live ? F.rr[j].q_tok : nan;
+    if (A.kl) A.kl[o] = live ? F.rr[j].kl : nan;
+    if (A.tv) A.tv[o] = live ? F.rr[j].tv : nan;
   }
   if (lane == 0) {
     A.accept_len[b] = k;
-    if (A.new_len) A.new_len[b] = A.kv_len[b] - gam + k;
+    if (A.new_len) A.new_len[b] = kvl - gam + k;
   }
 }
 
@@ -918,7 +1025,7 @@ constexpr int kEbf16 = 32;
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 struct Layout {
-  size_t stats, tvabs, total;
+  size_t stats, tvabs, xlogit, total;
 };
 
 Layout layout(int B, int gamma_max, int n_chunks) {
@@ -926,13 +1033,21 @@ Layout layout(int B, int gamma_max, int n_chunks) {
   Layout L;
   L.stats = 0;
   L.tvabs = align256(rows * n_chunks * kRecBytes);
-  L.total = L.tvabs + align256(rows * n_chunks * sizeof(double));
+  L.xlogit = L.tvabs + align256(rows * n_chunks * sizeof(double));
+  L.total = L.xlogit + align256(rows * 2 * sizeof(float));
   return L;
 }
 
 template <bool BF16>
 const void* sweep_fn() {
   return (const void*)accept_sweep_kernel<BF16, BF16 ? kEbf16 : kEf32>;
+}
+
+int resident_per_cu(const void* fn, size_t lds) {
+  int per_cu = 1;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kThreads, lds) != hipSuccess || per_cu < 1)
+    per_cu = 1;
+  return per_cu;
 }
 
 }  // namespace
@@ -945,18 +1060,14 @@ int accept_plan(int B, int gamma_max, int V, int dtype, AcceptPlan* plan) {
   const int Bl = B < kMaxSeqs ? B : kMaxSeqs;
   if ((size_t)Bl * (gamma_max + 1) * plan->n_chunks * kRecBytes >= 0x7fffffffu) return SR_EUNSUPPORTED;
   plan->workspace_bytes = layout(B, gamma_max, plan->n_chunks).total;
-  // persistent grid: every workgroup resident at once, a multiple of the
-  // chunks per row, and no more than the largest possible task count
   const int cus = device_cu_count();
   if (cus <= 0) return SR_ELAUNCH;
-  int per_cu = 1;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, bf16 ? sweep_fn<true>() : sweep_fn<false>(),
-                                                   kThreads, Bl * sizeof(int)) != hipSuccess || per_cu < 1)
-    per_cu = 1;
-  const long cap = (long)cus * per_cu;
+  const long max_tasks = (long)Bl * (gamma_max + 1) * plan->n_chunks;
+  // persistent grid: every workgroup resident at once, a multiple of the
+  // chunks per row, and no more than the largest possible task count
+  const long cap = (long)cus * resident_per_cu(bf16 ? sweep_fn<true>() : sweep_fn<false>(), Bl * sizeof(int));
   long grid = cap / plan->n_chunks * plan->n_chunks;
   if (grid == 0) grid = cap;
-  const long max_tasks = (long)Bl * (gamma_max + 1) * plan->n_chunks;
   if (grid > max_tasks) grid = max_tasks;
   plan->grid = (int)grid;
   return SR_OK;
@@ -1000,13 +1111,13 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
     A.nc = plan.n_chunks;
     A.stats = (u32x4*)(ws + L.stats) + (size_t)b0 * G1 * plan.n_chunks * 2;
     A.tvabs = (double*)(ws + L.tvabs) + (size_t)b0 * G1 * plan.n_chunks;
+    A.xlogit = (float*)(ws + L.xlogit) + (size_t)b0 * G1 * 2;
     A.status = status;
+    const size_t lds = Bl * sizeof(int);
     if (dtype == SR_BF16)
-      hipLaunchKernelGGL((accept_sweep_kernel<true, kEbf16>), dim3(plan.grid), dim3(kThreads), Bl * sizeof(int),
-                         stream, A);
+      hipLaunchKernelGGL((accept_sweep_kernel<true, kEbf16>), dim3(plan.grid), dim3(kThreads), lds, stream, A);
     else
-      hipLaunchKernelGGL((accept_sweep_kernel<false, kEf32>), dim3(plan.grid), dim3(kThreads), Bl * sizeof(int),
-                         stream, A);
+      hipLaunchKernelGGL((accept_sweep_kernel<false, kEf32>), dim3(plan.grid), dim3(kThreads), lds, stream, A);
     if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
     if (dtype == SR_BF16)
       hipLaunchKernelGGL((accept_finish_kernel<true, kEbf16>), dim3(Bl), dim3(64 * nw), 0, stream, A);
