@@ -35,6 +35,16 @@ against (|u_acc - a_j|, and the distance of u_res * W to the two CDF values
 bracketing t, divided by W). A margin below 1e-6 marks a boundary case whose
 discrete outcome may legitimately differ under fp32 arithmetic.
 
+Sampling variants (the paper's "chosen sampling rule": greedy or
+probabilistic acceptance, with the sampling parameters of the logits
+processors). Temperature T > 0 replaces every distribution above by
+softmax(z / T) -- p, q, the divergences, the acceptance test, the residual and
+the bonus draw alike -- so T = 1 is the rule above. T = 0 is greedy decoding:
+p and q become one-hot at their argmax (lowest vocabulary index on ties), a
+draft is accepted iff it is argmax p_j (no uniform is used), the extra token is
+argmax p_k, a_j, p(x) and q(x) are 1 or 0, TV_j is 0 when the two argmaxes
+agree and 1 otherwise, and KL_j is 0 or +infinity likewise.
+
 Data errors (status bits, same meaning as the library's): 1 gamma_b outside
 [0, gamma_max]; 2 kv_len_b < gamma_b + 1 (only when kv_len is given);
 4 a draft outside [0, V); 8 a needed uniform outside [0, 1). Such a sequence
@@ -106,8 +116,47 @@ def inverse_cdf(w, u: float):
     return t, margin
 
 
-def accept_sequence(P, Q, drafts, gamma, u_acc, u_res, gmax, V):
-    """One sequence. P [>= gamma+1, V], Q [>= gamma, V] fp64 logits."""
+def accept_sequence_greedy(P, Q, drafts, gamma, gmax, V):
+    """One sequence under greedy decoding (temperature 0). Uniforms are not used."""
+    res = dict(
+        accept_len=-1, tokens=np.full(gmax + 1, -1, dtype=np.int64),
+        accept_prob=np.full(gmax, np.nan), p_tok=np.full(gmax, np.nan),
+        q_tok=np.full(gmax, np.nan), kl=np.full(gmax, np.nan), tv=np.full(gmax, np.nan),
+        lse_p=np.full(gmax + 1, np.nan), lse_q=np.full(gmax, np.nan),
+        margin=np.inf, status=0,
+    )
+    g = int(gamma)
+    if not (0 <= g <= gmax):
+        res["status"] = ST_GAMMA
+        return res
+    if any(not (0 <= int(drafts[j]) < V) for j in range(g)):
+        res["status"] = ST_TOKEN
+        return res
+    ap = [int(np.argmax(P[j])) for j in range(g + 1)]  # first occurrence: lowest index on ties
+    aq = [int(np.argmax(Q[j])) for j in range(g)]
+    k = g
+    for j in range(g):
+        x = int(drafts[j])
+        same = ap[j] == aq[j]
+        res["tv"][j] = 0.0 if same else 1.0
+        res["kl"][j] = 0.0 if same else np.inf
+        res["p_tok"][j] = 1.0 if x == ap[j] else 0.0
+        res["q_tok"][j] = 1.0 if x == aq[j] else 0.0
+        res["accept_prob"][j] = res["p_tok"][j]
+        if k == g and x != ap[j]:
+            k = j
+    res["accept_len"] = k
+    res["tokens"][:k] = np.asarray(drafts[:k], dtype=np.int64)
+    res["tokens"][k] = ap[k]
+    return res
+
+
+def accept_sequence(P, Q, drafts, gamma, u_acc, u_res, gmax, V, temperature=1.0):
+    """One sequence. P [>= gamma+1, V], Q [>= gamma, V] fp64 logits; every
+    distribution is softmax(logits / temperature) (temperature > 0)."""
+    if temperature != 1.0:
+        P = np.asarray(P, dtype=np.float64) / temperature
+        Q = np.asarray(Q, dtype=np.float64) / temperature
     res = dict(
         accept_len=-1, tokens=np.full(gmax + 1, -1, dtype=np.int64),
         accept_prob=np.full(gmax, np.nan), p_tok=np.full(gmax, np.nan),
@@ -171,8 +220,8 @@ def accept_sequence(P, Q, drafts, gamma, u_acc, u_res, gmax, V):
     return res
 
 
-def accept_and_diverge(p_logits, q_logits, drafts, gamma, u_acc, u_res, kv_len=None, seqs=None):
-    """Reference accept-and-diverge pass over a batch.
+def accept_and_diverge(p_logits, q_logits, drafts, gamma, u_acc, u_res, kv_len=None, seqs=None, temperature=1.0):
+    """Reference accept-and-diverge pass over a batch (temperature 0: greedy).
 
     p_logits [B, gmax+1, V] and q_logits [B, gmax, V]: fp32, fp64, or bf16 bit
     patterns (uint16). drafts [B, gmax] int; gamma [B]; u_acc [B, gmax];
@@ -204,7 +253,10 @@ def accept_and_diverge(p_logits, q_logits, drafts, gamma, u_acc, u_res, kv_len=N
         gg = max(0, min(g, gmax))
         P = decode_logits(p_logits[b, : gg + 1])
         Q = decode_logits(q_logits[b, :gg])
-        r = accept_sequence(P, Q, drafts[b], g, u_acc[b], u_res[b], gmax, V)
+        if temperature == 0:
+            r = accept_sequence_greedy(P, Q, drafts[b], g, gmax, V)
+        else:
+            r = accept_sequence(P, Q, drafts[b], g, u_acc[b], u_res[b], gmax, V, temperature)
         out["status"] |= r["status"]
         if r["status"]:
             continue
