@@ -209,6 +209,34 @@ def main():
         "algorithmic_bytes": dom_bytes, "avg_launch_us": round(dom_ms * 1e3, 2),
     }
 
+    # sampling variants of the accept call on the same inputs (greedy drafts
+    # are the workload's drafts; only the timing is reported)
+    variants = {}
+    for T in (0.0, 0.7):
+        for i in range(args.warmup):
+            s = sets[i % R]
+            a = s["acc"]
+            sr.specrouter_accept_and_diverge_sampled(
+                s["p"], s["ql"], s["drafts"], s["gamma"], s["u_acc"], s["u_res"], s["kv_in"], a.accept_len,
+                a.out_tokens, a.new_len, a.accept_prob, a.p_tok, a.q_tok, a.kl, a.tv, a.workspace, s["st"],
+                temperature=T)
+        e0, e1 = ev(), ev()
+        torch.cuda.synchronize()
+        e0.record()
+        for i in range(K):
+            s = sets[i % R]
+            a = s["acc"]
+            sr.specrouter_accept_and_diverge_sampled(
+                s["p"], s["ql"], s["drafts"], s["gamma"], s["u_acc"], s["u_res"], s["kv_in"], a.accept_len,
+                a.out_tokens, a.new_len, a.accept_prob, a.p_tok, a.q_tok, a.kl, a.tv, a.workspace, s["st"],
+                temperature=T)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / K * 1e3
+        name = "accept_greedy" if T == 0 else f"accept_temperature_{T}"
+        variants[name] = {"us": round(us, 2), "GB/s": round(acc_bytes / us / 1e3, 1)}
+    status |= int(sum(int(s["st"].item()) for s in sets))
+
     cpu = None
     if not args.no_cpu:
         cpu = cpu_baseline(inp, args.cpu_seqs)
@@ -243,6 +271,7 @@ def main():
                                    "traffic": measured_traffic("accept_and_diverge", shape.name)},
             "rollback": {"us": round(rb_ms * 1e3, 2), "algorithmic_bytes": rb_bytes},
         },
+        "sampling_variants": variants,
         "mean_accept_len": round(mean_accept, 3),
         "status_bits": status,
         "cpu_baseline": cpu,

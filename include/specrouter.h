@@ -53,7 +53,7 @@
 extern "C" {
 #endif
 
-#define SPECROUTER_ABI_VERSION 1
+#define SPECROUTER_ABI_VERSION 2
 #define SPECROUTER_MAX_GAMMA 16
 
 /* Host-side return codes. */
@@ -167,6 +167,45 @@ int specrouter_accept_and_diverge(const void* p_logits, int64_t p_batch_stride,
                                   float* p_tok, float* q_tok, float* kl, float* tv, int B,
                                   int gamma_max, int V, void* workspace, size_t workspace_bytes,
                                   int32_t* status, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Accept and diverge under a sampling rule (Section 2.2 step 3: the chosen
+ * sampling rule, greedy or probabilistic acceptance; the sampling parameters
+ * of the logits processors, Section 4.1).
+ *
+ * temperature T > 0: every distribution of specrouter_accept_and_diverge
+ *   becomes softmax(logits / T) -- p and q, the acceptance test, the residual
+ *   and bonus draws, TV and KL alike (T = 1 is specrouter_accept_and_diverge).
+ *   The drafts are assumed drawn from the draft model's softmax(logits / T).
+ * temperature 0: greedy decoding. p_j and q_j are one-hot at their argmax
+ *   (the lowest vocabulary index among equal maxima); draft x_j is accepted
+ *   iff x_j == argmax p_j, and the extra token is argmax p_k. u_accept and
+ *   u_resample are not read (may be NULL); accept_prob, p_tok and q_tok are 1
+ *   or 0, TV_j is 0 when argmax p_j == argmax q_j and 1 otherwise, KL_j is 0
+ *   or +infinity likewise. No SR_ST_UNIFORM check is made.
+ * top_k, top_p: reserved; must be 0 and 1 (else SR_EUNSUPPORTED).
+ * A NULL sampling pointer means temperature 1. The sampling struct is a host
+ * pointer, read before the call returns. temperature must be finite and >= 0
+ * (else SR_EINVAL). All other arguments, the workspace and the outputs are as
+ * for specrouter_accept_and_diverge.
+ */
+typedef struct specrouter_sampling {
+  float temperature;
+  int top_k;
+  float top_p;
+} specrouter_sampling;
+
+int specrouter_accept_and_diverge_sampled(const void* p_logits, int64_t p_batch_stride,
+                                          const void* q_logits, int64_t q_batch_stride,
+                                          int logits_dtype, const int32_t* draft_tokens,
+                                          const int32_t* gamma, const float* u_accept,
+                                          const float* u_resample, const int32_t* kv_len,
+                                          int32_t* accept_len, int32_t* out_tokens,
+                                          int32_t* new_len, float* accept_prob, float* p_tok,
+                                          float* q_tok, float* kl, float* tv, int B,
+                                          int gamma_max, int V,
+                                          const specrouter_sampling* sampling, void* workspace,
+                                          size_t workspace_bytes, int32_t* status, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Rollback (Section 4.4, logical rollback and Eq. 9).

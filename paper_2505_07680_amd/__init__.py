@@ -17,6 +17,7 @@ from ._lib import (
     load,
     specrouter_abi_version,
     specrouter_accept_and_diverge,
+    specrouter_accept_and_diverge_sampled,
     specrouter_accept_workspace_size,
     specrouter_rollback,
     specrouter_status_string,
@@ -33,6 +34,7 @@ __all__ = [
     "load",
     "specrouter_abi_version",
     "specrouter_accept_and_diverge",
+    "specrouter_accept_and_diverge_sampled",
     "specrouter_accept_workspace_size",
     "specrouter_rollback",
     "specrouter_status_string",

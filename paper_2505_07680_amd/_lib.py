@@ -33,6 +33,12 @@ _c_d = ctypes.c_double
 _c_dp = ctypes.POINTER(ctypes.c_double)
 _c_ip = ctypes.POINTER(ctypes.c_int32)
 
+class SamplingParams(ctypes.Structure):
+    """specrouter_sampling: temperature (0 = greedy), top_k (0), top_p (1)."""
+
+    _fields_ = [("temperature", ctypes.c_float), ("top_k", ctypes.c_int), ("top_p", ctypes.c_float)]
+
+
 _SIGNATURES = {
     "specrouter_abi_version": (_c_i, []),
     "specrouter_status_string": (ctypes.c_char_p, [_c_i]),
@@ -45,6 +51,11 @@ _SIGNATURES = {
     "specrouter_accept_and_diverge": (
         _c_i,
         [_c_p, _c_i64, _c_p, _c_i64, _c_i] + [_c_p] * 13 + [_c_i] * 3 + [_c_p, _c_sz, _c_p, _c_p],
+    ),
+    "specrouter_accept_and_diverge_sampled": (
+        _c_i,
+        [_c_p, _c_i64, _c_p, _c_i64, _c_i] + [_c_p] * 13 + [_c_i] * 3
+        + [ctypes.POINTER(SamplingParams), _c_p, _c_sz, _c_p, _c_p],
     ),
     "specrouter_rollback": (_c_i, [_c_p] * 4 + [_c_i, _c_i, _c_p, _c_p]),
     # chain scheduler (host code; host pointers)
@@ -177,6 +188,23 @@ def specrouter_accept_and_diverge(p_logits, q_logits, draft_tokens, gamma, u_acc
                                   kv_len, accept_len, out_tokens, new_len, accept_prob, p_tok,
                                   q_tok, kl, tv, workspace, status=None):
     """p_logits [B, gmax+1, V]; q_logits [B, gmax, V] (rows contiguous, batch stride free)."""
+    _accept(p_logits, q_logits, draft_tokens, gamma, u_accept, u_resample, kv_len, accept_len, out_tokens,
+            new_len, accept_prob, p_tok, q_tok, kl, tv, workspace, status, None)
+
+
+def specrouter_accept_and_diverge_sampled(p_logits, q_logits, draft_tokens, gamma, u_accept, u_resample,
+                                          kv_len, accept_len, out_tokens, new_len, accept_prob, p_tok,
+                                          q_tok, kl, tv, workspace, status=None, temperature=1.0, top_k=0,
+                                          top_p=1.0):
+    """As specrouter_accept_and_diverge under softmax(logits / temperature);
+    temperature 0 is greedy decoding (u_accept and u_resample may be None)."""
+    _accept(p_logits, q_logits, draft_tokens, gamma, u_accept, u_resample, kv_len, accept_len, out_tokens,
+            new_len, accept_prob, p_tok, q_tok, kl, tv, workspace, status,
+            SamplingParams(float(temperature), int(top_k), float(top_p)))
+
+
+def _accept(p_logits, q_logits, draft_tokens, gamma, u_accept, u_resample, kv_len, accept_len, out_tokens,
+            new_len, accept_prob, p_tok, q_tok, kl, tv, workspace, status, sampling):
     tensors = (p_logits, q_logits, draft_tokens, gamma, u_accept, u_resample, kv_len, accept_len,
                out_tokens, new_len, accept_prob, p_tok, q_tok, kl, tv, workspace, status)
     _dev(*tensors)
@@ -193,19 +221,21 @@ def specrouter_accept_and_diverge(p_logits, q_logits, draft_tokens, gamma, u_acc
         if logits_dtype_code(q_logits) != code:
             raise TypeError("p_logits and q_logits must share a dtype")
         qs = _row_view(q_logits, gmax, V, "q_logits")
-    if u_resample.shape != (B, G1) or (gmax > 0 and u_accept.shape != (B, gmax)):
+    if (u_resample is not None and u_resample.shape != (B, G1)) or (
+            gmax > 0 and u_accept is not None and u_accept.shape != (B, gmax)):
         raise ValueError("u_accept [B, gmax] and u_resample [B, gmax+1] expected")
     for t in (accept_prob, p_tok, q_tok, kl, tv):
         if t is not None and (t.shape != (B, gmax) or t.dtype != torch.float32):
             raise ValueError("float outputs must be fp32 [B, gamma_max]")
     ws_bytes = workspace.numel() * workspace.element_size()
-    rc = load().specrouter_accept_and_diverge(
+    rc = load().specrouter_accept_and_diverge_sampled(
         _ptr(p_logits), ps, _ptr(q_logits), qs, code, _ptr(draft_tokens), _ptr(gamma),
         _ptr(u_accept), _ptr(u_resample), _ptr(kv_len), _ptr(accept_len), _ptr(out_tokens),
         _ptr(new_len), _ptr(accept_prob), _ptr(p_tok), _ptr(q_tok), _ptr(kl), _ptr(tv),
-        B, gmax, V, _ptr(workspace), ws_bytes, _ptr(status), _stream(),
+        B, gmax, V, None if sampling is None else ctypes.byref(sampling), _ptr(workspace), ws_bytes,
+        _ptr(status), _stream(),
     )
-    _check(rc, "specrouter_accept_and_diverge")
+    _check(rc, "specrouter_accept_and_diverge" + ("" if sampling is None else "_sampled"))
 
 
 def specrouter_rollback(kv_len, cache_mask, new_len, phys_len=None, status=None, L_cap=None):

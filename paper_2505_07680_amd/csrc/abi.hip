@@ -94,19 +94,25 @@ size_t specrouter_accept_workspace_size(int B, int gamma_max, int V, int logits_
   return plan.workspace_bytes;
 }
 
-int specrouter_accept_and_diverge(const void* p_logits, int64_t p_batch_stride,
-                                  const void* q_logits, int64_t q_batch_stride, int logits_dtype,
-                                  const int32_t* draft_tokens, const int32_t* gamma,
-                                  const float* u_accept, const float* u_resample,
-                                  const int32_t* kv_len, int32_t* accept_len,
-                                  int32_t* out_tokens, int32_t* new_len, float* accept_prob,
-                                  float* p_tok, float* q_tok, float* kl, float* tv, int B,
-                                  int gamma_max, int V, void* workspace, size_t workspace_bytes,
-                                  int32_t* status, void* stream) {
+int specrouter_accept_and_diverge_sampled(const void* p_logits, int64_t p_batch_stride,
+                                          const void* q_logits, int64_t q_batch_stride, int logits_dtype,
+                                          const int32_t* draft_tokens, const int32_t* gamma,
+                                          const float* u_accept, const float* u_resample,
+                                          const int32_t* kv_len, int32_t* accept_len,
+                                          int32_t* out_tokens, int32_t* new_len, float* accept_prob,
+                                          float* p_tok, float* q_tok, float* kl, float* tv, int B,
+                                          int gamma_max, int V, const specrouter_sampling* sampling,
+                                          void* workspace, size_t workspace_bytes, int32_t* status,
+                                          void* stream) {
+  const float temperature = sampling ? sampling->temperature : 1.f;
+  if (!(temperature >= 0.f && temperature < __builtin_inff())) return SR_EINVAL;
+  if (sampling && (sampling->top_k != 0 || sampling->top_p != 1.f)) return SR_EUNSUPPORTED;
+  const bool greedy = temperature == 0.f;
   if (B <= 0 || gamma_max < 0 || gamma_max > SPECROUTER_MAX_GAMMA || V <= 0) return SR_EINVAL;
   if (logits_dtype != SR_F32 && logits_dtype != SR_BF16) return SR_EUNSUPPORTED;
-  if (!p_logits || !gamma || !u_resample || !accept_len || !out_tokens) return SR_EINVAL;
-  if (gamma_max > 0 && (!q_logits || !draft_tokens || !u_accept)) return SR_EINVAL;
+  if (!p_logits || !gamma || !accept_len || !out_tokens) return SR_EINVAL;
+  if (!greedy && !u_resample) return SR_EINVAL;
+  if (gamma_max > 0 && (!q_logits || !draft_tokens || (!greedy && !u_accept))) return SR_EINVAL;
   if (new_len && !kv_len) return SR_EINVAL;
   if (p_batch_stride < (int64_t)(gamma_max + 1) * V) return SR_EINVAL;
   if (gamma_max > 0 && q_batch_stride < (int64_t)gamma_max * V) return SR_EINVAL;
@@ -123,7 +129,23 @@ int specrouter_accept_and_diverge(const void* p_logits, int64_t p_batch_stride,
   return sr::launch_accept(p_logits, p_batch_stride, q_logits, q_batch_stride, logits_dtype,
                            draft_tokens, gamma, u_accept, u_resample, kv_len, accept_len,
                            out_tokens, new_len, accept_prob, p_tok, q_tok, kl, tv, B, gamma_max,
-                           V, workspace, plan, status, (hipStream_t)stream);
+                           V, temperature, workspace, plan, status, (hipStream_t)stream);
+}
+
+int specrouter_accept_and_diverge(const void* p_logits, int64_t p_batch_stride,
+                                  const void* q_logits, int64_t q_batch_stride, int logits_dtype,
+                                  const int32_t* draft_tokens, const int32_t* gamma,
+                                  const float* u_accept, const float* u_resample,
+                                  const int32_t* kv_len, int32_t* accept_len,
+                                  int32_t* out_tokens, int32_t* new_len, float* accept_prob,
+                                  float* p_tok, float* q_tok, float* kl, float* tv, int B,
+                                  int gamma_max, int V, void* workspace, size_t workspace_bytes,
+                                  int32_t* status, void* stream) {
+  return specrouter_accept_and_diverge_sampled(p_logits, p_batch_stride, q_logits, q_batch_stride,
+                                               logits_dtype, draft_tokens, gamma, u_accept, u_resample,
+                                               kv_len, accept_len, out_tokens, new_len, accept_prob, p_tok,
+                                               q_tok, kl, tv, B, gamma_max, V, nullptr, workspace,
+                                               workspace_bytes, status, stream);
 }
 
 int specrouter_rollback(int32_t* kv_len, uint8_t* cache_mask, const int32_t* new_len,

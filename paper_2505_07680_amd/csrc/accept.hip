@@ -44,6 +44,7 @@
 // draw can differ from exact arithmetic only when u*W lies within ~1e-7 W of
 // a CDF breakpoint.
 
+#include <limits.h>
 #include <math.h>
 
 #include "sr_internal.h"
@@ -155,6 +156,8 @@ struct Args {
   float* kl;
   float* tv;
   int B, gmax, V, nc;
+  float lg;       // log2(e) / T: softmax(z / T) entries are 2^((z - m) lg)
+  double inv_t;   // 1 / T
   u32x4* stats;     // [B][gmax+1][nc] records, two 16-byte halves each
   double* tvabs;    // [B][gmax+1][nc] sum |P - Q| per chunk (pair rows)
   float* xlogit;    // [B][gmax+1][2] the draft token's p and q logits (pair rows)
@@ -185,14 +188,16 @@ struct RowNorm {
   float M;     // row maximum (-inf: none)
   double S;    // sum of the chunks' rescaled sums (>= 1 when M is finite)
   float invS;  // 1/S rounded to fp32
+  float lg;    // log2(e) / T
   __device__ float factor(float m) const {  // f_c for a chunk whose maximum is m
-    return m == kNegInf ? 0.f : exp2_hw((m - M) * kLog2e) * invS;
+    return m == kNegInf ? 0.f : exp2_hw((m - M) * lg) * invS;
   }
-  __device__ double log_norm() const { return (double)M + log(S); }  // ln sum e^z
+  __device__ double log_norm(double inv_t) const { return (double)M * inv_t + log(S); }  // ln sum e^(z/T)
 };
 
-__device__ __forceinline__ RowNorm row_norm(const float (&m)[kSlots], const double (&s)[kSlots]) {
+__device__ __forceinline__ RowNorm row_norm(const float (&m)[kSlots], const double (&s)[kSlots], float lg) {
   RowNorm r;
+  r.lg = lg;
   float ml = kNegInf;
 #pragma unroll
   for (int i = 0; i < kSlots; ++i) ml = fmaxf(ml, m[i]);
@@ -201,7 +206,7 @@ __device__ __forceinline__ RowNorm row_norm(const float (&m)[kSlots], const doub
   if (r.M != kNegInf) {
 #pragma unroll
     for (int i = 0; i < kSlots; ++i)
-      if (m[i] != kNegInf) acc += s[i] * (double)exp2_hw((m[i] - r.M) * kLog2e);
+      if (m[i] != kNegInf) acc += s[i] * (double)exp2_hw((m[i] - r.M) * lg);
   }
   r.S = wave_sum_d(acc);
   r.invS = r.S > 0.0 ? (float)(1.0 / r.S) : 0.f;
@@ -210,10 +215,12 @@ __device__ __forceinline__ RowNorm row_norm(const float (&m)[kSlots], const doub
 
 
 // Inclusive prefix over sequences of their live-row counts (gamma_b + 1, or 0
-// for an invalid gamma), in LDS. Each thread scans a contiguous segment.
+// for an invalid gamma), in LDS. Each thread scans a contiguous segment; the
+// segment totals are scanned across the workgroup in parallel.
 __device__ void build_row_table(const int32_t* gamma, int gmax, int B, int* rows) {
-  __shared__ int part[kThreads];
+  __shared__ int wsum[kThreads / 64];
   const int tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
   const int per = (B + kThreads - 1) / kThreads;
   const int b0 = min(tid * per, B), b1 = min(b0 + per, B);
   int run = 0;
@@ -222,18 +229,11 @@ __device__ void build_row_table(const int32_t* gamma, int gmax, int B, int* rows
     run += (g >= 0 && g <= gmax) ? g + 1 : 0;
     rows[b] = run;
   }
-  part[tid] = run;
+  const int incl = wave_incl_scan_i(run);
+  if (lane == 63) wsum[w] = incl;
   __syncthreads();
-  if (tid == 0) {
-    int acc = 0;
-    for (int i = 0; i < kThreads; ++i) {
-      const int v = part[i];
-      part[i] = acc;
-      acc += v;
-    }
-  }
-  __syncthreads();
-  const int off = part[tid];
+  int off = incl - run;
+  for (int i = 0; i < w; ++i) off += wsum[i];
   for (int b = b0; b < b1; ++b) rows[b] += off;
   __syncthreads();
 }
@@ -339,7 +339,8 @@ __device__ __forceinline__ void issue_loads(const Args& A, const TaskInfo& t, Ra
 struct SweepShared {
   float m[2][kWaves];
   double s[3][kWaves];
-  float f[2];  // this chunk's factors f_c for p and q
+  float f[2];        // this chunk's factors f_c for p and q
+  int ix[2][kWaves];  // greedy: the waves' argmax indices of p and q
 };
 
 template <bool BF16, int E>
@@ -400,8 +401,9 @@ struct Sweep {
 
     // exponentials, sums, KL numerator; groups of four are summed as
     // (a0 + a1) + (a2 + a3), then a tree over groups
-    const float rp = cmp == kNegInf ? 0.f : cmp * kLog2e;
-    const float rq = cmq == kNegInf ? 0.f : cmq * kLog2e;
+    const float lg = A.lg;
+    const float rp = cmp == kNegInf ? 0.f : cmp * lg;
+    const float rq = cmq == kNegInf ? 0.f : cmq * lg;
     double dsp, dsq = 0.0, dkl = 0.0;
     if (t.pair) {
       float gp[E / 4], gq[E / 4], gk[E / 4];
@@ -413,8 +415,8 @@ struct Sweep {
           const int e = g * 4 + i;
           const bool in = in_v(e);
           const float zp = r.gp(e), zq = r.gq(e);
-          ep[i] = in ? exp2_hw(fmaf(zp, kLog2e, -rp)) : 0.f;
-          eq[i] = in ? exp2_hw(fmaf(zq, kLog2e, -rq)) : 0.f;
+          ep[i] = in ? exp2_hw(fmaf(zp, lg, -rp)) : 0.f;
+          eq[i] = in ? exp2_hw(fmaf(zq, lg, -rq)) : 0.f;
           kt[i] = ep[i] > 0.f ? ep[i] * (zp - zq) : 0.f;
           if constexpr (!BF16) {
             r.p[e] = ep[i];
@@ -437,7 +439,7 @@ struct Sweep {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const float zp = r.gp(g * 4 + i);
-          ep[i] = in_v(g * 4 + i) ? exp2_hw(fmaf(zp, kLog2e, -rp)) : 0.f;
+          ep[i] = in_v(g * 4 + i) ? exp2_hw(fmaf(zp, lg, -rp)) : 0.f;
         }
         gp[g] = (ep[0] + ep[1]) + (ep[2] + ep[3]);
       }
@@ -462,6 +464,62 @@ struct Sweep {
       __builtin_amdgcn_raw_buffer_store_b128(w0, rs_stats, (uint32_t)(rec * kRecBytes), 0, kDeviceCoherent);
       __builtin_amdgcn_raw_buffer_store_b128(w1, rs_stats, (uint32_t)(rec * kRecBytes + 16), 0, kDeviceCoherent);
     }
+  }
+
+  // Greedy decoding: the chunk's maxima of p and q and the lowest index
+  // holding each, published as the chunk's record (indices in the sum fields).
+  __device__ __forceinline__ void argmax_pass(const TaskInfo& t, const Raw<BF16, E>& r) {
+    const int base = t.c * kChunk + w * (64 * E);
+    float bp = kNegInf, bq = kNegInf;
+    int ip = -1, iq = -1;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {  // a lane's entries in ascending index order
+      const int idx = base + ((e / VEC) * 64 + lane) * VEC + e % VEC;
+      const bool in = idx < A.V;
+      const float zp = r.gp(e), zq = r.gq(e);
+      if (in && (ip < 0 || zp > bp)) {
+        bp = zp;
+        ip = idx;
+      }
+      if (in && (iq < 0 || zq > bq)) {
+        bq = zq;
+        iq = idx;
+      }
+    }
+    const float mp = wave_max(bp);
+    const int jp = wave_min_i(ip >= 0 && bp == mp ? ip : INT_MAX);
+    float mq = kNegInf;
+    int jq = INT_MAX;
+    if (t.pair) {
+      mq = wave_max(bq);
+      jq = wave_min_i(iq >= 0 && bq == mq ? iq : INT_MAX);
+    }
+    if (lane == 0) {
+      sh.m[0][w] = mp;
+      sh.m[1][w] = mq;
+      sh.ix[0][w] = jp;
+      sh.ix[1][w] = jq;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      StatRec sr;
+      sr.mp = max_waves(sh.m[0]);
+      sr.mq = max_waves(sh.m[1]);
+      int ap = INT_MAX, aq = INT_MAX;
+      for (int i = 0; i < kWaves; ++i) {
+        if (sh.m[0][i] == sr.mp) ap = min(ap, sh.ix[0][i]);
+        if (sh.m[1][i] == sr.mq) aq = min(aq, sh.ix[1][i]);
+      }
+      sr.sp = (double)ap;
+      sr.sq = (double)aq;
+      sr.kl = 0.0;
+      u32x4 w0, w1;
+      pack_rec(sr, w0, w1);
+      const size_t rec = (size_t)t.row * nc + t.c;
+      __builtin_amdgcn_raw_buffer_store_b128(w0, rs_stats, (uint32_t)(rec * kRecBytes), 0, kDeviceCoherent);
+      __builtin_amdgcn_raw_buffer_store_b128(w1, rs_stats, (uint32_t)(rec * kRecBytes + 16), 0, kDeviceCoherent);
+    }
+    __syncthreads();  // the next task rewrites sh.m and sh.ix
   }
 
   // One wave: re-load the records of a pair row until all of them are
@@ -493,8 +551,8 @@ struct Sweep {
       }
       __builtin_amdgcn_s_sleep(2);
     }
-    const RowNorm np = row_norm(m1, s1);
-    const RowNorm nq = row_norm(m2, s2);
+    const RowNorm np = row_norm(m1, s1, A.lg);
+    const RowNorm nq = row_norm(m2, s2, A.lg);
     if (lane == 0) {
       sh.f[0] = np.factor(cmp);
       sh.f[1] = nq.factor(cmq);
@@ -506,8 +564,9 @@ struct Sweep {
   // kernel.
   __device__ __forceinline__ void tv_pass(const TaskInfo& t, const Raw<BF16, E>& r, float cmp, float cmq) {
     const float fp = sh.f[0], fq = sh.f[1];
-    const float rp = cmp == kNegInf ? 0.f : cmp * kLog2e;
-    const float rq = cmq == kNegInf ? 0.f : cmq * kLog2e;
+    const float lg = A.lg;
+    const float rp = cmp == kNegInf ? 0.f : cmp * lg;
+    const float rq = cmq == kNegInf ? 0.f : cmq * lg;
     const int base = t.c * kChunk + w * (64 * E);
     float ga[E / 4];
 #pragma unroll
@@ -520,8 +579,8 @@ struct Sweep {
         if constexpr (BF16) {
           const bool in = base + ((e / VEC) * 64 + lane) * VEC < A.V;
           const float zp = r.gp(e), zq = r.gq(e);
-          ep = in ? exp2_hw(fmaf(zp, kLog2e, -rp)) : 0.f;
-          eq = in ? exp2_hw(fmaf(zq, kLog2e, -rq)) : 0.f;
+          ep = in ? exp2_hw(fmaf(zp, lg, -rp)) : 0.f;
+          eq = in ? exp2_hw(fmaf(zq, lg, -rq)) : 0.f;
         } else {
           ep = r.p[e];
           eq = r.q[e];
@@ -594,6 +653,37 @@ accept_sweep_kernel(Args A) {
     cur = nxt;
     cmp = cmp_n;
     cmq = cmq_n;
+  }
+}
+
+// Greedy decoding: one pass of chunk argmaxes, no second pass and no waiting
+// (workgroup w takes tasks w, w + G, ..., loading one task ahead).
+template <bool BF16, int E>
+__global__ void __launch_bounds__(kThreads)
+accept_argmax_kernel(Args A) {
+  extern __shared__ int s_rows[];
+  __shared__ SweepShared sh;
+  Sweep<BF16, E> S(A, sh);
+  build_row_table(A.gamma, A.gmax, A.B, s_rows);
+  const long n_tasks = (long)s_rows[A.B - 1] * S.nc;
+  long task = blockIdx.x;
+  if (task >= n_tasks) return;
+  TaskInfo t = decode_task<BF16>(A, s_rows, task);
+  Raw<BF16, E> cur;
+  issue_loads<BF16, E>(A, t, cur);
+  for (;;) {
+    const long task_n = task + gridDim.x;
+    const bool more = task_n < n_tasks;
+    const TaskInfo tn = decode_task<BF16>(A, s_rows, more ? task_n : task);
+    Raw<BF16, E> nxt;
+    __builtin_amdgcn_sched_barrier(0);
+    issue_loads<BF16, E>(A, tn, nxt);
+    __builtin_amdgcn_sched_barrier(0);
+    S.argmax_pass(t, cur);
+    if (!more) break;
+    task = task_n;
+    t = tn;
+    cur = nxt;
   }
 }
 
@@ -781,8 +871,8 @@ accept_finish_kernel(Args A) {
         R.ta[i] = 0.0;
       }
     }
-    const RowNorm np = row_norm(R.mp, R.sp);
-    const RowNorm nq = row_norm(R.mq, R.sq);
+    const RowNorm np = row_norm(R.mp, R.sp, A.lg);
+    const RowNorm nq = row_norm(R.mq, R.sq, A.lg);
     // chunk masses with the same factors the sweep's sum |P - Q| used
     double my_res = 0.0;
 #pragma unroll
@@ -808,7 +898,7 @@ accept_finish_kernel(Args A) {
       F.resid[j] = residual ? 1 : 0;
     }
     if (!pair) continue;  // the bonus row needs no divergences
-    const double Lp = np.log_norm(), Lq = nq.log_norm();
+    const double Lp = np.log_norm(A.inv_t), Lq = nq.log_norm(A.inv_t);
     double tvd = 0.0, kld = 0.0;
 #pragma unroll
     for (int i = 0; i < kSlots; ++i) {
@@ -816,10 +906,10 @@ accept_finish_kernel(Args A) {
       kld += R.kl[i] * (double)np.factor(R.mp[i]);
     }
     tvd = 0.5 * wave_sum_d(tvd);
-    kld = wave_sum_d(kld) - (Lp - Lq);
+    kld = A.inv_t * wave_sum_d(kld) - (Lp - Lq);
     // p(x), q(x) and a = min(1, p(x)/q(x)): one exponential per lane (0-2)
-    const double lpx = (double)zpx - Lp;
-    const double lqx = (double)zqx - Lq;
+    const double lpx = (double)zpx * A.inv_t - Lp;
+    const double lqx = (double)zqx * A.inv_t - Lq;
     const double arg = lane == 0 ? lpx : (lane == 1 ? lqx : lpx - lqx);
     const double ex = exp(arg);
     const double pt = lane_value(ex, 0), qt = lane_value(ex, 1), rt = lane_value(ex, 2);
@@ -895,14 +985,16 @@ accept_finish_kernel(Args A) {
       RowNorm np, nq;
       np.M = F.norm[k][0];
       np.invS = F.norm[k][1];
+      np.lg = A.lg;
       nq.M = pair ? F.norm[k][2] : kNegInf;
       nq.invS = pair ? F.norm[k][3] : 0.f;
+      nq.lg = A.lg;
       s_k = k;
       s_cs = cs;
       s_resid = residual ? 1 : 0;
       s_rem = target - pre;
-      s_fac[0] = cmp == kNegInf ? 0.f : cmp * kLog2e;
-      s_fac[1] = cmq == kNegInf ? 0.f : cmq * kLog2e;
+      s_fac[0] = cmp == kNegInf ? 0.f : cmp * A.lg;
+      s_fac[1] = cmq == kNegInf ? 0.f : cmq * A.lg;
       s_fac[2] = np.factor(cmp);
       s_fac[3] = nq.factor(cmq);
     }
@@ -941,9 +1033,9 @@ accept_finish_kernel(Args A) {
           float wv = 0.f;
           if (x0 + e < A.V) {
 #pragma clang fp contract(off)
-            const float ep = exp2_hw(fmaf(zp[e], kLog2e, -rp));
+            const float ep = exp2_hw(fmaf(zp[e], A.lg, -rp));
             if (residual) {
-              const float eq = exp2_hw(fmaf(zq[e], kLog2e, -rq));
+              const float eq = exp2_hw(fmaf(zq[e], A.lg, -rq));
               wv = fmaxf(ep * fp - eq * fq, 0.f);
             } else {
               wv = ep * fp;
@@ -1018,6 +1110,103 @@ accept_finish_kernel(Args A) {
   }
 }
 
+// Greedy finish kernel: one workgroup per sequence, one wave per live row.
+// A row's argmax is the lowest index holding the largest of its chunk maxima;
+// draft x_j is accepted iff it is argmax p_j, the extra token is argmax p_k,
+// and the outputs are the one-hot values (a_j, p(x), q(x) in {0, 1}; TV_j 0
+// or 1 and KL_j 0 or +infinity as the two argmaxes agree or not).
+__global__ void __launch_bounds__(1024)
+accept_finish_greedy_kernel(Args A) {
+  __shared__ int s_x[kMaxRows], s_ap[kMaxRows];
+  __shared__ RowRes s_rr[kMaxRows];
+  __shared__ uint32_t s_bad;
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = tid >> 6;
+  const int nw = blockDim.x >> 6;
+  const int G1 = A.gmax + 1;
+  const int nslot = (A.nc + 63) / 64;
+  const int gam = A.gamma[b];
+  if (tid == 0) s_bad = 0;
+  if (tid < A.gmax) s_x[tid] = A.drafts[(size_t)b * A.gmax + tid];
+  const int kvl = A.kv_len ? A.kv_len[b] : 0;
+  if (gam < 0 || gam > A.gmax) {
+    if (w == 0) write_invalid(A, b, SR_ST_GAMMA);
+    return;  // the sweep touched no row of this sequence
+  }
+  __syncthreads();
+  if (tid <= gam) {
+    uint32_t bad = 0;
+    if (tid < gam && (s_x[tid] < 0 || s_x[tid] >= A.V)) bad |= SR_ST_TOKEN;
+    if (tid == 0 && A.kv_len && kvl < gam + 1) bad |= SR_ST_KVLEN;
+    if (bad) atomicOr(&s_bad, bad);
+  }
+  for (int j = w; j <= gam; j += nw) {
+    const bool pair = j < gam;
+    RowRecs R;
+    load_row(A, b * G1 + j, pair, R);
+    float mp = kNegInf, mq = kNegInf;
+#pragma unroll
+    for (int i = 0; i < kSlots; ++i) {
+      mp = fmaxf(mp, R.mp[i]);
+      mq = fmaxf(mq, R.mq[i]);
+    }
+    mp = wave_max(mp);
+    int ap = INT_MAX, aq = INT_MAX;
+#pragma unroll
+    for (int i = 0; i < kSlots; ++i) {
+      const int cc = lane * nslot + i;
+      if (i < nslot && cc < A.nc && R.mp[i] == mp) ap = min(ap, (int)R.sp[i]);
+    }
+    ap = wave_min_i(ap);
+    if (pair) {
+      mq = wave_max(mq);
+#pragma unroll
+      for (int i = 0; i < kSlots; ++i) {
+        const int cc = lane * nslot + i;
+        if (i < nslot && cc < A.nc && R.mq[i] == mq) aq = min(aq, (int)R.sq[i]);
+      }
+      aq = wave_min_i(aq);
+    }
+    if (lane == 0) {
+      s_ap[j] = ap;
+      if (pair) {
+        const int x = s_x[j];
+        const float hit_p = x == ap ? 1.f : 0.f, hit_q = x == aq ? 1.f : 0.f;
+        s_rr[j] = RowRes{(double)hit_p, hit_p, hit_q, ap == aq ? 0.f : __builtin_inff(), ap == aq ? 0.f : 1.f};
+      }
+    }
+  }
+  __syncthreads();
+  if (w != 0) return;
+  if (s_bad) {
+    clear_records(A, b, gam);
+    write_invalid(A, b, s_bad);
+    return;
+  }
+  const unsigned long long rmask = __ballot(lane < gam && s_x[lane < gam ? lane : 0] != s_ap[lane < gam ? lane : 0]);
+  const int k = rmask ? (__ffsll((long long)rmask) - 1) : gam;
+  const int tok = s_ap[k];
+  clear_records(A, b, gam);
+  int32_t* ot = A.out_tokens + (size_t)b * G1;
+  for (int j = lane; j <= A.gmax; j += 64) ot[j] = j < k ? s_x[j] : (j == k ? tok : -1);
+  const float nan = __builtin_nanf("");
+  for (int j = lane; j < A.gmax; j += 64) {
+    const size_t o = (size_t)b * A.gmax + j;
+    const bool live = j < gam;
+    if (A.accept_prob) A.accept_prob[o] = live ? (float)s_rr[j].a : nan;
+    if (A.p_tok) A.p_tok[o] = live ? s_rr[j].p_tok : nan;
+    if (A.q_tok) A.q_tok[o] = live ? s_rr[j].q_tok : nan;
+    if (A.kl) A.kl[o] = live ? s_rr[j].kl : nan;
+    if (A.tv) A.tv[o] = live ? s_rr[j].tv : nan;
+  }
+  if (lane == 0) {
+    A.accept_len[b] = k;
+    if (A.new_len) A.new_len[b] = kvl - gam + k;
+  }
+}
+
 // Entries per lane per chunk.
 constexpr int kEf32 = 16;
 constexpr int kEbf16 = 32;
@@ -1077,9 +1266,10 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
                   int dtype, const int32_t* drafts, const int32_t* gamma, const float* u_acc,
                   const float* u_res, const int32_t* kv_len, int32_t* accept_len,
                   int32_t* out_tokens, int32_t* new_len, float* accept_prob, float* p_tok,
-                  float* q_tok, float* kl, float* tv, int B, int gamma_max, int V,
+                  float* q_tok, float* kl, float* tv, int B, int gamma_max, int V, float temperature,
                   void* workspace, const AcceptPlan& plan, int32_t* status, hipStream_t stream) {
   const Layout L = layout(B, gamma_max, plan.n_chunks);
+  const bool greedy = temperature == 0.f;
   const int G1 = gamma_max + 1;
   const size_t esz = dtype == SR_BF16 ? 2 : 4;
   char* ws = (char*)workspace;
@@ -1095,7 +1285,7 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
     A.drafts = drafts ? drafts + (size_t)b0 * gamma_max : nullptr;
     A.gamma = gamma + b0;
     A.u_acc = u_acc ? u_acc + (size_t)b0 * gamma_max : nullptr;
-    A.u_res = u_res + (size_t)b0 * G1;
+    A.u_res = u_res ? u_res + (size_t)b0 * G1 : nullptr;
     A.kv_len = kv_len ? kv_len + b0 : nullptr;
     A.accept_len = accept_len + b0;
     A.out_tokens = out_tokens + (size_t)b0 * G1;
@@ -1113,7 +1303,19 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
     A.tvabs = (double*)(ws + L.tvabs) + (size_t)b0 * G1 * plan.n_chunks;
     A.xlogit = (float*)(ws + L.xlogit) + (size_t)b0 * G1 * 2;
     A.status = status;
+    A.lg = greedy ? 0.f : (float)(1.4426950408889634 / (double)temperature);
+    A.inv_t = greedy ? 0.0 : 1.0 / (double)temperature;
     const size_t lds = Bl * sizeof(int);
+    if (greedy) {
+      if (dtype == SR_BF16)
+        hipLaunchKernelGGL((accept_argmax_kernel<true, kEbf16>), dim3(plan.grid), dim3(kThreads), lds, stream, A);
+      else
+        hipLaunchKernelGGL((accept_argmax_kernel<false, kEf32>), dim3(plan.grid), dim3(kThreads), lds, stream, A);
+      if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
+      hipLaunchKernelGGL(accept_finish_greedy_kernel, dim3(Bl), dim3(64 * nw), 0, stream, A);
+      if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
+      continue;
+    }
     if (dtype == SR_BF16)
       hipLaunchKernelGGL((accept_sweep_kernel<true, kEbf16>), dim3(plan.grid), dim3(kThreads), lds, stream, A);
     else

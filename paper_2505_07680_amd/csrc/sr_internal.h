@@ -143,6 +143,32 @@ __device__ __forceinline__ float sum_across_rows(float x) {
   return e + o;
 }
 
+__device__ __forceinline__ int wave_min_i(int x) {
+  x = min(x, (int)dpp_u32<dpp::kXor1>((uint32_t)x));
+  x = min(x, (int)dpp_u32<dpp::kXor2>((uint32_t)x));
+  x = min(x, (int)dpp_u32<dpp::kHalfMirror>((uint32_t)x));
+  x = min(x, (int)dpp_u32<dpp::kMirror>((uint32_t)x));
+  uint32_t e, o;
+  swap_halves<false>((uint32_t)x, e, o);
+  x = min((int)e, (int)o);
+  swap_halves<true>((uint32_t)x, e, o);
+  return min((int)e, (int)o);
+}
+
+// Wave-wide inclusive prefix sum of an int in ascending lane order: DPP row
+// shifts inside each 16-lane row (lanes without a source read 0), then the
+// totals of the earlier rows.
+__device__ __forceinline__ int wave_incl_scan_i(int x) {
+  x += (int)dpp_u32<0x111>((uint32_t)x);  // row_shr:1
+  x += (int)dpp_u32<0x112>((uint32_t)x);  // row_shr:2
+  x += (int)dpp_u32<0x114>((uint32_t)x);  // row_shr:4
+  x += (int)dpp_u32<0x118>((uint32_t)x);  // row_shr:8
+  const int r0 = __builtin_amdgcn_readlane(x, 15), r1 = __builtin_amdgcn_readlane(x, 31);
+  const int r2 = __builtin_amdgcn_readlane(x, 47);
+  const int row = (threadIdx.x & 63) >> 4;
+  return x + (row == 0 ? 0 : row == 1 ? r0 : row == 2 ? r0 + r1 : r0 + r1 + r2);
+}
+
 // The value of lane `src` (wave-uniform) in every lane.
 __device__ __forceinline__ int lane_value(int x, int src) { return __builtin_amdgcn_readlane(x, src); }
 __device__ __forceinline__ double lane_value(double x, int src) {
@@ -233,7 +259,7 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
                   int dtype, const int32_t* drafts, const int32_t* gamma, const float* u_acc,
                   const float* u_res, const int32_t* kv_len, int32_t* accept_len,
                   int32_t* out_tokens, int32_t* new_len, float* accept_prob, float* p_tok,
-                  float* q_tok, float* kl, float* tv, int B, int gamma_max, int V,
+                  float* q_tok, float* kl, float* tv, int B, int gamma_max, int V, float temperature,
                   void* workspace, const AcceptPlan& plan, int32_t* status, hipStream_t stream);
 
 int launch_rollback(int32_t* kv_len, uint8_t* cache_mask, const int32_t* new_len,

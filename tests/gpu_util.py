@@ -42,7 +42,7 @@ def run_attention(inp, mask=None, q=None):
 
 
 def run_accept(p_logits, q_logits, drafts, gamma, u_acc, u_res, kv_len=None, bufs=None,
-               p_dev=None, q_dev=None):
+               p_dev=None, q_dev=None, temperature=None):
     B, G1, V = p_logits.shape if p_dev is None else p_dev.shape
     code = sr.SR_BF16 if (p_dev is None and p_logits.dtype == np.uint16) or (
         p_dev is not None and p_dev.element_size() == 2) else sr.SR_F32
@@ -52,12 +52,15 @@ def run_accept(p_logits, q_logits, drafts, gamma, u_acc, u_res, kv_len=None, buf
         bufs = sr.AcceptBuffers(B, G1 - 1, V, code)
     bufs.status.zero_()
     kvd = None if kv_len is None else dev(np.asarray(kv_len, np.int32))
-    sr.specrouter_accept_and_diverge(
-        pd, qd, dev(np.asarray(drafts, np.int32)), dev(np.asarray(gamma, np.int32)),
-        dev(np.asarray(u_acc, np.float32)), dev(np.asarray(u_res, np.float32)), kvd,
-        bufs.accept_len, bufs.out_tokens, bufs.new_len if kvd is not None else None,
-        bufs.accept_prob, bufs.p_tok, bufs.q_tok, bufs.kl, bufs.tv, bufs.workspace, bufs.status,
-    )
+    args = (pd, qd, dev(np.asarray(drafts, np.int32)), dev(np.asarray(gamma, np.int32)),
+            None if u_acc is None else dev(np.asarray(u_acc, np.float32)),
+            None if u_res is None else dev(np.asarray(u_res, np.float32)), kvd,
+            bufs.accept_len, bufs.out_tokens, bufs.new_len if kvd is not None else None,
+            bufs.accept_prob, bufs.p_tok, bufs.q_tok, bufs.kl, bufs.tv, bufs.workspace, bufs.status)
+    if temperature is None:
+        sr.specrouter_accept_and_diverge(*args)
+    else:
+        sr.specrouter_accept_and_diverge_sampled(*args, temperature=temperature)
     torch.cuda.synchronize()
     res = dict(
         accept_len=host(bufs.accept_len), out_tokens=host(bufs.out_tokens),

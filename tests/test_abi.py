@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.specrouter_abi_version() == 1
+    assert lib.specrouter_abi_version() == 2
     for code in (0, -1, -2, -3, -4, 1, 2, 4, 8, 16, 32):
         s = lib.specrouter_status_string(code)
         assert s and s != b"unknown code"
@@ -94,6 +94,31 @@ def test_accept_rejects_bad_host_arguments(lib):
     bad = list(base)
     bad[2] = None  # q_logits missing with gamma_max > 0
     assert lib.specrouter_accept_and_diverge(*bad) == _lib.SR_EINVAL
+
+
+@no_device
+def test_sampled_accept_rejects_bad_sampling_parameters(lib):
+    p = ctypes.c_void_p(4096)
+    B, G, V = 2, 4, 1000
+    S = _lib.SamplingParams
+
+    def call(sampling, u_acc=p, u_res=p):
+        args = ([p, (G + 1) * V, p, G * V, _lib.SR_F32, p, p, u_acc, u_res, None, p, p] + [None] * 6
+                + [B, G, V, None if sampling is None else ctypes.byref(sampling), None, 0, None, None])
+        return lib.specrouter_accept_and_diverge_sampled(*args)
+
+    # valid sampling parameters pass the argument checks and stop at the launch
+    # plan (no device here) or the empty workspace
+    later = (_lib.SR_EWORKSPACE, _lib.SR_ELAUNCH)
+    assert call(None) in later
+    assert call(S(0.7, 0, 1.0)) in later
+    assert call(S(0.0, 0, 1.0), u_acc=None, u_res=None) in later  # greedy reads no uniforms
+    for t in (-0.5, float("nan"), float("inf")):
+        assert call(S(t, 0, 1.0)) == _lib.SR_EINVAL
+    assert call(S(1.0, 5, 1.0)) == _lib.SR_EUNSUPPORTED
+    assert call(S(1.0, 0, 0.9)) == _lib.SR_EUNSUPPORTED
+    assert call(S(0.5, 0, 1.0), u_acc=None) == _lib.SR_EINVAL  # sampling needs the uniforms
+    assert call(S(0.5, 0, 1.0), u_res=None) == _lib.SR_EINVAL
 
 
 @no_device

@@ -1,0 +1,126 @@
+"""GPU parity of the sampling variants (specrouter_accept_and_diverge_sampled)
+against the CPU reference on the same seeded inputs:
+
+  * temperature T > 0: the tolerances of the plain rule (lengths and tokens
+    bit-exact outside boundary cases, probabilities 1e-5, divergences 1e-4);
+  * greedy (T = 0): every output exact -- lengths, tokens (lowest index among
+    equal maxima, also across chunks), and the 0/1/+inf per-position values.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from workloads import CONFIGS, level_inputs, small_shape
+from workloads.gen import bf16_bits_from_f32
+
+from gpu_util import check_accept, run_accept
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _library():
+    import paper_2505_07680_amd as sr
+
+    sr.load()
+    assert torch.cuda.is_available()
+    yield
+    torch.cuda.synchronize()
+
+
+def say(msg):
+    print(f"[gpu-test] {msg}", flush=True)
+
+
+SHAPES = [
+    small_shape(name="s-f32", B=7, V=5000, gamma=(0, 6), seed=41),
+    small_shape(name="s-bf16", B=6, V=12288, gamma=(1, 5), seed=42, logits="bf16"),
+    small_shape(name="s-f32-wide", B=3, V=128256, gamma=(2, 4), seed=43),
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: s.name)
+@pytest.mark.parametrize("T", [0.5, 1.7])
+def test_temperature_matches_reference(shape, T):
+    inp = level_inputs(shape, kv=False)
+    say(f"sampling {shape.name} T={T}")
+    got = run_accept(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, inp.u_acc, inp.u_res, temperature=T)
+    ref = oracle.accept_and_diverge(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, inp.u_acc, inp.u_res,
+                                    temperature=T)
+    assert got["status"] == ref["status"] == 0
+    nb, nbm = check_accept(got, ref)
+    say(f"  ok ({nb} boundary, {nbm} differ)")
+
+
+def _check_greedy(got, ref):
+    assert got["status"] == ref["status"]
+    np.testing.assert_array_equal(got["accept_len"], ref["accept_len"])
+    np.testing.assert_array_equal(got["out_tokens"], ref["out_tokens"])
+    for key in ("accept_prob", "p_tok", "q_tok", "tv", "kl"):
+        np.testing.assert_array_equal(got[key], ref[key].astype(np.float32), err_msg=key)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: s.name)
+def test_greedy_matches_reference(shape):
+    inp = level_inputs(shape, kv=False)
+    # drafts from the draft model's argmax half of the time, so that greedy accepts happen
+    from oracle.accept import decode_logits
+
+    q = decode_logits(inp.q_logits)
+    drafts = inp.drafts.copy()
+    rng = np.random.default_rng(shape.seed)
+    for b in range(shape.B):
+        for j in range(int(inp.gamma[b])):
+            if rng.random() < 0.5:
+                drafts[b, j] = int(np.argmax(q[b, j]))
+    say(f"greedy {shape.name}")
+    got = run_accept(inp.p_logits, inp.q_logits, drafts, inp.gamma, None, None, temperature=0.0)
+    ref = oracle.accept_and_diverge(inp.p_logits, inp.q_logits, drafts, inp.gamma, None, None, temperature=0.0)
+    _check_greedy(got, ref)
+    say(f"  ok (mean accepted {got['accept_len'].mean():.2f})")
+
+
+def test_greedy_ties_resolve_to_the_lowest_index_across_chunks():
+    B, G, V = 4, 3, 128256
+    rng = np.random.default_rng(7)
+    P = rng.normal(0, 1, (B, G + 1, V)).astype(np.float32)
+    Q = rng.normal(0, 1, (B, G, V)).astype(np.float32)
+    # equal maxima in different chunks, in different waves of one chunk, and in one lane
+    for b, spots in enumerate([(70000, 5000), (9000, 4100), (3, 1), (128255, 64)]):
+        for j in range(G + 1):
+            P[b, j, list(spots)] = 50.0
+        for j in range(G):
+            Q[b, j, list(spots)] = 40.0
+    drafts = np.tile(np.array([[5000, 4100, 1, 64]]).T, (1, G)).astype(np.int32)
+    gamma = np.full(B, G, np.int32)
+    got = run_accept(P, Q, drafts, gamma, None, None, temperature=0.0)
+    ref = oracle.accept_and_diverge(P, Q, drafts, gamma, None, None, temperature=0.0)
+    _check_greedy(got, ref)
+    assert (got["accept_len"] == G).all()
+    # bf16 logits tie often by themselves
+    Pb, Qb = bf16_bits_from_f32(np.round(P)), bf16_bits_from_f32(np.round(Q))
+    got = run_accept(Pb, Qb, drafts, gamma, None, None, temperature=0.0)
+    ref = oracle.accept_and_diverge(Pb, Qb, drafts, gamma, None, None, temperature=0.0)
+    _check_greedy(got, ref)
+
+
+def test_config2_shaped_temperature_and_greedy_sampled():
+    shape = CONFIGS[2]
+    inp = level_inputs(shape, kv=False)
+    seqs = [0, 5, 11, 15]
+    for T in (0.8, 0.0):
+        say(f"config2 T={T}")
+        ua = None if T == 0 else inp.u_acc
+        ur = None if T == 0 else inp.u_res
+        got = run_accept(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, ua, ur, temperature=T)
+        ref = oracle.accept_and_diverge(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, ua, ur, seqs=seqs,
+                                        temperature=T)
+        if T == 0:
+            for b in seqs:
+                assert got["accept_len"][b] == ref["accept_len"][b]
+                np.testing.assert_array_equal(got["out_tokens"][b], ref["out_tokens"][b])
+                np.testing.assert_array_equal(got["tv"][b], ref["tv"][b].astype(np.float32))
+        else:
+            check_accept(got, ref, seqs=seqs)
