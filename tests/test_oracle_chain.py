@@ -168,8 +168,8 @@ def test_a_wrong_target_draft_distribution_breaks_losslessness():
 
 
 def test_window_and_consensus_edge_cases():
-    g, d = chain.window([0, 4, 9, -1], [[7, -1, -1], [1, 2, 3], [1, 2, 3], [0, 0, 0]], 4)
-    assert list(g) == [1, 4, -1, -1]  # k = 9 cannot come from 3 emitted slots
+    g, d = chain.window([0, 4, 9, -1], [[7, -1, -1, -1, -1], [1, 2, 3, 4, 5], [1, 2, 3, 4, 5], [0] * 5], 4)
+    assert list(g) == [1, 4, -1, -1]  # k = 9 cannot come from 5 emitted slots
     assert list(d[0]) == [7, 0, 0, 0] and list(d[3]) == [0, 0, 0, 0]
     up, lo, pend, n = chain.consensus([5, 5, 5], [0, 3, 2], [1, 0, -1], [[8, -1], [1, 2, 3, 4], [1, 2, 3]],
                                       [[8, 9], [6, -1], [-1]])
