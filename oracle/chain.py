@@ -31,6 +31,8 @@ from __future__ import annotations
 
 import numpy as np
 
+ST_CHAIN = 64  # accept lengths that one chain step cannot produce
+
 
 def window(accept_len, out_tokens, gamma_cap: int):
     """Next verifier level's window and drafts from the level below:
@@ -57,8 +59,11 @@ def consensus(ctx_len, k_lower, k_upper, out_lower, out_upper):
     pending for the next step: the lower level's own correction token when the
     upper level accepted it (k_upper = k_lower + 1), then the upper level's
     correction or bonus token. A sequence either level flagged (k < 0) keeps
-    ctx rows everywhere and gets no pending token.
-    Returns (len_upper, len_lower, pending [B, 2] padded with -1, n_pending)."""
+    ctx rows everywhere and gets no pending token; so does one whose lengths
+    cannot come from one chain step (k_upper > k_lower + 1, or an accept
+    length past its level's window), which also sets status bit ST_CHAIN.
+    Returns (len_upper, len_lower, pending [B, 2] padded with -1, n_pending,
+    status)."""
     ctx = np.asarray(ctx_len, dtype=np.int64)
     kl = np.asarray(k_lower, dtype=np.int64)
     ku = np.asarray(k_upper, dtype=np.int64)
@@ -67,9 +72,15 @@ def consensus(ctx_len, k_lower, k_upper, out_lower, out_upper):
     lo = np.empty(B, dtype=np.int32)
     pend = np.full((B, 2), -1, dtype=np.int32)
     npend = np.zeros(B, dtype=np.int32)
+    status = 0
+    wl, wu = (len(out_lower[0]), len(out_upper[0])) if B else (0, 0)
     for b in range(B):
         if kl[b] < 0 or ku[b] < 0:
             up[b] = lo[b] = ctx[b]
+            continue
+        if ku[b] > kl[b] + 1 or kl[b] >= wl or ku[b] >= wu:
+            up[b] = lo[b] = ctx[b]
+            status |= ST_CHAIN
             continue
         up[b] = ctx[b] + 1 + ku[b]
         lo[b] = ctx[b] + 1 + min(kl[b], ku[b])
@@ -79,7 +90,7 @@ def consensus(ctx_len, k_lower, k_upper, out_lower, out_upper):
         toks.append(int(out_upper[b][ku[b]]))
         pend[b, : len(toks)] = toks
         npend[b] = len(toks)
-    return up, lo, pend, npend
+    return up, lo, pend, npend, status
 
 
 def target_window(accept_len_int, gamma_tgt: int) -> np.ndarray:

@@ -111,7 +111,8 @@ def chain_outcomes(m, prefix, gamma2, gamma_cap):
             for p3, k3, e3 in verify_outcomes(m, prefix, drafts3, 3, 2):
                 out3 = np.full((1, gamma_cap + 1), -1)
                 out3[0, : k3 + 1] = e3
-                up, lo, pend, npend = chain.consensus([len(prefix)], [k2], [k3], out2, out3)
+                up, lo, pend, npend, st = chain.consensus([len(prefix)], [k2], [k3], out2, out3)
+                assert st == 0
                 # the emitted sequence and the rows each level keeps
                 assert e3[:k3] == e2[:k3]
                 assert up[0] == len(prefix) + 1 + k3 and lo[0] == len(prefix) + 1 + min(k2, k3)
@@ -171,9 +172,11 @@ def test_window_and_consensus_edge_cases():
     g, d = chain.window([0, 4, 9, -1], [[7, -1, -1, -1, -1], [1, 2, 3, 4, 5], [1, 2, 3, 4, 5], [0] * 5], 4)
     assert list(g) == [1, 4, -1, -1]  # k = 9 cannot come from 5 emitted slots
     assert list(d[0]) == [7, 0, 0, 0] and list(d[3]) == [0, 0, 0, 0]
-    up, lo, pend, n = chain.consensus([5, 5, 5], [0, 3, 2], [1, 0, -1], [[8, -1], [1, 2, 3, 4], [1, 2, 3]],
-                                      [[8, 9], [6, -1], [-1]])
-    assert list(up) == [7, 6, 5] and list(lo) == [6, 6, 5]
+    up, lo, pend, n, st = chain.consensus([5, 5, 5, 5], [0, 3, 2, 1], [1, 0, -1, 3],
+                                          [[8, -1, -1, -1]] + [[1, 2, 3, 4]] * 3,
+                                          [[8, 9, -1, -1]] + [[6, -1, -1, -1]] * 3)
+    assert list(up) == [7, 6, 5, 5] and list(lo) == [6, 6, 5, 5]
+    assert st == chain.ST_CHAIN and n[3] == 0  # k_upper = 3 > k_lower + 1: not one chain step
     assert list(pend[0]) == [8, 9] and n[0] == 2          # the target accepted M2's correction token
     assert list(pend[1]) == [6, -1] and n[1] == 1
     assert n[2] == 0                                       # flagged upstream: nothing kept, nothing pending
