@@ -235,6 +235,35 @@ def main():
         us = e0.elapsed_time(e1) / K * 1e3
         name = "accept_greedy" if T == 0 else f"accept_temperature_{T}"
         variants[name] = {"us": round(us, 2), "GB/s": round(acc_bytes / us / 1e3, 1)}
+    # chain glue between two verifier levels (window of a gamma-4 upper level
+    # and the consensus), on this step's accept outputs as the lower level
+    s = sets[0]
+    a = s["acc"]
+    cap4 = 4
+    g_n = torch.empty(B, dtype=torch.int32, device=dev)
+    d_n = torch.empty((B, cap4), dtype=torch.int32, device=dev)
+    kv_n = torch.empty(B, dtype=torch.int32, device=dev)
+    ctx_n = (s["kv_in"] - s["gamma"] - 1).contiguous()
+    lu, ll = torch.empty_like(g_n), torch.empty_like(g_n)
+    pend, npend = torch.empty((B, 2), dtype=torch.int32, device=dev), torch.empty_like(g_n)
+    ku = torch.zeros(B, dtype=torch.int32, device=dev)
+    ou = torch.zeros((B, cap4 + 1), dtype=torch.int32, device=dev)
+    glue = {}
+    for name, fn in (("window", lambda: sr.specrouter_chain_window(a.accept_len, a.out_tokens, cap4, g_n, d_n,
+                                                                   ctx_len=ctx_n, kv_len_next=kv_n)),
+                     ("consensus", lambda: sr.specrouter_chain_consensus(ctx_n, a.accept_len, a.out_tokens, ku, ou,
+                                                                         lu, ll, pend, npend, s["st"]))):
+        for _ in range(args.warmup):
+            fn()
+        e0, e1 = ev(), ev()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(K):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        glue[name + "_us"] = round(e0.elapsed_time(e1) / K * 1e3, 2)
+    variants["chain_glue"] = glue
     status |= int(sum(int(s["st"].item()) for s in sets))
 
     cpu = None

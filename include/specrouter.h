@@ -76,6 +76,7 @@ enum {
   SR_ST_UNIFORM = 8,        /* a needed uniform outside [0, 1) (NaN included) */
   SR_ST_ROLLBACK_GROW = 16, /* rollback asked to grow a sequence (treated as a no-op) */
   SR_ST_TIMEOUT = 32,       /* an inter-workgroup wait gave up (results of that call are invalid) */
+  SR_ST_CHAIN = 64,         /* accept lengths that one chain step cannot produce */
 };
 
 /* SPECROUTER_ABI_VERSION of the loaded library. */
@@ -224,6 +225,64 @@ int specrouter_accept_and_diverge_sampled(const void* p_logits, int64_t p_batch_
  */
 int specrouter_rollback(int32_t* kv_len, uint8_t* cache_mask, const int32_t* new_len,
                         int32_t* phys_len, int B, int L_cap, int32_t* status, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Multi-level chains (Section 3.1, multi-level verification; Section 4.3,
+ * VerifyProcessor repeated per level and RollbackProcessor's consensus).
+ *
+ * A chain step with drafter M1, an intermediate verifier and an upper
+ * verifier is: the intermediate level's verify step (attention, accept),
+ * specrouter_chain_window, the upper level's verify step with q_logits set to
+ * the intermediate level's p_logits rows (a strided view), then
+ * specrouter_chain_consensus and one specrouter_rollback per level. The
+ * tokens the upper level verifies are exact samples of the intermediate
+ * level's distribution and the window length is fixed before each of them is
+ * drawn, so the step emits tokens of the upper level's distribution. Longer
+ * chains repeat the pair of calls level by level.
+ */
+
+/* Window of the next verifier level (device pointers; stream as above).
+ * accept_len  i32 [B]: k_b of the level below (-1 for a flagged sequence)
+ * out_tokens  i32 [B][gamma_max+1]: its emitted tokens
+ * gamma_cap   the next level's window limit (1..SPECROUTER_MAX_GAMMA)
+ * ctx_len     i32 [B] or NULL: committed context length (without the pending
+ *             token) of the next level's cache
+ * gamma_next  i32 [B] out: min(k_b + 1, gamma_cap), or -1 when k_b < 0 or
+ *             k_b > gamma_max (the next level then flags SR_ST_GAMMA)
+ * drafts_next i32 [B][gamma_cap] out: the first gamma_next_b emitted tokens,
+ *             then 0
+ * kv_len_next i32 [B] out or NULL (NULL exactly when ctx_len is NULL):
+ *             ctx_len_b + 1 + max(gamma_next_b, 0), the next level's length
+ *             once its K/V rows for the pending token and the drafts are
+ *             written */
+int specrouter_chain_window(const int32_t* accept_len, const int32_t* out_tokens, int B,
+                            int gamma_max, int gamma_cap, const int32_t* ctx_len,
+                            int32_t* gamma_next, int32_t* drafts_next, int32_t* kv_len_next,
+                            void* stream);
+
+/* Consensus after the upper level (device pointers).
+ * ctx_len    i32 [B]: committed context length before the step (every level
+ *            then holds one row for the previous step's pending token)
+ * k_lower, out_lower [B], [B][gamma_max_lower+1]: the intermediate level's
+ *            accept lengths and emitted tokens
+ * k_upper, out_upper [B], [B][gamma_max_upper+1]: the upper level's
+ * len_upper  i32 [B] out: ctx + 1 + k_upper (rows the upper level keeps)
+ * len_lower  i32 [B] out: ctx + 1 + min(k_lower, k_upper) (rows the
+ *            intermediate and draft levels keep)
+ * pending    i32 [B][2] out: the tokens the lower levels must run first in
+ *            the next step -- out_lower[k_lower] when k_upper == k_lower + 1,
+ *            then out_upper[k_upper] -- padded with -1; the upper level's only
+ *            pending token is the last of them
+ * n_pending  i32 [B] out: 1 or 2 (0 for a sequence a level flagged)
+ * A flagged sequence (k < 0) keeps ctx rows and gets no pending token; so does
+ * one whose lengths one chain step cannot produce (k_upper > k_lower + 1 or a
+ * length past its window), which also sets SR_ST_CHAIN in *status. */
+int specrouter_chain_consensus(const int32_t* ctx_len, const int32_t* k_lower,
+                               const int32_t* out_lower, int gamma_max_lower,
+                               const int32_t* k_upper, const int32_t* out_upper,
+                               int gamma_max_upper, int B, int32_t* len_upper,
+                               int32_t* len_lower, int32_t* pending, int32_t* n_pending,
+                               int32_t* status, void* stream);
 
 #ifdef __cplusplus
 }

@@ -19,6 +19,8 @@ from ._lib import (
     specrouter_accept_and_diverge,
     specrouter_accept_and_diverge_sampled,
     specrouter_accept_workspace_size,
+    specrouter_chain_consensus,
+    specrouter_chain_window,
     specrouter_rollback,
     specrouter_status_string,
     specrouter_verify_attention,
@@ -36,6 +38,8 @@ __all__ = [
     "specrouter_accept_and_diverge",
     "specrouter_accept_and_diverge_sampled",
     "specrouter_accept_workspace_size",
+    "specrouter_chain_consensus",
+    "specrouter_chain_window",
     "specrouter_rollback",
     "specrouter_status_string",
     "specrouter_verify_attention",

@@ -22,7 +22,7 @@ HEADERS = [os.path.join(INCLUDE, "specrouter.h"), os.path.join(INCLUDE, "specrou
 
 SR_OK, SR_EINVAL, SR_EUNSUPPORTED, SR_EWORKSPACE, SR_ELAUNCH = 0, -1, -2, -3, -4
 SR_F32, SR_BF16 = 0, 1
-SR_ST_GAMMA, SR_ST_KVLEN, SR_ST_TOKEN, SR_ST_UNIFORM, SR_ST_ROLLBACK_GROW, SR_ST_TIMEOUT = 1, 2, 4, 8, 16, 32
+SR_ST_GAMMA, SR_ST_KVLEN, SR_ST_TOKEN, SR_ST_UNIFORM, SR_ST_ROLLBACK_GROW, SR_ST_TIMEOUT, SR_ST_CHAIN = 1, 2, 4, 8, 16, 32, 64
 
 _c_p = ctypes.c_void_p
 _c_i = ctypes.c_int
@@ -58,6 +58,8 @@ _SIGNATURES = {
         + [ctypes.POINTER(SamplingParams), _c_p, _c_sz, _c_p, _c_p],
     ),
     "specrouter_rollback": (_c_i, [_c_p] * 4 + [_c_i, _c_i, _c_p, _c_p]),
+    "specrouter_chain_window": (_c_i, [_c_p, _c_p, _c_i, _c_i, _c_i] + [_c_p] * 5),
+    "specrouter_chain_consensus": (_c_i, [_c_p, _c_p, _c_p, _c_i, _c_p, _c_p, _c_i, _c_i] + [_c_p] * 6),
     # chain scheduler (host code; host pointers)
     "specrouter_sched_create": (_c_i, [_c_i, _c_dp, _c_i, _c_i, _c_i, _c_d, _c_d, _c_d, ctypes.POINTER(_c_p)]),
     "specrouter_sched_destroy": (None, [_c_p]),
@@ -252,6 +254,39 @@ def specrouter_rollback(kv_len, cache_mask, new_len, phys_len=None, status=None,
     rc = load().specrouter_rollback(_ptr(kv_len), _ptr(cache_mask), _ptr(new_len), _ptr(phys_len),
                                     B, int(L_cap), _ptr(status), _stream())
     _check(rc, "specrouter_rollback")
+
+
+def specrouter_chain_window(accept_len, out_tokens, gamma_cap, gamma_next, drafts_next, ctx_len=None,
+                            kv_len_next=None):
+    """accept_len [B], out_tokens [B, gmax+1] of the level below -> gamma_next [B],
+    drafts_next [B, gamma_cap] (and kv_len_next [B] from ctx_len [B])."""
+    _dev(accept_len, out_tokens, gamma_next, drafts_next, ctx_len, kv_len_next)
+    for t, n in ((accept_len, "accept_len"), (out_tokens, "out_tokens"), (gamma_next, "gamma_next"),
+                 (drafts_next, "drafts_next"), (ctx_len, "ctx_len"), (kv_len_next, "kv_len_next")):
+        _i32(t, n)
+    B, G1 = out_tokens.shape
+    if drafts_next.shape != (B, gamma_cap) or gamma_next.shape != (B,) or accept_len.shape != (B,):
+        raise ValueError("accept_len [B], gamma_next [B] and drafts_next [B, gamma_cap] expected")
+    rc = load().specrouter_chain_window(_ptr(accept_len), _ptr(out_tokens), B, G1 - 1, int(gamma_cap),
+                                        _ptr(ctx_len), _ptr(gamma_next), _ptr(drafts_next), _ptr(kv_len_next),
+                                        _stream())
+    _check(rc, "specrouter_chain_window")
+
+
+def specrouter_chain_consensus(ctx_len, k_lower, out_lower, k_upper, out_upper, len_upper, len_lower, pending,
+                               n_pending, status=None):
+    """Rows each level keeps after a two-level verify and the pending tokens."""
+    _dev(ctx_len, k_lower, out_lower, k_upper, out_upper, len_upper, len_lower, pending, n_pending, status)
+    for t in (ctx_len, k_lower, out_lower, k_upper, out_upper, len_upper, len_lower, pending, n_pending):
+        _i32(t, "chain tensor")
+    B = ctx_len.shape[0]
+    if pending.shape != (B, 2) or out_lower.shape[0] != B or out_upper.shape[0] != B:
+        raise ValueError("pending [B, 2], out_lower [B, gl+1], out_upper [B, gu+1] expected")
+    rc = load().specrouter_chain_consensus(_ptr(ctx_len), _ptr(k_lower), _ptr(out_lower), out_lower.shape[1] - 1,
+                                           _ptr(k_upper), _ptr(out_upper), out_upper.shape[1] - 1, B,
+                                           _ptr(len_upper), _ptr(len_lower), _ptr(pending), _ptr(n_pending),
+                                           _ptr(status), _stream())
+    _check(rc, "specrouter_chain_consensus")
 
 
 # ----------------------------------------------------------------------------

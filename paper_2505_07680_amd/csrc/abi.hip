@@ -53,6 +53,7 @@ const char* specrouter_status_string(int code) {
     case SR_ST_UNIFORM: return "device data: uniform outside [0, 1)";
     case SR_ST_ROLLBACK_GROW: return "device data: rollback would grow a sequence (ignored)";
     case SR_ST_TIMEOUT: return "device: inter-workgroup wait timed out";
+    case SR_ST_CHAIN: return "device data: accept lengths one chain step cannot produce";
     default: return "unknown code";
   }
 }
@@ -146,6 +147,30 @@ int specrouter_accept_and_diverge(const void* p_logits, int64_t p_batch_stride,
                                                kv_len, accept_len, out_tokens, new_len, accept_prob, p_tok,
                                                q_tok, kl, tv, B, gamma_max, V, nullptr, workspace,
                                                workspace_bytes, status, stream);
+}
+
+int specrouter_chain_window(const int32_t* accept_len, const int32_t* out_tokens, int B, int gamma_max,
+                            int gamma_cap, const int32_t* ctx_len, int32_t* gamma_next, int32_t* drafts_next,
+                            int32_t* kv_len_next, void* stream) {
+  if (B <= 0 || gamma_max < 0 || gamma_max > SPECROUTER_MAX_GAMMA) return SR_EINVAL;
+  if (gamma_cap < 1 || gamma_cap > SPECROUTER_MAX_GAMMA) return SR_EINVAL;
+  if (!accept_len || !out_tokens || !gamma_next || !drafts_next) return SR_EINVAL;
+  if ((ctx_len == nullptr) != (kv_len_next == nullptr)) return SR_EINVAL;
+  return sr::launch_chain_window(accept_len, out_tokens, B, gamma_max, gamma_cap, ctx_len, gamma_next, drafts_next,
+                                 kv_len_next, (hipStream_t)stream);
+}
+
+int specrouter_chain_consensus(const int32_t* ctx_len, const int32_t* k_lower, const int32_t* out_lower,
+                               int gamma_max_lower, const int32_t* k_upper, const int32_t* out_upper,
+                               int gamma_max_upper, int B, int32_t* len_upper, int32_t* len_lower,
+                               int32_t* pending, int32_t* n_pending, int32_t* status, void* stream) {
+  if (B <= 0 || gamma_max_lower < 0 || gamma_max_lower > SPECROUTER_MAX_GAMMA) return SR_EINVAL;
+  if (gamma_max_upper < 0 || gamma_max_upper > SPECROUTER_MAX_GAMMA) return SR_EINVAL;
+  if (!ctx_len || !k_lower || !out_lower || !k_upper || !out_upper) return SR_EINVAL;
+  if (!len_upper || !len_lower || !pending || !n_pending) return SR_EINVAL;
+  return sr::launch_chain_consensus(ctx_len, k_lower, out_lower, gamma_max_lower, k_upper, out_upper,
+                                    gamma_max_upper, B, len_upper, len_lower, pending, n_pending, status,
+                                    (hipStream_t)stream);
 }
 
 int specrouter_rollback(int32_t* kv_len, uint8_t* cache_mask, const int32_t* new_len,

@@ -262,6 +262,14 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
                   float* q_tok, float* kl, float* tv, int B, int gamma_max, int V, float temperature,
                   void* workspace, const AcceptPlan& plan, int32_t* status, hipStream_t stream);
 
+int launch_chain_window(const int32_t* accept_len, const int32_t* out_tokens, int B, int gmax, int cap,
+                        const int32_t* ctx_len, int32_t* gamma_next, int32_t* drafts_next,
+                        int32_t* kv_len_next, hipStream_t stream);
+int launch_chain_consensus(const int32_t* ctx_len, const int32_t* k_lower, const int32_t* out_lower,
+                           int gmax_lower, const int32_t* k_upper, const int32_t* out_upper, int gmax_upper,
+                           int B, int32_t* len_upper, int32_t* len_lower, int32_t* pending,
+                           int32_t* n_pending, int32_t* status, hipStream_t stream);
+
 int launch_rollback(int32_t* kv_len, uint8_t* cache_mask, const int32_t* new_len,
                     int32_t* phys_len, int B, int L_cap, int32_t* status, hipStream_t stream);
 

@@ -38,7 +38,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 def test_version_and_status_strings(lib):
     assert lib.specrouter_abi_version() == 2
-    for code in (0, -1, -2, -3, -4, 1, 2, 4, 8, 16, 32):
+    for code in (0, -1, -2, -3, -4, 1, 2, 4, 8, 16, 32, 64):
         s = lib.specrouter_status_string(code)
         assert s and s != b"unknown code"
     assert lib.specrouter_status_string(12345) == b"unknown code"
@@ -119,6 +119,24 @@ def test_sampled_accept_rejects_bad_sampling_parameters(lib):
     assert call(S(1.0, 0, 0.9)) == _lib.SR_EUNSUPPORTED
     assert call(S(0.5, 0, 1.0), u_acc=None) == _lib.SR_EINVAL  # sampling needs the uniforms
     assert call(S(0.5, 0, 1.0), u_res=None) == _lib.SR_EINVAL
+
+
+@no_device
+def test_chain_calls_reject_bad_host_arguments(lib):
+    p = ctypes.c_void_p(4096)
+    win = [p, p, 4, 8, 4, None, p, p, None, None]
+    for i, v in ((2, 0), (3, -1), (3, 17), (4, 0), (4, 17), (0, None), (7, None)):
+        bad = list(win)
+        bad[i] = v
+        assert lib.specrouter_chain_window(*bad) == _lib.SR_EINVAL
+    bad = list(win)
+    bad[5] = p  # ctx_len without kv_len_next
+    assert lib.specrouter_chain_window(*bad) == _lib.SR_EINVAL
+    con = [p, p, p, 8, p, p, 4, 4, p, p, p, p, None, None]
+    for i, v in ((3, -1), (6, 17), (7, 0), (0, None), (2, None), (10, None)):
+        bad = list(con)
+        bad[i] = v
+        assert lib.specrouter_chain_consensus(*bad) == _lib.SR_EINVAL
 
 
 @no_device
