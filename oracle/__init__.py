@@ -14,7 +14,10 @@ Plain, slow, fp64 numpy code written from the paper (arXiv 2505.07680):
   * rollback.rollback -- logical rollback of each sequence's cache to its
     accepted prefix and the common physical length (Section 4.4, Eq. 9);
   * chain -- glue of the three-level chain (which tokens and lengths the next
-    level sees, and each level's rollback target).
+    level sees, and each level's rollback target);
+  * kvcache -- appending a step's K/V rows at a per-sequence or shared
+    cursor, compaction of the valid rows, Eq. 9's physical truncation
+    (Section 4.4).
 
 It shares no code with the HIP path: inputs arrive as plain numpy arrays
 (bf16 as raw uint16 bit patterns, decoded here) and outputs are returned as
@@ -24,7 +27,7 @@ numpy arrays.
 from .accept import accept_and_diverge, decode_logits
 from .attention import decode_bf16, verify_attention
 from .rollback import rollback
-from . import chain
+from . import chain, kvcache
 
 ST_GAMMA = 1
 ST_KVLEN = 2
@@ -39,6 +42,7 @@ __all__ = [
     "verify_attention",
     "rollback",
     "chain",
+    "kvcache",
     "ST_GAMMA",
     "ST_KVLEN",
     "ST_TOKEN",
