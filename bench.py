@@ -264,6 +264,46 @@ def main():
         torch.cuda.synchronize()
         glue[name + "_us"] = round(e0.elapsed_time(e1) / K * 1e3, 2)
     variants["chain_glue"] = glue
+
+    # KV-cache state: append this step's rows (per-sequence cursors) and
+    # compact a cache with 2% holes, on scratch caches of the workload's shape
+    kc = torch.empty_like(sets[0]["k"])
+    vc = torch.empty_like(sets[0]["v"])
+    kn = torch.empty((B, G1, Hkv, D), dtype=torch.int16, device=dev).random_(-(1 << 14), 1 << 14)
+    vn = torch.empty_like(kn)
+    ctx_len = (s["kv_in"] - s["gamma"] - 1).contiguous()
+    kvw = ctx_len.clone()
+    mk = s["mask_in"].clone()
+    e0, e1 = ev(), ev()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(K):
+        kvw.copy_(ctx_len)
+        sr.specrouter_kv_append(kn, vn, s["gamma"], kc, vc, mk, kvw, status=s["st"])
+    e1.record()
+    torch.cuda.synchronize()
+    app_us = e0.elapsed_time(e1) / K * 1e3
+    holes = torch.rand((B, cap), device=dev) < 0.02
+    mask_h = (s["mask_in"].bool() & ~holes).to(torch.uint8)
+    first = [int(np.argmax(~(mask_h[b, : inp.kv_len[b]].cpu().numpy().astype(bool)))) for b in range(B)]
+    moved = int(sum(int(inp.kv_len[b]) - first[b] for b in range(B)))  # rows from the first hole on (upper bound)
+    comp_ms = []
+    for i in range(max(3, K // 20)):
+        mk.copy_(mask_h)
+        kvw.copy_(s["kv_in"])
+        c0, c1 = ev(), ev()
+        c0.record()
+        sr.specrouter_kv_compact(kc, vc, mk, kvw, s["st"])
+        c1.record()
+        torch.cuda.synchronize()
+        comp_ms.append(c0.elapsed_time(c1))
+    comp_us = float(np.median(comp_ms)) * 1e3
+    comp_bytes = moved * Hkv * D * 2 * 2 * 2  # K and V rows, read and written
+    variants["kv_state"] = {
+        "append_us": round(app_us, 2), "append_bytes": int(B * G1 * Hkv * D * 2 * 2 * 2),
+        "compact_us": round(comp_us, 2), "compact_GB/s": round(comp_bytes / comp_us / 1e3, 1),
+        "compact_note": "2% random holes; bytes = rows from each sequence's first hole, read and written",
+    }
     status |= int(sum(int(s["st"].item()) for s in sets))
 
     cpu = None

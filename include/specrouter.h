@@ -227,6 +227,40 @@ int specrouter_rollback(int32_t* kv_len, uint8_t* cache_mask, const int32_t* new
                         int32_t* phys_len, int B, int L_cap, int32_t* status, void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* KV-cache state (Section 4.4, StateManager: logical validity mask, Eq. 8;
+ * rollback and physical truncation, Eq. 9). Device pointers; cache layout as
+ * for specrouter_verify_attention; D in {64, 128}; K/V bytes are moved
+ * verbatim.
+ *
+ * specrouter_kv_append: write a step's new rows -- the pending token and the
+ * drafts, gamma_b + 1 rows of k_new/v_new bf16 [B][gamma_max+1][Hkv][D]
+ * (16-byte aligned) -- at the sequence's cursor, mark them valid in
+ * cache_mask (if not NULL) and set kv_len[b] = cursor + gamma_b + 1. The
+ * cursor is kv_len[b] when shared_len is NULL (per-sequence layout), else
+ * *shared_len, one physical length for the whole batch (the paper's layout:
+ * a sequence that rolled back further than the others keeps masked holes
+ * between its last valid row and the shared length; rows are never shifted).
+ * A sequence with gamma_b outside [0, gamma_max] (SR_ST_GAMMA), kv_len[b]
+ * outside [0, L_cap] or cursor + gamma_b + 1 > L_cap (SR_ST_KVLEN) is left
+ * untouched. *shared_len is not changed: after a rollback it is the
+ * rollback's phys_len (Eq. 9's L - r_min); after an append it is the largest
+ * new kv_len.
+ *
+ * specrouter_kv_compact: reclaim the holes. For every sequence the rows j <
+ * kv_len[b] with cache_mask[b][j] != 0 move, in order and in place, to the
+ * front; the mask becomes 1 on [0, n) and 0 on [n, old kv_len[b]); kv_len[b]
+ * = n. Rows past n keep stale bytes (masked). Attention over the compacted
+ * cache equals attention over the holed one. Two kernels; reads and writes
+ * every K/V row from the first hole on.
+ */
+int specrouter_kv_append(const void* k_new, const void* v_new, const int32_t* gamma,
+                         void* k_cache, void* v_cache, uint8_t* cache_mask, int32_t* kv_len,
+                         const int32_t* shared_len, int B, int gamma_max, int Hkv, int D,
+                         int L_cap, int32_t* status, void* stream);
+int specrouter_kv_compact(void* k_cache, void* v_cache, uint8_t* cache_mask, int32_t* kv_len,
+                          int B, int Hkv, int D, int L_cap, int32_t* status, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Multi-level chains (Section 3.1, multi-level verification; Section 4.3,
  * VerifyProcessor repeated per level and RollbackProcessor's consensus).
  *

@@ -21,6 +21,8 @@ from ._lib import (
     specrouter_accept_workspace_size,
     specrouter_chain_consensus,
     specrouter_chain_window,
+    specrouter_kv_append,
+    specrouter_kv_compact,
     specrouter_rollback,
     specrouter_status_string,
     specrouter_verify_attention,
@@ -40,6 +42,8 @@ __all__ = [
     "specrouter_accept_workspace_size",
     "specrouter_chain_consensus",
     "specrouter_chain_window",
+    "specrouter_kv_append",
+    "specrouter_kv_compact",
     "specrouter_rollback",
     "specrouter_status_string",
     "specrouter_verify_attention",

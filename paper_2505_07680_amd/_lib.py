@@ -59,6 +59,8 @@ _SIGNATURES = {
     ),
     "specrouter_rollback": (_c_i, [_c_p] * 4 + [_c_i, _c_i, _c_p, _c_p]),
     "specrouter_chain_window": (_c_i, [_c_p, _c_p, _c_i, _c_i, _c_i] + [_c_p] * 5),
+    "specrouter_kv_append": (_c_i, [_c_p] * 8 + [_c_i] * 5 + [_c_p, _c_p]),
+    "specrouter_kv_compact": (_c_i, [_c_p] * 4 + [_c_i] * 4 + [_c_p, _c_p]),
     "specrouter_chain_consensus": (_c_i, [_c_p, _c_p, _c_p, _c_i, _c_p, _c_p, _c_i, _c_i] + [_c_p] * 6),
     # chain scheduler (host code; host pointers)
     "specrouter_sched_create": (_c_i, [_c_i, _c_dp, _c_i, _c_i, _c_i, _c_d, _c_d, _c_d, ctypes.POINTER(_c_p)]),
@@ -287,6 +289,40 @@ def specrouter_chain_consensus(ctx_len, k_lower, out_lower, k_upper, out_upper, 
                                            _ptr(len_upper), _ptr(len_lower), _ptr(pending), _ptr(n_pending),
                                            _ptr(status), _stream())
     _check(rc, "specrouter_chain_consensus")
+
+
+def specrouter_kv_append(k_new, v_new, gamma, k_cache, v_cache, cache_mask, kv_len, shared_len=None, status=None):
+    """k_new/v_new [B, gmax+1, Hkv, D] bf16 -> k_cache/v_cache [B, Hkv, L_cap, D] at each cursor."""
+    _dev(k_new, v_new, gamma, k_cache, v_cache, cache_mask, kv_len, shared_len, status)
+    _i32(gamma, "gamma")
+    _i32(kv_len, "kv_len")
+    B, G1, Hkv, D = k_new.shape
+    L_cap = k_cache.shape[2]
+    if v_new.shape != k_new.shape or k_cache.shape != (B, Hkv, L_cap, D) or v_cache.shape != k_cache.shape:
+        raise ValueError("k_new/v_new [B, gmax+1, Hkv, D] and k_cache/v_cache [B, Hkv, L_cap, D] expected")
+    for t in (k_new, v_new, k_cache, v_cache):
+        if not t.is_contiguous() or t.element_size() != 2:
+            raise ValueError("K/V tensors must be contiguous bf16")
+    if cache_mask is not None and (cache_mask.shape != (B, L_cap) or not cache_mask.is_contiguous()):
+        raise ValueError("cache_mask must be u8 [B, L_cap]")
+    rc = load().specrouter_kv_append(_ptr(k_new), _ptr(v_new), _ptr(gamma), _ptr(k_cache), _ptr(v_cache),
+                                     _ptr(cache_mask), _ptr(kv_len), _ptr(shared_len), B, G1 - 1, Hkv, D, L_cap,
+                                     _ptr(status), _stream())
+    _check(rc, "specrouter_kv_append")
+
+
+def specrouter_kv_compact(k_cache, v_cache, cache_mask, kv_len, status=None):
+    _dev(k_cache, v_cache, cache_mask, kv_len, status)
+    _i32(kv_len, "kv_len")
+    B, Hkv, L_cap, D = k_cache.shape
+    if v_cache.shape != k_cache.shape or cache_mask.shape != (B, L_cap):
+        raise ValueError("k_cache/v_cache [B, Hkv, L_cap, D] and cache_mask [B, L_cap] expected")
+    for t in (k_cache, v_cache, cache_mask):
+        if not t.is_contiguous():
+            raise ValueError("cache tensors must be contiguous")
+    rc = load().specrouter_kv_compact(_ptr(k_cache), _ptr(v_cache), _ptr(cache_mask), _ptr(kv_len), B, Hkv, D, L_cap,
+                                      _ptr(status), _stream())
+    _check(rc, "specrouter_kv_compact")
 
 
 # ----------------------------------------------------------------------------

@@ -173,6 +173,26 @@ int specrouter_chain_consensus(const int32_t* ctx_len, const int32_t* k_lower, c
                                     (hipStream_t)stream);
 }
 
+int specrouter_kv_append(const void* k_new, const void* v_new, const int32_t* gamma, void* k_cache, void* v_cache,
+                         uint8_t* cache_mask, int32_t* kv_len, const int32_t* shared_len, int B, int gamma_max,
+                         int Hkv, int D, int L_cap, int32_t* status, void* stream) {
+  if (B <= 0 || gamma_max < 0 || gamma_max > SPECROUTER_MAX_GAMMA || Hkv <= 0 || L_cap <= 0) return SR_EINVAL;
+  if (D != 64 && D != 128) return SR_EUNSUPPORTED;
+  if (!k_new || !v_new || !gamma || !k_cache || !v_cache || !kv_len) return SR_EINVAL;
+  if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(k_cache) || !aligned16(v_cache)) return SR_EINVAL;
+  return sr::launch_kv_append(k_new, v_new, gamma, k_cache, v_cache, cache_mask, kv_len, shared_len, B, gamma_max,
+                              Hkv, D, L_cap, status, (hipStream_t)stream);
+}
+
+int specrouter_kv_compact(void* k_cache, void* v_cache, uint8_t* cache_mask, int32_t* kv_len, int B, int Hkv, int D,
+                          int L_cap, int32_t* status, void* stream) {
+  if (B <= 0 || Hkv <= 0 || L_cap <= 0) return SR_EINVAL;
+  if (D != 64 && D != 128) return SR_EUNSUPPORTED;
+  if (!k_cache || !v_cache || !cache_mask || !kv_len) return SR_EINVAL;
+  if (!aligned16(k_cache) || !aligned16(v_cache)) return SR_EINVAL;
+  return sr::launch_kv_compact(k_cache, v_cache, cache_mask, kv_len, B, Hkv, D, L_cap, status, (hipStream_t)stream);
+}
+
 int specrouter_rollback(int32_t* kv_len, uint8_t* cache_mask, const int32_t* new_len,
                         int32_t* phys_len, int B, int L_cap, int32_t* status, void* stream) {
   if (!kv_len || !new_len || B <= 0 || L_cap <= 0) return SR_EINVAL;

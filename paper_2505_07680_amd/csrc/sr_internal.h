@@ -270,6 +270,12 @@ int launch_chain_consensus(const int32_t* ctx_len, const int32_t* k_lower, const
                            int B, int32_t* len_upper, int32_t* len_lower, int32_t* pending,
                            int32_t* n_pending, int32_t* status, hipStream_t stream);
 
+int launch_kv_append(const void* k_new, const void* v_new, const int32_t* gamma, void* k_cache, void* v_cache,
+                     uint8_t* cache_mask, int32_t* kv_len, const int32_t* shared_len, int B, int gamma_max,
+                     int Hkv, int D, int L_cap, int32_t* status, hipStream_t stream);
+int launch_kv_compact(void* k_cache, void* v_cache, uint8_t* cache_mask, int32_t* kv_len, int B, int Hkv, int D,
+                      int L_cap, int32_t* status, hipStream_t stream);
+
 int launch_rollback(int32_t* kv_len, uint8_t* cache_mask, const int32_t* new_len,
                     int32_t* phys_len, int B, int L_cap, int32_t* status, hipStream_t stream);
 
