@@ -40,8 +40,9 @@
  *
  * Shapes: B sequences; gamma_max >= max_b gamma_b (0..16); Hq query heads and
  * Hkv kv heads with Hq % Hkv == 0 (query head h reads kv head h / (Hq/Hkv));
- * head dimension D in {64, 128}; L_cap cache rows per (sequence, kv head);
- * vocabulary size V.
+ * head dimension D in {64, 128}; L_cap cache rows per (sequence, kv head),
+ * at most SPECROUTER_MAX_CACHE_ROWS for the attention call (its slabs are
+ * addressed with 32-bit byte offsets); vocabulary size V.
  */
 #ifndef SPECROUTER_H
 #define SPECROUTER_H
@@ -55,6 +56,7 @@ extern "C" {
 
 #define SPECROUTER_ABI_VERSION 2
 #define SPECROUTER_MAX_GAMMA 16
+#define SPECROUTER_MAX_CACHE_ROWS (1 << 22)
 
 /* Host-side return codes. */
 enum {
@@ -111,8 +113,10 @@ const char* specrouter_status_string(int code);
  * workspace  device scratch of specrouter_verify_attention_workspace_size()
  *            bytes (may be NULL when that size is 0). Zero-fill it once before
  *            its first use; every call leaves it in that state again (it holds
- *            per-(sequence, kv head) arrival counters of the cache splits)
- * Precision: bf16 products, fp32 accumulation and softmax.
+ *            per-(sequence, kv head, query chunk) arrival counters of the cache
+ *            splits, and their partial results)
+ * Precision: bf16 products, fp32 accumulation and softmax, in a fixed order
+ * (repeated calls give identical bits).
  */
 size_t specrouter_verify_attention_workspace_size(int B, int gamma_max, int Hq, int Hkv, int D,
                                                   int L_cap);

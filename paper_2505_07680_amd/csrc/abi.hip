@@ -31,7 +31,7 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 bool attention_shape_ok(int B, int gamma_max, int Hq, int Hkv, int L_cap) {
   return B > 0 && gamma_max >= 0 && gamma_max <= SPECROUTER_MAX_GAMMA && Hq > 0 && Hkv > 0 &&
-         Hq % Hkv == 0 && L_cap >= gamma_max + 1 && B <= 65535;
+         Hq % Hkv == 0 && L_cap >= gamma_max + 1 && L_cap <= SPECROUTER_MAX_CACHE_ROWS && B <= 65535;
 }
 
 }  // namespace

@@ -8,15 +8,17 @@
 // the key loop); the four states are merged through LDS at the end. When the
 // cache is split, each split publishes its (max, sum, unnormalised output)
 // partial and bumps a per-(b, g, query chunk) arrival counter; the last
-// workgroup to arrive merges all partials and writes the output, then resets
-// the counter, so the workspace is left ready for the next call.
+// workgroup to arrive merges all partials in split order and writes the
+// output, then resets the counter, so the workspace is left ready for the
+// next call. The summation order is fixed, so results are reproducible.
 //
 // Per 16-key wave tile:
 //   * K and V rows are fetched with coalesced 16-byte loads into a two-deep
 //     register ring, so two tiles are in flight while one is computed, and
-//     staged in a wave-private LDS slot; V rows that are invalid (past the
-//     split/kv_len, or mask 0) are zeroed while staging, so whatever those
-//     rows hold never reaches the output;
+//     staged in a wave-private LDS slot; rows at or past kv_len are fetched
+//     out of the buffer range (they read as zero, with no memory traffic) and
+//     V rows under mask 0 are zeroed while staging, so whatever those rows
+//     hold never reaches the output;
 //   * S^T = K Q^T on MFMA (v_mfma_f32_16x16x32_bf16: 16 keys x 16 queries per
 //     block, K=32 over the head dimension); each lane then holds 4 scores of
 //     ONE query, so the softmax max/sum need only two cross-lane steps;
@@ -40,17 +42,19 @@ typedef float floatx2 __attribute__((ext_vector_type(2)));
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kWaveKeys = 16;
-constexpr int kTileKeys = kWaves * kWaveKeys;
 // At most three 16-row query groups per workgroup: more rows than that go to
 // further query chunks (their K/V reads are largely served by the XCD's L2,
 // as the chunks of one (sequence, kv head, split) run on one XCD at the same
 // time), which keeps the accumulators in VGPRs at two waves per SIMD.
 constexpr int kMaxNQ = 3;
-constexpr float kLazy = 8.f;
+constexpr float kLazy = 8.f;  // log2 headroom of the lazily rescaled softmax reference
 // Arrival counters sit one per 128-byte line: the splits of different
-// (sequence, kv head) pairs then never contend for one line.
+// (sequence, kv head, query chunk) jobs then never contend for one line.
 constexpr int kCounterStride = 32;
-constexpr int kMaxSplitKeys = 4224;  // keys per split at most (about 2 MB of K/V at D = 128)  // log2 headroom of the lazily rescaled softmax reference
+constexpr int kMaxSplitKeys = 4224;  // keys per split at most (about 2 MB of K/V at D = 128)
+// Byte offset past the end of any K/V slab (slabs are below 2^31 bytes): a
+// buffer load there returns zero without touching memory.
+constexpr uint32_t kOutOfRange = 0x7ffffff0u;
 
 template <int D>
 struct Geo {
@@ -68,8 +72,9 @@ struct Lds {
   static constexpr int MQ = 16 * NQ;
   static constexpr int kStage = kWaves * Geo<D>::kWaveBytes + MQ * Geo<D>::kKStride;
   // Merge of the four wave states: the columns are reduced in kPasses passes
-  // so that the four fp32 slices fit in about 48 KB.
-  static constexpr int kPasses = (kWaves * MQ * D * 4 <= 49152) ? 1 : (kWaves * MQ * D * 2 <= 49152) ? 2 : 4;
+  // so that the four fp32 slices fit in 72 KB (two workgroups per CU still
+  // fit in its 160 KB of LDS).
+  static constexpr int kPasses = (kWaves * MQ * D * 4 <= 73728) ? 1 : (kWaves * MQ * D * 2 <= 73728) ? 2 : 4;
   static constexpr int kDp = D / kPasses;                 // columns per pass
   static constexpr int kRowStride = kDp + 4;              // floats; padded against bank conflicts
   static constexpr int kSlot = MQ * kRowStride;           // floats per wave slice
@@ -100,11 +105,6 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <bool B>
-struct Flag {
-  static constexpr bool value = B;
-};
-
 template <int D>
 struct Stage {  // one 16-key wave tile in flight
   u32x4 k[Geo<D>::kLoads], v[Geo<D>::kLoads];
@@ -123,7 +123,7 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
                   const uint16_t* __restrict__ vc, const uint8_t* __restrict__ mask,
                   const int32_t* __restrict__ kv_len, const int32_t* __restrict__ gamma,
                   float* __restrict__ out, float* __restrict__ part_o,
-                  float* __restrict__ part_ml, uint32_t* __restrict__ arrivals, int B, int gmax,
+                  float* __restrict__ part_ml, uint32_t* __restrict__ counters, int B, int gmax,
                   int Hq, int Hkv, int L_cap, float scale_log2, int split_keys, int n_splits,
                   int q_chunks, int32_t* __restrict__ status) {
   using GG = Geo<D>;
@@ -137,10 +137,11 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
   // (and the query chunks of one pair and split share an XCD and its L2), and
   // the later splits, which only long sequences have, start first.
   const int P = B * Hkv;
-  const int pair_id = (int)(blockIdx.x % (unsigned)P);
   const int rest = (int)(blockIdx.x / (unsigned)P);
   const int split = n_splits - 1 - rest % n_splits;
-  const int qc = rest / n_splits;
+  const int job = (int)(blockIdx.x % (unsigned)P) * q_chunks + rest / n_splits;
+  const int qc = job % q_chunks;
+  const int pair_id = job / q_chunks;
   const int g = pair_id % Hkv;
   const int b = pair_id / Hkv;
   const int G = Hq / Hkv;
@@ -154,9 +155,8 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
   const int row0 = qc * MQ;
   const int row_end = min(R, row0 + MQ);
   const int Mb = valid ? G * (gam + 1) : 0;
-  const int key_begin = split * split_keys;
-  const int key_end = valid ? min(key_begin + split_keys, L) : 0;
-  const bool work = row0 < Mb && key_begin < key_end;
+  const int ns = valid ? (L + split_keys - 1) / split_keys : 0;  // splits that hold keys
+  const bool work = row0 < Mb && split < ns;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -197,39 +197,45 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
     for (int db = 0; db < DB; ++db) o[db][qg] = floatx4{0.f, 0.f, 0.f, 0.f};
   }
 
-  const int n_tiles = (key_end - key_begin + kTileKeys - 1) / kTileKeys;
+  // Wave tile j holds keys [16 j, 16 j + 16). Split s owns the keys
+  // [s split_keys, (s + 1) split_keys), dealt round-robin to its four waves,
+  // so a wave's tiles are first, first + 4, first + 8, ... below j_end.
+  const int first = split * (split_keys / kWaveKeys) + w;
+  const int j_end = min((L + kWaveKeys - 1) / kWaveKeys, (split + 1) * (split_keys / kWaveKeys));
+  const int row_lim = min(L, j_end * kWaveKeys);  // a refill past the wave's last tile reads nothing
 
-  // Loads are unconditional (rows clamped to the split's last valid key), so
-  // the loop body issues a fixed number of loads per tile and each stage
-  // waits only for its own loads; refetches past the end hit the same line.
+  // Every fetch issues the same loads (rows at or past kv_len, and tiles past
+  // the wave's last, read out of range, as zero, with no traffic), so each
+  // wait covers exactly the loads it needs, in the first iteration as in
+  // every later one.
   const uint8_t* mload = mrow ? mrow : (const uint8_t*)kslab;
   // K/V slabs of (b, g) as buffer resources: 32-bit row offsets
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(kslab, (size_t)L_cap * D * 2);
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(vslab, (size_t)L_cap * D * 2);
-  const uint32_t lane_off = (uint32_t)(lane / GG::kChunksPerRow) * (D * 2) + (uint32_t)(lane % GG::kChunksPerRow) * 16;
-  auto fetch = [&](int t, Stage<D>& st) __attribute__((always_inline)) {
-    const int kb0 = key_begin + t * kTileKeys + w * kWaveKeys;
+  const int lane_row = lane / GG::kChunksPerRow;
+  const uint32_t lane_col = (uint32_t)(lane % GG::kChunksPerRow) * 16;
+  auto fetch = [&](int j, Stage<D>& st) __attribute__((always_inline)) {
+    const int kb0 = j * kWaveKeys;
 #pragma unroll
     for (int u = 0; u < GG::kLoads; ++u) {
-      // rows past the split's last key re-read that key (same cache lines)
-      const int r0 = min(kb0 + u * GG::kRowsPerLoad, key_end - 1);
-      const uint32_t off = (uint32_t)r0 * (D * 2) + lane_off;
+      const int row = kb0 + u * GG::kRowsPerLoad + lane_row;
+      const uint32_t off = row < row_lim ? (uint32_t)row * (D * 2) + lane_col : kOutOfRange;
       st.k[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, 0));
       st.v[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, 0));
     }
-    st.mbyte = mload[min(kb0 + (lane & (kWaveKeys - 1)), key_end - 1)];
+    st.mbyte = mload[min(kb0 + (lane & (kWaveKeys - 1)), L - 1)];
   };
-
-  // Stage ring entry st (tile t) in LDS, refill it with tile t + 2 when
-  // Refill::value (so nothing is fetched past the last tile), then compute.
-  auto consume = [&](int t, Stage<D>& st, auto refill) __attribute__((always_inline)) {
-    const int kb0 = key_begin + t * kTileKeys + w * kWaveKeys;
-    const bool key_ok = lane < kWaveKeys && kb0 + lane < key_end && (mrow == nullptr || st.mbyte != 0u);
+  // Ring entry st holds tile j: stage it in LDS, refill it with the wave's
+  // next-but-one tile, compute tile j, and leave the refilled tile's number
+  // in j.
+  auto step = [&](int& j, Stage<D>& st) __attribute__((always_inline)) {
+    const int kb0 = j * kWaveKeys;
+    const bool key_ok = lane < kWaveKeys && kb0 + lane < L && (mrow == nullptr || st.mbyte != 0u);
     const uint32_t vbits = (uint32_t)__ballot(key_ok) & 0xffffu;
     const bool all_rows = vbits == 0xffffu;  // wave-uniform
 #pragma unroll
     for (int u = 0; u < GG::kLoads; ++u) {
-      const int rl = u * GG::kRowsPerLoad + lane / GG::kChunksPerRow;
+      const int rl = u * GG::kRowsPerLoad + lane_row;
       const int c = lane % GG::kChunksPerRow;
       *(u32x4*)(kst + rl * GG::kKStride + c * 16) = st.k[u];
       const u32x4 vv = (all_rows || ((vbits >> rl) & 1u)) ? st.v[u] : u32x4{0u, 0u, 0u, 0u};
@@ -238,12 +244,13 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
       *(uint2*)(dst + 2) = make_uint2(vv.z, vv.w);
     }
     wave_lds_sync();
-    if constexpr (decltype(refill)::value) {
-      __builtin_amdgcn_sched_barrier(0);
-      fetch(t + 2, st);  // two tiles in flight during the compute below
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    if (t >= n_tiles || kb0 >= key_end) return;  // wave-uniform: nothing of this tile to compute
+    const int nx = j + 2 * kWaves;
+    __builtin_amdgcn_sched_barrier(0);
+    fetch(nx, st);  // two tiles in flight during the compute below
+    __builtin_amdgcn_sched_barrier(0);
+    const int jc = j;
+    j = nx;
+    if (jc >= j_end) return;  // wave-uniform: past the wave's last tile
     const bool full = vbits == 0xffffu && kb0 + kWaveKeys - 1 <= causal0;  // wave-uniform
     // ---- S^T = K Q^T (16 keys x 16 queries per group)
     floatx4 sacc[NQ];
@@ -330,11 +337,10 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
     wave_lds_sync();  // this tile's LDS reads are issued before the slot is rewritten
   };
 
-  // Issue order: this workgroup's query rows, then the first two ring
-  // entries; the query rows are staged in LDS while the K/V tiles are still
-  // in flight. Each group of loads is kept together (no interleaving by the
-  // scheduler) so every wait covers exactly the loads it needs, in the first
-  // iteration as in every later one.
+  // Issue order: this workgroup's query rows, then the two ring entries; the
+  // query rows are staged in LDS while the K/V tiles are still in flight.
+  // Each group is kept together (no interleaving by the scheduler), so every
+  // wait covers exactly what it needs: a step waits for its own tile only.
   constexpr int kQChunks = MQ * GG::kChunksPerRow;
   constexpr int kQLoads = (kQChunks + kThreads - 1) / kThreads;
   u32x4 qv[kQLoads];
@@ -347,42 +353,28 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
   }
   __builtin_amdgcn_sched_barrier(0);
   Stage<D> sa, sb;
-  fetch(0, sa);
+  int ja = first;
+  int jb = first + kWaves;
+  fetch(ja, sa);
   __builtin_amdgcn_sched_barrier(0);
-  fetch(1, sb);
+  fetch(jb, sb);
   __builtin_amdgcn_sched_barrier(0);
+  // (unconditional: a thread past the last chunk rewrites that chunk with
+  // the same value, and no load is moved into a branch after the K/V loads)
 #pragma unroll
   for (int u = 0; u < kQLoads; ++u) {
-    const int idx = tid + u * kThreads;
-    if (idx < kQChunks) {
-      const int rl = idx / GG::kChunksPerRow;
-      const u32x4 val = row0 + rl < Mb ? qv[u] : u32x4{0u, 0u, 0u, 0u};
-      *(u32x4*)(qst + rl * GG::kKStride + (idx % GG::kChunksPerRow) * 16) = val;
-    }
+    const int idx = min(tid + u * kThreads, kQChunks - 1);
+    const int rl = idx / GG::kChunksPerRow;
+    const u32x4 val = row0 + rl < Mb ? qv[u] : u32x4{0u, 0u, 0u, 0u};
+    *(u32x4*)(qst + rl * GG::kKStride + (idx % GG::kChunksPerRow) * 16) = val;
   }
   __syncthreads();
 
-  // sa holds tile t and sb tile t + 1 at the top of each iteration.
-  int t = 0;
-#ifdef ATT_PEEL
-  for (; t + 3 < n_tiles; t += 2) {
-    consume(t, sa, Flag<true>{});
-    consume(t + 1, sb, Flag<true>{});
+  // sa and sb hold the wave's next two tiles (ja < jb).
+  while (ja < j_end) {
+    step(ja, sa);
+    step(jb, sb);
   }
-  if (t + 2 < n_tiles) {
-    consume(t, sa, Flag<true>{});
-    consume(t + 1, sb, Flag<false>{});
-    consume(t + 2, sa, Flag<false>{});
-  } else {
-    consume(t, sa, Flag<false>{});
-    consume(t + 1, sb, Flag<false>{});
-  }
-#else
-  for (; t < n_tiles; t += 2) {
-    consume(t, sa, Flag<true>{});
-    consume(t + 1, sb, Flag<true>{});
-  }
-#endif
   __syncthreads();
 
   // ---- merge the four wave states (every wave and lane takes part)
@@ -418,9 +410,8 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
     }
   }
 
-  // Splits of this (b, g) that hold keys; with a single one the result is
-  // final here, otherwise it is published as a partial.
-  const int ns = (L + split_keys - 1) / split_keys;
+  // With a single split holding keys the result is final here, otherwise it
+  // is published as the split's partial.
   const size_t pair = (size_t)(b * Hkv + g);
   const int n_rec = (int)((size_t)n_splits * P) * R;  // records in the partial arrays
   const __amdgpu_buffer_rsrc_t rs_o = partial_rsrc(part_o, (uint32_t)((size_t)n_rec * D * 4));
@@ -466,15 +457,15 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
   }
   if (ns == 1) return;
 
-  // ---- arrive: the last split of this chunk to finish merges all partials
+  // ---- arrive: the last split of this job to finish merges all partials
   stores_done();
   __syncthreads();
   __shared__ uint32_t last_flag;
   if (tid == 0) {
-    uint32_t* cnt = arrivals + (pair * q_chunks + qc) * kCounterStride;
+    uint32_t* cnt = counters + (size_t)job * kCounterStride;
     const uint32_t before = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const bool last = before == (uint32_t)(ns - 1);
-    if (last) st_dev(cnt, 0u);  // every split of this chunk has arrived: reset for the next call
+    if (last) st_dev(cnt, 0u);  // every split of this job has arrived: reset for the next call
     last_flag = last ? 1u : 0u;
   }
   __syncthreads();
@@ -597,13 +588,13 @@ int launch_verify_attention(const void* q, const void* k_cache, const void* v_ca
                             const AttentionPlan& plan, int32_t* status, hipStream_t stream) {
   const int G = Hq / Hkv;
   const int R = G * (gamma_max + 1);
-  uint32_t* arrivals = (uint32_t*)workspace;
+  uint32_t* counters = (uint32_t*)workspace;
   float* part_o = workspace ? (float*)((char*)workspace + plan.part_offset) : nullptr;
   float* part_ml = part_o ? part_o + (size_t)B * Hkv * plan.n_splits * R * D : nullptr;
   dim3 grid((unsigned)((long)plan.n_splits * plan.q_chunks * B * Hkv));
   hipLaunchKernelGGL(pick_split(D, plan.nq), grid, dim3(kThreads), 0, stream,
                      (const uint16_t*)q, (const uint16_t*)k_cache, (const uint16_t*)v_cache,
-                     cache_mask, kv_len, gamma, out, part_o, part_ml, arrivals, B, gamma_max, Hq, Hkv,
+                     cache_mask, kv_len, gamma, out, part_o, part_ml, counters, B, gamma_max, Hq, Hkv,
                      L_cap, scale * kLog2e, plan.split_keys, plan.n_splits, plan.q_chunks, status);
   if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
   return SR_OK;
