@@ -2,8 +2,10 @@
 """Verify-step benchmark on one MI355X.
 
 One step = the whole verify hot path at one verifier level for one batch:
-verification attention, accept-and-diverge, rollback (three C-ABI calls on
-one stream). Inputs are seeded synthetic data of the named workload and are
+verification attention, then accept-and-diverge with the rollback applied by
+its finishing kernel (two C-ABI calls on one stream:
+specrouter_verify_attention, specrouter_accept_and_rollback). The standalone
+rollback call is timed on its own as well. Inputs are seeded synthetic data of the named workload and are
 resident in HBM before timing starts. To keep the 256 MB last-level cache
 from serving repeated steps, R copies of the inputs live at different HBM
 addresses and step s uses copy s mod R.
@@ -160,21 +162,19 @@ def main():
         if evs:
             evs[1].record()
         a = s["acc"]
-        sr.specrouter_accept_and_diverge(s["p"], s["ql"], s["drafts"], s["gamma"], s["u_acc"], s["u_res"],
-                                         s["kv_in"], a.accept_len, a.out_tokens, a.new_len, a.accept_prob,
-                                         a.p_tok, a.q_tok, a.kl, a.tv, a.workspace, s["st"])
+        sr.specrouter_accept_and_rollback(s["p"], s["ql"], s["drafts"], s["gamma"], s["u_acc"], s["u_res"],
+                                          s["kv_in"], a.accept_len, a.out_tokens, a.new_len, a.accept_prob,
+                                          a.p_tok, a.q_tok, a.kl, a.tv, s["kv_work"], s["mask_work"], s["phys"],
+                                          a.workspace, s["st"])
         if evs:
             evs[2].record()
-        sr.specrouter_rollback(s["kv_work"], s["mask_work"], a.new_len, s["phys"], s["st"])
-        if evs:
-            evs[3].record()
 
     for i in range(args.warmup):
         step(sets[i % R])
     torch.cuda.synchronize()
 
     K = args.steps
-    evs = [[ev() for _ in range(4)] for _ in range(K)]
+    evs = [[ev() for _ in range(3)] for _ in range(K)]
     start, stop = ev(), ev()
     torch.cuda.synchronize()
     start.record()
@@ -187,7 +187,6 @@ def main():
     total_ms = start.elapsed_time(stop)
     att_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
     acc_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    rb_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
 
     status = int(sum(int(s["st"].item()) for s in sets))
     acc0 = sets[0]["acc"]
@@ -197,15 +196,17 @@ def main():
     value = drafts_per_step * K / (total_ms / 1e3)
 
     att_gbs = att_bytes / (att_ms / 1e3) / 1e9
-    acc_gbs = acc_bytes / (acc_ms / 1e3) / 1e9
+    acc_gbs = (acc_bytes + rb_bytes) / (acc_ms / 1e3) / 1e9
     # the roofline is reported for the entry point that takes the longest
-    dominant = "verify_attention" if att_ms >= acc_ms else "accept_and_diverge"
-    dom_bytes, dom_ms = (att_bytes, att_ms) if dominant == "verify_attention" else (acc_bytes, acc_ms)
+    dominant = "verify_attention" if att_ms >= acc_ms else "accept_and_rollback"
+    dom_bytes, dom_ms = (att_bytes, att_ms) if dominant == "verify_attention" else (acc_bytes + rb_bytes, acc_ms)
     dom_gbs = dom_bytes / (dom_ms / 1e3) / 1e9
     roofline = {
         "bound": "hbm", "kernel": "specrouter_" + dominant,
         "achieved": round(dom_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-        "frac": round(dom_gbs / PEAK_HBM_GBS, 4), "traffic": measured_traffic(dominant, shape.name),
+        "frac": round(dom_gbs / PEAK_HBM_GBS, 4),
+        "traffic": measured_traffic("verify_attention" if dominant == "verify_attention" else "accept_and_diverge",
+                                    shape.name),
         "algorithmic_bytes": dom_bytes, "avg_launch_us": round(dom_ms * 1e3, 2),
     }
 
@@ -274,6 +275,24 @@ def main():
         "note": "GPU time per call (HIP graph replay)",
     }
     variants["chain_glue"] = glue
+    # the standalone entry points the step fuses: rollback alone (graph
+    # replay) and accept-and-diverge alone (HIP events)
+    kv_rb, mask_rb = s["kv_in"].clone(), s["mask_in"].clone()  # new_len <= kv_in: a pure rollback
+    rb_us = graph_us(lambda: sr.specrouter_rollback(kv_rb, mask_rb, a.new_len, s["phys"], s["st"]))
+    e0, e1 = ev(), ev()
+    torch.cuda.synchronize()
+    e0.record()
+    for i in range(K):
+        s2 = sets[i % R]
+        a2 = s2["acc"]
+        sr.specrouter_accept_and_diverge(s2["p"], s2["ql"], s2["drafts"], s2["gamma"], s2["u_acc"], s2["u_res"],
+                                         s2["kv_in"], a2.accept_len, a2.out_tokens, a2.new_len, a2.accept_prob,
+                                         a2.p_tok, a2.q_tok, a2.kl, a2.tv, a2.workspace, s2["st"])
+    e1.record()
+    torch.cuda.synchronize()
+    acc_only_us = e0.elapsed_time(e1) / K * 1e3
+    variants["accept_alone"] = {"us": round(acc_only_us, 2), "GB/s": round(acc_bytes / acc_only_us / 1e3, 1),
+                                "note": "specrouter_accept_and_diverge without the rollback"}
 
     # KV-cache state: append this step's rows (per-sequence cursors) and
     # compact a cache with 2% holes, on scratch caches of the workload's shape
@@ -341,10 +360,13 @@ def main():
             "verify_attention": {"us": round(att_ms * 1e3, 2), "GB/s": round(att_gbs, 1),
                                  "frac": round(att_gbs / PEAK_HBM_GBS, 4), "algorithmic_bytes": att_bytes,
                                  "traffic": measured_traffic("verify_attention", shape.name)},
-            "accept_and_diverge": {"us": round(acc_ms * 1e3, 2), "GB/s": round(acc_gbs, 1),
-                                   "frac": round(acc_gbs / PEAK_HBM_GBS, 4), "algorithmic_bytes": acc_bytes,
-                                   "traffic": measured_traffic("accept_and_diverge", shape.name)},
-            "rollback": {"us": round(rb_ms * 1e3, 2), "algorithmic_bytes": rb_bytes},
+            "accept_and_rollback": {"us": round(acc_ms * 1e3, 2), "GB/s": round(acc_gbs, 1),
+                                    "frac": round(acc_gbs / PEAK_HBM_GBS, 4),
+                                    "algorithmic_bytes": acc_bytes + rb_bytes,
+                                    "traffic": measured_traffic("accept_and_diverge", shape.name),
+                                    "note": "accept-and-diverge with the rollback done by its finish kernel"},
+            "rollback": {"us": round(rb_us, 2), "algorithmic_bytes": rb_bytes,
+                         "note": "the standalone rollback call (not part of the step), HIP graph replay"},
         },
         "sampling_variants": variants,
         "mean_accept_len": round(mean_accept, 3),

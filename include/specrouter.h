@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define SPECROUTER_ABI_VERSION 2
+#define SPECROUTER_ABI_VERSION 3
 #define SPECROUTER_MAX_GAMMA 16
 #define SPECROUTER_MAX_CACHE_ROWS (1 << 22)
 
@@ -229,6 +229,34 @@ int specrouter_accept_and_diverge_sampled(const void* p_logits, int64_t p_batch_
  */
 int specrouter_rollback(int32_t* kv_len, uint8_t* cache_mask, const int32_t* new_len,
                         int32_t* phys_len, int B, int L_cap, int32_t* status, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Accept-and-diverge followed by the rollback, in one call (Section 2.2
+ * steps 3-4 and Section 4.4): the same results as
+ * specrouter_accept_and_diverge_sampled(...) with these arguments, then
+ * specrouter_rollback(cache_kv_len, cache_mask, <its new_len>, phys_len, B,
+ * L_cap, status), bit for bit -- outputs, lengths, mask, phys_len and status
+ * bits. The rollback of each sequence is done by the accept's own finishing
+ * step as soon as that sequence's outcome is known, so the verify step needs
+ * one launch fewer.
+ *
+ * kv_len        required here (the accept's new length is kv_len - gamma_b + k_b)
+ * new_len       may be NULL (the rollback uses the value internally)
+ * cache_kv_len  i32 [B] in/out, the lengths rolled back (may be kv_len itself)
+ * cache_mask    u8 [B][L_cap] in/out, or NULL
+ * phys_len      i32 [1] out (max over sequences of the new lengths), or NULL
+ * L_cap         > 0, the cache rows per sequence
+ * The workspace is the accept's (specrouter_accept_workspace_size); a call of
+ * either accept entry point leaves it ready for the other.
+ */
+int specrouter_accept_and_rollback(const void* p_logits, int64_t p_batch_stride, const void* q_logits,
+                                   int64_t q_batch_stride, int logits_dtype, const int32_t* draft_tokens,
+                                   const int32_t* gamma, const float* u_accept, const float* u_resample,
+                                   const int32_t* kv_len, int32_t* accept_len, int32_t* out_tokens,
+                                   int32_t* new_len, float* accept_prob, float* p_tok, float* q_tok, float* kl,
+                                   float* tv, int B, int gamma_max, int V, const specrouter_sampling* sampling,
+                                   int32_t* cache_kv_len, uint8_t* cache_mask, int32_t* phys_len, int L_cap,
+                                   void* workspace, size_t workspace_bytes, int32_t* status, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* KV-cache state (Section 4.4, StateManager: logical validity mask, Eq. 8;

@@ -18,6 +18,7 @@ from ._lib import (
     specrouter_abi_version,
     specrouter_accept_and_diverge,
     specrouter_accept_and_diverge_sampled,
+    specrouter_accept_and_rollback,
     specrouter_accept_workspace_size,
     specrouter_chain_consensus,
     specrouter_chain_window,
@@ -39,6 +40,7 @@ __all__ = [
     "specrouter_abi_version",
     "specrouter_accept_and_diverge",
     "specrouter_accept_and_diverge_sampled",
+    "specrouter_accept_and_rollback",
     "specrouter_accept_workspace_size",
     "specrouter_chain_consensus",
     "specrouter_chain_window",

@@ -57,6 +57,11 @@ _SIGNATURES = {
         [_c_p, _c_i64, _c_p, _c_i64, _c_i] + [_c_p] * 13 + [_c_i] * 3
         + [ctypes.POINTER(SamplingParams), _c_p, _c_sz, _c_p, _c_p],
     ),
+    "specrouter_accept_and_rollback": (
+        _c_i,
+        [_c_p, _c_i64, _c_p, _c_i64, _c_i] + [_c_p] * 13 + [_c_i] * 3
+        + [ctypes.POINTER(SamplingParams), _c_p, _c_p, _c_p, _c_i, _c_p, _c_sz, _c_p, _c_p],
+    ),
     "specrouter_rollback": (_c_i, [_c_p] * 4 + [_c_i, _c_i, _c_p, _c_p]),
     "specrouter_chain_window": (_c_i, [_c_p, _c_p, _c_i, _c_i, _c_i] + [_c_p] * 5),
     "specrouter_kv_append": (_c_i, [_c_p] * 8 + [_c_i] * 5 + [_c_p, _c_p]),
@@ -207,8 +212,30 @@ def specrouter_accept_and_diverge_sampled(p_logits, q_logits, draft_tokens, gamm
             SamplingParams(float(temperature), int(top_k), float(top_p)))
 
 
+def specrouter_accept_and_rollback(p_logits, q_logits, draft_tokens, gamma, u_accept, u_resample, kv_len,
+                                   accept_len, out_tokens, new_len, accept_prob, p_tok, q_tok, kl, tv,
+                                   cache_kv_len, cache_mask, phys_len, workspace, status=None, temperature=1.0,
+                                   L_cap=None):
+    """specrouter_accept_and_diverge_sampled, then specrouter_rollback of
+    cache_kv_len / cache_mask to the accepted lengths, in one call."""
+    _dev(cache_kv_len, cache_mask, phys_len)
+    _i32(cache_kv_len, "cache_kv_len")
+    B = out_tokens.shape[0]
+    if cache_kv_len.shape != (B,):
+        raise ValueError("cache_kv_len must be [B]")
+    if cache_mask is not None:
+        if cache_mask.shape[0] != B or not cache_mask.is_contiguous():
+            raise ValueError("cache_mask must be contiguous [B, L_cap]")
+        L_cap = cache_mask.shape[1]
+    if L_cap is None:
+        raise ValueError("L_cap is required when cache_mask is None")
+    _accept(p_logits, q_logits, draft_tokens, gamma, u_accept, u_resample, kv_len, accept_len, out_tokens,
+            new_len, accept_prob, p_tok, q_tok, kl, tv, workspace, status,
+            SamplingParams(float(temperature), 0, 1.0), rollback=(cache_kv_len, cache_mask, phys_len, int(L_cap)))
+
+
 def _accept(p_logits, q_logits, draft_tokens, gamma, u_accept, u_resample, kv_len, accept_len, out_tokens,
-            new_len, accept_prob, p_tok, q_tok, kl, tv, workspace, status, sampling):
+            new_len, accept_prob, p_tok, q_tok, kl, tv, workspace, status, sampling, rollback=None):
     tensors = (p_logits, q_logits, draft_tokens, gamma, u_accept, u_resample, kv_len, accept_len,
                out_tokens, new_len, accept_prob, p_tok, q_tok, kl, tv, workspace, status)
     _dev(*tensors)
@@ -232,13 +259,17 @@ def _accept(p_logits, q_logits, draft_tokens, gamma, u_accept, u_resample, kv_le
         if t is not None and (t.shape != (B, gmax) or t.dtype != torch.float32):
             raise ValueError("float outputs must be fp32 [B, gamma_max]")
     ws_bytes = workspace.numel() * workspace.element_size()
-    rc = load().specrouter_accept_and_diverge_sampled(
-        _ptr(p_logits), ps, _ptr(q_logits), qs, code, _ptr(draft_tokens), _ptr(gamma),
-        _ptr(u_accept), _ptr(u_resample), _ptr(kv_len), _ptr(accept_len), _ptr(out_tokens),
-        _ptr(new_len), _ptr(accept_prob), _ptr(p_tok), _ptr(q_tok), _ptr(kl), _ptr(tv),
-        B, gmax, V, None if sampling is None else ctypes.byref(sampling), _ptr(workspace), ws_bytes,
-        _ptr(status), _stream(),
-    )
+    common = (_ptr(p_logits), ps, _ptr(q_logits), qs, code, _ptr(draft_tokens), _ptr(gamma),
+              _ptr(u_accept), _ptr(u_resample), _ptr(kv_len), _ptr(accept_len), _ptr(out_tokens),
+              _ptr(new_len), _ptr(accept_prob), _ptr(p_tok), _ptr(q_tok), _ptr(kl), _ptr(tv),
+              B, gmax, V, None if sampling is None else ctypes.byref(sampling))
+    if rollback is not None:
+        rkv, rmask, rphys, L_cap = rollback
+        rc = load().specrouter_accept_and_rollback(*common, _ptr(rkv), _ptr(rmask), _ptr(rphys), L_cap,
+                                                   _ptr(workspace), ws_bytes, _ptr(status), _stream())
+        _check(rc, "specrouter_accept_and_rollback")
+        return
+    rc = load().specrouter_accept_and_diverge_sampled(*common, _ptr(workspace), ws_bytes, _ptr(status), _stream())
     _check(rc, "specrouter_accept_and_diverge" + ("" if sampling is None else "_sampled"))
 
 

@@ -34,6 +34,41 @@ bool attention_shape_ok(int B, int gamma_max, int Hq, int Hkv, int L_cap) {
          Hq % Hkv == 0 && L_cap >= gamma_max + 1 && L_cap <= SPECROUTER_MAX_CACHE_ROWS && B <= 65535;
 }
 
+// Checks and launch shared by the accept entry points (rollback NULL: none).
+int accept_impl(const void* p_logits, int64_t p_batch_stride, const void* q_logits, int64_t q_batch_stride,
+                int logits_dtype, const int32_t* draft_tokens, const int32_t* gamma, const float* u_accept,
+                const float* u_resample, const int32_t* kv_len, int32_t* accept_len, int32_t* out_tokens,
+                int32_t* new_len, float* accept_prob, float* p_tok, float* q_tok, float* kl, float* tv, int B,
+                int gamma_max, int V, const specrouter_sampling* sampling, const sr::AcceptRollback* rollback,
+                void* workspace, size_t workspace_bytes, int32_t* status, void* stream) {
+  const float temperature = sampling ? sampling->temperature : 1.f;
+  if (!(temperature >= 0.f && temperature < __builtin_inff())) return SR_EINVAL;
+  if (sampling && (sampling->top_k != 0 || sampling->top_p != 1.f)) return SR_EUNSUPPORTED;
+  const bool greedy = temperature == 0.f;
+  if (B <= 0 || gamma_max < 0 || gamma_max > SPECROUTER_MAX_GAMMA || V <= 0) return SR_EINVAL;
+  if (logits_dtype != SR_F32 && logits_dtype != SR_BF16) return SR_EUNSUPPORTED;
+  if (!p_logits || !gamma || !accept_len || !out_tokens) return SR_EINVAL;
+  if (!greedy && !u_resample) return SR_EINVAL;
+  if (gamma_max > 0 && (!q_logits || !draft_tokens || (!greedy && !u_accept))) return SR_EINVAL;
+  if (new_len && !kv_len) return SR_EINVAL;
+  if (p_batch_stride < (int64_t)(gamma_max + 1) * V) return SR_EINVAL;
+  if (gamma_max > 0 && q_batch_stride < (int64_t)gamma_max * V) return SR_EINVAL;
+  const int esz = logits_dtype == SR_BF16 ? 2 : 4;
+  if (((int64_t)V * esz) % 16 != 0 || (p_batch_stride * esz) % 16 != 0 || !aligned16(p_logits))
+    return SR_EUNSUPPORTED;
+  if (gamma_max > 0 && ((q_batch_stride * esz) % 16 != 0 || !aligned16(q_logits)))
+    return SR_EUNSUPPORTED;
+  sr::AcceptPlan plan;
+  const int rc = sr::accept_plan(B, gamma_max, V, logits_dtype, &plan);
+  if (rc != SR_OK) return rc;
+  if (!workspace || workspace_bytes < plan.workspace_bytes || !aligned16(workspace))
+    return SR_EWORKSPACE;
+  return sr::launch_accept(p_logits, p_batch_stride, q_logits, q_batch_stride, logits_dtype,
+                           draft_tokens, gamma, u_accept, u_resample, kv_len, accept_len,
+                           out_tokens, new_len, accept_prob, p_tok, q_tok, kl, tv, B, gamma_max,
+                           V, temperature, rollback, workspace, plan, status, (hipStream_t)stream);
+}
+
 }  // namespace
 
 extern "C" {
@@ -105,32 +140,24 @@ int specrouter_accept_and_diverge_sampled(const void* p_logits, int64_t p_batch_
                                           int gamma_max, int V, const specrouter_sampling* sampling,
                                           void* workspace, size_t workspace_bytes, int32_t* status,
                                           void* stream) {
-  const float temperature = sampling ? sampling->temperature : 1.f;
-  if (!(temperature >= 0.f && temperature < __builtin_inff())) return SR_EINVAL;
-  if (sampling && (sampling->top_k != 0 || sampling->top_p != 1.f)) return SR_EUNSUPPORTED;
-  const bool greedy = temperature == 0.f;
-  if (B <= 0 || gamma_max < 0 || gamma_max > SPECROUTER_MAX_GAMMA || V <= 0) return SR_EINVAL;
-  if (logits_dtype != SR_F32 && logits_dtype != SR_BF16) return SR_EUNSUPPORTED;
-  if (!p_logits || !gamma || !accept_len || !out_tokens) return SR_EINVAL;
-  if (!greedy && !u_resample) return SR_EINVAL;
-  if (gamma_max > 0 && (!q_logits || !draft_tokens || (!greedy && !u_accept))) return SR_EINVAL;
-  if (new_len && !kv_len) return SR_EINVAL;
-  if (p_batch_stride < (int64_t)(gamma_max + 1) * V) return SR_EINVAL;
-  if (gamma_max > 0 && q_batch_stride < (int64_t)gamma_max * V) return SR_EINVAL;
-  const int esz = logits_dtype == SR_BF16 ? 2 : 4;
-  if (((int64_t)V * esz) % 16 != 0 || (p_batch_stride * esz) % 16 != 0 || !aligned16(p_logits))
-    return SR_EUNSUPPORTED;
-  if (gamma_max > 0 && ((q_batch_stride * esz) % 16 != 0 || !aligned16(q_logits)))
-    return SR_EUNSUPPORTED;
-  sr::AcceptPlan plan;
-  const int rc = sr::accept_plan(B, gamma_max, V, logits_dtype, &plan);
-  if (rc != SR_OK) return rc;
-  if (!workspace || workspace_bytes < plan.workspace_bytes || !aligned16(workspace))
-    return SR_EWORKSPACE;
-  return sr::launch_accept(p_logits, p_batch_stride, q_logits, q_batch_stride, logits_dtype,
-                           draft_tokens, gamma, u_accept, u_resample, kv_len, accept_len,
-                           out_tokens, new_len, accept_prob, p_tok, q_tok, kl, tv, B, gamma_max,
-                           V, temperature, workspace, plan, status, (hipStream_t)stream);
+  return accept_impl(p_logits, p_batch_stride, q_logits, q_batch_stride, logits_dtype, draft_tokens, gamma,
+                     u_accept, u_resample, kv_len, accept_len, out_tokens, new_len, accept_prob, p_tok, q_tok, kl,
+                     tv, B, gamma_max, V, sampling, nullptr, workspace, workspace_bytes, status, stream);
+}
+
+int specrouter_accept_and_rollback(const void* p_logits, int64_t p_batch_stride, const void* q_logits,
+                                   int64_t q_batch_stride, int logits_dtype, const int32_t* draft_tokens,
+                                   const int32_t* gamma, const float* u_accept, const float* u_resample,
+                                   const int32_t* kv_len, int32_t* accept_len, int32_t* out_tokens,
+                                   int32_t* new_len, float* accept_prob, float* p_tok, float* q_tok, float* kl,
+                                   float* tv, int B, int gamma_max, int V, const specrouter_sampling* sampling,
+                                   int32_t* cache_kv_len, uint8_t* cache_mask, int32_t* phys_len, int L_cap,
+                                   void* workspace, size_t workspace_bytes, int32_t* status, void* stream) {
+  if (!kv_len || !cache_kv_len || L_cap <= 0) return SR_EINVAL;
+  const sr::AcceptRollback rb{cache_kv_len, cache_mask, phys_len, L_cap};
+  return accept_impl(p_logits, p_batch_stride, q_logits, q_batch_stride, logits_dtype, draft_tokens, gamma,
+                     u_accept, u_resample, kv_len, accept_len, out_tokens, new_len, accept_prob, p_tok, q_tok, kl,
+                     tv, B, gamma_max, V, sampling, &rb, workspace, workspace_bytes, status, stream);
 }
 
 int specrouter_accept_and_diverge(const void* p_logits, int64_t p_batch_stride,

@@ -162,6 +162,13 @@ struct Args {
   double* tvabs;    // [B][gmax+1][nc] sum |P - Q| per chunk (pair rows)
   float* xlogit;    // [B][gmax+1][2] the draft token's p and q logits (pair rows)
   int32_t* status;
+  // rollback applied by the finish kernel (rb_kv NULL: none)
+  int32_t* rb_kv;     // [B] cache lengths, in/out
+  uint8_t* rb_mask;   // [B][L_cap] validity mask, or NULL
+  int32_t* rb_phys;   // max over all sequences of the new lengths, or NULL
+  uint32_t* rb_ctr;   // workspace: {sequences finished, running max (sign bit flipped)}
+  int rb_lcap;
+  int B_total;        // sequences of the whole call (over all launches)
 };
 
 // exp2_hw drops weights under 2^-126 of their chunk's largest. The sweep and
@@ -709,6 +716,42 @@ __device__ void write_invalid(const Args& A, int b, uint32_t bits) {
   }
 }
 
+// Rollback of sequence b to `want` rows (Section 4.4, Eq. 9), exactly as the
+// rollback call does it: a length outside [0, L_cap] or a negative target is
+// flagged and left alone, a target above the length is flagged and ignored;
+// otherwise the mask entries [n, old) are cleared and the length becomes
+// n = min(old, want). The physical length (the maximum over all sequences of
+// the resulting lengths) is written by whichever sequence finishes last: a
+// counter and a running maximum in the workspace, reset by that sequence for
+// the next call. Called by one whole wave.
+__device__ void finish_rollback(const Args& A, int b, int want) {
+  if (!A.rb_kv) return;
+  const int lane = threadIdx.x & 63;
+  const int old = A.rb_kv[b];
+  int n = old;
+  int32_t st = 0;
+  if (old < 0 || old > A.rb_lcap || want < 0) {
+    st = SR_ST_KVLEN;
+  } else {
+    if (want > old) st = SR_ST_ROLLBACK_GROW;
+    n = min(old, want);
+    if (A.rb_mask)
+      for (int x = n + lane; x < old; x += 64) A.rb_mask[(size_t)b * A.rb_lcap + x] = 0;
+  }
+  if (lane == 0) {
+    A.rb_kv[b] = n;
+    if (st && A.status) atomicOr(A.status, st);
+    __hip_atomic_fetch_max(A.rb_ctr + 1, (uint32_t)n ^ 0x80000000u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t done = __hip_atomic_fetch_add(A.rb_ctr, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    if (done == (uint32_t)(A.B_total - 1)) {  // the last sequence: every maximum is in
+      const uint32_t m = __hip_atomic_load(A.rb_ctr + 1, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+      if (A.rb_phys) *A.rb_phys = (int32_t)(m ^ 0x80000000u);
+      st_dev(A.rb_ctr + 1, 0u);
+      st_dev(A.rb_ctr, 0u);
+    }
+  }
+}
+
 // Zero the records of sequence b's live rows (the "not yet written" state the
 // next call's sweep waits on). Called by one whole wave.
 __device__ void clear_records(const Args& A, int b, int gam) {
@@ -826,7 +869,10 @@ accept_finish_kernel(Args A) {
     }
   }
   if (gam < 0 || gam > A.gmax) {
-    if (w == 0) write_invalid(A, b, SR_ST_GAMMA);
+    if (w == 0) {
+      write_invalid(A, b, SR_ST_GAMMA);
+      finish_rollback(A, b, kvl);
+    }
     return;  // the sweep touched no row of this sequence
   }
   __syncthreads();
@@ -925,6 +971,7 @@ accept_finish_kernel(Args A) {
     if (w == 0) {
       clear_records(A, b, gam);  // every wave has finished reading them
       write_invalid(A, b, s_bad);
+      finish_rollback(A, b, kvl);
     }
     return;
   }
@@ -1108,6 +1155,7 @@ accept_finish_kernel(Args A) {
     A.accept_len[b] = k;
     if (A.new_len) A.new_len[b] = kvl - gam + k;
   }
+  finish_rollback(A, b, kvl - gam + k);
 }
 
 // Greedy finish kernel: one workgroup per sequence, one wave per live row.
@@ -1132,7 +1180,10 @@ accept_finish_greedy_kernel(Args A) {
   if (tid < A.gmax) s_x[tid] = A.drafts[(size_t)b * A.gmax + tid];
   const int kvl = A.kv_len ? A.kv_len[b] : 0;
   if (gam < 0 || gam > A.gmax) {
-    if (w == 0) write_invalid(A, b, SR_ST_GAMMA);
+    if (w == 0) {
+      write_invalid(A, b, SR_ST_GAMMA);
+      finish_rollback(A, b, kvl);
+    }
     return;  // the sweep touched no row of this sequence
   }
   __syncthreads();
@@ -1183,6 +1234,7 @@ accept_finish_greedy_kernel(Args A) {
   if (s_bad) {
     clear_records(A, b, gam);
     write_invalid(A, b, s_bad);
+    finish_rollback(A, b, kvl);
     return;
   }
   const unsigned long long rmask = __ballot(lane < gam && s_x[lane < gam ? lane : 0] != s_ap[lane < gam ? lane : 0]);
@@ -1205,6 +1257,7 @@ accept_finish_greedy_kernel(Args A) {
     A.accept_len[b] = k;
     if (A.new_len) A.new_len[b] = kvl - gam + k;
   }
+  finish_rollback(A, b, kvl - gam + k);
 }
 
 // Entries per lane per chunk.
@@ -1214,7 +1267,7 @@ constexpr int kEbf16 = 32;
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 struct Layout {
-  size_t stats, tvabs, xlogit, total;
+  size_t stats, tvabs, xlogit, rb, total;
 };
 
 Layout layout(int B, int gamma_max, int n_chunks) {
@@ -1223,7 +1276,8 @@ Layout layout(int B, int gamma_max, int n_chunks) {
   L.stats = 0;
   L.tvabs = align256(rows * n_chunks * kRecBytes);
   L.xlogit = L.tvabs + align256(rows * n_chunks * sizeof(double));
-  L.total = L.xlogit + align256(rows * 2 * sizeof(float));
+  L.rb = L.xlogit + align256(rows * 2 * sizeof(float));  // the rollback's counter and maximum
+  L.total = L.rb + 256;
   return L;
 }
 
@@ -1267,7 +1321,8 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
                   const float* u_res, const int32_t* kv_len, int32_t* accept_len,
                   int32_t* out_tokens, int32_t* new_len, float* accept_prob, float* p_tok,
                   float* q_tok, float* kl, float* tv, int B, int gamma_max, int V, float temperature,
-                  void* workspace, const AcceptPlan& plan, int32_t* status, hipStream_t stream) {
+                  const AcceptRollback* rollback, void* workspace, const AcceptPlan& plan, int32_t* status,
+                  hipStream_t stream) {
   const Layout L = layout(B, gamma_max, plan.n_chunks);
   const bool greedy = temperature == 0.f;
   const int G1 = gamma_max + 1;
@@ -1303,6 +1358,12 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
     A.tvabs = (double*)(ws + L.tvabs) + (size_t)b0 * G1 * plan.n_chunks;
     A.xlogit = (float*)(ws + L.xlogit) + (size_t)b0 * G1 * 2;
     A.status = status;
+    A.rb_kv = rollback ? rollback->kv_len + b0 : nullptr;
+    A.rb_mask = rollback && rollback->mask ? rollback->mask + (size_t)b0 * rollback->L_cap : nullptr;
+    A.rb_phys = rollback ? rollback->phys_len : nullptr;
+    A.rb_ctr = (uint32_t*)(ws + L.rb);
+    A.rb_lcap = rollback ? rollback->L_cap : 0;
+    A.B_total = B;
     A.lg = greedy ? 0.f : (float)(1.4426950408889634 / (double)temperature);
     A.inv_t = greedy ? 0.0 : 1.0 / (double)temperature;
     const size_t lds = Bl * sizeof(int);

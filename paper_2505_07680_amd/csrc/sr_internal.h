@@ -255,12 +255,22 @@ struct AcceptPlan {
 
 int accept_plan(int B, int gamma_max, int V, int dtype, AcceptPlan* plan);
 
+// Rollback applied by the accept call itself (after each sequence's outcome):
+// the same update as launch_rollback with new_len = the accept's new length.
+struct AcceptRollback {
+  int32_t* kv_len;    // [B] cache lengths, in/out
+  uint8_t* mask;      // [B][L_cap] validity mask, or NULL
+  int32_t* phys_len;  // max over sequences of the new lengths, or NULL
+  int L_cap;
+};
+
 int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, int64_t q_stride,
                   int dtype, const int32_t* drafts, const int32_t* gamma, const float* u_acc,
                   const float* u_res, const int32_t* kv_len, int32_t* accept_len,
                   int32_t* out_tokens, int32_t* new_len, float* accept_prob, float* p_tok,
                   float* q_tok, float* kl, float* tv, int B, int gamma_max, int V, float temperature,
-                  void* workspace, const AcceptPlan& plan, int32_t* status, hipStream_t stream);
+                  const AcceptRollback* rollback, void* workspace, const AcceptPlan& plan, int32_t* status,
+                  hipStream_t stream);
 
 int launch_chain_window(const int32_t* accept_len, const int32_t* out_tokens, int B, int gmax, int cap,
                         const int32_t* ctx_len, int32_t* gamma_next, int32_t* drafts_next,

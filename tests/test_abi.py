@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.specrouter_abi_version() == 2
+    assert lib.specrouter_abi_version() == 3
     for code in (0, -1, -2, -3, -4, 1, 2, 4, 8, 16, 32, 64):
         s = lib.specrouter_status_string(code)
         assert s and s != b"unknown code"
@@ -119,6 +119,22 @@ def test_sampled_accept_rejects_bad_sampling_parameters(lib):
     assert call(S(1.0, 0, 0.9)) == _lib.SR_EUNSUPPORTED
     assert call(S(0.5, 0, 1.0), u_acc=None) == _lib.SR_EINVAL  # sampling needs the uniforms
     assert call(S(0.5, 0, 1.0), u_res=None) == _lib.SR_EINVAL
+
+
+@no_device
+def test_accept_and_rollback_rejects_bad_host_arguments(lib):
+    p = ctypes.c_void_p(4096)
+    B, G, V = 2, 4, 1000
+
+    def call(kv=p, cache=p, L_cap=64):
+        args = ([p, (G + 1) * V, p, G * V, _lib.SR_F32, p, p, p, p, kv, p, p] + [None] * 6
+                + [B, G, V, None, cache, None, None, L_cap, None, 0, None, None])
+        return lib.specrouter_accept_and_rollback(*args)
+
+    assert call() in (_lib.SR_EWORKSPACE, _lib.SR_ELAUNCH)  # arguments fine, then no workspace or device
+    assert call(kv=None) == _lib.SR_EINVAL  # the new lengths need kv_len
+    assert call(cache=None) == _lib.SR_EINVAL
+    assert call(L_cap=0) == _lib.SR_EINVAL
 
 
 @no_device
