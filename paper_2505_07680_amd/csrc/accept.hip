@@ -166,9 +166,8 @@ struct Args {
   int32_t* rb_kv;     // [B] cache lengths, in/out
   uint8_t* rb_mask;   // [B][L_cap] validity mask, or NULL
   int32_t* rb_phys;   // max over all sequences of the new lengths, or NULL
-  uint32_t* rb_ctr;   // workspace: {sequences finished, running max (sign bit flipped)}
   int rb_lcap;
-  int B_total;        // sequences of the whole call (over all launches)
+  int rb_reset;       // this launch's sweep sets *rb_phys to INT_MIN first (the call's first launch)
 };
 
 // exp2_hw drops weights under 2^-126 of their chunk's largest. The sweep and
@@ -616,6 +615,7 @@ accept_sweep_kernel(Args A) {
   __shared__ SweepShared sh;
   Sweep<BF16, E> S(A, sh);
   const int w = S.w;
+  if (A.rb_reset && A.rb_phys && blockIdx.x == 0 && threadIdx.x == 0) *A.rb_phys = INT_MIN;  // see finish_rollback
 
   build_row_table(A.gamma, A.gmax, A.B, s_rows);
   const long n_tasks = (long)s_rows[A.B - 1] * S.nc;
@@ -671,6 +671,7 @@ accept_argmax_kernel(Args A) {
   extern __shared__ int s_rows[];
   __shared__ SweepShared sh;
   Sweep<BF16, E> S(A, sh);
+  if (A.rb_reset && A.rb_phys && blockIdx.x == 0 && threadIdx.x == 0) *A.rb_phys = INT_MIN;  // see finish_rollback
   build_row_table(A.gamma, A.gmax, A.B, s_rows);
   const long n_tasks = (long)s_rows[A.B - 1] * S.nc;
   long task = blockIdx.x;
@@ -716,18 +717,19 @@ __device__ void write_invalid(const Args& A, int b, uint32_t bits) {
   }
 }
 
-// Rollback of sequence b to `want` rows (Section 4.4, Eq. 9), exactly as the
-// rollback call does it: a length outside [0, L_cap] or a negative target is
-// flagged and left alone, a target above the length is flagged and ignored;
-// otherwise the mask entries [n, old) are cleared and the length becomes
-// n = min(old, want). The physical length (the maximum over all sequences of
-// the resulting lengths) is written by whichever sequence finishes last: a
-// counter and a running maximum in the workspace, reset by that sequence for
-// the next call. Called by one whole wave.
-__device__ void finish_rollback(const Args& A, int b, int want) {
+// Rollback of sequence b from `old` to `want` rows (Section 4.4, Eq. 9),
+// exactly as the rollback call does it: a length outside [0, L_cap] or a
+// negative target is flagged and left alone, a target above the length is
+// flagged and ignored; otherwise the mask entries [n, old) are cleared and
+// the length becomes n = min(old, want). The physical length is the maximum
+// of the resulting lengths over all sequences: the call's first sweep launch
+// sets it to INT_MIN and every sequence folds its length in with an atomic
+// maximum (no result is waited for). `old` is read at the start of the
+// finish kernel, so the rollback adds no round trip. Called by one whole
+// wave.
+__device__ void finish_rollback(const Args& A, int b, int old, int want) {
   if (!A.rb_kv) return;
   const int lane = threadIdx.x & 63;
-  const int old = A.rb_kv[b];
   int n = old;
   int32_t st = 0;
   if (old < 0 || old > A.rb_lcap || want < 0) {
@@ -741,14 +743,7 @@ __device__ void finish_rollback(const Args& A, int b, int want) {
   if (lane == 0) {
     A.rb_kv[b] = n;
     if (st && A.status) atomicOr(A.status, st);
-    __hip_atomic_fetch_max(A.rb_ctr + 1, (uint32_t)n ^ 0x80000000u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const uint32_t done = __hip_atomic_fetch_add(A.rb_ctr, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    if (done == (uint32_t)(A.B_total - 1)) {  // the last sequence: every maximum is in
-      const uint32_t m = __hip_atomic_load(A.rb_ctr + 1, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
-      if (A.rb_phys) *A.rb_phys = (int32_t)(m ^ 0x80000000u);
-      st_dev(A.rb_ctr + 1, 0u);
-      st_dev(A.rb_ctr, 0u);
-    }
+    if (A.rb_phys) atomicMax(A.rb_phys, n);
   }
 }
 
@@ -857,6 +852,7 @@ accept_finish_kernel(Args A) {
     F.ures[j] = ur;
   }
   const int kvl = A.kv_len ? A.kv_len[b] : 0;
+  const int rb_old = A.rb_kv ? A.rb_kv[b] : 0;
   // row w's records and draft logits, in the same round trip (pair or bonus
   // row is decided once gamma has arrived)
   RowRecs R0;
@@ -871,7 +867,7 @@ accept_finish_kernel(Args A) {
   if (gam < 0 || gam > A.gmax) {
     if (w == 0) {
       write_invalid(A, b, SR_ST_GAMMA);
-      finish_rollback(A, b, kvl);
+      finish_rollback(A, b, rb_old, kvl);
     }
     return;  // the sweep touched no row of this sequence
   }
@@ -971,7 +967,7 @@ accept_finish_kernel(Args A) {
     if (w == 0) {
       clear_records(A, b, gam);  // every wave has finished reading them
       write_invalid(A, b, s_bad);
-      finish_rollback(A, b, kvl);
+      finish_rollback(A, b, rb_old, kvl);
     }
     return;
   }
@@ -1155,7 +1151,7 @@ accept_finish_kernel(Args A) {
     A.accept_len[b] = k;
     if (A.new_len) A.new_len[b] = kvl - gam + k;
   }
-  finish_rollback(A, b, kvl - gam + k);
+  finish_rollback(A, b, rb_old, kvl - gam + k);
 }
 
 // Greedy finish kernel: one workgroup per sequence, one wave per live row.
@@ -1179,10 +1175,11 @@ accept_finish_greedy_kernel(Args A) {
   if (tid == 0) s_bad = 0;
   if (tid < A.gmax) s_x[tid] = A.drafts[(size_t)b * A.gmax + tid];
   const int kvl = A.kv_len ? A.kv_len[b] : 0;
+  const int rb_old = A.rb_kv ? A.rb_kv[b] : 0;
   if (gam < 0 || gam > A.gmax) {
     if (w == 0) {
       write_invalid(A, b, SR_ST_GAMMA);
-      finish_rollback(A, b, kvl);
+      finish_rollback(A, b, rb_old, kvl);
     }
     return;  // the sweep touched no row of this sequence
   }
@@ -1234,7 +1231,7 @@ accept_finish_greedy_kernel(Args A) {
   if (s_bad) {
     clear_records(A, b, gam);
     write_invalid(A, b, s_bad);
-    finish_rollback(A, b, kvl);
+    finish_rollback(A, b, rb_old, kvl);
     return;
   }
   const unsigned long long rmask = __ballot(lane < gam && s_x[lane < gam ? lane : 0] != s_ap[lane < gam ? lane : 0]);
@@ -1257,7 +1254,7 @@ accept_finish_greedy_kernel(Args A) {
     A.accept_len[b] = k;
     if (A.new_len) A.new_len[b] = kvl - gam + k;
   }
-  finish_rollback(A, b, kvl - gam + k);
+  finish_rollback(A, b, rb_old, kvl - gam + k);
 }
 
 // Entries per lane per chunk.
@@ -1267,7 +1264,7 @@ constexpr int kEbf16 = 32;
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 struct Layout {
-  size_t stats, tvabs, xlogit, rb, total;
+  size_t stats, tvabs, xlogit, total;
 };
 
 Layout layout(int B, int gamma_max, int n_chunks) {
@@ -1276,8 +1273,7 @@ Layout layout(int B, int gamma_max, int n_chunks) {
   L.stats = 0;
   L.tvabs = align256(rows * n_chunks * kRecBytes);
   L.xlogit = L.tvabs + align256(rows * n_chunks * sizeof(double));
-  L.rb = L.xlogit + align256(rows * 2 * sizeof(float));  // the rollback's counter and maximum
-  L.total = L.rb + 256;
+  L.total = L.xlogit + align256(rows * 2 * sizeof(float));
   return L;
 }
 
@@ -1361,9 +1357,8 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
     A.rb_kv = rollback ? rollback->kv_len + b0 : nullptr;
     A.rb_mask = rollback && rollback->mask ? rollback->mask + (size_t)b0 * rollback->L_cap : nullptr;
     A.rb_phys = rollback ? rollback->phys_len : nullptr;
-    A.rb_ctr = (uint32_t*)(ws + L.rb);
     A.rb_lcap = rollback ? rollback->L_cap : 0;
-    A.B_total = B;
+    A.rb_reset = b0 == 0 ? 1 : 0;
     A.lg = greedy ? 0.f : (float)(1.4426950408889634 / (double)temperature);
     A.inv_t = greedy ? 0.0 : 1.0 / (double)temperature;
     const size_t lds = Bl * sizeof(int);
