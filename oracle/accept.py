@@ -45,6 +45,23 @@ draft is accepted iff it is argmax p_j (no uniform is used), the extra token is
 argmax p_k, a_j, p(x) and q(x) are 1 or 0, TV_j is 0 when the two argmaxes
 agree and 1 otherwise, and KL_j is 0 or +infinity likewise.
 
+Top-k / top-p (the remaining logits processors, applied after the
+temperature, in that order, to every verifier row p_j and every draft row
+q_j alike -- the drafter samples from its filtered distribution and the
+verifier judges with its own; the rule above then runs on the filtered
+distributions unchanged, so its output is distributed as the filtered p):
+  top-k (1 <= k < V; 0 or k >= V is off): keep the entries whose logit is at
+    least the k-th largest logit; entries tied with it are all kept.
+  top-p (0 < p < 1; 1 is off): with r the softmax of the top-k result, keep
+    entry v iff the r-mass of the entries with a strictly larger logit is
+    below p. Equal logits are kept or removed together, the largest is always
+    kept. For distinct logits this is the usual rule (sort ascending, drop the
+    entries whose cumulative mass is at most 1 - p).
+A row's top-p margin is the smallest |mass above - p| over its distinct
+logits; a sequence with a margin below 1e-5 on any of its rows is marked as
+a boundary case (its filtered sets may legitimately differ under fp32 sums).
+Greedy decoding (T = 0) is unaffected (the largest logit is always kept).
+
 Data errors (status bits, same meaning as the library's): 1 gamma_b outside
 [0, gamma_max]; 2 kv_len_b < gamma_b + 1 (only when kv_len is given);
 4 a draft outside [0, V); 8 a needed uniform outside [0, 1). Such a sequence
@@ -61,6 +78,7 @@ ST_TOKEN = 4
 ST_UNIFORM = 8
 
 BOUNDARY = 1e-6
+FILTER_BOUNDARY = 1e-5
 
 
 def decode_logits(x) -> np.ndarray:
@@ -76,6 +94,28 @@ def log_softmax(z) -> np.ndarray:
     z = np.asarray(z, dtype=np.float64)
     m = np.max(z)
     return z - (m + np.log(np.sum(np.exp(z - m))))
+
+
+def filter_logits(z, top_k=0, top_p=1.0):
+    """Top-k then top-p on one row of (temperature-scaled) logits; removed
+    entries become -inf. Returns (filtered logits, top-p margin)."""
+    z = np.array(z, dtype=np.float64)
+    V = z.shape[0]
+    if 0 < top_k < V:
+        kth = np.sort(z)[V - top_k]  # the k-th largest value
+        z = np.where(z >= kth, z, -np.inf)
+    margin = np.inf
+    if top_p < 1.0:
+        r = np.exp(log_softmax(z))
+        vals, group = np.unique(z, return_inverse=True)  # ascending distinct values
+        mass = np.bincount(group, weights=r, minlength=vals.shape[0])
+        above = np.cumsum(mass[::-1])[::-1] - mass       # mass of the strictly larger values
+        keep = above < top_p
+        live = np.isfinite(vals)
+        if live.any():
+            margin = float(np.min(np.abs(above[live] - top_p)))
+        z = np.where(keep[group], z, -np.inf)
+    return z, margin
 
 
 def total_variation(p, q) -> float:
@@ -151,18 +191,27 @@ def accept_sequence_greedy(P, Q, drafts, gamma, gmax, V):
     return res
 
 
-def accept_sequence(P, Q, drafts, gamma, u_acc, u_res, gmax, V, temperature=1.0):
+def accept_sequence(P, Q, drafts, gamma, u_acc, u_res, gmax, V, temperature=1.0, top_k=0, top_p=1.0):
     """One sequence. P [>= gamma+1, V], Q [>= gamma, V] fp64 logits; every
-    distribution is softmax(logits / temperature) (temperature > 0)."""
+    distribution is softmax(logits / temperature) (temperature > 0), after
+    top-k / top-p filtering of each row."""
     if temperature != 1.0:
         P = np.asarray(P, dtype=np.float64) / temperature
         Q = np.asarray(Q, dtype=np.float64) / temperature
+    filter_margin = np.inf
+    if (0 < top_k < V) or top_p < 1.0:
+        P = np.array(P, dtype=np.float64)
+        Q = np.array(Q, dtype=np.float64)
+        for rows in (P, Q):
+            for j in range(rows.shape[0]):
+                rows[j], m = filter_logits(rows[j], top_k, top_p)
+                filter_margin = min(filter_margin, m)
     res = dict(
         accept_len=-1, tokens=np.full(gmax + 1, -1, dtype=np.int64),
         accept_prob=np.full(gmax, np.nan), p_tok=np.full(gmax, np.nan),
         q_tok=np.full(gmax, np.nan), kl=np.full(gmax, np.nan), tv=np.full(gmax, np.nan),
         lse_p=np.full(gmax + 1, np.nan), lse_q=np.full(gmax, np.nan),
-        margin=np.inf, status=0,
+        margin=np.inf, filter_margin=filter_margin, status=0,
     )
     g = int(gamma)
     if not (0 <= g <= gmax):
@@ -220,8 +269,10 @@ def accept_sequence(P, Q, drafts, gamma, u_acc, u_res, gmax, V, temperature=1.0)
     return res
 
 
-def accept_and_diverge(p_logits, q_logits, drafts, gamma, u_acc, u_res, kv_len=None, seqs=None, temperature=1.0):
-    """Reference accept-and-diverge pass over a batch (temperature 0: greedy).
+def accept_and_diverge(p_logits, q_logits, drafts, gamma, u_acc, u_res, kv_len=None, seqs=None, temperature=1.0,
+                       top_k=0, top_p=1.0):
+    """Reference accept-and-diverge pass over a batch (temperature 0: greedy;
+    top_k / top_p: the logits processors, off by default).
 
     p_logits [B, gmax+1, V] and q_logits [B, gmax, V]: fp32, fp64, or bf16 bit
     patterns (uint16). drafts [B, gmax] int; gamma [B]; u_acc [B, gmax];
@@ -256,7 +307,7 @@ def accept_and_diverge(p_logits, q_logits, drafts, gamma, u_acc, u_res, kv_len=N
         if temperature == 0:
             r = accept_sequence_greedy(P, Q, drafts[b], g, gmax, V)
         else:
-            r = accept_sequence(P, Q, drafts[b], g, u_acc[b], u_res[b], gmax, V, temperature)
+            r = accept_sequence(P, Q, drafts[b], g, u_acc[b], u_res[b], gmax, V, temperature, top_k, top_p)
         out["status"] |= r["status"]
         if r["status"]:
             continue
@@ -266,7 +317,7 @@ def accept_and_diverge(p_logits, q_logits, drafts, gamma, u_acc, u_res, kv_len=N
             out[key][b] = r[key]
         out["lse_p"][b] = r["lse_p"]
         out["margin"][b] = r["margin"]
-        out["boundary"][b] = r["margin"] < BOUNDARY
+        out["boundary"][b] = r["margin"] < BOUNDARY or r.get("filter_margin", np.inf) < FILTER_BOUNDARY
         if kv_len is not None:
             out["new_len"][b] = int(kv_len[b]) - g + r["accept_len"]
     return out
