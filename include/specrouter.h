@@ -188,7 +188,19 @@ int specrouter_accept_and_diverge(const void* p_logits, int64_t p_batch_stride,
  *   u_resample are not read (may be NULL); accept_prob, p_tok and q_tok are 1
  *   or 0, TV_j is 0 when argmax p_j == argmax q_j and 1 otherwise, KL_j is 0
  *   or +infinity likewise. No SR_ST_UNIFORM check is made.
- * top_k, top_p: reserved; must be 0 and 1 (else SR_EUNSUPPORTED).
+ * top_k, top_p (T > 0 only; greedy decoding keeps the argmax anyway): the
+ *   logits processors after the temperature, applied to every verifier row
+ *   and every draft row alike (the drafts are assumed drawn from the filtered
+ *   draft distribution); every output is then computed on the filtered
+ *   distributions. top_k in [1, V) keeps the logits that are at least the
+ *   k-th largest (ties with it all kept); 0 or >= V is off. top_p in (0, 1)
+ *   keeps a logit iff the mass, under softmax of what top-k kept, of the
+ *   strictly larger logits is below top_p (ties kept or dropped together;
+ *   the largest logit always stays); 1 is off. top_k < 0 or top_p outside
+ *   (0, 1] is SR_EINVAL. With a filter on, one extra kernel finds each row's
+ *   threshold first (a radix select over the row); top-p decides on fp32
+ *   masses, so a logit whose larger mass is within ~1e-7 of top_p may fall
+ *   either way.
  * A NULL sampling pointer means temperature 1. The sampling struct is a host
  * pointer, read before the call returns. temperature must be finite and >= 0
  * (else SR_EINVAL). All other arguments, the workspace and the outputs are as

@@ -294,7 +294,7 @@ def accept_and_diverge(p_logits, q_logits, drafts, gamma, u_acc, u_res, kv_len=N
         q_tok=np.full((B, gmax), np.nan), kl=np.full((B, gmax), np.nan),
         tv=np.full((B, gmax), np.nan), lse_p=np.full((B, gmax1), np.nan),
         lse_q=np.full((B, gmax), np.nan), margin=np.full(B, np.inf),
-        boundary=np.zeros(B, dtype=bool), status=0,
+        boundary=np.zeros(B, dtype=bool), filter_boundary=np.zeros(B, dtype=bool), status=0,
     )
     for b in (range(B) if seqs is None else seqs):
         g = int(gamma[b])
@@ -317,7 +317,8 @@ def accept_and_diverge(p_logits, q_logits, drafts, gamma, u_acc, u_res, kv_len=N
             out[key][b] = r[key]
         out["lse_p"][b] = r["lse_p"]
         out["margin"][b] = r["margin"]
-        out["boundary"][b] = r["margin"] < BOUNDARY or r.get("filter_margin", np.inf) < FILTER_BOUNDARY
+        out["filter_boundary"][b] = r.get("filter_margin", np.inf) < FILTER_BOUNDARY
+        out["boundary"][b] = r["margin"] < BOUNDARY or out["filter_boundary"][b]
         if kv_len is not None:
             out["new_len"][b] = int(kv_len[b]) - g + r["accept_len"]
     return out

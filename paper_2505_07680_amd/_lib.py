@@ -215,7 +215,7 @@ def specrouter_accept_and_diverge_sampled(p_logits, q_logits, draft_tokens, gamm
 def specrouter_accept_and_rollback(p_logits, q_logits, draft_tokens, gamma, u_accept, u_resample, kv_len,
                                    accept_len, out_tokens, new_len, accept_prob, p_tok, q_tok, kl, tv,
                                    cache_kv_len, cache_mask, phys_len, workspace, status=None, temperature=1.0,
-                                   L_cap=None):
+                                   L_cap=None, top_k=0, top_p=1.0):
     """specrouter_accept_and_diverge_sampled, then specrouter_rollback of
     cache_kv_len / cache_mask to the accepted lengths, in one call."""
     _dev(cache_kv_len, cache_mask, phys_len)
@@ -231,7 +231,8 @@ def specrouter_accept_and_rollback(p_logits, q_logits, draft_tokens, gamma, u_ac
         raise ValueError("L_cap is required when cache_mask is None")
     _accept(p_logits, q_logits, draft_tokens, gamma, u_accept, u_resample, kv_len, accept_len, out_tokens,
             new_len, accept_prob, p_tok, q_tok, kl, tv, workspace, status,
-            SamplingParams(float(temperature), 0, 1.0), rollback=(cache_kv_len, cache_mask, phys_len, int(L_cap)))
+            SamplingParams(float(temperature), int(top_k), float(top_p)),
+            rollback=(cache_kv_len, cache_mask, phys_len, int(L_cap)))
 
 
 def _accept(p_logits, q_logits, draft_tokens, gamma, u_accept, u_resample, kv_len, accept_len, out_tokens,

@@ -42,8 +42,10 @@ int accept_impl(const void* p_logits, int64_t p_batch_stride, const void* q_logi
                 int gamma_max, int V, const specrouter_sampling* sampling, const sr::AcceptRollback* rollback,
                 void* workspace, size_t workspace_bytes, int32_t* status, void* stream) {
   const float temperature = sampling ? sampling->temperature : 1.f;
+  const int top_k = sampling ? sampling->top_k : 0;
+  const float top_p = sampling ? sampling->top_p : 1.f;
   if (!(temperature >= 0.f && temperature < __builtin_inff())) return SR_EINVAL;
-  if (sampling && (sampling->top_k != 0 || sampling->top_p != 1.f)) return SR_EUNSUPPORTED;
+  if (top_k < 0 || !(top_p > 0.f && top_p <= 1.f)) return SR_EINVAL;
   const bool greedy = temperature == 0.f;
   if (B <= 0 || gamma_max < 0 || gamma_max > SPECROUTER_MAX_GAMMA || V <= 0) return SR_EINVAL;
   if (logits_dtype != SR_F32 && logits_dtype != SR_BF16) return SR_EUNSUPPORTED;
@@ -66,7 +68,8 @@ int accept_impl(const void* p_logits, int64_t p_batch_stride, const void* q_logi
   return sr::launch_accept(p_logits, p_batch_stride, q_logits, q_batch_stride, logits_dtype,
                            draft_tokens, gamma, u_accept, u_resample, kv_len, accept_len,
                            out_tokens, new_len, accept_prob, p_tok, q_tok, kl, tv, B, gamma_max,
-                           V, temperature, rollback, workspace, plan, status, (hipStream_t)stream);
+                           V, temperature, top_k, top_p, rollback, workspace, plan, status,
+                           (hipStream_t)stream);
 }
 
 }  // namespace

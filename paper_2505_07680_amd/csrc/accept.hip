@@ -15,8 +15,9 @@
 // chunks per row, so the chunks of one row are processed at the same time by
 // neighbouring workgroups. Per task:
 //   1. chunk maxima of p and q, then the sums of exp(z - max) and the KL
-//      numerator sum exp(p - max_p) (p - q), merged over the four waves in a
-//      fixed order and published as one record with device-coherent stores;
+//      numerator sum exp(p - max_p) ((p - max_p) - (q - max_q)), merged over
+//      the four waves in a fixed order and published as one record with
+//      device-coherent stores;
 //   2. pair rows only: one wave re-loads the row's records until all of them
 //      are present, merges them into the two log-normalisers (fp64, fixed
 //      order; the finish kernel merges identically, so both get bit-identical
@@ -80,7 +81,7 @@ struct StatRec {
   float mp, mq;  // chunk maxima of the p and q logits (-inf: none)
   double sp;     // sum exp(p - mp)
   double sq;     // sum exp(q - mq)
-  double kl;     // sum exp(p - mp) (p - q)
+  double kl;     // sum exp(p - mp) ((p - mp) - (q - mq))
 };
 // In memory: four 8-byte words {mp | mq << 32, sp, sq, kl}, each inverted.
 constexpr int kRecBytes = 32;
@@ -161,6 +162,7 @@ struct Args {
   u32x4* stats;     // [B][gmax+1][nc] records, two 16-byte halves each
   double* tvabs;    // [B][gmax+1][nc] sum |P - Q| per chunk (pair rows)
   float* xlogit;    // [B][gmax+1][2] the draft token's p and q logits (pair rows)
+  float* thr;       // [B][gmax+1][2] top-k / top-p thresholds of the p and q rows, or NULL (no filtering)
   int32_t* status;
   // rollback applied by the finish kernel (rb_kv NULL: none)
   int32_t* rb_kv;     // [B] cache lengths, in/out
@@ -278,6 +280,32 @@ struct Raw<true, E> {
   }
 };
 
+// Set the entries below a threshold to -inf (the top-k / top-p filter).
+template <int E>
+__device__ __forceinline__ void mask_below(Raw<false, E>& r, float tp, float tq) {
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    r.p[e] = r.p[e] >= tp ? r.p[e] : kNegInf;
+    r.q[e] = r.q[e] >= tq ? r.q[e] : kNegInf;
+  }
+}
+__device__ __forceinline__ uint32_t mask_pair(uint32_t w, float t) {
+  constexpr uint32_t kNegInfBf16 = 0xff80u;
+  const uint32_t lo = bf16_lo(w) >= t ? (w & 0xffffu) : kNegInfBf16;
+  const uint32_t hi = bf16_hi(w) >= t ? (w >> 16) : kNegInfBf16;
+  return lo | (hi << 16);
+}
+template <int E>
+__device__ __forceinline__ void mask_below(Raw<true, E>& r, float tp, float tq) {
+#pragma unroll
+  for (int v = 0; v < E / 8; ++v)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      r.p[v][i] = mask_pair(r.p[v][i], tp);
+      r.q[v][i] = mask_pair(r.q[v][i], tq);
+    }
+}
+
 struct TaskInfo {
   int b, j, c, row;
   int x;  // the row's draft token (pair rows; -1 for a bonus row)
@@ -368,6 +396,11 @@ struct Sweep {
   // (and, for fp32, the exponentials in r).
   __device__ __forceinline__ void first_pass(const TaskInfo& t, Raw<BF16, E>& r, float& cmp, float& cmq) {
     const int base = t.c * kChunk + w * (64 * E);
+    if (A.thr) {  // top-k / top-p: entries below the row's threshold become -inf (workgroup-uniform branch)
+      const float tp = A.thr[(size_t)t.row * 2];
+      const float tq = t.pair ? A.thr[(size_t)t.row * 2 + 1] : kNegInf;
+      mask_below(r, tp, tq);
+    }
     // The draft token's two logits, for the finish kernel's acceptance test:
     // the lane that holds entry x stores them (once per row).
     const int xo = t.x - base;  // offset of x in this wave's entries
@@ -410,6 +443,11 @@ struct Sweep {
     const float lg = A.lg;
     const float rp = cmp == kNegInf ? 0.f : cmp * lg;
     const float rq = cmq == kNegInf ? 0.f : cmq * lg;
+    // the KL numerator on logits relative to the chunk maxima, so that the
+    // row-level merge subtracts no large terms (two rows whose filtered
+    // distributions coincide give exactly zero)
+    const float op = cmp == kNegInf ? 0.f : cmp;
+    const float oq = cmq == kNegInf ? 0.f : cmq;
     double dsp, dsq = 0.0, dkl = 0.0;
     if (t.pair) {
       float gp[E / 4], gq[E / 4], gk[E / 4];
@@ -423,7 +461,7 @@ struct Sweep {
           const float zp = r.gp(e), zq = r.gq(e);
           ep[i] = in ? exp2_hw(fmaf(zp, lg, -rp)) : 0.f;
           eq[i] = in ? exp2_hw(fmaf(zq, lg, -rq)) : 0.f;
-          kt[i] = ep[i] > 0.f ? ep[i] * (zp - zq) : 0.f;
+          kt[i] = ep[i] > 0.f ? ep[i] * ((zp - op) - (zq - oq)) : 0.f;
           if constexpr (!BF16) {
             r.p[e] = ep[i];
             r.q[e] = eq[i];
@@ -941,14 +979,19 @@ accept_finish_kernel(Args A) {
     }
     if (!pair) continue;  // the bonus row needs no divergences
     const double Lp = np.log_norm(A.inv_t), Lq = nq.log_norm(A.inv_t);
+    // KL = (1/T) sum_c f_c (kl_c + s_c ((m_c - M_p) - (m'_c - M_q))) - (ln S_p - ln S_q),
+    // kl_c being the chunk's numerator relative to its maxima m_c (p) and m'_c (q)
     double tvd = 0.0, kld = 0.0;
 #pragma unroll
     for (int i = 0; i < kSlots; ++i) {
       tvd += R.ta[i];
-      kld += R.kl[i] * (double)np.factor(R.mp[i]);
+      if (R.mp[i] != kNegInf) {
+        const double dm = ((double)R.mp[i] - (double)np.M) - ((double)R.mq[i] - (double)nq.M);
+        kld += (double)np.factor(R.mp[i]) * (R.kl[i] + R.sp[i] * dm);
+      }
     }
     tvd = 0.5 * wave_sum_d(tvd);
-    kld = A.inv_t * wave_sum_d(kld) - (Lp - Lq);
+    kld = A.inv_t * wave_sum_d(kld) - (log(np.S) - log(nq.S));
     // p(x), q(x) and a = min(1, p(x)/q(x)): one exponential per lane (0-2)
     const double lpx = (double)zpx * A.inv_t - Lp;
     const double lqx = (double)zqx * A.inv_t - Lq;
@@ -1052,6 +1095,9 @@ accept_finish_kernel(Args A) {
     constexpr int kPass = 256 * kPerT;
     const bool residual = s_resid != 0;
     const float rp = s_fac[0], rq = s_fac[1], fp = s_fac[2], fq = s_fac[3];
+    const bool filt = A.thr != nullptr;
+    const float thr_p = filt ? A.thr[((size_t)b * G1 + k) * 2] : kNegInf;
+    const float thr_q = filt && k < gam ? A.thr[((size_t)b * G1 + k) * 2 + 1] : kNegInf;
     const char* prow = (const char*)A.p + ((size_t)b * A.p_stride + (size_t)k * A.V) * esz;
     const char* qrow = (const char*)A.q + ((size_t)b * A.q_stride + (size_t)k * A.V) * esz;
     const double rem0 = s_rem;
@@ -1070,6 +1116,13 @@ accept_finish_kernel(Args A) {
         if (residual) {
 #pragma unroll
           for (int v = 0; v < kPerT / VEC; ++v) Elt<BF16>::load(qrow, min(x0 + v * VEC, A.V - VEC), zq + v * VEC);
+        }
+        if (filt) {  // the same top-k / top-p filter the sweep applied
+#pragma unroll
+          for (int e = 0; e < kPerT; ++e) {
+            zp[e] = zp[e] >= thr_p ? zp[e] : kNegInf;
+            zq[e] = zq[e] >= thr_q ? zq[e] : kNegInf;
+          }
         }
 #pragma unroll
         for (int e = 0; e < kPerT; ++e) {
@@ -1152,6 +1205,223 @@ accept_finish_kernel(Args A) {
     if (A.new_len) A.new_len[b] = kvl - gam + k;
   }
   finish_rollback(A, b, rb_old, kvl - gam + k);
+}
+
+// ============================================================================
+// Top-k / top-p thresholds (the logits processors after the temperature)
+//
+// One workgroup of 1024 threads per live row (verifier rows p_0..p_gamma,
+// draft rows q_0..q_{gamma-1}). Logits are compared through an
+// order-preserving 32-bit key (-0 counted as +0), and the threshold is found
+// by a most-significant-digit radix select, 8 bits per level (4 levels for
+// fp32 keys, 2 for bf16, whose low 16 bits are fixed by the sign). Every level
+// is one pass over the row (read again from the caches) that histograms the
+// next digit of the keys that still match the selected prefix, in per-wave
+// LDS histograms that are then summed:
+//   top-k: counts; the bucket holding the k-th largest key is the one where
+//     the count of larger keys first reaches k;
+//   top-p: masses 2^((z - M) log2(e)/T) (fp32 terms, fp64 sums) over the keys
+//     top-k kept; the bucket of the smallest kept logit is the lowest
+//     non-empty bucket whose mass above (the larger buckets plus the mass
+//     above the prefix) is below p times the total.
+// The row's threshold t (a logit value; entries below it are removed) goes to
+// thr[b][j][p or q]. Keys are exact, so top-k matches the exact rule; top-p
+// decides on fp32 masses, so it may differ from exact arithmetic only when
+// the mass above a logit is within ~1e-7 of p.
+
+constexpr int kFiltThreads = 1024;
+constexpr int kFiltWaves = kFiltThreads / 64;
+
+__device__ __forceinline__ uint32_t order_key(float z) {
+  const uint32_t u = __float_as_uint(z + 0.f);  // -0 -> +0
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key_value(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+struct FiltShared {
+  uint32_t cnt[kFiltWaves][256];
+  double mass[kFiltWaves][256];
+  uint32_t wmax[kFiltWaves];
+  uint32_t pick;    // selected bucket
+  uint32_t need;    // top-k: keys still to count at the selected prefix
+  double above;     // top-p: mass above the selected prefix
+  double total;     // top-p: mass of the keys top-k kept
+};
+
+template <bool BF16>
+__global__ void __launch_bounds__(kFiltThreads)
+accept_filter_kernel(Args A, int top_k, float top_p) {
+  constexpr int VEC = Elt<BF16>::VEC;
+  constexpr int kLevels = BF16 ? 2 : 4;
+  __shared__ FiltShared F;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int per_seq = 2 * A.gmax + 1;  // p rows 0..gmax, then q rows 0..gmax-1
+  const int b = (int)blockIdx.x / per_seq, r = (int)blockIdx.x % per_seq;
+  const bool is_q = r > A.gmax;
+  const int j = is_q ? r - (A.gmax + 1) : r;
+  const int gam = A.gamma[b];
+  if (gam < 0 || gam > A.gmax || (is_q ? j >= gam : j > gam)) return;  // not a live row
+  const size_t esz = BF16 ? 2 : 4;
+  const char* row = is_q ? (const char*)A.q + ((size_t)b * A.q_stride + (size_t)j * A.V) * esz
+                         : (const char*)A.p + ((size_t)b * A.p_stride + (size_t)j * A.V) * esz;
+  const int V = A.V;
+
+  auto clear = [&]() {
+    for (int i = tid; i < kFiltWaves * 256; i += kFiltThreads) {
+      (&F.cnt[0][0])[i] = 0u;
+      (&F.mass[0][0])[i] = 0.0;
+    }
+  };
+  // One pass: histogram digit `shift` of the keys with (key & pmask) == prefix
+  // and key >= lo (masses relative to the logit M when with_mass).
+  auto pass = [&](uint32_t prefix, uint32_t pmask, int shift, uint32_t lo, bool with_mass, float M,
+                  uint32_t& kmax) {
+    for (int x0 = tid * VEC; x0 < V; x0 += kFiltThreads * VEC) {
+      float z[VEC];
+      Elt<BF16>::load(row, x0, z);
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) {
+        const uint32_t key = order_key(z[i]);
+        kmax = max(kmax, key);
+        if ((key & pmask) == prefix && key >= lo) {
+          const uint32_t d = (key >> shift) & 255u;
+          atomicAdd(&F.cnt[w][d], 1u);
+          if (with_mass) atomicAdd(&F.mass[w][d], (double)exp2_hw((z[i] - M) * A.lg));
+        }
+      }
+    }
+    __syncthreads();
+    for (int d = tid; d < 256; d += kFiltThreads) {  // sum the per-wave histograms into wave 0's
+      uint32_t c = 0;
+      double m = 0.0;
+      for (int i = 0; i < kFiltWaves; ++i) {
+        c += F.cnt[i][d];
+        m += F.mass[i][d];
+      }
+      F.cnt[0][d] = c;
+      F.mass[0][d] = m;
+    }
+    __syncthreads();
+  };
+
+  // ---- top-k: radix select of the k-th largest key
+  uint32_t prefix = 0u, pmask = 0u, kmax = 0u;
+  uint32_t lo = 0u;  // keys below lo are removed
+  bool have_max = false;
+  if (top_k > 0) {
+    if (tid == 0) F.need = (uint32_t)top_k;
+    for (int lev = 0; lev < kLevels; ++lev) {
+      const int shift = 24 - 8 * lev;
+      clear();
+      __syncthreads();
+      pass(prefix, pmask, shift, 0u, false, 0.f, kmax);
+      if (w == 0) {  // lane l holds buckets 255 - 4l .. 252 - 4l (descending)
+        uint32_t c[4], s = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          c[i] = F.cnt[0][255 - 4 * lane - i];
+          s += c[i];
+        }
+        const uint32_t incl = (uint32_t)wave_incl_scan_i((int)s);  // keys in buckets above and in this lane's
+        const uint32_t need = F.need;
+        uint32_t run = incl - s;  // keys in the higher buckets
+        int hit = -1;
+        uint32_t hneed = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (hit < 0 && run < need && need <= run + c[i]) {
+            hit = 255 - 4 * lane - i;
+            hneed = need - run;
+          }
+          run += c[i];
+        }
+        const unsigned long long bal = __ballot(hit >= 0);
+        const int src = bal ? __ffsll((long long)bal) - 1 : 0;
+        const int pick = lane_value(hit, src);
+        const int nneed = lane_value((int)hneed, src);
+        if (lane == 0) {
+          F.pick = (uint32_t)max(pick, 0);
+          F.need = (uint32_t)nneed;
+        }
+      }
+      __syncthreads();
+      prefix |= F.pick << shift;
+      pmask |= 255u << shift;
+    }
+    if (BF16) prefix |= (prefix & 0x80000000u) ? 0u : 0xffffu;  // the fixed low half of bf16 keys
+    lo = prefix;
+    have_max = true;
+  }
+
+  // ---- top-p over the keys top-k kept
+  uint32_t thr_key = lo;
+  if (top_p < 1.f) {
+    if (!have_max) {  // the row maximum M first
+      for (int x0 = tid * VEC; x0 < V; x0 += kFiltThreads * VEC) {
+        float z[VEC];
+        Elt<BF16>::load(row, x0, z);
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) kmax = max(kmax, order_key(z[i]));
+      }
+    }
+    const uint32_t wm = (uint32_t)wave_max_i((int)(kmax ^ 0x80000000u)) ^ 0x80000000u;  // unsigned max
+    if (lane == 0) F.wmax[w] = wm;
+    __syncthreads();
+    uint32_t m = 0u;
+    for (int i = 0; i < kFiltWaves; ++i) m = max(m, F.wmax[i]);
+    const float M = key_value(m);
+    prefix = 0u;
+    pmask = 0u;
+    if (tid == 0) F.above = 0.0;
+    for (int lev = 0; lev < kLevels; ++lev) {
+      const int shift = 24 - 8 * lev;
+      clear();
+      __syncthreads();
+      uint32_t dummy = 0u;
+      pass(prefix, pmask, shift, lo, true, M, dummy);
+      if (w == 0) {
+        uint32_t c[4];
+        double ms[4], s = 0.0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          c[i] = F.cnt[0][255 - 4 * lane - i];
+          ms[i] = F.mass[0][255 - 4 * lane - i];
+          s += ms[i];
+        }
+        const double incl = wave_incl_scan(s);
+        if (lev == 0 && lane == 63) F.total = incl;  // the mass of every key top-k kept
+        const double bar = (double)top_p * (lev == 0 ? lane_value(incl, 63) : F.total);
+        double run = F.above + (incl - s);  // mass above this lane's first bucket
+        int low = -1;
+        double low_above = 0.0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (c[i] > 0 && run < bar) {  // a non-empty bucket whose mass above is below p * total
+            low = 255 - 4 * lane - i;
+            low_above = run;
+          }
+          run += ms[i];
+        }
+        // the lowest such bucket: the last lane (in descending bucket order) that has one
+        const unsigned long long bal = __ballot(low >= 0);
+        const int src = bal ? 63 - __clzll((long long)bal) : 0;
+        const int pick = lane_value(low, src);
+        const double pa = lane_value(low_above, src);
+        if (lane == 0) {
+          F.pick = (uint32_t)max(pick, 0);
+          F.above = pa;
+        }
+      }
+      __syncthreads();
+      prefix |= F.pick << shift;
+      pmask |= 255u << shift;
+    }
+    if (BF16) prefix |= (prefix & 0x80000000u) ? 0u : 0xffffu;
+    thr_key = prefix;
+  }
+  if (tid == 0) A.thr[((size_t)b * (A.gmax + 1) + j) * 2 + (is_q ? 1 : 0)] = key_value(thr_key);
 }
 
 // Greedy finish kernel: one workgroup per sequence, one wave per live row.
@@ -1264,7 +1534,7 @@ constexpr int kEbf16 = 32;
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 struct Layout {
-  size_t stats, tvabs, xlogit, total;
+  size_t stats, tvabs, xlogit, thr, total;
 };
 
 Layout layout(int B, int gamma_max, int n_chunks) {
@@ -1273,7 +1543,8 @@ Layout layout(int B, int gamma_max, int n_chunks) {
   L.stats = 0;
   L.tvabs = align256(rows * n_chunks * kRecBytes);
   L.xlogit = L.tvabs + align256(rows * n_chunks * sizeof(double));
-  L.total = L.xlogit + align256(rows * 2 * sizeof(float));
+  L.thr = L.xlogit + align256(rows * 2 * sizeof(float));
+  L.total = L.thr + align256(rows * 2 * sizeof(float));
   return L;
 }
 
@@ -1317,8 +1588,8 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
                   const float* u_res, const int32_t* kv_len, int32_t* accept_len,
                   int32_t* out_tokens, int32_t* new_len, float* accept_prob, float* p_tok,
                   float* q_tok, float* kl, float* tv, int B, int gamma_max, int V, float temperature,
-                  const AcceptRollback* rollback, void* workspace, const AcceptPlan& plan, int32_t* status,
-                  hipStream_t stream) {
+                  int top_k, float top_p, const AcceptRollback* rollback, void* workspace,
+                  const AcceptPlan& plan, int32_t* status, hipStream_t stream) {
   const Layout L = layout(B, gamma_max, plan.n_chunks);
   const bool greedy = temperature == 0.f;
   const int G1 = gamma_max + 1;
@@ -1354,6 +1625,11 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
     A.tvabs = (double*)(ws + L.tvabs) + (size_t)b0 * G1 * plan.n_chunks;
     A.xlogit = (float*)(ws + L.xlogit) + (size_t)b0 * G1 * 2;
     A.status = status;
+    // top-k / top-p only under sampling (greedy keeps the argmax anyway)
+    const int k_eff = top_k > 0 && top_k < V ? top_k : 0;
+    const float p_eff = top_p < 1.f ? top_p : 1.f;
+    const bool filt = !greedy && (k_eff > 0 || p_eff < 1.f);
+    A.thr = filt ? (float*)(ws + L.thr) + (size_t)b0 * G1 * 2 : nullptr;
     A.rb_kv = rollback ? rollback->kv_len + b0 : nullptr;
     A.rb_mask = rollback && rollback->mask ? rollback->mask + (size_t)b0 * rollback->L_cap : nullptr;
     A.rb_phys = rollback ? rollback->phys_len : nullptr;
@@ -1371,6 +1647,14 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
       hipLaunchKernelGGL(accept_finish_greedy_kernel, dim3(Bl), dim3(64 * nw), 0, stream, A);
       if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
       continue;
+    }
+    if (filt) {  // the rows' top-k / top-p thresholds first
+      const dim3 grid_f((unsigned)(Bl * (2 * G1 - 1)));
+      if (dtype == SR_BF16)
+        hipLaunchKernelGGL(accept_filter_kernel<true>, grid_f, dim3(kFiltThreads), 0, stream, A, k_eff, p_eff);
+      else
+        hipLaunchKernelGGL(accept_filter_kernel<false>, grid_f, dim3(kFiltThreads), 0, stream, A, k_eff, p_eff);
+      if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
     }
     if (dtype == SR_BF16)
       hipLaunchKernelGGL((accept_sweep_kernel<true, kEbf16>), dim3(plan.grid), dim3(kThreads), lds, stream, A);

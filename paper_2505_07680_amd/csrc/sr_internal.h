@@ -269,8 +269,8 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
                   const float* u_res, const int32_t* kv_len, int32_t* accept_len,
                   int32_t* out_tokens, int32_t* new_len, float* accept_prob, float* p_tok,
                   float* q_tok, float* kl, float* tv, int B, int gamma_max, int V, float temperature,
-                  const AcceptRollback* rollback, void* workspace, const AcceptPlan& plan, int32_t* status,
-                  hipStream_t stream);
+                  int top_k, float top_p, const AcceptRollback* rollback, void* workspace,
+                  const AcceptPlan& plan, int32_t* status, hipStream_t stream);
 
 int launch_chain_window(const int32_t* accept_len, const int32_t* out_tokens, int B, int gmax, int cap,
                         const int32_t* ctx_len, int32_t* gamma_next, int32_t* drafts_next,

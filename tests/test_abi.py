@@ -115,8 +115,11 @@ def test_sampled_accept_rejects_bad_sampling_parameters(lib):
     assert call(S(0.0, 0, 1.0), u_acc=None, u_res=None) in later  # greedy reads no uniforms
     for t in (-0.5, float("nan"), float("inf")):
         assert call(S(t, 0, 1.0)) == _lib.SR_EINVAL
-    assert call(S(1.0, 5, 1.0)) == _lib.SR_EUNSUPPORTED
-    assert call(S(1.0, 0, 0.9)) == _lib.SR_EUNSUPPORTED
+    assert call(S(1.0, 5, 1.0)) in later  # top-k
+    assert call(S(1.0, 0, 0.9)) in later  # top-p
+    assert call(S(1.0, 40, 0.95)) in later
+    for k, tp in ((-1, 1.0), (0, 0.0), (0, -0.5), (0, 1.5), (0, float("nan"))):
+        assert call(S(1.0, k, tp)) == _lib.SR_EINVAL
     assert call(S(0.5, 0, 1.0), u_acc=None) == _lib.SR_EINVAL  # sampling needs the uniforms
     assert call(S(0.5, 0, 1.0), u_res=None) == _lib.SR_EINVAL
 

@@ -124,3 +124,72 @@ def test_config2_shaped_temperature_and_greedy_sampled():
                 np.testing.assert_array_equal(got["tv"][b], ref["tv"][b].astype(np.float32))
         else:
             check_accept(got, ref, seqs=seqs)
+
+
+# ---------------------------------------------------------------- top-k / top-p
+
+def _check_filtered(got, ref):
+    """check_accept on the sequences whose filtered sets the reference
+    decides with a margin (fp32 top-p sums may differ right at p)."""
+    keep = [b for b in range(ref["accept_len"].shape[0]) if not ref["filter_boundary"][b]]
+    nb, nbm = check_accept(got, ref, seqs=keep)
+    return len(ref["accept_len"]) - len(keep), nb, nbm
+
+
+FILTERS = [(1, 1.0), (7, 1.0), (50, 1.0), (0, 0.5), (0, 0.9), (20, 0.8), (3000, 0.95)]
+
+
+@pytest.mark.parametrize("shape", SHAPES[:2], ids=lambda s: s.name)
+@pytest.mark.parametrize("top_k,top_p", FILTERS)
+def test_top_k_top_p_match_reference(shape, top_k, top_p):
+    inp = level_inputs(shape, kv=False)
+    T = 0.8
+    say(f"filtered {shape.name} T={T} top_k={top_k} top_p={top_p}")
+    got = run_accept(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, inp.u_acc, inp.u_res, temperature=T,
+                     top_k=top_k, top_p=top_p)
+    ref = oracle.accept_and_diverge(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, inp.u_acc, inp.u_res,
+                                    temperature=T, top_k=top_k, top_p=top_p)
+    assert got["status"] == ref["status"] == 0
+    nf, nb, nbm = _check_filtered(got, ref)
+    say(f"  ok ({nf} filter-boundary sequences skipped, {nb} boundary, {nbm} differ)")
+
+
+def test_top_k_one_with_argmax_drafts_is_greedy_on_device():
+    shape = small_shape(name="k1", B=8, V=12288, gamma=(2, 6), seed=44, logits="bf16")
+    inp = level_inputs(shape, kv=False)
+    from oracle.accept import decode_logits
+
+    q = decode_logits(inp.q_logits)
+    drafts = inp.drafts.copy()
+    for b in range(shape.B):
+        for j in range(int(inp.gamma[b])):
+            drafts[b, j] = int(np.argmax(q[b, j]))  # what a one-hot draft distribution emits
+    got = run_accept(inp.p_logits, inp.q_logits, drafts, inp.gamma, inp.u_acc, inp.u_res, temperature=1.3, top_k=1)
+    ref = oracle.accept_and_diverge(inp.p_logits, inp.q_logits, drafts, inp.gamma, None, None, temperature=0.0)
+    np.testing.assert_array_equal(got["accept_len"], ref["accept_len"])
+    np.testing.assert_array_equal(got["out_tokens"], ref["out_tokens"])
+
+
+def test_filters_off_are_the_plain_rule():
+    shape = SHAPES[0]
+    inp = level_inputs(shape, kv=False)
+    a = run_accept(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, inp.u_acc, inp.u_res, temperature=0.8)
+    for k, p in ((0, 1.0), (shape.V, 1.0), (shape.V + 7, 1.0)):
+        b = run_accept(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, inp.u_acc, inp.u_res, temperature=0.8,
+                       top_k=k, top_p=p)
+        for key in a:
+            np.testing.assert_array_equal(np.asarray(b[key]), np.asarray(a[key]), err_msg=key)
+
+
+def test_filtered_config2_shape():
+    """The filter at the paper-scale vocabulary (one sequence sampled per row kind)."""
+    inp = level_inputs(CONFIGS[2], kv=False)
+    seqs = [0, 7]
+    say("filtered config 2 shape: top_k 40, top_p 0.9")
+    got = run_accept(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, inp.u_acc, inp.u_res, temperature=1.0,
+                     top_k=40, top_p=0.9)
+    ref = oracle.accept_and_diverge(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, inp.u_acc, inp.u_res,
+                                    temperature=1.0, top_k=40, top_p=0.9, seqs=seqs)
+    assert got["status"] == 0
+    keep = [b for b in seqs if not ref["filter_boundary"][b]]
+    check_accept(got, ref, seqs=keep)
