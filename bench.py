@@ -55,6 +55,7 @@ KERNEL_SOURCES = {
     "verify_attention": ["attention.hip", "sr_internal.h"],
     "accept_and_diverge": ["accept.hip", "sr_internal.h"],
     "rollback": ["rollback.hip", "sr_internal.h"],
+    "accept_filter": ["accept.hip", "sr_internal.h"],
 }
 
 
@@ -229,14 +230,14 @@ def main():
     # sampling variants of the accept call on the same inputs (greedy drafts
     # are the workload's drafts; only the timing is reported)
     variants = {}
-    for T in (0.0, 0.7):
+    for T, tk, tp in ((0.0, 0, 1.0), (0.7, 0, 1.0), (0.7, 50, 1.0), (0.7, 0, 0.9), (0.7, 50, 0.9)):
         for i in range(args.warmup):
             s = sets[i % R]
             a = s["acc"]
             sr.specrouter_accept_and_diverge_sampled(
                 s["p"], s["ql"], s["drafts"], s["gamma"], s["u_acc"], s["u_res"], s["kv_in"], a.accept_len,
                 a.out_tokens, a.new_len, a.accept_prob, a.p_tok, a.q_tok, a.kl, a.tv, a.workspace, s["st"],
-                temperature=T)
+                temperature=T, top_k=tk, top_p=tp)
         e0, e1 = ev(), ev()
         torch.cuda.synchronize()
         e0.record()
@@ -246,11 +247,12 @@ def main():
             sr.specrouter_accept_and_diverge_sampled(
                 s["p"], s["ql"], s["drafts"], s["gamma"], s["u_acc"], s["u_res"], s["kv_in"], a.accept_len,
                 a.out_tokens, a.new_len, a.accept_prob, a.p_tok, a.q_tok, a.kl, a.tv, a.workspace, s["st"],
-                temperature=T)
+                temperature=T, top_k=tk, top_p=tp)
         e1.record()
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) / K * 1e3
         name = "accept_greedy" if T == 0 else f"accept_temperature_{T}"
+        name += (f"_top_k_{tk}" if tk else "") + (f"_top_p_{tp}" if tp < 1 else "")
         variants[name] = {"us": round(us, 2), "GB/s": round(acc_bytes / us / 1e3, 1)}
     # chain glue between two verifier levels (window of a gamma-4 upper level
     # and the consensus), on this step's accept outputs as the lower level

@@ -269,13 +269,13 @@ __device__ __forceinline__ uint32_t fresh(uint32_t x) {
 }
 template <int E>
 struct Raw<true, E> {
-  u32x4 p[E / 8], q[E / 8];
+  u32x4 pk[E / 8], qk[E / 8];  // as loaded
   __device__ float gp(int e) const {
-    const uint32_t w = fresh(p[e / 8][(e % 8) / 2]);
+    const uint32_t w = fresh(pk[e / 8][(e % 8) / 2]);
     return (e & 1) ? bf16_hi(w) : bf16_lo(w);
   }
   __device__ float gq(int e) const {
-    const uint32_t w = fresh(q[e / 8][(e % 8) / 2]);
+    const uint32_t w = fresh(qk[e / 8][(e % 8) / 2]);
     return (e & 1) ? bf16_hi(w) : bf16_lo(w);
   }
 };
@@ -301,8 +301,8 @@ __device__ __forceinline__ void mask_below(Raw<true, E>& r, float tp, float tq) 
   for (int v = 0; v < E / 8; ++v)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      r.p[v][i] = mask_pair(r.p[v][i], tp);
-      r.q[v][i] = mask_pair(r.q[v][i], tq);
+      r.pk[v][i] = mask_pair(r.pk[v][i], tp);
+      r.qk[v][i] = mask_pair(r.qk[v][i], tq);
     }
 }
 
@@ -349,7 +349,7 @@ __device__ __forceinline__ void issue_loads(const Args& A, const TaskInfo& t, Ra
   for (int v = 0; v < NV; ++v) {
     const int x = min(base + (v * 64 + lane) * VEC, A.V - VEC);
     if constexpr (BF16) {
-      r.p[v] = *(const u32x4*)((const uint16_t*)t.prow + x);
+      r.pk[v] = *(const u32x4*)((const uint16_t*)t.prow + x);
     } else {
       const floatx4 f = *(const floatx4*)((const float*)t.prow + x);
 #pragma unroll
@@ -360,7 +360,7 @@ __device__ __forceinline__ void issue_loads(const Args& A, const TaskInfo& t, Ra
   for (int v = 0; v < NV; ++v) {
     const int x = min(base + (v * 64 + lane) * VEC, A.V - VEC);
     if constexpr (BF16) {
-      r.q[v] = *(const u32x4*)((const uint16_t*)t.qrow + x);
+      r.qk[v] = *(const u32x4*)((const uint16_t*)t.qrow + x);
     } else {
       const floatx4 f = *(const floatx4*)((const float*)t.qrow + x);
 #pragma unroll
@@ -1213,24 +1213,33 @@ accept_finish_kernel(Args A) {
 // One workgroup of 1024 threads per live row (verifier rows p_0..p_gamma,
 // draft rows q_0..q_{gamma-1}). Logits are compared through an
 // order-preserving 32-bit key (-0 counted as +0), and the threshold is found
-// by a most-significant-digit radix select, 8 bits per level (4 levels for
-// fp32 keys, 2 for bf16, whose low 16 bits are fixed by the sign). Every level
-// is one pass over the row (read again from the caches) that histograms the
-// next digit of the keys that still match the selected prefix, in per-wave
-// LDS histograms that are then summed:
-//   top-k: counts; the bucket holding the k-th largest key is the one where
-//     the count of larger keys first reaches k;
+// by a most-significant-digit radix select: a 12-bit first digit (sign,
+// exponent and three mantissa bits, so that logits of one row spread over
+// many bins), then 10 + 10 bits for fp32 keys or 4 bits for bf16 keys (whose
+// low 16 bits are fixed by the sign). Each level histograms the digit of the
+// keys that still match the selected prefix into one LDS histogram shared by
+// the waves:
+//   top-k: counts; the bin holding the k-th largest key is the one where the
+//     count of larger keys first reaches k;
 //   top-p: masses 2^((z - M) log2(e)/T) (fp32 terms, fp64 sums) over the keys
-//     top-k kept; the bucket of the smallest kept logit is the lowest
-//     non-empty bucket whose mass above (the larger buckets plus the mass
-//     above the prefix) is below p times the total.
-// The row's threshold t (a logit value; entries below it are removed) goes to
-// thr[b][j][p or q]. Keys are exact, so top-k matches the exact rule; top-p
-// decides on fp32 masses, so it may differ from exact arithmetic only when
-// the mass above a logit is within ~1e-7 of p.
+//     top-k kept; the bin of the smallest kept logit is the lowest non-empty
+//     bin whose mass above (the larger bins plus the mass above the prefix)
+//     is below p times the total.
+// The first level reads the row from memory. When the selected bin (or, with
+// top-p to follow, the bin and every key above it) holds at most kFiltCap
+// keys, one more read gathers those keys into LDS and the remaining levels
+// (and the whole of top-p after top-k) run on them there; otherwise every
+// level reads the row again. Under top-p alone one read before the first
+// level finds the row maximum M. The threshold t (a logit value; entries
+// below it are removed) goes to thr[b][j][p or q]. Keys are exact, so top-k
+// matches the exact rule; top-p decides on fp32 masses, so it may differ from
+// exact arithmetic only when the mass above a logit is within ~1e-7 of p.
 
 constexpr int kFiltThreads = 1024;
 constexpr int kFiltWaves = kFiltThreads / 64;
+constexpr int kFiltBins = 4096;  // the widest digit: 12 bits
+constexpr int kFiltCap = 8064;   // candidate keys held in LDS (two workgroups fit a CU's 160 KB)
+constexpr int kFiltUnroll = 4;   // row loads in flight per thread
 
 __device__ __forceinline__ uint32_t order_key(float z) {
   const uint32_t u = __float_as_uint(z + 0.f);  // -0 -> +0
@@ -1241,20 +1250,202 @@ __device__ __forceinline__ float key_value(uint32_t k) {
 }
 
 struct FiltShared {
-  uint32_t cnt[kFiltWaves][256];
-  double mass[kFiltWaves][256];
+  uint32_t cnt[kFiltBins];
+  double mass[kFiltBins];
+  uint32_t cand[kFiltCap];
+  uint32_t wtot_u[kFiltWaves];
+  double wtot_d[kFiltWaves];
   uint32_t wmax[kFiltWaves];
-  uint32_t pick;    // selected bucket
-  uint32_t need;    // top-k: keys still to count at the selected prefix
-  double above;     // top-p: mass above the selected prefix
-  double total;     // top-p: mass of the keys top-k kept
+  uint32_t n;      // candidates gathered so far
+  uint32_t pick;   // selected bin
+  uint32_t need;   // top-k: keys still to count inside the selected bin
+  uint32_t nge;    // top-k: keys in the selected bin and the bins above it
+  uint32_t cpick;  // top-p: keys in the selected bin
+  int lowest;      // top-p: the lowest qualifying bin
+  double above;    // top-p: mass above the selected prefix
+  double total;    // top-p: mass of the keys top-k kept
 };
+
+// Digit layout of level l: bits [shift, shift + bits) of the key.
+template <bool BF16>
+__device__ __forceinline__ int filt_shift(int l) {
+  return l == 0 ? 20 : BF16 ? 16 : l == 1 ? 10 : 0;
+}
+template <bool BF16>
+__device__ __forceinline__ int filt_bits(int l) {
+  return l == 0 ? 12 : BF16 ? 4 : 10;
+}
+
+// Block-wide exclusive prefix sums in thread order (a fixed order).
+__device__ __forceinline__ uint32_t filt_excl_scan(FiltShared& F, uint32_t s) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const uint32_t incl = (uint32_t)wave_incl_scan_i((int)s);
+  if (lane == 63) F.wtot_u[w] = incl;
+  __syncthreads();
+  uint32_t base = 0u;
+  for (int i = 0; i < w; ++i) base += F.wtot_u[i];
+  return base + incl - s;
+}
+__device__ __forceinline__ double filt_excl_scan(FiltShared& F, double s, double& total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const double incl = wave_incl_scan(s);
+  if (lane == 63) F.wtot_d[w] = incl;
+  __syncthreads();
+  double base = 0.0;
+  total = 0.0;
+  for (int i = 0; i < kFiltWaves; ++i) {
+    if (i == w) base = total;
+    total += F.wtot_d[i];
+  }
+  return base + incl - s;
+}
+
+// Histogram pass over the row in memory: digit (key >> shift) & dmask of the
+// keys with (key & pmask) == prefix and key >= lo; kmax collects every key.
+template <bool BF16, bool MASS>
+__device__ void filt_hist_row(FiltShared& F, const char* row, int V, uint32_t prefix, uint32_t pmask, int shift,
+                              uint32_t dmask, uint32_t lo, float M, float lg, uint32_t& kmax) {
+  constexpr int VEC = Elt<BF16>::VEC;
+  constexpr int STEP = kFiltThreads * VEC;
+  for (int x0 = (int)threadIdx.x * VEC; x0 < V; x0 += STEP * kFiltUnroll) {
+    float z[kFiltUnroll][VEC];
+#pragma unroll
+    for (int u = 0; u < kFiltUnroll; ++u)
+      if (x0 + u * STEP < V) Elt<BF16>::load(row, x0 + u * STEP, z[u]);
+#pragma unroll
+    for (int u = 0; u < kFiltUnroll; ++u) {
+      if (x0 + u * STEP >= V) break;
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) {
+        const uint32_t key = order_key(z[u][i]);
+        kmax = max(kmax, key);
+        if ((key & pmask) == prefix && key >= lo) {
+          const uint32_t d = (key >> shift) & dmask;
+          atomicAdd(&F.cnt[d], 1u);
+          if (MASS) atomicAdd(&F.mass[d], (double)exp2_hw((z[u][i] - M) * lg));
+        }
+      }
+    }
+  }
+}
+
+// The same over the n candidate keys in LDS.
+template <bool MASS>
+__device__ void filt_hist_cand(FiltShared& F, int n, uint32_t prefix, uint32_t pmask, int shift, uint32_t dmask,
+                               uint32_t lo, float M, float lg) {
+  for (int i = threadIdx.x; i < n; i += kFiltThreads) {
+    const uint32_t key = F.cand[i];
+    if ((key & pmask) == prefix && key >= lo) {
+      const uint32_t d = (key >> shift) & dmask;
+      atomicAdd(&F.cnt[d], 1u);
+      if (MASS) atomicAdd(&F.mass[d], (double)exp2_hw((key_value(key) - M) * lg));
+    }
+  }
+}
+
+// Gathers the row's keys in [klo, khi] into F.cand (F.n counts them; the
+// caller has checked that they fit).
+template <bool BF16>
+__device__ void filt_gather_row(FiltShared& F, const char* row, int V, uint32_t klo, uint32_t khi) {
+  constexpr int VEC = Elt<BF16>::VEC;
+  constexpr int STEP = kFiltThreads * VEC;
+  for (int x0 = (int)threadIdx.x * VEC; x0 < V; x0 += STEP * kFiltUnroll) {
+    float z[kFiltUnroll][VEC];
+#pragma unroll
+    for (int u = 0; u < kFiltUnroll; ++u)
+      if (x0 + u * STEP < V) Elt<BF16>::load(row, x0 + u * STEP, z[u]);
+#pragma unroll
+    for (int u = 0; u < kFiltUnroll; ++u) {
+      if (x0 + u * STEP >= V) break;
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) {
+        const uint32_t key = order_key(z[u][i]);
+        if (key >= klo && key <= khi) {
+          const uint32_t slot = atomicAdd(&F.n, 1u);
+          if (slot < (uint32_t)kFiltCap) F.cand[slot] = key;
+        }
+      }
+    }
+  }
+}
+
+// Thread t owns bins nb-1-t*per down to nb-t*per-per (descending order).
+struct FiltOwn {
+  int per, own, hi;
+  __device__ explicit FiltOwn(int nb) {
+    per = nb > kFiltThreads ? nb / kFiltThreads : 1;
+    own = (int)threadIdx.x * per < nb ? per : 0;
+    hi = nb - 1 - (int)threadIdx.x * per;
+  }
+};
+
+// top-k: the bin holding the need-th largest key of the histogram.
+__device__ void filt_select_count(FiltShared& F, int nb, uint32_t need) {
+  const FiltOwn o(nb);
+  uint32_t c[4], s = 0u;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    c[i] = i < o.own ? F.cnt[o.hi - i] : 0u;
+    s += c[i];
+  }
+  uint32_t run = filt_excl_scan(F, s);  // keys in the higher bins
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if (i < o.own && run < need && need <= run + c[i]) {
+      F.pick = (uint32_t)(o.hi - i);
+      F.need = need - run;
+      F.nge = run + c[i];
+    }
+    run += c[i];
+  }
+  __syncthreads();
+}
+
+// top-p: the lowest non-empty bin whose mass above is below p times the
+// total (the total is this histogram's at the first level).
+__device__ void filt_select_mass(FiltShared& F, int nb, float top_p, bool first) {
+  const FiltOwn o(nb);
+  const double above = F.above;
+  uint32_t c[4];
+  double ms[4], s = 0.0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    c[i] = i < o.own ? F.cnt[o.hi - i] : 0u;
+    ms[i] = i < o.own ? F.mass[o.hi - i] : 0.0;
+    s += ms[i];
+  }
+  double all;
+  double run = above + filt_excl_scan(F, s, all);  // mass above this thread's first bin
+  const double total = first ? all : F.total;
+  const double bar = (double)top_p * total;
+  int low = -1;
+  double low_above = 0.0;
+  uint32_t low_cnt = 0u;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if (i < o.own && c[i] > 0u && run < bar) {
+      low = o.hi - i;
+      low_above = run;
+      low_cnt = c[i];
+    }
+    run += ms[i];
+  }
+  if (low >= 0) atomicMin(&F.lowest, low);
+  __syncthreads();
+  if (low >= 0 && low == F.lowest) {
+    F.pick = (uint32_t)low;
+    F.above = low_above;
+    F.cpick = low_cnt;
+  }
+  if (first && threadIdx.x == 0) F.total = total;
+  __syncthreads();
+}
 
 template <bool BF16>
 __global__ void __launch_bounds__(kFiltThreads)
 accept_filter_kernel(Args A, int top_k, float top_p) {
   constexpr int VEC = Elt<BF16>::VEC;
-  constexpr int kLevels = BF16 ? 2 : 4;
+  constexpr int kLevels = BF16 ? 2 : 3;
   __shared__ FiltShared F;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int per_seq = 2 * A.gmax + 1;  // p rows 0..gmax, then q rows 0..gmax-1
@@ -1268,87 +1459,62 @@ accept_filter_kernel(Args A, int top_k, float top_p) {
                          : (const char*)A.p + ((size_t)b * A.p_stride + (size_t)j * A.V) * esz;
   const int V = A.V;
 
-  auto clear = [&]() {
-    for (int i = tid; i < kFiltWaves * 256; i += kFiltThreads) {
-      (&F.cnt[0][0])[i] = 0u;
-      (&F.mass[0][0])[i] = 0.0;
+  auto clear = [&](int nb) {
+    __syncthreads();  // every thread is done with the previous level's histogram and picks
+    for (int i = tid; i < nb; i += kFiltThreads) {
+      F.cnt[i] = 0u;
+      F.mass[i] = 0.0;
     }
-  };
-  // One pass: histogram digit `shift` of the keys with (key & pmask) == prefix
-  // and key >= lo (masses relative to the logit M when with_mass).
-  auto pass = [&](uint32_t prefix, uint32_t pmask, int shift, uint32_t lo, bool with_mass, float M,
-                  uint32_t& kmax) {
-    for (int x0 = tid * VEC; x0 < V; x0 += kFiltThreads * VEC) {
-      float z[VEC];
-      Elt<BF16>::load(row, x0, z);
-#pragma unroll
-      for (int i = 0; i < VEC; ++i) {
-        const uint32_t key = order_key(z[i]);
-        kmax = max(kmax, key);
-        if ((key & pmask) == prefix && key >= lo) {
-          const uint32_t d = (key >> shift) & 255u;
-          atomicAdd(&F.cnt[w][d], 1u);
-          if (with_mass) atomicAdd(&F.mass[w][d], (double)exp2_hw((z[i] - M) * A.lg));
-        }
-      }
-    }
-    __syncthreads();
-    for (int d = tid; d < 256; d += kFiltThreads) {  // sum the per-wave histograms into wave 0's
-      uint32_t c = 0;
-      double m = 0.0;
-      for (int i = 0; i < kFiltWaves; ++i) {
-        c += F.cnt[i][d];
-        m += F.mass[i][d];
-      }
-      F.cnt[0][d] = c;
-      F.mass[0][d] = m;
+    if (tid == 0) {
+      F.pick = 0u;
+      F.need = 1u;
+      F.nge = 0u;
+      F.cpick = 0u;
+      F.lowest = INT_MAX;
     }
     __syncthreads();
   };
+  // Gathers the keys in [klo, khi] into F.cand; returns their count.
+  auto gather = [&](uint32_t klo, uint32_t khi) {
+    __syncthreads();  // every thread has read the picks (and is done with F.cand)
+    if (tid == 0) F.n = 0u;
+    __syncthreads();
+    filt_gather_row<BF16>(F, row, V, klo, khi);
+    __syncthreads();
+    return (int)min(F.n, (uint32_t)kFiltCap);
+  };
+  int ncand = 0;        // keys in F.cand
+  bool cand_ge = false;  // F.cand holds every key >= lo
 
   // ---- top-k: radix select of the k-th largest key
-  uint32_t prefix = 0u, pmask = 0u, kmax = 0u;
+  uint32_t kmax = 0u;
   uint32_t lo = 0u;  // keys below lo are removed
   bool have_max = false;
   if (top_k > 0) {
-    if (tid == 0) F.need = (uint32_t)top_k;
-    for (int lev = 0; lev < kLevels; ++lev) {
-      const int shift = 24 - 8 * lev;
-      clear();
+    uint32_t prefix = 0u, pmask = 0u, need = (uint32_t)top_k;
+    bool in_lds = false;
+    for (int l = 0; l < kLevels; ++l) {
+      const int sh = filt_shift<BF16>(l), nb = 1 << filt_bits<BF16>(l);
+      clear(nb);
+      if (in_lds)
+        filt_hist_cand<false>(F, ncand, prefix, pmask, sh, (uint32_t)nb - 1u, 0u, 0.f, 0.f);
+      else
+        filt_hist_row<BF16, false>(F, row, V, prefix, pmask, sh, (uint32_t)nb - 1u, 0u, 0.f, 0.f, kmax);
       __syncthreads();
-      pass(prefix, pmask, shift, 0u, false, 0.f, kmax);
-      if (w == 0) {  // lane l holds buckets 255 - 4l .. 252 - 4l (descending)
-        uint32_t c[4], s = 0;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          c[i] = F.cnt[0][255 - 4 * lane - i];
-          s += c[i];
-        }
-        const uint32_t incl = (uint32_t)wave_incl_scan_i((int)s);  // keys in buckets above and in this lane's
-        const uint32_t need = F.need;
-        uint32_t run = incl - s;  // keys in the higher buckets
-        int hit = -1;
-        uint32_t hneed = 0;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          if (hit < 0 && run < need && need <= run + c[i]) {
-            hit = 255 - 4 * lane - i;
-            hneed = need - run;
-          }
-          run += c[i];
-        }
-        const unsigned long long bal = __ballot(hit >= 0);
-        const int src = bal ? __ffsll((long long)bal) - 1 : 0;
-        const int pick = lane_value(hit, src);
-        const int nneed = lane_value((int)hneed, src);
-        if (lane == 0) {
-          F.pick = (uint32_t)max(pick, 0);
-          F.need = (uint32_t)nneed;
-        }
+      filt_select_count(F, nb, need);
+      const uint32_t pick = F.pick;
+      need = F.need;
+      // with top-p to follow, keep every key from this bin up (top-p's input)
+      const uint32_t want = top_p < 1.f ? F.nge : F.cnt[pick];
+      const uint32_t pbase = prefix | (pick << sh);
+      const uint32_t pspan = (1u << sh) - 1u;  // the bits below this digit
+      prefix = pbase;
+      pmask |= ((uint32_t)nb - 1u) << sh;
+      if (l == 0 && want <= (uint32_t)kFiltCap) {
+        ncand = gather(pbase, top_p < 1.f ? 0xffffffffu : (pbase | pspan));
+        in_lds = true;
+        cand_ge = top_p < 1.f;
       }
-      __syncthreads();
-      prefix |= F.pick << shift;
-      pmask |= 255u << shift;
     }
     if (BF16) prefix |= (prefix & 0x80000000u) ? 0u : 0xffffu;  // the fixed low half of bf16 keys
     lo = prefix;
@@ -1359,64 +1525,48 @@ accept_filter_kernel(Args A, int top_k, float top_p) {
   uint32_t thr_key = lo;
   if (top_p < 1.f) {
     if (!have_max) {  // the row maximum M first
-      for (int x0 = tid * VEC; x0 < V; x0 += kFiltThreads * VEC) {
-        float z[VEC];
-        Elt<BF16>::load(row, x0, z);
+      constexpr int STEP = kFiltThreads * VEC;
+      for (int x0 = tid * VEC; x0 < V; x0 += STEP * kFiltUnroll) {
+        float z[kFiltUnroll][VEC];
 #pragma unroll
-        for (int i = 0; i < VEC; ++i) kmax = max(kmax, order_key(z[i]));
+        for (int u = 0; u < kFiltUnroll; ++u)
+          if (x0 + u * STEP < V) Elt<BF16>::load(row, x0 + u * STEP, z[u]);
+#pragma unroll
+        for (int u = 0; u < kFiltUnroll; ++u) {
+          if (x0 + u * STEP >= V) break;
+#pragma unroll
+          for (int i = 0; i < VEC; ++i) kmax = max(kmax, order_key(z[u][i]));
+        }
       }
     }
     const uint32_t wm = (uint32_t)wave_max_i((int)(kmax ^ 0x80000000u)) ^ 0x80000000u;  // unsigned max
     if (lane == 0) F.wmax[w] = wm;
+    if (tid == 0) F.above = 0.0;
     __syncthreads();
     uint32_t m = 0u;
     for (int i = 0; i < kFiltWaves; ++i) m = max(m, F.wmax[i]);
     const float M = key_value(m);
-    prefix = 0u;
-    pmask = 0u;
-    if (tid == 0) F.above = 0.0;
-    for (int lev = 0; lev < kLevels; ++lev) {
-      const int shift = 24 - 8 * lev;
-      clear();
-      __syncthreads();
+    uint32_t prefix = 0u, pmask = 0u;
+    bool in_lds = cand_ge;
+    for (int l = 0; l < kLevels; ++l) {
+      const int sh = filt_shift<BF16>(l), nb = 1 << filt_bits<BF16>(l);
+      clear(nb);
       uint32_t dummy = 0u;
-      pass(prefix, pmask, shift, lo, true, M, dummy);
-      if (w == 0) {
-        uint32_t c[4];
-        double ms[4], s = 0.0;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          c[i] = F.cnt[0][255 - 4 * lane - i];
-          ms[i] = F.mass[0][255 - 4 * lane - i];
-          s += ms[i];
-        }
-        const double incl = wave_incl_scan(s);
-        if (lev == 0 && lane == 63) F.total = incl;  // the mass of every key top-k kept
-        const double bar = (double)top_p * (lev == 0 ? lane_value(incl, 63) : F.total);
-        double run = F.above + (incl - s);  // mass above this lane's first bucket
-        int low = -1;
-        double low_above = 0.0;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          if (c[i] > 0 && run < bar) {  // a non-empty bucket whose mass above is below p * total
-            low = 255 - 4 * lane - i;
-            low_above = run;
-          }
-          run += ms[i];
-        }
-        // the lowest such bucket: the last lane (in descending bucket order) that has one
-        const unsigned long long bal = __ballot(low >= 0);
-        const int src = bal ? 63 - __clzll((long long)bal) : 0;
-        const int pick = lane_value(low, src);
-        const double pa = lane_value(low_above, src);
-        if (lane == 0) {
-          F.pick = (uint32_t)max(pick, 0);
-          F.above = pa;
-        }
-      }
+      if (in_lds)
+        filt_hist_cand<true>(F, ncand, prefix, pmask, sh, (uint32_t)nb - 1u, lo, M, A.lg);
+      else
+        filt_hist_row<BF16, true>(F, row, V, prefix, pmask, sh, (uint32_t)nb - 1u, lo, M, A.lg, dummy);
       __syncthreads();
-      prefix |= F.pick << shift;
-      pmask |= 255u << shift;
+      filt_select_mass(F, nb, top_p, l == 0);
+      const uint32_t pick = F.pick, cpick = F.cpick;
+      const uint32_t pbase = prefix | (pick << sh);
+      const uint32_t pspan = (1u << sh) - 1u;
+      prefix = pbase;
+      pmask |= ((uint32_t)nb - 1u) << sh;
+      if (l == 0 && !in_lds && cpick <= (uint32_t)kFiltCap) {
+        ncand = gather(max(pbase, lo), pbase | pspan);
+        in_lds = true;
+      }
     }
     if (BF16) prefix |= (prefix & 0x80000000u) ? 0u : 0xffffu;
     thr_key = prefix;

@@ -38,6 +38,7 @@ ENTRY_KERNELS = {  # kernel-name fragments launched by each entry point
     "verify_attention": ["attn_split_kernel"],
     "accept_and_diverge": ["accept_sweep_kernel", "accept_finish_kernel"],
     "rollback": ["rollback_kernel"],
+    "accept_filter": ["accept_filter_kernel"],  # top-k / top-p thresholds (sampling variants only)
 }
 COPY_KERNEL = "copyBuffer"
 

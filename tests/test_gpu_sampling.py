@@ -154,6 +154,34 @@ def test_top_k_top_p_match_reference(shape, top_k, top_p):
     say(f"  ok ({nf} filter-boundary sequences skipped, {nb} boundary, {nbm} differ)")
 
 
+@pytest.mark.parametrize("logits", ["f32", "bf16"])
+@pytest.mark.parametrize("top_k,top_p", [(9000, 1.0), (0, 0.5), (9000, 0.6), (40, 0.7)])
+def test_filters_on_a_narrow_logit_range(logits, top_k, top_p):
+    """Every logit in [1, 1.1): the whole row shares one first-level digit of
+    the threshold search, more keys than its LDS candidate buffer holds, so
+    the search reads the row at every level. The logits sit on a grid of 512
+    values (ties of ~40 keys; bf16 rounds them to 13 values), so that top-p's
+    cumulative masses move in steps well above the boundary margin."""
+    shape = small_shape(name=f"narrow-{logits}", B=6, V=20000, gamma=(1, 3), seed=71, logits=logits)
+    inp = level_inputs(shape, kv=False)
+    rng = np.random.default_rng(71)
+
+    def narrow(like):
+        z = (1.0 + 0.1 * rng.integers(0, 512, like.shape) / 512.0).astype(np.float32)
+        return (z.view(np.uint32) >> 16).astype(np.uint16) if logits == "bf16" else z
+
+    p_l, q_l = narrow(inp.p_logits), narrow(inp.q_logits)
+    say(f"narrow logits {logits} top_k={top_k} top_p={top_p}")
+    got = run_accept(p_l, q_l, inp.drafts, inp.gamma, inp.u_acc, inp.u_res, temperature=0.8, top_k=top_k,
+                     top_p=top_p)
+    ref = oracle.accept_and_diverge(p_l, q_l, inp.drafts, inp.gamma, inp.u_acc, inp.u_res, temperature=0.8,
+                                    top_k=top_k, top_p=top_p)
+    assert got["status"] == ref["status"] == 0
+    nf, nb, nbm = _check_filtered(got, ref)
+    assert nf < shape.B
+    say(f"  ok ({nf} filter-boundary sequences skipped, {nb} boundary, {nbm} differ)")
+
+
 def test_top_k_one_with_argmax_drafts_is_greedy_on_device():
     shape = small_shape(name="k1", B=8, V=12288, gamma=(2, 6), seed=44, logits="bf16")
     inp = level_inputs(shape, kv=False)
