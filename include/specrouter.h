@@ -157,7 +157,7 @@ int specrouter_verify_attention(const void* q, const void* k_cache, const void* 
  *               j >= gamma_b (and all entries of a bad sequence) are NaN
  * workspace     device scratch of specrouter_accept_workspace_size() bytes; it
  *               must be zero-filled before its FIRST use and every call leaves
- *               it zero-filled again (its counters reset themselves)
+ *               it zero-filled again (each call clears the records it wrote)
  * Logits must be finite or -inf; a row that is entirely -inf is not supported.
  * Requires (V * element size) % 16 == 0 and 16-byte aligned logits pointers and
  * strides, else SR_EUNSUPPORTED.
