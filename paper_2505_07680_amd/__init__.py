@@ -2,7 +2,8 @@
 
 The compute lives in libspecrouter.so (hand-written HIP kernels behind a C
 ABI, declared in include/specrouter.h) together with the host-side chain
-scheduler (include/specrouter_sched.h); this package holds their sources, the
+scheduler (include/specrouter_sched.h) and an HBM read-bandwidth probe
+(include/specrouter_probe.h); this package holds their sources, the
 build script and a thin ctypes binding with the same function names as the C
 entry points.
 """
@@ -22,6 +23,7 @@ from ._lib import (
     specrouter_accept_workspace_size,
     specrouter_chain_consensus,
     specrouter_chain_window,
+    specrouter_hbm_read_probe,
     specrouter_kv_append,
     specrouter_kv_compact,
     specrouter_rollback,
@@ -44,6 +46,7 @@ __all__ = [
     "specrouter_accept_workspace_size",
     "specrouter_chain_consensus",
     "specrouter_chain_window",
+    "specrouter_hbm_read_probe",
     "specrouter_kv_append",
     "specrouter_kv_compact",
     "specrouter_rollback",

@@ -18,7 +18,7 @@ import torch
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libspecrouter.so")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
-HEADERS = [os.path.join(INCLUDE, "specrouter.h"), os.path.join(INCLUDE, "specrouter_sched.h")]
+HEADERS = [os.path.join(INCLUDE, h) for h in ("specrouter.h", "specrouter_sched.h", "specrouter_probe.h")]
 
 SR_OK, SR_EINVAL, SR_EUNSUPPORTED, SR_EWORKSPACE, SR_ELAUNCH = 0, -1, -2, -3, -4
 SR_F32, SR_BF16 = 0, 1
@@ -67,6 +67,7 @@ _SIGNATURES = {
     "specrouter_kv_append": (_c_i, [_c_p] * 8 + [_c_i] * 5 + [_c_p, _c_p]),
     "specrouter_kv_compact": (_c_i, [_c_p] * 4 + [_c_i] * 4 + [_c_p, _c_p]),
     "specrouter_chain_consensus": (_c_i, [_c_p, _c_p, _c_p, _c_i, _c_p, _c_p, _c_i, _c_i] + [_c_p] * 6),
+    "specrouter_hbm_read_probe": (_c_i, [_c_p, _c_sz, _c_p, _c_p]),
     # chain scheduler (host code; host pointers)
     "specrouter_sched_create": (_c_i, [_c_i, _c_dp, _c_i, _c_i, _c_i, _c_d, _c_d, _c_d, ctypes.POINTER(_c_p)]),
     "specrouter_sched_destroy": (None, [_c_p]),
@@ -272,6 +273,16 @@ def _accept(p_logits, q_logits, draft_tokens, gamma, u_accept, u_resample, kv_le
         return
     rc = load().specrouter_accept_and_diverge_sampled(*common, _ptr(workspace), ws_bytes, _ptr(status), _stream())
     _check(rc, "specrouter_accept_and_diverge" + ("" if sampling is None else "_sampled"))
+
+
+def specrouter_hbm_read_probe(buf, sink=None):
+    """Stream the bytes of the contiguous device tensor `buf` once (the read
+    bandwidth probe); `sink` is an optional one-element int32 device tensor."""
+    _dev(buf, sink)
+    if not buf.is_contiguous():
+        raise ValueError("buf must be contiguous")
+    rc = load().specrouter_hbm_read_probe(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), _stream())
+    _check(rc, "specrouter_hbm_read_probe")
 
 
 def specrouter_rollback(kv_len, cache_mask, new_len, phys_len=None, status=None, L_cap=None):

@@ -55,6 +55,11 @@ constexpr int kMaxSplitKeys = 4224;  // keys per split at most (about 2 MB of K/
 // Byte offset past the end of any K/V slab (slabs are below 2^31 bytes): a
 // buffer load there returns zero without touching memory.
 constexpr uint32_t kOutOfRange = 0x7ffffff0u;
+// Cache-policy operand of the K/V loads when one workgroup is the only
+// reader of its K/V tiles (a single query chunk): non-temporal. With several
+// query chunks the others re-read the same tiles, which then should stay in
+// the caches (plain loads).
+constexpr int kStreamLoad = 2;
 
 template <int D>
 struct Geo {
@@ -117,7 +122,7 @@ struct Occ {
   static constexpr int kMinWaves = NQ <= 3 ? 2 : 1;
 };
 
-template <int D, int NQ>
+template <int D, int NQ, bool NT>
 __global__ void __launch_bounds__(kThreads, Occ<NQ>::kMinWaves)
 attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
                   const uint16_t* __restrict__ vc, const uint8_t* __restrict__ mask,
@@ -220,8 +225,8 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
     for (int u = 0; u < GG::kLoads; ++u) {
       const int row = kb0 + u * GG::kRowsPerLoad + lane_row;
       const uint32_t off = row < row_lim ? (uint32_t)row * (D * 2) + lane_col : kOutOfRange;
-      st.k[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, 0));
-      st.v[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, 0));
+      st.k[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, NT ? kStreamLoad : 0));
+      st.v[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, NT ? kStreamLoad : 0));
     }
     st.mbyte = mload[min(kb0 + (lane & (kWaveKeys - 1)), L - 1)];
   };
@@ -531,15 +536,17 @@ typedef void (*SplitKernel)(const uint16_t*, const uint16_t*, const uint16_t*, c
                             int, int, int, int, float, int, int, int, int32_t*);
 
 template <int D>
-SplitKernel pick_split(int nq) {
-  switch (nq) {
-    case 1: return attn_split_kernel<D, 1>;
-    case 2: return attn_split_kernel<D, 2>;
-    default: return attn_split_kernel<D, 3>;
+SplitKernel pick_split(int nq, int q_chunks) {
+  switch (nq) {  // one or two query groups never need a second query chunk
+    case 1: return attn_split_kernel<D, 1, true>;
+    case 2: return attn_split_kernel<D, 2, true>;
+    default: return q_chunks == 1 ? attn_split_kernel<D, 3, true> : attn_split_kernel<D, 3, false>;
   }
 }
 
-SplitKernel pick_split(int D, int nq) { return D == 64 ? pick_split<64>(nq) : pick_split<128>(nq); }
+SplitKernel pick_split(int D, int nq, int q_chunks) {
+  return D == 64 ? pick_split<64>(nq, q_chunks) : pick_split<128>(nq, q_chunks);
+}
 
 }  // namespace
 
@@ -551,7 +558,7 @@ int attention_plan(int B, int gamma_max, int Hq, int Hkv, int D, int L_cap, Atte
   const int cus = device_cu_count();
   if (cus <= 0) return SR_ELAUNCH;
   int per_cu = 1;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void*)pick_split(D, plan->nq),
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void*)pick_split(D, plan->nq, plan->q_chunks),
                                                    kThreads, 0) != hipSuccess || per_cu < 1)
     per_cu = 1;
   const long pairs = (long)B * Hkv * plan->q_chunks;
@@ -592,7 +599,7 @@ int launch_verify_attention(const void* q, const void* k_cache, const void* v_ca
   float* part_o = workspace ? (float*)((char*)workspace + plan.part_offset) : nullptr;
   float* part_ml = part_o ? part_o + (size_t)B * Hkv * plan.n_splits * R * D : nullptr;
   dim3 grid((unsigned)((long)plan.n_splits * plan.q_chunks * B * Hkv));
-  hipLaunchKernelGGL(pick_split(D, plan.nq), grid, dim3(kThreads), 0, stream,
+  hipLaunchKernelGGL(pick_split(D, plan.nq, plan.q_chunks), grid, dim3(kThreads), 0, stream,
                      (const uint16_t*)q, (const uint16_t*)k_cache, (const uint16_t*)v_cache,
                      cache_mask, kv_len, gamma, out, part_o, part_ml, counters, B, gamma_max, Hq, Hkv,
                      L_cap, scale * kLog2e, plan.split_keys, plan.n_splits, plan.q_chunks, status);

@@ -163,3 +163,12 @@ def test_rollback_rejects_bad_host_arguments(lib):
     p = ctypes.c_void_p(4096)
     assert lib.specrouter_rollback(None, None, p, None, 4, 16, None, None) == _lib.SR_EINVAL
     assert lib.specrouter_rollback(p, None, p, None, 0, 16, None, None) == _lib.SR_EINVAL
+
+
+def test_probe_rejects_bad_arguments_without_a_device():
+    lib = _lib.load()
+    assert lib.specrouter_hbm_read_probe(None, 1024, None, None) == _lib.SR_EINVAL
+    fake = ctypes.c_void_p(1 << 20)  # never dereferenced: the checks come first
+    assert lib.specrouter_hbm_read_probe(fake, 0, None, None) == _lib.SR_EINVAL
+    assert lib.specrouter_hbm_read_probe(fake, 1000, None, None) == _lib.SR_EINVAL
+    assert lib.specrouter_hbm_read_probe(ctypes.c_void_p((1 << 20) + 4), 1024, None, None) == _lib.SR_EINVAL
