@@ -115,7 +115,7 @@ def measured_traffic(entry, workload):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py: this build runs on exactly one GPU (the verify step shards by sequence with "
+        print("bench.py: this implementation runs on exactly one GPU (the verify step shards by sequence with "
               "no cross-GPU exchange). Use --gpus 1.", file=sys.stderr)
         sys.exit(2)
 

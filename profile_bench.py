@@ -1,7 +1,7 @@
 #!/usr/bin/env python3
 """rocprofv3 passes over bench.py and the summaries kept under profiles/.
 
-  python profile_bench.py [--config 2] [--raw gpurun_out/prof]
+  python profile_bench.py [--config 2] [--raw DIR]   (raw profiler output; default prof_raw/)
 
 Three profiler runs of `bench.py --no-cpu` for one workload, each a child
 process under its own time limit:
@@ -85,7 +85,7 @@ def main():
     ap.add_argument("--config", type=int, default=2)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--pmc-steps", type=int, default=10)
-    ap.add_argument("--raw", default=os.path.join(HERE, "gpurun_out", "prof"))
+    ap.add_argument("--raw", default=os.path.join(HERE, "prof_raw"))
     ap.add_argument("--parse-only", action="store_true", help="summarise an earlier run's raw output")
     args = ap.parse_args()
     os.environ["TMPDIR"] = "/tmp"
