@@ -311,7 +311,7 @@ struct TaskInfo {
   int x;  // the row's draft token (pair rows; -1 for a bonus row)
   bool pair;
   const char* prow;
-  const char* qrow;  // the p row itself for a bonus row (its loads then hit cached lines)
+  const char* qrow;  // the draft row (a pair row), or the p row for a bonus row (never read)
 };
 
 template <bool BF16>
@@ -356,15 +356,19 @@ __device__ __forceinline__ void issue_loads(const Args& A, const TaskInfo& t, Ra
       for (int i = 0; i < 4; ++i) r.p[v * 4 + i] = f[i];
     }
   }
+  // The draft row through a buffer resource: a bonus row has none, so its
+  // resource is empty and the same loads return zeros with no memory traffic.
+  constexpr uint32_t kEsz = BF16 ? 2u : 4u;
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(t.qrow, t.pair ? (size_t)A.V * kEsz : 0);
 #pragma unroll
   for (int v = 0; v < NV; ++v) {
     const int x = min(base + (v * 64 + lane) * VEC, A.V - VEC);
+    const u32x4 u = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rq, (uint32_t)x * kEsz, 0, 0));
     if constexpr (BF16) {
-      r.qk[v] = *(const u32x4*)((const uint16_t*)t.qrow + x);
+      r.qk[v] = u;
     } else {
-      const floatx4 f = *(const floatx4*)((const float*)t.qrow + x);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) r.q[v * 4 + i] = f[i];
+      for (int i = 0; i < 4; ++i) r.q[v * 4 + i] = __uint_as_float(u[i]);
     }
   }
 }
