@@ -40,7 +40,7 @@ def _cache_state(inp, cap, rng, holes=0.2):
     return kv, mask
 
 
-def _both(inp, cache_kv, mask, cap, temperature, calls=1):
+def _both(inp, cache_kv, mask, cap, temperature, calls=1, top_k=0, top_p=1.0):
     """Runs the separate pair and the fused call `calls` times on the same
     inputs (fresh cache state each time, shared workspaces) and returns the
     results of the last call of each."""
@@ -60,11 +60,12 @@ def _both(inp, cache_kv, mask, cap, temperature, calls=1):
             args = (p, q, d, g, ua, ur, kv_in, a.accept_len, a.out_tokens, a.new_len, a.accept_prob, a.p_tok,
                     a.q_tok, a.kl, a.tv)
             if k == "sep":
-                sr.specrouter_accept_and_diverge_sampled(*args, a.workspace, a.status, temperature=temperature)
+                sr.specrouter_accept_and_diverge_sampled(*args, a.workspace, a.status, temperature=temperature,
+                                                         top_k=top_k, top_p=top_p)
                 sr.specrouter_rollback(kvc, mk, a.new_len, phys, a.status)
             else:
                 sr.specrouter_accept_and_rollback(*args, kvc, mk, phys, a.workspace, a.status,
-                                                  temperature=temperature)
+                                                  temperature=temperature, top_k=top_k, top_p=top_p)
             torch.cuda.synchronize()
             r = {n: host(getattr(a, n)) for n in OUTS}
             r.update(kv=host(kvc), mask=host(mk), phys=int(host(phys)[0]), status=int(host(a.status)[0]))
@@ -96,6 +97,20 @@ def test_fused_equals_accept_then_rollback(temperature, logits):
     np.testing.assert_array_equal(fused["kv"], ref_kv)
     np.testing.assert_array_equal(fused["mask"], ref_mask)
     assert fused["phys"] == ref_phys and ref_st == 0
+
+
+@pytest.mark.parametrize("top_k,top_p", [(20, 1.0), (0, 0.85), (50, 0.9)])
+def test_fused_with_top_k_top_p(top_k, top_p):
+    """The filtered sampling rule through the fused call: the same bits as the
+    filtered accept call followed by the rollback."""
+    rng = np.random.default_rng(14)
+    inp = level_inputs(small_shape(name="ar-filt", B=10, V=12288, gamma=(0, 6), seed=64), kv=False)
+    cap = int(inp.kv_len.max()) + 8
+    cache_kv, mask = _cache_state(inp, cap, rng)
+    say(f"accept+rollback top_k={top_k} top_p={top_p}")
+    sep, fused = _both(inp, cache_kv, mask, cap, 0.8, calls=2, top_k=top_k, top_p=top_p)
+    assert sep["status"] == 0
+    _same(sep, fused)
 
 
 def test_fused_data_errors_match():
