@@ -6,11 +6,18 @@ verification attention, then accept-and-diverge with the rollback applied by
 its finishing kernel (two C-ABI calls on one stream:
 specrouter_verify_attention, specrouter_accept_and_rollback). The standalone
 rollback call is timed on its own as well. `value` comes from K steps timed
-with events at the two ends only; the per-entry-point durations (and the
-roofline) from a second run of K steps with an event around each call. Inputs are seeded synthetic data of the named workload and are
-resident in HBM before timing starts. To keep the 256 MB last-level cache
-from serving repeated steps, R copies of the inputs live at different HBM
-addresses and step s uses copy s mod R.
+with events at the two ends only; each entry point's average duration (and
+the roofline) from K back-to-back calls of that entry point alone, again with
+events at the two ends only. Inputs are seeded synthetic data of the named
+workload and are resident in HBM before timing starts. To keep the 256 MB
+last-level cache from serving repeated steps, R copies of the inputs live at
+different HBM addresses and step s uses copy s mod R. Every step rolls back a
+fresh copy of the cache lengths and validity mask (staged before the timed
+region), so the fused rollback clears the rejected rows on every step.
+
+Default workload: the ragged 256-sequence batch (B = 256, bf16 logits), the
+largest single-GPU configuration; --config 2 is the Llama-3-8B-shaped
+16-sequence batch, --config 3 the three-level chain.
 
 Prints ONE JSON line (rank 0) with the throughput in verified draft tokens/s,
 the roofline of the dominant kernel (HIP events over the timed region), and
@@ -42,7 +49,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--config", type=int, default=5)
     ap.add_argument("--rotate", type=int, default=0, help="input copies (0 = enough to exceed 1 GB)")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-seqs", type=int, default=0, help="sequences in the CPU-baseline sample")
@@ -160,7 +167,6 @@ def main():
                     + ((gam + 1) * Hq * D * 4).sum()           # live output rows (fp32)
                     + kv_len.sum())                            # cache-mask bytes
     acc_bytes = int(((2 * gam + 1) * V * esz).sum())           # live verifier and draft logit rows
-    rb_bytes = int(B * 12 + kv_len.sum())                      # lengths + mask rows (upper bound)
     set_bytes = inp.k.nbytes + inp.v.nbytes + inp.p_logits.nbytes + inp.q_logits.nbytes
     R = args.rotate or max(2, int(np.ceil(1.2e9 / set_bytes)))
 
@@ -170,8 +176,8 @@ def main():
         base_mask[b, : inp.kv_len[b]] = 1
     for r in range(R):
         s = dict(
-            q=up(inp.q), k=up(inp.k), v=up(inp.v), kv_in=up(inp.kv_len), kv_work=up(inp.kv_len),
-            gamma=up(inp.gamma), mask_in=up(base_mask), mask_work=up(base_mask),
+            q=up(inp.q), k=up(inp.k), v=up(inp.v), kv_in=up(inp.kv_len),
+            gamma=up(inp.gamma), mask_in=up(base_mask),
             p=up(inp.p_logits), ql=up(inp.q_logits), drafts=up(inp.drafts),
             u_acc=up(inp.u_acc), u_res=up(inp.u_res),
             out=torch.empty((B, G1, Hq, D), dtype=torch.float32, device=dev),
@@ -191,53 +197,62 @@ def main():
 
     ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
 
-    def step(s, evs=None):
-        if evs:
-            evs[0].record()
+    K = args.steps
+    # One fresh (cache lengths, validity mask) pair per rolled-back call, so
+    # every timed call's rollback clears the rejected rows; refilled from the
+    # pristine state outside the timed regions.
+    n_work = max(K, args.warmup, 1)
+    work = [(torch.empty(B, dtype=torch.int32, device=dev), torch.empty((B, cap), dtype=torch.uint8, device=dev))
+            for _ in range(n_work)]
+
+    def refill():
+        for kw, mw in work:
+            kw.copy_(sets[0]["kv_in"])
+            mw.copy_(sets[0]["mask_in"])
+        torch.cuda.synchronize()
+
+    def attention(s):
         sr.specrouter_verify_attention(s["q"], s["k"], s["v"], s["mask_in"], s["kv_in"], s["gamma"],
                                        s["out"], inp.scale, s["ws"], s["st"])
-        if evs:
-            evs[1].record()
+
+    def accept(s, w):
         a = s["acc"]
         sr.specrouter_accept_and_rollback(s["p"], s["ql"], s["drafts"], s["gamma"], s["u_acc"], s["u_res"],
                                           s["kv_in"], a.accept_len, a.out_tokens, a.new_len, a.accept_prob,
-                                          a.p_tok, a.q_tok, a.kl, a.tv, s["kv_work"], s["mask_work"], s["phys"],
-                                          a.workspace, s["st"])
-        if evs:
-            evs[2].record()
+                                          a.p_tok, a.q_tok, a.kl, a.tv, w[0], w[1], s["phys"], a.workspace, s["st"])
 
+    def step(s, w):
+        attention(s)
+        accept(s, w)
+
+    refill()
     for i in range(args.warmup):
-        step(sets[i % R])
-    torch.cuda.synchronize()
+        step(sets[i % R], work[i % n_work])
+    refill()
 
-    K = args.steps
-    # Timed region 1 (the metric): K steps with events only at its two ends.
-    start, stop = ev(), ev()
-    torch.cuda.synchronize()
-    start.record()
+    def timed(fn):
+        """ms for K calls of fn(i), events at the two ends only."""
+        e0, e1 = ev(), ev()
+        torch.cuda.synchronize()
+        e0.record()
+        for i in range(K):
+            fn(i)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1)
+
+    # Timed region 1 (the metric): K whole steps.
     t_wall = time.perf_counter()
-    for i in range(K):
-        step(sets[i % R])
-    stop.record()
-    torch.cuda.synchronize()
+    total_ms = timed(lambda i: step(sets[i % R], work[i]))
     wall = time.perf_counter() - t_wall
-    total_ms = start.elapsed_time(stop)
-    # Timed region 2 (each entry point's launch duration, for the roofline):
-    # the same K steps with an event before and after each call. An event is
-    # a barrier packet on the stream (the next launch waits for it), so these
-    # durations include the launch and are upper bounds; the step is slower
-    # in this region than in region 1.
-    evs = [[ev() for _ in range(3)] for _ in range(K)]
-    e_start, e_stop = ev(), ev()
-    torch.cuda.synchronize()
-    e_start.record()
-    for i in range(K):
-        step(sets[i % R], evs[i])
-    e_stop.record()
-    torch.cuda.synchronize()
-    ms_per_step_events = e_start.elapsed_time(e_stop) / K
-    att_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    acc_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    # Each entry point's average duration (the roofline): K back-to-back calls
+    # of it alone on the same rotated inputs.
+    att_ms = timed(lambda i: attention(sets[i % R])) / K
+    refill()
+    acc_ms = timed(lambda i: accept(sets[i % R], work[i])) / K
+    # the mask bytes the rollback clears: the rejected rows of every sequence
+    acc_k = sets[0]["acc"].accept_len.cpu().numpy().astype(np.int64)
+    rb_bytes = int(B * 12 + (gam - np.maximum(acc_k, 0)).sum())
 
     status = int(sum(int(s["st"].item()) for s in sets))
     acc0 = sets[0]["acc"]
@@ -384,8 +399,10 @@ def main():
     status |= int(sum(int(s["st"].item()) for s in sets))
 
     cpu = None
+    boundary = None
     if not args.no_cpu:
         cpu = cpu_baseline(inp, args.cpu_seqs)
+        boundary = boundary_check(inp, acc0)
     sched = scheduler_timing(sr, sets[0]["gamma"], acc0.accept_len, acc0.tv)
     probe = hbm_probe(sr, dev, ev)
 
@@ -397,7 +414,6 @@ def main():
         "steps": K,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 5),
-        "ms_per_step_with_kernel_events": round(ms_per_step_events, 5),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -428,6 +444,7 @@ def main():
         "sampling_variants": variants,
         "mean_accept_len": round(mean_accept, 3),
         "status_bits": status,
+        "boundary": boundary,
         "cpu_baseline": cpu,
         "scheduler": sched,
         "host_wall_s": round(wall, 4),
@@ -579,11 +596,54 @@ def chain_bench(args, sr, shape):
         "mean_k_int": round(float(ab_i.accept_len.float().mean().item()), 3),
         "mean_k_tgt": round(float(ab_t.accept_len.float().mean().item()), 3),
         "status_bits": status,
-        "cpu_baseline": None,
-        "note": "three-level chain step; the oracle's CPU timing is reported for the single-level workloads",
+        "cpu_baseline": None if args.no_cpu else chain_cpu_baseline(ci, shape),
+        "note": "three-level chain step (intermediate and target levels); the draft level's decode attention apart",
         "input_gen_s": round(gen_s, 2),
     }
     print(json.dumps(line), flush=True)
+
+
+def chain_cpu_baseline(ci, shape, target_s=10.0):
+    """The CPU reference on whole chain steps of a prefix of the batch, one
+    sequence at a time until about target_s has elapsed: the intermediate
+    level's attention and accept, the target's window, attention and accept
+    (its draft rows the intermediate level's verifier rows), and both
+    rollbacks; counts the drafts of both levels."""
+    import oracle
+
+    inter, t = ci["inter"], ci["target"]
+    z2 = ci["z"][1]
+    B, ctx, gt = shape.B, shape.ctx, shape.gamma_tgt
+    dt, done, drafts = 0.0, 0, 0
+    for b in range(B):
+        t0 = time.perf_counter()
+        oracle.verify_attention(inter.q, inter.k, inter.v, inter.kv_len, inter.gamma, inter.scale, seqs=[b])
+        r2 = oracle.accept_and_diverge(inter.p_logits, inter.q_logits, inter.drafts, inter.gamma, inter.u_acc,
+                                       inter.u_res, kv_len=inter.kv_len, seqs=[b])
+        g3 = oracle.chain.target_window(r2["accept_len"], gt)
+        d3 = oracle.chain.target_drafts(r2["out_tokens"], g3, gt)
+        kv3 = (ctx + g3 + 1).astype(np.int32)
+        oracle.verify_attention(t["q"], t["k"], t["v"], kv3, g3, t["scale"], seqs=[b])
+        r3 = oracle.accept_and_diverge(t["p_logits"], z2[:, :gt], d3, g3, t["u_acc"], t["u_res"], kv_len=kv3,
+                                       seqs=[b])
+        up_len, lo_len, _ = oracle.chain.rollback_targets(ctx, r2["accept_len"][[b]], r3["accept_len"][[b]])
+        oracle.rollback(kv3[[b]], None, up_len)
+        oracle.rollback(inter.kv_len[[b]], None, lo_len)
+        dt += time.perf_counter() - t0
+        done += 1
+        drafts += int(inter.gamma[b]) + int(g3[b])
+        if dt >= target_s:
+            break
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        cores = os.cpu_count()
+    threads = os.environ.get("OPENBLAS_NUM_THREADS") or os.environ.get("OMP_NUM_THREADS") or str(cores)
+    return {
+        "value": round(drafts / dt, 2), "unit": "tokens/s", "cores": int(min(cores, int(threads))), "kind": "oracle",
+        "sample": f"{done} of {B} sequences, whole two-level chain steps one sequence at a time (fp64 numpy), "
+                  f"{dt:.1f} s",
+    }
 
 
 def scheduler_timing(sr, gamma, accept_len, tv, reps=2000):
@@ -613,6 +673,29 @@ def scheduler_timing(sr, gamma, accept_len, tv, reps=2000):
     s.close()
     return {"observe_step_us": round(obs_us, 2), "optimal_chain_us": round(sel_us, 2), "models": len(cap),
             "candidates": n_cand, "chain": chain, "note": "host C++ via the ctypes binding, per call"}
+
+
+def boundary_check(inp, acc):
+    """The accept outputs of the timed calls against the CPU reference on every
+    sequence of the batch: decisions must agree exactly except on boundary
+    cases (a uniform within 1e-6 of a CDF breakpoint or acceptance threshold),
+    which are counted, with the mismatches among them."""
+    import oracle
+
+    ref = oracle.accept_and_diverge(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, inp.u_acc, inp.u_res,
+                                    kv_len=inp.kv_len)
+    k = acc.accept_len.cpu().numpy()
+    toks = acc.out_tokens.cpu().numpy()
+    same = (k == ref["accept_len"]) & (toks == ref["out_tokens"]).all(axis=1)
+    bd = ref["boundary"].astype(bool)
+    return {
+        "sequences": int(k.shape[0]),
+        "boundary_cases": int(bd.sum()),
+        "boundary_mismatches": int((bd & ~same).sum()),
+        "mismatches_outside_boundary": int((~bd & ~same).sum()),
+        "min_margin": float(np.min(ref["margin"])),
+        "note": "GPU accept lengths and tokens vs the CPU reference on every sequence (margin < 1e-6 = boundary)",
+    }
 
 
 def cpu_baseline(inp, n_seqs, target_s=10.0, cap_s=30.0):

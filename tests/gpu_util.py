@@ -10,6 +10,11 @@ import paper_2505_07680_amd as sr
 
 # Parity tolerances.
 ATT_ATOL, ATT_RTOL = 2e-2, 1e-2      # bf16 in, fp32 accumulate
+# Relative L2 error of every (sequence, row, head) output vector. With
+# Q, K, V ~ N(0, 1) the outputs are small (RMS ~0.04 at 2K keys, ~0.01 at 32K),
+# so the elementwise bound above is loose there; this one is not (bf16
+# probabilities in the PV products give ~1e-3).
+ATT_REL_L2 = 1e-2
 PROB_RTOL = 1e-5                     # accept_prob, p_tok, q_tok
 DIV_RTOL, DIV_ATOL = 1e-4, 1e-7      # KL and TV (absolute floor for near-zero values)
 # KL's absolute floor: each row's log-normaliser carries the fp32 rounding of
@@ -88,9 +93,11 @@ def run_rollback(kv_len, mask, new_len, cap):
     return host(kv), (None if md is None else host(md)), int(host(phys)[0]), int(host(st)[0])
 
 
-def check_attention(got, want, seqs=None, atol=ATT_ATOL, rtol=ATT_RTOL):
-    """Elementwise |got - want| <= atol + rtol |want|; returns the worst relative L2 error
-    over (sequence, row, head) vectors with a non-negligible reference."""
+def check_attention(got, want, seqs=None, atol=ATT_ATOL, rtol=ATT_RTOL, rel_l2=ATT_REL_L2):
+    """Elementwise |got - want| <= atol + rtol |want|, and the relative L2 error
+    ||got - want|| / ||want|| of every (sequence, row, head) vector with a
+    non-zero reference at most rel_l2 (a vector whose reference is zero must
+    be zero). Returns the worst relative L2 error."""
     if seqs is not None:
         got, want = got[list(seqs)], want[list(seqs)]
     assert np.isfinite(got).all(), "non-finite attention output"
@@ -99,8 +106,11 @@ def check_attention(got, want, seqs=None, atol=ATT_ATOL, rtol=ATT_RTOL):
     assert not bad.any(), f"{bad.sum()} attention elements outside tolerance; max err {err.max():.3e}"
     num = np.linalg.norm(got - want, axis=-1)
     den = np.linalg.norm(want, axis=-1)
-    live = den > 1e-6
-    return float((num[live] / den[live]).max()) if live.any() else 0.0
+    live = den > 0
+    assert (num[~live] == 0).all(), "output rows whose reference is zero are not zero"
+    worst = float((num[live] / den[live]).max()) if live.any() else 0.0
+    assert worst <= rel_l2, f"attention relative L2 error {worst:.3e} > {rel_l2:.0e}"
+    return worst
 
 
 def _close(got, want, rtol, atol=0.0):
