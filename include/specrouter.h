@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define SPECROUTER_ABI_VERSION 3
+#define SPECROUTER_ABI_VERSION 4
 #define SPECROUTER_MAX_GAMMA 16
 #define SPECROUTER_MAX_CACHE_ROWS (1 << 22)
 
@@ -77,7 +77,7 @@ enum {
   SR_ST_TOKEN = 4,          /* a draft token outside [0, V) */
   SR_ST_UNIFORM = 8,        /* a needed uniform outside [0, 1) (NaN included) */
   SR_ST_ROLLBACK_GROW = 16, /* rollback asked to grow a sequence (treated as a no-op) */
-  SR_ST_TIMEOUT = 32,       /* an inter-workgroup wait gave up (results of that call are invalid) */
+  SR_ST_TIMEOUT = 32,       /* not set since ABI version 4 (accept waits are bounded and recover) */
   SR_ST_CHAIN = 64,         /* accept lengths that one chain step cannot produce */
 };
 
@@ -157,10 +157,17 @@ int specrouter_verify_attention(const void* q, const void* k_cache, const void* 
  *               j >= gamma_b (and all entries of a bad sequence) are NaN
  * workspace     device scratch of specrouter_accept_workspace_size() bytes; it
  *               must be zero-filled before its FIRST use and every call leaves
- *               it zero-filled again (each call clears the records it wrote)
- * Logits must be finite or -inf; a row that is entirely -inf is not supported.
- * Requires (V * element size) % 16 == 0 and 16-byte aligned logits pointers and
- * strides, else SR_EUNSUPPORTED.
+ *               it zero-filled again, whatever shape the next call has (each
+ *               call clears every word it wrote)
+ * Logits must be finite or -inf, with |logit| / T < 2^23; a row that is
+ * entirely -inf is not supported. Any V from 1 to 524281: rows need no
+ * alignment, but the logits pointers and the batch strides (in bytes) must be
+ * multiples of 16, else SR_EUNSUPPORTED (with V * element size not a multiple
+ * of 16, allocate each sequence's rows with a padded batch stride).
+ * The kernels need no co-residency of their workgroups: no workgroup waits
+ * without bound (a bounded wait for the other chunks of a row falls back to
+ * recomputing that chunk's sum later), so other work on the device slows the
+ * call down but never stalls it; repeated calls give identical bits.
  */
 size_t specrouter_accept_workspace_size(int B, int gamma_max, int V, int logits_dtype);
 int specrouter_accept_and_diverge(const void* p_logits, int64_t p_batch_stride,

@@ -1,142 +1,142 @@
 // Accept-and-diverge for gfx950: speculative accept/reject with residual
 // resampling and the bonus token (Section 2.2 steps 3-4, probabilistic
 // acceptance; Eq. 2), plus per-position total variation distance (Eq. 5) and
-// KL divergence, in one pass over the verifier and draft logits.
+// KL divergence, in one launch and one pass over the verifier and draft
+// logits.
 //
-// Rows and chunks. A live row is one (sequence b, position j <= gamma_b): for
-// j < gamma_b the verifier row p_j together with the draft row q_j (a "pair
-// row"), for j = gamma_b the verifier row alone (it feeds the bonus token).
-// Each row is cut into chunks of 256*E vocabulary entries; a workgroup task is
-// one (row, chunk), each lane holding E entries of p and q in registers.
+// Rows, chunks, tasks. A live row is one (sequence b, position j <= gamma_b):
+// for j < gamma_b the verifier row p_j together with the draft row q_j (a
+// "pair row"), for j = gamma_b the verifier row alone (the bonus row). A row
+// is cut into chunks of 4096 vocabulary entries; a task is one (row, chunk),
+// each of the workgroup's four waves holding 1024 entries of it, 16 entries
+// of p (and q) per lane. Workgroup w takes tasks w, w + G, w + 2G, ... over
+// the live rows only (a row table built from gamma in LDS).
 //
-// Sweep kernel (persistent; the single pass over HBM). The grid is sized to be
-// resident at once. Workgroup w takes tasks w, w + G, w + 2G, ... over the live
-// rows only (a row table built from gamma in LDS), with G a multiple of the
-// chunks per row, so the chunks of one row are processed at the same time by
-// neighbouring workgroups. Per task:
-//   1. chunk maxima of p and q, then the sums of exp(z - max) and the KL
-//      numerator sum exp(p - max_p) ((p - max_p) - (q - max_q)), merged over
-//      the four waves in a fixed order and published as one record with
-//      device-coherent stores;
-//   2. pair rows only: one wave re-loads the row's records until all of them
-//      are present, merges them into the two log-normalisers (fp64, fixed
-//      order; the finish kernel merges identically, so both get bit-identical
-//      values), and every lane finishes sum |P - Q| over the entries still in
-//      its registers. The chunk's sum is stored for the finish kernel.
-// A record is four 8-byte words stored bit-inverted: a word that reads as all
-// zeros has not been written yet (the inverted pattern would be a NaN, which
-// no record holds), and naturally aligned 8-byte accesses are single-copy
-// atomic, so a waiting wave needs no counter, no atomics and no wait for its
-// own stores to complete. The finish kernel zeroes the records after use.
-// Only sum |P - Q| is needed: with d = P - Q, a chunk's residual mass
-// sum max(0, d) is (sum |d| + sum d) / 2 and sum d is the difference of the
-// chunk's P and Q masses, which the records already hold.
+// Row alignment. Loads are 16-byte vectors at 16-byte-aligned addresses. Row j
+// starts j*V entries after its sequence's (16-byte-aligned) first row, so it
+// sits phi_j = (j*V) mod (entries per 16 bytes) entries past an aligned
+// address, the same for p_j and q_j; a row is read from that aligned address
+// on, and the entries before its start and past its end are masked out (they
+// act as -inf logits). Any V is handled this way.
 //
-// Finish kernel (one workgroup per sequence, one wave per row): merges the
-// records into TV, KL, p(x), q(x) and a_j, runs the accept chain, and draws the
-// token: a prefix scan over the stopping row's chunk masses finds the chunk
-// that holds u*W, and that chunk alone is re-read and scanned in ascending
-// vocabulary order with its element weights computed exactly as in the sweep.
-// It also zeroes the sequence's records for the next call.
+// Sweep launch (one HBM read of every live logit). Workgroup g takes tasks
+// g, g + G, g + 2G, ... (G the persistent grid size, what fits on the device
+// at once) from an LDS table decoded a window at a time; task k+1's loads are
+// issued before task k's first pass, and pair task k's TV sum is formed during
+// step k+1:
+//  1. first pass: the chunk's maxima m, integer exponent shifts
+//     r = ceil(m log2(e)/T), the exponentials 2^x with x = z log2(e)/T - r
+//     (kept in registers until the TV sum; the largest lies in (1/2, 1]),
+//     their sums and the KL numerator sum e_p (x_p - x_q); one 32-byte record
+//     per chunk, published with device-coherent stores, bit-inverted so that
+//     an all-zero word means "not yet written" (naturally aligned 8-byte
+//     accesses are single-copy atomic);
+//  2. one step later, one wave (rotating over the four) has loaded the row's
+//     records (issued before the step's prefetch, so that they return during
+//     its first pass) and re-loads them until all are present (for at most
+//     about 200 us, then the task gives up, see below); it merges them into
+//     the row's normalisers in a fixed order (fp64) and the chunk's factors
+//     f_p = 2^(r_c - r_max)/S_p, f_q likewise (the shifts are integers, so
+//     2^(r_c - r_max) is exact); the lanes then sum |P - Q| over their
+//     entries, scaled so that one of the two factors is 1 (fma(a, rho, -b)
+//     with rho = min/max of the factors), and each wave publishes its part.
+// Waiting is bounded: a task whose row is not complete after the time limit
+// publishes a "skipped" mark instead of its sum, and the row's finaliser
+// recomputes that chunk's sum from memory with the same arithmetic. No
+// workgroup ever waits without bound, so the launch needs no co-residency of
+// its workgroups, and results do not depend on which workgroup computed what
+// (every merge is in a fixed order, every recomputation bit-identical).
+//
+// Finish launch (one workgroup per sequence): its waves finalise the rows,
+// TV_j = 1/2 sum |P - Q|, KL_j, p(x_j), q(x_j) and a_j from the records, the
+// sums and the draft token's logits, into LDS; wave 0 then runs the accept
+// chain, the draw (chunk masses of the stopping row rebuilt from its records,
+// the chunk holding u*W re-read and scanned in ascending vocabulary order with
+// its weights computed exactly as in the sweep), the outputs, the rollback,
+// and zeroes every workspace word the sequence's rows used, so the workspace
+// is all zero again when the call ends. The physical length is written by the
+// launch's last finished sequence.
+//
+// Greedy decoding (T = 0) runs the same launches with chunk argmaxes in place
+// of the first pass and no TV step or waiting.
 //
 // Precision: exponentials in fp32 (relative error ~1e-7; weights below 2^-126
-// of their chunk's largest flush to zero), every sum in fp64
-// beyond a lane's own entries; TV and KL carry ~1e-7 relative error, and a
-// draw can differ from exact arithmetic only when u*W lies within ~1e-7 W of
-// a CDF breakpoint.
+// of their chunk's largest flush to zero), every sum in fp64 beyond a
+// lane's 16 entries; the log-normalisers are r_max ln 2 + ln S in fp64 and
+// log-probabilities are formed from the exponent arguments actually used, so
+// rows with the same filtered distribution give KL = 0 and p(x) = q(x) to
+// fp64 rounding. A draw can differ from exact arithmetic only when u*W lies
+// within ~1e-7 W of a CDF breakpoint. Logits must satisfy |z|/T < 2^23 (the
+// shifts are exact fp32 integers).
 
 #include <limits.h>
 #include <math.h>
 
 #include "sr_internal.h"
 
+// v_mul_legacy_f32: 0 * x = 0 for every x (infinities and NaN included).
+extern "C" __device__ float sr_fmul_legacy(float, float) __asm("llvm.amdgcn.fmul.legacy");
+
 namespace sr {
 namespace {
 
-constexpr int kThreads = 256;  // sweep workgroup: four waves, one chunk per task
+constexpr int kThreads = 256;  // four waves, one task
 constexpr int kWaves = kThreads / 64;
-
-// Fixed-order merges of the per-wave partials.
-__device__ __forceinline__ float max_waves(const float* v) {
-  float m = v[0];
-#pragma unroll
-  for (int i = 1; i < kWaves; ++i) m = fmaxf(m, v[i]);
-  return m;
-}
-__device__ __forceinline__ double sum_waves(const double* v) {
-  double a = v[0];
-#pragma unroll
-  for (int i = 1; i < kWaves; ++i) a += v[i];
-  return a;
-}
-constexpr int kSlots = 2;                // chunk records per lane in the row merges
-constexpr int kMaxChunks = 64 * kSlots;  // chunks per row
+constexpr int kSlots = 2;               // chunk records per lane in a row merge
+constexpr int kMaxChunks = 64 * kSlots; // per row
 constexpr int kMaxRows = SPECROUTER_MAX_GAMMA + 1;
-constexpr int kMaxSeqs = 4096;           // sequences per sweep launch (row table in LDS)
-constexpr uint32_t kSpinLimit = 1u << 22;
-constexpr int kDeviceCoherent = 16;      // buffer cache-policy operand: sc1
+constexpr int kMaxSeqs = 4096;               // sequences per launch (row table in LDS)
+constexpr int kDeviceCoherent = 16;          // buffer cache-policy operand: sc1
+constexpr uint64_t kWaitTicks = 20000;       // 200 us of the 100 MHz real-time counter
+constexpr double kLn2 = 0.6931471805599453;
+constexpr double kSkipped = -1.0;            // a chunk sum left to the finaliser
 
-// Per-(row, chunk) record of the first pass, as values.
+// ---------------------------------------------------------------------------
+// Records
+
+// Per-(row, chunk) record of the first pass.
+//   sampling: rp, rq  integer exponent shifts (-inf: the chunk holds no live entry)
+//             sp, sq  sums of 2^(z lg - r), kl  sum e_p (x_p - x_q)
+//   greedy:   rp, rq  maxima of p and q; sp, sq  the lowest index holding them
+//             (INT_MAX: none), kl = 0
 struct StatRec {
-  float mp, mq;  // chunk maxima of the p and q logits (-inf: none)
-  double sp;     // sum exp(p - mp)
-  double sq;     // sum exp(q - mq)
-  double kl;     // sum exp(p - mp) ((p - mp) - (q - mq))
+  float rp, rq;
+  double sp, sq, kl;
 };
-// In memory: four 8-byte words {mp | mq << 32, sp, sq, kl}, each inverted.
 constexpr int kRecBytes = 32;
 
 __device__ __forceinline__ void pack_rec(const StatRec& r, u32x4& w0, u32x4& w1) {
-  const uint64_t a = ~((uint64_t)__float_as_uint(r.mp) | ((uint64_t)__float_as_uint(r.mq) << 32));
+  const uint64_t a = ~((uint64_t)__float_as_uint(r.rp) | ((uint64_t)__float_as_uint(r.rq) << 32));
   const uint64_t b = ~__builtin_bit_cast(uint64_t, r.sp);
   const uint64_t c = ~__builtin_bit_cast(uint64_t, r.sq);
   const uint64_t d = ~__builtin_bit_cast(uint64_t, r.kl);
   w0 = u32x4{(uint32_t)a, (uint32_t)(a >> 32), (uint32_t)b, (uint32_t)(b >> 32)};
   w1 = u32x4{(uint32_t)c, (uint32_t)(c >> 32), (uint32_t)d, (uint32_t)(d >> 32)};
 }
-// True when all four words have been written.
 __device__ __forceinline__ bool rec_present(const u32x4& w0, const u32x4& w1) {
   return (w0[0] | w0[1]) != 0u && (w0[2] | w0[3]) != 0u && (w1[0] | w1[1]) != 0u && (w1[2] | w1[3]) != 0u;
 }
 __device__ __forceinline__ StatRec unpack_rec(const u32x4& w0, const u32x4& w1) {
   StatRec r;
-  r.mp = __uint_as_float(~w0[0]);
-  r.mq = __uint_as_float(~w0[1]);
+  r.rp = __uint_as_float(~w0[0]);
+  r.rq = __uint_as_float(~w0[1]);
   r.sp = __builtin_bit_cast(double, ~((uint64_t)w0[2] | ((uint64_t)w0[3] << 32)));
   r.sq = __builtin_bit_cast(double, ~((uint64_t)w1[0] | ((uint64_t)w1[1] << 32)));
   r.kl = __builtin_bit_cast(double, ~((uint64_t)w1[2] | ((uint64_t)w1[3] << 32)));
   return r;
 }
 
-template <bool BF16>
-struct Elt;
-
-template <>
-struct Elt<false> {
-  static constexpr int VEC = 4;  // entries per 16-byte load
-  __device__ static void load(const void* row, int x, float* out) {
-    const floatx4 v = *(const floatx4*)((const float*)row + x);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) out[i] = v[i];
-  }
-  __device__ static float one(const void* row, int x) { return ((const float*)row)[x]; }
+// What a row's finaliser hands to its sequence's finisher.
+struct RowOut {
+  double a;                    // min(1, p(x)/q(x)); greedy: 1 or 0
+  float p_tok, q_tok, kl, tv;
+  int argp;                    // greedy: argmax of p
+  int pad;
 };
+static_assert(sizeof(RowOut) == 32, "RowOut is two 16-byte words");
 
-template <>
-struct Elt<true> {
-  static constexpr int VEC = 8;
-  __device__ static void load(const void* row, int x, float* out) {
-    const u32x4 u = *(const u32x4*)((const uint16_t*)row + x);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      out[2 * i] = bf16_lo(u[i]);
-      out[2 * i + 1] = bf16_hi(u[i]);
-    }
-  }
-  __device__ static float one(const void* row, int x) {
-    return __uint_as_float((uint32_t)((const uint16_t*)row)[x] << 16);
-  }
-};
+// ---------------------------------------------------------------------------
+// Arguments
 
 struct Args {
   const void* p;
@@ -156,77 +156,102 @@ struct Args {
   float* q_tok;
   float* kl;
   float* tv;
-  int B, gmax, V, nc;
-  float lg;       // log2(e) / T: softmax(z / T) entries are 2^((z - m) lg)
-  double inv_t;   // 1 / T
-  u32x4* stats;     // [B][gmax+1][nc] records, two 16-byte halves each
-  double* tvabs;    // [B][gmax+1][nc] sum |P - Q| per chunk (pair rows)
-  float* xlogit;    // [B][gmax+1][2] the draft token's p and q logits (pair rows)
-  float* thr;       // [B][gmax+1][2] top-k / top-p thresholds of the p and q rows, or NULL (no filtering)
+  int B, gmax, V, nc;       // sequences, gamma_max, vocabulary, chunks per row
+  float lg;                 // log2(e) / T: softmax(z / T) entries are 2^(z lg - r)
+  // workspace
+  u32x4* recs;       // [B][gmax+1][nc] records, two 16-byte words each
+  double* tva;       // [B][gmax+1][nc][4] each wave's sum |fma(a, rho, -b)| (pair rows), or kSkipped
+  float* xlogit;     // [B][gmax+1][4] the draft token's exponent arguments and shifts, p then q (pair rows)
+  float* thr;        // [B][gmax+1][2] top-k / top-p thresholds of the p and q rows, or NULL
+  uint32_t* fincnt;  // sequences of this launch finished
   int32_t* status;
-  // rollback applied by the finish kernel (rb_kv NULL: none)
-  int32_t* rb_kv;     // [B] cache lengths, in/out
-  uint8_t* rb_mask;   // [B][L_cap] validity mask, or NULL
-  int32_t* rb_phys;   // max over all sequences of the new lengths, or NULL
+  // rollback applied as each sequence finishes (rb_kv NULL: none)
+  int32_t* rb_kv;            // [B] cache lengths, in/out (this launch's sequences)
+  uint8_t* rb_mask;          // [B][L_cap] validity mask, or NULL
+  int32_t* rb_phys;          // max over all sequences of the new lengths, or NULL
+  const int32_t* rb_kv_all;  // the whole batch's cache lengths (rb_kv - n_before)
   int rb_lcap;
-  int rb_reset;       // this launch's sweep sets *rb_phys to INT_MIN first (the call's first launch)
+  int n_before;              // sequences of the call handled by earlier launches
 };
 
-// exp2_hw drops weights under 2^-126 of their chunk's largest. The sweep and
-// the finish kernel both use it, so a draw sees the same weights the chunk
-// sums were built from.
-
-// Pairwise sum of a lane's entries (a fixed tree, log2(N) roundings deep).
-template <int N>
-__device__ __forceinline__ float tree_sum(float (&v)[N]) {
-#pragma unroll
-  for (int s = N / 2; s > 0; s /= 2)
-#pragma unroll
-    for (int i = 0; i < s; ++i) v[i] += v[i + s];
-  return v[0];
-}
-
-// Normaliser of a row: its maximum M and S = sum over chunks of
-// s_c 2^((m_c - M) log2 e), so that softmax(z) = e^(z - M) / S. A chunk's
-// entries e^(z - m_c) (as the chunk sums hold them) turn into probabilities
-// by the factor f_c = 2^((m_c - M) log2 e) / S. The chunk records are held
-// lane-wise (chunk lane*nslot + i in slot i) and merged in a fixed order, so
-// the sweep and the finish kernel get bit-identical M, S and f_c.
-struct RowNorm {
-  float M;     // row maximum (-inf: none)
-  double S;    // sum of the chunks' rescaled sums (>= 1 when M is finite)
-  float invS;  // 1/S rounded to fp32
-  float lg;    // log2(e) / T
-  __device__ float factor(float m) const {  // f_c for a chunk whose maximum is m
-    return m == kNegInf ? 0.f : exp2_hw((m - M) * lg) * invS;
-  }
-  __device__ double log_norm(double inv_t) const { return (double)M * inv_t + log(S); }  // ln sum e^(z/T)
+// Task geometry: each lane holds 16 entries of p (and of q), 32 bytes of
+// bf16 or 64 of fp32; a task (chunk) is 4096 entries. (With 32 bf16 entries
+// per lane the exponentials kept for the deferred TV sum need more registers
+// than three workgroups per CU allow.)
+template <bool BF16>
+struct Vec {
+  static constexpr int N = BF16 ? 8 : 4;  // entries per 16-byte vector
+  static constexpr int esz = BF16 ? 2 : 4;
+  static constexpr int E = 16;                  // entries per lane per task
+  static constexpr int kWaveSpan = 64 * E;      // entries of one wave in a task
+  static constexpr int kChunk = kThreads * E;   // entries of a task
 };
 
-__device__ __forceinline__ RowNorm row_norm(const float (&m)[kSlots], const double (&s)[kSlots], float lg) {
-  RowNorm r;
-  r.lg = lg;
-  float ml = kNegInf;
+// A lane's E entries as loaded (E/N 16-byte vectors).
+template <bool BF16>
+struct Loaded {
+  u32x4 v[Vec<BF16>::E / Vec<BF16>::N];
+};
+
+template <bool BF16>
+__device__ __forceinline__ void widen(const Loaded<BF16>& L, float (&z)[Vec<BF16>::E]) {
+  constexpr int kE = Vec<BF16>::E;
+  if constexpr (BF16) {
 #pragma unroll
-  for (int i = 0; i < kSlots; ++i) ml = fmaxf(ml, m[i]);
-  r.M = wave_max(ml);
-  double acc = 0.0;
-  if (r.M != kNegInf) {
+    for (int i = 0; i < kE / 8; ++i)
 #pragma unroll
-    for (int i = 0; i < kSlots; ++i)
-      if (m[i] != kNegInf) acc += s[i] * (double)exp2_hw((m[i] - r.M) * lg);
+      for (int k = 0; k < 4; ++k) {
+        z[i * 8 + 2 * k] = bf16_lo(L.v[i][k]);
+        z[i * 8 + 2 * k + 1] = bf16_hi(L.v[i][k]);
+      }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kE / 4; ++i)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) z[i * 4 + k] = __uint_as_float(L.v[i][k]);
   }
-  r.S = wave_sum_d(acc);
-  r.invS = r.S > 0.0 ? (float)(1.0 / r.S) : 0.f;
-  return r;
 }
 
+// Aligned position (entries from the row's aligned start) of a lane's entry e
+// in the first-pass layout: vector e / N of the wave, lanes side by side.
+template <bool BF16>
+__device__ __forceinline__ int lane_pos(int wbase, int lane, int e) {
+  constexpr int N = Vec<BF16>::N;
+  return wbase + ((e / N) * 64 + lane) * N + e % N;
+}
+
+// Entries between row j's aligned start and its first entry.
+template <bool BF16>
+__device__ __forceinline__ int row_phase(const Args& A, int j) {
+  return (int)(((int64_t)j * A.V) % Vec<BF16>::N);
+}
+
+// One row of p (and q) as buffer resources over its aligned span.
+struct RowSpan {
+  __amdgpu_buffer_rsrc_t rp, rq;
+  int phi;
+};
+
+template <bool BF16>
+__device__ __forceinline__ RowSpan row_span(const Args& A, int b, int j, bool with_q) {
+  constexpr int N = Vec<BF16>::N, esz = Vec<BF16>::esz;
+  RowSpan s;
+  s.phi = row_phase<BF16>(A, j);
+  // bytes up to the 16-byte boundary after the row's last entry: the last
+  // vector is read whole (it never leaves the 16-byte block holding the row's
+  // last byte), vectors wholly past it read zero
+  const size_t span = (size_t)((s.phi + A.V + N - 1) / N) * 16;
+  const char* pr = (const char*)A.p + ((int64_t)b * A.p_stride + (int64_t)j * A.V - s.phi) * esz;
+  s.rp = make_rsrc(pr, span);
+  const char* qr = with_q ? (const char*)A.q + ((int64_t)b * A.q_stride + (int64_t)j * A.V - s.phi) * esz : pr;
+  s.rq = make_rsrc(qr, with_q ? span : 0);
+  return s;
+}
 
 // Inclusive prefix over sequences of their live-row counts (gamma_b + 1, or 0
-// for an invalid gamma), in LDS. Each thread scans a contiguous segment; the
-// segment totals are scanned across the workgroup in parallel.
+// for an invalid gamma), in LDS.
 __device__ void build_row_table(const int32_t* gamma, int gmax, int B, int* rows) {
-  __shared__ int wsum[kThreads / 64];
+  __shared__ int wsum[kWaves];
   const int tid = threadIdx.x;
   const int lane = tid & 63, w = tid >> 6;
   const int per = (B + kThreads - 1) / kThreads;
@@ -246,506 +271,525 @@ __device__ void build_row_table(const int32_t* gamma, int gmax, int B, int* rows
   __syncthreads();
 }
 
-// ============================================================================
-// Sweep kernel
-
-// One task's entries as loaded: fp32 entries are replaced by their
-// exponentials in the first pass and kept for the second; bf16 entries stay
-// packed and the second pass recomputes the exponentials (the registers then
-// hold twice as many entries per byte of HBM read).
-template <bool BF16, int E>
-struct Raw;
-template <int E>
-struct Raw<false, E> {
-  float p[E], q[E];  // exponentials after the first pass
-  __device__ float gp(int e) const { return p[e]; }
-  __device__ float gq(int e) const { return q[e]; }
-};
-// An opaque copy: each phase unpacks bf16 entries afresh instead of the
-// compiler keeping every unpacked value live from the first use to the last.
-__device__ __forceinline__ uint32_t fresh(uint32_t x) {
-  asm volatile("" : "+v"(x));
-  return x;
-}
-template <int E>
-struct Raw<true, E> {
-  u32x4 pk[E / 8], qk[E / 8];  // as loaded
-  __device__ float gp(int e) const {
-    const uint32_t w = fresh(pk[e / 8][(e % 8) / 2]);
-    return (e & 1) ? bf16_hi(w) : bf16_lo(w);
-  }
-  __device__ float gq(int e) const {
-    const uint32_t w = fresh(qk[e / 8][(e % 8) / 2]);
-    return (e & 1) ? bf16_hi(w) : bf16_lo(w);
-  }
-};
-
-// Set the entries below a threshold to -inf (the top-k / top-p filter).
-template <int E>
-__device__ __forceinline__ void mask_below(Raw<false, E>& r, float tp, float tq) {
-#pragma unroll
-  for (int e = 0; e < E; ++e) {
-    r.p[e] = r.p[e] >= tp ? r.p[e] : kNegInf;
-    r.q[e] = r.q[e] >= tq ? r.q[e] : kNegInf;
-  }
-}
-__device__ __forceinline__ uint32_t mask_pair(uint32_t w, float t) {
-  constexpr uint32_t kNegInfBf16 = 0xff80u;
-  const uint32_t lo = bf16_lo(w) >= t ? (w & 0xffffu) : kNegInfBf16;
-  const uint32_t hi = bf16_hi(w) >= t ? (w >> 16) : kNegInfBf16;
-  return lo | (hi << 16);
-}
-template <int E>
-__device__ __forceinline__ void mask_below(Raw<true, E>& r, float tp, float tq) {
-#pragma unroll
-  for (int v = 0; v < E / 8; ++v)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      r.pk[v][i] = mask_pair(r.pk[v][i], tp);
-      r.qk[v][i] = mask_pair(r.qk[v][i], tq);
-    }
-}
-
 struct TaskInfo {
-  int b, j, c, row;
-  int x;  // the row's draft token (pair rows; -1 for a bonus row)
-  bool pair;
-  const char* prow;
-  const char* qrow;  // the draft row (a pair row), or the p row for a bonus row (never read)
+  int b, j, c, row, x, gam, phi;
+  float thp, thq;  // the row's top-k / top-p thresholds (read only when A.thr is set)
+  bool pair, full;
 };
+
+// A workgroup's tasks, decoded a window at a time into LDS, one per thread:
+// sequence (12 bits), position (5), live-row count (5) and chunk (7) packed in
+// one word, the draft token and the row's thresholds. The task loop then
+// reads its next task with no division, search or global load.
+constexpr int kTab = kThreads;
+struct TaskTable {
+  int pack[kTab];
+  int x[kTab];
+  float thp[kTab], thq[kTab];
+};
+
+// Tasks k0 .. k0 + kTab - 1 of this workgroup (task blockIdx.x + k * gridDim.x).
+__device__ void fill_tasks(const Args& A, const int* rows, long n_tasks, int k0, TaskTable& tab) {
+  const int tid = threadIdx.x;
+  const long task = blockIdx.x + (long)(k0 + tid) * gridDim.x;
+  if (task < n_tasks) {
+    const int rank = (int)(task / A.nc), c = (int)(task % A.nc);
+    int lo = 0, hi = A.B - 1;  // first sequence whose prefix exceeds rank
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (rows[mid] > rank) hi = mid;
+      else lo = mid + 1;
+    }
+    const int first = lo ? rows[lo - 1] : 0;
+    const int j = rank - first, gam = rows[lo] - first - 1;
+    const int row = lo * (A.gmax + 1) + j;
+    tab.pack[tid] = lo | (j << 12) | (gam << 17) | (c << 22);
+    tab.x[tid] = j < gam ? A.drafts[(size_t)lo * A.gmax + j] : -1;
+    tab.thp[tid] = A.thr ? A.thr[(size_t)row * 2] : kNegInf;
+    tab.thq[tid] = A.thr && j < gam ? A.thr[(size_t)row * 2 + 1] : kNegInf;
+  }
+  __syncthreads();
+}
 
 template <bool BF16>
-__device__ __forceinline__ TaskInfo decode_task(const Args& A, const int* rows, long task) {
+__device__ __forceinline__ TaskInfo decode_task(const Args& A, const TaskTable& tab, int k) {
   TaskInfo t;
-  const int rank = (int)(task / A.nc);
-  t.c = (int)(task % A.nc);
-  int lo = 0, hi = A.B - 1;  // first sequence whose prefix exceeds rank
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (rows[mid] > rank) hi = mid;
-    else lo = mid + 1;
-  }
-  t.b = lo;
-  const int first = lo ? rows[lo - 1] : 0;
-  t.j = rank - first;
-  t.pair = t.j < rows[lo] - first - 1;
+  const int i = k % kTab;
+  const int pk = __builtin_amdgcn_readfirstlane(tab.pack[i]);
+  t.b = pk & 0xfff;
+  t.j = (pk >> 12) & 31;
+  t.gam = (pk >> 17) & 31;
+  t.c = pk >> 22;
+  t.pair = t.j < t.gam;
   t.row = t.b * (A.gmax + 1) + t.j;
-  const size_t esz = BF16 ? 2 : 4;
-  t.prow = (const char*)A.p + ((size_t)t.b * A.p_stride + (size_t)t.j * A.V) * esz;
-  t.qrow = t.pair ? (const char*)A.q + ((size_t)t.b * A.q_stride + (size_t)t.j * A.V) * esz : t.prow;
-  t.x = t.pair ? A.drafts[(size_t)t.b * A.gmax + t.j] : -1;  // uniform: a scalar load
+  t.phi = row_phase<BF16>(A, t.j);
+  constexpr int kChunk = Vec<BF16>::kChunk;
+  t.full = t.c * kChunk >= t.phi && (t.c + 1) * kChunk <= t.phi + A.V;
+  t.x = __builtin_amdgcn_readfirstlane(tab.x[i]);
+  t.thp = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(tab.thp[i])));
+  t.thq = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(tab.thq[i])));
   return t;
 }
 
-// Issue the loads of one task (always the same count, so the waits of the
-// task before it stay exact). Offsets past V are clamped into the row.
-template <bool BF16, int E>
-__device__ __forceinline__ void issue_loads(const Args& A, const TaskInfo& t, Raw<BF16, E>& r) {
-  constexpr int VEC = Elt<BF16>::VEC;
-  constexpr int NV = E / VEC;
+// One task's loads (always the same count). A bonus row's draft resource is
+// empty: its loads return zeros without memory traffic.
+// With live false the resources are empty too (a prefetch past the last task).
+template <bool BF16>
+__device__ __forceinline__ void issue_loads(const Args& A, const TaskInfo& t, Loaded<BF16>& lp, Loaded<BF16>& lq,
+                                            bool live = true) {
+  constexpr int N = Vec<BF16>::N, esz = Vec<BF16>::esz, kE = Vec<BF16>::E;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int wbase = t.c * Vec<BF16>::kChunk + w * Vec<BF16>::kWaveSpan;
+  RowSpan s = row_span<BF16>(A, t.b, t.j, t.pair);
+  if (!live) s.rp = s.rq = make_rsrc(A.p, 0);
+#pragma unroll
+  for (int i = 0; i < kE / N; ++i)
+    lp.v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                            s.rp, (uint32_t)((wbase + (i * 64 + lane) * N) * esz), 0, 0));
+#pragma unroll
+  for (int i = 0; i < kE / N; ++i)
+    lq.v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                            s.rq, (uint32_t)((wbase + (i * 64 + lane) * N) * esz), 0, 0));
+}
+
+// Entries outside the row (before its start or past its end) become -inf.
+template <bool BF16>
+__device__ __forceinline__ void mask_range(float (&z)[Vec<BF16>::E], int wbase, int phi, int V) {
+  constexpr int kE = Vec<BF16>::E;
   const int lane = threadIdx.x & 63;
-  const int base = t.c * (kThreads * E) + (threadIdx.x >> 6) * (64 * E);
 #pragma unroll
-  for (int v = 0; v < NV; ++v) {
-    const int x = min(base + (v * 64 + lane) * VEC, A.V - VEC);
-    if constexpr (BF16) {
-      r.pk[v] = *(const u32x4*)((const uint16_t*)t.prow + x);
-    } else {
-      const floatx4 f = *(const floatx4*)((const float*)t.prow + x);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) r.p[v * 4 + i] = f[i];
-    }
+  for (int e = 0; e < kE; ++e) {
+    const int i = lane_pos<BF16>(wbase, lane, e) - phi;
+    z[e] = (i >= 0 && i < V) ? z[e] : kNegInf;
   }
-  // The draft row through a buffer resource: a bonus row has none, so its
-  // resource is empty and the same loads return zeros with no memory traffic.
-  constexpr uint32_t kEsz = BF16 ? 2u : 4u;
-  const __amdgpu_buffer_rsrc_t rq = make_rsrc(t.qrow, t.pair ? (size_t)A.V * kEsz : 0);
+}
+template <int kE>
+__device__ __forceinline__ void mask_below(float (&z)[kE], float t) {
 #pragma unroll
-  for (int v = 0; v < NV; ++v) {
-    const int x = min(base + (v * 64 + lane) * VEC, A.V - VEC);
-    const u32x4 u = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rq, (uint32_t)x * kEsz, 0, 0));
-    if constexpr (BF16) {
-      r.qk[v] = u;
-    } else {
+  for (int e = 0; e < kE; ++e) z[e] = z[e] >= t ? z[e] : kNegInf;
+}
+
+// Pairwise sum of a lane's entries (a fixed tree).
+template <int kE>
+__device__ __forceinline__ float tree_sum(const float (&v)[kE]) {
+  float a[kE];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) r.q[v * 4 + i] = __uint_as_float(u[i]);
+  for (int i = 0; i < kE; ++i) a[i] = v[i];
+#pragma unroll
+  for (int s = kE / 2; s > 0; s /= 2)
+#pragma unroll
+    for (int i = 0; i < s; ++i) a[i] += a[i + s];
+  return a[0];
+}
+
+__device__ __forceinline__ uint32_t rec_off(int row, int nc, int c) {
+  return (uint32_t)(((size_t)row * nc + c) * kRecBytes);
+}
+
+// ---------------------------------------------------------------------------
+// First pass (the workgroup: one task)
+
+// Per-task workgroup state.
+struct TaskShared {
+  float m[2][kWaves];      // the waves' maxima of p and q
+  double s[3][kWaves];     // the waves' sums (p, q, KL numerator; greedy: argmax indices in s[0..1])
+  float rho;               // TV parameters of the task's chunk
+  int swap;
+  int ok;                  // the row's records were all present in time
+};
+
+// The draft token's exponent arguments x_p, x_q and its chunk's shifts, for
+// the acceptance test (p(x) = 2^x_p 2^(r_c - r_max) / S_p, the kernel's own
+// distribution): the lane that holds the token stores them (once per row).
+template <bool BF16>
+__device__ __forceinline__ void store_xlogit(const Args& A, const TaskInfo& t, int wbase,
+                                             const float (&zp)[Vec<BF16>::E], const float (&zq)[Vec<BF16>::E],
+                                             float rp, float rq) {
+  constexpr int N = Vec<BF16>::N, kE = Vec<BF16>::E, kWaveSpan = Vec<BF16>::kWaveSpan;
+  const int lane = threadIdx.x & 63;
+  const int xo = t.x + t.phi - wbase;  // aligned offset of x in this wave's entries
+  if (t.x < 0 || t.x >= A.V || xo < 0 || xo >= kWaveSpan) return;
+  if (lane != (xo % (64 * N)) / N) return;
+  const int ex = (xo / (64 * N)) * N + xo % N;
+  float vp = 0.f, vq = 0.f;
+#pragma unroll
+  for (int e = 0; e < kE; ++e)
+    if (e == ex) {
+      vp = zp[e];
+      vq = zq[e];
     }
+  float* o = A.xlogit + (size_t)t.row * 4;
+  st_dev(o, fmaf(vp, A.lg, -rp));
+  st_dev(o + 1, rp);
+  st_dev(o + 2, fmaf(vq, A.lg, -rq));
+  st_dev(o + 3, rq);
+}
+
+__device__ __forceinline__ void store_rec(const __amdgpu_buffer_rsrc_t& rs, uint32_t off, const StatRec& r) {
+  u32x4 w0, w1;
+  pack_rec(r, w0, w1);
+  __builtin_amdgcn_raw_buffer_store_b128(w0, rs, off, 0, kDeviceCoherent);
+  __builtin_amdgcn_raw_buffer_store_b128(w1, rs, off + 16, 0, kDeviceCoherent);
+}
+
+// Raw logits of one wave's entries, masked: entries outside the row and below
+// the row's top-k / top-p threshold become -inf.
+template <bool BF16>
+__device__ __forceinline__ void masked_logits(const Args& A, const TaskInfo& t, int wbase, const Loaded<BF16>& Lp,
+                                              const Loaded<BF16>& Lq, float (&zp)[Vec<BF16>::E],
+                                              float (&zq)[Vec<BF16>::E]) {
+  widen<BF16>(Lp, zp);
+  widen<BF16>(Lq, zq);
+  if (!t.full) {
+    mask_range<BF16>(zp, wbase, t.phi, A.V);
+    mask_range<BF16>(zq, wbase, t.phi, A.V);
+  }
+  if (A.thr) {  // workgroup-uniform
+    mask_below(zp, t.thp);
+    if (t.pair) mask_below(zq, t.thq);
   }
 }
 
-// Workgroup state of the sweep and its two passes over a task.
-struct SweepShared {
-  float m[2][kWaves];
-  double s[3][kWaves];
-  float f[2];        // this chunk's factors f_c for p and q
-  int ix[2][kWaves];  // greedy: the waves' argmax indices of p and q
+// Integer exponent shift of a maximum (0 for an empty chunk, whose entries
+// are all -inf and give 0 anyway).
+__device__ __forceinline__ float shift_of(float m, float lg) { return m == kNegInf ? 0.f : ceilf(m * lg); }
+
+// The exponentials of one wave's entries under shifts rp, rq, their sums and
+// the KL numerator (groups of four entries summed as (a0 + a1) + (a2 + a3),
+// then a tree over the groups).
+template <int kE>
+__device__ __forceinline__ void wave_exps(const float (&zp)[kE], const float (&zq)[kE], float lg, float rp, float rq,
+                                          bool pair, float (&ep)[kE], float (&eq)[kE], double& sp, double& sq,
+                                          double& kl) {
+  float gp[kE / 4], gq[kE / 4], gk[kE / 4];
+#pragma unroll
+  for (int g = 0; g < kE / 4; ++g) {
+    float kt[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e = g * 4 + i;
+      const float xp = fmaf(zp[e], lg, -rp);
+      const float xq = fmaf(zq[e], lg, -rq);
+      ep[e] = exp2_hw(xp);
+      eq[e] = pair ? exp2_hw(xq) : 0.f;
+      kt[i] = pair ? sr_fmul_legacy(ep[e], xp - xq) : 0.f;  // 0 where p is -inf, +inf where only q is
+    }
+    gp[g] = (ep[g * 4] + ep[g * 4 + 1]) + (ep[g * 4 + 2] + ep[g * 4 + 3]);
+    gq[g] = (eq[g * 4] + eq[g * 4 + 1]) + (eq[g * 4 + 2] + eq[g * 4 + 3]);
+    gk[g] = (kt[0] + kt[1]) + (kt[2] + kt[3]);
+  }
+  sp = wave_sum_d((double)tree_sum(gp));
+  sq = pair ? wave_sum_d((double)tree_sum(gq)) : 0.0;
+  kl = pair ? wave_sum_d((double)tree_sum(gk)) : 0.0;
+}
+
+// Sampling: the chunk's maxima (over the waves), shifts, exponentials (left
+// in ep/eq), sums and the KL numerator; thread 0 publishes the chunk's record.
+template <bool BF16>
+__device__ __forceinline__ void first_pass(const Args& A, const TaskInfo& t, const Loaded<BF16>& Lp,
+                                           const Loaded<BF16>& Lq, float (&ep)[Vec<BF16>::E],
+                                           float (&eq)[Vec<BF16>::E], TaskShared& sh,
+                                           const __amdgpu_buffer_rsrc_t& rs_recs) {
+  constexpr int kE = Vec<BF16>::E;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int wbase = t.c * Vec<BF16>::kChunk + w * Vec<BF16>::kWaveSpan;
+  float mp = kNegInf, mq = kNegInf;
+  {
+    float zp[kE], zq[kE];
+    masked_logits<BF16>(A, t, wbase, Lp, Lq, zp, zq);
+#pragma unroll
+    for (int e = 0; e < kE; ++e) {
+      mp = fmaxf(mp, zp[e]);
+      mq = fmaxf(mq, zq[e]);
+    }
+  }
+  mp = wave_max(mp);
+  if (t.pair) mq = wave_max(mq);
+  if (lane == 0) {
+    sh.m[0][w] = mp;
+    sh.m[1][w] = mq;
+  }
+  __syncthreads();
+  float cmp = sh.m[0][0], cmq = sh.m[1][0];
+#pragma unroll
+  for (int i = 1; i < kWaves; ++i) {
+    cmp = fmaxf(cmp, sh.m[0][i]);
+    cmq = fmaxf(cmq, sh.m[1][i]);
+  }
+  if (!t.pair) cmq = kNegInf;
+  const float rp = shift_of(cmp, A.lg), rq = shift_of(cmq, A.lg);
+  // The logits are widened again from the loaded vectors (made opaque, so
+  // the first widening is not kept live across the reduction).
+  Loaded<BF16> Lp2 = Lp, Lq2 = Lq;
+#pragma unroll
+  for (int i = 0; i < kE / Vec<BF16>::N; ++i) {
+    asm volatile("" : "+v"(Lp2.v[i]));
+    asm volatile("" : "+v"(Lq2.v[i]));
+  }
+  float zp[kE], zq[kE];
+  masked_logits<BF16>(A, t, wbase, Lp2, Lq2, zp, zq);
+  if (t.pair) store_xlogit<BF16>(A, t, wbase, zp, zq, rp, rq);
+  double sp, sq, kl;
+  wave_exps(zp, zq, A.lg, rp, rq, t.pair, ep, eq, sp, sq, kl);
+  if (lane == 0) {
+    sh.s[0][w] = sp;
+    sh.s[1][w] = sq;
+    sh.s[2][w] = kl;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    StatRec r;
+    r.rp = cmp == kNegInf ? kNegInf : rp;
+    r.rq = cmq == kNegInf ? kNegInf : rq;
+    r.sp = ((sh.s[0][0] + sh.s[0][1]) + sh.s[0][2]) + sh.s[0][3];
+    r.sq = ((sh.s[1][0] + sh.s[1][1]) + sh.s[1][2]) + sh.s[1][3];
+    r.kl = ((sh.s[2][0] + sh.s[2][1]) + sh.s[2][2]) + sh.s[2][3];
+    store_rec(rs_recs, rec_off(t.row, A.nc, t.c), r);
+  }
+}
+
+// Greedy decoding: the chunk's maxima of p and q and the lowest index holding
+// each (lanes scan their entries in ascending index order).
+template <bool BF16>
+__device__ __forceinline__ void argmax_pass(const Args& A, const TaskInfo& t, const Loaded<BF16>& Lp,
+                                            const Loaded<BF16>& Lq, TaskShared& sh,
+                                            const __amdgpu_buffer_rsrc_t& rs_recs) {
+  constexpr int kE = Vec<BF16>::E;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int wbase = t.c * Vec<BF16>::kChunk + w * Vec<BF16>::kWaveSpan;
+  float zp[kE], zq[kE];
+  widen<BF16>(Lp, zp);
+  widen<BF16>(Lq, zq);
+  float bp = kNegInf, bq = kNegInf;
+  int ip = INT_MAX, iq = INT_MAX;
+#pragma unroll
+  for (int e = 0; e < kE; ++e) {
+    const int i = lane_pos<BF16>(wbase, lane, e) - t.phi;
+    const bool in = t.full || (i >= 0 && i < A.V);
+    if (in && (ip == INT_MAX || zp[e] > bp)) {
+      bp = zp[e];
+      ip = i;
+    }
+    if (in && (iq == INT_MAX || zq[e] > bq)) {
+      bq = zq[e];
+      iq = i;
+    }
+  }
+  const float mp = wave_max(bp);
+  const int jp = wave_min_i(ip != INT_MAX && bp == mp ? ip : INT_MAX);
+  float mq = kNegInf;
+  int jq = INT_MAX;
+  if (t.pair) {
+    mq = wave_max(bq);
+    jq = wave_min_i(iq != INT_MAX && bq == mq ? iq : INT_MAX);
+  }
+  if (lane == 0) {
+    sh.m[0][w] = mp;
+    sh.m[1][w] = mq;
+    sh.s[0][w] = (double)jp;
+    sh.s[1][w] = (double)jq;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    StatRec r;
+    r.rp = kNegInf;
+    r.rq = kNegInf;
+    int ap = INT_MAX, aq = INT_MAX;
+    for (int i = 0; i < kWaves; ++i) {
+      r.rp = fmaxf(r.rp, sh.m[0][i]);
+      r.rq = fmaxf(r.rq, sh.m[1][i]);
+    }
+    for (int i = 0; i < kWaves; ++i) {
+      if (sh.m[0][i] == r.rp) ap = min(ap, (int)sh.s[0][i]);
+      if (sh.m[1][i] == r.rq) aq = min(aq, (int)sh.s[1][i]);
+    }
+    r.sp = (double)ap;
+    r.sq = (double)aq;
+    r.kl = 0.0;
+    store_rec(rs_recs, rec_off(t.row, A.nc, t.c), r);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Row merges (one wave; the same code wherever a row is merged, so every
+// merge of a row gives the same bits)
+
+// A row's chunk records, lane-wise: chunk lane * kSlots + i in slot i.
+struct RowRecs {
+  float rp[kSlots], rq[kSlots];
+  double sp[kSlots], sq[kSlots], kl[kSlots];
 };
 
-template <bool BF16, int E>
-struct Sweep {
-  static constexpr int VEC = Elt<BF16>::VEC;
-  static constexpr int kChunk = kThreads * E;
-  const Args& A;
-  SweepShared& sh;
-  const int tid, lane, w, nc, nslot;
-  const __amdgpu_buffer_rsrc_t rs_stats;
+// A row's record words as loaded (device-coherent loads), lane-wise.
+struct RecWords {
+  u32x4 w[kSlots][2];
+};
 
-  __device__ Sweep(const Args& a, SweepShared& s)
-      : A(a), sh(s), tid(threadIdx.x), lane(threadIdx.x & 63), w(threadIdx.x >> 6), nc(a.nc),
-        nslot((a.nc + 63) / 64),
-        rs_stats(make_rsrc(a.stats, (size_t)a.B * (a.gmax + 1) * a.nc * kRecBytes)) {}
-
-  // First pass over a task's entries: chunk maxima, exponentials, sums, KL
-  // numerator, and the published record. Leaves the chunk maxima in cmp/cmq
-  // (and, for fp32, the exponentials in r).
-  __device__ __forceinline__ void first_pass(const TaskInfo& t, Raw<BF16, E>& r, float& cmp, float& cmq) {
-    const int base = t.c * kChunk + w * (64 * E);
-    if (A.thr) {  // top-k / top-p: entries below the row's threshold become -inf (workgroup-uniform branch)
-      const float tp = A.thr[(size_t)t.row * 2];
-      const float tq = t.pair ? A.thr[(size_t)t.row * 2 + 1] : kNegInf;
-      mask_below(r, tp, tq);
-    }
-    // The draft token's two logits, for the finish kernel's acceptance test:
-    // the lane that holds entry x stores them (once per row).
-    const int xo = t.x - base;  // offset of x in this wave's entries
-    if (xo >= 0 && xo < 64 * E && lane == (xo % (64 * VEC)) / VEC) {
-      const int ex = (xo / (64 * VEC)) * VEC + xo % VEC;
-      float zp = 0.f, zq = 0.f;
+__device__ __forceinline__ void issue_recs(const Args& A, const __amdgpu_buffer_rsrc_t& rs, int row, RecWords& W) {
+  const int lane = threadIdx.x & 63;
 #pragma unroll
-      for (int e = 0; e < E; ++e)
-        if (e == ex) {
-          zp = r.gp(e);
-          zq = r.gq(e);
-        }
-      A.xlogit[(size_t)t.row * 2] = zp;
-      A.xlogit[(size_t)t.row * 2 + 1] = zq;
-    }
-    auto in_v = [&](int e) __attribute__((always_inline)) {  // entry e lies below V
-      return base + ((e / VEC) * 64 + lane) * VEC < A.V;
-    };
-    float mp = kNegInf, mq = kNegInf;
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const bool in = in_v(e);
-      const float zp = r.gp(e), zq = r.gq(e);  // unconditional: then a select
-      mp = fmaxf(mp, in ? zp : kNegInf);
-      mq = fmaxf(mq, in && t.pair ? zq : kNegInf);
-      if (e % 8 == 7) __builtin_amdgcn_sched_barrier(0);  // unpack eight entries at a time
-    }
-    mp = wave_max(mp);
-    if (t.pair) mq = wave_max(mq);
-    if (lane == 0) {
-      sh.m[0][w] = mp;
-      sh.m[1][w] = mq;
-    }
-    __syncthreads();
-    cmp = max_waves(sh.m[0]);
-    cmq = max_waves(sh.m[1]);
-
-    // exponentials, sums, KL numerator; groups of four are summed as
-    // (a0 + a1) + (a2 + a3), then a tree over groups
-    const float lg = A.lg;
-    const float rp = cmp == kNegInf ? 0.f : cmp * lg;
-    const float rq = cmq == kNegInf ? 0.f : cmq * lg;
-    // the KL numerator on logits relative to the chunk maxima, so that the
-    // row-level merge subtracts no large terms (two rows whose filtered
-    // distributions coincide give exactly zero)
-    const float op = cmp == kNegInf ? 0.f : cmp;
-    const float oq = cmq == kNegInf ? 0.f : cmq;
-    double dsp, dsq = 0.0, dkl = 0.0;
-    if (t.pair) {
-      float gp[E / 4], gq[E / 4], gk[E / 4];
-#pragma unroll
-      for (int g = 0; g < E / 4; ++g) {
-        float ep[4], eq[4], kt[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int e = g * 4 + i;
-          const bool in = in_v(e);
-          const float zp = r.gp(e), zq = r.gq(e);
-          ep[i] = in ? exp2_hw(fmaf(zp, lg, -rp)) : 0.f;
-          eq[i] = in ? exp2_hw(fmaf(zq, lg, -rq)) : 0.f;
-          kt[i] = ep[i] > 0.f ? ep[i] * ((zp - op) - (zq - oq)) : 0.f;
-          if constexpr (!BF16) {
-            r.p[e] = ep[i];
-            r.q[e] = eq[i];
-          }
-        }
-        gp[g] = (ep[0] + ep[1]) + (ep[2] + ep[3]);
-        gq[g] = (eq[0] + eq[1]) + (eq[2] + eq[3]);
-        gk[g] = (kt[0] + kt[1]) + (kt[2] + kt[3]);
-        __builtin_amdgcn_sched_barrier(0);  // bounds live ranges: one group at a time
-      }
-      dsp = wave_sum_d((double)tree_sum(gp));
-      dsq = wave_sum_d((double)tree_sum(gq));
-      dkl = wave_sum_d((double)tree_sum(gk));
-    } else {
-      float gp[E / 4];
-#pragma unroll
-      for (int g = 0; g < E / 4; ++g) {
-        float ep[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float zp = r.gp(g * 4 + i);
-          ep[i] = in_v(g * 4 + i) ? exp2_hw(fmaf(zp, lg, -rp)) : 0.f;
-        }
-        gp[g] = (ep[0] + ep[1]) + (ep[2] + ep[3]);
-      }
-      dsp = wave_sum_d((double)tree_sum(gp));
-    }
-    if (lane == 0) {
-      sh.s[0][w] = dsp;
-      sh.s[1][w] = dsq;
-      sh.s[2][w] = dkl;
-    }
-    __syncthreads();
-    if (tid == 0) {
-      const size_t rec = (size_t)t.row * nc + t.c;
-      StatRec sr;
-      sr.mp = cmp;
-      sr.mq = cmq;
-      sr.sp = sum_waves(sh.s[0]);
-      sr.sq = sum_waves(sh.s[1]);
-      sr.kl = sum_waves(sh.s[2]);
-      u32x4 w0, w1;
-      pack_rec(sr, w0, w1);
-      __builtin_amdgcn_raw_buffer_store_b128(w0, rs_stats, (uint32_t)(rec * kRecBytes), 0, kDeviceCoherent);
-      __builtin_amdgcn_raw_buffer_store_b128(w1, rs_stats, (uint32_t)(rec * kRecBytes + 16), 0, kDeviceCoherent);
-    }
+  for (int i = 0; i < kSlots; ++i) {
+    const int c = lane * kSlots + i;
+    const uint32_t off = rec_off(row, A.nc, c < A.nc ? c : 0);
+    W.w[i][0] = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, kDeviceCoherent);
+    W.w[i][1] = __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16, 0, kDeviceCoherent);
   }
+}
 
-  // Greedy decoding: the chunk's maxima of p and q and the lowest index
-  // holding each, published as the chunk's record (indices in the sum fields).
-  __device__ __forceinline__ void argmax_pass(const TaskInfo& t, const Raw<BF16, E>& r) {
-    const int base = t.c * kChunk + w * (64 * E);
-    float bp = kNegInf, bq = kNegInf;
-    int ip = -1, iq = -1;
+// The records from their words; true (wave-uniform) when all are present.
+__device__ __forceinline__ bool decode_recs(const Args& A, const RecWords& W, RowRecs& R) {
+  const int lane = threadIdx.x & 63;
+  bool ok = true;
 #pragma unroll
-    for (int e = 0; e < E; ++e) {  // a lane's entries in ascending index order
-      const int idx = base + ((e / VEC) * 64 + lane) * VEC + e % VEC;
-      const bool in = idx < A.V;
-      const float zp = r.gp(e), zq = r.gq(e);
-      if (in && (ip < 0 || zp > bp)) {
-        bp = zp;
-        ip = idx;
-      }
-      if (in && (iq < 0 || zq > bq)) {
-        bq = zq;
-        iq = idx;
-      }
-    }
-    const float mp = wave_max(bp);
-    const int jp = wave_min_i(ip >= 0 && bp == mp ? ip : INT_MAX);
-    float mq = kNegInf;
-    int jq = INT_MAX;
-    if (t.pair) {
-      mq = wave_max(bq);
-      jq = wave_min_i(iq >= 0 && bq == mq ? iq : INT_MAX);
-    }
-    if (lane == 0) {
-      sh.m[0][w] = mp;
-      sh.m[1][w] = mq;
-      sh.ix[0][w] = jp;
-      sh.ix[1][w] = jq;
-    }
-    __syncthreads();
-    if (tid == 0) {
-      StatRec sr;
-      sr.mp = max_waves(sh.m[0]);
-      sr.mq = max_waves(sh.m[1]);
-      int ap = INT_MAX, aq = INT_MAX;
-      for (int i = 0; i < kWaves; ++i) {
-        if (sh.m[0][i] == sr.mp) ap = min(ap, sh.ix[0][i]);
-        if (sh.m[1][i] == sr.mq) aq = min(aq, sh.ix[1][i]);
-      }
-      sr.sp = (double)ap;
-      sr.sq = (double)aq;
-      sr.kl = 0.0;
-      u32x4 w0, w1;
-      pack_rec(sr, w0, w1);
-      const size_t rec = (size_t)t.row * nc + t.c;
-      __builtin_amdgcn_raw_buffer_store_b128(w0, rs_stats, (uint32_t)(rec * kRecBytes), 0, kDeviceCoherent);
-      __builtin_amdgcn_raw_buffer_store_b128(w1, rs_stats, (uint32_t)(rec * kRecBytes + 16), 0, kDeviceCoherent);
-    }
-    __syncthreads();  // the next task rewrites sh.m and sh.ix
+  for (int i = 0; i < kSlots; ++i) {
+    const int c = lane * kSlots + i;
+    const bool in = c < A.nc;
+    const u32x4 w0 = W.w[i][0], w1 = W.w[i][1];
+    ok = ok && (!in || rec_present(w0, w1));
+    const StatRec r = unpack_rec(w0, w1);
+    R.rp[i] = in ? r.rp : kNegInf;
+    R.rq[i] = in ? r.rq : kNegInf;
+    R.sp[i] = in ? r.sp : 0.0;
+    R.sq[i] = in ? r.sq : 0.0;
+    R.kl[i] = in ? r.kl : 0.0;
   }
+  return __ballot(!ok) == 0ull;
+}
 
-  // One wave: re-load the records of a pair row until all of them are
-  // present, merge them into the row's normalisers and leave the chunk's
-  // factors in sh.f (lane 0 writes them).
-  __device__ __forceinline__ void row_factors(const TaskInfo& t, float cmp, float cmq) {
-    float m1[kSlots], m2[kSlots];
-    double s1[kSlots], s2[kSlots];
-    for (uint32_t it = 0;; ++it) {
-      bool ok = true;
+// Loads the records; true (wave-uniform) when all are present.
+__device__ __forceinline__ bool load_recs(const Args& A, const __amdgpu_buffer_rsrc_t& rs, int row, RowRecs& R) {
+  RecWords W;
+  issue_recs(A, rs, row, W);
+  return decode_recs(A, W, R);
+}
+
+// A distribution's normaliser: the largest shift r_max and
+// S = sum_c s_c 2^(r_c - r_max), so that its entries are 2^x 2^(r_c - r_max) / S
+// (shifts are integers: 2^(r_c - r_max) is exact).
+struct Norm {
+  float rM;
+  double S;
+};
+
+__device__ __forceinline__ double pow2(float r, float rM) {
+  return r == kNegInf ? 0.0 : ldexp(1.0, (int)(r - rM));
+}
+
+__device__ __forceinline__ Norm merge_norm(const float (&r)[kSlots], const double (&s)[kSlots]) {
+  float m = kNegInf;
 #pragma unroll
-      for (int i = 0; i < kSlots; ++i) {
-        const int cc = lane * nslot + i;
-        const bool in = i < nslot && cc < nc;
-        const uint32_t off = (uint32_t)(((size_t)t.row * nc + (in ? cc : 0)) * kRecBytes);
-        const u32x4 w0 = __builtin_amdgcn_raw_buffer_load_b128(rs_stats, off, 0, kDeviceCoherent);
-        const u32x4 w1 = __builtin_amdgcn_raw_buffer_load_b128(rs_stats, off + 16, 0, kDeviceCoherent);
-        ok = ok && (!in || rec_present(w0, w1));
-        const StatRec sr = unpack_rec(w0, w1);
-        m1[i] = in ? sr.mp : kNegInf;
-        m2[i] = in ? sr.mq : kNegInf;
-        s1[i] = in ? sr.sp : 0.0;
-        s2[i] = in ? sr.sq : 0.0;
-      }
-      if (__ballot(!ok) == 0ull) break;
-      if (it == kSpinLimit) {
-        if (lane == 0 && A.status) atomicOr(A.status, SR_ST_TIMEOUT);
-        break;
-      }
+  for (int i = 0; i < kSlots; ++i) m = fmaxf(m, r[i]);
+  Norm n;
+  n.rM = wave_max(m);
+  double acc = 0.0;
+  if (n.rM != kNegInf) {
+#pragma unroll
+    for (int i = 0; i < kSlots; ++i) acc += s[i] * pow2(r[i], n.rM);
+  }
+  n.S = wave_sum_d(acc);
+  return n;
+}
+
+// Factor turning a chunk's exponentials into probabilities.
+__device__ __forceinline__ double factor(float r, const Norm& n) {
+  return (r == kNegInf || !(n.S > 0.0)) ? 0.0 : pow2(r, n.rM) / n.S;
+}
+
+// The TV sum of a chunk with factors fp, fq is scale * sum |fma(a, rho, -b)|,
+// (a, b) = (e_q, e_p) if swap else (e_p, e_q): the larger factor is scale, the
+// ratio rho <= 1 multiplies the other side (rows with equal factors subtract
+// exactly).
+struct TvPar {
+  double scale;
+  float rho;
+  bool swap;
+};
+__device__ __forceinline__ TvPar tv_par(double fp, double fq) {
+  TvPar t;
+  t.swap = fp > fq;
+  t.scale = t.swap ? fp : fq;
+  t.rho = t.scale > 0.0 ? (float)((t.swap ? fq : fp) / t.scale) : 0.f;
+  return t;
+}
+
+// One wave's part of a chunk's TV sum.
+template <int kE>
+__device__ __forceinline__ double tv_wave(const float (&ep)[kE], const float (&eq)[kE], float rho, bool swap) {
+  float g[kE / 4];
+#pragma unroll
+  for (int k = 0; k < kE / 4; ++k) {
+    float d[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float a = swap ? eq[k * 4 + i] : ep[k * 4 + i];
+      const float b = swap ? ep[k * 4 + i] : eq[k * 4 + i];
+      d[i] = fabsf(fmaf(a, rho, -b));
+    }
+    g[k] = (d[0] + d[1]) + (d[2] + d[3]);
+  }
+  return wave_sum_d((double)tree_sum(g));
+}
+// A chunk's TV sum from its waves' parts, in a fixed order.
+__device__ __forceinline__ double tv_chunk(const double (&part)[kWaves]) {
+  return ((part[0] + part[1]) + part[2]) + part[3];
+}
+
+__device__ __forceinline__ float lane_float(float x, int src) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), src));
+}
+
+// The chunk's shifts from the lane-wise records.
+__device__ __forceinline__ void chunk_shifts(const RowRecs& R, int c, float& rp, float& rq) {
+  const int src = c / kSlots, slot = c % kSlots;
+  rp = kNegInf;
+  rq = kNegInf;
+#pragma unroll
+  for (int i = 0; i < kSlots; ++i)
+    if (i == slot) {
+      rp = lane_float(R.rp[i], src);
+      rq = lane_float(R.rq[i], src);
+    }
+}
+
+// Wave 0: the row's records from the words of a first attempt (W, issued
+// earlier), else re-loaded until all are present (for a bounded time); merge
+// them and leave the task's TV parameters in LDS.
+__device__ __forceinline__ void poll_row(const Args& A, const __amdgpu_buffer_rsrc_t& rs, const TaskInfo& t,
+                                         const RecWords& W, TaskShared& sh) {
+  const int lane = threadIdx.x & 63;
+  RowRecs R;
+  bool ok = decode_recs(A, W, R);
+  if (!ok) {
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    for (;;) {
       __builtin_amdgcn_s_sleep(2);
+      ok = load_recs(A, rs, t.row, R);
+      if (ok || __builtin_amdgcn_s_memrealtime() - t0 > kWaitTicks) break;
     }
-    const RowNorm np = row_norm(m1, s1, A.lg);
-    const RowNorm nq = row_norm(m2, s2, A.lg);
+  }
+  if (ok) {
+    const Norm np = merge_norm(R.rp, R.sp);
+    const Norm nq = merge_norm(R.rq, R.sq);
+    float rpc, rqc;
+    chunk_shifts(R, t.c, rpc, rqc);
+    const TvPar p = tv_par(factor(rpc, np), factor(rqc, nq));
     if (lane == 0) {
-      sh.f[0] = np.factor(cmp);
-      sh.f[1] = nq.factor(cmq);
+      sh.rho = p.rho;
+      sh.swap = p.swap ? 1 : 0;
     }
   }
-
-  // Every wave, after a barrier that follows row_factors: sum |P - Q| over the
-  // entries kept from the first pass; the chunk's sum is stored for the finish
-  // kernel.
-  __device__ __forceinline__ void tv_pass(const TaskInfo& t, const Raw<BF16, E>& r, float cmp, float cmq) {
-    const float fp = sh.f[0], fq = sh.f[1];
-    const float lg = A.lg;
-    const float rp = cmp == kNegInf ? 0.f : cmp * lg;
-    const float rq = cmq == kNegInf ? 0.f : cmq * lg;
-    const int base = t.c * kChunk + w * (64 * E);
-    float ga[E / 4];
-#pragma unroll
-    for (int g = 0; g < E / 4; ++g) {
-      float a[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int e = g * 4 + i;
-        float ep, eq;
-        if constexpr (BF16) {
-          const bool in = base + ((e / VEC) * 64 + lane) * VEC < A.V;
-          const float zp = r.gp(e), zq = r.gq(e);
-          ep = in ? exp2_hw(fmaf(zp, lg, -rp)) : 0.f;
-          eq = in ? exp2_hw(fmaf(zq, lg, -rq)) : 0.f;
-        } else {
-          ep = r.p[e];
-          eq = r.q[e];
-        }
-        {
-          // separately rounded products: identical p and q rows give exactly zero
-#pragma clang fp contract(off)
-          a[i] = fabsf(ep * fp - eq * fq);
-        }
-      }
-      ga[g] = (a[0] + a[1]) + (a[2] + a[3]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    const double dtv = wave_sum_d((double)tree_sum(ga));
-    if (lane == 0) sh.s[0][w] = dtv;
-    __syncthreads();
-    if (tid == 0) A.tvabs[(size_t)t.row * nc + t.c] = sum_waves(sh.s[0]);
-  }
-};
-
-// Persistent sweep: workgroup w takes tasks w, w + G, w + 2G, ... two deep.
-template <bool BF16, int E>
-__global__ void __launch_bounds__(kThreads)
-accept_sweep_kernel(Args A) {
-  extern __shared__ int s_rows[];  // [B] inclusive prefix of live rows
-  __shared__ SweepShared sh;
-  Sweep<BF16, E> S(A, sh);
-  const int w = S.w;
-  if (A.rb_reset && A.rb_phys && blockIdx.x == 0 && threadIdx.x == 0) *A.rb_phys = INT_MIN;  // see finish_rollback
-
-  build_row_table(A.gamma, A.gmax, A.B, s_rows);
-  const long n_tasks = (long)s_rows[A.B - 1] * S.nc;
-
-  // Pipeline: the second pass of task i runs after the loads of task i+1 are
-  // issued and before its first pass, so the other chunks of task i's row have
-  // had a whole first pass to publish. Every LDS slot is rewritten only after a
-  // barrier that follows its last read.
-  long task = blockIdx.x;
-  if (task >= n_tasks) return;
-  TaskInfo t = decode_task<BF16>(A, s_rows, task);
-  Raw<BF16, E> cur;
-  issue_loads<BF16, E>(A, t, cur);
-  float cmp, cmq;
-  S.first_pass(t, cur, cmp, cmq);
-  for (;;) {
-    const long task_n = task + gridDim.x;
-    const bool more = task_n < n_tasks;
-    const TaskInfo tn = decode_task<BF16>(A, s_rows, more ? task_n : task);  // past the end: reload (cached)
-    Raw<BF16, E> nxt;
-    // Waves 1-3 prefetch first. Wave 0 polls the row's records first (a wave's
-    // loads complete in issue order, so its poll would otherwise also wait for
-    // its prefetch) and prefetches after.
-    __builtin_amdgcn_sched_barrier(0);
-    if (w != 0 || !t.pair) issue_loads<BF16, E>(A, tn, nxt);
-    __builtin_amdgcn_sched_barrier(0);
-    if (t.pair) {  // workgroup-uniform
-      if (w == 0) {
-        S.row_factors(t, cmp, cmq);
-        __builtin_amdgcn_sched_barrier(0);
-        issue_loads<BF16, E>(A, tn, nxt);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      __syncthreads();
-      S.tv_pass(t, cur, cmp, cmq);
-    }
-    if (!more) break;
-    float cmp_n, cmq_n;
-    S.first_pass(tn, nxt, cmp_n, cmq_n);
-    task = task_n;
-    t = tn;
-    cur = nxt;
-    cmp = cmp_n;
-    cmq = cmq_n;
-  }
+  if (lane == 0) sh.ok = ok ? 1 : 0;
 }
 
-// Greedy decoding: one pass of chunk argmaxes, no second pass and no waiting
-// (workgroup w takes tasks w, w + G, ..., loading one task ahead).
-template <bool BF16, int E>
-__global__ void __launch_bounds__(kThreads)
-accept_argmax_kernel(Args A) {
-  extern __shared__ int s_rows[];
-  __shared__ SweepShared sh;
-  Sweep<BF16, E> S(A, sh);
-  if (A.rb_reset && A.rb_phys && blockIdx.x == 0 && threadIdx.x == 0) *A.rb_phys = INT_MIN;  // see finish_rollback
-  build_row_table(A.gamma, A.gmax, A.B, s_rows);
-  const long n_tasks = (long)s_rows[A.B - 1] * S.nc;
-  long task = blockIdx.x;
-  if (task >= n_tasks) return;
-  TaskInfo t = decode_task<BF16>(A, s_rows, task);
-  Raw<BF16, E> cur;
-  issue_loads<BF16, E>(A, t, cur);
-  for (;;) {
-    const long task_n = task + gridDim.x;
-    const bool more = task_n < n_tasks;
-    const TaskInfo tn = decode_task<BF16>(A, s_rows, more ? task_n : task);
-    Raw<BF16, E> nxt;
-    __builtin_amdgcn_sched_barrier(0);
-    issue_loads<BF16, E>(A, tn, nxt);
-    __builtin_amdgcn_sched_barrier(0);
-    S.argmax_pass(t, cur);
-    if (!more) break;
-    task = task_n;
-    t = tn;
-    cur = nxt;
-  }
-}
-
-// ============================================================================
-// Finish kernel
+// ---------------------------------------------------------------------------
+// Sequence outputs (one wave)
 
 __device__ void write_invalid(const Args& A, int b, uint32_t bits) {
   const int lane = threadIdx.x & 63;
   if (lane == 0) {
     A.accept_len[b] = -1;
     if (A.new_len) A.new_len[b] = A.kv_len[b];
-    if (A.status) atomicOr(A.status, (int32_t)bits);
+    if (A.status && bits) atomicOr(A.status, (int32_t)bits);
   }
   for (int j = lane; j <= A.gmax; j += 64) A.out_tokens[(size_t)b * (A.gmax + 1) + j] = -1;
   const float nan = __builtin_nanf("");
@@ -762,13 +806,8 @@ __device__ void write_invalid(const Args& A, int b, uint32_t bits) {
 // Rollback of sequence b from `old` to `want` rows (Section 4.4, Eq. 9),
 // exactly as the rollback call does it: a length outside [0, L_cap] or a
 // negative target is flagged and left alone, a target above the length is
-// flagged and ignored; otherwise the mask entries [n, old) are cleared and
-// the length becomes n = min(old, want). The physical length is the maximum
-// of the resulting lengths over all sequences: the call's first sweep launch
-// sets it to INT_MIN and every sequence folds its length in with an atomic
-// maximum (no result is waited for). `old` is read at the start of the
-// finish kernel, so the rollback adds no round trip. Called by one whole
-// wave.
+// flagged and ignored; otherwise the mask entries [n, old) are cleared and the
+// length becomes n = min(old, want). `old` is read when the sequence finishes.
 __device__ void finish_rollback(const Args& A, int b, int old, int want) {
   if (!A.rb_kv) return;
   const int lane = threadIdx.x & 63;
@@ -783,23 +822,218 @@ __device__ void finish_rollback(const Args& A, int b, int old, int want) {
       for (int x = n + lane; x < old; x += 64) A.rb_mask[(size_t)b * A.rb_lcap + x] = 0;
   }
   if (lane == 0) {
-    A.rb_kv[b] = n;
+    st_dev((uint32_t*)A.rb_kv + b, (uint32_t)n);
     if (st && A.status) atomicOr(A.status, st);
-    if (A.rb_phys) atomicMax(A.rb_phys, n);
   }
 }
 
-// Zero the records of sequence b's live rows (the "not yet written" state the
-// next call's sweep waits on). Called by one whole wave.
-__device__ void clear_records(const Args& A, int b, int gam) {
-  const size_t first = (size_t)b * (A.gmax + 1) * A.nc * 2;
-  const size_t n = (size_t)(gam + 1) * A.nc * 2;
-  for (size_t i = threadIdx.x & 63; i < n; i += 64) A.stats[first + i] = u32x4{0u, 0u, 0u, 0u};
+// One wave, after its sequences' rollbacks have completed: count them; the
+// launch's last finished sequence writes the physical length, the maximum of
+// the rolled-back lengths of the whole batch so far (Eq. 9), and resets the
+// counter.
+__device__ void count_finished(const Args& A, uint32_t n) {
+  if (!A.rb_kv || !A.rb_phys || n == 0) return;
+  const int lane = threadIdx.x & 63;
+  stores_done();
+  uint32_t old = 0;
+  if (lane == 0) old = __hip_atomic_fetch_add(A.fincnt, n, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  old = (uint32_t)__builtin_amdgcn_readfirstlane((int)old);
+  if (old + n != (uint32_t)A.B) return;
+  int m = INT_MIN;
+  for (int b = lane; b < A.n_before + A.B; b += 64) m = max(m, (int)ld_dev((const uint32_t*)A.rb_kv_all + b));
+  m = wave_max_i(m);
+  if (lane == 0) {
+    *A.rb_phys = m;
+    st_dev(A.fincnt, 0u);
+  }
 }
 
-// Wave-wide inclusive prefix sum (fp64) in ascending lane order: DPP row
-// shifts inside each 16-lane row, then the totals of the earlier rows.
-__device__ __forceinline__ double wave_incl_scan(double x) {
+// Zero every workspace word sequence b's rows used, so the workspace is all
+// zero again when the call ends: the next call, whatever its shape, lays its
+// regions over these bytes, and its polls take any non-zero record word for a
+// published one.
+__device__ void clear_sequence(const Args& A, int b, int gam) {
+  const int lane = threadIdx.x & 63;
+  const size_t r0 = (size_t)b * (A.gmax + 1);
+  const u32x4 z4 = u32x4{0u, 0u, 0u, 0u};
+  // the records with device-coherent stores
+  const uint32_t nrec = (uint32_t)((gam + 1) * A.nc * 2);  // 16-byte words
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(A.recs + r0 * A.nc * 2, (size_t)nrec * 16);
+  for (uint32_t i = lane; i < nrec; i += 64) __builtin_amdgcn_raw_buffer_store_b128(z4, rs, i * 16u, 0, kDeviceCoherent);
+  for (size_t i = lane; i < (size_t)gam * A.nc * kWaves; i += 64) A.tva[r0 * A.nc * kWaves + i] = 0.0;
+  for (int i = lane; i < 2 * (gam + 1); i += 64)
+    if (A.thr) A.thr[r0 * 2 + i] = 0.f;
+  for (int i = lane; i < 4 * gam; i += 64) A.xlogit[r0 * 4 + i] = 0.f;
+}
+
+// ---------------------------------------------------------------------------
+// Row finaliser (wave 0 of the workgroup whose task completed the row)
+
+// A chunk's TV sum: its four waves' parts (device-coherent loads) in a fixed
+// order; kSkipped if any part was left to the finaliser; 0 past the row.
+__device__ __forceinline__ double load_tv_chunk(const Args& A, int row, int c) {
+  if (c >= A.nc) return 0.0;
+  const double* p = A.tva + ((size_t)row * A.nc + c) * kWaves;
+  double part[kWaves];
+  bool skipped = false;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    part[w] = __hip_atomic_load(p + w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    skipped = skipped || part[w] == kSkipped;
+  }
+  return skipped ? kSkipped : tv_chunk(part);
+}
+
+// Recompute the sums of the chunks whose owners gave up waiting, from memory,
+// with the owners' arithmetic and layout (one wave takes the four waves'
+// entries in turn and combines their parts in the same order: same bits).
+template <bool BF16>
+__device__ void redo_skipped(const Args& A, int b, int j, const RowRecs& R, const Norm& np, const Norm& nq,
+                             double (&tva)[kSlots]) {
+  constexpr int N = Vec<BF16>::N, esz = Vec<BF16>::esz, kE = Vec<BF16>::E;
+  constexpr int kChunk = Vec<BF16>::kChunk, kWaveSpan = Vec<BF16>::kWaveSpan;
+  const int lane = threadIdx.x & 63;
+  const RowSpan s = row_span<BF16>(A, b, j, true);
+  const int row = b * (A.gmax + 1) + j;
+  for (;;) {
+    int cl = -1;
+#pragma unroll
+    for (int i = kSlots - 1; i >= 0; --i)
+      if (tva[i] == kSkipped) cl = lane * kSlots + i;
+    const unsigned long long pend = __ballot(cl >= 0);
+    if (!pend) break;
+    const int src = __ffsll((long long)pend) - 1;
+    const int c = __builtin_amdgcn_readlane(cl, src);  // the lowest skipped chunk of that lane
+    float rpc, rqc;
+    chunk_shifts(R, c, rpc, rqc);
+    const float rp = rpc == kNegInf ? 0.f : rpc, rq = rqc == kNegInf ? 0.f : rqc;
+    const TvPar par = tv_par(factor(rpc, np), factor(rqc, nq));
+    TaskInfo t;
+    t.c = c;
+    t.row = row;
+    t.pair = true;
+    t.phi = s.phi;
+    t.full = c * kChunk >= s.phi && (c + 1) * kChunk <= s.phi + A.V;
+    t.thp = A.thr ? A.thr[(size_t)row * 2] : kNegInf;
+    t.thq = A.thr ? A.thr[(size_t)row * 2 + 1] : kNegInf;
+    double part[kWaves];
+#pragma unroll
+    for (int ww = 0; ww < kWaves; ++ww) {
+      const int wbase = c * kChunk + ww * kWaveSpan;
+      Loaded<BF16> lp, lq;
+#pragma unroll
+      for (int i = 0; i < kE / N; ++i) {
+        const uint32_t off = (uint32_t)((wbase + (i * 64 + lane) * N) * esz);
+        lp.v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(s.rp, off, 0, 0));
+        lq.v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(s.rq, off, 0, 0));
+      }
+      float zp[kE], zq[kE], ep[kE], eq[kE];
+      masked_logits<BF16>(A, t, wbase, lp, lq, zp, zq);
+#pragma unroll
+      for (int e = 0; e < kE; ++e) {
+        ep[e] = exp2_hw(fmaf(zp[e], A.lg, -rp));
+        eq[e] = exp2_hw(fmaf(zq[e], A.lg, -rq));
+      }
+      part[ww] = tv_wave(ep, eq, par.rho, par.swap);
+    }
+    const double sum = tv_chunk(part);  // the owners' parts, combined as the finaliser combines them
+    if (lane == src) {
+#pragma unroll
+      for (int i = 0; i < kSlots; ++i)
+        if (lane * kSlots + i == c) tva[i] = sum;
+    }
+  }
+}
+
+template <bool BF16, bool GREEDY>
+__device__ RowOut finalize_row(const Args& A, int b, int j, int gam, const __amdgpu_buffer_rsrc_t& rs_recs) {
+  const int lane = threadIdx.x & 63;
+  const int row = b * (A.gmax + 1) + j;
+  const bool pair = j < gam;
+  RowRecs R;
+  load_recs(A, rs_recs, row, R);  // all present: the sweep launch has completed
+  RowOut o;
+  o.pad = 0;
+  o.argp = -1;
+  const int x = pair ? A.drafts[(size_t)b * A.gmax + j] : -1;
+  const bool xin = x >= 0 && x < A.V;
+  const float nan = __builtin_nanf("");
+  if constexpr (GREEDY) {
+    float mp = kNegInf, mq = kNegInf;
+#pragma unroll
+    for (int i = 0; i < kSlots; ++i) {
+      mp = fmaxf(mp, R.rp[i]);
+      mq = fmaxf(mq, R.rq[i]);
+    }
+    mp = wave_max(mp);
+    mq = wave_max(mq);
+    int ap = INT_MAX, aq = INT_MAX;
+#pragma unroll
+    for (int i = 0; i < kSlots; ++i) {
+      const bool in = lane * kSlots + i < A.nc;
+      if (in && R.rp[i] == mp) ap = min(ap, (int)R.sp[i]);
+      if (in && R.rq[i] == mq) aq = min(aq, (int)R.sq[i]);
+    }
+    ap = wave_min_i(ap);
+    aq = wave_min_i(aq);
+    o.argp = ap;
+    const float hp = x == ap ? 1.f : 0.f, hq = x == aq ? 1.f : 0.f;
+    o.a = pair ? (double)hp : 0.0;
+    o.p_tok = pair ? hp : nan;
+    o.q_tok = pair ? hq : nan;
+    o.kl = pair ? (ap == aq ? 0.f : __builtin_inff()) : nan;
+    o.tv = pair ? (ap == aq ? 0.f : 1.f) : nan;
+  } else {
+    const Norm np = merge_norm(R.rp, R.sp);
+    o.a = 0.0;
+    o.p_tok = o.q_tok = o.kl = o.tv = nan;
+    if (pair) {
+      const Norm nq = merge_norm(R.rq, R.sq);
+      double tva[kSlots];
+#pragma unroll
+      for (int i = 0; i < kSlots; ++i) tva[i] = load_tv_chunk(A, row, lane * kSlots + i);
+      redo_skipped<BF16>(A, b, j, R, np, nq, tva);
+      // TV = 1/2 sum_c scale_c tva_c;
+      // KL = sum_c f_c (ln2 kl_c + ln2 s_c d_c) - ln(S_p / S_q) sum_c f_c s_c with
+      // d_c = (r_c - r_max) - (r'_c - r'_max) (integers): the log-ratio of an
+      // entry is ln2 (x_p - x_q) + ln2 d_c - ln(S_p / S_q)
+      double tvs = 0.0, klt = 0.0, mass = 0.0;
+#pragma unroll
+      for (int i = 0; i < kSlots; ++i) {
+        const double fp = factor(R.rp[i], np), fq = factor(R.rq[i], nq);
+        tvs += tv_par(fp, fq).scale * tva[i];
+        if (fp > 0.0) {
+          const double d = ((double)R.rp[i] - (double)np.rM) - ((double)R.rq[i] - (double)nq.rM);
+          klt += fp * (kLn2 * R.kl[i] + kLn2 * d * R.sp[i]);
+          mass += fp * R.sp[i];
+        }
+      }
+      const double tv = 0.5 * wave_sum_d(tvs);
+      const double kl = wave_sum_d(klt) - log(np.S / nq.S) * wave_sum_d(mass);
+      // p(x), q(x) as the kernel's own entries 2^x 2^(r_c - r_max) / S (the
+      // exponentials the sums were built from), a = min(1, p(x)/q(x))
+      double px = __builtin_nan(""), qx = __builtin_nan("");
+      if (xin) {
+        const float* xs = A.xlogit + (size_t)row * 4;
+        const float xp = ld_dev(xs), rpx = ld_dev(xs + 1), xq = ld_dev(xs + 2), rqx = ld_dev(xs + 3);
+        px = (double)exp2_hw(xp) * pow2(rpx, np.rM) / np.S;
+        qx = (double)exp2_hw(xq) * pow2(rqx, nq.rM) / nq.S;
+      }
+      o.a = !xin ? __builtin_nan("") : (qx == 0.0 || px >= qx) ? 1.0 : px / qx;
+      o.p_tok = xin ? (float)px : nan;
+      o.q_tok = xin ? (float)qx : nan;
+      o.kl = (float)kl;
+      o.tv = (float)tv;
+    }
+  }
+  return o;
+}
+
+// ---------------------------------------------------------------------------
+// Sequence finisher (one wave)
+
+// Wave-wide inclusive prefix sum (fp64) in ascending lane order.
+__device__ __forceinline__ double wave_incl_scan_d(double x) {
   x = x + dpp_f64<0x111>(x);  // row_shr:1 (lanes without a source read 0)
   x = x + dpp_f64<0x112>(x);  // row_shr:2
   x = x + dpp_f64<0x114>(x);  // row_shr:4
@@ -810,405 +1044,346 @@ __device__ __forceinline__ double wave_incl_scan(double x) {
   return x + (row == 0 ? 0.0 : row == 1 ? r0 : row == 2 ? r01 : r01 + r2);
 }
 
-struct RowRes {
-  double a;
-  float p_tok, q_tok, kl, tv;
-};
-
-// A row's chunk records, lane-wise (chunk lane*nslot + i in slot i).
-struct RowRecs {
-  float mp[kSlots], mq[kSlots];
-  double sp[kSlots], sq[kSlots], kl[kSlots], ta[kSlots];
-};
-
-__device__ __forceinline__ void load_row(const Args& A, int row, bool pair, RowRecs& R) {
+// The token drawn from row k of sequence b: from the residual max(0, p_k - q_k)
+// if k < gamma and it has mass, else from p_k; the smallest x with
+// C(x) > u W in ascending vocabulary order (the last entry with weight if
+// rounding leaves none). The chunk holding u W is found from the chunk
+// masses, then scanned in four passes of 1024 entries (16 consecutive entries
+// per lane), its weights computed exactly as in the sweep.
+template <bool BF16>
+__device__ int draw_token(const Args& A, int b, int k, int gam, float u, const __amdgpu_buffer_rsrc_t& rs_recs) {
+  constexpr int N = Vec<BF16>::N, esz = Vec<BF16>::esz, kE = Vec<BF16>::E;
+  constexpr int kChunk = Vec<BF16>::kChunk, kWaveSpan = Vec<BF16>::kWaveSpan;
   const int lane = threadIdx.x & 63;
-  const int nslot = (A.nc + 63) / 64;
+  const int row = b * (A.gmax + 1) + k;
+  const bool pair = k < gam;
+  RowRecs R;
+  load_recs(A, rs_recs, row, R);
+  const Norm np = merge_norm(R.rp, R.sp);
+  const Norm nq = pair ? merge_norm(R.rq, R.sq) : Norm{kNegInf, 0.0};
+  double mres[kSlots], mp[kSlots];
+  double my_res = 0.0;
 #pragma unroll
   for (int i = 0; i < kSlots; ++i) {
-    const int cc = lane * nslot + i;
-    const bool in = i < nslot && cc < A.nc;
-    const StatRec r = in ? unpack_rec(A.stats[((size_t)row * A.nc + cc) * 2], A.stats[((size_t)row * A.nc + cc) * 2 + 1])
-                         : StatRec{kNegInf, kNegInf, 0.0, 0.0, 0.0};
-    R.mp[i] = r.mp;
-    R.sp[i] = r.sp;
-    R.mq[i] = pair ? r.mq : kNegInf;
-    R.sq[i] = pair ? r.sq : 0.0;
-    R.kl[i] = pair ? r.kl : 0.0;
-    R.ta[i] = in && pair ? A.tvabs[(size_t)row * A.nc + cc] : 0.0;
+    const int c = lane * kSlots + i;
+    const double fp = factor(R.rp[i], np);
+    mp[i] = fp * R.sp[i];
+    mres[i] = 0.0;
+    if (pair && c < A.nc) {
+      const double fq = factor(R.rq[i], nq);
+      const double t = load_tv_chunk(A, row, c);
+      mres[i] = fmax(0.0, 0.5 * (tv_par(fp, fq).scale * t + mp[i] - fq * R.sq[i]));
+    }
+    my_res += mres[i];
   }
+  const bool resid = pair && wave_sum_d(my_res) > 0.0;
+  double m[kSlots], my = 0.0;
+  int my_last = -1;
+#pragma unroll
+  for (int i = 0; i < kSlots; ++i) {
+    m[i] = resid ? mres[i] : mp[i];
+    my += m[i];
+    if (m[i] > 0.0) my_last = lane * kSlots + i;
+  }
+  const double incl = wave_incl_scan_d(my);
+  const double W = lane_value(incl, 63);
+  const double target = (double)u * W;
+  // the first chunk with weight whose end exceeds the target
+  int c = -1;
+  double pre = 0.0;
+  const unsigned long long hit = __ballot(incl > target && my > 0.0);
+  if (hit) {
+    const int hl = __ffsll((long long)hit) - 1;
+    double run = incl - my;
+    int found = -1;
+    double fpre = 0.0;
+#pragma unroll
+    for (int i = 0; i < kSlots; ++i) {
+      if (found < 0 && m[i] > 0.0 && run + m[i] > target) {
+        found = lane * kSlots + i;
+        fpre = run;
+      }
+      run += m[i];
+    }
+    c = lane_value(found, hl);
+    pre = lane_value(fpre, hl);
+  } else {  // rounding put the target at the very end: the last chunk with weight
+    c = max(wave_max_i(my_last), 0);
+    double before = 0.0;
+#pragma unroll
+    for (int i = 0; i < kSlots; ++i)
+      if (lane * kSlots + i < c) before += m[i];
+    pre = wave_sum_d(before);
+  }
+  const double rem = target - pre;
+  // that chunk's shifts and factors, as the sweep used them
+  float rpc, rqc;
+  chunk_shifts(R, c, rpc, rqc);
+  const double fp = factor(rpc, np);
+  const TvPar par = tv_par(fp, resid ? factor(rqc, nq) : 0.0);
+  const double scale = resid ? par.scale : fp;
+  const float rp = rpc == kNegInf ? 0.f : rpc, rq = rqc == kNegInf ? 0.f : rqc;
+  const RowSpan s = row_span<BF16>(A, b, k, resid);
+  const float tp = A.thr ? A.thr[(size_t)row * 2] : kNegInf;
+  const float tq = A.thr && resid ? A.thr[(size_t)row * 2 + 1] : kNegInf;
+  double carry = 0.0;
+  int tok = -1, last = -1;
+  for (int pass = 0; pass < kWaves && tok < 0; ++pass) {
+    const int pos0 = c * kChunk + pass * kWaveSpan + lane * kE;
+    Loaded<BF16> lp, lq;
+#pragma unroll
+    for (int i = 0; i < kE / N; ++i) {
+      const uint32_t off = (uint32_t)((pos0 + i * N) * esz);
+      lp.v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(s.rp, off, 0, 0));
+      lq.v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(s.rq, off, 0, 0));
+    }
+    float zp[kE], zq[kE], wt[kE];
+    widen<BF16>(lp, zp);
+    widen<BF16>(lq, zq);
+    double sum = 0.0;
+    int mine = -1;
+#pragma unroll
+    for (int e = 0; e < kE; ++e) {
+      const int i = pos0 + e - s.phi;
+      const bool in = i >= 0 && i < A.V;
+      const float vp = in && zp[e] >= tp ? zp[e] : kNegInf;
+      const float vq = in && zq[e] >= tq ? zq[e] : kNegInf;
+      const float ep = exp2_hw(fmaf(vp, A.lg, -rp));
+      float wv;
+      if (resid) {
+        const float eq = exp2_hw(fmaf(vq, A.lg, -rq));
+        const float d = par.swap ? -fmaf(eq, par.rho, -ep) : fmaf(ep, par.rho, -eq);
+        wv = fmaxf(d, 0.f);
+      } else {
+        wv = ep;
+      }
+      wt[e] = wv;
+      sum += (double)wv;
+      if (wv > 0.f) mine = i;
+    }
+    sum *= scale;
+    last = max(last, wave_max_i(mine));
+    const double sincl = carry + wave_incl_scan_d(sum);
+    const unsigned long long h = __ballot(sincl > rem && sum > 0.0);
+    if (h) {
+      const int hl = __ffsll((long long)h) - 1;
+      double run = sincl - sum;
+      int found = -1;
+      for (int e = 0; e < kE; ++e) {
+        run += (double)wt[e] * scale;
+        if (found < 0 && wt[e] > 0.f && run > rem) found = pos0 + e - s.phi;
+      }
+      tok = __builtin_amdgcn_readlane(found >= 0 ? found : mine, hl);
+    }
+    carry = lane_value(sincl, 63);
+  }
+  if (tok < 0) tok = last < 0 ? 0 : last;  // the target lies past the chunk's total (rounding)
+  return tok;
 }
 
-// What the accept chain and the draw need of one row, kept in LDS by the
-// wave that merged the row: the chunks' masses (p, and the residual
-// max(0, p - q) for a pair row) and maxima, and the row's normalisers.
-struct FinishShared {
-  double mass[kMaxRows][2][kMaxChunks];  // [row][p, residual][chunk]
-  float cmax[kMaxRows][2][kMaxChunks];   // [row][p, q][chunk] chunk maxima
-  float norm[kMaxRows][4];               // M_p, 1/S_p, M_q, 1/S_q
-  int resid[kMaxRows];                   // the residual has positive mass
-  RowRes rr[kMaxRows];
-  int x[kMaxRows];
-  float uacc[kMaxRows], ures[kMaxRows];
-};
-
-// Finish kernel: one workgroup per sequence with at least four waves.
-//   load:  every thread loads its position's draft and uniforms together
-//          with gamma (one round trip);
-//   rows:  one wave per live row j <= gamma merges the row's records (the
-//          draft token's two logits are loaded alongside) into a_j, p(x),
-//          q(x), TV_j and KL_j, and leaves the row's chunk masses, maxima
-//          and normalisers in LDS;
-//   chain: wave 0 finds the stopping row k and, from k's chunk masses, the
-//          chunk that holds u*W and the offset of u*W inside it;
-//   draw:  waves 0-3 re-read that chunk (each thread a contiguous run of
-//          entries), weigh it exactly as the sweep did, and a block-wide
-//          prefix scan in ascending vocabulary order finds the token.
-template <bool BF16, int E>
-__global__ void __launch_bounds__(1024)
-accept_finish_kernel(Args A) {
-  constexpr int VEC = Elt<BF16>::VEC;
-  constexpr int kChunk = kThreads * E;
-  __shared__ FinishShared F;
-  __shared__ uint32_t s_bad;
-  __shared__ int s_k, s_cs, s_resid, s_hit[4], s_last[4], s_tok;
-  __shared__ double s_rem, s_wt[4];
-  __shared__ float s_fac[4];  // rp, rq, fp, fq of the draw chunk
-  const int b = blockIdx.x;
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int w = tid >> 6;
-  const int nw = blockDim.x >> 6;
+template <bool BF16, bool GREEDY>
+__device__ void finish_sequence(const Args& A, int b, int gam, const RowOut* rows,
+                                const __amdgpu_buffer_rsrc_t& rs_recs) {
+  const int lane = threadIdx.x & 63;
   const int G1 = A.gmax + 1;
-  const int nslot = (A.nc + 63) / 64;
-  // ---- load: gamma and the per-position inputs in one round trip
-  const int gam = A.gamma[b];
-  if (tid == 0) s_bad = 0;
-  if (tid < G1) {
-    const int j = tid;
-    const int x = j < A.gmax ? A.drafts[(size_t)b * A.gmax + j] : -1;
-    const float ua = j < A.gmax ? A.u_acc[(size_t)b * A.gmax + j] : 0.f;
-    const float ur = A.u_res[(size_t)b * G1 + j];
-    F.x[j] = x;
-    F.uacc[j] = ua;
-    F.ures[j] = ur;
+  // per-position inputs (one round trip) and the row results (LDS)
+  int x = -1;
+  float ua = 0.f, ur = 0.f;
+  double a = 0.0;
+  int argp = -1;
+  float o_p = 0.f, o_q = 0.f, o_kl = 0.f, o_tv = 0.f;
+  if (lane <= gam) {
+    if (lane < gam) x = A.drafts[(size_t)b * A.gmax + lane];
+    if (!GREEDY) {
+      if (lane < gam) ua = A.u_acc[(size_t)b * A.gmax + lane];
+      ur = A.u_res[(size_t)b * G1 + lane];
+    }
+    const RowOut& ro = rows[lane];
+    a = ro.a;
+    o_p = ro.p_tok;
+    o_q = ro.q_tok;
+    o_kl = ro.kl;
+    o_tv = ro.tv;
+    argp = ro.argp;
   }
   const int kvl = A.kv_len ? A.kv_len[b] : 0;
   const int rb_old = A.rb_kv ? A.rb_kv[b] : 0;
-  // row w's records and draft logits, in the same round trip (pair or bonus
-  // row is decided once gamma has arrived)
-  RowRecs R0;
-  float zx0[2] = {0.f, 0.f};
-  if (w <= A.gmax) {
-    load_row(A, b * G1 + w, true, R0);
-    if (w < A.gmax) {
-      zx0[0] = A.xlogit[((size_t)b * G1 + w) * 2];
-      zx0[1] = A.xlogit[((size_t)b * G1 + w) * 2 + 1];
-    }
+  // data checks
+  uint32_t bad = 0;
+  if (lane < gam) {
+    if (x < 0 || x >= A.V) bad |= SR_ST_TOKEN;
+    if (!GREEDY && !(ua >= 0.f && ua < 1.f)) bad |= SR_ST_UNIFORM;
   }
-  if (gam < 0 || gam > A.gmax) {
-    if (w == 0) {
-      write_invalid(A, b, SR_ST_GAMMA);
-      finish_rollback(A, b, rb_old, kvl);
-    }
-    return;  // the sweep touched no row of this sequence
-  }
-  __syncthreads();
-  // ---- data checks
-  if (tid <= gam) {
-    uint32_t bad = 0;
-    const int j = tid;
-    if (j < gam) {
-      const int x = F.x[j];
-      if (x < 0 || x >= A.V) bad |= SR_ST_TOKEN;
-      const float u = F.uacc[j];
-      if (!(u >= 0.f && u < 1.f)) bad |= SR_ST_UNIFORM;
-    }
-    const float u = F.ures[j];
-    if (!(u >= 0.f && u < 1.f)) bad |= SR_ST_UNIFORM;
-    if (j == 0 && A.kv_len && kvl < gam + 1) bad |= SR_ST_KVLEN;
-    if (bad) atomicOr(&s_bad, bad);
-  }
-  // ---- rows (one wave per live row)
-  const size_t esz = BF16 ? 2 : 4;
-  for (int j = w; j <= gam; j += nw) {
-    const bool pair = j < gam;
-    const int x = pair ? F.x[j] : -1;
-    const bool xin = x >= 0 && x < A.V;
-    RowRecs R;
-    float zpx, zqx;
-    if (j == w) {
-      R = R0;
-      zpx = zx0[0];
-      zqx = zx0[1];
-    } else {  // a second row for this wave (gamma_max + 1 > waves)
-      load_row(A, b * G1 + j, true, R);
-      zpx = A.xlogit[((size_t)b * G1 + j) * 2];
-      zqx = A.xlogit[((size_t)b * G1 + j) * 2 + 1];
-    }
-    if (!pair) {  // the bonus row: p only
-#pragma unroll
-      for (int i = 0; i < kSlots; ++i) {
-        R.mq[i] = kNegInf;
-        R.sq[i] = 0.0;
-        R.kl[i] = 0.0;
-        R.ta[i] = 0.0;
-      }
-    }
-    const RowNorm np = row_norm(R.mp, R.sp, A.lg);
-    const RowNorm nq = row_norm(R.mq, R.sq, A.lg);
-    // chunk masses with the same factors the sweep's sum |P - Q| used
-    double my_res = 0.0;
-#pragma unroll
-    for (int i = 0; i < kSlots; ++i) {
-      const int cc = lane * nslot + i;
-      const double pm = R.sp[i] * (double)np.factor(R.mp[i]);
-      const double qm = R.sq[i] * (double)nq.factor(R.mq[i]);
-      const double rm = pair ? fmax(0.0, 0.5 * (R.ta[i] + pm - qm)) : 0.0;
-      my_res += rm;
-      if (i < nslot && cc < A.nc) {
-        F.mass[j][0][cc] = pm;
-        F.mass[j][1][cc] = rm;
-        F.cmax[j][0][cc] = R.mp[i];
-        F.cmax[j][1][cc] = R.mq[i];
-      }
-    }
-    const bool residual = pair && wave_sum_d(my_res) > 0.0;
-    if (lane == 0) {
-      F.norm[j][0] = np.M;
-      F.norm[j][1] = np.invS;
-      F.norm[j][2] = nq.M;
-      F.norm[j][3] = nq.invS;
-      F.resid[j] = residual ? 1 : 0;
-    }
-    if (!pair) continue;  // the bonus row needs no divergences
-    const double Lp = np.log_norm(A.inv_t), Lq = nq.log_norm(A.inv_t);
-    // KL = (1/T) sum_c f_c (kl_c + s_c ((m_c - M_p) - (m'_c - M_q))) - (ln S_p - ln S_q),
-    // kl_c being the chunk's numerator relative to its maxima m_c (p) and m'_c (q)
-    double tvd = 0.0, kld = 0.0;
-#pragma unroll
-    for (int i = 0; i < kSlots; ++i) {
-      tvd += R.ta[i];
-      if (R.mp[i] != kNegInf) {
-        const double dm = ((double)R.mp[i] - (double)np.M) - ((double)R.mq[i] - (double)nq.M);
-        kld += (double)np.factor(R.mp[i]) * (R.kl[i] + R.sp[i] * dm);
-      }
-    }
-    tvd = 0.5 * wave_sum_d(tvd);
-    kld = A.inv_t * wave_sum_d(kld) - (log(np.S) - log(nq.S));
-    // p(x), q(x) and a = min(1, p(x)/q(x)): one exponential per lane (0-2)
-    const double lpx = (double)zpx * A.inv_t - Lp;
-    const double lqx = (double)zqx * A.inv_t - Lq;
-    const double arg = lane == 0 ? lpx : (lane == 1 ? lqx : lpx - lqx);
-    const double ex = exp(arg);
-    const double pt = lane_value(ex, 0), qt = lane_value(ex, 1), rt = lane_value(ex, 2);
-    if (lane == 0) {
-      double a = __builtin_nan("");
-      if (xin) a = (lqx == -INFINITY || lpx >= lqx) ? 1.0 : rt;
-      F.rr[j] = RowRes{a, xin ? (float)pt : __builtin_nanf(""), xin ? (float)qt : __builtin_nanf(""), (float)kld,
-                       (float)tvd};
-    }
-  }
-  __syncthreads();
-  if (s_bad) {
-    if (w == 0) {
-      clear_records(A, b, gam);  // every wave has finished reading them
-      write_invalid(A, b, s_bad);
-      finish_rollback(A, b, rb_old, kvl);
-    }
+  if (!GREEDY && lane <= gam && !(ur >= 0.f && ur < 1.f)) bad |= SR_ST_UNIFORM;
+  if (lane == 0 && A.kv_len && kvl < gam + 1) bad |= SR_ST_KVLEN;
+  uint32_t bits = 0;
+  if (__ballot(bad & SR_ST_TOKEN)) bits |= SR_ST_TOKEN;
+  if (__ballot(bad & SR_ST_UNIFORM)) bits |= SR_ST_UNIFORM;
+  if (__ballot(bad & SR_ST_KVLEN)) bits |= SR_ST_KVLEN;
+  if (bits) {
+    write_invalid(A, b, bits);
+    finish_rollback(A, b, rb_old, kvl);
+    clear_sequence(A, b, gam);
+    count_finished(A, 1);
     return;
   }
-  // ---- accept chain and the chunk of the draw (wave 0)
-  if (w == 0) {
-    bool rej = false;
-    if (lane < gam) rej = !((double)F.uacc[lane] < F.rr[lane].a);
-    const unsigned long long rmask = __ballot(rej);
-    const int k = rmask ? (__ffsll((long long)rmask) - 1) : gam;
-    const bool residual = F.resid[k] != 0;
-    double mass[kSlots];
-    double my = 0.0;
-    int my_last = -1;
-#pragma unroll
-    for (int i = 0; i < kSlots; ++i) {
-      const int cc = lane * nslot + i;
-      const bool in = i < nslot && cc < A.nc;
-      mass[i] = in ? F.mass[k][residual ? 1 : 0][cc] : 0.0;
-      my += mass[i];
-      if (mass[i] > 0.0) my_last = cc;
-    }
-    const double incl = wave_incl_scan(my);
-    const double W = lane_value(incl, 63);
-    const double target = (double)F.ures[k] * W;
-    // the first chunk with positive mass whose end exceeds the target
-    int cs = -1;
-    double pre = 0.0;
-    const unsigned long long hit = __ballot(incl > target && my > 0.0);
-    if (hit) {
-      const int hl = __ffsll((long long)hit) - 1;
-      double run = incl - my;
-      int found = -1;
-      double fpre = 0.0;
-#pragma unroll
-      for (int i = 0; i < kSlots; ++i) {
-        if (found < 0 && mass[i] > 0.0 && run + mass[i] > target) {
-          found = lane * nslot + i;
-          fpre = run;
-        }
-        run += mass[i];
-      }
-      cs = lane_value(found, hl);
-      pre = lane_value(fpre, hl);
-    }
-    if (cs < 0) {  // rounding put the target at the very end: the last chunk with mass
-      cs = max(wave_max_i(my_last), 0);
-      double before = 0.0;
-#pragma unroll
-      for (int i = 0; i < kSlots; ++i)
-        if (lane * nslot + i < cs) before += mass[i];
-      pre = wave_sum_d(before);
-    }
-    if (lane == 0) {
-      // the chunk's maxima and factors, as the sweep used them
-      const bool pair = k < gam;
-      const float cmp = F.cmax[k][0][cs];
-      const float cmq = pair ? F.cmax[k][1][cs] : kNegInf;
-      RowNorm np, nq;
-      np.M = F.norm[k][0];
-      np.invS = F.norm[k][1];
-      np.lg = A.lg;
-      nq.M = pair ? F.norm[k][2] : kNegInf;
-      nq.invS = pair ? F.norm[k][3] : 0.f;
-      nq.lg = A.lg;
-      s_k = k;
-      s_cs = cs;
-      s_resid = residual ? 1 : 0;
-      s_rem = target - pre;
-      s_fac[0] = cmp == kNegInf ? 0.f : cmp * A.lg;
-      s_fac[1] = cmq == kNegInf ? 0.f : cmq * A.lg;
-      s_fac[2] = np.factor(cmp);
-      s_fac[3] = nq.factor(cmq);
-    }
+  // the accept chain
+  const bool rej = lane < gam && (GREEDY ? x != argp : !((double)ua < a));
+  const unsigned long long rmask = __ballot(rej);
+  const int k = rmask ? (__ffsll((long long)rmask) - 1) : gam;
+  int tok;
+  if constexpr (GREEDY) {
+    tok = __builtin_amdgcn_readlane(argp, k);
+  } else {
+    tok = draw_token<BF16>(A, b, k, gam, lane_float(ur, k), rs_recs);
   }
-  __syncthreads();
-  // ---- the draw: waves 0-3 scan chunk cs in ascending vocabulary order, in
-  // passes of 4096 entries (thread t of a pass holds 16 consecutive entries);
-  // every wave reaches every barrier, only waves 0-3 work between them
-  const int k = s_k;
-  {
-    constexpr int kPerT = 16;
-    constexpr int kPass = 256 * kPerT;
-    const bool residual = s_resid != 0;
-    const float rp = s_fac[0], rq = s_fac[1], fp = s_fac[2], fq = s_fac[3];
-    const bool filt = A.thr != nullptr;
-    const float thr_p = filt ? A.thr[((size_t)b * G1 + k) * 2] : kNegInf;
-    const float thr_q = filt && k < gam ? A.thr[((size_t)b * G1 + k) * 2 + 1] : kNegInf;
-    const char* prow = (const char*)A.p + ((size_t)b * A.p_stride + (size_t)k * A.V) * esz;
-    const char* qrow = (const char*)A.q + ((size_t)b * A.q_stride + (size_t)k * A.V) * esz;
-    const double rem0 = s_rem;
-    double carry = 0.0;  // mass of the earlier passes
-    int last_tok = -1;
-    if (tid == 0) s_tok = -1;
-    for (int pass = 0; pass < kChunk / kPass; ++pass) {
-      float wt[kPerT];
-      double sum = 0.0, incl = 0.0;
-      int mine = -1;
-      const int x0 = s_cs * kChunk + pass * kPass + tid * kPerT;
-      if (w < 4) {
-        float zp[kPerT], zq[kPerT];
-#pragma unroll
-        for (int v = 0; v < kPerT / VEC; ++v) Elt<BF16>::load(prow, min(x0 + v * VEC, A.V - VEC), zp + v * VEC);
-        if (residual) {
-#pragma unroll
-          for (int v = 0; v < kPerT / VEC; ++v) Elt<BF16>::load(qrow, min(x0 + v * VEC, A.V - VEC), zq + v * VEC);
-        }
-        if (filt) {  // the same top-k / top-p filter the sweep applied
-#pragma unroll
-          for (int e = 0; e < kPerT; ++e) {
-            zp[e] = zp[e] >= thr_p ? zp[e] : kNegInf;
-            zq[e] = zq[e] >= thr_q ? zq[e] : kNegInf;
-          }
-        }
-#pragma unroll
-        for (int e = 0; e < kPerT; ++e) {
-          float wv = 0.f;
-          if (x0 + e < A.V) {
-#pragma clang fp contract(off)
-            const float ep = exp2_hw(fmaf(zp[e], A.lg, -rp));
-            if (residual) {
-              const float eq = exp2_hw(fmaf(zq[e], A.lg, -rq));
-              wv = fmaxf(ep * fp - eq * fq, 0.f);
-            } else {
-              wv = ep * fp;
-            }
-          }
-          wt[e] = wv;
-          sum += (double)wv;
-          if (wv > 0.f) mine = x0 + e;
-        }
-        incl = wave_incl_scan(sum);
-        const int lmax = wave_max_i(mine);
-        if (lane == 63) s_wt[w] = incl;
-        if (lane == 0) s_last[w] = lmax;
-      }
-      __syncthreads();
-      const double total = ((s_wt[0] + s_wt[1]) + s_wt[2]) + s_wt[3];
-      const double rem = rem0 - carry;
-      for (int i = 0; i < 4; ++i) last_tok = max(last_tok, s_last[i]);
-      const bool here = rem < total;  // workgroup-uniform
-      if (here && w < 4) {
-        double excl_w = 0.0;
-        for (int i = 0; i < w; ++i) excl_w += s_wt[i];
-        incl += excl_w;
-        const unsigned long long h = __ballot(incl > rem && sum > 0.0);
-        if (lane == 0) s_hit[w] = h ? __ffsll((long long)h) - 1 : -1;
-      }
-      __syncthreads();
-      if (here) {
-        if (w < 4) {
-          int hw = -1;
-          for (int i = 0; i < 4; ++i)
-            if (hw < 0 && s_hit[i] >= 0) hw = i;
-          if (hw == w && lane == s_hit[w]) {
-            double run = incl - sum;
-            int found = -1;
-#pragma unroll
-            for (int e = 0; e < kPerT; ++e) {
-              run += (double)wt[e];
-              if (found < 0 && wt[e] > 0.f && run > rem) found = x0 + e;
-            }
-            s_tok = found >= 0 ? found : mine;
-          }
-          if (hw < 0 && tid == 0) s_tok = last_tok < 0 ? 0 : last_tok;  // rounding: the pass's last positive entry
-        }
-        break;  // workgroup-uniform
-      }
-      carry += total;
-    }
-    __syncthreads();
-    if (tid == 0 && s_tok < 0) s_tok = last_tok < 0 ? 0 : last_tok;  // the target lies past the chunk's total
-  }
-  __syncthreads();
-  if (w != 0) return;
-  const int tok = s_tok;
-  clear_records(A, b, gam);  // every read of them is done
-  // ---- outputs
+  // outputs
   int32_t* ot = A.out_tokens + (size_t)b * G1;
-  for (int j = lane; j <= A.gmax; j += 64) ot[j] = j < k ? F.x[j] : (j == k ? tok : -1);
+  if (lane <= A.gmax) ot[lane] = lane < k ? x : (lane == k ? tok : -1);
   const float nan = __builtin_nanf("");
-  for (int j = lane; j < A.gmax; j += 64) {
-    const size_t o = (size_t)b * A.gmax + j;
-    const bool live = j < gam;
-    if (A.accept_prob) A.accept_prob[o] = live ? (float)F.rr[j].a : nan;
-    if (A.p_tok) A.p_tok[o] = live ? F.rr[j].p_tok : nan;
-    if (A.q_tok) A.q_tok[o] = live ? F.rr[j].q_tok : nan;
-    if (A.kl) A.kl[o] = live ? F.rr[j].kl : nan;
-    if (A.tv) A.tv[o] = live ? F.rr[j].tv : nan;
+  if (lane < A.gmax) {
+    const size_t o = (size_t)b * A.gmax + lane;
+    const bool live = lane < gam;
+    if (A.accept_prob) A.accept_prob[o] = live ? (float)a : nan;
+    if (A.p_tok) A.p_tok[o] = live ? o_p : nan;
+    if (A.q_tok) A.q_tok[o] = live ? o_q : nan;
+    if (A.kl) A.kl[o] = live ? o_kl : nan;
+    if (A.tv) A.tv[o] = live ? o_tv : nan;
   }
   if (lane == 0) {
     A.accept_len[b] = k;
     if (A.new_len) A.new_len[b] = kvl - gam + k;
   }
   finish_rollback(A, b, rb_old, kvl - gam + k);
+  clear_sequence(A, b, gam);
+  count_finished(A, 1);
+}
+
+// Sequences whose gamma is out of range have no rows: workgroup 0 writes
+// their invalid outputs and rollbacks first (all its threads, one sequence
+// per wave at a time).
+// ---------------------------------------------------------------------------
+// The launches
+
+// One step of the sweep, task k (cur): wave 0 issues the loads of the previous
+// task's row records (they are ahead of the prefetch in its queue, so they
+// return during this task's first pass); every wave issues the next task's
+// loads; the first pass of task k; then the previous task's TV sum, with its
+// exponentials kept in registers. Returns whether a next task exists.
+template <bool BF16, bool GREEDY>
+__device__ __forceinline__ bool sweep_step(const Args& A, const int* s_rows, long n_tasks, int n_my, int k,
+                                           TaskTable& tab, TaskShared& sh, const __amdgpu_buffer_rsrc_t& rs_recs,
+                                           const TaskInfo& cur, const Loaded<BF16>& lp, const Loaded<BF16>& lq,
+                                           float (&ep)[Vec<BF16>::E], float (&eq)[Vec<BF16>::E], TaskInfo prev,
+                                           bool has_prev, const float (&pp)[Vec<BF16>::E],
+                                           const float (&pq)[Vec<BF16>::E], TaskInfo& nxt, Loaded<BF16>& np_,
+                                           Loaded<BF16>& nq_) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const bool tv = !GREEDY && has_prev && prev.pair;  // workgroup-uniform
+  // The poll and the merge of the records go to wave k mod 4, so that every
+  // SIMD gets its share of that work.
+  const bool poller = w == (k & (kWaves - 1));
+  RecWords W;
+  if (tv && poller) issue_recs(A, rs_recs, prev.row, W);
+  // The table is refilled when the next task starts a new window (every read
+  // of the old window came before the previous task's barriers); past the
+  // end the prefetch reads through an empty resource.
+  const bool more = k + 1 < n_my;
+  if (more && (k + 1) % kTab == 0) fill_tasks(A, s_rows, n_tasks, k + 1, tab);
+  nxt = decode_task<BF16>(A, tab, more ? k + 1 : k);
+  issue_loads<BF16>(A, nxt, np_, nq_, more);
+  if constexpr (GREEDY) argmax_pass<BF16>(A, cur, lp, lq, sh, rs_recs);
+  else first_pass<BF16>(A, cur, lp, lq, ep, eq, sh, rs_recs);
+  if (tv) {
+    if (poller) poll_row(A, rs_recs, prev, W, sh);
+    __syncthreads();
+    const double part = sh.ok ? tv_wave(pp, pq, sh.rho, sh.swap != 0) : kSkipped;
+    if (lane == 0)
+      __hip_atomic_store(A.tva + ((size_t)prev.row * A.nc + prev.c) * kWaves + w, part, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+  }
+  return more;
+}
+
+// The TV sum of the last task (nothing left to overlap its poll with).
+template <bool BF16>
+__device__ __forceinline__ void sweep_last_tv(const Args& A, TaskShared& sh, const __amdgpu_buffer_rsrc_t& rs_recs,
+                                              const TaskInfo& prev, const float (&pp)[Vec<BF16>::E],
+                                              const float (&pq)[Vec<BF16>::E]) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (!prev.pair) return;
+  if (w == 0) {
+    RecWords W;
+    issue_recs(A, rs_recs, prev.row, W);
+    poll_row(A, rs_recs, prev, W, sh);
+  }
+  __syncthreads();
+  const double part = sh.ok ? tv_wave(pp, pq, sh.rho, sh.swap != 0) : kSkipped;
+  if (lane == 0)
+    __hip_atomic_store(A.tva + ((size_t)prev.row * A.nc + prev.c) * kWaves + w, part, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Sweep: workgroup g takes tasks g, g + G, g + 2G, ... (G the grid size),
+// loading one task ahead and finishing each pair task's TV sum during the next
+// task. The loop body is unrolled twice so that the two sets of loaded vectors
+// and of exponentials swap roles without copies.
+template <bool BF16, bool GREEDY>
+__global__ void __launch_bounds__(kThreads, 2) accept_kernel(Args A) {
+  constexpr int E = Vec<BF16>::E;
+  extern __shared__ int s_rows[];  // [B] inclusive prefix of live rows
+  __shared__ TaskShared sh;
+  __shared__ TaskTable tab;
+  build_row_table(A.gamma, A.gmax, A.B, s_rows);
+  const long n_tasks = (long)s_rows[A.B - 1] * A.nc;
+  if (blockIdx.x >= n_tasks) return;
+  const int n_my = (int)((n_tasks - blockIdx.x + gridDim.x - 1) / gridDim.x);  // this workgroup's tasks
+  const __amdgpu_buffer_rsrc_t rs_recs = make_rsrc(A.recs, (size_t)A.B * (A.gmax + 1) * A.nc * kRecBytes);
+  fill_tasks(A, s_rows, n_tasks, 0, tab);
+  TaskInfo ta = decode_task<BF16>(A, tab, 0), tb = ta;
+  Loaded<BF16> pa, qa, pb, qb;
+  issue_loads<BF16>(A, ta, pa, qa);
+  float epa[E], eqa[E], epb[E], eqb[E];
+  bool has_prev = false;
+  for (int k = 0;; k += 2) {
+    if (!sweep_step<BF16, GREEDY>(A, s_rows, n_tasks, n_my, k, tab, sh, rs_recs, ta, pa, qa, epa, eqa, tb, has_prev,
+                                  epb, eqb, tb, pb, qb)) {
+      if (!GREEDY) sweep_last_tv<BF16>(A, sh, rs_recs, ta, epa, eqa);
+      break;
+    }
+    has_prev = true;
+    if (!sweep_step<BF16, GREEDY>(A, s_rows, n_tasks, n_my, k + 1, tab, sh, rs_recs, tb, pb, qb, epb, eqb, ta, true,
+                                  epa, eqa, ta, pa, qa)) {
+      if (!GREEDY) sweep_last_tv<BF16>(A, sh, rs_recs, tb, epb, eqb);
+      break;
+    }
+  }
+}
+
+// Finish: one workgroup per sequence, after the sweep. Its waves finalise the
+// sequence's rows (wave w takes rows w, w + 4, ...) into LDS; wave 0 then runs
+// the accept chain, the draw, the outputs, the rollback and the record reset.
+// A sequence with gamma outside [0, gamma_max] gets the invalid outputs.
+template <bool BF16, bool GREEDY>
+__global__ void __launch_bounds__(kThreads) accept_finish_kernel(Args A) {
+  __shared__ RowOut s_out[kMaxRows];
+  const int b = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int gam = A.gamma[b];
+  if (!(gam >= 0 && gam <= A.gmax)) {
+    if (w == 0) {
+      write_invalid(A, b, SR_ST_GAMMA);
+      finish_rollback(A, b, A.rb_kv ? A.rb_kv[b] : 0, A.kv_len ? A.kv_len[b] : 0);
+      count_finished(A, 1);
+    }
+    return;
+  }
+  const __amdgpu_buffer_rsrc_t rs_recs = make_rsrc(A.recs, (size_t)A.B * (A.gmax + 1) * A.nc * kRecBytes);
+  for (int j = w; j <= gam; j += kWaves) {
+    const RowOut o = finalize_row<BF16, GREEDY>(A, b, j, gam, rs_recs);
+    if (lane == 0) s_out[j] = o;
+  }
+  __syncthreads();
+  if (w == 0) finish_sequence<BF16, GREEDY>(A, b, gam, s_out, rs_recs);
 }
 
 // ============================================================================
@@ -1225,25 +1400,30 @@ accept_finish_kernel(Args A) {
 // the waves:
 //   top-k: counts; the bin holding the k-th largest key is the one where the
 //     count of larger keys first reaches k;
-//   top-p: masses 2^((z - M) log2(e)/T) (fp32 terms, fp64 sums) over the keys
-//     top-k kept; the bin of the smallest kept logit is the lowest non-empty
-//     bin whose mass above (the larger bins plus the mass above the prefix)
-//     is below p times the total.
-// The first level reads the row from memory. When the selected bin (or, with
-// top-p to follow, the bin and every key above it) holds at most kFiltCap
-// keys, one more read gathers those keys into LDS and the remaining levels
-// (and the whole of top-p after top-k) run on them there; otherwise every
-// level reads the row again. Under top-p alone one read before the first
-// level finds the row maximum M. The threshold t (a logit value; entries
-// below it are removed) goes to thr[b][j][p or q]. Keys are exact, so top-k
-// matches the exact rule; top-p decides on fp32 masses, so it may differ from
-// exact arithmetic only when the mass above a logit is within ~1e-7 of p.
+//   top-p: masses over the keys top-k kept; the bin of the smallest kept logit
+//     is the lowest non-empty bin whose mass above (the larger bins plus the
+//     mass above the prefix) is below p times the total.
+// Masses are accumulated as 64-bit fixed-point integers (each term rounded to
+// 2^-40), so the sums do not depend on the order of the LDS atomics and every
+// call decides the same way. The first level reads the row once: counts, the
+// row maximum M and, for top-p, each bin's mass relative to the largest value
+// the bin can hold (terms 2^((z - top of bin) log2(e)/T) <= 1, rescaled to M
+// afterwards, so no earlier pass for M is needed). When the selected bin (or,
+// with top-p to follow, the bin and every key above it) holds at most kFiltCap
+// keys, a second read gathers them into LDS and the remaining levels (and the
+// whole of top-p after top-k) run there: a row is read twice. A row whose
+// logits crowd into one bin is read again at each further level. The
+// threshold t (a logit value; entries below it are removed) goes to
+// thr[b][j][p or q]. Keys are exact, so top-k matches the exact rule; top-p
+// decides on masses with ~1e-7 relative error, so a logit whose larger mass is
+// within about that of p may fall either way.
 
 constexpr int kFiltThreads = 1024;
 constexpr int kFiltWaves = kFiltThreads / 64;
 constexpr int kFiltBins = 4096;  // the widest digit: 12 bits
 constexpr int kFiltCap = 8064;   // candidate keys held in LDS (two workgroups fit a CU's 160 KB)
 constexpr int kFiltUnroll = 4;   // row loads in flight per thread
+constexpr double kFix = 1099511627776.0;  // 2^40: fixed-point scale of a mass term
 
 __device__ __forceinline__ uint32_t order_key(float z) {
   const uint32_t u = __float_as_uint(z + 0.f);  // -0 -> +0
@@ -1252,10 +1432,12 @@ __device__ __forceinline__ uint32_t order_key(float z) {
 __device__ __forceinline__ float key_value(uint32_t k) {
   return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
 }
+// round(t 2^40) for a term t in [0, 1]
+__device__ __forceinline__ uint64_t fixed_term(float t) { return (uint64_t)((double)t * kFix + 0.5); }
 
 struct FiltShared {
   uint32_t cnt[kFiltBins];
-  double mass[kFiltBins];
+  uint64_t mass[kFiltBins];  // fixed point
   uint32_t cand[kFiltCap];
   uint32_t wtot_u[kFiltWaves];
   double wtot_d[kFiltWaves];
@@ -1266,7 +1448,7 @@ struct FiltShared {
   uint32_t nge;    // top-k: keys in the selected bin and the bins above it
   uint32_t cpick;  // top-p: keys in the selected bin
   int lowest;      // top-p: the lowest qualifying bin
-  double above;    // top-p: mass above the selected prefix
+  double above;    // top-p: mass above the selected prefix (units of 2^(M lg))
   double total;    // top-p: mass of the keys top-k kept
 };
 
@@ -1292,7 +1474,7 @@ __device__ __forceinline__ uint32_t filt_excl_scan(FiltShared& F, uint32_t s) {
 }
 __device__ __forceinline__ double filt_excl_scan(FiltShared& F, double s, double& total) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const double incl = wave_incl_scan(s);
+  const double incl = wave_incl_scan_d(s);
   if (lane == 63) F.wtot_d[w] = incl;
   __syncthreads();
   double base = 0.0;
@@ -1304,36 +1486,73 @@ __device__ __forceinline__ double filt_excl_scan(FiltShared& F, double s, double
   return base + incl - s;
 }
 
-// Histogram pass over the row in memory: digit (key >> shift) & dmask of the
-// keys with (key & pmask) == prefix and key >= lo; kmax collects every key.
-template <bool BF16, bool MASS>
-__device__ void filt_hist_row(FiltShared& F, const char* row, int V, uint32_t prefix, uint32_t pmask, int shift,
-                              uint32_t dmask, uint32_t lo, float M, float lg, uint32_t& kmax) {
-  constexpr int VEC = Elt<BF16>::VEC;
-  constexpr int STEP = kFiltThreads * VEC;
-  for (int x0 = (int)threadIdx.x * VEC; x0 < V; x0 += STEP * kFiltUnroll) {
-    float z[kFiltUnroll][VEC];
+// A row in aligned 16-byte vectors: vector v holds entries v*N - phi .. v*N - phi + N - 1.
+template <bool BF16>
+struct FiltRow {
+  __amdgpu_buffer_rsrc_t rs;
+  int phi, V, nvec;
+  __device__ void load(int v, float (&z)[Vec<BF16>::N]) const {
+    constexpr int N = Vec<BF16>::N;
+    const u32x4 u = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, (uint32_t)v * 16u, 0, 0));
+    if constexpr (BF16) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        z[2 * k] = bf16_lo(u[k]);
+        z[2 * k + 1] = bf16_hi(u[k]);
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < N; ++k) z[k] = __uint_as_float(u[k]);
+    }
+  }
+  __device__ bool valid(int v, int k) const {
+    const int i = v * Vec<BF16>::N + k - phi;
+    return i >= 0 && i < V;
+  }
+};
+
+// Visits every entry of the row (f(z)) with kFiltUnroll vector loads in flight per thread.
+template <bool BF16, typename Fn>
+__device__ __forceinline__ void filt_scan_row(const FiltRow<BF16>& R, Fn&& f) {
+  constexpr int N = Vec<BF16>::N;
+  for (int v0 = (int)threadIdx.x; v0 < R.nvec; v0 += kFiltThreads * kFiltUnroll) {
+    float z[kFiltUnroll][N];
 #pragma unroll
     for (int u = 0; u < kFiltUnroll; ++u)
-      if (x0 + u * STEP < V) Elt<BF16>::load(row, x0 + u * STEP, z[u]);
+      if (v0 + u * kFiltThreads < R.nvec) R.load(v0 + u * kFiltThreads, z[u]);
 #pragma unroll
     for (int u = 0; u < kFiltUnroll; ++u) {
-      if (x0 + u * STEP >= V) break;
+      const int v = v0 + u * kFiltThreads;
+      if (v >= R.nvec) break;
 #pragma unroll
-      for (int i = 0; i < VEC; ++i) {
-        const uint32_t key = order_key(z[u][i]);
-        kmax = max(kmax, key);
-        if ((key & pmask) == prefix && key >= lo) {
-          const uint32_t d = (key >> shift) & dmask;
-          atomicAdd(&F.cnt[d], 1u);
-          if (MASS) atomicAdd(&F.mass[d], (double)exp2_hw((z[u][i] - M) * lg));
-        }
-      }
+      for (int k = 0; k < N; ++k)
+        if (R.valid(v, k)) f(z[u][k]);
     }
   }
 }
 
-// The same over the n candidate keys in LDS.
+// Histogram pass over the row in memory: digit (key >> shift) & dmask of the
+// keys with (key & pmask) == prefix and key >= lo; kmax collects every key.
+// Masses (MASS): relative to M (rel_bin false), or to the top of each
+// first-level bin (rel_bin true, prefix empty).
+template <bool BF16, bool MASS>
+__device__ void filt_hist_row(FiltShared& F, const FiltRow<BF16>& R, uint32_t prefix, uint32_t pmask, int shift,
+                              uint32_t dmask, uint32_t lo, float M, float lg, bool rel_bin, uint32_t& kmax) {
+  filt_scan_row<BF16>(R, [&](float z) {
+    const uint32_t key = order_key(z);
+    kmax = max(kmax, key);
+    if ((key & pmask) == prefix && key >= lo) {
+      const uint32_t d = (key >> shift) & dmask;
+      atomicAdd(&F.cnt[d], 1u);
+      if (MASS && z != kNegInf) {
+        const float top = rel_bin ? key_value((d << shift) | ((1u << shift) - 1u)) : M;
+        atomicAdd((unsigned long long*)&F.mass[d], (unsigned long long)fixed_term(exp2_hw((z - top) * lg)));
+      }
+    }
+  });
+}
+
+// The same over the n candidate keys in LDS (masses relative to M).
 template <bool MASS>
 __device__ void filt_hist_cand(FiltShared& F, int n, uint32_t prefix, uint32_t pmask, int shift, uint32_t dmask,
                                uint32_t lo, float M, float lg) {
@@ -1342,7 +1561,9 @@ __device__ void filt_hist_cand(FiltShared& F, int n, uint32_t prefix, uint32_t p
     if ((key & pmask) == prefix && key >= lo) {
       const uint32_t d = (key >> shift) & dmask;
       atomicAdd(&F.cnt[d], 1u);
-      if (MASS) atomicAdd(&F.mass[d], (double)exp2_hw((key_value(key) - M) * lg));
+      const float z = key_value(key);
+      if (MASS && z != kNegInf)
+        atomicAdd((unsigned long long*)&F.mass[d], (unsigned long long)fixed_term(exp2_hw((z - M) * lg)));
     }
   }
 }
@@ -1350,27 +1571,14 @@ __device__ void filt_hist_cand(FiltShared& F, int n, uint32_t prefix, uint32_t p
 // Gathers the row's keys in [klo, khi] into F.cand (F.n counts them; the
 // caller has checked that they fit).
 template <bool BF16>
-__device__ void filt_gather_row(FiltShared& F, const char* row, int V, uint32_t klo, uint32_t khi) {
-  constexpr int VEC = Elt<BF16>::VEC;
-  constexpr int STEP = kFiltThreads * VEC;
-  for (int x0 = (int)threadIdx.x * VEC; x0 < V; x0 += STEP * kFiltUnroll) {
-    float z[kFiltUnroll][VEC];
-#pragma unroll
-    for (int u = 0; u < kFiltUnroll; ++u)
-      if (x0 + u * STEP < V) Elt<BF16>::load(row, x0 + u * STEP, z[u]);
-#pragma unroll
-    for (int u = 0; u < kFiltUnroll; ++u) {
-      if (x0 + u * STEP >= V) break;
-#pragma unroll
-      for (int i = 0; i < VEC; ++i) {
-        const uint32_t key = order_key(z[u][i]);
-        if (key >= klo && key <= khi) {
-          const uint32_t slot = atomicAdd(&F.n, 1u);
-          if (slot < (uint32_t)kFiltCap) F.cand[slot] = key;
-        }
-      }
+__device__ void filt_gather_row(FiltShared& F, const FiltRow<BF16>& R, uint32_t klo, uint32_t khi) {
+  filt_scan_row<BF16>(R, [&](float z) {
+    const uint32_t key = order_key(z);
+    if (key >= klo && key <= khi) {
+      const uint32_t slot = atomicAdd(&F.n, 1u);
+      if (slot < (uint32_t)kFiltCap) F.cand[slot] = key;
     }
-  }
+  });
 }
 
 // Thread t owns bins nb-1-t*per down to nb-t*per-per (descending order).
@@ -1406,8 +1614,11 @@ __device__ void filt_select_count(FiltShared& F, int nb, uint32_t need) {
 }
 
 // top-p: the lowest non-empty bin whose mass above is below p times the
-// total (the total is this histogram's at the first level).
-__device__ void filt_select_mass(FiltShared& F, int nb, float top_p, bool first) {
+// total (the total is this histogram's at the first level). Bin masses are
+// in units of 2^(M lg); first-level row histograms hold them relative to the
+// top of each bin (rel_bin) and are rescaled here.
+__device__ void filt_select_mass(FiltShared& F, int nb, float top_p, bool first, bool rel_bin, int shift, float M,
+                                 float lg) {
   const FiltOwn o(nb);
   const double above = F.above;
   uint32_t c[4];
@@ -1415,7 +1626,13 @@ __device__ void filt_select_mass(FiltShared& F, int nb, float top_p, bool first)
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     c[i] = i < o.own ? F.cnt[o.hi - i] : 0u;
-    ms[i] = i < o.own ? F.mass[o.hi - i] : 0.0;
+    double m = i < o.own ? (double)F.mass[o.hi - i] / kFix : 0.0;
+    if (rel_bin && m > 0.0) {
+      const uint32_t d = (uint32_t)(o.hi - i);
+      const float top = key_value((d << shift) | ((1u << shift) - 1u));
+      m *= exp2(((double)top - (double)M) * (double)lg);
+    }
+    ms[i] = m;
     s += ms[i];
   }
   double all;
@@ -1446,9 +1663,8 @@ __device__ void filt_select_mass(FiltShared& F, int nb, float top_p, bool first)
 }
 
 template <bool BF16>
-__global__ void __launch_bounds__(kFiltThreads)
-accept_filter_kernel(Args A, int top_k, float top_p) {
-  constexpr int VEC = Elt<BF16>::VEC;
+__global__ void __launch_bounds__(kFiltThreads) accept_filter_kernel(Args A, int top_k, float top_p) {
+  constexpr int N = Vec<BF16>::N, esz = Vec<BF16>::esz;
   constexpr int kLevels = BF16 ? 2 : 3;
   __shared__ FiltShared F;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -1458,16 +1674,19 @@ accept_filter_kernel(Args A, int top_k, float top_p) {
   const int j = is_q ? r - (A.gmax + 1) : r;
   const int gam = A.gamma[b];
   if (gam < 0 || gam > A.gmax || (is_q ? j >= gam : j > gam)) return;  // not a live row
-  const size_t esz = BF16 ? 2 : 4;
-  const char* row = is_q ? (const char*)A.q + ((size_t)b * A.q_stride + (size_t)j * A.V) * esz
-                         : (const char*)A.p + ((size_t)b * A.p_stride + (size_t)j * A.V) * esz;
-  const int V = A.V;
+  FiltRow<BF16> R;
+  R.V = A.V;
+  R.phi = (int)(((int64_t)j * A.V) % N);
+  R.nvec = (R.phi + A.V + N - 1) / N;
+  const char* base = is_q ? (const char*)A.q + ((int64_t)b * A.q_stride + (int64_t)j * A.V - R.phi) * esz
+                          : (const char*)A.p + ((int64_t)b * A.p_stride + (int64_t)j * A.V - R.phi) * esz;
+  R.rs = make_rsrc(base, (size_t)R.nvec * 16);
 
   auto clear = [&](int nb) {
     __syncthreads();  // every thread is done with the previous level's histogram and picks
     for (int i = tid; i < nb; i += kFiltThreads) {
       F.cnt[i] = 0u;
-      F.mass[i] = 0.0;
+      F.mass[i] = 0ull;
     }
     if (tid == 0) {
       F.pick = 0u;
@@ -1483,17 +1702,26 @@ accept_filter_kernel(Args A, int top_k, float top_p) {
     __syncthreads();  // every thread has read the picks (and is done with F.cand)
     if (tid == 0) F.n = 0u;
     __syncthreads();
-    filt_gather_row<BF16>(F, row, V, klo, khi);
+    filt_gather_row<BF16>(F, R, klo, khi);
     __syncthreads();
     return (int)min(F.n, (uint32_t)kFiltCap);
   };
-  int ncand = 0;        // keys in F.cand
+  // The block-wide maximum of kmax.
+  auto block_max = [&](uint32_t kmax) {
+    const uint32_t wm = (uint32_t)wave_max_i((int)(kmax ^ 0x80000000u)) ^ 0x80000000u;  // unsigned max
+    if (lane == 0) F.wmax[w] = wm;
+    __syncthreads();
+    uint32_t m = 0u;
+    for (int i = 0; i < kFiltWaves; ++i) m = max(m, F.wmax[i]);
+    return m;
+  };
+  int ncand = 0;         // keys in F.cand
   bool cand_ge = false;  // F.cand holds every key >= lo
+  uint32_t lo = 0u;      // keys below lo are removed
+  uint32_t kmax = 0u;
+  bool first_read_done = false;  // a top-p first level over the row is already in the histogram
 
   // ---- top-k: radix select of the k-th largest key
-  uint32_t kmax = 0u;
-  uint32_t lo = 0u;  // keys below lo are removed
-  bool have_max = false;
   if (top_k > 0) {
     uint32_t prefix = 0u, pmask = 0u, need = (uint32_t)top_k;
     bool in_lds = false;
@@ -1503,7 +1731,7 @@ accept_filter_kernel(Args A, int top_k, float top_p) {
       if (in_lds)
         filt_hist_cand<false>(F, ncand, prefix, pmask, sh, (uint32_t)nb - 1u, 0u, 0.f, 0.f);
       else
-        filt_hist_row<BF16, false>(F, row, V, prefix, pmask, sh, (uint32_t)nb - 1u, 0u, 0.f, 0.f, kmax);
+        filt_hist_row<BF16, false>(F, R, prefix, pmask, sh, (uint32_t)nb - 1u, 0u, 0.f, 0.f, false, kmax);
       __syncthreads();
       filt_select_count(F, nb, need);
       const uint32_t pick = F.pick;
@@ -1522,46 +1750,38 @@ accept_filter_kernel(Args A, int top_k, float top_p) {
     }
     if (BF16) prefix |= (prefix & 0x80000000u) ? 0u : 0xffffu;  // the fixed low half of bf16 keys
     lo = prefix;
-    have_max = true;
+  } else if (top_p < 1.f) {
+    // top-p alone: the first level's counts, masses (relative to each bin's
+    // top) and the row maximum in one read
+    clear(1 << filt_bits<BF16>(0));
+    filt_hist_row<BF16, true>(F, R, 0u, 0u, filt_shift<BF16>(0), (uint32_t)(1 << filt_bits<BF16>(0)) - 1u, 0u,
+                              0.f, A.lg, true, kmax);
+    __syncthreads();
+    first_read_done = true;
   }
 
   // ---- top-p over the keys top-k kept
   uint32_t thr_key = lo;
   if (top_p < 1.f) {
-    if (!have_max) {  // the row maximum M first
-      constexpr int STEP = kFiltThreads * VEC;
-      for (int x0 = tid * VEC; x0 < V; x0 += STEP * kFiltUnroll) {
-        float z[kFiltUnroll][VEC];
-#pragma unroll
-        for (int u = 0; u < kFiltUnroll; ++u)
-          if (x0 + u * STEP < V) Elt<BF16>::load(row, x0 + u * STEP, z[u]);
-#pragma unroll
-        for (int u = 0; u < kFiltUnroll; ++u) {
-          if (x0 + u * STEP >= V) break;
-#pragma unroll
-          for (int i = 0; i < VEC; ++i) kmax = max(kmax, order_key(z[u][i]));
-        }
-      }
-    }
-    const uint32_t wm = (uint32_t)wave_max_i((int)(kmax ^ 0x80000000u)) ^ 0x80000000u;  // unsigned max
-    if (lane == 0) F.wmax[w] = wm;
+    const float M = key_value(block_max(kmax));
     if (tid == 0) F.above = 0.0;
     __syncthreads();
-    uint32_t m = 0u;
-    for (int i = 0; i < kFiltWaves; ++i) m = max(m, F.wmax[i]);
-    const float M = key_value(m);
     uint32_t prefix = 0u, pmask = 0u;
     bool in_lds = cand_ge;
     for (int l = 0; l < kLevels; ++l) {
       const int sh = filt_shift<BF16>(l), nb = 1 << filt_bits<BF16>(l);
-      clear(nb);
-      uint32_t dummy = 0u;
-      if (in_lds)
-        filt_hist_cand<true>(F, ncand, prefix, pmask, sh, (uint32_t)nb - 1u, lo, M, A.lg);
-      else
-        filt_hist_row<BF16, true>(F, row, V, prefix, pmask, sh, (uint32_t)nb - 1u, lo, M, A.lg, dummy);
-      __syncthreads();
-      filt_select_mass(F, nb, top_p, l == 0);
+      const bool rel_bin = l == 0 && first_read_done;
+      if (!rel_bin) {
+        clear(nb);
+        if (in_lds)
+          filt_hist_cand<true>(F, ncand, prefix, pmask, sh, (uint32_t)nb - 1u, lo, M, A.lg);
+        else {
+          uint32_t dummy = 0u;
+          filt_hist_row<BF16, true>(F, R, prefix, pmask, sh, (uint32_t)nb - 1u, lo, M, A.lg, false, dummy);
+        }
+        __syncthreads();
+      }
+      filt_select_mass(F, nb, top_p, l == 0, rel_bin, sh, M, A.lg);
       const uint32_t pick = F.pick, cpick = F.cpick;
       const uint32_t pbase = prefix | (pick << sh);
       const uint32_t pspan = (1u << sh) - 1u;
@@ -1578,133 +1798,33 @@ accept_filter_kernel(Args A, int top_k, float top_p) {
   if (tid == 0) A.thr[((size_t)b * (A.gmax + 1) + j) * 2 + (is_q ? 1 : 0)] = key_value(thr_key);
 }
 
-// Greedy finish kernel: one workgroup per sequence, one wave per live row.
-// A row's argmax is the lowest index holding the largest of its chunk maxima;
-// draft x_j is accepted iff it is argmax p_j, the extra token is argmax p_k,
-// and the outputs are the one-hot values (a_j, p(x), q(x) in {0, 1}; TV_j 0
-// or 1 and KL_j 0 or +infinity as the two argmaxes agree or not).
-__global__ void __launch_bounds__(1024)
-accept_finish_greedy_kernel(Args A) {
-  __shared__ int s_x[kMaxRows], s_ap[kMaxRows];
-  __shared__ RowRes s_rr[kMaxRows];
-  __shared__ uint32_t s_bad;
-  const int b = blockIdx.x;
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int w = tid >> 6;
-  const int nw = blockDim.x >> 6;
-  const int G1 = A.gmax + 1;
-  const int nslot = (A.nc + 63) / 64;
-  const int gam = A.gamma[b];
-  if (tid == 0) s_bad = 0;
-  if (tid < A.gmax) s_x[tid] = A.drafts[(size_t)b * A.gmax + tid];
-  const int kvl = A.kv_len ? A.kv_len[b] : 0;
-  const int rb_old = A.rb_kv ? A.rb_kv[b] : 0;
-  if (gam < 0 || gam > A.gmax) {
-    if (w == 0) {
-      write_invalid(A, b, SR_ST_GAMMA);
-      finish_rollback(A, b, rb_old, kvl);
-    }
-    return;  // the sweep touched no row of this sequence
-  }
-  __syncthreads();
-  if (tid <= gam) {
-    uint32_t bad = 0;
-    if (tid < gam && (s_x[tid] < 0 || s_x[tid] >= A.V)) bad |= SR_ST_TOKEN;
-    if (tid == 0 && A.kv_len && kvl < gam + 1) bad |= SR_ST_KVLEN;
-    if (bad) atomicOr(&s_bad, bad);
-  }
-  for (int j = w; j <= gam; j += nw) {
-    const bool pair = j < gam;
-    RowRecs R;
-    load_row(A, b * G1 + j, pair, R);
-    float mp = kNegInf, mq = kNegInf;
-#pragma unroll
-    for (int i = 0; i < kSlots; ++i) {
-      mp = fmaxf(mp, R.mp[i]);
-      mq = fmaxf(mq, R.mq[i]);
-    }
-    mp = wave_max(mp);
-    int ap = INT_MAX, aq = INT_MAX;
-#pragma unroll
-    for (int i = 0; i < kSlots; ++i) {
-      const int cc = lane * nslot + i;
-      if (i < nslot && cc < A.nc && R.mp[i] == mp) ap = min(ap, (int)R.sp[i]);
-    }
-    ap = wave_min_i(ap);
-    if (pair) {
-      mq = wave_max(mq);
-#pragma unroll
-      for (int i = 0; i < kSlots; ++i) {
-        const int cc = lane * nslot + i;
-        if (i < nslot && cc < A.nc && R.mq[i] == mq) aq = min(aq, (int)R.sq[i]);
-      }
-      aq = wave_min_i(aq);
-    }
-    if (lane == 0) {
-      s_ap[j] = ap;
-      if (pair) {
-        const int x = s_x[j];
-        const float hit_p = x == ap ? 1.f : 0.f, hit_q = x == aq ? 1.f : 0.f;
-        s_rr[j] = RowRes{(double)hit_p, hit_p, hit_q, ap == aq ? 0.f : __builtin_inff(), ap == aq ? 0.f : 1.f};
-      }
-    }
-  }
-  __syncthreads();
-  if (w != 0) return;
-  if (s_bad) {
-    clear_records(A, b, gam);
-    write_invalid(A, b, s_bad);
-    finish_rollback(A, b, rb_old, kvl);
-    return;
-  }
-  const unsigned long long rmask = __ballot(lane < gam && s_x[lane < gam ? lane : 0] != s_ap[lane < gam ? lane : 0]);
-  const int k = rmask ? (__ffsll((long long)rmask) - 1) : gam;
-  const int tok = s_ap[k];
-  clear_records(A, b, gam);
-  int32_t* ot = A.out_tokens + (size_t)b * G1;
-  for (int j = lane; j <= A.gmax; j += 64) ot[j] = j < k ? s_x[j] : (j == k ? tok : -1);
-  const float nan = __builtin_nanf("");
-  for (int j = lane; j < A.gmax; j += 64) {
-    const size_t o = (size_t)b * A.gmax + j;
-    const bool live = j < gam;
-    if (A.accept_prob) A.accept_prob[o] = live ? (float)s_rr[j].a : nan;
-    if (A.p_tok) A.p_tok[o] = live ? s_rr[j].p_tok : nan;
-    if (A.q_tok) A.q_tok[o] = live ? s_rr[j].q_tok : nan;
-    if (A.kl) A.kl[o] = live ? s_rr[j].kl : nan;
-    if (A.tv) A.tv[o] = live ? s_rr[j].tv : nan;
-  }
-  if (lane == 0) {
-    A.accept_len[b] = k;
-    if (A.new_len) A.new_len[b] = kvl - gam + k;
-  }
-  finish_rollback(A, b, rb_old, kvl - gam + k);
-}
-
-// Entries per lane per chunk.
-constexpr int kEf32 = 16;
-constexpr int kEbf16 = 32;
+// ============================================================================
+// Plan and launch
 
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 struct Layout {
-  size_t stats, tvabs, xlogit, thr, total;
+  size_t recs, tva, xlogit, thr, fincnt, total;
 };
 
-Layout layout(int B, int gamma_max, int n_chunks) {
+Layout layout(int B, int gamma_max, int nc) {
   const size_t rows = (size_t)B * (gamma_max + 1);
   Layout L;
-  L.stats = 0;
-  L.tvabs = align256(rows * n_chunks * kRecBytes);
-  L.xlogit = L.tvabs + align256(rows * n_chunks * sizeof(double));
-  L.thr = L.xlogit + align256(rows * 2 * sizeof(float));
-  L.total = L.thr + align256(rows * 2 * sizeof(float));
+  L.recs = 0;
+  L.tva = L.recs + align256(rows * nc * kRecBytes);
+  L.xlogit = L.tva + align256(rows * nc * kWaves * sizeof(double));
+  L.thr = L.xlogit + align256(rows * 4 * sizeof(float));
+  L.fincnt = L.thr + align256(rows * 2 * sizeof(float));
+  L.total = L.fincnt + 256;
   return L;
 }
 
-template <bool BF16>
-const void* sweep_fn() {
-  return (const void*)accept_sweep_kernel<BF16, BF16 ? kEbf16 : kEf32>;
+// Chunks per row: the row's aligned span is at most V + N - 1 entries.
+int chunks_per_row(int V, int dtype) {
+  const int N = dtype == SR_BF16 ? 8 : 4;
+  const int chunk = dtype == SR_BF16 ? Vec<true>::kChunk : Vec<false>::kChunk;
+  const int span = V % N == 0 ? V : V + N - 1;
+  return (span + chunk - 1) / chunk;
 }
 
 int resident_per_cu(const void* fn, size_t lds) {
@@ -1714,27 +1834,36 @@ int resident_per_cu(const void* fn, size_t lds) {
   return per_cu;
 }
 
-}  // namespace
-
-int accept_plan(int B, int gamma_max, int V, int dtype, AcceptPlan* plan) {
-  const bool bf16 = dtype == SR_BF16;
-  plan->chunk = kThreads * (bf16 ? kEbf16 : kEf32);
-  plan->n_chunks = (V + plan->chunk - 1) / plan->chunk;
-  if (plan->n_chunks > kMaxChunks) return SR_EUNSUPPORTED;
-  const int Bl = B < kMaxSeqs ? B : kMaxSeqs;
-  if ((size_t)Bl * (gamma_max + 1) * plan->n_chunks * kRecBytes >= 0x7fffffffu) return SR_EUNSUPPORTED;
-  plan->workspace_bytes = layout(B, gamma_max, plan->n_chunks).total;
+// The persistent grid of a launch: what fits on the device at once, a
+// multiple of the chunks per row (the chunks of a row are then taken up
+// together), and no more than the task count. 0: no device.
+int persistent_grid(const void* fn, long max_tasks, int Bl, int nc) {
   const int cus = device_cu_count();
-  if (cus <= 0) return SR_ELAUNCH;
-  const long max_tasks = (long)Bl * (gamma_max + 1) * plan->n_chunks;
-  // persistent grid: every workgroup resident at once, a multiple of the
-  // chunks per row, and no more than the largest possible task count
-  const long cap = (long)cus * resident_per_cu(bf16 ? sweep_fn<true>() : sweep_fn<false>(), Bl * sizeof(int));
-  long grid = cap / plan->n_chunks * plan->n_chunks;
+  if (cus <= 0) return 0;
+  const long cap = (long)cus * resident_per_cu(fn, Bl * sizeof(int));
+  long grid = cap / nc * nc;
   if (grid == 0) grid = cap;
   if (grid > max_tasks) grid = max_tasks;
-  plan->grid = (int)grid;
-  return SR_OK;
+  return grid < 1 ? 1 : (int)grid;
+}
+
+}  // namespace
+
+size_t accept_workspace_bytes(int B, int gamma_max, int V, int dtype) {
+  if (B <= 0 || gamma_max < 0 || gamma_max > SPECROUTER_MAX_GAMMA || V <= 0) return 0;
+  if (dtype != SR_F32 && dtype != SR_BF16) return 0;
+  const int nc = chunks_per_row(V, dtype);
+  if (nc > kMaxChunks) return 0;
+  const int Bl = B < kMaxSeqs ? B : kMaxSeqs;
+  if ((size_t)Bl * (gamma_max + 1) * nc * kRecBytes >= 0x7fffffffu) return 0;
+  return layout(B, gamma_max, nc).total;
+}
+
+int accept_plan(int B, int gamma_max, int V, int dtype, AcceptPlan* plan) {
+  plan->chunk = dtype == SR_BF16 ? Vec<true>::kChunk : Vec<false>::kChunk;
+  plan->n_chunks = chunks_per_row(V, dtype);
+  plan->workspace_bytes = accept_workspace_bytes(B, gamma_max, V, dtype);
+  return plan->workspace_bytes == 0 ? SR_EUNSUPPORTED : SR_OK;
 }
 
 int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, int64_t q_stride,
@@ -1744,15 +1873,20 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
                   float* q_tok, float* kl, float* tv, int B, int gamma_max, int V, float temperature,
                   int top_k, float top_p, const AcceptRollback* rollback, void* workspace,
                   const AcceptPlan& plan, int32_t* status, hipStream_t stream) {
-  const Layout L = layout(B, gamma_max, plan.n_chunks);
+  const int nc = plan.n_chunks;
+  const Layout L = layout(B, gamma_max, nc);
   const bool greedy = temperature == 0.f;
   const int G1 = gamma_max + 1;
   const size_t esz = dtype == SR_BF16 ? 2 : 4;
   char* ws = (char*)workspace;
-  const int nw = G1 < 4 ? 4 : (G1 < 16 ? G1 : 16);  // the draw uses waves 0-3
-  // sequences in launches of at most kMaxSeqs (the sweep's row table)
+  // top-k / top-p only under sampling (greedy keeps the argmax anyway)
+  const int k_eff = top_k > 0 && top_k < V ? top_k : 0;
+  const float p_eff = top_p < 1.f ? top_p : 1.f;
+  const bool filt = !greedy && (k_eff > 0 || p_eff < 1.f);
+  // sequences in launches of at most kMaxSeqs (the row table)
   for (int b0 = 0; b0 < B; b0 += kMaxSeqs) {
     const int Bl = B - b0 < kMaxSeqs ? B - b0 : kMaxSeqs;
+    const size_t r0 = (size_t)b0 * G1;
     Args A;
     A.p = (const char*)p_logits + (size_t)b0 * p_stride * esz;
     A.p_stride = p_stride;
@@ -1761,10 +1895,10 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
     A.drafts = drafts ? drafts + (size_t)b0 * gamma_max : nullptr;
     A.gamma = gamma + b0;
     A.u_acc = u_acc ? u_acc + (size_t)b0 * gamma_max : nullptr;
-    A.u_res = u_res ? u_res + (size_t)b0 * G1 : nullptr;
+    A.u_res = u_res ? u_res + r0 : nullptr;
     A.kv_len = kv_len ? kv_len + b0 : nullptr;
     A.accept_len = accept_len + b0;
-    A.out_tokens = out_tokens + (size_t)b0 * G1;
+    A.out_tokens = out_tokens + r0;
     A.new_len = new_len ? new_len + b0 : nullptr;
     A.accept_prob = accept_prob ? accept_prob + (size_t)b0 * gamma_max : nullptr;
     A.p_tok = p_tok ? p_tok + (size_t)b0 * gamma_max : nullptr;
@@ -1774,34 +1908,26 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
     A.B = Bl;
     A.gmax = gamma_max;
     A.V = V;
-    A.nc = plan.n_chunks;
-    A.stats = (u32x4*)(ws + L.stats) + (size_t)b0 * G1 * plan.n_chunks * 2;
-    A.tvabs = (double*)(ws + L.tvabs) + (size_t)b0 * G1 * plan.n_chunks;
-    A.xlogit = (float*)(ws + L.xlogit) + (size_t)b0 * G1 * 2;
+    A.nc = nc;
+    A.lg = greedy ? 0.f : (float)(1.4426950408889634 / (double)temperature);
+    A.recs = (u32x4*)(ws + L.recs) + r0 * nc * 2;
+    A.tva = (double*)(ws + L.tva) + r0 * nc * kWaves;
+    A.xlogit = (float*)(ws + L.xlogit) + r0 * 4;
+    A.thr = filt ? (float*)(ws + L.thr) + r0 * 2 : nullptr;
+    A.fincnt = (uint32_t*)(ws + L.fincnt);
     A.status = status;
-    // top-k / top-p only under sampling (greedy keeps the argmax anyway)
-    const int k_eff = top_k > 0 && top_k < V ? top_k : 0;
-    const float p_eff = top_p < 1.f ? top_p : 1.f;
-    const bool filt = !greedy && (k_eff > 0 || p_eff < 1.f);
-    A.thr = filt ? (float*)(ws + L.thr) + (size_t)b0 * G1 * 2 : nullptr;
     A.rb_kv = rollback ? rollback->kv_len + b0 : nullptr;
     A.rb_mask = rollback && rollback->mask ? rollback->mask + (size_t)b0 * rollback->L_cap : nullptr;
     A.rb_phys = rollback ? rollback->phys_len : nullptr;
+    A.rb_kv_all = rollback ? rollback->kv_len : nullptr;
     A.rb_lcap = rollback ? rollback->L_cap : 0;
-    A.rb_reset = b0 == 0 ? 1 : 0;
-    A.lg = greedy ? 0.f : (float)(1.4426950408889634 / (double)temperature);
-    A.inv_t = greedy ? 0.0 : 1.0 / (double)temperature;
-    const size_t lds = Bl * sizeof(int);
-    if (greedy) {
-      if (dtype == SR_BF16)
-        hipLaunchKernelGGL((accept_argmax_kernel<true, kEbf16>), dim3(plan.grid), dim3(kThreads), lds, stream, A);
-      else
-        hipLaunchKernelGGL((accept_argmax_kernel<false, kEf32>), dim3(plan.grid), dim3(kThreads), lds, stream, A);
-      if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
-      hipLaunchKernelGGL(accept_finish_greedy_kernel, dim3(Bl), dim3(64 * nw), 0, stream, A);
-      if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
-      continue;
-    }
+    A.n_before = b0;
+    const long max_tasks = (long)Bl * G1 * nc;
+    const void* fn = dtype == SR_BF16 ? (greedy ? (const void*)accept_kernel<true, true> : (const void*)accept_kernel<true, false>)
+                                      : (greedy ? (const void*)accept_kernel<false, true> : (const void*)accept_kernel<false, false>);
+    const int n_wg = persistent_grid(fn, max_tasks, Bl, nc);
+    if (n_wg == 0) return SR_ELAUNCH;
+    const size_t lds = Bl * sizeof(int);  // the row table
     if (filt) {  // the rows' top-k / top-p thresholds first
       const dim3 grid_f((unsigned)(Bl * (2 * G1 - 1)));
       if (dtype == SR_BF16)
@@ -1810,15 +1936,23 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
         hipLaunchKernelGGL(accept_filter_kernel<false>, grid_f, dim3(kFiltThreads), 0, stream, A, k_eff, p_eff);
       if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
     }
-    if (dtype == SR_BF16)
-      hipLaunchKernelGGL((accept_sweep_kernel<true, kEbf16>), dim3(plan.grid), dim3(kThreads), lds, stream, A);
-    else
-      hipLaunchKernelGGL((accept_sweep_kernel<false, kEf32>), dim3(plan.grid), dim3(kThreads), lds, stream, A);
+    const dim3 grid((unsigned)n_wg), block(kThreads);
+    if (dtype == SR_BF16) {
+      if (greedy) hipLaunchKernelGGL((accept_kernel<true, true>), grid, block, lds, stream, A);
+      else hipLaunchKernelGGL((accept_kernel<true, false>), grid, block, lds, stream, A);
+    } else {
+      if (greedy) hipLaunchKernelGGL((accept_kernel<false, true>), grid, block, lds, stream, A);
+      else hipLaunchKernelGGL((accept_kernel<false, false>), grid, block, lds, stream, A);
+    }
     if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
-    if (dtype == SR_BF16)
-      hipLaunchKernelGGL((accept_finish_kernel<true, kEbf16>), dim3(Bl), dim3(64 * nw), 0, stream, A);
-    else
-      hipLaunchKernelGGL((accept_finish_kernel<false, kEf32>), dim3(Bl), dim3(64 * nw), 0, stream, A);
+    const dim3 grid_s((unsigned)Bl);
+    if (dtype == SR_BF16) {
+      if (greedy) hipLaunchKernelGGL((accept_finish_kernel<true, true>), grid_s, block, 0, stream, A);
+      else hipLaunchKernelGGL((accept_finish_kernel<true, false>), grid_s, block, 0, stream, A);
+    } else {
+      if (greedy) hipLaunchKernelGGL((accept_finish_kernel<false, true>), grid_s, block, 0, stream, A);
+      else hipLaunchKernelGGL((accept_finish_kernel<false, false>), grid_s, block, 0, stream, A);
+    }
     if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
   }
   return SR_OK;

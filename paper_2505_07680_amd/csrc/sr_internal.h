@@ -249,11 +249,13 @@ int launch_verify_attention(const void* q, const void* k_cache, const void* v_ca
 struct AcceptPlan {
   int chunk;          // vocabulary entries per workgroup task
   int n_chunks;       // chunks per row
-  int grid;           // persistent grid size (multiple of n_chunks)
   size_t workspace_bytes;
 };
 
 int accept_plan(int B, int gamma_max, int V, int dtype, AcceptPlan* plan);
+// The workspace bytes an accept call of this shape needs (0: unsupported
+// shape); host arithmetic only, no device query.
+size_t accept_workspace_bytes(int B, int gamma_max, int V, int dtype);
 
 // Rollback applied by the accept call itself (after each sequence's outcome):
 // the same update as launch_rollback with new_len = the accept's new length.

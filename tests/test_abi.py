@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.specrouter_abi_version() == 3
+    assert lib.specrouter_abi_version() == 4
     for code in (0, -1, -2, -3, -4, 1, 2, 4, 8, 16, 32, 64):
         s = lib.specrouter_status_string(code)
         assert s and s != b"unknown code"

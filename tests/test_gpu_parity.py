@@ -98,6 +98,44 @@ SMALL = [
 ]
 
 
+# Vocabularies whose rows are not a whole number of 16-byte vectors (rows
+# start at every phase inside a vector): Section 2.1's softmax over the whole
+# vocabulary, whatever its size.
+GENERAL_V = [
+    small_shape(name="v32001-f32", B=6, V=32001, gamma=(0, 8), seed=31),
+    small_shape(name="v50257-bf16", B=6, V=50257, gamma=(0, 8), logits="bf16", seed=32),
+    small_shape(name="v4099-f32", B=5, V=4099, gamma=(1, 8), seed=33),
+    small_shape(name="v4101-bf16", B=5, V=4101, gamma=(1, 8), logits="bf16", seed=34),
+    small_shape(name="v7-f32", B=3, V=7, gamma=(1, 5), seed=35),
+]
+
+
+def _padded(x):
+    """x [B, R, V] on the device with each sequence's rows contiguous and the
+    batch stride rounded up to a multiple of 16 bytes (the C ABI's rule)."""
+    B, R, V = x.shape
+    per = 16 // x.itemsize
+    S = (R * V + per - 1) // per * per
+    flat = np.zeros(B * S, dtype=x.dtype)
+    for b in range(B):
+        flat[b * S: b * S + R * V] = x[b].reshape(-1)
+    t = dev(flat)
+    return torch.as_strided(t, (B, R, V), (S, V, 1))
+
+
+@pytest.mark.parametrize("shape", GENERAL_V, ids=lambda s: s.name)
+def test_accept_general_vocabulary(shape):
+    inp = level_inputs(shape, kv=False)
+    say(f"{shape.name}: accept B={inp.B} V={inp.p_logits.shape[2]}")
+    acc = run_accept(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, inp.u_acc, inp.u_res, inp.kv_len,
+                     p_dev=_padded(inp.p_logits), q_dev=_padded(inp.q_logits))
+    ref = oracle.accept_and_diverge(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, inp.u_acc, inp.u_res,
+                                    kv_len=inp.kv_len)
+    assert acc["status"] == 0
+    nb, nbm = check_accept(acc, ref)
+    say(f"{shape.name}: ok ({nb} boundary cases, {nbm} differing)")
+
+
 @pytest.mark.parametrize("shape", SMALL, ids=lambda s: s.name)
 @pytest.mark.parametrize("masked", [False, True], ids=["nomask", "mask"])
 def test_small_shapes(shape, masked):
