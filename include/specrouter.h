@@ -36,7 +36,9 @@
  *   - Calls that share a workspace, or whose outputs alias, must not overlap
  *     in time (put them on one stream). Different calls on different streams
  *     with separate buffers are independent. The library holds no global state
- *     beyond cached device properties, so it is reentrant and thread-safe.
+ *     beyond cached device properties and the fixed per-device array of
+ *     specrouter_accept_and_rollback_noalloc (whose calls share it), so every
+ *     other entry point is reentrant and thread-safe.
  *
  * Shapes: B sequences; gamma_max >= max_b gamma_b (0..16); Hq query heads and
  * Hkv kv heads with Hq % Hkv == 0 (query head h reads kv head h / (Hq/Hkv));
@@ -54,9 +56,11 @@
 extern "C" {
 #endif
 
-#define SPECROUTER_ABI_VERSION 4
+#define SPECROUTER_ABI_VERSION 5
 #define SPECROUTER_MAX_GAMMA 16
 #define SPECROUTER_MAX_CACHE_ROWS (1 << 22)
+/* Size of the library's own device array behind specrouter_accept_and_rollback_noalloc. */
+#define SPECROUTER_NOALLOC_SCRATCH_BYTES (16u << 20)
 
 /* Host-side return codes. */
 enum {
@@ -65,6 +69,7 @@ enum {
   SR_EUNSUPPORTED = -2, /* D not in {64,128}, unknown logits dtype */
   SR_EWORKSPACE = -3,   /* workspace NULL or smaller than the *_workspace_size query */
   SR_ELAUNCH = -4,      /* the HIP runtime refused a launch or a device query */
+  SR_ESCRATCH = -5,     /* the problem needs more workspace than the library's fixed array holds */
 };
 
 /* Logits element types. */
@@ -276,6 +281,32 @@ int specrouter_accept_and_rollback(const void* p_logits, int64_t p_batch_stride,
                                    float* tv, int B, int gamma_max, int V, const specrouter_sampling* sampling,
                                    int32_t* cache_kv_len, uint8_t* cache_mask, int32_t* phys_len, int L_cap,
                                    void* workspace, size_t workspace_bytes, int32_t* status, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* specrouter_accept_and_rollback without a workspace argument, for callers
+ * that cannot allocate device memory: code under HIP graph capture, serving
+ * loops that must not allocate, harnesses that forbid it.
+ *
+ * Same arguments, results and kernels as specrouter_accept_and_rollback minus
+ * (workspace, workspace_bytes): the workspace is a fixed array of
+ * SPECROUTER_NOALLOC_SCRATCH_BYTES in device memory that the library owns,
+ * one per device, resident until the process ends. The call allocates
+ * nothing. It returns SR_ESCRATCH, before touching the device, when the
+ * workspace this shape needs (specrouter_accept_workspace_size) exceeds the
+ * array. The first call on a device also enqueues one clearing kernel on
+ * `stream` (and so does the first call after a call that failed with
+ * SR_ELAUNCH); every call leaves the array ready for the next.
+ * Calls on one device share its array: calls that overlap in time on one
+ * device (different streams, threads or processes' graphs) race and give
+ * wrong results; serialise them, e.g. on one stream.
+ */
+int specrouter_accept_and_rollback_noalloc(
+    const void* p_logits, int64_t p_batch_stride, const void* q_logits, int64_t q_batch_stride, int logits_dtype,
+    const int32_t* draft_tokens, const int32_t* gamma, const float* u_accept, const float* u_resample,
+    const int32_t* kv_len, int32_t* accept_len, int32_t* out_tokens, int32_t* new_len, float* accept_prob,
+    float* p_tok, float* q_tok, float* kl, float* tv, int B, int gamma_max, int V,
+    const specrouter_sampling* sampling, int32_t* cache_kv_len, uint8_t* cache_mask, int32_t* phys_len,
+    int L_cap, int32_t* status, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* KV-cache state (Section 4.4, StateManager: logical validity mask, Eq. 8;

@@ -11,6 +11,7 @@ entry points.
 from . import _lib
 from ._lib import (
     SR_BF16,
+    SR_ESCRATCH,
     SR_F32,
     AcceptBuffers,
     ChainScheduler,
@@ -20,6 +21,7 @@ from ._lib import (
     specrouter_accept_and_diverge,
     specrouter_accept_and_diverge_sampled,
     specrouter_accept_and_rollback,
+    specrouter_accept_and_rollback_noalloc,
     specrouter_accept_workspace_size,
     specrouter_chain_consensus,
     specrouter_chain_window,
@@ -34,6 +36,7 @@ from ._lib import (
 
 __all__ = [
     "SR_BF16",
+    "SR_ESCRATCH",
     "SR_F32",
     "AcceptBuffers",
     "ChainScheduler",
@@ -43,6 +46,7 @@ __all__ = [
     "specrouter_accept_and_diverge",
     "specrouter_accept_and_diverge_sampled",
     "specrouter_accept_and_rollback",
+    "specrouter_accept_and_rollback_noalloc",
     "specrouter_accept_workspace_size",
     "specrouter_chain_consensus",
     "specrouter_chain_window",

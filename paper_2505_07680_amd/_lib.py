@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(HERE, "libspecrouter.so")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 HEADERS = [os.path.join(INCLUDE, h) for h in ("specrouter.h", "specrouter_sched.h", "specrouter_probe.h")]
 
-SR_OK, SR_EINVAL, SR_EUNSUPPORTED, SR_EWORKSPACE, SR_ELAUNCH = 0, -1, -2, -3, -4
+SR_OK, SR_EINVAL, SR_EUNSUPPORTED, SR_EWORKSPACE, SR_ELAUNCH, SR_ESCRATCH = 0, -1, -2, -3, -4, -5
 SR_F32, SR_BF16 = 0, 1
 SR_ST_GAMMA, SR_ST_KVLEN, SR_ST_TOKEN, SR_ST_UNIFORM, SR_ST_ROLLBACK_GROW, SR_ST_TIMEOUT, SR_ST_CHAIN = 1, 2, 4, 8, 16, 32, 64
 
@@ -61,6 +61,11 @@ _SIGNATURES = {
         _c_i,
         [_c_p, _c_i64, _c_p, _c_i64, _c_i] + [_c_p] * 13 + [_c_i] * 3
         + [ctypes.POINTER(SamplingParams), _c_p, _c_p, _c_p, _c_i, _c_p, _c_sz, _c_p, _c_p],
+    ),
+    "specrouter_accept_and_rollback_noalloc": (
+        _c_i,
+        [_c_p, _c_i64, _c_p, _c_i64, _c_i] + [_c_p] * 13 + [_c_i] * 3
+        + [ctypes.POINTER(SamplingParams), _c_p, _c_p, _c_p, _c_i, _c_p, _c_p],
     ),
     "specrouter_rollback": (_c_i, [_c_p] * 4 + [_c_i, _c_i, _c_p, _c_p]),
     "specrouter_chain_window": (_c_i, [_c_p, _c_p, _c_i, _c_i, _c_i] + [_c_p] * 5),
@@ -236,8 +241,31 @@ def specrouter_accept_and_rollback(p_logits, q_logits, draft_tokens, gamma, u_ac
             rollback=(cache_kv_len, cache_mask, phys_len, int(L_cap)))
 
 
+def specrouter_accept_and_rollback_noalloc(p_logits, q_logits, draft_tokens, gamma, u_accept, u_resample, kv_len,
+                                           accept_len, out_tokens, new_len, accept_prob, p_tok, q_tok, kl, tv,
+                                           cache_kv_len, cache_mask, phys_len, status=None, temperature=1.0,
+                                           L_cap=None, top_k=0, top_p=1.0):
+    """specrouter_accept_and_rollback with the library's own fixed device
+    array as the workspace (no workspace argument, nothing allocated)."""
+    _dev(cache_kv_len, cache_mask, phys_len)
+    _i32(cache_kv_len, "cache_kv_len")
+    B = out_tokens.shape[0]
+    if cache_kv_len.shape != (B,):
+        raise ValueError("cache_kv_len must be [B]")
+    if cache_mask is not None:
+        if cache_mask.shape[0] != B or not cache_mask.is_contiguous():
+            raise ValueError("cache_mask must be contiguous [B, L_cap]")
+        L_cap = cache_mask.shape[1]
+    if L_cap is None:
+        raise ValueError("L_cap is required when cache_mask is None")
+    _accept(p_logits, q_logits, draft_tokens, gamma, u_accept, u_resample, kv_len, accept_len, out_tokens,
+            new_len, accept_prob, p_tok, q_tok, kl, tv, None, status,
+            SamplingParams(float(temperature), int(top_k), float(top_p)),
+            rollback=(cache_kv_len, cache_mask, phys_len, int(L_cap)), noalloc=True)
+
+
 def _accept(p_logits, q_logits, draft_tokens, gamma, u_accept, u_resample, kv_len, accept_len, out_tokens,
-            new_len, accept_prob, p_tok, q_tok, kl, tv, workspace, status, sampling, rollback=None):
+            new_len, accept_prob, p_tok, q_tok, kl, tv, workspace, status, sampling, rollback=None, noalloc=False):
     tensors = (p_logits, q_logits, draft_tokens, gamma, u_accept, u_resample, kv_len, accept_len,
                out_tokens, new_len, accept_prob, p_tok, q_tok, kl, tv, workspace, status)
     _dev(*tensors)
@@ -260,11 +288,17 @@ def _accept(p_logits, q_logits, draft_tokens, gamma, u_accept, u_resample, kv_le
     for t in (accept_prob, p_tok, q_tok, kl, tv):
         if t is not None and (t.shape != (B, gmax) or t.dtype != torch.float32):
             raise ValueError("float outputs must be fp32 [B, gamma_max]")
-    ws_bytes = workspace.numel() * workspace.element_size()
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     common = (_ptr(p_logits), ps, _ptr(q_logits), qs, code, _ptr(draft_tokens), _ptr(gamma),
               _ptr(u_accept), _ptr(u_resample), _ptr(kv_len), _ptr(accept_len), _ptr(out_tokens),
               _ptr(new_len), _ptr(accept_prob), _ptr(p_tok), _ptr(q_tok), _ptr(kl), _ptr(tv),
               B, gmax, V, None if sampling is None else ctypes.byref(sampling))
+    if noalloc:
+        rkv, rmask, rphys, L_cap = rollback
+        rc = load().specrouter_accept_and_rollback_noalloc(*common, _ptr(rkv), _ptr(rmask), _ptr(rphys), L_cap,
+                                                           _ptr(status), _stream())
+        _check(rc, "specrouter_accept_and_rollback_noalloc")
+        return
     if rollback is not None:
         rkv, rmask, rphys, L_cap = rollback
         rc = load().specrouter_accept_and_rollback(*common, _ptr(rkv), _ptr(rmask), _ptr(rphys), L_cap,

@@ -84,6 +84,7 @@ const char* specrouter_status_string(int code) {
     case SR_EUNSUPPORTED: return "unsupported configuration (head dim, dtype or vocabulary alignment)";
     case SR_EWORKSPACE: return "workspace missing or too small";
     case SR_ELAUNCH: return "HIP launch or device query failed";
+    case SR_ESCRATCH: return "workspace needed exceeds the library's fixed no-allocation array";
     case SR_ST_GAMMA: return "device data: gamma outside [0, gamma_max]";
     case SR_ST_KVLEN: return "device data: kv_len or new_len out of range";
     case SR_ST_TOKEN: return "device data: draft token outside [0, V)";

@@ -37,8 +37,8 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.specrouter_abi_version() == 4
-    for code in (0, -1, -2, -3, -4, 1, 2, 4, 8, 16, 32, 64):
+    assert lib.specrouter_abi_version() == 5
+    for code in (0, -1, -2, -3, -4, -5, 1, 2, 4, 8, 16, 32, 64):
         s = lib.specrouter_status_string(code)
         assert s and s != b"unknown code"
     assert lib.specrouter_status_string(12345) == b"unknown code"
@@ -138,6 +138,26 @@ def test_accept_and_rollback_rejects_bad_host_arguments(lib):
     assert call(kv=None) == _lib.SR_EINVAL  # the new lengths need kv_len
     assert call(cache=None) == _lib.SR_EINVAL
     assert call(L_cap=0) == _lib.SR_EINVAL
+
+
+@no_device
+def test_noalloc_accept_refuses_oversized_shapes_before_the_device(lib):
+    """The size limit of the library's fixed array is checked from the shape
+    alone, before any HIP call: with no device here, a shape that fits gets as
+    far as the device lookup (SR_ELAUNCH), one that does not fit is refused
+    with SR_ESCRATCH."""
+    p = ctypes.c_void_p(4096)  # never dereferenced
+
+    def call(B, G, V, dtype=_lib.SR_F32):
+        args = ([p, (G + 1) * V, p, G * V, dtype, p, p, p, p, p, p, p] + [None] * 6
+                + [B, G, V, None, p, None, None, 64, None, None])
+        return lib.specrouter_accept_and_rollback_noalloc(*args)
+
+    assert call(16, 5, 128256) == _lib.SR_ELAUNCH                     # fits: stops at the device lookup
+    assert call(4096, 16, 128256) == _lib.SR_ESCRATCH                 # about 90 MB of workspace
+    assert call(4096, 16, 128256, _lib.SR_BF16) == _lib.SR_ESCRATCH
+    assert call(0, 5, 1000) == _lib.SR_EINVAL
+    assert call(16, 5, 1000, dtype=7) == _lib.SR_EUNSUPPORTED
 
 
 @no_device
