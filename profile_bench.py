@@ -114,8 +114,15 @@ def main():
     write, cal_w = read_counter(os.path.join(raw, "WRITE_SIZE"), "WRITE_SIZE")
 
     def mean_kib(per, frag):
-        vals = [v for k, vs in per.items() if frag in k for v in vs]
-        return (sum(vals) / len(vals), len(vals)) if vals else (None, 0)
+        """Mean over the dispatches of the kernel (full name, template
+        arguments included) that contains frag and was dispatched most often:
+        the verify step's instantiation, not a greedy or filtered variant."""
+        names = [k for k in per if frag in k]
+        if not names:
+            return None, 0, None
+        k = max(names, key=lambda n: len(per[n]))
+        vals = per[k]
+        return sum(vals) / len(vals), len(vals), k
 
     if cal_f <= 0 or cal_w <= 0:
         raise SystemExit("calibration copy reads zero")
@@ -135,13 +142,14 @@ def main():
         total_f = total_w = 0.0
         lines = []
         for fr in frags:
-            kf, nf = mean_kib(fetch, fr)
-            kw, nw = mean_kib(write, fr)
+            kf, nf, name = mean_kib(fetch, fr)
+            kw, nw, _ = mean_kib(write, fr)
             if kf is None or kw is None:
                 continue
             total_f += kf * 1024 * f_scale
             total_w += kw * 1024 * w_scale
-            lines.append(f"| {fr} | {kf:.1f} | {kw:.1f} | {nf} |")
+            short = name.replace("(anonymous namespace)::", "").split("(")[0]
+            lines.append(f"| {short[:90]} | {kf:.1f} | {kw:.1f} | {nf} |")
         per_call = int(round(total_f + total_w))
         counters.setdefault(entry, {})[workload] = {
             "source_hash": kernel_source_hash(entry), "bytes_per_call": per_call,
@@ -159,7 +167,8 @@ def main():
                f"WRITE_SIZE {cal_w:.0f} KiB; scale factors {f_scale:.4f} (read) and {w_scale:.4f} (write).",
                f"Calibrated HBM traffic per call: {total_f / 1e6:.2f} MB read + {total_w / 1e6:.2f} MB written "
                f"= {per_call / 1e6:.2f} MB.", f"Kernel source hash: {kernel_source_hash(entry)}.", "",
-               "Commands (run from /tmp, TMPDIR=/tmp):", "", "```", rel(cmd_trace)]
+               f"Made by `python3 profile_bench.py --config {args.config} --raw <dir>` on the GPU, which runs "
+               "(from /tmp, TMPDIR=/tmp):", "", "```", rel(cmd_trace)]
         md += [rel(c) for c in cmds_pmc.values()] + ["```", ""]
         with open(os.path.join(HERE, "profiles", f"{entry}_{workload}.md"), "w") as f:
             f.write("\n".join(md))
