@@ -82,6 +82,7 @@ namespace {
 
 constexpr int kThreads = 256;  // four waves, one task
 constexpr int kWaves = kThreads / 64;
+constexpr int kFinWaves = 8;  // waves of a finish workgroup
 constexpr int kSlots = 2;               // chunk records per lane in a row merge
 constexpr int kMaxChunks = 64 * kSlots; // per row
 constexpr int kMaxRows = SPECROUTER_MAX_GAMMA + 1;
@@ -867,22 +868,219 @@ __device__ void clear_sequence(const Args& A, int b, int gam) {
 }
 
 // ---------------------------------------------------------------------------
-// Row finaliser (wave 0 of the workgroup whose task completed the row)
+// The draw (one wave)
 
-// A chunk's TV sum: its four waves' parts (device-coherent loads) in a fixed
-// order; kSkipped if any part was left to the finaliser; 0 past the row.
-__device__ __forceinline__ double load_tv_chunk(const Args& A, int row, int c) {
-  if (c >= A.nc) return 0.0;
-  const double* p = A.tva + ((size_t)row * A.nc + c) * kWaves;
-  double part[kWaves];
-  bool skipped = false;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
-    part[w] = __hip_atomic_load(p + w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    skipped = skipped || part[w] == kSkipped;
-  }
-  return skipped ? kSkipped : tv_chunk(part);
+// Wave-wide inclusive prefix sum (fp64) in ascending lane order.
+__device__ __forceinline__ double wave_incl_scan_d(double x) {
+  x = x + dpp_f64<0x111>(x);  // row_shr:1 (lanes without a source read 0)
+  x = x + dpp_f64<0x112>(x);  // row_shr:2
+  x = x + dpp_f64<0x114>(x);  // row_shr:4
+  x = x + dpp_f64<0x118>(x);  // row_shr:8
+  const double r0 = lane_value(x, 15), r1 = lane_value(x, 31), r2 = lane_value(x, 47);
+  const int row = (threadIdx.x & 63) >> 4;
+  const double r01 = r0 + r1;
+  return x + (row == 0 ? 0.0 : row == 1 ? r0 : row == 2 ? r01 : r01 + r2);
 }
+
+// The draw at row k of sequence b: from the residual max(0, p_k - q_k) if
+// k < gamma and it has mass, else from p_k; the smallest x with C(x) > u W in
+// ascending vocabulary order (the last entry with weight if rounding leaves
+// none). Two steps: the row's finaliser finds the chunk holding u W from the
+// chunk masses (its records R, normalisers np, nq and chunk TV sums tva) and
+// leaves a plan; once the stopping row is known, four waves scan that chunk,
+// one pass of 1024 entries each (16 consecutive entries per lane), with its
+// weights computed exactly as in the sweep, and combine their sums in pass
+// order.
+struct DrawPlan {
+  double rem;    // the target's offset into the chunk's mass
+  double scale;  // factor turning the scan's weights into probabilities
+  float rp, rq, rho, tp, tq;
+  int c, resid, swap;
+};
+
+template <bool BF16>
+__device__ DrawPlan draw_plan(const Args& A, int b, int k, int gam, float u, const RowRecs& R, const Norm& np,
+                              const Norm& nq, const double (&tva)[kSlots]) {
+  const int lane = threadIdx.x & 63;
+  const int row = b * (A.gmax + 1) + k;
+  const bool pair = k < gam;
+  double mres[kSlots], mp[kSlots];
+  double my_res = 0.0;
+#pragma unroll
+  for (int i = 0; i < kSlots; ++i) {
+    const int c = lane * kSlots + i;
+    const double fp = factor(R.rp[i], np);
+    mp[i] = fp * R.sp[i];
+    mres[i] = 0.0;
+    if (pair && c < A.nc) {
+      const double fq = factor(R.rq[i], nq);
+      mres[i] = fmax(0.0, 0.5 * (tv_par(fp, fq).scale * tva[i] + mp[i] - fq * R.sq[i]));
+    }
+    my_res += mres[i];
+  }
+  const bool resid = pair && wave_sum_d(my_res) > 0.0;
+  double m[kSlots], my = 0.0;
+  int my_last = -1;
+#pragma unroll
+  for (int i = 0; i < kSlots; ++i) {
+    m[i] = resid ? mres[i] : mp[i];
+    my += m[i];
+    if (m[i] > 0.0) my_last = lane * kSlots + i;
+  }
+  const double incl = wave_incl_scan_d(my);
+  const double W = lane_value(incl, 63);
+  const double target = (double)u * W;
+  // the first chunk with weight whose end exceeds the target
+  int c = -1;
+  double pre = 0.0;
+  const unsigned long long hit = __ballot(incl > target && my > 0.0);
+  if (hit) {
+    const int hl = __ffsll((long long)hit) - 1;
+    double run = incl - my;
+    int found = -1;
+    double fpre = 0.0;
+#pragma unroll
+    for (int i = 0; i < kSlots; ++i) {
+      if (found < 0 && m[i] > 0.0 && run + m[i] > target) {
+        found = lane * kSlots + i;
+        fpre = run;
+      }
+      run += m[i];
+    }
+    c = lane_value(found, hl);
+    pre = lane_value(fpre, hl);
+  } else {  // rounding put the target at the very end: the last chunk with weight
+    c = max(wave_max_i(my_last), 0);
+    double before = 0.0;
+#pragma unroll
+    for (int i = 0; i < kSlots; ++i)
+      if (lane * kSlots + i < c) before += m[i];
+    pre = wave_sum_d(before);
+  }
+  const double rem = target - pre;
+  // that chunk's shifts and factors, as the sweep used them
+  float rpc, rqc;
+  chunk_shifts(R, c, rpc, rqc);
+  const double fp = factor(rpc, np);
+  const TvPar par = tv_par(fp, resid ? factor(rqc, nq) : 0.0);
+  const double scale = resid ? par.scale : fp;
+  const float rp = rpc == kNegInf ? 0.f : rpc, rq = rqc == kNegInf ? 0.f : rqc;
+  DrawPlan d;
+  d.rem = rem;
+  d.scale = scale;
+  d.rp = rp;
+  d.rq = rq;
+  d.rho = par.rho;
+  d.swap = par.swap ? 1 : 0;
+  d.resid = resid ? 1 : 0;
+  d.c = c;
+  d.tp = A.thr ? A.thr[(size_t)row * 2] : kNegInf;
+  d.tq = A.thr && resid ? A.thr[(size_t)row * 2 + 1] : kNegInf;
+  return d;
+}
+
+// One pass of the scan (this wave's quarter of the chunk): a lane's weights
+// and the last index among them with weight.
+template <bool BF16>
+__device__ __forceinline__ void draw_weights(const Args& A, int b, int k, const DrawPlan& d, int pass,
+                                             float (&wt)[Vec<BF16>::E], int& mine) {
+  constexpr int N = Vec<BF16>::N, esz = Vec<BF16>::esz, kE = Vec<BF16>::E;
+  const int lane = threadIdx.x & 63;
+  const RowSpan s = row_span<BF16>(A, b, k, d.resid != 0);
+  const int pos0 = d.c * Vec<BF16>::kChunk + pass * Vec<BF16>::kWaveSpan + lane * kE;
+  Loaded<BF16> lp, lq;
+#pragma unroll
+  for (int i = 0; i < kE / N; ++i) {
+    const uint32_t off = (uint32_t)((pos0 + i * N) * esz);
+    lp.v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(s.rp, off, 0, 0));
+    lq.v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(s.rq, off, 0, 0));
+  }
+  float zp[kE], zq[kE];
+  widen<BF16>(lp, zp);
+  widen<BF16>(lq, zq);
+  mine = -1;
+#pragma unroll
+  for (int e = 0; e < kE; ++e) {
+    const int i = pos0 + e - s.phi;
+    const bool in = i >= 0 && i < A.V;
+    const float vp = in && zp[e] >= d.tp ? zp[e] : kNegInf;
+    const float vq = in && zq[e] >= d.tq ? zq[e] : kNegInf;
+    const float ep = exp2_hw(fmaf(vp, A.lg, -d.rp));
+    float wv;
+    if (d.resid) {
+      const float eq = exp2_hw(fmaf(vq, A.lg, -d.rq));
+      const float dd = d.swap ? -fmaf(eq, d.rho, -ep) : fmaf(ep, d.rho, -eq);
+      wv = fmaxf(dd, 0.f);
+    } else {
+      wv = ep;
+    }
+    wt[e] = wv;
+    if (wv > 0.f) mine = i;
+  }
+}
+
+// Shared state of the scan.
+struct DrawShared {
+  double tot[kWaves];   // each pass's total (its prefix at lane 63)
+  int hit[kWaves];      // the pass holds the target
+  int last[kWaves];     // the pass's last index with weight
+  int tok;
+};
+
+// The four waves (w < 4) scan the chunk of plan d; returns the token (valid in
+// waves 0-3 after the call; every wave of the workgroup must call it).
+template <bool BF16>
+__device__ int draw_scan(const Args& A, int b, int k, const DrawPlan& d, DrawShared& ds) {
+  constexpr int kE = Vec<BF16>::E;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  float wt[kE];
+  int mine = -1;
+  double lsum = 0.0, pincl = 0.0;
+  if (w < kWaves) {
+    draw_weights<BF16>(A, b, k, d, w, wt, mine);
+    double acc = 0.0;
+#pragma unroll
+    for (int e = 0; e < kE; ++e) acc += (double)wt[e];
+    lsum = acc * d.scale;
+    pincl = wave_incl_scan_d(lsum);
+    const int last = wave_max_i(mine);
+    if (lane == 63) ds.tot[w] = pincl;
+    if (lane == 0) ds.last[w] = last;
+  }
+  __syncthreads();
+  if (w < kWaves) {
+    double carry = 0.0;  // the previous passes' totals, in pass order
+    for (int i = 0; i < w; ++i) carry += ds.tot[i];
+    const double sincl = carry + pincl;
+    const unsigned long long h = __ballot(sincl > d.rem && lsum > 0.0);
+    if (lane == 0) ds.hit[w] = h ? 1 : 0;
+    if (h) {
+      const int pos0 = d.c * Vec<BF16>::kChunk + w * Vec<BF16>::kWaveSpan + lane * kE;
+      const int phi = row_phase<BF16>(A, k);
+      const int hl = __ffsll((long long)h) - 1;
+      double run = sincl - lsum;
+      int found = -1;
+#pragma unroll
+      for (int e = 0; e < kE; ++e) {
+        run += (double)wt[e] * d.scale;
+        if (found < 0 && wt[e] > 0.f && run > d.rem) found = pos0 + e - phi;
+      }
+      const int t = __builtin_amdgcn_readlane(found >= 0 ? found : mine, hl);
+      if (lane == 0) ds.last[w] = ~t;  // a hit: its token (bit-inverted), read below
+    }
+  }
+  __syncthreads();
+  int tok = -1, last = -1;
+  for (int i = 0; i < kWaves; ++i) {
+    if (tok < 0 && ds.hit[i]) tok = ~ds.last[i];
+    if (!ds.hit[i]) last = max(last, ds.last[i]);
+  }
+  if (tok < 0) tok = last < 0 ? 0 : last;  // the target lies past the chunk's total (rounding)
+  return tok;
+}
+
+// ---------------------------------------------------------------------------
+// Row finaliser (wave 0 of the workgroup whose task completed the row)
 
 // Recompute the sums of the chunks whose owners gave up waiting, from memory,
 // with the owners' arithmetic and layout (one wave takes the four waves'
@@ -945,17 +1143,41 @@ __device__ void redo_skipped(const Args& A, int b, int j, const RowRecs& R, cons
   }
 }
 
+// Row j of sequence b (one wave): its row results, and (sampling) the plan of
+// the draw the sequence would make if it stopped at row j, from u_res[j]; the
+// finisher uses one of those once the accept chain is known. Every load the
+// row needs is issued first, then consumed.
 template <bool BF16, bool GREEDY>
-__device__ RowOut finalize_row(const Args& A, int b, int j, int gam, const __amdgpu_buffer_rsrc_t& rs_recs) {
+__device__ RowOut finalize_row(const Args& A, int b, int j, int gam, const __amdgpu_buffer_rsrc_t& rs_recs,
+                               DrawPlan& plan) {
   const int lane = threadIdx.x & 63;
   const int row = b * (A.gmax + 1) + j;
   const bool pair = j < gam;
+  RecWords W;
+  issue_recs(A, rs_recs, row, W);  // all present: the sweep launch has completed
+  double part[kSlots][kWaves];
+  float xs[4] = {0.f, 0.f, 0.f, 0.f};
+  float u = 0.f;
+  if (!GREEDY) {
+    if (pair) {
+#pragma unroll
+      for (int i = 0; i < kSlots; ++i) {
+        const int c = lane * kSlots + i;
+        const double* tp = A.tva + ((size_t)row * A.nc + (c < A.nc ? c : 0)) * kWaves;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) part[i][w] = tp[w];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) xs[i] = A.xlogit[(size_t)row * 4 + i];
+    }
+    u = A.u_res[row];
+  }
+  const int x = pair ? A.drafts[(size_t)b * A.gmax + j] : -1;
   RowRecs R;
-  load_recs(A, rs_recs, row, R);  // all present: the sweep launch has completed
+  decode_recs(A, W, R);
   RowOut o;
   o.pad = 0;
   o.argp = -1;
-  const int x = pair ? A.drafts[(size_t)b * A.gmax + j] : -1;
   const bool xin = x >= 0 && x < A.V;
   const float nan = __builtin_nanf("");
   if constexpr (GREEDY) {
@@ -985,13 +1207,21 @@ __device__ RowOut finalize_row(const Args& A, int b, int j, int gam, const __amd
     o.tv = pair ? (ap == aq ? 0.f : 1.f) : nan;
   } else {
     const Norm np = merge_norm(R.rp, R.sp);
+    Norm nq = Norm{kNegInf, 0.0};
+    double tva[kSlots];
+#pragma unroll
+    for (int i = 0; i < kSlots; ++i) {
+      // a chunk's TV sum: its four waves' parts in a fixed order; kSkipped if
+      // any part was left to the finaliser; 0 past the row
+      bool skipped = false;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) skipped = skipped || part[i][w] == kSkipped;
+      tva[i] = lane * kSlots + i >= A.nc ? 0.0 : skipped ? kSkipped : tv_chunk(part[i]);
+    }
     o.a = 0.0;
     o.p_tok = o.q_tok = o.kl = o.tv = nan;
     if (pair) {
-      const Norm nq = merge_norm(R.rq, R.sq);
-      double tva[kSlots];
-#pragma unroll
-      for (int i = 0; i < kSlots; ++i) tva[i] = load_tv_chunk(A, row, lane * kSlots + i);
+      nq = merge_norm(R.rq, R.sq);
       redo_skipped<BF16>(A, b, j, R, np, nq, tva);
       // TV = 1/2 sum_c scale_c tva_c;
       // KL = sum_c f_c (ln2 kl_c + ln2 s_c d_c) - ln(S_p / S_q) sum_c f_c s_c with
@@ -1014,10 +1244,8 @@ __device__ RowOut finalize_row(const Args& A, int b, int j, int gam, const __amd
       // exponentials the sums were built from), a = min(1, p(x)/q(x))
       double px = __builtin_nan(""), qx = __builtin_nan("");
       if (xin) {
-        const float* xs = A.xlogit + (size_t)row * 4;
-        const float xp = ld_dev(xs), rpx = ld_dev(xs + 1), xq = ld_dev(xs + 2), rqx = ld_dev(xs + 3);
-        px = (double)exp2_hw(xp) * pow2(rpx, np.rM) / np.S;
-        qx = (double)exp2_hw(xq) * pow2(rqx, nq.rM) / nq.S;
+        px = (double)exp2_hw(xs[0]) * pow2(xs[1], np.rM) / np.S;
+        qx = (double)exp2_hw(xs[2]) * pow2(xs[3], nq.rM) / nq.S;
       }
       o.a = !xin ? __builtin_nan("") : (qx == 0.0 || px >= qx) ? 1.0 : px / qx;
       o.p_tok = xin ? (float)px : nan;
@@ -1025,6 +1253,7 @@ __device__ RowOut finalize_row(const Args& A, int b, int j, int gam, const __amd
       o.kl = (float)kl;
       o.tv = (float)tv;
     }
+    plan = draw_plan<BF16>(A, b, j, gam, u, R, np, nq, tva);
   }
   return o;
 }
@@ -1032,210 +1261,81 @@ __device__ RowOut finalize_row(const Args& A, int b, int j, int gam, const __amd
 // ---------------------------------------------------------------------------
 // Sequence finisher (one wave)
 
-// Wave-wide inclusive prefix sum (fp64) in ascending lane order.
-__device__ __forceinline__ double wave_incl_scan_d(double x) {
-  x = x + dpp_f64<0x111>(x);  // row_shr:1 (lanes without a source read 0)
-  x = x + dpp_f64<0x112>(x);  // row_shr:2
-  x = x + dpp_f64<0x114>(x);  // row_shr:4
-  x = x + dpp_f64<0x118>(x);  // row_shr:8
-  const double r0 = lane_value(x, 15), r1 = lane_value(x, 31), r2 = lane_value(x, 47);
-  const int row = (threadIdx.x & 63) >> 4;
-  const double r01 = r0 + r1;
-  return x + (row == 0 ? 0.0 : row == 1 ? r0 : row == 2 ? r01 : r01 + r2);
-}
+// What the finisher's waves share.
+struct FinShared {
+  DrawShared ds;
+  uint32_t bits;
+  int k;
+};
 
-// The token drawn from row k of sequence b: from the residual max(0, p_k - q_k)
-// if k < gamma and it has mass, else from p_k; the smallest x with
-// C(x) > u W in ascending vocabulary order (the last entry with weight if
-// rounding leaves none). The chunk holding u W is found from the chunk
-// masses, then scanned in four passes of 1024 entries (16 consecutive entries
-// per lane), its weights computed exactly as in the sweep.
-template <bool BF16>
-__device__ int draw_token(const Args& A, int b, int k, int gam, float u, const __amdgpu_buffer_rsrc_t& rs_recs) {
-  constexpr int N = Vec<BF16>::N, esz = Vec<BF16>::esz, kE = Vec<BF16>::E;
-  constexpr int kChunk = Vec<BF16>::kChunk, kWaveSpan = Vec<BF16>::kWaveSpan;
-  const int lane = threadIdx.x & 63;
-  const int row = b * (A.gmax + 1) + k;
-  const bool pair = k < gam;
-  RowRecs R;
-  load_recs(A, rs_recs, row, R);
-  const Norm np = merge_norm(R.rp, R.sp);
-  const Norm nq = pair ? merge_norm(R.rq, R.sq) : Norm{kNegInf, 0.0};
-  double mres[kSlots], mp[kSlots];
-  double my_res = 0.0;
-#pragma unroll
-  for (int i = 0; i < kSlots; ++i) {
-    const int c = lane * kSlots + i;
-    const double fp = factor(R.rp[i], np);
-    mp[i] = fp * R.sp[i];
-    mres[i] = 0.0;
-    if (pair && c < A.nc) {
-      const double fq = factor(R.rq[i], nq);
-      const double t = load_tv_chunk(A, row, c);
-      mres[i] = fmax(0.0, 0.5 * (tv_par(fp, fq).scale * t + mp[i] - fq * R.sq[i]));
-    }
-    my_res += mres[i];
-  }
-  const bool resid = pair && wave_sum_d(my_res) > 0.0;
-  double m[kSlots], my = 0.0;
-  int my_last = -1;
-#pragma unroll
-  for (int i = 0; i < kSlots; ++i) {
-    m[i] = resid ? mres[i] : mp[i];
-    my += m[i];
-    if (m[i] > 0.0) my_last = lane * kSlots + i;
-  }
-  const double incl = wave_incl_scan_d(my);
-  const double W = lane_value(incl, 63);
-  const double target = (double)u * W;
-  // the first chunk with weight whose end exceeds the target
-  int c = -1;
-  double pre = 0.0;
-  const unsigned long long hit = __ballot(incl > target && my > 0.0);
-  if (hit) {
-    const int hl = __ffsll((long long)hit) - 1;
-    double run = incl - my;
-    int found = -1;
-    double fpre = 0.0;
-#pragma unroll
-    for (int i = 0; i < kSlots; ++i) {
-      if (found < 0 && m[i] > 0.0 && run + m[i] > target) {
-        found = lane * kSlots + i;
-        fpre = run;
-      }
-      run += m[i];
-    }
-    c = lane_value(found, hl);
-    pre = lane_value(fpre, hl);
-  } else {  // rounding put the target at the very end: the last chunk with weight
-    c = max(wave_max_i(my_last), 0);
-    double before = 0.0;
-#pragma unroll
-    for (int i = 0; i < kSlots; ++i)
-      if (lane * kSlots + i < c) before += m[i];
-    pre = wave_sum_d(before);
-  }
-  const double rem = target - pre;
-  // that chunk's shifts and factors, as the sweep used them
-  float rpc, rqc;
-  chunk_shifts(R, c, rpc, rqc);
-  const double fp = factor(rpc, np);
-  const TvPar par = tv_par(fp, resid ? factor(rqc, nq) : 0.0);
-  const double scale = resid ? par.scale : fp;
-  const float rp = rpc == kNegInf ? 0.f : rpc, rq = rqc == kNegInf ? 0.f : rqc;
-  const RowSpan s = row_span<BF16>(A, b, k, resid);
-  const float tp = A.thr ? A.thr[(size_t)row * 2] : kNegInf;
-  const float tq = A.thr && resid ? A.thr[(size_t)row * 2 + 1] : kNegInf;
-  double carry = 0.0;
-  int tok = -1, last = -1;
-  for (int pass = 0; pass < kWaves && tok < 0; ++pass) {
-    const int pos0 = c * kChunk + pass * kWaveSpan + lane * kE;
-    Loaded<BF16> lp, lq;
-#pragma unroll
-    for (int i = 0; i < kE / N; ++i) {
-      const uint32_t off = (uint32_t)((pos0 + i * N) * esz);
-      lp.v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(s.rp, off, 0, 0));
-      lq.v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(s.rq, off, 0, 0));
-    }
-    float zp[kE], zq[kE], wt[kE];
-    widen<BF16>(lp, zp);
-    widen<BF16>(lq, zq);
-    double sum = 0.0;
-    int mine = -1;
-#pragma unroll
-    for (int e = 0; e < kE; ++e) {
-      const int i = pos0 + e - s.phi;
-      const bool in = i >= 0 && i < A.V;
-      const float vp = in && zp[e] >= tp ? zp[e] : kNegInf;
-      const float vq = in && zq[e] >= tq ? zq[e] : kNegInf;
-      const float ep = exp2_hw(fmaf(vp, A.lg, -rp));
-      float wv;
-      if (resid) {
-        const float eq = exp2_hw(fmaf(vq, A.lg, -rq));
-        const float d = par.swap ? -fmaf(eq, par.rho, -ep) : fmaf(ep, par.rho, -eq);
-        wv = fmaxf(d, 0.f);
-      } else {
-        wv = ep;
-      }
-      wt[e] = wv;
-      sum += (double)wv;
-      if (wv > 0.f) mine = i;
-    }
-    sum *= scale;
-    last = max(last, wave_max_i(mine));
-    const double sincl = carry + wave_incl_scan_d(sum);
-    const unsigned long long h = __ballot(sincl > rem && sum > 0.0);
-    if (h) {
-      const int hl = __ffsll((long long)h) - 1;
-      double run = sincl - sum;
-      int found = -1;
-      for (int e = 0; e < kE; ++e) {
-        run += (double)wt[e] * scale;
-        if (found < 0 && wt[e] > 0.f && run > rem) found = pos0 + e - s.phi;
-      }
-      tok = __builtin_amdgcn_readlane(found >= 0 ? found : mine, hl);
-    }
-    carry = lane_value(sincl, 63);
-  }
-  if (tok < 0) tok = last < 0 ? 0 : last;  // the target lies past the chunk's total (rounding)
-  return tok;
-}
-
+// The sequence's outcome (every wave of the workgroup calls it): wave 0 reads
+// the per-position inputs, checks them and runs the accept chain; the first
+// four waves scan the stopping row's chunk for the drawn token (greedy: the
+// row's argmax); wave 0 writes the outputs and the rollback while the last
+// wave zeroes the sequence's workspace words.
 template <bool BF16, bool GREEDY>
-__device__ void finish_sequence(const Args& A, int b, int gam, const RowOut* rows,
-                                const __amdgpu_buffer_rsrc_t& rs_recs) {
-  const int lane = threadIdx.x & 63;
+__device__ void finish_sequence(const Args& A, int b, int gam, const RowOut* rows, const DrawPlan* plans,
+                                FinShared& fs) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int G1 = A.gmax + 1;
-  // per-position inputs (one round trip) and the row results (LDS)
   int x = -1;
-  float ua = 0.f, ur = 0.f;
   double a = 0.0;
-  int argp = -1;
   float o_p = 0.f, o_q = 0.f, o_kl = 0.f, o_tv = 0.f;
-  if (lane <= gam) {
-    if (lane < gam) x = A.drafts[(size_t)b * A.gmax + lane];
-    if (!GREEDY) {
-      if (lane < gam) ua = A.u_acc[(size_t)b * A.gmax + lane];
-      ur = A.u_res[(size_t)b * G1 + lane];
+  int kvl = 0, rb_old = 0;
+  if (w == 0) {
+    float ua = 0.f, ur = 0.f;
+    int argp = -1;
+    if (lane <= gam) {
+      if (lane < gam) x = A.drafts[(size_t)b * A.gmax + lane];
+      if (!GREEDY) {
+        if (lane < gam) ua = A.u_acc[(size_t)b * A.gmax + lane];
+        ur = A.u_res[(size_t)b * G1 + lane];
+      }
+      const RowOut& ro = rows[lane];
+      a = ro.a;
+      o_p = ro.p_tok;
+      o_q = ro.q_tok;
+      o_kl = ro.kl;
+      o_tv = ro.tv;
+      argp = ro.argp;
     }
-    const RowOut& ro = rows[lane];
-    a = ro.a;
-    o_p = ro.p_tok;
-    o_q = ro.q_tok;
-    o_kl = ro.kl;
-    o_tv = ro.tv;
-    argp = ro.argp;
+    kvl = A.kv_len ? A.kv_len[b] : 0;
+    rb_old = A.rb_kv ? A.rb_kv[b] : 0;
+    // data checks
+    uint32_t bad = 0;
+    if (lane < gam) {
+      if (x < 0 || x >= A.V) bad |= SR_ST_TOKEN;
+      if (!GREEDY && !(ua >= 0.f && ua < 1.f)) bad |= SR_ST_UNIFORM;
+    }
+    if (!GREEDY && lane <= gam && !(ur >= 0.f && ur < 1.f)) bad |= SR_ST_UNIFORM;
+    if (lane == 0 && A.kv_len && kvl < gam + 1) bad |= SR_ST_KVLEN;
+    uint32_t bits = 0;
+    if (__ballot(bad & SR_ST_TOKEN)) bits |= SR_ST_TOKEN;
+    if (__ballot(bad & SR_ST_UNIFORM)) bits |= SR_ST_UNIFORM;
+    if (__ballot(bad & SR_ST_KVLEN)) bits |= SR_ST_KVLEN;
+    // the accept chain
+    const bool rej = lane < gam && (GREEDY ? x != argp : !((double)ua < a));
+    const unsigned long long rmask = __ballot(rej);
+    if (lane == 0) {
+      fs.bits = bits;
+      fs.k = rmask ? (__ffsll((long long)rmask) - 1) : gam;
+    }
   }
-  const int kvl = A.kv_len ? A.kv_len[b] : 0;
-  const int rb_old = A.rb_kv ? A.rb_kv[b] : 0;
-  // data checks
-  uint32_t bad = 0;
-  if (lane < gam) {
-    if (x < 0 || x >= A.V) bad |= SR_ST_TOKEN;
-    if (!GREEDY && !(ua >= 0.f && ua < 1.f)) bad |= SR_ST_UNIFORM;
+  __syncthreads();
+  const uint32_t bits = fs.bits;
+  const int k = fs.k;
+  int tok = 0;
+  if (!bits) {  // workgroup-uniform
+    if constexpr (GREEDY) tok = rows[k].argp;
+    else tok = draw_scan<BF16>(A, b, k, plans[k], fs.ds);
   }
-  if (!GREEDY && lane <= gam && !(ur >= 0.f && ur < 1.f)) bad |= SR_ST_UNIFORM;
-  if (lane == 0 && A.kv_len && kvl < gam + 1) bad |= SR_ST_KVLEN;
-  uint32_t bits = 0;
-  if (__ballot(bad & SR_ST_TOKEN)) bits |= SR_ST_TOKEN;
-  if (__ballot(bad & SR_ST_UNIFORM)) bits |= SR_ST_UNIFORM;
-  if (__ballot(bad & SR_ST_KVLEN)) bits |= SR_ST_KVLEN;
+  if (w == kFinWaves - 1) clear_sequence(A, b, gam);
+  if (w != 0) return;
   if (bits) {
     write_invalid(A, b, bits);
     finish_rollback(A, b, rb_old, kvl);
-    clear_sequence(A, b, gam);
     count_finished(A, 1);
     return;
-  }
-  // the accept chain
-  const bool rej = lane < gam && (GREEDY ? x != argp : !((double)ua < a));
-  const unsigned long long rmask = __ballot(rej);
-  const int k = rmask ? (__ffsll((long long)rmask) - 1) : gam;
-  int tok;
-  if constexpr (GREEDY) {
-    tok = __builtin_amdgcn_readlane(argp, k);
-  } else {
-    tok = draw_token<BF16>(A, b, k, gam, lane_float(ur, k), rs_recs);
   }
   // outputs
   int32_t* ot = A.out_tokens + (size_t)b * G1;
@@ -1255,7 +1355,6 @@ __device__ void finish_sequence(const Args& A, int b, int gam, const RowOut* row
     if (A.new_len) A.new_len[b] = kvl - gam + k;
   }
   finish_rollback(A, b, rb_old, kvl - gam + k);
-  clear_sequence(A, b, gam);
   count_finished(A, 1);
 }
 
@@ -1360,13 +1459,17 @@ __global__ void __launch_bounds__(kThreads, 2) accept_kernel(Args A) {
   }
 }
 
-// Finish: one workgroup per sequence, after the sweep. Its waves finalise the
-// sequence's rows (wave w takes rows w, w + 4, ...) into LDS; wave 0 then runs
-// the accept chain, the draw, the outputs, the rollback and the record reset.
-// A sequence with gamma outside [0, gamma_max] gets the invalid outputs.
+// Finish: one workgroup per sequence, after the sweep. Its eight waves
+// finalise the sequence's rows (wave w takes rows w, w + 8, ...) into LDS,
+// each with the plan of the draw the sequence would make if it stopped there;
+// then the sequence's outcome (finish_sequence). A sequence with gamma
+// outside [0, gamma_max] gets the invalid outputs.
+
 template <bool BF16, bool GREEDY>
-__global__ void __launch_bounds__(kThreads) accept_finish_kernel(Args A) {
+__global__ void __launch_bounds__(64 * kFinWaves) accept_finish_kernel(Args A) {
   __shared__ RowOut s_out[kMaxRows];
+  __shared__ DrawPlan s_plan[kMaxRows];
+  __shared__ FinShared fs;
   const int b = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int gam = A.gamma[b];
   if (!(gam >= 0 && gam <= A.gmax)) {
@@ -1378,12 +1481,16 @@ __global__ void __launch_bounds__(kThreads) accept_finish_kernel(Args A) {
     return;
   }
   const __amdgpu_buffer_rsrc_t rs_recs = make_rsrc(A.recs, (size_t)A.B * (A.gmax + 1) * A.nc * kRecBytes);
-  for (int j = w; j <= gam; j += kWaves) {
-    const RowOut o = finalize_row<BF16, GREEDY>(A, b, j, gam, rs_recs);
-    if (lane == 0) s_out[j] = o;
+  for (int j = w; j <= gam; j += kFinWaves) {
+    DrawPlan plan;
+    const RowOut o = finalize_row<BF16, GREEDY>(A, b, j, gam, rs_recs, plan);
+    if (lane == 0) {
+      s_out[j] = o;
+      if (!GREEDY) s_plan[j] = plan;
+    }
   }
   __syncthreads();
-  if (w == 0) finish_sequence<BF16, GREEDY>(A, b, gam, s_out, rs_recs);
+  finish_sequence<BF16, GREEDY>(A, b, gam, s_out, s_plan, fs);
 }
 
 // ============================================================================
@@ -1945,13 +2052,13 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
       else hipLaunchKernelGGL((accept_kernel<false, false>), grid, block, lds, stream, A);
     }
     if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
-    const dim3 grid_s((unsigned)Bl);
+    const dim3 grid_s((unsigned)Bl), block_s(64 * kFinWaves);
     if (dtype == SR_BF16) {
-      if (greedy) hipLaunchKernelGGL((accept_finish_kernel<true, true>), grid_s, block, 0, stream, A);
-      else hipLaunchKernelGGL((accept_finish_kernel<true, false>), grid_s, block, 0, stream, A);
+      if (greedy) hipLaunchKernelGGL((accept_finish_kernel<true, true>), grid_s, block_s, 0, stream, A);
+      else hipLaunchKernelGGL((accept_finish_kernel<true, false>), grid_s, block_s, 0, stream, A);
     } else {
-      if (greedy) hipLaunchKernelGGL((accept_finish_kernel<false, true>), grid_s, block, 0, stream, A);
-      else hipLaunchKernelGGL((accept_finish_kernel<false, false>), grid_s, block, 0, stream, A);
+      if (greedy) hipLaunchKernelGGL((accept_finish_kernel<false, true>), grid_s, block_s, 0, stream, A);
+      else hipLaunchKernelGGL((accept_finish_kernel<false, false>), grid_s, block_s, 0, stream, A);
     }
     if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
   }
