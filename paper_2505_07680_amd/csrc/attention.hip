@@ -1,21 +1,27 @@
 // Verification attention for gfx950 (Section 2.2 step 2; Section 4.4, Eq. 8).
 //
-// Work decomposition. One workgroup (4 waves) handles one (sequence b, kv head
-// g, query chunk, key split). All G*(gamma_b+1) query rows that read kv head g
-// (the GQA group times the new positions) are processed together, so every K/V
-// byte of the split is read from HBM exactly once. Each wave owns 16 of every
-// 64 keys and keeps its own online-softmax state (no workgroup barrier inside
-// the key loop); the four states are merged through LDS at the end. When the
+// Work decomposition. One workgroup handles one (sequence b, kv head g, query
+// chunk, key split). All G*(gamma_b+1) query rows that read kv head g (the GQA
+// group times the new positions) are processed together, so every K/V byte of
+// the split is read from HBM exactly once. Four key streams: stream s owns 16
+// of every 64 keys and keeps its own online-softmax state; the four states
+// are merged through LDS at the end. Up to 48 query rows, a workgroup is four
+// waves, one per stream, with no workgroup barrier inside the key loop. Up
+// to 96 rows it is eight waves in two query groups: the two waves of a
+// stream each fetch half of every K/V tile into a shared LDS slot (double
+// buffered, one workgroup barrier per tile) and each computes its own group's
+// rows over the whole tile, so the tile is still read once. When the
 // cache is split, each split publishes its (max, sum, unnormalised output)
 // partial and bumps a per-(b, g, query chunk) arrival counter; the last
 // workgroup to arrive merges all partials in split order and writes the
 // output, then resets the counter, so the workspace is left ready for the
 // next call. The summation order is fixed, so results are reproducible.
 //
-// Per 16-key wave tile:
-//   * K and V rows are fetched with coalesced 16-byte loads into a two-deep
-//     register ring, so two tiles are in flight while one is computed, and
-//     staged in a wave-private LDS slot; rows at or past kv_len are fetched
+// Per 16-key tile of a stream:
+//   * K and V rows are fetched with coalesced 16-byte loads into a register
+//     ring (two tiles deep, or four half tiles with two query groups), so
+//     loads stay in flight while a tile is computed, and staged in the
+//     stream's LDS slot; rows at or past kv_len are fetched
 //     out of the buffer range (they read as zero, with no memory traffic) and
 //     V rows under mask 0 are zeroed while staging, so whatever those rows
 //     hold never reaches the output;
@@ -39,14 +45,13 @@ typedef short shortx4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float floatx2 __attribute__((ext_vector_type(2)));
 
-constexpr int kWaves = 4;
-constexpr int kThreads = 64 * kWaves;
+constexpr int kWaves = 4;  // key streams
 constexpr int kWaveKeys = 16;
-// At most three 16-row query groups per workgroup: more rows than that go to
-// further query chunks (their K/V reads are largely served by the XCD's L2,
-// as the chunks of one (sequence, kv head, split) run on one XCD at the same
-// time), which keeps the accumulators in VGPRs at two waves per SIMD.
+// At most three 16-row query blocks per wave (the accumulators stay in 256
+// registers at two waves per SIMD) and two query groups per workgroup: more
+// than 96 rows go to further query chunks, which read the same K/V again.
 constexpr int kMaxNQ = 3;
+constexpr int kMaxQG = 2;
 constexpr float kLazy = 8.f;  // log2 headroom of the lazily rescaled softmax reference
 // Arrival counters sit one per 128-byte line: the splits of different
 // (sequence, kv head, query chunk) jobs then never contend for one line.
@@ -72,19 +77,29 @@ struct Geo {
   static constexpr int kWaveBytes = kSlotK + kWaveKeys * kVStride;
 };
 
-template <int D, int NQ>
+// Threads, ring depth and LDS buffers per slot of a workgroup with QG query
+// groups: with two groups each wave fetches half of a tile, so a four-deep
+// ring of half tiles holds the registers of a two-deep ring of whole ones.
+template <int QG>
+struct Shape {
+  static constexpr int kThreads = 64 * kWaves * QG;
+  static constexpr int kRing = QG == 1 ? 2 : 4;
+  static constexpr int kBufs = QG == 1 ? 1 : 2;
+};
+
+template <int D, int NQ, int QG>
 struct Lds {
   static constexpr int MQ = 16 * NQ;
-  static constexpr int kStage = kWaves * Geo<D>::kWaveBytes + MQ * Geo<D>::kKStride;
-  // Merge of the four wave states: the columns are reduced in kPasses passes
-  // so that the four fp32 slices fit in 72 KB (two workgroups per CU still
-  // fit in its 160 KB of LDS).
+  static constexpr int kStage = kWaves * Shape<QG>::kBufs * Geo<D>::kWaveBytes + QG * MQ * Geo<D>::kKStride;
+  // Merge of the four stream states of each query group: the columns are
+  // reduced in kPasses passes so that a group's four fp32 slices fit in 72 KB
+  // (two four-wave workgroups per CU, or one of eight, fit in its 160 KB).
   static constexpr int kPasses = (kWaves * MQ * D * 4 <= 73728) ? 1 : (kWaves * MQ * D * 2 <= 73728) ? 2 : 4;
   static constexpr int kDp = D / kPasses;                 // columns per pass
   static constexpr int kRowStride = kDp + 4;              // floats; padded against bank conflicts
   static constexpr int kSlot = MQ * kRowStride;           // floats per wave slice
-  static constexpr int kMl = kWaves * kSlot * 4;          // byte offset of the (m, l) exchange
-  static constexpr int kComb = kMl + (kWaves + 1) * 2 * MQ * 4;
+  static constexpr int kMl = QG * kWaves * kSlot * 4;     // byte offset of the (m, l) exchange
+  static constexpr int kComb = kMl + QG * (kWaves + 1) * 2 * MQ * 4;
   static constexpr int kBytes = kStage > kComb ? kStage : kComb;
 };
 
@@ -110,20 +125,14 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <int D>
-struct Stage {  // one 16-key wave tile in flight
-  u32x4 k[Geo<D>::kLoads], v[Geo<D>::kLoads];
+template <int D, int QG>
+struct Stage {  // one wave's part of a 16-key tile in flight
+  u32x4 k[Geo<D>::kLoads / QG], v[Geo<D>::kLoads / QG];
   uint32_t mbyte;  // validity byte of key (lane mod 16), evaluated when consumed
 };
 
-// 2 waves per SIMD for up to 3 query groups (all fits in 256 registers).
-template <int NQ>
-struct Occ {
-  static constexpr int kMinWaves = NQ <= 3 ? 2 : 1;
-};
-
-template <int D, int NQ, bool NT>
-__global__ void __launch_bounds__(kThreads, Occ<NQ>::kMinWaves)
+template <int D, int NQ, int QG, bool NT>
+__global__ void __launch_bounds__(Shape<QG>::kThreads, 2)
 attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
                   const uint16_t* __restrict__ vc, const uint8_t* __restrict__ mask,
                   const int32_t* __restrict__ kv_len, const int32_t* __restrict__ gamma,
@@ -134,7 +143,11 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
   using GG = Geo<D>;
   constexpr int MQ = 16 * NQ;
   constexpr int DB = D / 16;
-  __shared__ __attribute__((aligned(16))) unsigned char lds[Lds<D, NQ>::kBytes];
+  constexpr int kT = Shape<QG>::kThreads;
+  constexpr int kRing = Shape<QG>::kRing;
+  constexpr int kBufs = Shape<QG>::kBufs;
+  constexpr int kLd = GG::kLoads / QG;  // 16-byte loads per lane per tensor per tile
+  __shared__ __attribute__((aligned(16))) unsigned char lds[Lds<D, NQ, QG>::kBytes];
 
   // Workgroup order: (sequence, kv head) pair fastest, then key split in
   // descending order, then query chunk. Workgroups are dealt to the XCDs
@@ -157,8 +170,8 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
   if (!valid && split == 0 && qc == 0 && g == 0 && threadIdx.x == 0 && status) {
     atomicOr(status, (gam < 0 || gam > gmax) ? SR_ST_GAMMA : SR_ST_KVLEN);
   }
-  const int row0 = qc * MQ;
-  const int row_end = min(R, row0 + MQ);
+  const int row0 = qc * QG * MQ;
+  const int row_end = min(R, row0 + QG * MQ);
   const int Mb = valid ? G * (gam + 1) : 0;
   const int ns = valid ? (L + split_keys - 1) / split_keys : 0;  // splits that hold keys
   const bool work = row0 < Mb && split < ns;
@@ -166,6 +179,9 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = tid >> 6;
+  const int ws = w % kWaves;  // key stream
+  const int h = w / kWaves;   // query group: rows rbase .. rbase + MQ - 1
+  const int rbase = row0 + h * MQ;
   const int l16 = lane & 15;
   const int lg = lane >> 4;
 
@@ -173,19 +189,17 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
     // Nothing to compute. Split 0 of a query chunk without live rows (or of an
     // invalid sequence) owns those output rows and writes them as zero.
     if (split == 0) {
-      for (int idx = tid; idx < (row_end - row0) * (D / 4); idx += kThreads) {
+      for (int idx = tid; idx < (row_end - row0) * (D / 4); idx += kT) {
         const int r = row0 + idx / (D / 4);
         const int d4 = idx % (D / 4);
-        const int i = r / G, h = g * G + r % G;
-        *(float4*)(out + ((size_t)(b * (gmax + 1) + i) * Hq + h) * D + d4 * 4) = make_float4(0.f, 0.f, 0.f, 0.f);
+        const int i = r / G, hh = g * G + r % G;
+        *(float4*)(out + ((size_t)(b * (gmax + 1) + i) * Hq + hh) * D + d4 * 4) = make_float4(0.f, 0.f, 0.f, 0.f);
       }
     }
     return;
   }
 
-  unsigned char* qst = lds + kWaves * GG::kWaveBytes;
-  unsigned char* kst = lds + w * GG::kWaveBytes;
-  unsigned char* vst = kst + GG::kSlotK;
+  unsigned char* qst = lds + kWaves * kBufs * GG::kWaveBytes;
   const size_t slab = ((size_t)b * Hkv + g) * (size_t)L_cap;
   const uint16_t* kslab = kc + slab * D;
   const uint16_t* vslab = vc + slab * D;
@@ -202,15 +216,17 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
     for (int db = 0; db < DB; ++db) o[db][qg] = floatx4{0.f, 0.f, 0.f, 0.f};
   }
 
-  // Wave tile j holds keys [16 j, 16 j + 16). Split s owns the keys
-  // [s split_keys, (s + 1) split_keys), dealt round-robin to its four waves,
-  // so a wave's tiles are first, first + 4, first + 8, ... below j_end.
-  const int first = split * (split_keys / kWaveKeys) + w;
+  // Tile j holds keys [16 j, 16 j + 16). Split s owns the keys
+  // [s split_keys, (s + 1) split_keys), dealt round-robin to the four
+  // streams, so a stream's tiles are first, first + 4, first + 8, ... below
+  // j_end.
+  const int first0 = split * (split_keys / kWaveKeys);
+  const int first = first0 + ws;
   const int j_end = min((L + kWaveKeys - 1) / kWaveKeys, (split + 1) * (split_keys / kWaveKeys));
-  const int row_lim = min(L, j_end * kWaveKeys);  // a refill past the wave's last tile reads nothing
+  const int row_lim = min(L, j_end * kWaveKeys);  // a refill past the stream's last tile reads nothing
 
   // Every fetch issues the same loads (rows at or past kv_len, and tiles past
-  // the wave's last, read out of range, as zero, with no traffic), so each
+  // the stream's last, read out of range, as zero, with no traffic), so each
   // wait covers exactly the loads it needs, in the first iteration as in
   // every later one.
   const uint8_t* mload = mrow ? mrow : (const uint8_t*)kslab;
@@ -218,46 +234,52 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(kslab, (size_t)L_cap * D * 2);
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(vslab, (size_t)L_cap * D * 2);
   const int lane_row = lane / GG::kChunksPerRow;
-  const uint32_t lane_col = (uint32_t)(lane % GG::kChunksPerRow) * 16;
-  auto fetch = [&](int j, Stage<D>& st) __attribute__((always_inline)) {
+  const int lane_chunk = lane % GG::kChunksPerRow;
+  const uint32_t lane_col = (uint32_t)lane_chunk * 16;
+  // this wave's rows of a tile: load u covers rows (h kLd + u) kRowsPerLoad + lane_row
+  auto fetch = [&](int j, Stage<D, QG>& st) __attribute__((always_inline)) {
     const int kb0 = j * kWaveKeys;
 #pragma unroll
-    for (int u = 0; u < GG::kLoads; ++u) {
-      const int row = kb0 + u * GG::kRowsPerLoad + lane_row;
+    for (int u = 0; u < kLd; ++u) {
+      const int row = kb0 + (h * kLd + u) * GG::kRowsPerLoad + lane_row;
       const uint32_t off = row < row_lim ? (uint32_t)row * (D * 2) + lane_col : kOutOfRange;
       st.k[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, NT ? kStreamLoad : 0));
       st.v[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, NT ? kStreamLoad : 0));
     }
     st.mbyte = mload[min(kb0 + (lane & (kWaveKeys - 1)), L - 1)];
   };
-  // Ring entry st holds tile j: stage it in LDS, refill it with the wave's
-  // next-but-one tile, compute tile j, and leave the refilled tile's number
-  // in j.
-  auto step = [&](int& j, Stage<D>& st) __attribute__((always_inline)) {
+  // Ring entry st holds tile j: stage it in LDS buffer buf of the stream's
+  // slot, refill it with the stream's tile kRing further on, compute tile j,
+  // and leave the refilled tile's number in j.
+  auto step = [&](int& j, Stage<D, QG>& st, int buf) __attribute__((always_inline)) {
+    unsigned char* kst = lds + (ws * kBufs + buf) * GG::kWaveBytes;
+    unsigned char* vst = kst + GG::kSlotK;
     const int kb0 = j * kWaveKeys;
     const bool key_ok = lane < kWaveKeys && kb0 + lane < L && (mrow == nullptr || st.mbyte != 0u);
     const uint32_t vbits = (uint32_t)__ballot(key_ok) & 0xffffu;
     const bool all_rows = vbits == 0xffffu;  // wave-uniform
 #pragma unroll
-    for (int u = 0; u < GG::kLoads; ++u) {
-      const int rl = u * GG::kRowsPerLoad + lane_row;
-      const int c = lane % GG::kChunksPerRow;
-      *(u32x4*)(kst + rl * GG::kKStride + c * 16) = st.k[u];
+    for (int u = 0; u < kLd; ++u) {
+      const int rl = (h * kLd + u) * GG::kRowsPerLoad + lane_row;
+      *(u32x4*)(kst + rl * GG::kKStride + lane_chunk * 16) = st.k[u];
       const u32x4 vv = (all_rows || ((vbits >> rl) & 1u)) ? st.v[u] : u32x4{0u, 0u, 0u, 0u};
-      uint32_t* dst = (uint32_t*)(vst + rl * GG::kVStride + c * 16);
+      uint32_t* dst = (uint32_t*)(vst + rl * GG::kVStride + lane_chunk * 16);
       *(uint2*)dst = make_uint2(vv.x, vv.y);
       *(uint2*)(dst + 2) = make_uint2(vv.z, vv.w);
     }
-    wave_lds_sync();
-    const int nx = j + 2 * kWaves;
+    if constexpr (QG == 1)
+      wave_lds_sync();
+    else
+      __syncthreads();  // both halves of the tile are in the slot
+    const int nx = j + kRing * kWaves;
     __builtin_amdgcn_sched_barrier(0);
-    fetch(nx, st);  // two tiles in flight during the compute below
+    fetch(nx, st);  // the ring's other tiles and this refill stay in flight during the compute below
     __builtin_amdgcn_sched_barrier(0);
     const int jc = j;
     j = nx;
-    if (jc >= j_end) return;  // wave-uniform: past the wave's last tile
+    if (jc >= j_end || rbase >= Mb) return;  // wave-uniform: past the stream's last tile, or no live rows
     const bool full = vbits == 0xffffu && kb0 + kWaveKeys - 1 <= causal0;  // wave-uniform
-    // ---- S^T = K Q^T (16 keys x 16 queries per group)
+    // ---- S^T = K Q^T (16 keys x 16 queries per block)
     floatx4 sacc[NQ];
 #pragma unroll
     for (int qg = 0; qg < NQ; ++qg) sacc[qg] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -267,8 +289,8 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
       const bf16x8 ka = *(const bf16x8*)(kst + l16 * GG::kKStride + col);
 #pragma unroll
       for (int qg = 0; qg < NQ; ++qg) {
-        if (row0 + qg * 16 < Mb) {
-          const bf16x8 qb = *(const bf16x8*)(qst + (qg * 16 + l16) * GG::kKStride + col);
+        if (rbase + qg * 16 < Mb) {
+          const bf16x8 qb = *(const bf16x8*)(qst + (h * MQ + qg * 16 + l16) * GG::kKStride + col);
           sacc[qg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb, sacc[qg], 0, 0, 0);
         }
       }
@@ -277,8 +299,8 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
     shortx4 pb[NQ];
 #pragma unroll
     for (int qg = 0; qg < NQ; ++qg) {
-      if (row0 + qg * 16 < Mb) {
-        const int r = row0 + qg * 16 + l16;
+      if (rbase + qg * 16 < Mb) {
+        const int r = rbase + qg * 16 + l16;
         float s[4];
         float mt = kNegInf;
         if (full) {
@@ -336,66 +358,82 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
       const shortx4 va = __builtin_bit_cast(shortx4, make_uint2(v0 | (v1 << 16), v2 | (v3 << 16)));
 #pragma unroll
       for (int qg = 0; qg < NQ; ++qg) {
-        if (row0 + qg * 16 < Mb) o[db][qg] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb[qg], o[db][qg], 0, 0, 0);
+        if (rbase + qg * 16 < Mb) o[db][qg] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb[qg], o[db][qg], 0, 0, 0);
       }
     }
-    wave_lds_sync();  // this tile's LDS reads are issued before the slot is rewritten
+    // One query group: this tile's LDS reads are issued before the slot is
+    // rewritten. Two: the slot's other buffer takes the next tile, and the
+    // barrier of the step after it orders every read of this one first.
+    if constexpr (QG == 1) wave_lds_sync();
   };
 
-  // Issue order: this workgroup's query rows, then the two ring entries; the
-  // query rows are staged in LDS while the K/V tiles are still in flight.
-  // Each group is kept together (no interleaving by the scheduler), so every
-  // wait covers exactly what it needs: a step waits for its own tile only.
-  constexpr int kQChunks = MQ * GG::kChunksPerRow;
-  constexpr int kQLoads = (kQChunks + kThreads - 1) / kThreads;
+  // Issue order: this workgroup's query rows, then the ring; the query rows
+  // are staged in LDS while the K/V tiles are still in flight. Each group is
+  // kept together (no interleaving by the scheduler), so every wait covers
+  // exactly what it needs: a step waits for its own tile only.
+  constexpr int kQChunks = QG * MQ * GG::kChunksPerRow;
+  constexpr int kQLoads = (kQChunks + kT - 1) / kT;
   u32x4 qv[kQLoads];
 #pragma unroll
   for (int u = 0; u < kQLoads; ++u) {
-    const int idx = min(tid + u * kThreads, kQChunks - 1);
+    const int idx = min(tid + u * kT, kQChunks - 1);
     const int r = min(row0 + idx / GG::kChunksPerRow, Mb - 1);  // rows past Mb are zeroed below
-    const int i = r / G, h = g * G + r % G;
-    qv[u] = *(const u32x4*)(q + ((size_t)(b * (gmax + 1) + i) * Hq + h) * D + (idx % GG::kChunksPerRow) * 8);
+    const int i = r / G, hh = g * G + r % G;
+    qv[u] = *(const u32x4*)(q + ((size_t)(b * (gmax + 1) + i) * Hq + hh) * D + (idx % GG::kChunksPerRow) * 8);
   }
   __builtin_amdgcn_sched_barrier(0);
-  Stage<D> sa, sb;
-  int ja = first;
-  int jb = first + kWaves;
-  fetch(ja, sa);
-  __builtin_amdgcn_sched_barrier(0);
-  fetch(jb, sb);
-  __builtin_amdgcn_sched_barrier(0);
+  Stage<D, QG> ring[kRing];
+  int jr[kRing];
+#pragma unroll
+  for (int r = 0; r < kRing; ++r) {
+    jr[r] = first + r * kWaves;
+    fetch(jr[r], ring[r]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
   // (unconditional: a thread past the last chunk rewrites that chunk with
   // the same value, and no load is moved into a branch after the K/V loads)
 #pragma unroll
   for (int u = 0; u < kQLoads; ++u) {
-    const int idx = min(tid + u * kThreads, kQChunks - 1);
+    const int idx = min(tid + u * kT, kQChunks - 1);
     const int rl = idx / GG::kChunksPerRow;
     const u32x4 val = row0 + rl < Mb ? qv[u] : u32x4{0u, 0u, 0u, 0u};
     *(u32x4*)(qst + rl * GG::kKStride + (idx % GG::kChunksPerRow) * 16) = val;
   }
   __syncthreads();
 
-  // sa and sb hold the wave's next two tiles (ja < jb).
-  while (ja < j_end) {
-    step(ja, sa);
-    step(jb, sb);
-  }
-  __syncthreads();
-
-  // ---- merge the four wave states (every wave and lane takes part)
-  using LL = Lds<D, NQ>;
-  float* slots = (float*)lds;                    // [kWaves][MQ][kRowStride]
-  float* mlx = (float*)(lds + LL::kMl);          // [kWaves][2][MQ]: each wave's (m, l)
-  float* mlf = mlx + kWaves * 2 * MQ;            // [2][MQ]: merged (M, L)
-  if (lg == 0) {
+  // The ring holds the stream's next kRing tiles (ascending). With two query
+  // groups every wave runs the same number of rounds (counted on stream 0,
+  // whose tiles come first), so the barriers inside the steps pair up; a step
+  // past a stream's last tile still stages (zeros) and meets the barrier.
+  if constexpr (QG == 1) {
+    while (jr[0] < j_end) {
 #pragma unroll
-    for (int qg = 0; qg < NQ; ++qg) {
-      mlx[(w * 2) * MQ + qg * 16 + l16] = m_run[qg];
-      mlx[(w * 2 + 1) * MQ + qg * 16 + l16] = l_run[qg];
+      for (int r = 0; r < kRing; ++r) step(jr[r], ring[r], 0);
+    }
+  } else {
+    const int rounds = (j_end - first0 + kRing * kWaves - 1) / (kRing * kWaves);
+    for (int it = 0; it < rounds; ++it) {
+#pragma unroll
+      for (int r = 0; r < kRing; ++r) step(jr[r], ring[r], r % kBufs);
     }
   }
   __syncthreads();
-  float cw[NQ];  // this wave's weight exp2(m_w - M) per row group
+
+  // ---- merge the four stream states of each query group (every wave and lane takes part)
+  using LL = Lds<D, NQ, QG>;
+  const int tg = tid - h * 64 * kWaves;                               // thread index in the group
+  float* slots = (float*)lds + h * kWaves * LL::kSlot;                  // [kWaves][MQ][kRowStride]
+  float* mlx = (float*)(lds + LL::kMl) + h * (kWaves + 1) * 2 * MQ;     // [kWaves][2][MQ]: each stream's (m, l)
+  float* mlf = mlx + kWaves * 2 * MQ;                                   // [2][MQ]: merged (M, L)
+  if (lg == 0) {
+#pragma unroll
+    for (int qg = 0; qg < NQ; ++qg) {
+      mlx[(ws * 2) * MQ + qg * 16 + l16] = m_run[qg];
+      mlx[(ws * 2 + 1) * MQ + qg * 16 + l16] = l_run[qg];
+    }
+  }
+  __syncthreads();
+  float cw[NQ];  // this stream's weight exp2(m_w - M) per row block
 #pragma unroll
   for (int qg = 0; qg < NQ; ++qg) {
     const int rl = qg * 16 + l16;
@@ -409,7 +447,7 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
       Lsum += c * mlx[(v * 2 + 1) * MQ + rl];
     }
     cw[qg] = M == kNegInf ? 0.f : exp2f(m_run[qg] - M);
-    if (w == 0 && lg == 0) {
+    if (ws == 0 && lg == 0) {
       mlf[rl] = M;
       mlf[MQ + rl] = Lsum;
     }
@@ -421,7 +459,7 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
   const int n_rec = (int)((size_t)n_splits * P) * R;  // records in the partial arrays
   const __amdgpu_buffer_rsrc_t rs_o = partial_rsrc(part_o, (uint32_t)((size_t)n_rec * D * 4));
   const __amdgpu_buffer_rsrc_t rs_ml = partial_rsrc(part_ml, (uint32_t)((size_t)n_rec * 8));
-  constexpr int kItemsP = (MQ * (LL::kDp / 4) + kThreads - 1) / kThreads;
+  constexpr int kItemsP = (MQ * (LL::kDp / 4) + 64 * kWaves - 1) / (64 * kWaves);
 #pragma unroll
   for (int pass = 0; pass < LL::kPasses; ++pass) {
     __syncthreads();  // (m, l) exchange read / previous pass's slices consumed
@@ -431,17 +469,17 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
         const int col = db * 16 + lg * 4 - pass * LL::kDp;
-        if (col >= 0 && col < LL::kDp) *(floatx4*)(slots + (w * MQ + rl) * LL::kRowStride + col) = o[db][qg] * cw[qg];
+        if (col >= 0 && col < LL::kDp) *(floatx4*)(slots + (ws * MQ + rl) * LL::kRowStride + col) = o[db][qg] * cw[qg];
       }
     }
     __syncthreads();
 #pragma unroll
     for (int k = 0; k < kItemsP; ++k) {
-      const int idx = tid + k * kThreads;
+      const int idx = tg + k * 64 * kWaves;
       if (idx >= MQ * (LL::kDp / 4)) continue;
       const int rl = idx / (LL::kDp / 4);
       const int c4 = idx % (LL::kDp / 4);
-      const int r = row0 + rl;
+      const int r = rbase + rl;
       if (r >= row_end) continue;
       floatx4 sum = *(const floatx4*)(slots + rl * LL::kRowStride + c4 * 4);
 #pragma unroll
@@ -449,8 +487,8 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
       const int col = pass * LL::kDp + c4 * 4;
       if (ns == 1) {
         const float Lr = mlf[MQ + rl];
-        const int i = r / G, h = g * G + r % G;
-        *(floatx4*)(out + ((size_t)(b * (gmax + 1) + i) * Hq + h) * D + col) =
+        const int i = r / G, hh = g * G + r % G;
+        *(floatx4*)(out + ((size_t)(b * (gmax + 1) + i) * Hq + hh) * D + col) =
             (r < Mb && Lr > 0.f) ? sum * (1.f / Lr) : floatx4{0.f, 0.f, 0.f, 0.f};
       } else if (r < Mb) {
         const uint32_t rec = (uint32_t)((pair * n_splits + split) * R + r);
@@ -479,7 +517,7 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
 
   // Each thread owns kItems (row, 4 columns) items and folds the splits in
   // with a running max, kGroup splits per round of loads.
-  constexpr int kItems = (MQ * (D / 4) + kThreads - 1) / kThreads;
+  constexpr int kItems = (QG * MQ * (D / 4) + kT - 1) / kT;
   constexpr int kGroup = kItems >= 16 ? 1 : (16 / kItems > 8 ? 8 : 16 / kItems);
   const int n_items = (row_end - row0) * (D / 4);
   float mx[kItems], den[kItems];
@@ -498,7 +536,7 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
 #pragma unroll
       for (int k = 0; k < kItems; ++k) {
         const int sp = min(sp0 + j, ns - 1);  // repeats of the last split are discarded below
-        const int idx = min(tid + k * kThreads, n_items - 1);
+        const int idx = min(tid + k * kT, n_items - 1);
         const int r = min(row0 + idx / (D / 4), Mb - 1);  // rows past Mb hold no partial; their result is discarded
         const uint32_t rec = (uint32_t)((pair * n_splits + sp) * R + r);
         ml2[j][k] = __builtin_bit_cast(floatx2, __builtin_amdgcn_raw_buffer_load_b64(rs_ml, rec * 8, 0, kDeviceCoherent));
@@ -521,13 +559,13 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
   }
 #pragma unroll
   for (int k = 0; k < kItems; ++k) {
-    const int idx = tid + k * kThreads;
+    const int idx = tid + k * kT;
     if (idx >= n_items) continue;
     const int r = row0 + idx / (D / 4);
     const bool live = r < Mb && den[k] > 0.f;
     const floatx4 res = live ? acc[k] * (1.f / den[k]) : floatx4{0.f, 0.f, 0.f, 0.f};
-    const int i = r / G, h = g * G + r % G;
-    *(floatx4*)(out + ((size_t)(b * (gmax + 1) + i) * Hq + h) * D + (idx % (D / 4)) * 4) = res;
+    const int i = r / G, hh = g * G + r % G;
+    *(floatx4*)(out + ((size_t)(b * (gmax + 1) + i) * Hq + hh) * D + (idx % (D / 4)) * 4) = res;
   }
 }
 
@@ -535,17 +573,24 @@ typedef void (*SplitKernel)(const uint16_t*, const uint16_t*, const uint16_t*, c
                             const int32_t*, const int32_t*, float*, float*, float*, uint32_t*, int,
                             int, int, int, int, float, int, int, int, int32_t*);
 
+// A single query chunk reads its K/V tiles once (non-temporal loads); with
+// several chunks the others read the same tiles again, which then should
+// stay in the caches.
 template <int D>
-SplitKernel pick_split(int nq, int q_chunks) {
-  switch (nq) {  // one or two query groups never need a second query chunk
-    case 1: return attn_split_kernel<D, 1, true>;
-    case 2: return attn_split_kernel<D, 2, true>;
-    default: return q_chunks == 1 ? attn_split_kernel<D, 3, true> : attn_split_kernel<D, 3, false>;
+SplitKernel pick_split(int nq, int qg, int q_chunks) {
+  if (qg == 1) {
+    switch (nq) {
+      case 1: return attn_split_kernel<D, 1, 1, true>;
+      case 2: return attn_split_kernel<D, 2, 1, true>;
+      default: return attn_split_kernel<D, 3, 1, true>;
+    }
   }
+  if (nq == 2) return attn_split_kernel<D, 2, 2, true>;
+  return q_chunks == 1 ? attn_split_kernel<D, 3, 2, true> : attn_split_kernel<D, 3, 2, false>;
 }
 
-SplitKernel pick_split(int D, int nq, int q_chunks) {
-  return D == 64 ? pick_split<64>(nq, q_chunks) : pick_split<128>(nq, q_chunks);
+SplitKernel pick_split(int D, int nq, int qg, int q_chunks) {
+  return D == 64 ? pick_split<64>(nq, qg, q_chunks) : pick_split<128>(nq, qg, q_chunks);
 }
 
 }  // namespace
@@ -553,13 +598,25 @@ SplitKernel pick_split(int D, int nq, int q_chunks) {
 int attention_plan(int B, int gamma_max, int Hq, int Hkv, int D, int L_cap, AttentionPlan* plan) {
   const int G = Hq / Hkv;
   const int R = G * (gamma_max + 1);
-  plan->nq = R <= 16 * kMaxNQ ? (R + 15) / 16 : kMaxNQ;
-  plan->q_chunks = (R + 16 * plan->nq - 1) / (16 * plan->nq);
+  // Up to 48 rows: one four-wave group of ceil(R / 16) row blocks. Beyond:
+  // two groups of two (up to 64 rows) or three blocks, in as many query
+  // chunks of 96 rows as needed.
+  if (R <= 16 * kMaxNQ) {
+    plan->qg = 1;
+    plan->nq = (R + 15) / 16;
+  } else {
+    plan->qg = kMaxQG;
+    plan->nq = R <= 2 * 32 ? 2 : kMaxNQ;
+  }
+  const int rows_per_chunk = 16 * plan->nq * plan->qg;
+  plan->q_chunks = (R + rows_per_chunk - 1) / rows_per_chunk;
   const int cus = device_cu_count();
   if (cus <= 0) return SR_ELAUNCH;
   int per_cu = 1;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void*)pick_split(D, plan->nq, plan->q_chunks),
-                                                   kThreads, 0) != hipSuccess || per_cu < 1)
+  const int threads = plan->qg == 1 ? Shape<1>::kThreads : Shape<kMaxQG>::kThreads;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+          &per_cu, (const void*)pick_split(D, plan->nq, plan->qg, plan->q_chunks), threads, 0) != hipSuccess ||
+      per_cu < 1)
     per_cu = 1;
   const long pairs = (long)B * Hkv * plan->q_chunks;
   const long target = (long)cus * per_cu;
@@ -599,7 +656,8 @@ int launch_verify_attention(const void* q, const void* k_cache, const void* v_ca
   float* part_o = workspace ? (float*)((char*)workspace + plan.part_offset) : nullptr;
   float* part_ml = part_o ? part_o + (size_t)B * Hkv * plan.n_splits * R * D : nullptr;
   dim3 grid((unsigned)((long)plan.n_splits * plan.q_chunks * B * Hkv));
-  hipLaunchKernelGGL(pick_split(D, plan.nq, plan.q_chunks), grid, dim3(kThreads), 0, stream,
+  const int threads = plan.qg == 1 ? Shape<1>::kThreads : Shape<kMaxQG>::kThreads;
+  hipLaunchKernelGGL(pick_split(D, plan.nq, plan.qg, plan.q_chunks), grid, dim3(threads), 0, stream,
                      (const uint16_t*)q, (const uint16_t*)k_cache, (const uint16_t*)v_cache,
                      cache_mask, kv_len, gamma, out, part_o, part_ml, counters, B, gamma_max, Hq, Hkv,
                      L_cap, scale * kLog2e, plan.split_keys, plan.n_splits, plan.q_chunks, status);

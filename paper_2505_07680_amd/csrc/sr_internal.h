@@ -230,7 +230,8 @@ __device__ __forceinline__ void stores_done() {
 // validated by the C ABI layer.
 
 struct AttentionPlan {
-  int nq;          // 16-row query groups per workgroup
+  int nq;          // 16-row query blocks per wave
+  int qg;          // query groups (of four waves) per workgroup
   int q_chunks;    // workgroups along the query rows of one (sequence, kv head)
   int split_keys;  // keys per split (multiple of 32)
   int n_splits;    // splits along the cache

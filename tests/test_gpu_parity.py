@@ -299,12 +299,15 @@ def test_runs_are_bitwise_deterministic():
 
 
 # One shape per kernel instantiation the launch plan can pick: head dim 64 or
-# 128; 16-row query groups per workgroup nq = ceil(G (gamma_max + 1) / 16)
-# capped at 3 (1, 2, 3, and 3 with a second query chunk, where the K/V loads
-# carry no non-temporal hint); each with many cache splits (a few long
-# sequences) and with a single split (enough short sequences to fill the
-# device, no workspace).
-_INSTANCES = [(G, g, tag) for G, g, tag in ((4, 3, "nq1"), (4, 5, "nq2"), (4, 8, "nq3"), (8, 8, "nq3-2chunks"))]
+# 128; R = G (gamma_max + 1) query rows per kv head: up to 48 rows one group
+# of nq = ceil(R / 16) 16-row blocks per wave (nq1, nq2, nq3); beyond, two
+# query groups of two blocks (up to 64 rows) or three (up to 96 rows per
+# query chunk, then a second chunk, whose K/V loads carry no non-temporal
+# hint), also with ragged gamma so that a group can have no live rows; each
+# with many cache splits (a few long sequences) and with a single split
+# (enough short sequences to fill the device, no workspace).
+_INSTANCES = [(4, (3, 3), "nq1"), (4, (5, 5), "nq2"), (4, (8, 8), "nq3"), (8, (6, 6), "qg2-nq2"),
+              (8, (8, 8), "qg2-nq3"), (8, (0, 8), "qg2-nq3-ragged"), (8, (12, 12), "qg2-nq3-2chunks")]
 SHARP = [(D, G, g, tag, split) for D in (64, 128) for G, g, tag in _INSTANCES for split in ("splits", "onesplit")]
 
 
@@ -314,20 +317,22 @@ def test_sharp_softmax_attention(D, G, g, tag, split):
     are O(1) and the elementwise bound bites (Section 4.4, Eq. 8)."""
     import paper_2505_07680_amd as sr
 
-    seed = 240 + D + 10 * G + g
+    seed = 240 + D + 10 * G + g[1]
+    gmax = g[1]
     if split == "splits":
-        shape = small_shape(name=f"sharp-{tag}", B=2, Hq=2 * G, Hkv=2, D=D, gamma=(g, g), ctx=(2500, 3500),
+        B = 3 if g[0] < g[1] else 2
+        shape = small_shape(name=f"sharp-{tag}", B=B, Hq=2 * G, Hkv=2, D=D, gamma=g, ctx=(2500, 3500),
                             V=1000, seed=seed)
-        assert sr.specrouter_verify_attention_workspace_size(2, g, 2 * G, 2, D, shape.cap) > 0
+        assert sr.specrouter_verify_attention_workspace_size(B, gmax, 2 * G, 2, D, shape.cap) > 0
     else:
         Hkv, B = 16, 16
         while B < 512:
-            shape = small_shape(name=f"sharp1-{tag}", B=B, Hq=Hkv * G, Hkv=Hkv, D=D, gamma=(g, g),
+            shape = small_shape(name=f"sharp1-{tag}", B=B, Hq=Hkv * G, Hkv=Hkv, D=D, gamma=g,
                                 ctx=(60, 180), V=1000, seed=seed)
-            if sr.specrouter_verify_attention_workspace_size(B, g, Hkv * G, Hkv, D, shape.cap) == 0:
+            if sr.specrouter_verify_attention_workspace_size(B, gmax, Hkv * G, Hkv, D, shape.cap) == 0:
                 break  # one split: no partials, no workspace
             B *= 2
-        assert sr.specrouter_verify_attention_workspace_size(B, g, Hkv * G, Hkv, D, shape.cap) == 0
+        assert sr.specrouter_verify_attention_workspace_size(B, gmax, Hkv * G, Hkv, D, shape.cap) == 0
     inp = level_inputs(shape, logits=False)
     q = bf16_bits_from_f32(f32_from_bf16_bits(inp.q) * 8.0)
     got, _ = run_attention(inp, q=q)
