@@ -1498,8 +1498,22 @@ __global__ void __launch_bounds__(64 * kFinWaves) accept_finish_kernel(Args A) {
 //
 // One workgroup of 1024 threads per live row (verifier rows p_0..p_gamma,
 // draft rows q_0..q_{gamma-1}). Logits are compared through an
-// order-preserving 32-bit key (-0 counted as +0), and the threshold is found
-// by a most-significant-digit radix select: a 12-bit first digit (sign,
+// order-preserving 32-bit key (-0 counted as +0).
+//
+// Candidate path (one read of the row): every thread keeps the kFiltTop
+// largest keys it sees and the largest key it dropped; for top-p alone it
+// also sums the row's mass 2^(z log2(e)/T) (relative to a per-thread
+// reference, rescaled to the row maximum at the end, summed in thread
+// order). The kept keys (at most 1024 kFiltTop) go to LDS and the threshold
+// is selected among them by the radix select below. It is exact when every
+// key at or above the threshold is a candidate: top-k needs the largest
+// dropped key to be at most the k-th largest candidate (strictly below it
+// when top-p follows, whose input must then be complete); top-p alone needs
+// it strictly below the selected key and the candidates' mass from that key
+// up to reach p times the row's total (else a lower, dropped key could be
+// the threshold). A row that fails these checks takes the exact path.
+//
+// Exact path: a most-significant-digit radix select over the row: a 12-bit first digit (sign,
 // exponent and three mantissa bits, so that logits of one row spread over
 // many bins), then 10 + 10 bits for fp32 keys or 4 bits for bf16 keys (whose
 // low 16 bits are fixed by the sign). Each level histograms the digit of the
@@ -1530,6 +1544,7 @@ constexpr int kFiltWaves = kFiltThreads / 64;
 constexpr int kFiltBins = 4096;  // the widest digit: 12 bits
 constexpr int kFiltCap = 8064;   // candidate keys held in LDS (two workgroups fit a CU's 160 KB)
 constexpr int kFiltUnroll = 4;   // row loads in flight per thread
+constexpr int kFiltTop = 7;      // candidate keys kept per thread (1024 kFiltTop <= kFiltCap)
 constexpr double kFix = 1099511627776.0;  // 2^40: fixed-point scale of a mass term
 
 __device__ __forceinline__ uint32_t order_key(float z) {
@@ -1631,9 +1646,14 @@ __device__ __forceinline__ void filt_scan_row(const FiltRow<BF16>& R, Fn&& f) {
     for (int u = 0; u < kFiltUnroll; ++u) {
       const int v = v0 + u * kFiltThreads;
       if (v >= R.nvec) break;
+      if (R.valid(v, 0) && R.valid(v, N - 1)) {  // the whole vector lies in the row
 #pragma unroll
-      for (int k = 0; k < N; ++k)
-        if (R.valid(v, k)) f(z[u][k]);
+        for (int k = 0; k < N; ++k) f(z[u][k]);
+      } else {
+#pragma unroll
+        for (int k = 0; k < N; ++k)
+          if (R.valid(v, k)) f(z[u][k]);
+      }
     }
   }
 }
@@ -1769,6 +1789,112 @@ __device__ void filt_select_mass(FiltShared& F, int nb, float top_p, bool first,
   __syncthreads();
 }
 
+// The block-wide maximum of an unsigned key.
+__device__ __forceinline__ uint32_t filt_block_max(FiltShared& F, uint32_t x) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const uint32_t wm = (uint32_t)wave_max_i((int)(x ^ 0x80000000u)) ^ 0x80000000u;  // unsigned max
+  __syncthreads();  // earlier readers of F.wmax are done
+  if (lane == 0) F.wmax[w] = wm;
+  __syncthreads();
+  uint32_t m = 0u;
+  for (int i = 0; i < kFiltWaves; ++i) m = max(m, F.wmax[i]);
+  return m;
+}
+
+// Candidate path, the one read of the row: each thread's C largest keys
+// (kept in descending order by a min/max insertion network, 0 = empty) go to
+// F.cand (F.n of them, in thread order); returns the row's largest key and
+// the largest key any thread dropped (0 if none was dropped) and, with MASS,
+// the row's mass sum_z 2^((z - M) lg) for the row maximum M. Each thread sums
+// its terms relative to a reference that is raised, once per round of loads,
+// when the round's largest entry exceeds it by more than 2^8; the reference
+// is then rescaled to M and the threads' sums added in thread order. Rounds
+// whose vectors all lie inside the row skip the per-entry range test; in the
+// others, entries outside the row take key 0 and z = -inf (no effect on any
+// of these).
+template <bool BF16, bool MASS, int C>
+struct FiltCollect {
+  static constexpr int N = Vec<BF16>::N;
+  uint32_t top[C];
+  uint32_t ev = 0u, km = 0u;
+  double sum = 0.0;
+  float ref = kNegInf, lim = kNegInf;
+
+  template <bool MASKED>
+  __device__ __forceinline__ void round(const FiltRow<BF16>& R, int v0, float lg, float head) {
+    float z[kFiltUnroll][N];
+#pragma unroll
+    for (int u = 0; u < kFiltUnroll; ++u) R.load(MASKED ? min(v0 + u * kFiltThreads, R.nvec - 1) : v0 + u * kFiltThreads, z[u]);
+    float zmax = kNegInf;
+#pragma unroll
+    for (int u = 0; u < kFiltUnroll; ++u) {
+      const int v = v0 + u * kFiltThreads;
+#pragma unroll
+      for (int k = 0; k < N; ++k) {
+        const bool in = !MASKED || (v < R.nvec && R.valid(v, k));
+        if (MASKED) z[u][k] = in ? z[u][k] : kNegInf;
+        const uint32_t key = in ? order_key(z[u][k]) : 0u;
+        km = max(km, key);
+        ev = max(ev, min(top[C - 1], key));
+#pragma unroll
+        for (int i = C - 1; i > 0; --i) top[i] = max(top[i], min(top[i - 1], key));
+        top[0] = max(top[0], key);
+        if (MASS) zmax = fmaxf(zmax, z[u][k]);
+      }
+    }
+    if (MASS) {
+      if (zmax > lim) {  // (rare after the first rounds)
+        sum = ref == kNegInf ? 0.0 : sum * exp2((double)(ref - zmax) * (double)lg);
+        ref = zmax;
+        lim = zmax + head;
+      }
+      const float rl = ref == kNegInf ? 0.f : ref * lg;  // (ref = -inf: every entry so far is -inf)
+      float part = 0.f;
+#pragma unroll
+      for (int u = 0; u < kFiltUnroll; ++u)
+#pragma unroll
+        for (int k = 0; k < N; ++k) part += exp2_hw(fmaf(z[u][k], lg, -rl));
+      sum += (double)part;
+    }
+  }
+
+  __device__ void run(FiltShared& F, const FiltRow<BF16>& R, float lg, uint32_t& kmax, uint32_t& dropped,
+                      double& mass) {
+#pragma unroll
+    for (int i = 0; i < C; ++i) top[i] = 0u;
+    const float head = 8.f / lg;
+    // vectors [vlo, vhi] lie inside the row; a round covers kFiltThreads kFiltUnroll of them
+    const int vlo = R.phi > 0 ? 1 : 0;
+    const int vhi = (R.V + R.phi) / N - 1;
+    constexpr int kRound = kFiltThreads * kFiltUnroll;
+    for (int base = 0; base < R.nvec; base += kRound) {
+      const int v0 = base + (int)threadIdx.x;
+      if (base >= vlo && base + kRound - 1 <= vhi)  // workgroup-uniform
+        round<false>(R, v0, lg, head);
+      else
+        round<true>(R, v0, lg, head);
+    }
+    kmax = filt_block_max(F, km);
+    dropped = filt_block_max(F, ev);
+    if (MASS) {
+      const float M = key_value(kmax);
+      const double mine = ref == kNegInf ? 0.0 : sum * exp2((double)(ref - M) * (double)lg);
+      __syncthreads();  // F.wtot_d free
+      filt_excl_scan(F, mine, mass);
+    }
+    uint32_t c = 0u;
+#pragma unroll
+    for (int i = 0; i < C; ++i) c += top[i] != 0u ? 1u : 0u;
+    __syncthreads();  // F.wtot_u free
+    const uint32_t off = filt_excl_scan(F, c);
+#pragma unroll
+    for (int i = 0; i < C; ++i)
+      if (top[i] != 0u) F.cand[off + i] = top[i];
+    if (threadIdx.x == kFiltThreads - 1) F.n = off + c;
+    __syncthreads();
+  }
+};
+
 template <bool BF16>
 __global__ void __launch_bounds__(kFiltThreads) accept_filter_kernel(Args A, int top_k, float top_p) {
   constexpr int N = Vec<BF16>::N, esz = Vec<BF16>::esz;
@@ -1822,14 +1948,106 @@ __global__ void __launch_bounds__(kFiltThreads) accept_filter_kernel(Args A, int
     for (int i = 0; i < kFiltWaves; ++i) m = max(m, F.wmax[i]);
     return m;
   };
+  // ---- candidate path
+  uint32_t thr_key = 0u;
+  bool fast_ok = false;
+  {
+    const bool mass_needed = top_k == 0 && top_p < 1.f;
+    uint32_t ckmax = 0u, dropped = 0u;
+    double W = 0.0;
+    // top-k alone with k <= 64 keeps three candidates per thread (more than
+    // three of the k largest in one thread's share is rare), else seven
+    if (mass_needed) {
+      FiltCollect<BF16, true, kFiltTop> fc;
+      fc.run(F, R, A.lg, ckmax, dropped, W);
+    } else if (top_p >= 1.f && top_k <= 64) {
+      FiltCollect<BF16, false, 3> fc;
+      fc.run(F, R, A.lg, ckmax, dropped, W);
+    } else {
+      FiltCollect<BF16, false, kFiltTop> fc;
+      fc.run(F, R, A.lg, ckmax, dropped, W);
+    }
+    const float M = key_value(ckmax);
+    // The thresholds from the nc keys in F.cand, which hold every key above
+    // drop. True when exact; otherwise bound is a key at or below the true
+    // threshold (the candidates' own threshold: keys missing from them only
+    // lower it), or 0 when there is none.
+    auto select = [&](int nc, uint32_t drop, uint32_t& bound) -> bool {
+      bound = 0u;
+      if (top_k > nc) return false;  // fewer candidates than k
+      uint32_t lo = 0u;
+      if (top_k > 0) {  // the k-th largest candidate
+        uint32_t prefix = 0u, pmask = 0u, need = (uint32_t)top_k;
+        for (int l = 0; l < kLevels; ++l) {
+          const int sh = filt_shift<BF16>(l), nb = 1 << filt_bits<BF16>(l);
+          clear(nb);
+          filt_hist_cand<false>(F, nc, prefix, pmask, sh, (uint32_t)nb - 1u, 0u, 0.f, 0.f);
+          __syncthreads();
+          filt_select_count(F, nb, need);
+          need = F.need;
+          prefix |= F.pick << sh;
+          pmask |= ((uint32_t)nb - 1u) << sh;
+        }
+        if (BF16) prefix |= (prefix & 0x80000000u) ? 0u : 0xffffu;  // the fixed low half of bf16 keys
+        lo = prefix;
+        // every key at or above lo is a candidate (strictly above drop when
+        // top-p follows: its input must be complete)
+        if (!(top_p < 1.f ? drop < lo : drop <= lo)) {
+          bound = lo;
+          return false;
+        }
+      }
+      thr_key = lo;
+      if (top_p < 1.f) {  // top-p over the candidates top-k kept
+        __syncthreads();
+        if (tid == 0) {
+          F.above = 0.0;
+          F.total = W;  // top-p alone: the row's mass (after top-k: the first level's total)
+        }
+        __syncthreads();
+        uint32_t prefix = 0u, pmask = 0u;
+        double incl = 0.0;
+        for (int l = 0; l < kLevels; ++l) {
+          const int sh = filt_shift<BF16>(l), nb = 1 << filt_bits<BF16>(l);
+          clear(nb);
+          filt_hist_cand<true>(F, nc, prefix, pmask, sh, (uint32_t)nb - 1u, lo, M, A.lg);
+          __syncthreads();
+          filt_select_mass(F, nb, top_p, l == 0 && top_k > 0, false, sh, M, A.lg);
+          prefix |= F.pick << sh;
+          pmask |= ((uint32_t)nb - 1u) << sh;
+          incl = F.above + (double)F.mass[F.pick] / kFix;  // candidates' mass from the selected bin up
+        }
+        if (BF16) prefix |= (prefix & 0x80000000u) ? 0u : 0xffffu;
+        thr_key = prefix;
+        if (top_k == 0 && !(drop < thr_key && (incl >= (double)top_p * W || drop == 0u))) {
+          bound = thr_key;
+          return false;
+        }
+      }
+      return true;
+    };
+    uint32_t bound = 0u;
+    fast_ok = select((int)F.n, dropped, bound);
+    if (!fast_ok && bound > 0u) {
+      // a second read gathers every key at or above bound (none below it is
+      // then a candidate), when they fit in LDS
+      const int n2 = gather(bound, 0xffffffffu);
+      if (F.n <= (uint32_t)kFiltCap) {
+        uint32_t unused;
+        fast_ok = select(n2, bound - 1u, unused);
+      }
+    }
+  }
+
   int ncand = 0;         // keys in F.cand
   bool cand_ge = false;  // F.cand holds every key >= lo
   uint32_t lo = 0u;      // keys below lo are removed
   uint32_t kmax = 0u;
   bool first_read_done = false;  // a top-p first level over the row is already in the histogram
 
-  // ---- top-k: radix select of the k-th largest key
-  if (top_k > 0) {
+  // ---- exact path (rows the candidates do not settle)
+  // top-k: radix select of the k-th largest key
+  if (!fast_ok && top_k > 0) {
     uint32_t prefix = 0u, pmask = 0u, need = (uint32_t)top_k;
     bool in_lds = false;
     for (int l = 0; l < kLevels; ++l) {
@@ -1857,7 +2075,7 @@ __global__ void __launch_bounds__(kFiltThreads) accept_filter_kernel(Args A, int
     }
     if (BF16) prefix |= (prefix & 0x80000000u) ? 0u : 0xffffu;  // the fixed low half of bf16 keys
     lo = prefix;
-  } else if (top_p < 1.f) {
+  } else if (!fast_ok && top_p < 1.f) {
     // top-p alone: the first level's counts, masses (relative to each bin's
     // top) and the row maximum in one read
     clear(1 << filt_bits<BF16>(0));
@@ -1868,8 +2086,8 @@ __global__ void __launch_bounds__(kFiltThreads) accept_filter_kernel(Args A, int
   }
 
   // ---- top-p over the keys top-k kept
-  uint32_t thr_key = lo;
-  if (top_p < 1.f) {
+  if (!fast_ok) thr_key = lo;
+  if (!fast_ok && top_p < 1.f) {
     const float M = key_value(block_max(kmax));
     if (tid == 0) F.above = 0.0;
     __syncthreads();

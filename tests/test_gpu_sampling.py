@@ -221,3 +221,21 @@ def test_filtered_config2_shape():
     assert got["status"] == 0
     keep = [b for b in seqs if not ref["filter_boundary"][b]]
     check_accept(got, ref, seqs=keep)
+
+
+@pytest.mark.parametrize("logits", ["f32", "bf16"])
+def test_filtered_calls_are_bitwise_deterministic(logits):
+    """Top-p decides on bin masses summed by LDS atomics in whatever order the
+    lanes arrive; as fixed-point integers those sums, and so every decision
+    and output, must not depend on that order (Section 4.1's logits
+    processors): repeated calls give identical bits."""
+    shape = small_shape(name=f"det-{logits}", B=16, V=128256, gamma=(3, 6), seed=47, logits=logits)
+    inp = level_inputs(shape, kv=False)
+    for k, p in ((0, 0.9), (50, 0.9), (50, 1.0)):
+        runs = [run_accept(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, inp.u_acc, inp.u_res,
+                           temperature=0.7, top_k=k, top_p=p) for _ in range(3)]
+        assert runs[0]["status"] == 0
+        for r in runs[1:]:
+            for key in runs[0]:
+                np.testing.assert_array_equal(np.asarray(r[key]), np.asarray(runs[0][key]), err_msg=f"{key} k={k} p={p}")
+        say(f"filtered determinism {logits} top_k {k} top_p {p}: 3 identical calls")
