@@ -239,3 +239,65 @@ def test_filtered_calls_are_bitwise_deterministic(logits):
             for key in runs[0]:
                 np.testing.assert_array_equal(np.asarray(r[key]), np.asarray(runs[0][key]), err_msg=f"{key} k={k} p={p}")
         say(f"filtered determinism {logits} top_k {k} top_p {p}: 3 identical calls")
+
+
+def _concentrate(z, dtype, n_hot, level, rng):
+    """Raise n_hot entries of every row, all in the share of the filter's
+    first thread (16-byte vectors 0, 1024, 2048, ... of a row whose start is
+    16-byte aligned), to about `level`."""
+    per_vec = 4 if dtype == "f32" else 8
+    pos = np.array([1024 * per_vec * m + i for m in range(n_hot) for i in range(per_vec)])[:n_hot]
+    out = z.copy()
+    out[..., pos] = level + 0.05 * rng.standard_normal(out[..., pos].shape)
+    return out
+
+
+@pytest.mark.parametrize("logits", ["f32", "bf16"])
+@pytest.mark.parametrize("top_k,top_p,n_hot,level", [(50, 1.0, 40, 12.0), (0, 0.9, 30, 14.0), (50, 0.9, 40, 12.0)])
+def test_filter_when_the_largest_keys_crowd_one_thread(logits, top_k, top_p, n_hot, level):
+    """Most of the kept keys sit in one thread's share of the row, more than
+    the keys a thread keeps as candidates: the one-read selection cannot
+    vouch for its threshold and gathers the keys above its own (lower)
+    threshold in a second read; results match the reference (Section 4.1's
+    logits processors)."""
+    from oracle.accept import decode_logits
+
+    V = 128256  # rows 16-byte aligned in both dtypes
+    shape = small_shape(name=f"crowd-{logits}", B=3, V=V, gamma=(1, 2), seed=73, logits=logits)
+    inp = level_inputs(shape, kv=False)
+    rng = np.random.default_rng(73)
+    p = _concentrate(decode_logits(inp.p_logits), logits, n_hot, level, rng)
+    q = _concentrate(decode_logits(inp.q_logits), logits, n_hot, level, rng)
+    if logits == "bf16":
+        p, q = bf16_bits_from_f32(p.astype(np.float32)), bf16_bits_from_f32(q.astype(np.float32))
+    else:
+        p, q = p.astype(np.float32), q.astype(np.float32)
+    got = run_accept(p, q, inp.drafts, inp.gamma, inp.u_acc, inp.u_res, temperature=1.0, top_k=top_k, top_p=top_p)
+    ref = oracle.accept_and_diverge(p, q, inp.drafts, inp.gamma, inp.u_acc, inp.u_res, temperature=1.0,
+                                    top_k=top_k, top_p=top_p)
+    assert got["status"] == ref["status"] == 0
+    nf, nb, nbm = _check_filtered(got, ref)
+    assert nf < shape.B
+    say(f"crowded {logits} top_k={top_k} top_p={top_p}: ok ({nf} filter-boundary skipped)")
+
+
+@pytest.mark.parametrize("logits", ["f32", "bf16"])
+def test_top_p_keeping_most_of_a_flat_row(logits):
+    """Nearly equal logits: top-p 0.9 keeps about 90% of 20000 keys, more
+    than the candidates and more than LDS holds, so the threshold comes from
+    the radix select over the row itself."""
+    shape = small_shape(name=f"flat-{logits}", B=4, V=20000, gamma=(1, 2), seed=74, logits=logits)
+    inp = level_inputs(shape, kv=False)
+    rng = np.random.default_rng(74)
+    # 64 distinct values (ties of ~300 keys), so that the cumulative masses
+    # move in steps well above the boundary margin
+    z = lambda like: (0.05 * rng.integers(0, 64, like.shape) / 64.0).astype(np.float32)  # noqa: E731
+    p, q = z(inp.p_logits), z(inp.q_logits)
+    if logits == "bf16":
+        p, q = bf16_bits_from_f32(p), bf16_bits_from_f32(q)
+    got = run_accept(p, q, inp.drafts, inp.gamma, inp.u_acc, inp.u_res, temperature=1.0, top_p=0.9)
+    ref = oracle.accept_and_diverge(p, q, inp.drafts, inp.gamma, inp.u_acc, inp.u_res, temperature=1.0, top_p=0.9)
+    assert got["status"] == ref["status"] == 0
+    nf, nb, nbm = _check_filtered(got, ref)
+    assert nf < shape.B
+    say(f"flat {logits} top_p 0.9: ok ({nf} filter-boundary skipped)")
