@@ -1663,7 +1663,7 @@ __device__ __forceinline__ void filt_scan_row(const FiltRow<BF16>& R, Fn&& f) {
 // Masses (MASS): relative to M (rel_bin false), or to the top of each
 // first-level bin (rel_bin true, prefix empty).
 template <bool BF16, bool MASS>
-__device__ void filt_hist_row(FiltShared& F, const FiltRow<BF16>& R, uint32_t prefix, uint32_t pmask, int shift,
+__device__ __forceinline__ void filt_hist_row(FiltShared& F, const FiltRow<BF16>& R, uint32_t prefix, uint32_t pmask, int shift,
                               uint32_t dmask, uint32_t lo, float M, float lg, bool rel_bin, uint32_t& kmax) {
   filt_scan_row<BF16>(R, [&](float z) {
     const uint32_t key = order_key(z);
@@ -1681,7 +1681,7 @@ __device__ void filt_hist_row(FiltShared& F, const FiltRow<BF16>& R, uint32_t pr
 
 // The same over the n candidate keys in LDS (masses relative to M).
 template <bool MASS>
-__device__ void filt_hist_cand(FiltShared& F, int n, uint32_t prefix, uint32_t pmask, int shift, uint32_t dmask,
+__device__ __forceinline__ void filt_hist_cand(FiltShared& F, int n, uint32_t prefix, uint32_t pmask, int shift, uint32_t dmask,
                                uint32_t lo, float M, float lg) {
   for (int i = threadIdx.x; i < n; i += kFiltThreads) {
     const uint32_t key = F.cand[i];
@@ -1698,7 +1698,7 @@ __device__ void filt_hist_cand(FiltShared& F, int n, uint32_t prefix, uint32_t p
 // Gathers the row's keys in [klo, khi] into F.cand (F.n counts them; the
 // caller has checked that they fit).
 template <bool BF16>
-__device__ void filt_gather_row(FiltShared& F, const FiltRow<BF16>& R, uint32_t klo, uint32_t khi) {
+__device__ __forceinline__ void filt_gather_row(FiltShared& F, const FiltRow<BF16>& R, uint32_t klo, uint32_t khi) {
   filt_scan_row<BF16>(R, [&](float z) {
     const uint32_t key = order_key(z);
     if (key >= klo && key <= khi) {
@@ -1719,7 +1719,7 @@ struct FiltOwn {
 };
 
 // top-k: the bin holding the need-th largest key of the histogram.
-__device__ void filt_select_count(FiltShared& F, int nb, uint32_t need) {
+__device__ __forceinline__ void filt_select_count(FiltShared& F, int nb, uint32_t need) {
   const FiltOwn o(nb);
   uint32_t c[4], s = 0u;
 #pragma unroll
@@ -1744,7 +1744,7 @@ __device__ void filt_select_count(FiltShared& F, int nb, uint32_t need) {
 // total (the total is this histogram's at the first level). Bin masses are
 // in units of 2^(M lg); first-level row histograms hold them relative to the
 // top of each bin (rel_bin) and are rescaled here.
-__device__ void filt_select_mass(FiltShared& F, int nb, float top_p, bool first, bool rel_bin, int shift, float M,
+__device__ __forceinline__ void filt_select_mass(FiltShared& F, int nb, float top_p, bool first, bool rel_bin, int shift, float M,
                                  float lg) {
   const FiltOwn o(nb);
   const double above = F.above;
@@ -1858,8 +1858,8 @@ struct FiltCollect {
     }
   }
 
-  __device__ void run(FiltShared& F, const FiltRow<BF16>& R, float lg, uint32_t& kmax, uint32_t& dropped,
-                      double& mass) {
+  __device__ __forceinline__ void run(FiltShared& F, const FiltRow<BF16>& R, float lg, uint32_t& kmax,
+                                      uint32_t& dropped, double& mass) {
 #pragma unroll
     for (int i = 0; i < C; ++i) top[i] = 0u;
     const float head = 8.f / lg;
@@ -1915,7 +1915,7 @@ __global__ void __launch_bounds__(kFiltThreads) accept_filter_kernel(Args A, int
                           : (const char*)A.p + ((int64_t)b * A.p_stride + (int64_t)j * A.V - R.phi) * esz;
   R.rs = make_rsrc(base, (size_t)R.nvec * 16);
 
-  auto clear = [&](int nb) {
+  auto clear = [&](int nb) __attribute__((always_inline)) {
     __syncthreads();  // every thread is done with the previous level's histogram and picks
     for (int i = tid; i < nb; i += kFiltThreads) {
       F.cnt[i] = 0u;
@@ -1931,7 +1931,7 @@ __global__ void __launch_bounds__(kFiltThreads) accept_filter_kernel(Args A, int
     __syncthreads();
   };
   // Gathers the keys in [klo, khi] into F.cand; returns their count.
-  auto gather = [&](uint32_t klo, uint32_t khi) {
+  auto gather = [&](uint32_t klo, uint32_t khi) __attribute__((always_inline)) {
     __syncthreads();  // every thread has read the picks (and is done with F.cand)
     if (tid == 0) F.n = 0u;
     __syncthreads();
@@ -1940,7 +1940,7 @@ __global__ void __launch_bounds__(kFiltThreads) accept_filter_kernel(Args A, int
     return (int)min(F.n, (uint32_t)kFiltCap);
   };
   // The block-wide maximum of kmax.
-  auto block_max = [&](uint32_t kmax) {
+  auto block_max = [&](uint32_t kmax) __attribute__((always_inline)) {
     const uint32_t wm = (uint32_t)wave_max_i((int)(kmax ^ 0x80000000u)) ^ 0x80000000u;  // unsigned max
     if (lane == 0) F.wmax[w] = wm;
     __syncthreads();
@@ -1972,7 +1972,7 @@ __global__ void __launch_bounds__(kFiltThreads) accept_filter_kernel(Args A, int
     // drop. True when exact; otherwise bound is a key at or below the true
     // threshold (the candidates' own threshold: keys missing from them only
     // lower it), or 0 when there is none.
-    auto select = [&](int nc, uint32_t drop, uint32_t& bound) -> bool {
+    auto select = [&](int nc, uint32_t drop, uint32_t& bound) __attribute__((always_inline)) -> bool {
       bound = 0u;
       if (top_k > nc) return false;  // fewer candidates than k
       uint32_t lo = 0u;
