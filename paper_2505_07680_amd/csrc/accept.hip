@@ -1261,6 +1261,35 @@ __device__ RowOut finalize_row(const Args& A, int b, int j, int gam, const __amd
 // ---------------------------------------------------------------------------
 // Sequence finisher (one wave)
 
+// A sequence's per-position inputs as wave 0 holds them (lane j: position j),
+// loaded when the finish kernel starts so that they are in registers when
+// the accept chain needs them.
+struct SeqIn {
+  int x;         // draft token x_j (lane < gamma), else -1
+  float ua, ur;  // u_acc[j], u_res[j]
+  int kvl, rb_old;
+};
+
+template <bool GREEDY>
+__device__ __forceinline__ SeqIn load_seq_inputs(const Args& A, int b, int gam) {
+  const int lane = threadIdx.x & 63;
+  const int G1 = A.gmax + 1;
+  SeqIn in;
+  in.x = -1;
+  in.ua = 0.f;
+  in.ur = 0.f;
+  if (lane <= gam) {
+    if (lane < gam) in.x = A.drafts[(size_t)b * A.gmax + lane];
+    if (!GREEDY) {
+      if (lane < gam) in.ua = A.u_acc[(size_t)b * A.gmax + lane];
+      in.ur = A.u_res[(size_t)b * G1 + lane];
+    }
+  }
+  in.kvl = A.kv_len ? A.kv_len[b] : 0;
+  in.rb_old = A.rb_kv ? A.rb_kv[b] : 0;
+  return in;
+}
+
 // What the finisher's waves share.
 struct FinShared {
   DrawShared ds;
@@ -1275,7 +1304,7 @@ struct FinShared {
 // wave zeroes the sequence's workspace words.
 template <bool BF16, bool GREEDY>
 __device__ void finish_sequence(const Args& A, int b, int gam, const RowOut* rows, const DrawPlan* plans,
-                                FinShared& fs) {
+                                const SeqIn& in, FinShared& fs) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int G1 = A.gmax + 1;
   int x = -1;
@@ -1283,14 +1312,10 @@ __device__ void finish_sequence(const Args& A, int b, int gam, const RowOut* row
   float o_p = 0.f, o_q = 0.f, o_kl = 0.f, o_tv = 0.f;
   int kvl = 0, rb_old = 0;
   if (w == 0) {
-    float ua = 0.f, ur = 0.f;
+    const float ua = in.ua, ur = in.ur;
+    x = in.x;
     int argp = -1;
     if (lane <= gam) {
-      if (lane < gam) x = A.drafts[(size_t)b * A.gmax + lane];
-      if (!GREEDY) {
-        if (lane < gam) ua = A.u_acc[(size_t)b * A.gmax + lane];
-        ur = A.u_res[(size_t)b * G1 + lane];
-      }
       const RowOut& ro = rows[lane];
       a = ro.a;
       o_p = ro.p_tok;
@@ -1299,8 +1324,8 @@ __device__ void finish_sequence(const Args& A, int b, int gam, const RowOut* row
       o_tv = ro.tv;
       argp = ro.argp;
     }
-    kvl = A.kv_len ? A.kv_len[b] : 0;
-    rb_old = A.rb_kv ? A.rb_kv[b] : 0;
+    kvl = in.kvl;
+    rb_old = in.rb_old;
     // data checks
     uint32_t bad = 0;
     if (lane < gam) {
@@ -1480,6 +1505,8 @@ __global__ void __launch_bounds__(64 * kFinWaves) accept_finish_kernel(Args A) {
     }
     return;
   }
+  SeqIn in;
+  if (w == 0) in = load_seq_inputs<GREEDY>(A, b, gam);
   const __amdgpu_buffer_rsrc_t rs_recs = make_rsrc(A.recs, (size_t)A.B * (A.gmax + 1) * A.nc * kRecBytes);
   for (int j = w; j <= gam; j += kFinWaves) {
     DrawPlan plan;
@@ -1490,7 +1517,7 @@ __global__ void __launch_bounds__(64 * kFinWaves) accept_finish_kernel(Args A) {
     }
   }
   __syncthreads();
-  finish_sequence<BF16, GREEDY>(A, b, gam, s_out, s_plan, fs);
+  finish_sequence<BF16, GREEDY>(A, b, gam, s_out, s_plan, in, fs);
 }
 
 // ============================================================================
