@@ -178,7 +178,7 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int w = tid >> 6;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, so branches on it are scalar
   const int ws = w % kWaves;  // key stream
   const int h = w / kWaves;   // query group: rows rbase .. rbase + MQ - 1
   const int rbase = row0 + h * MQ;
@@ -325,14 +325,19 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
         // exceeds it by more than kLazy (log2 units), so P stays below
         // 2^kLazy and the output accumulators are rescaled only then
         // (skipped by the whole wave when no row needs it).
+        // (straight-line: every exponential is computed and selected, no
+        // per-entry branches)
         const bool grow = mt > m_run[qg] + kLazy;
         const float mref = grow ? mt : m_run[qg];
-        const float alpha = grow ? (m_run[qg] == kNegInf ? 0.f : exp2_hw(m_run[qg] - mt)) : 1.f;
+        // exp2(-inf) = 0 covers a first reference (the old one -inf); equal
+        // references, -inf ones included, give 1
+        const float alpha = m_run[qg] == mref ? 1.f : exp2_hw(m_run[qg] - mref);
+        const float mr = mref == kNegInf ? 0.f : mref;  // (-inf: every score of the row so far is -inf)
         float pk[4];
         float ls = 0.f;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          pk[e] = mref == kNegInf ? 0.f : (full ? exp2_hw(fmaf(s[e], scale_log2, -mref)) : exp2_hw(s[e] - mref));
+          pk[e] = exp2_hw(full ? fmaf(s[e], scale_log2, -mr) : s[e] - mr);
           ls += pk[e];
         }
         ls = sum_across_rows(ls);
