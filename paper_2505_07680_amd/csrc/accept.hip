@@ -1032,7 +1032,7 @@ struct DrawShared {
 template <bool BF16>
 __device__ int draw_scan(const Args& A, int b, int k, const DrawPlan& d, DrawShared& ds) {
   constexpr int kE = Vec<BF16>::E;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, w = wave_id();
   float wt[kE];
   int mine = -1;
   double lsum = 0.0, pincl = 0.0;
@@ -1305,7 +1305,7 @@ struct FinShared {
 template <bool BF16, bool GREEDY>
 __device__ void finish_sequence(const Args& A, int b, int gam, const RowOut* rows, const DrawPlan* plans,
                                 const SeqIn& in, FinShared& fs) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, w = wave_id();
   const int G1 = A.gmax + 1;
   int x = -1;
   double a = 0.0;
@@ -1495,7 +1495,7 @@ __global__ void __launch_bounds__(64 * kFinWaves) accept_finish_kernel(Args A) {
   __shared__ RowOut s_out[kMaxRows];
   __shared__ DrawPlan s_plan[kMaxRows];
   __shared__ FinShared fs;
-  const int b = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int b = blockIdx.x, lane = threadIdx.x & 63, w = wave_id();
   const int gam = A.gamma[b];
   if (!(gam >= 0 && gam <= A.gmax)) {
     if (w == 0) {
@@ -1613,7 +1613,7 @@ __device__ __forceinline__ int filt_bits(int l) {
 
 // Block-wide exclusive prefix sums in thread order (a fixed order).
 __device__ __forceinline__ uint32_t filt_excl_scan(FiltShared& F, uint32_t s) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, w = wave_id();
   const uint32_t incl = (uint32_t)wave_incl_scan_i((int)s);
   if (lane == 63) F.wtot_u[w] = incl;
   __syncthreads();
@@ -1622,7 +1622,7 @@ __device__ __forceinline__ uint32_t filt_excl_scan(FiltShared& F, uint32_t s) {
   return base + incl - s;
 }
 __device__ __forceinline__ double filt_excl_scan(FiltShared& F, double s, double& total) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, w = wave_id();
   const double incl = wave_incl_scan_d(s);
   if (lane == 63) F.wtot_d[w] = incl;
   __syncthreads();
@@ -1818,7 +1818,7 @@ __device__ __forceinline__ void filt_select_mass(FiltShared& F, int nb, float to
 
 // The block-wide maximum of an unsigned key.
 __device__ __forceinline__ uint32_t filt_block_max(FiltShared& F, uint32_t x) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, w = wave_id();
   const uint32_t wm = (uint32_t)wave_max_i((int)(x ^ 0x80000000u)) ^ 0x80000000u;  // unsigned max
   __syncthreads();  // earlier readers of F.wmax are done
   if (lane == 0) F.wmax[w] = wm;
@@ -1927,7 +1927,7 @@ __global__ void __launch_bounds__(kFiltThreads) accept_filter_kernel(Args A, int
   constexpr int N = Vec<BF16>::N, esz = Vec<BF16>::esz;
   constexpr int kLevels = BF16 ? 2 : 3;
   __shared__ FiltShared F;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int per_seq = 2 * A.gmax + 1;  // p rows 0..gmax, then q rows 0..gmax-1
   const int b = (int)blockIdx.x / per_seq, r = (int)blockIdx.x % per_seq;
   const bool is_q = r > A.gmax;

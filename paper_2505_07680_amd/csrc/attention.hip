@@ -178,7 +178,7 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, so branches on it are scalar
+  const int w = wave_id();
   const int ws = w % kWaves;  // key stream
   const int h = w / kWaves;   // query group: rows rbase .. rbase + MQ - 1
   const int rbase = row0 + h * MQ;

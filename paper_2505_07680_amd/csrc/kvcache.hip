@@ -128,7 +128,7 @@ kv_compact_mask_kernel(uint8_t* __restrict__ mask, int32_t* __restrict__ kv_len,
   }
   int cnt = 0;
   for (int p = threadIdx.x; p < L; p += kKvThreads) cnt += mask[(size_t)b * L_cap + p] != 0;
-  const int w = threadIdx.x >> 6;
+  const int w = wave_id();
   const int tot = wave_incl_scan_i(cnt);
   if ((threadIdx.x & 63) == 63) s_part[w] = tot;
   __syncthreads();

@@ -46,7 +46,7 @@ rollback_kernel(int32_t* __restrict__ kv_len, uint8_t* __restrict__ mask,
     mx = max(mx, __shfl_xor(mx, off, 64));
     st |= __shfl_xor(st, off, 64);
   }
-  const int w = threadIdx.x >> 6;
+  const int w = wave_id();
   if ((threadIdx.x & 63) == 0) {
     red_max[w] = mx;
     red_st[w] = st;

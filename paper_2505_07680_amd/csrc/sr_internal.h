@@ -17,6 +17,9 @@ constexpr float kNegInf = -__builtin_inff();
 
 // Hardware 2^x (one instruction; results below 2^-126 flush to zero).
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+// The wave's index in its workgroup, as a wave-uniform (scalar) value, so that
+// branches on it are scalar branches rather than exec-mask regions.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
 
 // Buffer resource for raw buffer loads/stores over [base, base + bytes):
 // offsets are 32-bit and accesses past the end read zero / are dropped.
