@@ -69,7 +69,9 @@ constexpr int kStreamLoad = 2;
 template <int D>
 struct Geo {
   static constexpr int kKStride = D * 2 + 16;  // LDS bytes per staged K (and Q) row
-  static constexpr int kVStride = D * 2 + 8;   // LDS bytes per staged V row
+  // LDS bytes per staged V row: four consecutive rows' 32-byte column blocks
+  // fall on different banks for the transposing reads of the V^T operand
+  static constexpr int kVStride = D * 2 + 32;
   static constexpr int kChunksPerRow = D / 8;  // 16-byte chunks per row
   static constexpr int kRowsPerLoad = 64 / kChunksPerRow;
   static constexpr int kLoads = kWaveKeys / kRowsPerLoad;  // 16-byte loads per lane per tensor per tile
@@ -353,14 +355,14 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
       }
     }
     // ---- O^T += V^T P^T (K = 16 keys)
+    // The V^T operand (lane: column l16 of the block, keys lg*4 .. lg*4+3) by
+    // the LDS transposing read: in each 16-lane group, lane j names the four
+    // columns 4 (j mod 4) .. +3 of key row lg*4 + j/4, and lane i receives
+    // column i of the group's four key rows.
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      const unsigned char* vcol = vst + (lg * 4) * GG::kVStride + (db * 16 + l16) * 2;
-      const uint32_t v0 = *(const uint16_t*)(vcol);
-      const uint32_t v1 = *(const uint16_t*)(vcol + GG::kVStride);
-      const uint32_t v2 = *(const uint16_t*)(vcol + 2 * GG::kVStride);
-      const uint32_t v3 = *(const uint16_t*)(vcol + 3 * GG::kVStride);
-      const shortx4 va = __builtin_bit_cast(shortx4, make_uint2(v0 | (v1 << 16), v2 | (v3 << 16)));
+      const unsigned char* vrow = vst + (lg * 4 + (l16 >> 2)) * GG::kVStride + (db * 16 + (l16 & 3) * 4) * 2;
+      const shortx4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) shortx4*)vrow);
 #pragma unroll
       for (int qg = 0; qg < NQ; ++qg) {
         if (rbase + qg * 16 < Mb) o[db][qg] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb[qg], o[db][qg], 0, 0, 0);
