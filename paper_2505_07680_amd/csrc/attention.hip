@@ -133,8 +133,10 @@ struct Stage {  // one wave's part of a 16-key tile in flight
   uint32_t mbyte;  // validity byte of key (lane mod 16), evaluated when consumed
 };
 
+// Waves per SIMD the register allocation must allow: three for one row block
+// (168 registers), else two (256).
 template <int D, int NQ, int QG, bool NT>
-__global__ void __launch_bounds__(Shape<QG>::kThreads, 2)
+__global__ void __launch_bounds__(Shape<QG>::kThreads, NQ == 1 && QG == 1 ? 3 : 2)
 attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
                   const uint16_t* __restrict__ vc, const uint8_t* __restrict__ mask,
                   const int32_t* __restrict__ kv_len, const int32_t* __restrict__ gamma,
@@ -289,16 +291,19 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
     for (int ks = 0; ks < D / 32; ++ks) {
       const int col = (ks * 32 + lg * 8) * 2;
       const bf16x8 ka = *(const bf16x8*)(kst + l16 * GG::kKStride + col);
+      bf16x8 qb[NQ];
 #pragma unroll
-      for (int qg = 0; qg < NQ; ++qg) {
-        if (rbase + qg * 16 < Mb) {
-          const bf16x8 qb = *(const bf16x8*)(qst + (h * MQ + qg * 16 + l16) * GG::kKStride + col);
-          sacc[qg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb, sacc[qg], 0, 0, 0);
-        }
-      }
+      for (int qg = 0; qg < NQ; ++qg) qb[qg] = *(const bf16x8*)(qst + (h * MQ + qg * 16 + l16) * GG::kKStride + col);
+#pragma unroll
+      for (int qg = 0; qg < NQ; ++qg) sacc[qg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb[qg], sacc[qg], 0, 0, 0);
     }
     // ---- mask, online softmax, P in bf16 (lane: keys lg*4 + e of query l16)
+    // Row blocks without live rows go through both products too (on zero
+    // query rows and zero P): a branch around each MFMA costs more than the
+    // MFMA. Only the softmax is skipped for them.
     shortx4 pb[NQ];
+#pragma unroll
+    for (int qg = 0; qg < NQ; ++qg) pb[qg] = shortx4{0, 0, 0, 0};
 #pragma unroll
     for (int qg = 0; qg < NQ; ++qg) {
       if (rbase + qg * 16 < Mb) {
@@ -365,7 +370,7 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
       const shortx4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) shortx4*)vrow);
 #pragma unroll
       for (int qg = 0; qg < NQ; ++qg) {
-        if (rbase + qg * 16 < Mb) o[db][qg] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb[qg], o[db][qg], 0, 0, 0);
+        o[db][qg] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb[qg], o[db][qg], 0, 0, 0);
       }
     }
     // One query group: this tile's LDS reads are issued before the slot is
