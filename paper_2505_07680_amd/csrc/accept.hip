@@ -394,8 +394,7 @@ __device__ __forceinline__ uint32_t rec_off(int row, int nc, int c) {
 struct TaskShared {
   float m[2][kWaves];      // the waves' maxima of p and q
   double s[3][kWaves];     // the waves' sums (p, q, KL numerator; greedy: argmax indices in s[0..1])
-  float rho;               // TV parameters of the task's chunk
-  int swap;
+  float rho_p, rho_q;      // TV parameters of the task's chunk
   int ok;                  // the row's records were all present in time
 };
 
@@ -696,36 +695,35 @@ __device__ __forceinline__ double factor(float r, const Norm& n) {
   return (r == kNegInf || !(n.S > 0.0)) ? 0.0 : pow2(r, n.rM) / n.S;
 }
 
-// The TV sum of a chunk with factors fp, fq is scale * sum |fma(a, rho, -b)|,
-// (a, b) = (e_q, e_p) if swap else (e_p, e_q): the larger factor is scale, the
-// ratio rho <= 1 multiplies the other side (rows with equal factors subtract
-// exactly).
+// The TV sum of a chunk with factors fp, fq is scale * sum |fma(e_p, rho_p,
+// -e_q rho_q)|: the larger factor is scale, and of the two ratios rho = f/scale
+// the larger side's is exactly 1 (so rows with equal factors subtract
+// exactly, and the product on that side is exact).
 struct TvPar {
   double scale;
-  float rho;
-  bool swap;
+  float rho_p, rho_q;
 };
 __device__ __forceinline__ TvPar tv_par(double fp, double fq) {
   TvPar t;
-  t.swap = fp > fq;
-  t.scale = t.swap ? fp : fq;
-  t.rho = t.scale > 0.0 ? (float)((t.swap ? fq : fp) / t.scale) : 0.f;
+  t.scale = fp > fq ? fp : fq;
+  t.rho_p = t.scale > 0.0 ? (float)(fp / t.scale) : 0.f;
+  t.rho_q = t.scale > 0.0 ? (float)(fq / t.scale) : 0.f;
   return t;
+}
+// One entry's scaled difference e_p rho_p - e_q rho_q.
+__device__ __forceinline__ float tv_diff(float ep, float eq, float rho_p, float rho_q) {
+  return fmaf(ep, rho_p, -(eq * rho_q));
 }
 
 // One wave's part of a chunk's TV sum.
 template <int kE>
-__device__ __forceinline__ double tv_wave(const float (&ep)[kE], const float (&eq)[kE], float rho, bool swap) {
+__device__ __forceinline__ double tv_wave(const float (&ep)[kE], const float (&eq)[kE], float rho_p, float rho_q) {
   float g[kE / 4];
 #pragma unroll
   for (int k = 0; k < kE / 4; ++k) {
     float d[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float a = swap ? eq[k * 4 + i] : ep[k * 4 + i];
-      const float b = swap ? ep[k * 4 + i] : eq[k * 4 + i];
-      d[i] = fabsf(fmaf(a, rho, -b));
-    }
+    for (int i = 0; i < 4; ++i) d[i] = fabsf(tv_diff(ep[k * 4 + i], eq[k * 4 + i], rho_p, rho_q));
     g[k] = (d[0] + d[1]) + (d[2] + d[3]);
   }
   return wave_sum_d((double)tree_sum(g));
@@ -775,8 +773,8 @@ __device__ __forceinline__ void poll_row(const Args& A, const __amdgpu_buffer_rs
     chunk_shifts(R, t.c, rpc, rqc);
     const TvPar p = tv_par(factor(rpc, np), factor(rqc, nq));
     if (lane == 0) {
-      sh.rho = p.rho;
-      sh.swap = p.swap ? 1 : 0;
+      sh.rho_p = p.rho_p;
+      sh.rho_q = p.rho_q;
     }
   }
   if (lane == 0) sh.ok = ok ? 1 : 0;
@@ -894,8 +892,8 @@ __device__ __forceinline__ double wave_incl_scan_d(double x) {
 struct DrawPlan {
   double rem;    // the target's offset into the chunk's mass
   double scale;  // factor turning the scan's weights into probabilities
-  float rp, rq, rho, tp, tq;
-  int c, resid, swap;
+  float rp, rq, rho_p, rho_q, tp, tq;
+  int c, resid;
 };
 
 template <bool BF16>
@@ -970,8 +968,8 @@ __device__ DrawPlan draw_plan(const Args& A, int b, int k, int gam, float u, con
   d.scale = scale;
   d.rp = rp;
   d.rq = rq;
-  d.rho = par.rho;
-  d.swap = par.swap ? 1 : 0;
+  d.rho_p = par.rho_p;
+  d.rho_q = par.rho_q;
   d.resid = resid ? 1 : 0;
   d.c = c;
   d.tp = A.thr ? A.thr[(size_t)row * 2] : kNegInf;
@@ -1009,7 +1007,7 @@ __device__ __forceinline__ void draw_weights(const Args& A, int b, int k, const 
     float wv;
     if (d.resid) {
       const float eq = exp2_hw(fmaf(vq, A.lg, -d.rq));
-      const float dd = d.swap ? -fmaf(eq, d.rho, -ep) : fmaf(ep, d.rho, -eq);
+      const float dd = tv_diff(ep, eq, d.rho_p, d.rho_q);
       wv = fmaxf(dd, 0.f);
     } else {
       wv = ep;
@@ -1132,7 +1130,7 @@ __device__ void redo_skipped(const Args& A, int b, int j, const RowRecs& R, cons
         ep[e] = exp2_hw(fmaf(zp[e], A.lg, -rp));
         eq[e] = exp2_hw(fmaf(zq[e], A.lg, -rq));
       }
-      part[ww] = tv_wave(ep, eq, par.rho, par.swap);
+      part[ww] = tv_wave(ep, eq, par.rho_p, par.rho_q);
     }
     const double sum = tv_chunk(part);  // the owners' parts, combined as the finaliser combines them
     if (lane == src) {
@@ -1421,7 +1419,7 @@ __device__ __forceinline__ bool sweep_step(const Args& A, const int* s_rows, lon
   if (tv) {
     if (poller) poll_row(A, rs_recs, prev, W, sh);
     __syncthreads();
-    const double part = sh.ok ? tv_wave(pp, pq, sh.rho, sh.swap != 0) : kSkipped;
+    const double part = sh.ok ? tv_wave(pp, pq, sh.rho_p, sh.rho_q) : kSkipped;
     if (lane == 0)
       __hip_atomic_store(A.tva + ((size_t)prev.row * A.nc + prev.c) * kWaves + w, part, __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
@@ -1442,7 +1440,7 @@ __device__ __forceinline__ void sweep_last_tv(const Args& A, TaskShared& sh, con
     poll_row(A, rs_recs, prev, W, sh);
   }
   __syncthreads();
-  const double part = sh.ok ? tv_wave(pp, pq, sh.rho, sh.swap != 0) : kSkipped;
+  const double part = sh.ok ? tv_wave(pp, pq, sh.rho_p, sh.rho_q) : kSkipped;
   if (lane == 0)
     __hip_atomic_store(A.tva + ((size_t)prev.row * A.nc + prev.c) * kWaves + w, part, __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
