@@ -392,10 +392,16 @@ __device__ __forceinline__ uint32_t rec_off(int row, int nc, int c) {
 
 // Per-task workgroup state.
 struct TaskShared {
-  float m[2][kWaves];      // the waves' maxima of p and q
+  float m[2][kWaves];      // the waves' shifts of p and q (-inf: no entry); greedy: their maxima
   double s[3][kWaves];     // the waves' sums (p, q, KL numerator; greedy: argmax indices in s[0..1])
-  float rho_p, rho_q;      // TV parameters of the task's chunk
+  float rM_p, rM_q;        // the TV step's row normalisers (largest chunk shift, sum)
+  double S_p, S_q;
   int ok;                  // the row's records were all present in time
+};
+
+// A wave's exponent shifts for p and q (-inf where the wave has no entry).
+struct WaveShift {
+  float rp, rq;
 };
 
 // The draft token's exponent arguments x_p, x_q and its chunk's shifts, for
@@ -483,69 +489,74 @@ __device__ __forceinline__ void wave_exps(const float (&zp)[kE], const float (&z
   kl = pair ? wave_sum_d((double)tree_sum(gk)) : 0.0;
 }
 
-// Sampling: the chunk's maxima (over the waves), shifts, exponentials (left
-// in ep/eq), sums and the KL numerator; thread 0 publishes the chunk's record.
+// Sampling: each wave's maxima and shifts (its own: no exchange between the
+// waves before the exponentials), exponentials (left in ep/eq), sums and KL
+// numerator; thread 0 folds the four waves into the chunk's record, in the
+// chunk's shifts (the largest of the waves'; the rescaling factors are powers
+// of two). Returns the wave's shifts, which its TV step needs.
 template <bool BF16>
-__device__ __forceinline__ void first_pass(const Args& A, const TaskInfo& t, const Loaded<BF16>& Lp,
-                                           const Loaded<BF16>& Lq, float (&ep)[Vec<BF16>::E],
-                                           float (&eq)[Vec<BF16>::E], TaskShared& sh,
-                                           const __amdgpu_buffer_rsrc_t& rs_recs) {
+__device__ __forceinline__ WaveShift first_pass(const Args& A, const TaskInfo& t, const Loaded<BF16>& Lp,
+                                                const Loaded<BF16>& Lq, float (&ep)[Vec<BF16>::E],
+                                                float (&eq)[Vec<BF16>::E], TaskShared& sh,
+                                                const __amdgpu_buffer_rsrc_t& rs_recs) {
   constexpr int kE = Vec<BF16>::E;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int wbase = t.c * Vec<BF16>::kChunk + w * Vec<BF16>::kWaveSpan;
+  float zp[kE], zq[kE];
+  masked_logits<BF16>(A, t, wbase, Lp, Lq, zp, zq);
   float mp = kNegInf, mq = kNegInf;
-  {
-    float zp[kE], zq[kE];
-    masked_logits<BF16>(A, t, wbase, Lp, Lq, zp, zq);
 #pragma unroll
-    for (int e = 0; e < kE; ++e) {
-      mp = fmaxf(mp, zp[e]);
-      mq = fmaxf(mq, zq[e]);
-    }
+  for (int e = 0; e < kE; ++e) {
+    mp = fmaxf(mp, zp[e]);
+    mq = fmaxf(mq, zq[e]);
   }
   mp = wave_max(mp);
-  if (t.pair) mq = wave_max(mq);
-  if (lane == 0) {
-    sh.m[0][w] = mp;
-    sh.m[1][w] = mq;
-  }
-  __syncthreads();
-  float cmp = sh.m[0][0], cmq = sh.m[1][0];
-#pragma unroll
-  for (int i = 1; i < kWaves; ++i) {
-    cmp = fmaxf(cmp, sh.m[0][i]);
-    cmq = fmaxf(cmq, sh.m[1][i]);
-  }
-  if (!t.pair) cmq = kNegInf;
-  const float rp = shift_of(cmp, A.lg), rq = shift_of(cmq, A.lg);
-  // The logits are widened again from the loaded vectors (made opaque, so
-  // the first widening is not kept live across the reduction).
-  Loaded<BF16> Lp2 = Lp, Lq2 = Lq;
-#pragma unroll
-  for (int i = 0; i < kE / Vec<BF16>::N; ++i) {
-    asm volatile("" : "+v"(Lp2.v[i]));
-    asm volatile("" : "+v"(Lq2.v[i]));
-  }
-  float zp[kE], zq[kE];
-  masked_logits<BF16>(A, t, wbase, Lp2, Lq2, zp, zq);
+  mq = t.pair ? wave_max(mq) : kNegInf;
+  const float rp = shift_of(mp, A.lg), rq = shift_of(mq, A.lg);
   if (t.pair) store_xlogit<BF16>(A, t, wbase, zp, zq, rp, rq);
   double sp, sq, kl;
   wave_exps(zp, zq, A.lg, rp, rq, t.pair, ep, eq, sp, sq, kl);
+  WaveShift ws;
+  ws.rp = mp == kNegInf ? kNegInf : rp;
+  ws.rq = mq == kNegInf ? kNegInf : rq;
   if (lane == 0) {
+    sh.m[0][w] = ws.rp;
+    sh.m[1][w] = ws.rq;
     sh.s[0][w] = sp;
     sh.s[1][w] = sq;
     sh.s[2][w] = kl;
   }
   __syncthreads();
   if (tid == 0) {
+    float rpc = kNegInf, rqc = kNegInf;
+#pragma unroll
+    for (int i = 0; i < kWaves; ++i) {
+      rpc = fmaxf(rpc, sh.m[0][i]);
+      rqc = fmaxf(rqc, sh.m[1][i]);
+    }
+    // e in the chunk's shifts = e_w 2^(r_w - r_c); the KL terms' exponent
+    // difference gains (r_p,w - r_p,c) - (r_q,w - r_q,c) (0 where q has no
+    // entry: those terms are 0 or +inf already)
     StatRec r;
-    r.rp = cmp == kNegInf ? kNegInf : rp;
-    r.rq = cmq == kNegInf ? kNegInf : rq;
-    r.sp = ((sh.s[0][0] + sh.s[0][1]) + sh.s[0][2]) + sh.s[0][3];
-    r.sq = ((sh.s[1][0] + sh.s[1][1]) + sh.s[1][2]) + sh.s[1][3];
-    r.kl = ((sh.s[2][0] + sh.s[2][1]) + sh.s[2][2]) + sh.s[2][3];
+    r.rp = rpc;
+    r.rq = rqc;
+    r.sp = 0.0;
+    r.sq = 0.0;
+    r.kl = 0.0;
+#pragma unroll
+    for (int i = 0; i < kWaves; ++i) {
+      const float rpw = sh.m[0][i], rqw = sh.m[1][i];
+      if (rpw != kNegInf) {
+        const double f = ldexp(1.0, (int)(rpw - rpc));
+        const double d = rqw == kNegInf ? 0.0 : (double)(rpw - rpc) - (double)(rqw - rqc);
+        r.sp += f * sh.s[0][i];
+        r.kl += f * (sh.s[2][i] + d * sh.s[0][i]);
+      }
+      if (rqw != kNegInf) r.sq += ldexp(1.0, (int)(rqw - rqc)) * sh.s[1][i];
+    }
     store_rec(rs_recs, rec_off(t.row, A.nc, t.c), r);
   }
+  return ws;
 }
 
 // Greedy decoding: the chunk's maxima of p and q and the lowest index holding
@@ -737,22 +748,9 @@ __device__ __forceinline__ float lane_float(float x, int src) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), src));
 }
 
-// The chunk's shifts from the lane-wise records.
-__device__ __forceinline__ void chunk_shifts(const RowRecs& R, int c, float& rp, float& rq) {
-  const int src = c / kSlots, slot = c % kSlots;
-  rp = kNegInf;
-  rq = kNegInf;
-#pragma unroll
-  for (int i = 0; i < kSlots; ++i)
-    if (i == slot) {
-      rp = lane_float(R.rp[i], src);
-      rq = lane_float(R.rq[i], src);
-    }
-}
-
-// Wave 0: the row's records from the words of a first attempt (W, issued
-// earlier), else re-loaded until all are present (for a bounded time); merge
-// them and leave the task's TV parameters in LDS.
+// The polling wave: the row's records from the words of a first attempt (W,
+// issued earlier), else re-loaded until all are present (for a bounded
+// time); merge them and leave the row's normalisers in LDS.
 __device__ __forceinline__ void poll_row(const Args& A, const __amdgpu_buffer_rsrc_t& rs, const TaskInfo& t,
                                          const RecWords& W, TaskShared& sh) {
   const int lane = threadIdx.x & 63;
@@ -769,15 +767,23 @@ __device__ __forceinline__ void poll_row(const Args& A, const __amdgpu_buffer_rs
   if (ok) {
     const Norm np = merge_norm(R.rp, R.sp);
     const Norm nq = merge_norm(R.rq, R.sq);
-    float rpc, rqc;
-    chunk_shifts(R, t.c, rpc, rqc);
-    const TvPar p = tv_par(factor(rpc, np), factor(rqc, nq));
     if (lane == 0) {
-      sh.rho_p = p.rho_p;
-      sh.rho_q = p.rho_q;
+      sh.rM_p = np.rM;
+      sh.S_p = np.S;
+      sh.rM_q = nq.rM;
+      sh.S_q = nq.S;
     }
   }
   if (lane == 0) sh.ok = ok ? 1 : 0;
+}
+
+// A wave's share of a chunk's TV sum, scaled: scale * sum |e_p rho_p - e_q rho_q|
+// with the wave's own factors against the row normalisers.
+template <int kE>
+__device__ __forceinline__ double tv_wave_scaled(const float (&ep)[kE], const float (&eq)[kE], const WaveShift& ws,
+                                                 const Norm& np, const Norm& nq) {
+  const TvPar par = tv_par(factor(ws.rp, np), factor(ws.rq, nq));
+  return par.scale * tv_wave(ep, eq, par.rho_p, par.rho_q);
 }
 
 // ---------------------------------------------------------------------------
@@ -890,9 +896,9 @@ __device__ __forceinline__ double wave_incl_scan_d(double x) {
 // weights computed exactly as in the sweep, and combine their sums in pass
 // order.
 struct DrawPlan {
-  double rem;    // the target's offset into the chunk's mass
-  double scale;  // factor turning the scan's weights into probabilities
-  float rp, rq, rho_p, rho_q, tp, tq;
+  double rem;       // the target's offset into the chunk's mass
+  double S_p, S_q;  // the row normalisers: each pass's factors come from them
+  float rM_p, rM_q, tp, tq;
   int c, resid;
 };
 
@@ -912,7 +918,7 @@ __device__ DrawPlan draw_plan(const Args& A, int b, int k, int gam, float u, con
     mres[i] = 0.0;
     if (pair && c < A.nc) {
       const double fq = factor(R.rq[i], nq);
-      mres[i] = fmax(0.0, 0.5 * (tv_par(fp, fq).scale * tva[i] + mp[i] - fq * R.sq[i]));
+      mres[i] = fmax(0.0, 0.5 * (tva[i] + mp[i] - fq * R.sq[i]));
     }
     my_res += mres[i];
   }
@@ -956,20 +962,12 @@ __device__ DrawPlan draw_plan(const Args& A, int b, int k, int gam, float u, con
     pre = wave_sum_d(before);
   }
   const double rem = target - pre;
-  // that chunk's shifts and factors, as the sweep used them
-  float rpc, rqc;
-  chunk_shifts(R, c, rpc, rqc);
-  const double fp = factor(rpc, np);
-  const TvPar par = tv_par(fp, resid ? factor(rqc, nq) : 0.0);
-  const double scale = resid ? par.scale : fp;
-  const float rp = rpc == kNegInf ? 0.f : rpc, rq = rqc == kNegInf ? 0.f : rqc;
   DrawPlan d;
   d.rem = rem;
-  d.scale = scale;
-  d.rp = rp;
-  d.rq = rq;
-  d.rho_p = par.rho_p;
-  d.rho_q = par.rho_q;
+  d.rM_p = np.rM;
+  d.S_p = np.S;
+  d.rM_q = nq.rM;
+  d.S_q = nq.S;
   d.resid = resid ? 1 : 0;
   d.c = c;
   d.tp = A.thr ? A.thr[(size_t)row * 2] : kNegInf;
@@ -977,11 +975,14 @@ __device__ DrawPlan draw_plan(const Args& A, int b, int k, int gam, float u, con
   return d;
 }
 
-// One pass of the scan (this wave's quarter of the chunk): a lane's weights
-// and the last index among them with weight.
+// One pass of the scan (this wave's quarter of the chunk, which one sweep
+// wave held): a lane's weights and the last index among them with weight;
+// returns the factor turning the pass's weights into probabilities. The
+// pass's shifts are the sweep wave's own (its maxima over the same entries),
+// so the weights are the sweep's exponentials.
 template <bool BF16>
-__device__ __forceinline__ void draw_weights(const Args& A, int b, int k, const DrawPlan& d, int pass,
-                                             float (&wt)[Vec<BF16>::E], int& mine) {
+__device__ __forceinline__ double draw_weights(const Args& A, int b, int k, const DrawPlan& d, int pass,
+                                               float (&wt)[Vec<BF16>::E], int& mine) {
   constexpr int N = Vec<BF16>::N, esz = Vec<BF16>::esz, kE = Vec<BF16>::E;
   const int lane = threadIdx.x & 63;
   const RowSpan s = row_span<BF16>(A, b, k, d.resid != 0);
@@ -996,25 +997,39 @@ __device__ __forceinline__ void draw_weights(const Args& A, int b, int k, const 
   float zp[kE], zq[kE];
   widen<BF16>(lp, zp);
   widen<BF16>(lq, zq);
-  mine = -1;
+  float mp = kNegInf, mq = kNegInf;
 #pragma unroll
   for (int e = 0; e < kE; ++e) {
     const int i = pos0 + e - s.phi;
     const bool in = i >= 0 && i < A.V;
-    const float vp = in && zp[e] >= d.tp ? zp[e] : kNegInf;
-    const float vq = in && zq[e] >= d.tq ? zq[e] : kNegInf;
-    const float ep = exp2_hw(fmaf(vp, A.lg, -d.rp));
+    zp[e] = in && zp[e] >= d.tp ? zp[e] : kNegInf;
+    zq[e] = in && zq[e] >= d.tq ? zq[e] : kNegInf;
+    mp = fmaxf(mp, zp[e]);
+    mq = fmaxf(mq, zq[e]);
+  }
+  mp = wave_max(mp);
+  mq = d.resid ? wave_max(mq) : kNegInf;
+  const float rp = shift_of(mp, A.lg), rq = shift_of(mq, A.lg);
+  const WaveShift ws{mp == kNegInf ? kNegInf : rp, mq == kNegInf ? kNegInf : rq};
+  const Norm np{d.rM_p, d.S_p}, nq{d.rM_q, d.S_q};
+  const double fp = factor(ws.rp, np);
+  const TvPar par = tv_par(fp, d.resid ? factor(ws.rq, nq) : 0.0);
+  mine = -1;
+#pragma unroll
+  for (int e = 0; e < kE; ++e) {
+    const int i = pos0 + e - s.phi;
+    const float ep = exp2_hw(fmaf(zp[e], A.lg, -rp));
     float wv;
     if (d.resid) {
-      const float eq = exp2_hw(fmaf(vq, A.lg, -d.rq));
-      const float dd = tv_diff(ep, eq, d.rho_p, d.rho_q);
-      wv = fmaxf(dd, 0.f);
+      const float eq = exp2_hw(fmaf(zq[e], A.lg, -rq));
+      wv = fmaxf(tv_diff(ep, eq, par.rho_p, par.rho_q), 0.f);
     } else {
       wv = ep;
     }
     wt[e] = wv;
     if (wv > 0.f) mine = i;
   }
+  return d.resid ? par.scale : fp;
 }
 
 // Shared state of the scan.
@@ -1033,13 +1048,13 @@ __device__ int draw_scan(const Args& A, int b, int k, const DrawPlan& d, DrawSha
   const int lane = threadIdx.x & 63, w = wave_id();
   float wt[kE];
   int mine = -1;
-  double lsum = 0.0, pincl = 0.0;
+  double lsum = 0.0, pincl = 0.0, scale = 0.0;
   if (w < kWaves) {
-    draw_weights<BF16>(A, b, k, d, w, wt, mine);
+    scale = draw_weights<BF16>(A, b, k, d, w, wt, mine);
     double acc = 0.0;
 #pragma unroll
     for (int e = 0; e < kE; ++e) acc += (double)wt[e];
-    lsum = acc * d.scale;
+    lsum = acc * scale;
     pincl = wave_incl_scan_d(lsum);
     const int last = wave_max_i(mine);
     if (lane == 63) ds.tot[w] = pincl;
@@ -1060,7 +1075,7 @@ __device__ int draw_scan(const Args& A, int b, int k, const DrawPlan& d, DrawSha
       int found = -1;
 #pragma unroll
       for (int e = 0; e < kE; ++e) {
-        run += (double)wt[e] * d.scale;
+        run += (double)wt[e] * scale;
         if (found < 0 && wt[e] > 0.f && run > d.rem) found = pos0 + e - phi;
       }
       const int t = __builtin_amdgcn_readlane(found >= 0 ? found : mine, hl);
@@ -1100,10 +1115,6 @@ __device__ void redo_skipped(const Args& A, int b, int j, const RowRecs& R, cons
     if (!pend) break;
     const int src = __ffsll((long long)pend) - 1;
     const int c = __builtin_amdgcn_readlane(cl, src);  // the lowest skipped chunk of that lane
-    float rpc, rqc;
-    chunk_shifts(R, c, rpc, rqc);
-    const float rp = rpc == kNegInf ? 0.f : rpc, rq = rqc == kNegInf ? 0.f : rqc;
-    const TvPar par = tv_par(factor(rpc, np), factor(rqc, nq));
     TaskInfo t;
     t.c = c;
     t.row = row;
@@ -1125,12 +1136,23 @@ __device__ void redo_skipped(const Args& A, int b, int j, const RowRecs& R, cons
       }
       float zp[kE], zq[kE], ep[kE], eq[kE];
       masked_logits<BF16>(A, t, wbase, lp, lq, zp, zq);
+      // the owner wave's shifts: its maxima over these entries
+      float mp = kNegInf, mq = kNegInf;
+#pragma unroll
+      for (int e = 0; e < kE; ++e) {
+        mp = fmaxf(mp, zp[e]);
+        mq = fmaxf(mq, zq[e]);
+      }
+      mp = wave_max(mp);
+      mq = wave_max(mq);
+      const float rp = shift_of(mp, A.lg), rq = shift_of(mq, A.lg);
 #pragma unroll
       for (int e = 0; e < kE; ++e) {
         ep[e] = exp2_hw(fmaf(zp[e], A.lg, -rp));
         eq[e] = exp2_hw(fmaf(zq[e], A.lg, -rq));
       }
-      part[ww] = tv_wave(ep, eq, par.rho_p, par.rho_q);
+      const WaveShift ws{mp == kNegInf ? kNegInf : rp, mq == kNegInf ? kNegInf : rq};
+      part[ww] = tv_wave_scaled(ep, eq, ws, np, nq);
     }
     const double sum = tv_chunk(part);  // the owners' parts, combined as the finaliser combines them
     if (lane == src) {
@@ -1221,15 +1243,15 @@ __device__ RowOut finalize_row(const Args& A, int b, int j, int gam, const __amd
     if (pair) {
       nq = merge_norm(R.rq, R.sq);
       redo_skipped<BF16>(A, b, j, R, np, nq, tva);
-      // TV = 1/2 sum_c scale_c tva_c;
+      // TV = 1/2 sum_c tva_c (the waves' parts come scaled);
       // KL = sum_c f_c (ln2 kl_c + ln2 s_c d_c) - ln(S_p / S_q) sum_c f_c s_c with
       // d_c = (r_c - r_max) - (r'_c - r'_max) (integers): the log-ratio of an
       // entry is ln2 (x_p - x_q) + ln2 d_c - ln(S_p / S_q)
       double tvs = 0.0, klt = 0.0, mass = 0.0;
 #pragma unroll
       for (int i = 0; i < kSlots; ++i) {
-        const double fp = factor(R.rp[i], np), fq = factor(R.rq[i], nq);
-        tvs += tv_par(fp, fq).scale * tva[i];
+        const double fp = factor(R.rp[i], np);
+        tvs += tva[i];
         if (fp > 0.0) {
           const double d = ((double)R.rp[i] - (double)np.rM) - ((double)R.rq[i] - (double)nq.rM);
           klt += fp * (kLn2 * R.kl[i] + kLn2 * d * R.sp[i]);
@@ -1396,10 +1418,10 @@ template <bool BF16, bool GREEDY>
 __device__ __forceinline__ bool sweep_step(const Args& A, const int* s_rows, long n_tasks, int n_my, int k,
                                            TaskTable& tab, TaskShared& sh, const __amdgpu_buffer_rsrc_t& rs_recs,
                                            const TaskInfo& cur, const Loaded<BF16>& lp, const Loaded<BF16>& lq,
-                                           float (&ep)[Vec<BF16>::E], float (&eq)[Vec<BF16>::E], TaskInfo prev,
-                                           bool has_prev, const float (&pp)[Vec<BF16>::E],
-                                           const float (&pq)[Vec<BF16>::E], TaskInfo& nxt, Loaded<BF16>& np_,
-                                           Loaded<BF16>& nq_) {
+                                           float (&ep)[Vec<BF16>::E], float (&eq)[Vec<BF16>::E], WaveShift& ws,
+                                           TaskInfo prev, bool has_prev, const float (&pp)[Vec<BF16>::E],
+                                           const float (&pq)[Vec<BF16>::E], const WaveShift& pws, TaskInfo& nxt,
+                                           Loaded<BF16>& np_, Loaded<BF16>& nq_) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const bool tv = !GREEDY && has_prev && prev.pair;  // workgroup-uniform
   // The poll and the merge of the records go to wave k mod 4, so that every
@@ -1415,11 +1437,11 @@ __device__ __forceinline__ bool sweep_step(const Args& A, const int* s_rows, lon
   nxt = decode_task<BF16>(A, tab, more ? k + 1 : k);
   issue_loads<BF16>(A, nxt, np_, nq_, more);
   if constexpr (GREEDY) argmax_pass<BF16>(A, cur, lp, lq, sh, rs_recs);
-  else first_pass<BF16>(A, cur, lp, lq, ep, eq, sh, rs_recs);
+  else ws = first_pass<BF16>(A, cur, lp, lq, ep, eq, sh, rs_recs);
   if (tv) {
     if (poller) poll_row(A, rs_recs, prev, W, sh);
     __syncthreads();
-    const double part = sh.ok ? tv_wave(pp, pq, sh.rho_p, sh.rho_q) : kSkipped;
+    const double part = sh.ok ? tv_wave_scaled(pp, pq, pws, Norm{sh.rM_p, sh.S_p}, Norm{sh.rM_q, sh.S_q}) : kSkipped;
     if (lane == 0)
       __hip_atomic_store(A.tva + ((size_t)prev.row * A.nc + prev.c) * kWaves + w, part, __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
@@ -1431,7 +1453,7 @@ __device__ __forceinline__ bool sweep_step(const Args& A, const int* s_rows, lon
 template <bool BF16>
 __device__ __forceinline__ void sweep_last_tv(const Args& A, TaskShared& sh, const __amdgpu_buffer_rsrc_t& rs_recs,
                                               const TaskInfo& prev, const float (&pp)[Vec<BF16>::E],
-                                              const float (&pq)[Vec<BF16>::E]) {
+                                              const float (&pq)[Vec<BF16>::E], const WaveShift& pws) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   if (!prev.pair) return;
   if (w == 0) {
@@ -1440,7 +1462,7 @@ __device__ __forceinline__ void sweep_last_tv(const Args& A, TaskShared& sh, con
     poll_row(A, rs_recs, prev, W, sh);
   }
   __syncthreads();
-  const double part = sh.ok ? tv_wave(pp, pq, sh.rho_p, sh.rho_q) : kSkipped;
+  const double part = sh.ok ? tv_wave_scaled(pp, pq, pws, Norm{sh.rM_p, sh.S_p}, Norm{sh.rM_q, sh.S_q}) : kSkipped;
   if (lane == 0)
     __hip_atomic_store(A.tva + ((size_t)prev.row * A.nc + prev.c) * kWaves + w, part, __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
@@ -1466,17 +1488,18 @@ __global__ void __launch_bounds__(kThreads, 2) accept_kernel(Args A) {
   Loaded<BF16> pa, qa, pb, qb;
   issue_loads<BF16>(A, ta, pa, qa);
   float epa[E], eqa[E], epb[E], eqb[E];
+  WaveShift wsa{kNegInf, kNegInf}, wsb{kNegInf, kNegInf};
   bool has_prev = false;
   for (int k = 0;; k += 2) {
-    if (!sweep_step<BF16, GREEDY>(A, s_rows, n_tasks, n_my, k, tab, sh, rs_recs, ta, pa, qa, epa, eqa, tb, has_prev,
-                                  epb, eqb, tb, pb, qb)) {
-      if (!GREEDY) sweep_last_tv<BF16>(A, sh, rs_recs, ta, epa, eqa);
+    if (!sweep_step<BF16, GREEDY>(A, s_rows, n_tasks, n_my, k, tab, sh, rs_recs, ta, pa, qa, epa, eqa, wsa, tb,
+                                  has_prev, epb, eqb, wsb, tb, pb, qb)) {
+      if (!GREEDY) sweep_last_tv<BF16>(A, sh, rs_recs, ta, epa, eqa, wsa);
       break;
     }
     has_prev = true;
-    if (!sweep_step<BF16, GREEDY>(A, s_rows, n_tasks, n_my, k + 1, tab, sh, rs_recs, tb, pb, qb, epb, eqb, ta, true,
-                                  epa, eqa, ta, pa, qa)) {
-      if (!GREEDY) sweep_last_tv<BF16>(A, sh, rs_recs, tb, epb, eqb);
+    if (!sweep_step<BF16, GREEDY>(A, s_rows, n_tasks, n_my, k + 1, tab, sh, rs_recs, tb, pb, qb, epb, eqb, wsb, ta,
+                                  true, epa, eqa, wsa, ta, pa, qa)) {
+      if (!GREEDY) sweep_last_tv<BF16>(A, sh, rs_recs, tb, epb, eqb, wsb);
       break;
     }
   }
