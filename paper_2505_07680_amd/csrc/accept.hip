@@ -391,9 +391,18 @@ __device__ __forceinline__ uint32_t rec_off(int row, int nc, int c) {
 // First pass (the workgroup: one task)
 
 // Per-task workgroup state.
-struct TaskShared {
+// The waves' results of a task's first pass, read by thread 0 after one
+// barrier. Two sets, used by alternate tasks: a wave may start the next
+// task's first pass (and write its results) while thread 0 still reads this
+// task's, but not the one after (that waits for the next task's barrier,
+// which thread 0 reaches only after its reads).
+struct WaveSlots {
   float m[2][kWaves];      // the waves' shifts of p and q (-inf: no entry); greedy: their maxima
   double s[3][kWaves];     // the waves' sums (p, q, KL numerator; greedy: argmax indices in s[0..1])
+};
+
+struct TaskShared {
+  WaveSlots x[2];          // by task parity
   float rM_p, rM_q;        // the TV step's row normalisers (largest chunk shift, sum)
   double S_p, S_q;
   int ok;                  // the row's records were all present in time
@@ -497,7 +506,7 @@ __device__ __forceinline__ void wave_exps(const float (&zp)[kE], const float (&z
 template <bool BF16>
 __device__ __forceinline__ WaveShift first_pass(const Args& A, const TaskInfo& t, const Loaded<BF16>& Lp,
                                                 const Loaded<BF16>& Lq, float (&ep)[Vec<BF16>::E],
-                                                float (&eq)[Vec<BF16>::E], TaskShared& sh,
+                                                float (&eq)[Vec<BF16>::E], WaveSlots& sh,
                                                 const __amdgpu_buffer_rsrc_t& rs_recs) {
   constexpr int kE = Vec<BF16>::E;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -563,7 +572,7 @@ __device__ __forceinline__ WaveShift first_pass(const Args& A, const TaskInfo& t
 // each (lanes scan their entries in ascending index order).
 template <bool BF16>
 __device__ __forceinline__ void argmax_pass(const Args& A, const TaskInfo& t, const Loaded<BF16>& Lp,
-                                            const Loaded<BF16>& Lq, TaskShared& sh,
+                                            const Loaded<BF16>& Lq, WaveSlots& sh,
                                             const __amdgpu_buffer_rsrc_t& rs_recs) {
   constexpr int kE = Vec<BF16>::E;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -1436,8 +1445,8 @@ __device__ __forceinline__ bool sweep_step(const Args& A, const int* s_rows, lon
   if (more && (k + 1) % kTab == 0) fill_tasks(A, s_rows, n_tasks, k + 1, tab);
   nxt = decode_task<BF16>(A, tab, more ? k + 1 : k);
   issue_loads<BF16>(A, nxt, np_, nq_, more);
-  if constexpr (GREEDY) argmax_pass<BF16>(A, cur, lp, lq, sh, rs_recs);
-  else ws = first_pass<BF16>(A, cur, lp, lq, ep, eq, sh, rs_recs);
+  if constexpr (GREEDY) argmax_pass<BF16>(A, cur, lp, lq, sh.x[k & 1], rs_recs);
+  else ws = first_pass<BF16>(A, cur, lp, lq, ep, eq, sh.x[k & 1], rs_recs);
   if (tv) {
     if (poller) poll_row(A, rs_recs, prev, W, sh);
     __syncthreads();
