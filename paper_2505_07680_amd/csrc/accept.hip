@@ -391,11 +391,11 @@ __device__ __forceinline__ uint32_t rec_off(int row, int nc, int c) {
 // First pass (the workgroup: one task)
 
 // Per-task workgroup state.
-// The waves' results of a task's first pass, read by thread 0 after one
-// barrier. Two sets, used by alternate tasks: a wave may start the next
-// task's first pass (and write its results) while thread 0 still reads this
-// task's, but not the one after (that waits for the next task's barrier,
-// which thread 0 reaches only after its reads).
+// The waves' results of a task's first pass, read by the record's builder
+// after one barrier. Two sets, used by alternate tasks: a wave may start the
+// next task's first pass (and write its results) while the builder still
+// reads this task's, but not the one after (that waits for the next task's
+// barrier, which the builder reaches only after its reads).
 struct WaveSlots {
   float m[2][kWaves];      // the waves' shifts of p and q (-inf: no entry); greedy: their maxima
   double s[3][kWaves];     // the waves' sums (p, q, KL numerator; greedy: argmax indices in s[0..1])
@@ -500,14 +500,15 @@ __device__ __forceinline__ void wave_exps(const float (&zp)[kE], const float (&z
 
 // Sampling: each wave's maxima and shifts (its own: no exchange between the
 // waves before the exponentials), exponentials (left in ep/eq), sums and KL
-// numerator; thread 0 folds the four waves into the chunk's record, in the
-// chunk's shifts (the largest of the waves'; the rescaling factors are powers
-// of two). Returns the wave's shifts, which its TV step needs.
+// numerator; lane 0 of wave `builder` folds the four waves into the chunk's
+// record, in the chunk's shifts (the largest of the waves'; the rescaling
+// factors are powers of two). Returns the wave's shifts, which its TV step
+// needs.
 template <bool BF16>
 __device__ __forceinline__ WaveShift first_pass(const Args& A, const TaskInfo& t, const Loaded<BF16>& Lp,
                                                 const Loaded<BF16>& Lq, float (&ep)[Vec<BF16>::E],
                                                 float (&eq)[Vec<BF16>::E], WaveSlots& sh,
-                                                const __amdgpu_buffer_rsrc_t& rs_recs) {
+                                                const __amdgpu_buffer_rsrc_t& rs_recs, int builder) {
   constexpr int kE = Vec<BF16>::E;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int wbase = t.c * Vec<BF16>::kChunk + w * Vec<BF16>::kWaveSpan;
@@ -536,7 +537,7 @@ __device__ __forceinline__ WaveShift first_pass(const Args& A, const TaskInfo& t
     sh.s[2][w] = kl;
   }
   __syncthreads();
-  if (tid == 0) {
+  if (w == builder && lane == 0) {
     float rpc = kNegInf, rqc = kNegInf;
 #pragma unroll
     for (int i = 0; i < kWaves; ++i) {
@@ -1446,7 +1447,7 @@ __device__ __forceinline__ bool sweep_step(const Args& A, const int* s_rows, lon
   nxt = decode_task<BF16>(A, tab, more ? k + 1 : k);
   issue_loads<BF16>(A, nxt, np_, nq_, more);
   if constexpr (GREEDY) argmax_pass<BF16>(A, cur, lp, lq, sh.x[k & 1], rs_recs);
-  else ws = first_pass<BF16>(A, cur, lp, lq, ep, eq, sh.x[k & 1], rs_recs);
+  else ws = first_pass<BF16>(A, cur, lp, lq, ep, eq, sh.x[k & 1], rs_recs, (k + 2) & (kWaves - 1));
   if (tv) {
     if (poller) poll_row(A, rs_recs, prev, W, sh);
     __syncthreads();
