@@ -61,11 +61,12 @@
 // of the first pass and no TV step or waiting.
 //
 // Precision: exponentials in fp32 (relative error ~1e-7; weights below 2^-126
-// of their chunk's largest flush to zero), every sum in fp64 beyond a
-// lane's 16 entries; the log-normalisers are r_max ln 2 + ln S in fp64 and
-// log-probabilities are formed from the exponent arguments actually used, so
-// rows with the same filtered distribution give KL = 0 and p(x) = q(x) to
-// fp64 rounding. A draw can differ from exact arithmetic only when u*W lies
+// of their chunk's largest flush to zero), sums in fp32 over a wave's 1024
+// entries (a fixed tree: relative error at most ~6e-7 of the sum of
+// magnitudes) and in fp64 beyond; the log-normalisers are r_max ln 2 + ln S
+// in fp64 and log-probabilities are formed from the exponent arguments
+// actually used, so rows with the same filtered distribution give KL = 0 and
+// p(x) = q(x) to fp64 rounding. A draw can differ from exact arithmetic only when u*W lies
 // within ~1e-7 W of a CDF breakpoint. Logits must satisfy |z|/T < 2^23 (the
 // shifts are exact fp32 integers).
 
@@ -476,26 +477,38 @@ template <int kE>
 __device__ __forceinline__ void wave_exps(const float (&zp)[kE], const float (&zq)[kE], float lg, float rp, float rq,
                                           bool pair, float (&ep)[kE], float (&eq)[kE], double& sp, double& sq,
                                           double& kl) {
-  float gp[kE / 4], gq[kE / 4], gk[kE / 4];
+  float gp[kE / 4];
+  if (pair) {  // workgroup-uniform
+    float gq[kE / 4], gk[kE / 4];
 #pragma unroll
-  for (int g = 0; g < kE / 4; ++g) {
-    float kt[4];
+    for (int g = 0; g < kE / 4; ++g) {
+      float kt[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int e = g * 4 + i;
-      const float xp = fmaf(zp[e], lg, -rp);
-      const float xq = fmaf(zq[e], lg, -rq);
-      ep[e] = exp2_hw(xp);
-      eq[e] = pair ? exp2_hw(xq) : 0.f;
-      kt[i] = pair ? sr_fmul_legacy(ep[e], xp - xq) : 0.f;  // 0 where p is -inf, +inf where only q is
+      for (int i = 0; i < 4; ++i) {
+        const int e = g * 4 + i;
+        const float xp = fmaf(zp[e], lg, -rp);
+        const float xq = fmaf(zq[e], lg, -rq);
+        ep[e] = exp2_hw(xp);
+        eq[e] = exp2_hw(xq);
+        kt[i] = sr_fmul_legacy(ep[e], xp - xq);  // 0 where p is -inf, +inf where only q is
+      }
+      gp[g] = (ep[g * 4] + ep[g * 4 + 1]) + (ep[g * 4 + 2] + ep[g * 4 + 3]);
+      gq[g] = (eq[g * 4] + eq[g * 4 + 1]) + (eq[g * 4 + 2] + eq[g * 4 + 3]);
+      gk[g] = (kt[0] + kt[1]) + (kt[2] + kt[3]);
     }
-    gp[g] = (ep[g * 4] + ep[g * 4 + 1]) + (ep[g * 4 + 2] + ep[g * 4 + 3]);
-    gq[g] = (eq[g * 4] + eq[g * 4 + 1]) + (eq[g * 4 + 2] + eq[g * 4 + 3]);
-    gk[g] = (kt[0] + kt[1]) + (kt[2] + kt[3]);
+    sq = (double)wave_sum(tree_sum(gq));
+    kl = (double)wave_sum(tree_sum(gk));
+  } else {  // a bonus row: p alone (eq is not read)
+#pragma unroll
+    for (int g = 0; g < kE / 4; ++g) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) ep[g * 4 + i] = exp2_hw(fmaf(zp[g * 4 + i], lg, -rp));
+      gp[g] = (ep[g * 4] + ep[g * 4 + 1]) + (ep[g * 4 + 2] + ep[g * 4 + 3]);
+    }
+    sq = 0.0;
+    kl = 0.0;
   }
-  sp = wave_sum_d((double)tree_sum(gp));
-  sq = pair ? wave_sum_d((double)tree_sum(gq)) : 0.0;
-  kl = pair ? wave_sum_d((double)tree_sum(gk)) : 0.0;
+  sp = (double)wave_sum(tree_sum(gp));
 }
 
 // Sampling: each wave's maxima and shifts (its own: no exchange between the
@@ -747,7 +760,7 @@ __device__ __forceinline__ double tv_wave(const float (&ep)[kE], const float (&e
     for (int i = 0; i < 4; ++i) d[i] = fabsf(tv_diff(ep[k * 4 + i], eq[k * 4 + i], rho_p, rho_q));
     g[k] = (d[0] + d[1]) + (d[2] + d[3]);
   }
-  return wave_sum_d((double)tree_sum(g));
+  return (double)wave_sum(tree_sum(g));
 }
 // A chunk's TV sum from its waves' parts, in a fixed order.
 __device__ __forceinline__ double tv_chunk(const double (&part)[kWaves]) {

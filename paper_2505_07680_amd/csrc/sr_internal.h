@@ -45,15 +45,39 @@ __device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
   return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, C, 0xf, 0xf, false);
 }
 template <int C>
-__device__ __forceinline__ float dpp_f32(float x) {
-  return __uint_as_float(dpp_u32<C>(__float_as_uint(x)));
-}
-template <int C>
 __device__ __forceinline__ double dpp_f64(double x) {
   const uint64_t u = (uint64_t)__double_as_longlong(x);
   const uint64_t lo = dpp_u32<C>((uint32_t)u), hi = dpp_u32<C>((uint32_t)(u >> 32));
   return __longlong_as_double((long long)(lo | (hi << 32)));
 }
+// The same for the permutation patterns above (every lane has a source lane,
+// so no fill value is needed, and the compiler can fold the move into the
+// operation that reads it).
+template <int C>
+__device__ __forceinline__ uint32_t perm_u32(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, C, 0xf, 0xf, false);
+}
+template <int C>
+__device__ __forceinline__ float perm_f32(float x) {
+  return __uint_as_float(perm_u32<C>(__float_as_uint(x)));
+}
+template <int C>
+__device__ __forceinline__ double perm_f64(double x) {
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  const uint64_t lo = perm_u32<C>((uint32_t)u), hi = perm_u32<C>((uint32_t)(u >> 32));
+  return __longlong_as_double((long long)(lo | (hi << 32)));
+}
+
+// max(a, b) for non-NaN operands as the median of (a, b, +inf): one
+// instruction, without the quieting of the operands that fmaxf needs (the
+// +inf comes from an opaque scalar move, so that the compiler keeps the
+// median instead of turning it back into fmaxf).
+__device__ __forceinline__ float opaque_inf() {
+  float r;
+  asm("s_mov_b32 %0, 0x7f800000" : "=s"(r));
+  return r;
+}
+__device__ __forceinline__ float max_nn(float a, float b) { return __builtin_amdgcn_fmed3f(a, b, opaque_inf()); }
 
 // (value of the even row, value of the odd row) of each pair of 16-lane rows,
 // in every lane; with kHalf32 the same for the two 32-lane halves.
@@ -85,21 +109,21 @@ __device__ __forceinline__ void swap_halves_f64(double x, double& even, double& 
 // tree (pairs, quads, groups of 8, rows of 16, then the row pairs and halves,
 // the lower part always on the left).
 __device__ __forceinline__ float wave_max(float x) {
-  x = fmaxf(x, dpp_f32<dpp::kXor1>(x));
-  x = fmaxf(x, dpp_f32<dpp::kXor2>(x));
-  x = fmaxf(x, dpp_f32<dpp::kHalfMirror>(x));
-  x = fmaxf(x, dpp_f32<dpp::kMirror>(x));
+  x = max_nn(x, perm_f32<dpp::kXor1>(x));
+  x = max_nn(x, perm_f32<dpp::kXor2>(x));
+  x = max_nn(x, perm_f32<dpp::kHalfMirror>(x));
+  x = max_nn(x, perm_f32<dpp::kMirror>(x));
   float e, o;
   swap_halves_f32<false>(x, e, o);
-  x = fmaxf(e, o);
+  x = max_nn(e, o);
   swap_halves_f32<true>(x, e, o);
-  return fmaxf(e, o);
+  return max_nn(e, o);
 }
 __device__ __forceinline__ float wave_sum(float x) {
-  x = x + dpp_f32<dpp::kXor1>(x);
-  x = x + dpp_f32<dpp::kXor2>(x);
-  x = x + dpp_f32<dpp::kHalfMirror>(x);
-  x = x + dpp_f32<dpp::kMirror>(x);
+  x = x + perm_f32<dpp::kXor1>(x);
+  x = x + perm_f32<dpp::kXor2>(x);
+  x = x + perm_f32<dpp::kHalfMirror>(x);
+  x = x + perm_f32<dpp::kMirror>(x);
   float e, o;
   swap_halves_f32<false>(x, e, o);
   x = e + o;
@@ -107,10 +131,10 @@ __device__ __forceinline__ float wave_sum(float x) {
   return e + o;
 }
 __device__ __forceinline__ double wave_sum_d(double x) {
-  x = x + dpp_f64<dpp::kXor1>(x);
-  x = x + dpp_f64<dpp::kXor2>(x);
-  x = x + dpp_f64<dpp::kHalfMirror>(x);
-  x = x + dpp_f64<dpp::kMirror>(x);
+  x = x + perm_f64<dpp::kXor1>(x);
+  x = x + perm_f64<dpp::kXor2>(x);
+  x = x + perm_f64<dpp::kHalfMirror>(x);
+  x = x + perm_f64<dpp::kMirror>(x);
   double e, o;
   swap_halves_f64<false>(x, e, o);
   x = e + o;
@@ -118,10 +142,10 @@ __device__ __forceinline__ double wave_sum_d(double x) {
   return e + o;
 }
 __device__ __forceinline__ int wave_max_i(int x) {
-  x = max(x, (int)dpp_u32<dpp::kXor1>((uint32_t)x));
-  x = max(x, (int)dpp_u32<dpp::kXor2>((uint32_t)x));
-  x = max(x, (int)dpp_u32<dpp::kHalfMirror>((uint32_t)x));
-  x = max(x, (int)dpp_u32<dpp::kMirror>((uint32_t)x));
+  x = max(x, (int)perm_u32<dpp::kXor1>((uint32_t)x));
+  x = max(x, (int)perm_u32<dpp::kXor2>((uint32_t)x));
+  x = max(x, (int)perm_u32<dpp::kHalfMirror>((uint32_t)x));
+  x = max(x, (int)perm_u32<dpp::kMirror>((uint32_t)x));
   uint32_t e, o;
   swap_halves<false>((uint32_t)x, e, o);
   x = max((int)e, (int)o);
@@ -147,10 +171,10 @@ __device__ __forceinline__ float sum_across_rows(float x) {
 }
 
 __device__ __forceinline__ int wave_min_i(int x) {
-  x = min(x, (int)dpp_u32<dpp::kXor1>((uint32_t)x));
-  x = min(x, (int)dpp_u32<dpp::kXor2>((uint32_t)x));
-  x = min(x, (int)dpp_u32<dpp::kHalfMirror>((uint32_t)x));
-  x = min(x, (int)dpp_u32<dpp::kMirror>((uint32_t)x));
+  x = min(x, (int)perm_u32<dpp::kXor1>((uint32_t)x));
+  x = min(x, (int)perm_u32<dpp::kXor2>((uint32_t)x));
+  x = min(x, (int)perm_u32<dpp::kHalfMirror>((uint32_t)x));
+  x = min(x, (int)perm_u32<dpp::kMirror>((uint32_t)x));
   uint32_t e, o;
   swap_halves<false>((uint32_t)x, e, o);
   x = min((int)e, (int)o);
