@@ -117,9 +117,11 @@ const char* specrouter_status_string(int code);
  * scale      score scale, normally 1/sqrt(D); must be positive and finite (else SR_EINVAL)
  * workspace  device scratch of specrouter_verify_attention_workspace_size()
  *            bytes (may be NULL when that size is 0). Zero-fill it once before
- *            its first use; every call leaves it in that state again (it holds
+ *            its first use; every call leaves its counters zero again (it holds
  *            per-(sequence, kv head, query chunk) arrival counters of the cache
- *            splits, and their partial results)
+ *            splits, their partial results, and, when the call has more
+ *            workgroups than fit on the device at once, their dispatch order,
+ *            rewritten by every call)
  * Precision: bf16 products, fp32 accumulation and softmax, in a fixed order
  * (repeated calls give identical bits).
  */

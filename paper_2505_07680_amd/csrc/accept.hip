@@ -737,11 +737,28 @@ struct TvPar {
   double scale;
   float rho_p, rho_q;
 };
-__device__ __forceinline__ TvPar tv_par(double fp, double fq) {
+// 1/s (s > 0) from the hardware estimate and two Newton steps.
+__device__ __forceinline__ double recip(double s) {
+  double r = __builtin_amdgcn_rcp(s);
+  r = fma(r, fma(-s, r, 1.0), r);
+  return fma(r, fma(-s, r, 1.0), r);
+}
+// The factors of a wave with shifts ws against the row normalisers, without a
+// division: f = 2^(r_w - r_max)/S, and the smaller side's ratio is
+// 2^(k) S_big/S_small with k the difference of the shift offsets.
+__device__ __forceinline__ TvPar tv_par(const WaveShift& ws, const Norm& np, const Norm& nq) {
+  const bool hp = ws.rp != kNegInf && np.S > 0.0, hq = ws.rq != kNegInf && nq.S > 0.0;
+  const double ip = recip(hp ? np.S : 1.0), iq = recip(hq ? nq.S : 1.0);
+  const int a = hp ? (int)(ws.rp - np.rM) : 0, b = hq ? (int)(ws.rq - nq.rM) : 0;
+  const double fp = hp ? ldexp(ip, a) : 0.0, fq = hq ? ldexp(iq, b) : 0.0;
+  const bool both = hp && hq;
+  const float rq = both ? (float)ldexp(np.S * iq, b - a) : 0.f;  // f_q/f_p
+  const float rp = both ? (float)ldexp(nq.S * ip, a - b) : 0.f;  // f_p/f_q
+  const bool pbig = fp >= fq;
   TvPar t;
-  t.scale = fp > fq ? fp : fq;
-  t.rho_p = t.scale > 0.0 ? (float)(fp / t.scale) : 0.f;
-  t.rho_q = t.scale > 0.0 ? (float)(fq / t.scale) : 0.f;
+  t.scale = pbig ? fp : fq;
+  t.rho_p = pbig ? (hp ? 1.f : 0.f) : rp;
+  t.rho_q = pbig ? rq : 1.f;
   return t;
 }
 // One entry's scaled difference e_p rho_p - e_q rho_q.
@@ -805,7 +822,7 @@ __device__ __forceinline__ void poll_row(const Args& A, const __amdgpu_buffer_rs
 template <int kE>
 __device__ __forceinline__ double tv_wave_scaled(const float (&ep)[kE], const float (&eq)[kE], const WaveShift& ws,
                                                  const Norm& np, const Norm& nq) {
-  const TvPar par = tv_par(factor(ws.rp, np), factor(ws.rq, nq));
+  const TvPar par = tv_par(ws, np, nq);
   return par.scale * tv_wave(ep, eq, par.rho_p, par.rho_q);
 }
 
@@ -1036,7 +1053,7 @@ __device__ __forceinline__ double draw_weights(const Args& A, int b, int k, cons
   const WaveShift ws{mp == kNegInf ? kNegInf : rp, mq == kNegInf ? kNegInf : rq};
   const Norm np{d.rM_p, d.S_p}, nq{d.rM_q, d.S_q};
   const double fp = factor(ws.rp, np);
-  const TvPar par = tv_par(fp, d.resid ? factor(ws.rq, nq) : 0.0);
+  const TvPar par = d.resid ? tv_par(ws, np, nq) : TvPar{fp, 1.f, 0.f};
   mine = -1;
 #pragma unroll
   for (int e = 0; e < kE; ++e) {

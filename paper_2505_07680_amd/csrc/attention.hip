@@ -141,9 +141,10 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
                   const uint16_t* __restrict__ vc, const uint8_t* __restrict__ mask,
                   const int32_t* __restrict__ kv_len, const int32_t* __restrict__ gamma,
                   float* __restrict__ out, float* __restrict__ part_o,
-                  float* __restrict__ part_ml, uint32_t* __restrict__ counters, int B, int gmax,
-                  int Hq, int Hkv, int L_cap, float scale_log2, int split_keys, int n_splits,
-                  int q_chunks, int32_t* __restrict__ status) {
+                  float* __restrict__ part_ml, uint32_t* __restrict__ counters,
+                  const int32_t* __restrict__ order, int B, int gmax, int Hq, int Hkv, int L_cap,
+                  float scale_log2, int split_keys, int n_splits, int q_chunks,
+                  int32_t* __restrict__ status) {
   using GG = Geo<D>;
   constexpr int MQ = 16 * NQ;
   constexpr int DB = D / 16;
@@ -153,15 +154,20 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
   constexpr int kLd = GG::kLoads / QG;  // 16-byte loads per lane per tensor per tile
   __shared__ __attribute__((aligned(16))) unsigned char lds[Lds<D, NQ, QG>::kBytes];
 
-  // Workgroup order: (sequence, kv head) pair fastest, then key split in
-  // descending order, then query chunk. Workgroups are dealt to the XCDs
-  // round-robin, so each XCD gets every split of an even share of the pairs
-  // (and the query chunks of one pair and split share an XCD and its L2), and
-  // the later splits, which only long sequences have, start first.
+  // Workgroup order: with an order table (more workgroups than fit on the
+  // device at once), the table's: jobs by decreasing key count, so that the
+  // last workgroups to start are the shortest. Otherwise (sequence, kv head)
+  // pair fastest, then key split in descending order, then query chunk.
+  // Workgroups are dealt to the XCDs round-robin, so each XCD gets every
+  // split of an even share of the pairs (and the query chunks of one pair and
+  // split share an XCD and its L2).
   const int P = B * Hkv;
   const int rest = (int)(blockIdx.x / (unsigned)P);
-  const int split = n_splits - 1 - rest % n_splits;
-  const int job = (int)(blockIdx.x % (unsigned)P) * q_chunks + rest / n_splits;
+  const int code = order ? __builtin_amdgcn_readfirstlane(order[blockIdx.x])
+                         : ((int)(blockIdx.x % (unsigned)P) * q_chunks + rest / n_splits) * n_splits +
+                               (n_splits - 1 - rest % n_splits);
+  const int split = code % n_splits;
+  const int job = code / n_splits;
   const int qc = job % q_chunks;
   const int pair_id = job / q_chunks;
   const int g = pair_id % Hkv;
@@ -582,8 +588,65 @@ attn_split_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k
 }
 
 typedef void (*SplitKernel)(const uint16_t*, const uint16_t*, const uint16_t*, const uint8_t*,
-                            const int32_t*, const int32_t*, float*, float*, float*, uint32_t*, int,
-                            int, int, int, int, float, int, int, int, int32_t*);
+                            const int32_t*, const int32_t*, float*, float*, float*, uint32_t*,
+                            const int32_t*, int, int, int, int, int, float, int, int, int, int32_t*);
+
+// The dispatch order of the split workgroups when there are more than fit on
+// the device at once (one workgroup of kOrderThreads): every job (sequence,
+// kv head, query chunk, split) by decreasing key count (in 16-key tiles, a
+// counting sort), empty jobs last, so that the workgroups that start last
+// are the shortest and the device does not idle behind a few long ones.
+// Jobs of equal count take any order among themselves (the results do not
+// depend on the order). Entry: ((b Hkv + g) q_chunks + qc) n_splits + split;
+// the jobs of one (sequence, split) are consecutive, kv head fastest.
+constexpr int kOrderThreads = 1024;
+constexpr int kOrderBuckets = 1024;  // 0: empty; t: t tiles (the last bucket also takes longer jobs)
+static_assert(kOrderThreads == kOrderBuckets, "one scan element per thread");
+__global__ void __launch_bounds__(kOrderThreads)
+attn_order_kernel(const int32_t* __restrict__ kv_len, const int32_t* __restrict__ gamma, int B, int gmax,
+                  int Hkv, int q_chunks, int L_cap, int split_keys, int n_splits, int32_t* __restrict__ order) {
+  __shared__ int cnt[kOrderBuckets];
+  __shared__ int wsum[kOrderThreads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int per_item = Hkv * q_chunks;  // jobs of one (sequence, split)
+  const int n_items = B * n_splits;
+  auto bucket = [&](int item) __attribute__((always_inline)) {
+    const int b = item / n_splits, sp = item % n_splits;
+    const int gam = gamma[b], L = kv_len[b];
+    const bool valid = gam >= 0 && gam <= gmax && L >= gam + 1 && L <= L_cap;
+    const int len = valid ? min(L, (sp + 1) * split_keys) - sp * split_keys : 0;
+    return len <= 0 ? 0 : min((len + kWaveKeys - 1) / kWaveKeys, kOrderBuckets - 1);
+  };
+  for (int i = tid; i < kOrderBuckets; i += kOrderThreads) cnt[i] = 0;
+  __syncthreads();
+  for (int item = tid; item < n_items; item += kOrderThreads) atomicAdd(&cnt[bucket(item)], per_item);
+  __syncthreads();
+  // start of bucket t: the jobs of every longer bucket (thread t holds
+  // bucket kOrderBuckets - 1 - t, an inclusive scan in thread order)
+  const int t_b = kOrderBuckets - 1 - tid;
+  const int c = cnt[t_b];
+  int incl = c;
+  for (int d = 1; d < 64; d <<= 1) {
+    const int o = __shfl_up(incl, d, 64);
+    if (lane >= d) incl += o;
+  }
+  if (lane == 63) wsum[w] = incl;
+  __syncthreads();
+  for (int i = 0; i < w; ++i) incl += wsum[i];
+  __syncthreads();
+  cnt[t_b] = incl - c;  // now each bucket's next free position
+  __syncthreads();
+  for (int item = tid; item < n_items; item += kOrderThreads) {
+    const int pos = atomicAdd(&cnt[bucket(item)], per_item);
+    const int b = item / n_splits, sp = item % n_splits;
+    for (int j = 0; j < per_item; ++j) {
+      // kv head fastest: with a multiple of 8 heads the query chunks of one
+      // (pair, split) fall on one XCD and share its L2
+      const int qc = j / Hkv, g = j % Hkv;
+      order[pos + j] = ((b * Hkv + g) * q_chunks + qc) * n_splits + sp;
+    }
+  }
+}
 
 // A single query chunk reads its K/V tiles once (non-temporal loads); with
 // several chunks the others read the same tiles again, which then should
@@ -649,11 +712,15 @@ int attention_plan(int B, int gamma_max, int Hq, int Hkv, int D, int L_cap, Atte
   sk = (sk + kWaveKeys - 1) / kWaveKeys * kWaveKeys;
   plan->split_keys = sk;
   plan->n_splits = (L_cap + sk - 1) / sk;
-  // [arrival counters: B*Hkv*q_chunks, one per 128-byte line][partial o][partial (m, l)]
+  // [arrival counters: B*Hkv*q_chunks, one per 128-byte line][partial o][partial (m, l)][order]
   const size_t counters = (size_t)B * Hkv * plan->q_chunks * kCounterStride * sizeof(uint32_t);
   plan->part_offset = counters;
-  plan->workspace_bytes =
-      plan->n_splits > 1 ? counters + (size_t)B * Hkv * plan->n_splits * R * (D + 2) * sizeof(float) : 0;
+  size_t bytes = plan->n_splits > 1 ? counters + (size_t)B * Hkv * plan->n_splits * R * (D + 2) * sizeof(float) : 0;
+  const long n_jobs = (long)plan->n_splits * pairs;
+  plan->ordered = plan->n_splits > 1 && n_jobs > target ? 1 : 0;  // (a single split needs no workspace)
+  plan->order_offset = (bytes + 15) / 16 * 16;
+  if (plan->ordered) bytes = plan->order_offset + (size_t)n_jobs * sizeof(int32_t);
+  plan->workspace_bytes = bytes;
   return SR_OK;
 }
 
@@ -669,10 +736,16 @@ int launch_verify_attention(const void* q, const void* k_cache, const void* v_ca
   float* part_ml = part_o ? part_o + (size_t)B * Hkv * plan.n_splits * R * D : nullptr;
   dim3 grid((unsigned)((long)plan.n_splits * plan.q_chunks * B * Hkv));
   const int threads = plan.qg == 1 ? Shape<1>::kThreads : Shape<kMaxQG>::kThreads;
+  int32_t* order = plan.ordered ? (int32_t*)((char*)workspace + plan.order_offset) : nullptr;
+  if (order) {
+    hipLaunchKernelGGL(attn_order_kernel, dim3(1), dim3(kOrderThreads), 0, stream, kv_len, gamma, B, gamma_max,
+                       Hkv, plan.q_chunks, L_cap, plan.split_keys, plan.n_splits, order);
+    if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
+  }
   hipLaunchKernelGGL(pick_split(D, plan.nq, plan.qg, plan.q_chunks), grid, dim3(threads), 0, stream,
                      (const uint16_t*)q, (const uint16_t*)k_cache, (const uint16_t*)v_cache,
-                     cache_mask, kv_len, gamma, out, part_o, part_ml, counters, B, gamma_max, Hq, Hkv,
-                     L_cap, scale * kLog2e, plan.split_keys, plan.n_splits, plan.q_chunks, status);
+                     cache_mask, kv_len, gamma, out, part_o, part_ml, counters, order, B, gamma_max, Hq,
+                     Hkv, L_cap, scale * kLog2e, plan.split_keys, plan.n_splits, plan.q_chunks, status);
   if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
   return SR_OK;
 }

@@ -263,6 +263,8 @@ struct AttentionPlan {
   int split_keys;  // keys per split (multiple of 32)
   int n_splits;    // splits along the cache
   size_t part_offset;  // byte offset of the split partials in the workspace
+  int ordered;         // more workgroups than fit at once: dispatched longest job first
+  size_t order_offset;  // byte offset of the dispatch order in the workspace
   size_t workspace_bytes;
 };
 
