@@ -89,6 +89,7 @@ constexpr int kMaxChunks = 64 * kSlots; // per row
 constexpr int kMaxRows = SPECROUTER_MAX_GAMMA + 1;
 constexpr int kMaxSeqs = 4096;               // sequences per launch (row table in LDS)
 constexpr int kDeviceCoherent = 16;          // buffer cache-policy operand: sc1
+constexpr int kStreamLoad = 2;               // buffer cache-policy operand: non-temporal (the sweep reads each logit once)
 constexpr uint64_t kWaitTicks = 20000;       // 200 us of the 100 MHz real-time counter
 constexpr double kLn2 = 0.6931471805599453;
 constexpr double kSkipped = -1.0;            // a chunk sum left to the finaliser
@@ -347,11 +348,11 @@ __device__ __forceinline__ void issue_loads(const Args& A, const TaskInfo& t, Lo
 #pragma unroll
   for (int i = 0; i < kE / N; ++i)
     lp.v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                            s.rp, (uint32_t)((wbase + (i * 64 + lane) * N) * esz), 0, 0));
+                                            s.rp, (uint32_t)((wbase + (i * 64 + lane) * N) * esz), 0, kStreamLoad));
 #pragma unroll
   for (int i = 0; i < kE / N; ++i)
     lq.v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                            s.rq, (uint32_t)((wbase + (i * 64 + lane) * N) * esz), 0, 0));
+                                            s.rq, (uint32_t)((wbase + (i * 64 + lane) * N) * esz), 0, kStreamLoad));
 }
 
 // Entries outside the row (before its start or past its end) become -inf.
