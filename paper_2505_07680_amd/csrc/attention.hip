@@ -56,7 +56,7 @@ constexpr float kLazy = 8.f;  // log2 headroom of the lazily rescaled softmax re
 // Arrival counters sit one per 128-byte line: the splits of different
 // (sequence, kv head, query chunk) jobs then never contend for one line.
 constexpr int kCounterStride = 32;
-constexpr int kMaxSplitKeys = 4224;  // keys per split at most (about 2 MB of K/V at D = 128)
+constexpr int kMaxSplitKeys = 8448;  // keys per split at most (about 4 MB of K/V at D = 128)
 // Byte offset past the end of any K/V slab (slabs are below 2^31 bytes): a
 // buffer load there returns zero without touching memory.
 constexpr uint32_t kOutOfRange = 0x7ffffff0u;
@@ -717,7 +717,7 @@ int attention_plan(int B, int gamma_max, int Hq, int Hkv, int D, int L_cap, Atte
   plan->part_offset = counters;
   size_t bytes = plan->n_splits > 1 ? counters + (size_t)B * Hkv * plan->n_splits * R * (D + 2) * sizeof(float) : 0;
   const long n_jobs = (long)plan->n_splits * pairs;
-  plan->ordered = plan->n_splits > 1 && n_jobs > target ? 1 : 0;  // (a single split needs no workspace)
+  plan->ordered = n_jobs > target ? 1 : 0;
   plan->order_offset = (bytes + 15) / 16 * 16;
   if (plan->ordered) bytes = plan->order_offset + (size_t)n_jobs * sizeof(int32_t);
   plan->workspace_bytes = bytes;

@@ -1,6 +1,8 @@
 // HBM read-bandwidth probe: a plain streaming read, one contiguous block per
-// workgroup with many independent 16-byte loads in flight per CU, timed by the
-// caller as the practical ceiling for the verify step's memory-bound kernels.
+// workgroup with many independent 16-byte loads in flight per CU, with the
+// non-temporal hint (as the verify step's streaming loads carry it; plain
+// loads read about 12% slower), timed by the caller as the practical ceiling
+// for the verify step's memory-bound kernels.
 
 #include "specrouter_probe.h"
 #include "sr_internal.h"
@@ -22,7 +24,7 @@ probe_read_kernel(const u32x4* __restrict__ p, size_t n, uint32_t* __restrict__ 
   for (; i + (kInFlight - 1) * kThreads < end; i += kInFlight * kThreads) {
     u32x4 v[kInFlight];
 #pragma unroll
-    for (int u = 0; u < kInFlight; ++u) v[u] = p[i + u * kThreads];
+    for (int u = 0; u < kInFlight; ++u) v[u] = __builtin_nontemporal_load(p + i + u * kThreads);
 #pragma unroll
     for (int u = 0; u < kInFlight; ++u) acc ^= v[u][0] ^ v[u][1] ^ v[u][2] ^ v[u][3];
   }

@@ -305,7 +305,7 @@ def test_runs_are_bitwise_deterministic():
 # query chunk, then a second chunk, whose K/V loads carry no non-temporal
 # hint), also with ragged gamma so that a group can have no live rows; each
 # with many cache splits (a few long sequences) and with a single split
-# (enough short sequences to fill the device, no workspace).
+# (more short sequences than fit on the device at once).
 _INSTANCES = [(4, (3, 3), "nq1"), (4, (5, 5), "nq2"), (4, (8, 8), "nq3"), (8, (6, 6), "qg2-nq2"),
               (8, (8, 8), "qg2-nq3"), (8, (0, 8), "qg2-nq3-ragged"), (8, (12, 12), "qg2-nq3-2chunks")]
 SHARP = [(D, G, g, tag, split) for D in (64, 128) for G, g, tag in _INSTANCES for split in ("splits", "onesplit")]
@@ -325,14 +325,13 @@ def test_sharp_softmax_attention(D, G, g, tag, split):
                             V=1000, seed=seed)
         assert sr.specrouter_verify_attention_workspace_size(B, gmax, 2 * G, 2, D, shape.cap) > 0
     else:
-        Hkv, B = 16, 16
-        while B < 512:
-            shape = small_shape(name=f"sharp1-{tag}", B=B, Hq=Hkv * G, Hkv=Hkv, D=D, gamma=g,
-                                ctx=(60, 180), V=1000, seed=seed)
-            if sr.specrouter_verify_attention_workspace_size(B, gmax, Hkv * G, Hkv, D, shape.cap) == 0:
-                break  # one split: no partials, no workspace
-            B *= 2
-        assert sr.specrouter_verify_attention_workspace_size(B, gmax, Hkv * G, Hkv, D, shape.cap) == 0
+        # 64 sequences x 16 kv heads: more (sequence, kv head) pairs than an
+        # MI355X holds workgroups at once (at most 3 per CU), so the cache is
+        # not split; the workspace then holds only the workgroups' dispatch
+        # order
+        Hkv, B = 16, 64
+        shape = small_shape(name=f"sharp1-{tag}", B=B, Hq=Hkv * G, Hkv=Hkv, D=D, gamma=g, ctx=(60, 180),
+                            V=1000, seed=seed)
     inp = level_inputs(shape, logits=False)
     q = bf16_bits_from_f32(f32_from_bf16_bits(inp.q) * 8.0)
     got, _ = run_attention(inp, q=q)
@@ -340,6 +339,22 @@ def test_sharp_softmax_attention(D, G, g, tag, split):
     worst = check_attention(got, ref)
     rms = float(np.sqrt(np.mean(ref[np.abs(ref).sum(-1) > 0] ** 2)))
     say(f"sharp d{D} {tag} {split}: B={inp.B} worst relative L2 {worst:.2e}, output RMS {rms:.2f}")
+
+
+def test_longest_first_dispatch_with_cache_splits():
+    """More split workgroups than fit at once, with caches longer than one
+    split: the workgroups run in the order of a counting sort of their key
+    counts (longest first) and the splits of a sequence are merged as usual
+    (Section 4.4, Eq. 8). Two query groups of three blocks (one workgroup per
+    CU), 40 x 8 (sequence, kv head) pairs, contexts of 8500-9000 keys."""
+    shape = small_shape(name="ordered-splits", B=40, Hq=64, Hkv=8, D=64, gamma=(5, 8), ctx=(8500, 9000),
+                        V=1000, seed=271)
+    inp = level_inputs(shape, logits=False)
+    got, _ = run_attention(inp)
+    seqs = [0, 7, 19, 31, 39]
+    ref, _ = oracle.verify_attention(inp.q, inp.k, inp.v, inp.kv_len, inp.gamma, inp.scale, seqs=seqs)
+    worst = check_attention(got, ref, seqs=seqs)
+    say(f"ordered dispatch with splits: worst relative L2 {worst:.2e}")
 
 
 def test_rollback_idempotent_and_eq9():
