@@ -35,7 +35,7 @@ sys.path.insert(0, HERE)
 
 CAL_BYTES = 256 << 20  # bench.py's calibration copy
 ENTRY_KERNELS = {  # kernel-name fragments launched by each entry point
-    "verify_attention": ["attn_split_kernel"],
+    "verify_attention": ["attn_split_kernel", "attn_order_kernel"],
     "accept_and_diverge": ["accept_kernel", "accept_finish_kernel"],
     "rollback": ["rollback_kernel"],
     "accept_filter": ["accept_filter_kernel"],  # top-k / top-p thresholds (sampling variants only)
