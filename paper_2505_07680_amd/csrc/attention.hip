@@ -601,6 +601,7 @@ typedef void (*SplitKernel)(const uint16_t*, const uint16_t*, const uint16_t*, c
 // the jobs of one (sequence, split) are consecutive, kv head fastest.
 constexpr int kOrderThreads = 1024;
 constexpr int kOrderBuckets = 1024;  // 0: empty; t: t tiles (the last bucket also takes longer jobs)
+constexpr int kOrderKept = 4;        // buckets a thread keeps between the two passes
 static_assert(kOrderThreads == kOrderBuckets, "one scan element per thread");
 __global__ void __launch_bounds__(kOrderThreads)
 attn_order_kernel(const int32_t* __restrict__ kv_len, const int32_t* __restrict__ gamma, int B, int gmax,
@@ -617,9 +618,18 @@ attn_order_kernel(const int32_t* __restrict__ kv_len, const int32_t* __restrict_
     const int len = valid ? min(L, (sp + 1) * split_keys) - sp * split_keys : 0;
     return len <= 0 ? 0 : min((len + kWaveKeys - 1) / kWaveKeys, kOrderBuckets - 1);
   };
-  for (int i = tid; i < kOrderBuckets; i += kOrderThreads) cnt[i] = 0;
+  cnt[tid] = 0;
   __syncthreads();
-  for (int item = tid; item < n_items; item += kOrderThreads) atomicAdd(&cnt[bucket(item)], per_item);
+  // the first kOrderKept items of a thread keep their bucket for the second pass
+  int kept[kOrderKept];
+#pragma unroll
+  for (int u = 0; u < kOrderKept; ++u) {
+    const int item = tid + u * kOrderThreads;
+    kept[u] = item < n_items ? bucket(item) : 0;
+    if (item < n_items) atomicAdd(&cnt[kept[u]], per_item);
+  }
+  for (int item = tid + kOrderKept * kOrderThreads; item < n_items; item += kOrderThreads)
+    atomicAdd(&cnt[bucket(item)], per_item);
   __syncthreads();
   // start of bucket t: the jobs of every longer bucket (thread t holds
   // bucket kOrderBuckets - 1 - t, an inclusive scan in thread order)
@@ -633,11 +643,10 @@ attn_order_kernel(const int32_t* __restrict__ kv_len, const int32_t* __restrict_
   if (lane == 63) wsum[w] = incl;
   __syncthreads();
   for (int i = 0; i < w; ++i) incl += wsum[i];
+  cnt[t_b] = incl - c;  // now each bucket's next free position (each thread rewrites only its own)
   __syncthreads();
-  cnt[t_b] = incl - c;  // now each bucket's next free position
-  __syncthreads();
-  for (int item = tid; item < n_items; item += kOrderThreads) {
-    const int pos = atomicAdd(&cnt[bucket(item)], per_item);
+  auto place = [&](int item, int bk) __attribute__((always_inline)) {
+    const int pos = atomicAdd(&cnt[bk], per_item);
     const int b = item / n_splits, sp = item % n_splits;
     for (int j = 0; j < per_item; ++j) {
       // kv head fastest: with a multiple of 8 heads the query chunks of one
@@ -645,12 +654,15 @@ attn_order_kernel(const int32_t* __restrict__ kv_len, const int32_t* __restrict_
       const int qc = j / Hkv, g = j % Hkv;
       order[pos + j] = ((b * Hkv + g) * q_chunks + qc) * n_splits + sp;
     }
+  };
+#pragma unroll
+  for (int u = 0; u < kOrderKept; ++u) {
+    const int item = tid + u * kOrderThreads;
+    if (item < n_items) place(item, kept[u]);
   }
+  for (int item = tid + kOrderKept * kOrderThreads; item < n_items; item += kOrderThreads) place(item, bucket(item));
 }
 
-// A single query chunk reads its K/V tiles once (non-temporal loads); with
-// several chunks the others read the same tiles again, which then should
-// stay in the caches.
 template <int D>
 SplitKernel pick_split(int nq, int qg, int q_chunks) {
   if (qg == 1) {
