@@ -16,6 +16,10 @@
 // workgroup to arrive merges all partials in split order and writes the
 // output, then resets the counter, so the workspace is left ready for the
 // next call. The summation order is fixed, so results are reproducible.
+// When the workgroups outnumber what the device holds at once, a small
+// kernel first sorts the jobs by key count and the workgroups take them
+// longest first, so that the device does not idle behind a few long
+// workgroups at the end of a ragged batch.
 //
 // Per 16-key tile of a stream:
 //   * K and V rows are fetched with coalesced 16-byte loads into a register
