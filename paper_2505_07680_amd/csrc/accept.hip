@@ -35,11 +35,13 @@
 //     records (issued before the step's prefetch, so that they return during
 //     its first pass) and re-loads them until all are present (for at most
 //     about 200 us, then the task gives up, see below); it merges them into
-//     the row's normalisers in a fixed order (fp64) and the chunk's factors
-//     f_p = 2^(r_c - r_max)/S_p, f_q likewise (the shifts are integers, so
-//     2^(r_c - r_max) is exact); the lanes then sum |P - Q| over their
-//     entries, scaled so that one of the two factors is 1 (fma(a, rho, -b)
-//     with rho = min/max of the factors), and each wave publishes its part.
+//     the row's normalisers in a fixed order (fp64); each wave forms its own
+//     factors f_p = 2^(r_w - r_max)/S_p, f_q likewise, from its own shifts
+//     r_w (integers, so 2^(r_w - r_max) is exact; 1/S from the hardware
+//     reciprocal estimate and two Newton steps); the lanes then sum |P - Q|
+//     over their entries, scaled so that one of the two factors is 1
+//     (fma(a, rho, -b) with rho = min/max of the factors), and each wave
+//     publishes its part.
 // Waiting is bounded: a task whose row is not complete after the time limit
 // publishes a "skipped" mark instead of its sum, and the row's finaliser
 // recomputes that chunk's sum from memory with the same arithmetic. No
