@@ -24,11 +24,13 @@
 // at once) from an LDS table decoded a window at a time; task k+1's loads are
 // issued before task k's first pass, and pair task k's TV sum is formed during
 // step k+1:
-//  1. first pass: the chunk's maxima m, integer exponent shifts
-//     r = ceil(m log2(e)/T), the exponentials 2^x with x = z log2(e)/T - r
-//     (kept in registers until the TV sum; the largest lies in (1/2, 1]),
-//     their sums and the KL numerator sum e_p (x_p - x_q); one 32-byte record
-//     per chunk, published with device-coherent stores, bit-inverted so that
+//  1. first pass: each wave's maxima m over its 1024 entries, integer
+//     exponent shifts r = ceil(m log2(e)/T), the exponentials 2^x with
+//     x = z log2(e)/T - r (kept in registers until the TV sum; the largest
+//     lies in (1/2, 1]), their sums and the KL numerator sum e_p (x_p - x_q);
+//     after one barrier a builder wave folds the four waves into the chunk's
+//     shifts (the largest; powers of two) and one 32-byte record per chunk,
+//     published with device-coherent stores, bit-inverted so that
 //     an all-zero word means "not yet written" (naturally aligned 8-byte
 //     accesses are single-copy atomic);
 //  2. one step later, one wave (rotating over the four) has loaded the row's
