@@ -345,12 +345,14 @@ def test_longest_first_dispatch_with_cache_splits():
     """More split workgroups than fit at once, with caches longer than one
     split: the workgroups run in the order of a counting sort of their key
     counts (longest first) and the splits of a sequence are merged as usual
-    (Section 4.4, Eq. 8). Two query groups of three blocks (one workgroup per
+    (Section 4.4, Eq. 8); a second call gives the same bits. Two query groups of three blocks (one workgroup per
     CU), 40 x 8 (sequence, kv head) pairs, contexts of 8500-9000 keys."""
     shape = small_shape(name="ordered-splits", B=40, Hq=64, Hkv=8, D=64, gamma=(5, 8), ctx=(8500, 9000),
                         V=1000, seed=271)
     inp = level_inputs(shape, logits=False)
     got, _ = run_attention(inp)
+    again, _ = run_attention(inp)  # jobs of equal length start in any order: the same bits
+    np.testing.assert_array_equal(got, again)
     seqs = [0, 7, 19, 31, 39]
     ref, _ = oracle.verify_attention(inp.q, inp.k, inp.v, inp.kv_len, inp.gamma, inp.scale, seqs=seqs)
     worst = check_attention(got, ref, seqs=seqs)
