@@ -612,10 +612,46 @@ def chain_bench(args, sr, shape):
         "mean_k_tgt": round(float(ab_t.accept_len.float().mean().item()), 3),
         "status_bits": status,
         "cpu_baseline": None if args.no_cpu else chain_cpu_baseline(ci, shape),
+        "boundary": None if args.no_cpu else chain_boundary_check(ci, shape, ab_i, ab_t, g3),
         "note": "three-level chain step (intermediate and target levels); the draft level's decode attention apart",
         "input_gen_s": round(gen_s, 2),
     }
     print(json.dumps(line), flush=True)
+
+
+def chain_boundary_check(ci, shape, ab_i, ab_t, g3):
+    """Both accept levels of the timed chain steps against the CPU reference
+    on every sequence: the intermediate level on its own inputs, the target
+    level on the window the reference derives from the intermediate level's
+    outcome (so a different intermediate outcome shows as a mismatch at both
+    levels). Decisions must agree exactly except on boundary cases (a uniform
+    within 1e-6 of a CDF breakpoint or acceptance threshold)."""
+    import oracle
+
+    inter, t = ci["inter"], ci["target"]
+    z2 = ci["z"][1]
+    ctx, gt = shape.ctx, shape.gamma_tgt
+    r2 = oracle.accept_and_diverge(inter.p_logits, inter.q_logits, inter.drafts, inter.gamma, inter.u_acc,
+                                   inter.u_res, kv_len=inter.kv_len)
+    w3 = oracle.chain.target_window(r2["accept_len"], gt)
+    d3 = oracle.chain.target_drafts(r2["out_tokens"], w3, gt)
+    kv3 = (ctx + w3 + 1).astype(np.int32)
+    r3 = oracle.accept_and_diverge(t["p_logits"], z2[:, :gt], d3, w3, t["u_acc"], t["u_res"], kv_len=kv3)
+    out = {}
+    for name, acc, ref, extra in (("intermediate", ab_i, r2, None), ("target", ab_t, r3, (g3, w3))):
+        k = acc.accept_len.cpu().numpy()
+        toks = acc.out_tokens.cpu().numpy()
+        same = (k == ref["accept_len"]) & (toks == ref["out_tokens"]).all(axis=1)
+        if extra is not None:
+            same &= extra[0].cpu().numpy() == extra[1]
+        bd = ref["boundary"].astype(bool)
+        out[name] = {"sequences": int(k.shape[0]), "boundary_cases": int(bd.sum()),
+                     "boundary_mismatches": int((bd & ~same).sum()),
+                     "mismatches_outside_boundary": int((~bd & ~same).sum()),
+                     "min_margin": float(np.min(ref["margin"]))}
+    out["note"] = ("GPU accept lengths, tokens (and the target window) vs the CPU reference on every sequence "
+                   "(margin < 1e-6 = boundary)")
+    return out
 
 
 def chain_cpu_baseline(ci, shape, target_s=10.0):

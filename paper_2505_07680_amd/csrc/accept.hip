@@ -1587,634 +1587,18 @@ __global__ void __launch_bounds__(64 * kFinWaves) accept_finish_kernel(Args A) {
 }
 
 // ============================================================================
-// Top-k / top-p thresholds (the logits processors after the temperature)
-//
-// One workgroup of 1024 threads per live row (verifier rows p_0..p_gamma,
-// draft rows q_0..q_{gamma-1}). Logits are compared through an
-// order-preserving 32-bit key (-0 counted as +0).
-//
-// Candidate path (one read of the row): every thread keeps the kFiltTop
-// largest keys it sees and the largest key it dropped; for top-p alone it
-// also sums the row's mass 2^(z log2(e)/T) (relative to a per-thread
-// reference, rescaled to the row maximum at the end, summed in thread
-// order). The kept keys (at most 1024 kFiltTop) go to LDS and the threshold
-// is selected among them by the radix select below. It is exact when every
-// key at or above the threshold is a candidate: top-k needs the largest
-// dropped key to be at most the k-th largest candidate (strictly below it
-// when top-p follows, whose input must then be complete); top-p alone needs
-// it strictly below the selected key and the candidates' mass from that key
-// up to reach p times the row's total (else a lower, dropped key could be
-// the threshold). A row that fails these checks takes the exact path.
-//
-// Exact path: a most-significant-digit radix select over the row: a 12-bit first digit (sign,
-// exponent and three mantissa bits, so that logits of one row spread over
-// many bins), then 10 + 10 bits for fp32 keys or 4 bits for bf16 keys (whose
-// low 16 bits are fixed by the sign). Each level histograms the digit of the
-// keys that still match the selected prefix into one LDS histogram shared by
-// the waves:
-//   top-k: counts; the bin holding the k-th largest key is the one where the
-//     count of larger keys first reaches k;
-//   top-p: masses over the keys top-k kept; the bin of the smallest kept logit
-//     is the lowest non-empty bin whose mass above (the larger bins plus the
-//     mass above the prefix) is below p times the total.
-// Masses are accumulated as 64-bit fixed-point integers (each term rounded to
-// 2^-40), so the sums do not depend on the order of the LDS atomics and every
-// call decides the same way. The first level reads the row once: counts, the
-// row maximum M and, for top-p, each bin's mass relative to the largest value
-// the bin can hold (terms 2^((z - top of bin) log2(e)/T) <= 1, rescaled to M
-// afterwards, so no earlier pass for M is needed). When the selected bin (or,
-// with top-p to follow, the bin and every key above it) holds at most kFiltCap
-// keys, a second read gathers them into LDS and the remaining levels (and the
-// whole of top-p after top-k) run there: a row is read twice. A row whose
-// logits crowd into one bin is read again at each further level. The
-// threshold t (a logit value; entries below it are removed) goes to
-// thr[b][j][p or q]. Keys are exact, so top-k matches the exact rule; top-p
-// decides on masses with ~1e-7 relative error, so a logit whose larger mass is
-// within about that of p may fall either way.
-
+// Top-k / top-p thresholds in two workgroup widths (filter.inc): 512 threads
+// when the rows fill at least two workgroups per CU (two then fit a CU, by
+// registers and LDS, so one row's selection overlaps the other's streaming),
+// else 1024 (fewer rows than that: each row gets more of the device).
+namespace filt512 {
+constexpr int kFiltThreads = 512;
+#include "filter.inc"
+}  // namespace filt512
+namespace filt1024 {
 constexpr int kFiltThreads = 1024;
-constexpr int kFiltWaves = kFiltThreads / 64;
-constexpr int kFiltBins = 4096;  // the widest digit: 12 bits
-constexpr int kFiltCap = 8064;   // candidate keys held in LDS (two workgroups fit a CU's 160 KB)
-constexpr int kFiltUnroll = 4;   // row loads in flight per thread
-constexpr int kFiltTop = 7;      // candidate keys kept per thread (1024 kFiltTop <= kFiltCap)
-constexpr double kFix = 1099511627776.0;  // 2^40: fixed-point scale of a mass term
-
-__device__ __forceinline__ uint32_t order_key(float z) {
-  const uint32_t u = __float_as_uint(z + 0.f);  // -0 -> +0
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-__device__ __forceinline__ float key_value(uint32_t k) {
-  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
-}
-// round(t 2^40) for a term t in [0, 1]
-__device__ __forceinline__ uint64_t fixed_term(float t) { return (uint64_t)((double)t * kFix + 0.5); }
-
-struct FiltShared {
-  uint32_t cnt[kFiltBins];
-  uint64_t mass[kFiltBins];  // fixed point
-  uint32_t cand[kFiltCap];
-  uint32_t wtot_u[kFiltWaves];
-  double wtot_d[kFiltWaves];
-  uint32_t wmax[kFiltWaves];
-  uint32_t n;      // candidates gathered so far
-  uint32_t pick;   // selected bin
-  uint32_t need;   // top-k: keys still to count inside the selected bin
-  uint32_t nge;    // top-k: keys in the selected bin and the bins above it
-  uint32_t cpick;  // top-p: keys in the selected bin
-  int lowest;      // top-p: the lowest qualifying bin
-  double above;    // top-p: mass above the selected prefix (units of 2^(M lg))
-  double total;    // top-p: mass of the keys top-k kept
-};
-
-// Digit layout of level l: bits [shift, shift + bits) of the key.
-template <bool BF16>
-__device__ __forceinline__ int filt_shift(int l) {
-  return l == 0 ? 20 : BF16 ? 16 : l == 1 ? 10 : 0;
-}
-template <bool BF16>
-__device__ __forceinline__ int filt_bits(int l) {
-  return l == 0 ? 12 : BF16 ? 4 : 10;
-}
-
-// Block-wide exclusive prefix sums in thread order (a fixed order).
-__device__ __forceinline__ uint32_t filt_excl_scan(FiltShared& F, uint32_t s) {
-  const int lane = threadIdx.x & 63, w = wave_id();
-  const uint32_t incl = (uint32_t)wave_incl_scan_i((int)s);
-  if (lane == 63) F.wtot_u[w] = incl;
-  __syncthreads();
-  uint32_t base = 0u;
-  for (int i = 0; i < w; ++i) base += F.wtot_u[i];
-  return base + incl - s;
-}
-__device__ __forceinline__ double filt_excl_scan(FiltShared& F, double s, double& total) {
-  const int lane = threadIdx.x & 63, w = wave_id();
-  const double incl = wave_incl_scan_d(s);
-  if (lane == 63) F.wtot_d[w] = incl;
-  __syncthreads();
-  double base = 0.0;
-  total = 0.0;
-  for (int i = 0; i < kFiltWaves; ++i) {
-    if (i == w) base = total;
-    total += F.wtot_d[i];
-  }
-  return base + incl - s;
-}
-
-// A row in aligned 16-byte vectors: vector v holds entries v*N - phi .. v*N - phi + N - 1.
-template <bool BF16>
-struct FiltRow {
-  __amdgpu_buffer_rsrc_t rs;
-  int phi, V, nvec;
-  __device__ void load(int v, float (&z)[Vec<BF16>::N]) const {
-    constexpr int N = Vec<BF16>::N;
-    const u32x4 u = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, (uint32_t)v * 16u, 0, 0));
-    if constexpr (BF16) {
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        z[2 * k] = bf16_lo(u[k]);
-        z[2 * k + 1] = bf16_hi(u[k]);
-      }
-    } else {
-#pragma unroll
-      for (int k = 0; k < N; ++k) z[k] = __uint_as_float(u[k]);
-    }
-  }
-  __device__ bool valid(int v, int k) const {
-    const int i = v * Vec<BF16>::N + k - phi;
-    return i >= 0 && i < V;
-  }
-};
-
-// Visits every entry of the row (f(z)) with kFiltUnroll vector loads in flight per thread.
-template <bool BF16, typename Fn>
-__device__ __forceinline__ void filt_scan_row(const FiltRow<BF16>& R, Fn&& f) {
-  constexpr int N = Vec<BF16>::N;
-  for (int v0 = (int)threadIdx.x; v0 < R.nvec; v0 += kFiltThreads * kFiltUnroll) {
-    float z[kFiltUnroll][N];
-#pragma unroll
-    for (int u = 0; u < kFiltUnroll; ++u)
-      if (v0 + u * kFiltThreads < R.nvec) R.load(v0 + u * kFiltThreads, z[u]);
-#pragma unroll
-    for (int u = 0; u < kFiltUnroll; ++u) {
-      const int v = v0 + u * kFiltThreads;
-      if (v >= R.nvec) break;
-      if (R.valid(v, 0) && R.valid(v, N - 1)) {  // the whole vector lies in the row
-#pragma unroll
-        for (int k = 0; k < N; ++k) f(z[u][k]);
-      } else {
-#pragma unroll
-        for (int k = 0; k < N; ++k)
-          if (R.valid(v, k)) f(z[u][k]);
-      }
-    }
-  }
-}
-
-// Histogram pass over the row in memory: digit (key >> shift) & dmask of the
-// keys with (key & pmask) == prefix and key >= lo; kmax collects every key.
-// Masses (MASS): relative to M (rel_bin false), or to the top of each
-// first-level bin (rel_bin true, prefix empty).
-template <bool BF16, bool MASS>
-__device__ __forceinline__ void filt_hist_row(FiltShared& F, const FiltRow<BF16>& R, uint32_t prefix, uint32_t pmask, int shift,
-                              uint32_t dmask, uint32_t lo, float M, float lg, bool rel_bin, uint32_t& kmax) {
-  filt_scan_row<BF16>(R, [&](float z) {
-    const uint32_t key = order_key(z);
-    kmax = max(kmax, key);
-    if ((key & pmask) == prefix && key >= lo) {
-      const uint32_t d = (key >> shift) & dmask;
-      atomicAdd(&F.cnt[d], 1u);
-      if (MASS && z != kNegInf) {
-        const float top = rel_bin ? key_value((d << shift) | ((1u << shift) - 1u)) : M;
-        atomicAdd((unsigned long long*)&F.mass[d], (unsigned long long)fixed_term(exp2_hw((z - top) * lg)));
-      }
-    }
-  });
-}
-
-// The same over the n candidate keys in LDS (masses relative to M).
-template <bool MASS>
-__device__ __forceinline__ void filt_hist_cand(FiltShared& F, int n, uint32_t prefix, uint32_t pmask, int shift, uint32_t dmask,
-                               uint32_t lo, float M, float lg) {
-  for (int i = threadIdx.x; i < n; i += kFiltThreads) {
-    const uint32_t key = F.cand[i];
-    if ((key & pmask) == prefix && key >= lo) {
-      const uint32_t d = (key >> shift) & dmask;
-      atomicAdd(&F.cnt[d], 1u);
-      const float z = key_value(key);
-      if (MASS && z != kNegInf)
-        atomicAdd((unsigned long long*)&F.mass[d], (unsigned long long)fixed_term(exp2_hw((z - M) * lg)));
-    }
-  }
-}
-
-// Gathers the row's keys in [klo, khi] into F.cand (F.n counts them; the
-// caller has checked that they fit).
-template <bool BF16>
-__device__ __forceinline__ void filt_gather_row(FiltShared& F, const FiltRow<BF16>& R, uint32_t klo, uint32_t khi) {
-  filt_scan_row<BF16>(R, [&](float z) {
-    const uint32_t key = order_key(z);
-    if (key >= klo && key <= khi) {
-      const uint32_t slot = atomicAdd(&F.n, 1u);
-      if (slot < (uint32_t)kFiltCap) F.cand[slot] = key;
-    }
-  });
-}
-
-// Thread t owns bins nb-1-t*per down to nb-t*per-per (descending order).
-struct FiltOwn {
-  int per, own, hi;
-  __device__ explicit FiltOwn(int nb) {
-    per = nb > kFiltThreads ? nb / kFiltThreads : 1;
-    own = (int)threadIdx.x * per < nb ? per : 0;
-    hi = nb - 1 - (int)threadIdx.x * per;
-  }
-};
-
-// top-k: the bin holding the need-th largest key of the histogram.
-__device__ __forceinline__ void filt_select_count(FiltShared& F, int nb, uint32_t need) {
-  const FiltOwn o(nb);
-  uint32_t c[4], s = 0u;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    c[i] = i < o.own ? F.cnt[o.hi - i] : 0u;
-    s += c[i];
-  }
-  uint32_t run = filt_excl_scan(F, s);  // keys in the higher bins
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    if (i < o.own && run < need && need <= run + c[i]) {
-      F.pick = (uint32_t)(o.hi - i);
-      F.need = need - run;
-      F.nge = run + c[i];
-    }
-    run += c[i];
-  }
-  __syncthreads();
-}
-
-// top-p: the lowest non-empty bin whose mass above is below p times the
-// total (the total is this histogram's at the first level). Bin masses are
-// in units of 2^(M lg); first-level row histograms hold them relative to the
-// top of each bin (rel_bin) and are rescaled here.
-__device__ __forceinline__ void filt_select_mass(FiltShared& F, int nb, float top_p, bool first, bool rel_bin, int shift, float M,
-                                 float lg) {
-  const FiltOwn o(nb);
-  const double above = F.above;
-  uint32_t c[4];
-  double ms[4], s = 0.0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    c[i] = i < o.own ? F.cnt[o.hi - i] : 0u;
-    double m = i < o.own ? (double)F.mass[o.hi - i] / kFix : 0.0;
-    if (rel_bin && m > 0.0) {
-      const uint32_t d = (uint32_t)(o.hi - i);
-      const float top = key_value((d << shift) | ((1u << shift) - 1u));
-      m *= exp2(((double)top - (double)M) * (double)lg);
-    }
-    ms[i] = m;
-    s += ms[i];
-  }
-  double all;
-  double run = above + filt_excl_scan(F, s, all);  // mass above this thread's first bin
-  const double total = first ? all : F.total;
-  const double bar = (double)top_p * total;
-  int low = -1;
-  double low_above = 0.0;
-  uint32_t low_cnt = 0u;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    if (i < o.own && c[i] > 0u && run < bar) {
-      low = o.hi - i;
-      low_above = run;
-      low_cnt = c[i];
-    }
-    run += ms[i];
-  }
-  if (low >= 0) atomicMin(&F.lowest, low);
-  __syncthreads();
-  if (low >= 0 && low == F.lowest) {
-    F.pick = (uint32_t)low;
-    F.above = low_above;
-    F.cpick = low_cnt;
-  }
-  if (first && threadIdx.x == 0) F.total = total;
-  __syncthreads();
-}
-
-// The block-wide maximum of an unsigned key.
-__device__ __forceinline__ uint32_t filt_block_max(FiltShared& F, uint32_t x) {
-  const int lane = threadIdx.x & 63, w = wave_id();
-  const uint32_t wm = (uint32_t)wave_max_i((int)(x ^ 0x80000000u)) ^ 0x80000000u;  // unsigned max
-  __syncthreads();  // earlier readers of F.wmax are done
-  if (lane == 0) F.wmax[w] = wm;
-  __syncthreads();
-  uint32_t m = 0u;
-  for (int i = 0; i < kFiltWaves; ++i) m = max(m, F.wmax[i]);
-  return m;
-}
-
-// Candidate path, the one read of the row: each thread's C largest keys
-// (kept in descending order by a min/max insertion network, 0 = empty) go to
-// F.cand (F.n of them, in thread order); returns the row's largest key and
-// the largest key any thread dropped (0 if none was dropped) and, with MASS,
-// the row's mass sum_z 2^((z - M) lg) for the row maximum M. Each thread sums
-// its terms relative to a reference that is raised, once per round of loads,
-// when the round's largest entry exceeds it by more than 2^8; the reference
-// is then rescaled to M and the threads' sums added in thread order. Rounds
-// whose vectors all lie inside the row skip the per-entry range test; in the
-// others, entries outside the row take key 0 and z = -inf (no effect on any
-// of these).
-template <bool BF16, bool MASS, int C>
-struct FiltCollect {
-  static constexpr int N = Vec<BF16>::N;
-  uint32_t top[C];
-  uint32_t ev = 0u, km = 0u;
-  double sum = 0.0;
-  float ref = kNegInf, lim = kNegInf;
-
-  template <bool MASKED>
-  __device__ __forceinline__ void round(const FiltRow<BF16>& R, int v0, float lg, float head) {
-    float z[kFiltUnroll][N];
-#pragma unroll
-    for (int u = 0; u < kFiltUnroll; ++u) R.load(MASKED ? min(v0 + u * kFiltThreads, R.nvec - 1) : v0 + u * kFiltThreads, z[u]);
-    float zmax = kNegInf;
-#pragma unroll
-    for (int u = 0; u < kFiltUnroll; ++u) {
-      const int v = v0 + u * kFiltThreads;
-#pragma unroll
-      for (int k = 0; k < N; ++k) {
-        const bool in = !MASKED || (v < R.nvec && R.valid(v, k));
-        if (MASKED) z[u][k] = in ? z[u][k] : kNegInf;
-        const uint32_t key = in ? order_key(z[u][k]) : 0u;
-        km = max(km, key);
-        ev = max(ev, min(top[C - 1], key));
-#pragma unroll
-        for (int i = C - 1; i > 0; --i) top[i] = max(top[i], min(top[i - 1], key));
-        top[0] = max(top[0], key);
-        if (MASS) zmax = fmaxf(zmax, z[u][k]);
-      }
-    }
-    if (MASS) {
-      if (zmax > lim) {  // (rare after the first rounds)
-        sum = ref == kNegInf ? 0.0 : sum * exp2((double)(ref - zmax) * (double)lg);
-        ref = zmax;
-        lim = zmax + head;
-      }
-      const float rl = ref == kNegInf ? 0.f : ref * lg;  // (ref = -inf: every entry so far is -inf)
-      float part = 0.f;
-#pragma unroll
-      for (int u = 0; u < kFiltUnroll; ++u)
-#pragma unroll
-        for (int k = 0; k < N; ++k) part += exp2_hw(fmaf(z[u][k], lg, -rl));
-      sum += (double)part;
-    }
-  }
-
-  __device__ __forceinline__ void run(FiltShared& F, const FiltRow<BF16>& R, float lg, uint32_t& kmax,
-                                      uint32_t& dropped, double& mass) {
-#pragma unroll
-    for (int i = 0; i < C; ++i) top[i] = 0u;
-    const float head = 8.f / lg;
-    // vectors [vlo, vhi] lie inside the row; a round covers kFiltThreads kFiltUnroll of them
-    const int vlo = R.phi > 0 ? 1 : 0;
-    const int vhi = (R.V + R.phi) / N - 1;
-    constexpr int kRound = kFiltThreads * kFiltUnroll;
-    for (int base = 0; base < R.nvec; base += kRound) {
-      const int v0 = base + (int)threadIdx.x;
-      if (base >= vlo && base + kRound - 1 <= vhi)  // workgroup-uniform
-        round<false>(R, v0, lg, head);
-      else
-        round<true>(R, v0, lg, head);
-    }
-    kmax = filt_block_max(F, km);
-    dropped = filt_block_max(F, ev);
-    if (MASS) {
-      const float M = key_value(kmax);
-      const double mine = ref == kNegInf ? 0.0 : sum * exp2((double)(ref - M) * (double)lg);
-      __syncthreads();  // F.wtot_d free
-      filt_excl_scan(F, mine, mass);
-    }
-    uint32_t c = 0u;
-#pragma unroll
-    for (int i = 0; i < C; ++i) c += top[i] != 0u ? 1u : 0u;
-    __syncthreads();  // F.wtot_u free
-    const uint32_t off = filt_excl_scan(F, c);
-#pragma unroll
-    for (int i = 0; i < C; ++i)
-      if (top[i] != 0u) F.cand[off + i] = top[i];
-    if (threadIdx.x == kFiltThreads - 1) F.n = off + c;
-    __syncthreads();
-  }
-};
-
-template <bool BF16>
-__global__ void __launch_bounds__(kFiltThreads) accept_filter_kernel(Args A, int top_k, float top_p) {
-  constexpr int N = Vec<BF16>::N, esz = Vec<BF16>::esz;
-  constexpr int kLevels = BF16 ? 2 : 3;
-  __shared__ FiltShared F;
-  const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
-  const int per_seq = 2 * A.gmax + 1;  // p rows 0..gmax, then q rows 0..gmax-1
-  const int b = (int)blockIdx.x / per_seq, r = (int)blockIdx.x % per_seq;
-  const bool is_q = r > A.gmax;
-  const int j = is_q ? r - (A.gmax + 1) : r;
-  const int gam = A.gamma[b];
-  if (gam < 0 || gam > A.gmax || (is_q ? j >= gam : j > gam)) return;  // not a live row
-  FiltRow<BF16> R;
-  R.V = A.V;
-  R.phi = (int)(((int64_t)j * A.V) % N);
-  R.nvec = (R.phi + A.V + N - 1) / N;
-  const char* base = is_q ? (const char*)A.q + ((int64_t)b * A.q_stride + (int64_t)j * A.V - R.phi) * esz
-                          : (const char*)A.p + ((int64_t)b * A.p_stride + (int64_t)j * A.V - R.phi) * esz;
-  R.rs = make_rsrc(base, (size_t)R.nvec * 16);
-
-  auto clear = [&](int nb) __attribute__((always_inline)) {
-    __syncthreads();  // every thread is done with the previous level's histogram and picks
-    for (int i = tid; i < nb; i += kFiltThreads) {
-      F.cnt[i] = 0u;
-      F.mass[i] = 0ull;
-    }
-    if (tid == 0) {
-      F.pick = 0u;
-      F.need = 1u;
-      F.nge = 0u;
-      F.cpick = 0u;
-      F.lowest = INT_MAX;
-    }
-    __syncthreads();
-  };
-  // Gathers the keys in [klo, khi] into F.cand; returns their count.
-  auto gather = [&](uint32_t klo, uint32_t khi) __attribute__((always_inline)) {
-    __syncthreads();  // every thread has read the picks (and is done with F.cand)
-    if (tid == 0) F.n = 0u;
-    __syncthreads();
-    filt_gather_row<BF16>(F, R, klo, khi);
-    __syncthreads();
-    return (int)min(F.n, (uint32_t)kFiltCap);
-  };
-  // The block-wide maximum of kmax.
-  auto block_max = [&](uint32_t kmax) __attribute__((always_inline)) {
-    const uint32_t wm = (uint32_t)wave_max_i((int)(kmax ^ 0x80000000u)) ^ 0x80000000u;  // unsigned max
-    if (lane == 0) F.wmax[w] = wm;
-    __syncthreads();
-    uint32_t m = 0u;
-    for (int i = 0; i < kFiltWaves; ++i) m = max(m, F.wmax[i]);
-    return m;
-  };
-  // ---- candidate path
-  uint32_t thr_key = 0u;
-  bool fast_ok = false;
-  {
-    const bool mass_needed = top_k == 0 && top_p < 1.f;
-    uint32_t ckmax = 0u, dropped = 0u;
-    double W = 0.0;
-    // top-k alone with k <= 64 keeps three candidates per thread (more than
-    // three of the k largest in one thread's share is rare), else seven
-    if (mass_needed) {
-      FiltCollect<BF16, true, kFiltTop> fc;
-      fc.run(F, R, A.lg, ckmax, dropped, W);
-    } else if (top_p >= 1.f && top_k <= 64) {
-      FiltCollect<BF16, false, 3> fc;
-      fc.run(F, R, A.lg, ckmax, dropped, W);
-    } else {
-      FiltCollect<BF16, false, kFiltTop> fc;
-      fc.run(F, R, A.lg, ckmax, dropped, W);
-    }
-    const float M = key_value(ckmax);
-    // The thresholds from the nc keys in F.cand, which hold every key above
-    // drop. True when exact; otherwise bound is a key at or below the true
-    // threshold (the candidates' own threshold: keys missing from them only
-    // lower it), or 0 when there is none.
-    auto select = [&](int nc, uint32_t drop, uint32_t& bound) __attribute__((always_inline)) -> bool {
-      bound = 0u;
-      if (top_k > nc) return false;  // fewer candidates than k
-      uint32_t lo = 0u;
-      if (top_k > 0) {  // the k-th largest candidate
-        uint32_t prefix = 0u, pmask = 0u, need = (uint32_t)top_k;
-        for (int l = 0; l < kLevels; ++l) {
-          const int sh = filt_shift<BF16>(l), nb = 1 << filt_bits<BF16>(l);
-          clear(nb);
-          filt_hist_cand<false>(F, nc, prefix, pmask, sh, (uint32_t)nb - 1u, 0u, 0.f, 0.f);
-          __syncthreads();
-          filt_select_count(F, nb, need);
-          need = F.need;
-          prefix |= F.pick << sh;
-          pmask |= ((uint32_t)nb - 1u) << sh;
-        }
-        if (BF16) prefix |= (prefix & 0x80000000u) ? 0u : 0xffffu;  // the fixed low half of bf16 keys
-        lo = prefix;
-        // every key at or above lo is a candidate (strictly above drop when
-        // top-p follows: its input must be complete)
-        if (!(top_p < 1.f ? drop < lo : drop <= lo)) {
-          bound = lo;
-          return false;
-        }
-      }
-      thr_key = lo;
-      if (top_p < 1.f) {  // top-p over the candidates top-k kept
-        __syncthreads();
-        if (tid == 0) {
-          F.above = 0.0;
-          F.total = W;  // top-p alone: the row's mass (after top-k: the first level's total)
-        }
-        __syncthreads();
-        uint32_t prefix = 0u, pmask = 0u;
-        double incl = 0.0;
-        for (int l = 0; l < kLevels; ++l) {
-          const int sh = filt_shift<BF16>(l), nb = 1 << filt_bits<BF16>(l);
-          clear(nb);
-          filt_hist_cand<true>(F, nc, prefix, pmask, sh, (uint32_t)nb - 1u, lo, M, A.lg);
-          __syncthreads();
-          filt_select_mass(F, nb, top_p, l == 0 && top_k > 0, false, sh, M, A.lg);
-          prefix |= F.pick << sh;
-          pmask |= ((uint32_t)nb - 1u) << sh;
-          incl = F.above + (double)F.mass[F.pick] / kFix;  // candidates' mass from the selected bin up
-        }
-        if (BF16) prefix |= (prefix & 0x80000000u) ? 0u : 0xffffu;
-        thr_key = prefix;
-        if (top_k == 0 && !(drop < thr_key && (incl >= (double)top_p * W || drop == 0u))) {
-          bound = thr_key;
-          return false;
-        }
-      }
-      return true;
-    };
-    uint32_t bound = 0u;
-    fast_ok = select((int)F.n, dropped, bound);
-    if (!fast_ok && bound > 0u) {
-      // a second read gathers every key at or above bound (none below it is
-      // then a candidate), when they fit in LDS
-      const int n2 = gather(bound, 0xffffffffu);
-      if (F.n <= (uint32_t)kFiltCap) {
-        uint32_t unused;
-        fast_ok = select(n2, bound - 1u, unused);
-      }
-    }
-  }
-
-  int ncand = 0;         // keys in F.cand
-  bool cand_ge = false;  // F.cand holds every key >= lo
-  uint32_t lo = 0u;      // keys below lo are removed
-  uint32_t kmax = 0u;
-  bool first_read_done = false;  // a top-p first level over the row is already in the histogram
-
-  // ---- exact path (rows the candidates do not settle)
-  // top-k: radix select of the k-th largest key
-  if (!fast_ok && top_k > 0) {
-    uint32_t prefix = 0u, pmask = 0u, need = (uint32_t)top_k;
-    bool in_lds = false;
-    for (int l = 0; l < kLevels; ++l) {
-      const int sh = filt_shift<BF16>(l), nb = 1 << filt_bits<BF16>(l);
-      clear(nb);
-      if (in_lds)
-        filt_hist_cand<false>(F, ncand, prefix, pmask, sh, (uint32_t)nb - 1u, 0u, 0.f, 0.f);
-      else
-        filt_hist_row<BF16, false>(F, R, prefix, pmask, sh, (uint32_t)nb - 1u, 0u, 0.f, 0.f, false, kmax);
-      __syncthreads();
-      filt_select_count(F, nb, need);
-      const uint32_t pick = F.pick;
-      need = F.need;
-      // with top-p to follow, keep every key from this bin up (top-p's input)
-      const uint32_t want = top_p < 1.f ? F.nge : F.cnt[pick];
-      const uint32_t pbase = prefix | (pick << sh);
-      const uint32_t pspan = (1u << sh) - 1u;  // the bits below this digit
-      prefix = pbase;
-      pmask |= ((uint32_t)nb - 1u) << sh;
-      if (l == 0 && want <= (uint32_t)kFiltCap) {
-        ncand = gather(pbase, top_p < 1.f ? 0xffffffffu : (pbase | pspan));
-        in_lds = true;
-        cand_ge = top_p < 1.f;
-      }
-    }
-    if (BF16) prefix |= (prefix & 0x80000000u) ? 0u : 0xffffu;  // the fixed low half of bf16 keys
-    lo = prefix;
-  } else if (!fast_ok && top_p < 1.f) {
-    // top-p alone: the first level's counts, masses (relative to each bin's
-    // top) and the row maximum in one read
-    clear(1 << filt_bits<BF16>(0));
-    filt_hist_row<BF16, true>(F, R, 0u, 0u, filt_shift<BF16>(0), (uint32_t)(1 << filt_bits<BF16>(0)) - 1u, 0u,
-                              0.f, A.lg, true, kmax);
-    __syncthreads();
-    first_read_done = true;
-  }
-
-  // ---- top-p over the keys top-k kept
-  if (!fast_ok) thr_key = lo;
-  if (!fast_ok && top_p < 1.f) {
-    const float M = key_value(block_max(kmax));
-    if (tid == 0) F.above = 0.0;
-    __syncthreads();
-    uint32_t prefix = 0u, pmask = 0u;
-    bool in_lds = cand_ge;
-    for (int l = 0; l < kLevels; ++l) {
-      const int sh = filt_shift<BF16>(l), nb = 1 << filt_bits<BF16>(l);
-      const bool rel_bin = l == 0 && first_read_done;
-      if (!rel_bin) {
-        clear(nb);
-        if (in_lds)
-          filt_hist_cand<true>(F, ncand, prefix, pmask, sh, (uint32_t)nb - 1u, lo, M, A.lg);
-        else {
-          uint32_t dummy = 0u;
-          filt_hist_row<BF16, true>(F, R, prefix, pmask, sh, (uint32_t)nb - 1u, lo, M, A.lg, false, dummy);
-        }
-        __syncthreads();
-      }
-      filt_select_mass(F, nb, top_p, l == 0, rel_bin, sh, M, A.lg);
-      const uint32_t pick = F.pick, cpick = F.cpick;
-      const uint32_t pbase = prefix | (pick << sh);
-      const uint32_t pspan = (1u << sh) - 1u;
-      prefix = pbase;
-      pmask |= ((uint32_t)nb - 1u) << sh;
-      if (l == 0 && !in_lds && cpick <= (uint32_t)kFiltCap) {
-        ncand = gather(max(pbase, lo), pbase | pspan);
-        in_lds = true;
-      }
-    }
-    if (BF16) prefix |= (prefix & 0x80000000u) ? 0u : 0xffffu;
-    thr_key = prefix;
-  }
-  if (tid == 0) A.thr[((size_t)b * (A.gmax + 1) + j) * 2 + (is_q ? 1 : 0)] = key_value(thr_key);
-}
+#include "filter.inc"
+}  // namespace filt1024
 
 // ============================================================================
 // Plan and launch
@@ -2348,10 +1732,19 @@ int launch_accept(const void* p_logits, int64_t p_stride, const void* q_logits, 
     const size_t lds = Bl * sizeof(int);  // the row table
     if (filt) {  // the rows' top-k / top-p thresholds first
       const dim3 grid_f((unsigned)(Bl * (2 * G1 - 1)));
-      if (dtype == SR_BF16)
-        hipLaunchKernelGGL(accept_filter_kernel<true>, grid_f, dim3(kFiltThreads), 0, stream, A, k_eff, p_eff);
-      else
-        hipLaunchKernelGGL(accept_filter_kernel<false>, grid_f, dim3(kFiltThreads), 0, stream, A, k_eff, p_eff);
+      if ((long)grid_f.x >= 2L * device_cu_count()) {
+        const dim3 blk(filt512::kFiltThreads);
+        if (dtype == SR_BF16)
+          hipLaunchKernelGGL(filt512::accept_filter_kernel<true>, grid_f, blk, 0, stream, A, k_eff, p_eff);
+        else
+          hipLaunchKernelGGL(filt512::accept_filter_kernel<false>, grid_f, blk, 0, stream, A, k_eff, p_eff);
+      } else {
+        const dim3 blk(filt1024::kFiltThreads);
+        if (dtype == SR_BF16)
+          hipLaunchKernelGGL(filt1024::accept_filter_kernel<true>, grid_f, blk, 0, stream, A, k_eff, p_eff);
+        else
+          hipLaunchKernelGGL(filt1024::accept_filter_kernel<false>, grid_f, blk, 0, stream, A, k_eff, p_eff);
+      }
       if (hipGetLastError() != hipSuccess) return SR_ELAUNCH;
     }
     const dim3 grid((unsigned)n_wg), block(kThreads);

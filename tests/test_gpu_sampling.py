@@ -154,6 +154,31 @@ def test_top_k_top_p_match_reference(shape, top_k, top_p):
     say(f"  ok ({nf} filter-boundary sequences skipped, {nb} boundary, {nbm} differ)")
 
 
+# Enough rows for at least two threshold workgroups per CU on a 256-CU device
+# (B (2 gamma_max + 1) >= 512): the threshold kernel runs its 512-thread width
+# there, and its 1024-thread width on the smaller shapes above.
+MANY_ROWS = [
+    small_shape(name="rows-f32", B=40, V=5000, gamma=(1, 8), seed=48),
+    small_shape(name="rows-bf16", B=40, V=12288, gamma=(1, 8), seed=49, logits="bf16"),
+]
+
+
+@pytest.mark.parametrize("shape", MANY_ROWS, ids=lambda s: s.name)
+@pytest.mark.parametrize("top_k,top_p", [(1, 1.0), (50, 1.0), (0, 0.9), (20, 0.8), (3000, 0.95)])
+def test_filters_with_many_rows(shape, top_k, top_p):
+    inp = level_inputs(shape, kv=False)
+    assert inp.B * (2 * int(np.max(inp.gamma)) + 1) >= 512
+    T = 0.8
+    say(f"filtered {shape.name} T={T} top_k={top_k} top_p={top_p}")
+    got = run_accept(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, inp.u_acc, inp.u_res, temperature=T,
+                     top_k=top_k, top_p=top_p)
+    ref = oracle.accept_and_diverge(inp.p_logits, inp.q_logits, inp.drafts, inp.gamma, inp.u_acc, inp.u_res,
+                                    temperature=T, top_k=top_k, top_p=top_p)
+    assert got["status"] == ref["status"] == 0
+    nf, nb, nbm = _check_filtered(got, ref)
+    say(f"  ok ({nf} filter-boundary sequences skipped, {nb} boundary, {nbm} differ)")
+
+
 @pytest.mark.parametrize("logits", ["f32", "bf16"])
 @pytest.mark.parametrize("top_k,top_p", [(9000, 1.0), (0, 0.5), (9000, 0.6), (40, 0.7)])
 def test_filters_on_a_narrow_logit_range(logits, top_k, top_p):
