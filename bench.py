@@ -62,7 +62,7 @@ KERNEL_SOURCES = {
     "verify_attention": ["attention.hip", "sr_internal.h"],
     "accept_and_diverge": ["accept.hip", "sr_internal.h"],
     "rollback": ["rollback.hip", "sr_internal.h"],
-    "accept_filter": ["accept.hip", "sr_internal.h"],
+    "accept_filter": ["accept.hip", "filter.inc", "sr_internal.h"],
 }
 
 
