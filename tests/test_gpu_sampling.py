@@ -277,9 +277,19 @@ def _concentrate(z, dtype, n_hot, level, rng):
     return out
 
 
+# (few rows: the threshold kernel's 1024-thread width; many rows, at least
+# two workgroups per CU: its 512-thread width, whose thread 0 holds vectors
+# 0, 512, 1024, ..., so the crowded keys still sit in one thread's share.
+# Both keep gamma <= 2: with more rows per sequence nearly every sequence
+# holds some row whose top-p margin is under the boundary limit, and no
+# sequence would be left to compare.)
+ROWS = {"few-rows": (3, (1, 2)), "many-rows": (180, (1, 2))}
+
+
+@pytest.mark.parametrize("rows", list(ROWS))
 @pytest.mark.parametrize("logits", ["f32", "bf16"])
 @pytest.mark.parametrize("top_k,top_p,n_hot,level", [(50, 1.0, 40, 12.0), (0, 0.9, 30, 14.0), (50, 0.9, 40, 12.0)])
-def test_filter_when_the_largest_keys_crowd_one_thread(logits, top_k, top_p, n_hot, level):
+def test_filter_when_the_largest_keys_crowd_one_thread(rows, logits, top_k, top_p, n_hot, level):
     """Most of the kept keys sit in one thread's share of the row, more than
     the keys a thread keeps as candidates: the one-read selection cannot
     vouch for its threshold and gathers the keys above its own (lower)
@@ -288,7 +298,8 @@ def test_filter_when_the_largest_keys_crowd_one_thread(logits, top_k, top_p, n_h
     from oracle.accept import decode_logits
 
     V = 128256  # rows 16-byte aligned in both dtypes
-    shape = small_shape(name=f"crowd-{logits}", B=3, V=V, gamma=(1, 2), seed=73, logits=logits)
+    B, gam = ROWS[rows]
+    shape = small_shape(name=f"crowd-{logits}-{rows}", B=B, V=V, gamma=gam, seed=73, logits=logits)
     inp = level_inputs(shape, kv=False)
     rng = np.random.default_rng(73)
     p = _concentrate(decode_logits(inp.p_logits), logits, n_hot, level, rng)
@@ -306,12 +317,14 @@ def test_filter_when_the_largest_keys_crowd_one_thread(logits, top_k, top_p, n_h
     say(f"crowded {logits} top_k={top_k} top_p={top_p}: ok ({nf} filter-boundary skipped)")
 
 
+@pytest.mark.parametrize("rows", list(ROWS))
 @pytest.mark.parametrize("logits", ["f32", "bf16"])
-def test_top_p_keeping_most_of_a_flat_row(logits):
+def test_top_p_keeping_most_of_a_flat_row(rows, logits):
     """Nearly equal logits: top-p 0.9 keeps about 90% of 20000 keys, more
     than the candidates and more than LDS holds, so the threshold comes from
     the radix select over the row itself."""
-    shape = small_shape(name=f"flat-{logits}", B=4, V=20000, gamma=(1, 2), seed=74, logits=logits)
+    B, gam = ROWS[rows]
+    shape = small_shape(name=f"flat-{logits}-{rows}", B=B + 1, V=20000, gamma=gam, seed=74, logits=logits)
     inp = level_inputs(shape, kv=False)
     rng = np.random.default_rng(74)
     # 64 distinct values (ties of ~300 keys), so that the cumulative masses
